@@ -1,0 +1,100 @@
+"""The sparse basis convolution and its gradients, by definition, in float64.
+
+CPU ORACLE -- test infrastructure only (see the package docstring).
+
+Forward (Section 3.1, the finite convolution sum with the kernel written as a
+linear combination of basis functions): for every output i,
+
+    y_i = sum_{j in N_i} f_j g(dx_ij),     g(dx) = sum_m p_m(dx) W_m,
+
+with f_j the C_in features of input j (a row vector), W_m a C_in x C_out
+matrix and p_m(dx_ij) the basis value v[e, m] of edge e = (i, j).  This is the
+plain definition; the method's reordering into sum_m (N_m F) W_m is *not*
+used here.
+
+Backward: the exact derivatives of the scalar <Y, dY> with respect to the
+features and the weights of that same sum, per edge:
+
+    dW_m += v[e, m] * f_j^T dy_i,        df_j += g(dx_ij) dy_i^T.
+
+Everything is evaluated in float64 on the exact input values (bf16 inputs are
+passed as the float32 numbers they denote).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .basis import edge_rows
+
+_CHUNK_DOUBLES = 1 << 24    # bound on the per-chunk kernel tensor
+
+
+def _edge_chunks(edges, per_edge):
+    step = max(1, _CHUNK_DOUBLES // max(1, per_edge))
+    for s in range(0, len(edges), step):
+        yield edges[s:s + step]
+
+
+def _edge_kernels(v_e, Wd):
+    """g(dx_e) = sum_m v[e, m] W_m for a block of edges: [n_e, C_in, C_out]."""
+    M, cin, cout = Wd.shape
+    return (v_e @ Wd.reshape(M, cin * cout)).reshape(len(v_e), cin, cout)
+
+
+def forward(row_ptr, col_idx, v, F, W, rows=None):
+    """Y[rows] (all rows when rows is None): y_i = sum_e f_j g(dx_e)."""
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    cols = np.asarray(col_idx, dtype=np.int64)
+    Fd = np.asarray(F, dtype=np.float64)
+    Wd = np.asarray(W, dtype=np.float64)
+    vd = np.asarray(v, dtype=np.float64)
+    M, cin, cout = Wd.shape
+    n_out = len(row_ptr) - 1
+    rows = np.arange(n_out) if rows is None else np.asarray(rows, dtype=np.int64)
+    Y = np.zeros((len(rows), cout))
+    lens = row_ptr[rows + 1] - row_ptr[rows]
+    edges = (np.repeat(row_ptr[rows] - np.cumsum(lens) + lens, lens)
+             + np.arange(int(lens.sum())))
+    local = np.repeat(np.arange(len(rows)), lens)
+    for pos in _edge_chunks(np.arange(len(edges)), cin * cout):
+        e = edges[pos]
+        K = _edge_kernels(vd[e], Wd)
+        contrib = np.matmul(Fd[cols[e]][:, None, :], K)[:, 0, :]
+        np.add.at(Y, local[pos], contrib)
+    return Y
+
+
+def backward(row_ptr, col_idx, v, F, W, dY, n_in, cols_subset=None, want_dW=True):
+    """(dF, dW): dF for all inputs (or only the rows `cols_subset`), dW [M, C_in, C_out]."""
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    cols = np.asarray(col_idx, dtype=np.int64)
+    Fd = np.asarray(F, dtype=np.float64)
+    Wd = np.asarray(W, dtype=np.float64)
+    vd = np.asarray(v, dtype=np.float64)
+    dYd = np.asarray(dY, dtype=np.float64)
+    M, cin, cout = Wd.shape
+    rows = edge_rows(row_ptr)
+
+    dW = None
+    if want_dW:
+        dW = np.zeros((M, cin, cout))
+        for e in _edge_chunks(np.arange(len(cols)), cin * M):
+            Fe = Fd[cols[e]]
+            Ye = dYd[rows[e]]
+            for m in range(M):
+                dW[m] += (Fe * vd[e, m:m + 1]).T @ Ye
+
+    if cols_subset is None:
+        sel = np.arange(len(cols))
+        target = np.arange(n_in)
+    else:
+        target = np.asarray(cols_subset, dtype=np.int64)
+        sel = np.nonzero(np.isin(cols, target))[0]
+    pos_of = np.full(n_in, -1, dtype=np.int64)
+    pos_of[target] = np.arange(len(target))
+    dF = np.zeros((len(target), cin))
+    for e in _edge_chunks(sel, cin * cout):
+        K = _edge_kernels(vd[e], Wd)
+        contrib = np.matmul(K, dYd[rows[e]][:, :, None])[:, :, 0]
+        np.add.at(dF, pos_of[cols[e]], contrib)
+    return dF, dW
