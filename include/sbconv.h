@@ -1,0 +1,271 @@
+/*
+ * sbconv -- sparse basis convolution on continuous domains (point clouds and
+ * event streams), after "Sparse Convolutions on Continuous Domains for Point
+ * Cloud and Event Stream Networks" (Jack, Maire, Denman, Eriksson, ACCV 2020).
+ *
+ * The operator (Section 3.1, the matrix-product form of the convolution):
+ *
+ *     Y = sum_m  N^(m) F W^(m)
+ *
+ *   F    [n_in,  C_in ]  features of the input points / events
+ *   W    [M, C_in, C_out] learned weights, one C_in x C_out matrix per basis fn
+ *   N^(m)[n_out, n_in]   sparse neighbourhood matrices sharing one pattern:
+ *                        entry (i, j) = p_m(x'_i - x_j) for j in the
+ *                        neighbourhood of output i, zero otherwise
+ *   Y    [n_out, C_out]
+ *
+ * Conventions of every entry point
+ *   - Array arguments are DEVICE pointers unless their name ends in _host.
+ *   - Every array is row-major and densely packed.  Buffers are owned by the
+ *     caller; the library keeps no pointer after a call returns and allocates
+ *     no device memory: temporary space comes from the `workspace` argument,
+ *     whose required size a *_workspace_size query gives.  workspace must be
+ *     256-byte aligned.
+ *   - Work is enqueued on `stream` and runs asynchronously; only a neighbour
+ *     search given a non-NULL nnz_host synchronises the stream (once).
+ *   - Outputs are overwritten, never accumulated into.
+ *   - Indices are int32; an edge count of 2^31 or more is an error.
+ *   - On an argument error nothing is enqueued and a status other than
+ *     SBC_OK is returned; sbc_last_error() then describes it (thread-local).
+ *   - Results are deterministic: no floating-point atomics are used, so the
+ *     same inputs give bitwise-identical outputs on every run.
+ *
+ * CSR layout of the neighbourhoods: rows are outputs i, row_ptr [n_out + 1],
+ * col_idx [E] holds input indices j, ascending within a row.  A ragged batch
+ * of clouds is the block-diagonal matrix of the per-cloud matrices with
+ * global column indices (Section 3.1, "Ragged Batching").
+ */
+#ifndef SBCONV_H
+#define SBCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SBC_OK = 0,
+    SBC_ERR_INVALID_ARG = 1,  /* null pointer, bad size, unknown enum, ...        */
+    SBC_ERR_CAPACITY = 2,     /* col_idx too small for the edges found            */
+    SBC_ERR_OVERFLOW = 3,     /* 2^31 or more edges                               */
+    SBC_ERR_UNSORTED = 4,     /* event timestamps decrease somewhere              */
+    SBC_ERR_OUT_OF_RANGE = 5, /* pixel outside the sensor, split outside [0, n]   */
+    SBC_ERR_WORKSPACE = 6,    /* workspace smaller than the size query's answer   */
+    SBC_ERR_HIP = 7,          /* a HIP runtime call failed                        */
+    SBC_ERR_UNSUPPORTED = 8   /* shape or basis with no kernel in this build      */
+} sbc_status;
+
+typedef enum {
+    SBC_F32 = 0,  /* float32 features, weights and gradients                    */
+    SBC_BF16 = 1  /* bfloat16 features, weights and upstream gradient; float32  */
+                  /* basis values, accumulation and outputs                      */
+} sbc_dtype;
+
+/*
+ * Basis functions p_m.  Point bases (Section 3.1: geometric monomials of the
+ * edge vector) use u = (x'_i - x_j) / r and the window w = (1 - |u|^2)^2:
+ *   SBC_BASIS_MONO4   M = 4: [1, ux, uy, uz] * w
+ *   SBC_BASIS_MONO8   M = 8: [1, ux, uy, uz, ux^2, uy^2, uz^2, ux*uy] * w
+ * Event basis (Section 3.2, the event kernel with one decay per pixel offset,
+ * lambda = 1/tau): u = (px_i - px_j, py_i - py_j) in the 3x3 block,
+ * dt = t_i - t_j >= 0;
+ *   SBC_BASIS_EVENT8  M = 8: p_m = [m == idx(u)] * exp(-dt / tau), with idx
+ *                     row-major over (uy, ux) and the centre offset removed
+ *                     (same-pixel edges have an all-zero basis row).
+ */
+typedef enum {
+    SBC_BASIS_MONO4 = 0,
+    SBC_BASIS_MONO8 = 1,
+    SBC_BASIS_EVENT8 = 2
+} sbc_basis;
+
+/*
+ * Evaluation order of the matrix products (Section 3.1, down- vs up-sampling
+ * convolutions and their cost table):
+ *   SPMM_FIRST  (N^(m) F) W^(m): gather-accumulate G = [N^(0)F ... N^(M-1)F]
+ *               [n_out, M*C_in], then one dense contraction with W.
+ *   GEMM_FIRST  N^(m) (F W^(m)): one dense contraction H = F [W^(0)..W^(M-1)]
+ *               [n_in, M*C_out], then gather-accumulate over H.
+ *   AUTO        the library picks by the multiply-add counts of both orders.
+ * The backward pass uses the transposed counterpart of the chosen order.
+ */
+typedef enum {
+    SBC_ORDER_AUTO = 0,
+    SBC_ORDER_SPMM_FIRST = 1,
+    SBC_ORDER_GEMM_FIRST = 2
+} sbc_order;
+
+/*
+ * The shared sparsity pattern of the N^(m) (rows = outputs).  Kernels read
+ * row extents from row_ptr on the device; nnz_bound only sizes per-edge
+ * temporaries and must be >= row_ptr[n_rows] (the exact E is best).
+ */
+typedef struct {
+    int32_t n_rows;           /* n_out                                          */
+    int32_t n_cols;           /* n_in                                           */
+    int64_t nnz_bound;        /* >= E = row_ptr[n_rows]                         */
+    const int32_t *row_ptr;   /* [n_rows + 1], row_ptr[0] = 0                   */
+    const int32_t *col_idx;   /* [E]                                            */
+} sbc_csr;
+
+/* Its transpose (rows = inputs), as produced by sbc_csr_transpose. */
+typedef struct {
+    int32_t n_cols;           /* n_in                                           */
+    const int32_t *col_ptr;   /* [n_cols + 1]                                   */
+    const int32_t *row_idx;   /* [E] output index of each entry, ascending      */
+    const int32_t *edge_perm; /* [E] CSR position of each entry                 */
+} sbc_csc;
+
+/*
+ * Coordinates the basis values are evaluated from (the paper evaluates the
+ * basis on the accelerator from the neighbour indices; Section 3.1, "Data
+ * Pipeline").  Point bases read x_in/x_out and radius; the event basis reads
+ * px/py/t and tau, for an in-place stream (outputs = inputs).
+ */
+typedef struct {
+    sbc_basis basis;
+    float radius;             /* points: r, > 0                                 */
+    float tau;                /* events: decay time, > 0, unit of t             */
+    const float *x_in;        /* points: [n_in, 3]                              */
+    const float *x_out;       /* points: [n_out, 3]                             */
+    const int32_t *px;        /* events: [n] pixel column                       */
+    const int32_t *py;        /* events: [n] pixel row                          */
+    const int32_t *t;         /* events: [n] timestamps, non-decreasing         */
+} sbc_geometry;
+
+/* Thread-local description of the last error of this thread ("" if none). */
+const char *sbc_last_error(void);
+const char *sbc_status_string(sbc_status status);
+/* Number of basis functions of a basis (0 for an unknown one). */
+int32_t sbc_basis_size(sbc_basis basis);
+
+/* ------------------------------------------------------------------------
+ * 1a. Point neighbourhoods (Section 3.1, "Neighborhoods"): for output i of
+ * cloud b, the inputs j of cloud b with d2 < r*r, where d2 is evaluated in
+ * float32 with round-to-nearest and no fused multiply-add as
+ *     dx = x'_i.x - x_j.x (y, z alike);  d2 = ((dx*dx) + (dy*dy)) + (dz*dz).
+ * k_cap > 0 truncates a row to its k_cap smallest (d2, j); k_cap <= 0 keeps
+ * the whole ball.  Rows are emitted in ascending j.
+ *
+ *   x_in [n_in, 3], x_out [n_out, 3]     device, float32
+ *   in_splits, out_splits [n_batch + 1]  device, int32: cloud b owns inputs
+ *                                        in_splits[b] .. in_splits[b+1]-1 and
+ *                                        outputs out_splits[b] .. likewise;
+ *                                        both start at 0 and end at n_in/n_out
+ *   row_ptr [n_out + 1]                  device, output; row_ptr[n_out] = E
+ *   col_idx [col_capacity]               device, output
+ *   nnz_host                             host, may be NULL.  Non-NULL: E is
+ *                                        read back (one stream synchronise);
+ *                                        E > col_capacity returns
+ *                                        SBC_ERR_CAPACITY with row_ptr filled
+ *                                        and col_idx untouched; malformed
+ *                                        splits return SBC_ERR_OUT_OF_RANGE.
+ *                                        NULL: nothing is synchronised; writes
+ *                                        past col_capacity are dropped, so the
+ *                                        caller checks row_ptr[n_out] <=
+ *                                        col_capacity before using col_idx.
+ * ------------------------------------------------------------------------ */
+size_t sbc_points_workspace_size(int32_t n_in, int32_t n_out, int32_t n_batch);
+sbc_status sbc_neighbour_search_points(const float *x_in, int32_t n_in, const int32_t *in_splits,
+                                       const float *x_out, int32_t n_out,
+                                       const int32_t *out_splits, int32_t n_batch, float radius,
+                                       int32_t k_cap, int32_t *row_ptr, int32_t *col_idx,
+                                       int64_t col_capacity, int64_t *nnz_host, void *workspace,
+                                       size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * 1b. Event neighbourhoods (Section 3.2: a small spatial block, extending
+ * backwards in time only): event i's neighbours are the events j < i with
+ * |px_i - px_j| <= half_extent, |py_i - py_j| <= half_extent and
+ * t_i - t_j <= window, in ascending j.  The stream is in place (outputs =
+ * inputs).
+ *
+ *   px, py, t [n]   device, int32; 0 <= px < width, 0 <= py < height, t
+ *                   non-decreasing.  Events violating this never fault: they
+ *                   are given no neighbours and, when nnz_host is non-NULL,
+ *                   SBC_ERR_OUT_OF_RANGE / SBC_ERR_UNSORTED is returned.
+ *   row_ptr, col_idx, col_capacity, nnz_host: as for points.
+ * ------------------------------------------------------------------------ */
+size_t sbc_events_workspace_size(int32_t n, int32_t width, int32_t height);
+sbc_status sbc_neighbour_search_events(const int32_t *px, const int32_t *py, const int32_t *t,
+                                       int32_t n, int32_t width, int32_t height,
+                                       int32_t half_extent, int32_t window, int32_t *row_ptr,
+                                       int32_t *col_idx, int64_t col_capacity, int64_t *nnz_host,
+                                       void *workspace, size_t workspace_bytes,
+                                       hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * 2. Basis values (Section 3.1, the values of the neighbourhood matrices):
+ * v[e, m] = p_m(edge e) as float32, edge-major [E, M], in CSR edge order.
+ * v must hold row_ptr[n_rows] * M floats.
+ * ------------------------------------------------------------------------ */
+sbc_status sbc_basis_eval(const sbc_csr *csr, const sbc_geometry *geometry, float *v,
+                          hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * 3. Transpose of the pattern, for the backward pass (Section 3.1,
+ * "Symmetry": N_IJ = N_JI^T relates a neighbourhood to its reverse).
+ * Stable: within a column, rows ascend.  col_ptr [n_cols + 1], row_idx and
+ * edge_perm [E] are outputs.
+ * ------------------------------------------------------------------------ */
+size_t sbc_transpose_workspace_size(int32_t n_cols, int64_t nnz_bound);
+sbc_status sbc_csr_transpose(const sbc_csr *csr, int32_t *col_ptr, int32_t *row_idx,
+                             int32_t *edge_perm, void *workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * 4. Forward: Y [n_out, C_out] float32 = sum_m N^(m) F W^(m) (Section 3.1,
+ * the matrix-product form).
+ *   v          [E, M] float32 basis values, or NULL to evaluate them inside the
+ *              kernels from `geometry` (then geometry must be non-NULL)
+ *   F          [n_in, C_in]      float32 or bf16 (dtype)
+ *   W          [M, C_in, C_out]  float32 or bf16 (dtype)
+ *   order      evaluation order (sbc_order)
+ * ------------------------------------------------------------------------ */
+/* Workspace of sbc_conv_forward and sbc_conv_backward (the larger of the two). */
+size_t sbc_conv_workspace_size(int32_t n_out, int32_t n_in, int64_t nnz_bound, int32_t M,
+                               int32_t C_in, int32_t C_out, sbc_dtype dtype, sbc_order order);
+sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v, const sbc_geometry *geometry,
+                            int32_t M, const void *F, const void *W, sbc_dtype dtype,
+                            int32_t C_in, int32_t C_out, float *Y, sbc_order order,
+                            void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * 5. Backward: the gradients of <Y, dY> with respect to F and W.
+ *   dY  [n_out, C_out]    float32 or bf16 (dtype)
+ *   dF  [n_in, C_in]      float32 output, or NULL to skip
+ *   dW  [M, C_in, C_out]  float32 output, or NULL to skip
+ *   csc                   the transpose of csr (sbc_csr_transpose)
+ * dW sums over every edge of the batch, in a fixed blocked order.
+ * ------------------------------------------------------------------------ */
+sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v,
+                             const sbc_geometry *geometry, int32_t M, const void *F,
+                             const void *W, const void *dY, sbc_dtype dtype, int32_t C_in,
+                             int32_t C_out, float *dF, float *dW, sbc_order order,
+                             void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Tracing, for measurement tools.  After sbc_trace_kernel(name, start, stop)
+ * every launch of the kernel called `name` made by the calling thread records
+ * `start` immediately before and `stop` immediately after itself on its
+ * launch stream (a later launch re-records them).  NULL events remove the
+ * entry, sbc_trace_clear() removes all entries.  sbc_kernel_names() lists the
+ * traceable names, comma-separated.  Events stay owned by the caller.
+ * ------------------------------------------------------------------------ */
+sbc_status sbc_trace_kernel(const char *name, hipEvent_t start, hipEvent_t stop);
+void sbc_trace_clear(void);
+const char *sbc_kernel_names(void);
+
+/* Order AUTO resolves to (SBC_ORDER_SPMM_FIRST or SBC_ORDER_GEMM_FIRST). */
+sbc_order sbc_resolve_order(int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t C_in,
+                            int32_t C_out, sbc_order order);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SBCONV_H */

@@ -1,0 +1,118 @@
+// sbc_basis_eval: materialise the values v[E, M] of the neighbourhood matrices
+// (Section 3.1, the entries of N^(m)).  One wave per group of 64 rows would
+// scatter the writes; instead every thread takes one edge and finds its row by
+// binary search in row_ptr, so that the [E, M] rows are written contiguously.
+#include "basis.hpp"
+#include "common.hpp"
+
+namespace sbc {
+
+__device__ __forceinline__ int32_t row_of_edge(const int32_t *__restrict__ row_ptr,
+                                               int32_t n_rows, int32_t e) {
+    int32_t lo = 0, hi = n_rows;  // row_ptr[lo] <= e < row_ptr[hi]
+    while (hi - lo > 1) {
+        int32_t mid = (lo + hi) >> 1;
+        if (row_ptr[mid] <= e) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+template <int kBasis>
+__global__ void __launch_bounds__(256)
+    basis_kernel(int32_t n_rows, const int32_t *__restrict__ row_ptr,
+                 const int32_t *__restrict__ col_idx, sbc_geometry g, float *__restrict__ v) {
+    constexpr int M = kBasis == SBC_BASIS_MONO4 ? 4 : 8;
+    const int32_t E = row_ptr[n_rows];
+    const double inv_r = 1.0 / (double)g.radius;
+    const float inv_tau = 1.0f / g.tau;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < E;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t i = row_of_edge(row_ptr, n_rows, (int32_t)e);
+        const int32_t j = col_idx[e];
+        float out[8];
+        if constexpr (kBasis == SBC_BASIS_EVENT8) {
+#pragma unroll
+            for (int m = 0; m < 8; ++m) out[m] = 0.f;
+            const int k = event_index(g.px[i] - g.px[j], g.py[i] - g.py[j]);
+            const float d = event_decay(g.t[i], g.t[j], inv_tau);
+#pragma unroll
+            for (int m = 0; m < 8; ++m)
+                if (m == k) out[m] = d;
+        } else {
+            point_basis<M>(g.x_out[3 * (int64_t)i], g.x_out[3 * (int64_t)i + 1],
+                           g.x_out[3 * (int64_t)i + 2], g.x_in[3 * (int64_t)j],
+                           g.x_in[3 * (int64_t)j + 1], g.x_in[3 * (int64_t)j + 2], inv_r, out);
+        }
+#pragma unroll
+        for (int m = 0; m < M; ++m) v[e * M + m] = out[m];
+    }
+}
+
+sbc_status check_geometry(const sbc_geometry *g, int32_t n_rows, int32_t n_cols) {
+    if (!g) return fail(SBC_ERR_INVALID_ARG, "geometry is null");
+    switch (g->basis) {
+        case SBC_BASIS_MONO4:
+        case SBC_BASIS_MONO8:
+            if (!(g->radius > 0.f)) return fail(SBC_ERR_INVALID_ARG, "radius must be > 0");
+            if ((n_rows > 0 && !g->x_out) || (n_cols > 0 && !g->x_in))
+                return fail(SBC_ERR_INVALID_ARG, "x_in / x_out is null");
+            return SBC_OK;
+        case SBC_BASIS_EVENT8:
+            if (!(g->tau > 0.f)) return fail(SBC_ERR_INVALID_ARG, "tau must be > 0");
+            if (n_rows != n_cols)
+                return fail(SBC_ERR_INVALID_ARG, "event streams are in place (n_rows == n_cols)");
+            if (n_rows > 0 && (!g->px || !g->py || !g->t))
+                return fail(SBC_ERR_INVALID_ARG, "px / py / t is null");
+            return SBC_OK;
+        default:
+            return fail(SBC_ERR_INVALID_ARG, "unknown basis");
+    }
+}
+
+sbc_status basis_eval_launch(const sbc_csr *csr, const sbc_geometry *g, float *v,
+                             hipStream_t stream) {
+    if (csr->n_rows == 0 || csr->nnz_bound <= 0) return SBC_OK;
+    int64_t blocks = (csr->nnz_bound + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    trace_before("basis", stream);
+    switch (g->basis) {
+        case SBC_BASIS_MONO4:
+            hipLaunchKernelGGL(basis_kernel<SBC_BASIS_MONO4>, dim3((unsigned)blocks), dim3(256), 0,
+                               stream, csr->n_rows, csr->row_ptr, csr->col_idx, *g, v);
+            break;
+        case SBC_BASIS_MONO8:
+            hipLaunchKernelGGL(basis_kernel<SBC_BASIS_MONO8>, dim3((unsigned)blocks), dim3(256), 0,
+                               stream, csr->n_rows, csr->row_ptr, csr->col_idx, *g, v);
+            break;
+        default:
+            hipLaunchKernelGGL(basis_kernel<SBC_BASIS_EVENT8>, dim3((unsigned)blocks), dim3(256), 0,
+                               stream, csr->n_rows, csr->row_ptr, csr->col_idx, *g, v);
+            break;
+    }
+    SBC_LAUNCH_CHECK();
+    trace_after("basis", stream);
+    return SBC_OK;
+}
+
+sbc_status check_csr(const sbc_csr *csr) {
+    if (!csr) return fail(SBC_ERR_INVALID_ARG, "csr is null");
+    if (csr->n_rows < 0 || csr->n_cols < 0 || csr->nnz_bound < 0)
+        return fail(SBC_ERR_INVALID_ARG, "negative csr size");
+    if (csr->nnz_bound > (int64_t)INT32_MAX) return fail(SBC_ERR_OVERFLOW, "2^31 or more edges");
+    if (!csr->row_ptr || (csr->nnz_bound > 0 && !csr->col_idx))
+        return fail(SBC_ERR_INVALID_ARG, "csr row_ptr / col_idx is null");
+    return SBC_OK;
+}
+
+}  // namespace sbc
+
+using namespace sbc;
+
+extern "C" sbc_status sbc_basis_eval(const sbc_csr *csr, const sbc_geometry *geometry, float *v,
+                                     hipStream_t stream) {
+    clear_error();
+    SBC_TRY(check_csr(csr));
+    SBC_TRY(check_geometry(geometry, csr->n_rows, csr->n_cols));
+    if (csr->nnz_bound > 0 && !v) return fail(SBC_ERR_INVALID_ARG, "v is null");
+    return basis_eval_launch(csr, geometry, v, stream);
+}

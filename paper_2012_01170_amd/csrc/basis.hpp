@@ -1,0 +1,55 @@
+// Basis functions p_m of the neighbourhood matrices, evaluated per edge on the
+// device (Section 3.1: the entries of N^(m) are the basis functions at the
+// edge vector; the paper computes them on the accelerator from the neighbour
+// indices).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "../../include/sbconv.h"
+
+namespace sbc {
+
+// Point monomials of u = (x'_i - x_j) / r times the window (1 - |u|^2)^2.
+// M = 4: [1, ux, uy, uz];  M = 8: [1, ux, uy, uz, ux^2, uy^2, uz^2, ux*uy].
+// Evaluated in float64 and rounded once: the coordinate differences are then
+// exact and 1 - |u|^2 keeps its relative accuracy near the ball's edge, where
+// float32 would cancel.
+template <int M>
+__device__ __forceinline__ void point_basis(float qx, float qy, float qz, float px, float py,
+                                            float pz, double inv_r, float *v) {
+    const double ux = ((double)qx - (double)px) * inv_r;
+    const double uy = ((double)qy - (double)py) * inv_r;
+    const double uz = ((double)qz - (double)pz) * inv_r;
+    const double a = 1.0 - (ux * ux + uy * uy + uz * uz);
+    const double w = a * a;
+    v[0] = (float)w;
+    v[1] = (float)(ux * w);
+    v[2] = (float)(uy * w);
+    v[3] = (float)(uz * w);
+    if constexpr (M == 8) {
+        v[4] = (float)(ux * ux * w);
+        v[5] = (float)(uy * uy * w);
+        v[6] = (float)(uz * uz * w);
+        v[7] = (float)(ux * uy * w);
+    }
+}
+
+// Event basis: index of pixel offset u = (ux, uy) in the 3x3 block, row-major
+// over (uy, ux) with the centre removed; -1 for the centre (and for offsets
+// outside the block, which no neighbourhood produces).
+__device__ __forceinline__ int event_index(int32_t ux, int32_t uy) {
+    if (ux < -1 || ux > 1 || uy < -1 || uy > 1) return -1;
+    const int k = (uy + 1) * 3 + (ux + 1);
+    return k == 4 ? -1 : (k < 4 ? k : k - 1);
+}
+
+// exp(-dt / tau) for an integer time gap dt >= 0.
+__device__ __forceinline__ float event_decay(int32_t ti, int32_t tj, float inv_tau) {
+    const float dt = (float)((int64_t)ti - (int64_t)tj);
+    return expf(-dt * inv_tau);
+}
+
+}  // namespace sbc

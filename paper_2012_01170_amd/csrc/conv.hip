@@ -1,0 +1,249 @@
+// sbc_conv_forward / sbc_conv_backward: Y = sum_m N^(m) F W^(m) and its
+// gradients (Section 3.1, the matrix-product form; its down- and up-sampling
+// evaluation orders and their multiply-add counts).
+//
+// SpMM-first ((N F) W):  G = [N^(m) F]_m  [n_out, M*C_in]   (gather, expand)
+//                        Y = G W_flat                        (MFMA)
+//   backward:  dW = G^T dY (split K over n_out), dG = dY W_flat^T (MFMA),
+//              dF = sum_m N^(m)T dG_m                        (gather, contract, CSC)
+// GEMM-first (N (F W)):  H = F [W^(m)]_m  [n_in, M*C_out]   (MFMA)
+//                        Y = sum_m N^(m) H_m                 (gather, contract)
+//   backward:  D = [N^(m)T dY]_m [n_in, M*C_out]            (gather, expand, CSC)
+//              dF = D Wt, dW = F^T D (split K over n_in)     (MFMA)
+// When v is NULL the basis values are evaluated into the workspace first.
+#include "basis.hpp"
+#include "common.hpp"
+#include "gemm.hpp"
+#include "spmm.hpp"
+
+namespace sbc {
+namespace {
+
+__device__ __forceinline__ float ldw(const float *p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float ldw(const uint16_t *p, int64_t i) {
+    return __uint_as_float((uint32_t)p[i] << 16);
+}
+
+// W [M, Ci, Co] -> out with element (m, c, p) at m*s_m + c*s_c + p*s_p, as float32.
+template <typename T>
+__global__ void permute_w_kernel(const T *__restrict__ W, int32_t M, int32_t Ci, int32_t Co,
+                                 int64_t s_m, int64_t s_c, int64_t s_p, float *__restrict__ out) {
+    const int64_t total = (int64_t)M * Ci * Co;
+    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < total;
+         x += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t p = (int32_t)(x % Co);
+        const int32_t c = (int32_t)((x / Co) % Ci);
+        const int32_t m = (int32_t)(x / ((int64_t)Co * Ci));
+        out[m * s_m + c * s_c + p * s_p] = ldw(W, x);
+    }
+}
+
+sbc_status permute_w(const void *W, bool bf16, int32_t M, int32_t Ci, int32_t Co, int64_t s_m,
+                     int64_t s_c, int64_t s_p, float *out, hipStream_t stream) {
+    int64_t total = (int64_t)M * Ci * Co;
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 1024) blocks = 1024;
+    if (bf16)
+        hipLaunchKernelGGL(permute_w_kernel<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                           static_cast<const uint16_t *>(W), M, Ci, Co, s_m, s_c, s_p, out);
+    else
+        hipLaunchKernelGGL(permute_w_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                           static_cast<const float *>(W), M, Ci, Co, s_m, s_c, s_p, out);
+    SBC_LAUNCH_CHECK();
+    return SBC_OK;
+}
+
+// dwp [C_in, M, C_out] -> dW [M, C_in, C_out]
+__global__ void permute_back_kernel(const float *__restrict__ dwp, int32_t M, int32_t Ci,
+                                    int32_t Co, float *__restrict__ dW) {
+    const int64_t total = (int64_t)M * Ci * Co;
+    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < total;
+         x += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t p = (int32_t)(x % Co);
+        const int32_t c = (int32_t)((x / Co) % Ci);
+        const int32_t m = (int32_t)(x / ((int64_t)Co * Ci));
+        dW[x] = dwp[((int64_t)c * M + m) * Co + p];
+    }
+}
+
+sbc_status permute_w_back(const float *dwp, int32_t M, int32_t Ci, int32_t Co, float *dW,
+                          hipStream_t stream) {
+    int64_t total = (int64_t)M * Ci * Co;
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(permute_back_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, dwp, M,
+                       Ci, Co, dW);
+    SBC_LAUNCH_CHECK();
+    return SBC_OK;
+}
+
+struct ConvWs {
+    float *v;        // [nnz, M]
+    float *inter;    // G / H / D
+    float *inter2;   // dG
+    float *wperm;    // permuted weights (GEMM-first)
+    float *dwperm;   // dW in [C_in, M, C_out] (D-route)
+    float *partial;  // split-K partial tiles
+};
+
+ConvWs carve_conv(void *base, int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t Ci,
+                  int32_t Co, sbc_order order, size_t *bytes) {
+    Carver cv(base);
+    ConvWs w{};
+    w.v = cv.take<float>((size_t)nnz * M);
+    const int64_t wsz = (int64_t)M * Ci * Co;
+    if (order == SBC_ORDER_SPMM_FIRST) {
+        w.inter = cv.take<float>((size_t)n_out * M * Ci);
+        w.inter2 = cv.take<float>((size_t)n_out * M * Ci);
+        size_t p1 = gemm_workspace_floats(M * Ci, Co, n_out);      // dW = G^T dY
+        size_t p2 = gemm_workspace_floats(n_out, Co, (int64_t)M * Ci);  // Y = G W
+        size_t p3 = gemm_workspace_floats(n_out, M * Ci, Co);      // dG = dY W^T
+        size_t p = p1 > p2 ? p1 : p2;
+        w.partial = cv.take<float>(p > p3 ? p : p3);
+    } else {
+        w.inter = cv.take<float>((size_t)n_in * M * Co);
+        w.wperm = cv.take<float>((size_t)wsz);
+        w.dwperm = cv.take<float>((size_t)wsz);
+        size_t p1 = gemm_workspace_floats(n_in, M * Co, Ci);       // H = F Wp
+        size_t p2 = gemm_workspace_floats(n_in, Ci, (int64_t)M * Co);  // dF = D Wt
+        size_t p3 = gemm_workspace_floats(Ci, M * Co, n_in);       // dW' = F^T D
+        size_t p = p1 > p2 ? p1 : p2;
+        w.partial = cv.take<float>(p > p3 ? p : p3);
+    }
+    if (bytes) *bytes = cv.used;
+    return w;
+}
+
+sbc_status check_conv_args(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,
+                           const void *F, const void *W, sbc_dtype dtype, int32_t Ci, int32_t Co) {
+    SBC_TRY(check_csr(csr));
+    if (M != 4 && M != 8) return fail(SBC_ERR_UNSUPPORTED, "M must be 4 or 8");
+    if (Ci <= 0 || Co <= 0) return fail(SBC_ERR_INVALID_ARG, "C_in and C_out must be > 0");
+    if (dtype != SBC_F32 && dtype != SBC_BF16) return fail(SBC_ERR_INVALID_ARG, "unknown dtype");
+    if (!W || (csr->n_cols > 0 && !F)) return fail(SBC_ERR_INVALID_ARG, "F or W is null");
+    if (!v) {
+        SBC_TRY(check_geometry(g, csr->n_rows, csr->n_cols));
+        const int32_t gm = g->basis == SBC_BASIS_MONO4 ? 4 : 8;
+        if (gm != M) return fail(SBC_ERR_INVALID_ARG, "M does not match the geometry's basis");
+    }
+    return SBC_OK;
+}
+
+}  // namespace
+}  // namespace sbc
+
+using namespace sbc;
+
+extern "C" sbc_order sbc_resolve_order(int32_t n_out, int32_t n_in, int64_t nnz, int32_t M,
+                                       int32_t C_in, int32_t C_out, sbc_order order) {
+    if (order == SBC_ORDER_SPMM_FIRST || order == SBC_ORDER_GEMM_FIRST) return order;
+    // multiply-adds of the two orders (the paper's cost table):
+    //   (N F) W:  M C_in (E + n_out C_out);   N (F W):  M C_out (E + n_in C_in)
+    const double E = (double)(nnz > 0 ? nnz : 0);
+    const double spmm_first = (double)M * C_in * (E + (double)n_out * C_out);
+    const double gemm_first = (double)M * C_out * (E + (double)n_in * C_in);
+    return spmm_first <= gemm_first ? SBC_ORDER_SPMM_FIRST : SBC_ORDER_GEMM_FIRST;
+}
+
+extern "C" size_t sbc_conv_workspace_size(int32_t n_out, int32_t n_in, int64_t nnz_bound,
+                                          int32_t M, int32_t C_in, int32_t C_out,
+                                          sbc_dtype /*dtype*/, sbc_order order) {
+    if (n_out < 0 || n_in < 0 || nnz_bound < 0 || M <= 0 || C_in <= 0 || C_out <= 0) return 0;
+    order = sbc_resolve_order(n_out, n_in, nnz_bound, M, C_in, C_out, order);
+    size_t bytes = 0;
+    carve_conv(nullptr, n_out, n_in, nnz_bound, M, C_in, C_out, order, &bytes);
+    return bytes;
+}
+
+extern "C" sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v,
+                                       const sbc_geometry *geometry, int32_t M, const void *F,
+                                       const void *W, sbc_dtype dtype, int32_t C_in,
+                                       int32_t C_out, float *Y, sbc_order order, void *workspace,
+                                       size_t workspace_bytes, hipStream_t stream) {
+    clear_error();
+    SBC_TRY(check_conv_args(csr, v, geometry, M, F, W, dtype, C_in, C_out));
+    if (!Y && csr->n_rows > 0) return fail(SBC_ERR_INVALID_ARG, "Y is null");
+    const int32_t n_out = csr->n_rows, n_in = csr->n_cols;
+    order = sbc_resolve_order(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order);
+    size_t need = 0;
+    ConvWs ws = carve_conv(workspace, n_out, n_in, csr->nnz_bound, M, C_in, C_out, order, &need);
+    if (!workspace || workspace_bytes < need)
+        return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_conv_workspace_size()");
+    const bool bf = dtype == SBC_BF16;
+    const float *vv = v;
+    if (!vv) {
+        SBC_TRY(basis_eval_launch(csr, geometry, ws.v, stream));
+        vv = ws.v;
+    }
+    if (order == SBC_ORDER_SPMM_FIRST) {
+        SBC_TRY(spmm(n_out, csr->row_ptr, csr->col_idx, nullptr, vv, M, F, bf, C_in, false,
+                     ws.inter, stream, "fwd_spmm"));
+        SBC_TRY(gemm(ws.inter, false, (int64_t)M * C_in, 1, W, bf, C_out, 1, Y, C_out, 1, n_out,
+                     C_out, (int64_t)M * C_in, ws.partial, stream, "fwd_gemm"));
+    } else {
+        // Wp [C_in, M, C_out]
+        SBC_TRY(permute_w(W, bf, M, C_in, C_out, C_out, (int64_t)M * C_out, 1, ws.wperm, stream));
+        SBC_TRY(gemm(F, bf, C_in, 1, ws.wperm, false, (int64_t)M * C_out, 1, ws.inter,
+                     (int64_t)M * C_out, 1, n_in, M * C_out, C_in, ws.partial, stream,
+                     "fwd_gemm_h"));
+        SBC_TRY(spmm(n_out, csr->row_ptr, csr->col_idx, nullptr, vv, M, ws.inter, false, C_out,
+                     true, Y, stream, "fwd_spmm_contract"));
+    }
+    return SBC_OK;
+}
+
+extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v,
+                                        const sbc_geometry *geometry, int32_t M, const void *F,
+                                        const void *W, const void *dY, sbc_dtype dtype,
+                                        int32_t C_in, int32_t C_out, float *dF, float *dW,
+                                        sbc_order order, void *workspace, size_t workspace_bytes,
+                                        hipStream_t stream) {
+    clear_error();
+    SBC_TRY(check_conv_args(csr, v, geometry, M, F, W, dtype, C_in, C_out));
+    if (!csc || !csc->col_ptr || csc->n_cols != csr->n_cols ||
+        (csr->nnz_bound > 0 && (!csc->row_idx || !csc->edge_perm)))
+        return fail(SBC_ERR_INVALID_ARG, "csc is null or does not match csr");
+    if (!dY && csr->n_rows > 0) return fail(SBC_ERR_INVALID_ARG, "dY is null");
+    const int32_t n_out = csr->n_rows, n_in = csr->n_cols;
+    order = sbc_resolve_order(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order);
+    size_t need = 0;
+    ConvWs ws = carve_conv(workspace, n_out, n_in, csr->nnz_bound, M, C_in, C_out, order, &need);
+    if (!workspace || workspace_bytes < need)
+        return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_conv_workspace_size()");
+    const bool bf = dtype == SBC_BF16;
+    const float *vv = v;
+    if (!vv) {
+        SBC_TRY(basis_eval_launch(csr, geometry, ws.v, stream));
+        vv = ws.v;
+    }
+    const int64_t K1 = (int64_t)M * C_in, K2 = (int64_t)M * C_out;
+    if (order == SBC_ORDER_SPMM_FIRST) {
+        SBC_TRY(spmm(n_out, csr->row_ptr, csr->col_idx, nullptr, vv, M, F, bf, C_in, false,
+                     ws.inter, stream, "bwd_spmm"));
+        if (dW)  // dW [M*C_in, C_out] = G^T dY
+            SBC_TRY(gemm(ws.inter, false, 1, K1, dY, bf, C_out, 1, dW, C_out, 1, (int32_t)K1,
+                         C_out, n_out, ws.partial, stream, "bwd_gemm_dw"));
+        if (dF) {  // dG = dY W_flat^T, then dF = N^T dG
+            SBC_TRY(gemm(dY, bf, C_out, 1, W, bf, 1, C_out, ws.inter2, K1, 1, n_out, (int32_t)K1,
+                         C_out, ws.partial, stream, "bwd_gemm_dg"));
+            SBC_TRY(spmm(n_in, csc->col_ptr, csc->row_idx, csc->edge_perm, vv, M, ws.inter2,
+                         false, C_in, true, dF, stream, "bwd_spmm_t"));
+        }
+    } else {
+        SBC_TRY(spmm(n_in, csc->col_ptr, csc->row_idx, csc->edge_perm, vv, M, dY, bf, C_out,
+                     false, ws.inter, stream, "bwd_spmm_t_expand"));
+        if (dF) {  // Wt [M, C_out, C_in]; dF = D Wt
+            SBC_TRY(permute_w(W, bf, M, C_in, C_out, (int64_t)C_out * C_in, 1, C_in, ws.wperm,
+                              stream));
+            SBC_TRY(gemm(ws.inter, false, K2, 1, ws.wperm, false, C_in, 1, dF, C_in, 1, n_in,
+                         C_in, K2, ws.partial, stream, "bwd_gemm_df"));
+        }
+        if (dW) {  // dW' [C_in, M*C_out] = F^T D, then back to [M, C_in, C_out]
+            SBC_TRY(gemm(F, bf, 1, C_in, ws.inter, false, K2, 1, ws.dwperm, K2, 1, C_in,
+                         (int32_t)K2, n_in, ws.partial, stream, "bwd_gemm_dw_t"));
+            // dwperm element (c, m, p) at c*M*C_out + m*C_out + p -> dW (m, c, p)
+            SBC_TRY(permute_w_back(ws.dwperm, M, C_in, C_out, dW, stream));
+        }
+    }
+    return SBC_OK;
+}

@@ -1,0 +1,304 @@
+// Backwards-in-time pixel-block neighbourhoods of an event stream
+// (Section 3.2: a small spatial neighbourhood extending backwards in time).
+//
+// Pipeline (all on the caller's stream):
+//   1. per-pixel event lists in stream order: count per pixel, scan, scatter,
+//      then each pixel's list is sorted by event index (lists are short);
+//      the lists carry the event timestamps alongside the indices;
+//   2. count pass, one thread per event i: for each pixel q of its block, the
+//      events of q with index < i and t >= t_i - window form one contiguous
+//      run of q's list (indices and times both ascend along it), found by two
+//      binary searches; the row length is the sum of the run lengths;
+//   3. scan -> row_ptr;
+//   4. fill pass: the (2h+1)^2 runs are merged by index into the row.
+// Events with a pixel outside the sensor get no neighbours and are in no
+// list; a decreasing timestamp raises a flag.  Neither can make a kernel
+// read or write out of bounds.
+#include <climits>
+
+#include "common.hpp"
+
+namespace sbc {
+namespace {
+
+constexpr int kMaxBlock = 7;  // half_extent <= 3: at most 7x7 pixels
+
+__device__ __forceinline__ bool valid_pixel(int32_t x, int32_t y, int32_t W, int32_t H) {
+    return x >= 0 && x < W && y >= 0 && y < H;
+}
+
+__global__ void pixel_count_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
+                                   const int32_t *__restrict__ t, int32_t n, int32_t W, int32_t H,
+                                   int32_t *__restrict__ pix_count, uint32_t *status) {
+    int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    int32_t x = px[i], y = py[i];
+    if (!valid_pixel(x, y, W, H)) {
+        atomicOr(status, (uint32_t)kFlagOutOfRange);
+        return;
+    }
+    if (i > 0 && t[i] < t[i - 1]) atomicOr(status, (uint32_t)kFlagUnsorted);
+    atomicAdd(&pix_count[(int64_t)y * W + x], 1);
+}
+
+__global__ void pixel_scatter_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
+                                     int32_t n, int32_t W, int32_t H, int32_t *__restrict__ cursor,
+                                     int32_t *__restrict__ list_unsorted) {
+    int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    int32_t x = px[i], y = py[i];
+    if (!valid_pixel(x, y, W, H)) return;
+    int32_t pos = atomicAdd(&cursor[(int64_t)y * W + x], 1);
+    list_unsorted[pos] = i;
+}
+
+// Timestamps alongside the sorted lists.  Only the first pix_start[npix]
+// list slots are filled (events off the sensor are not listed).
+__global__ void list_times_kernel(const int32_t *__restrict__ list, const int32_t *__restrict__ t,
+                                  const int32_t *__restrict__ pix_start, int64_t npix,
+                                  int32_t *__restrict__ list_t) {
+    int32_t p = blockIdx.x * blockDim.x + threadIdx.x;
+    if (p >= pix_start[npix]) return;
+    list_t[p] = t[list[p]];
+}
+
+// In [lo, hi) of `a` (ascending), first position with a[pos] >= v.
+__device__ __forceinline__ int32_t lower_bound(const int32_t *__restrict__ a, int32_t lo,
+                                               int32_t hi, int32_t v) {
+    while (lo < hi) {
+        int32_t mid = lo + ((hi - lo) >> 1);
+        if (a[mid] < v) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
+
+struct Runs {
+    int32_t lo[kMaxBlock * kMaxBlock];
+    int32_t hi[kMaxBlock * kMaxBlock];
+};
+
+template <int kSide>
+__device__ __forceinline__ int32_t find_runs(int32_t i, int32_t x, int32_t y, int32_t ti,
+                                             int32_t W, int32_t H, int64_t window,
+                                             const int32_t *__restrict__ pix_start,
+                                             const int32_t *__restrict__ list,
+                                             const int32_t *__restrict__ list_t, Runs &r) {
+    constexpr int h = kSide / 2;
+    // t_j >= t_i - window, computed without int32 overflow
+    const int64_t tmin64 = (int64_t)ti - window;
+    const int32_t tmin = tmin64 < (int64_t)INT_MIN ? INT_MIN : (int32_t)tmin64;
+    int32_t count = 0;
+#pragma unroll
+    for (int k = 0; k < kSide * kSide; ++k) {
+        const int32_t qx = x + (k % kSide) - h, qy = y + (k / kSide) - h;
+        int32_t lo = 0, hi = 0;
+        if (valid_pixel(qx, qy, W, H)) {
+            const int64_t q = (int64_t)qy * W + qx;
+            const int32_t s = pix_start[q], e = pix_start[q + 1];
+            hi = lower_bound(list, s, e, i);        // entries with index < i
+            lo = lower_bound(list_t, s, hi, tmin);  // ... and t >= t_i - window
+        }
+        r.lo[k] = lo;
+        r.hi[k] = hi;
+        count += hi - lo;
+    }
+    return count;
+}
+
+template <int kSide>
+__global__ void __launch_bounds__(256)
+    event_rows_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
+                      const int32_t *__restrict__ t, int32_t n, int32_t W, int32_t H,
+                      int32_t window, const int32_t *__restrict__ pix_start,
+                      const int32_t *__restrict__ list, const int32_t *__restrict__ list_t,
+                      int32_t *__restrict__ row_len, const int32_t *__restrict__ row_ptr,
+                      int32_t *__restrict__ col_idx, int64_t col_capacity) {
+    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int32_t x = px[i], y = py[i];
+    if (!valid_pixel(x, y, W, H)) {
+        if (row_len) row_len[i] = 0;
+        return;
+    }
+    Runs r;
+    const int32_t cnt = find_runs<kSide>(i, x, y, t[i], W, H, (int64_t)window, pix_start, list,
+                                         list_t, r);
+    if (row_len) {
+        row_len[i] = cnt;
+        return;
+    }
+    // merge the runs by event index (each run ascends; runs are disjoint)
+    int64_t dst = row_ptr[i];
+    int32_t head[kSide * kSide];
+#pragma unroll
+    for (int k = 0; k < kSide * kSide; ++k) head[k] = r.lo[k] < r.hi[k] ? list[r.lo[k]] : INT_MAX;
+    for (int32_t out = 0; out < cnt; ++out) {
+        int32_t best = INT_MAX, arg = 0;
+#pragma unroll
+        for (int k = 0; k < kSide * kSide; ++k) {
+            if (head[k] < best) {
+                best = head[k];
+                arg = k;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kSide * kSide; ++k) {
+            if (k == arg) {
+                ++r.lo[k];
+                head[k] = r.lo[k] < r.hi[k] ? list[r.lo[k]] : INT_MAX;
+            }
+        }
+        if (dst < col_capacity) col_idx[dst] = best;
+        ++dst;
+    }
+}
+
+struct EventsWs {
+    int32_t *pix_count;
+    int32_t *pix_start;
+    int32_t *cursor;
+    int32_t *list_unsorted;
+    int32_t *list;
+    int32_t *list_t;
+    int32_t *scratch;
+    int32_t *row_len;
+    int64_t *total;
+    uint32_t *status;
+    void *scan_ws;
+};
+
+EventsWs carve_events(void *base, int32_t n, int64_t npix, size_t *bytes) {
+    Carver cv(base);
+    EventsWs w;
+    w.pix_count = cv.take<int32_t>(npix);
+    w.pix_start = cv.take<int32_t>(npix + 1);
+    w.cursor = cv.take<int32_t>(npix + 1);
+    w.list_unsorted = cv.take<int32_t>(n);
+    w.list = cv.take<int32_t>(n);
+    w.list_t = cv.take<int32_t>(n);
+    w.scratch = cv.take<int32_t>(n);
+    w.row_len = cv.take<int32_t>(n);
+    w.total = cv.take<int64_t>(2);
+    w.status = cv.take<uint32_t>(4);
+    w.scan_ws = cv.take<char>(scan_workspace_bytes(npix > n ? npix : n));
+    if (bytes) *bytes = cv.used;
+    return w;
+}
+
+__global__ void copy_kernel(const int32_t *src, int32_t *dst, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+
+template <int kSide>
+void launch_rows(int32_t n, const int32_t *px, const int32_t *py, const int32_t *t, int32_t W,
+                 int32_t H, int32_t window, const EventsWs &ws, int32_t *row_len,
+                 const int32_t *row_ptr, int32_t *col_idx, int64_t cap, hipStream_t stream) {
+    hipLaunchKernelGGL((event_rows_kernel<kSide>), dim3(grid_for(n, 256)), dim3(256), 0, stream,
+                       px, py, t, n, W, H, window, ws.pix_start, ws.list, ws.list_t, row_len,
+                       row_ptr, col_idx, cap);
+}
+
+sbc_status rows_dispatch(int32_t half_extent, int32_t n, const int32_t *px, const int32_t *py,
+                         const int32_t *t, int32_t W, int32_t H, int32_t window,
+                         const EventsWs &ws, int32_t *row_len, const int32_t *row_ptr,
+                         int32_t *col_idx, int64_t cap, hipStream_t stream) {
+    const char *name = row_len ? "events_count" : "events_fill";
+    trace_before(name, stream);
+    switch (half_extent) {
+        case 0: launch_rows<1>(n, px, py, t, W, H, window, ws, row_len, row_ptr, col_idx, cap, stream); break;
+        case 1: launch_rows<3>(n, px, py, t, W, H, window, ws, row_len, row_ptr, col_idx, cap, stream); break;
+        case 2: launch_rows<5>(n, px, py, t, W, H, window, ws, row_len, row_ptr, col_idx, cap, stream); break;
+        case 3: launch_rows<7>(n, px, py, t, W, H, window, ws, row_len, row_ptr, col_idx, cap, stream); break;
+        default: return fail(SBC_ERR_UNSUPPORTED, "half_extent must be 0..3");
+    }
+    SBC_LAUNCH_CHECK();
+    trace_after(name, stream);
+    return SBC_OK;
+}
+
+}  // namespace
+}  // namespace sbc
+
+using namespace sbc;
+
+extern "C" size_t sbc_events_workspace_size(int32_t n, int32_t width, int32_t height) {
+    size_t bytes = 0;
+    int64_t npix = (int64_t)(width > 0 ? width : 0) * (height > 0 ? height : 0);
+    carve_events(nullptr, n > 0 ? n : 0, npix, &bytes);
+    return bytes;
+}
+
+extern "C" sbc_status sbc_neighbour_search_events(const int32_t *px, const int32_t *py,
+                                                  const int32_t *t, int32_t n, int32_t width,
+                                                  int32_t height, int32_t half_extent,
+                                                  int32_t window, int32_t *row_ptr,
+                                                  int32_t *col_idx, int64_t col_capacity,
+                                                  int64_t *nnz_host, void *workspace,
+                                                  size_t workspace_bytes, hipStream_t stream) {
+    clear_error();
+    if (n < 0 || width <= 0 || height <= 0)
+        return fail(SBC_ERR_INVALID_ARG, "n must be >= 0, width and height > 0");
+    if ((int64_t)width * height > (int64_t)INT32_MAX)
+        return fail(SBC_ERR_INVALID_ARG, "width * height must be < 2^31");
+    if (half_extent < 0 || half_extent > 3)
+        return fail(SBC_ERR_UNSUPPORTED, "half_extent must be 0..3");
+    if (window < 0) return fail(SBC_ERR_INVALID_ARG, "window must be >= 0");
+    if (!row_ptr || (n > 0 && (!px || !py || !t)))
+        return fail(SBC_ERR_INVALID_ARG, "null pointer argument");
+    if (col_capacity < 0 || (col_capacity > 0 && !col_idx))
+        return fail(SBC_ERR_INVALID_ARG, "col_idx is null or col_capacity < 0");
+    const int64_t npix = (int64_t)width * height;
+    size_t need = 0;
+    EventsWs ws = carve_events(workspace, n, npix, &need);
+    if (!workspace || workspace_bytes < need)
+        return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_events_workspace_size()");
+
+    SBC_TRY(fill_i32(reinterpret_cast<int32_t *>(ws.status), 0, 1, stream));
+    SBC_TRY(fill_i32(ws.pix_count, 0, npix, stream));
+    if (n > 0) {
+        hipLaunchKernelGGL(pixel_count_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream, px, py,
+                           t, n, width, height, ws.pix_count, ws.status);
+        SBC_LAUNCH_CHECK();
+    }
+    SBC_TRY(exclusive_scan_i32(ws.pix_count, ws.pix_start, npix, ws.total + 1, ws.scan_ws, stream));
+    if (n > 0) {
+        int g = grid_for(npix + 1, 256);
+        hipLaunchKernelGGL(copy_kernel, dim3(g > 4096 ? 4096 : g), dim3(256), 0, stream,
+                           ws.pix_start, ws.cursor, npix + 1);
+        SBC_LAUNCH_CHECK();
+        hipLaunchKernelGGL(pixel_scatter_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream, px,
+                           py, n, width, height, ws.cursor, ws.list_unsorted);
+        SBC_LAUNCH_CHECK();
+        // order each pixel's list by event index; the payload is unused
+        SBC_TRY(segmented_sort_pairs(ws.pix_start, (int32_t)npix, ws.list_unsorted,
+                                     ws.list_unsorted, ws.list, ws.scratch, stream));
+        // listed events = pix_start[npix] <= n; the kernel is sized by n and
+        // reads the true count from the end of the scan
+        hipLaunchKernelGGL(list_times_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream,
+                           ws.list, t, ws.pix_start, npix, ws.list_t);
+        SBC_LAUNCH_CHECK();
+        SBC_TRY(rows_dispatch(half_extent, n, px, py, t, width, height, window, ws, ws.row_len,
+                              nullptr, nullptr, 0, stream));
+    }
+    SBC_TRY(exclusive_scan_i32(ws.row_len, row_ptr, n, ws.total, ws.scan_ws, stream));
+    if (nnz_host) {
+        int64_t host[2];
+        uint32_t st = 0;
+        SBC_HIP_TRY(hipMemcpyAsync(host, ws.total, sizeof(host), hipMemcpyDeviceToHost, stream));
+        SBC_HIP_TRY(hipMemcpyAsync(&st, ws.status, sizeof(st), hipMemcpyDeviceToHost, stream));
+        SBC_HIP_TRY(hipStreamSynchronize(stream));
+        *nnz_host = host[0];
+        if (st & kFlagOutOfRange) return fail(SBC_ERR_OUT_OF_RANGE, "pixel outside the sensor");
+        if (st & kFlagUnsorted) return fail(SBC_ERR_UNSORTED, "timestamps must be non-decreasing");
+        if (host[0] > (int64_t)INT32_MAX) return fail(SBC_ERR_OVERFLOW, "2^31 or more edges");
+        if (host[0] > col_capacity)
+            return fail(SBC_ERR_CAPACITY, "col_capacity " + std::to_string(col_capacity) +
+                                              " < E = " + std::to_string(host[0]));
+    }
+    if (n > 0 && col_capacity > 0)
+        SBC_TRY(rows_dispatch(half_extent, n, px, py, t, width, height, window, ws, nullptr,
+                              row_ptr, col_idx, col_capacity, stream));
+    return SBC_OK;
+}

@@ -1,0 +1,488 @@
+// Ball (optionally k-capped) neighbourhoods of a ragged batch of point clouds
+// (Section 3.1, "Neighborhoods"; "Ragged Batching").
+//
+// Pipeline (all on the caller's stream):
+//   1. cell key of every input point: hash(cloud, floor(x / h)) with cell
+//      edge h = r (1 + 2^-10) evaluated in float64, so that any pair with
+//      float32 d2 < r*r lies in the same or an adjacent cell;
+//   2. counting sort of the inputs by key (count, scan, scatter) into a
+//      cell table of packed (x, y, z, j) records;
+//   3. count pass, one wave per output row: the 27 adjacent cells are hashed,
+//      duplicate buckets dropped, candidates tested by the canonical float32
+//      distance; row length = min(in-ball count, k_cap);
+//   4. scan of the row lengths -> row_ptr (E is read back only on request);
+//   5. fill pass, one wave per row: in-ball (d2, j) pairs are staged in LDS,
+//      truncated to the k_cap smallest by rank on (d2, j), and written in
+//      ascending j by rank on j.  Rows longer than the LDS stage rank against
+//      the candidate cells directly (same result, slower).
+// The hash only prunes: buckets shared by distinct cells or clouds add
+// candidates that the exact distance and cloud-range tests reject.
+#include <cfloat>
+#include <climits>
+
+#include "common.hpp"
+
+namespace sbc {
+namespace {
+
+constexpr int kWaves = 4;              // waves per block, one output row per wave
+constexpr int kStage = 512;            // in-ball candidates staged per wave in LDS
+constexpr double kCellMargin = 1.0 + 1.0 / 1024.0;
+
+struct PointRec {
+    float x, y, z;
+    int32_t j;
+};
+
+// Make this wave's LDS writes visible to all of its lanes before later reads.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    __builtin_amdgcn_wave_barrier();
+}
+
+__device__ __forceinline__ uint32_t hash_cell(int32_t b, int32_t cx, int32_t cy, int32_t cz) {
+    uint32_t h = (uint32_t)b * 0x9E3779B1u;
+    h ^= (uint32_t)cx * 0x85EBCA77u + 0x165667B1u + (h << 6) + (h >> 2);
+    h ^= (uint32_t)cy * 0xC2B2AE3Du + 0x27D4EB2Fu + (h << 6) + (h >> 2);
+    h ^= (uint32_t)cz * 0x61C88647u + 0x9E3779B9u + (h << 6) + (h >> 2);
+    h ^= h >> 15;
+    h *= 0x2C1B3C6Du;
+    h ^= h >> 12;
+    return h;
+}
+
+__device__ __forceinline__ int32_t cell_coord(float x, double inv_h) {
+    double c = floor((double)x * inv_h);
+    // clamping is monotone, so adjacent cells stay adjacent; NaN -> 0
+    if (!(c == c)) return 0;
+    if (c > 1073741824.0) c = 1073741824.0;
+    if (c < -1073741824.0) c = -1073741824.0;
+    return (int32_t)c;
+}
+
+// index b with splits[b] <= i < splits[b+1] (splits non-decreasing, n_batch+1 long)
+__device__ __forceinline__ int32_t cloud_of(const int32_t *splits, int32_t n_batch, int32_t i) {
+    int32_t lo = 0, hi = n_batch;  // answer in [0, n_batch)
+    while (hi - lo > 1) {
+        int32_t mid = (lo + hi) >> 1;
+        if (splits[mid] <= i) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+// Canonical float32 squared distance: no contraction, fixed association.
+__device__ __forceinline__ float sq_dist(float ax, float ay, float az, float bx, float by,
+                                         float bz) {
+    float dx = __fsub_rn(ax, bx);
+    float dy = __fsub_rn(ay, by);
+    float dz = __fsub_rn(az, bz);
+    return __fadd_rn(__fadd_rn(__fmul_rn(dx, dx), __fmul_rn(dy, dy)), __fmul_rn(dz, dz));
+}
+
+__global__ void check_splits_kernel(const int32_t *in_splits, const int32_t *out_splits,
+                                    int32_t n_batch, int32_t n_in, int32_t n_out,
+                                    uint32_t *status) {
+    int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b > n_batch) return;
+    bool bad = false;
+    if (b == 0) bad = in_splits[0] != 0 || out_splits[0] != 0;
+    if (b == n_batch) bad = bad || in_splits[b] != n_in || out_splits[b] != n_out;
+    if (b > 0) bad = bad || in_splits[b] < in_splits[b - 1] || out_splits[b] < out_splits[b - 1];
+    if (bad) atomicOr(status, (uint32_t)kFlagBadSplits);
+}
+
+__global__ void key_kernel(const float *__restrict__ x_in, int32_t n_in,
+                           const int32_t *__restrict__ in_splits, int32_t n_batch, double inv_h,
+                           uint32_t table_mask, uint32_t *__restrict__ keys,
+                           int32_t *__restrict__ counts) {
+    int32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= n_in) return;
+    int32_t b = cloud_of(in_splits, n_batch, j);
+    float x = x_in[3 * (int64_t)j], y = x_in[3 * (int64_t)j + 1], z = x_in[3 * (int64_t)j + 2];
+    uint32_t key = hash_cell(b, cell_coord(x, inv_h), cell_coord(y, inv_h), cell_coord(z, inv_h)) &
+                   table_mask;
+    keys[j] = key;
+    atomicAdd(&counts[key], 1);
+}
+
+__global__ void scatter_kernel(const float *__restrict__ x_in, int32_t n_in,
+                               const uint32_t *__restrict__ keys, int32_t *__restrict__ cursor,
+                               PointRec *__restrict__ table) {
+    int32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= n_in) return;
+    int32_t pos = atomicAdd(&cursor[keys[j]], 1);
+    PointRec r;
+    r.x = x_in[3 * (int64_t)j];
+    r.y = x_in[3 * (int64_t)j + 1];
+    r.z = x_in[3 * (int64_t)j + 2];
+    r.j = j;
+    table[pos] = r;
+}
+
+struct RowCtx {
+    float qx, qy, qz;
+    int32_t j_lo, j_hi;  // input range of the row's cloud
+    float r2;
+};
+
+// Per wave: bucket ranges of the 27 cells around the query, duplicates
+// removed; lane k < 27 holds cell k.  Returns the candidate count; lane k's
+// range start and its exclusive offset into the flattened candidate list go
+// to lds_start/lds_off (27 entries each).
+__device__ int32_t gather_buckets(const RowCtx &c, int32_t b, double inv_h, uint32_t table_mask,
+                                  const int32_t *__restrict__ cell_start, int32_t *lds_start,
+                                  int32_t *lds_off) {
+    const int lane = threadIdx.x & 63;
+    int32_t cx = cell_coord(c.qx, inv_h), cy = cell_coord(c.qy, inv_h), cz = cell_coord(c.qz, inv_h);
+    uint32_t bucket = 0xFFFFFFFFu;
+    int32_t s = 0, len = 0;
+    if (lane < 27) {
+        int32_t dx = lane % 3 - 1, dy = (lane / 3) % 3 - 1, dz = lane / 9 - 1;
+        bucket = hash_cell(b, cx + dx, cy + dy, cz + dz) & table_mask;
+    }
+    bool dup = false;
+    for (int q = 0; q < 27; ++q) {
+        uint32_t bq = __shfl(bucket, q, 64);
+        if (q < lane && bq == bucket) dup = true;
+    }
+    if (lane < 27 && !dup) {
+        s = cell_start[bucket];
+        len = cell_start[bucket + 1] - s;
+    }
+    // exclusive scan of len over the wave
+    int32_t incl = len;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        int32_t y = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += y;
+    }
+    int32_t total = __shfl(incl, 63, 64);
+    if (lane < 27) {
+        lds_start[lane] = s;
+        lds_off[lane] = incl - len;
+    }
+    return total;
+}
+
+// Candidate c (0 <= c < total) of the flattened bucket list -> table position.
+__device__ __forceinline__ int32_t candidate_pos(int32_t c, const int32_t *lds_start,
+                                                 const int32_t *lds_off) {
+    int32_t k = 0;
+#pragma unroll
+    for (int q = 1; q < 27; ++q) k = (lds_off[q] <= c) ? q : k;
+    // several lanes may share an offset when buckets are empty or duplicate:
+    // the largest q with off <= c has a non-empty range containing c
+    return lds_start[k] + (c - lds_off[k]);
+}
+
+__device__ __forceinline__ bool in_ball(const RowCtx &c, const PointRec &p, float *d2) {
+    if (p.j < c.j_lo || p.j >= c.j_hi) return false;
+    float d = sq_dist(c.qx, c.qy, c.qz, p.x, p.y, p.z);
+    *d2 = d;
+    return d < c.r2;
+}
+
+__device__ __forceinline__ bool key_less(float da, int32_t ja, float db, int32_t jb) {
+    return da < db || (da == db && ja < jb);
+}
+
+template <bool kFill>
+__global__ void __launch_bounds__(kWaves * 64)
+    rows_kernel(const float *__restrict__ x_out, int32_t n_out,
+                const int32_t *__restrict__ in_splits, const int32_t *__restrict__ out_splits,
+                int32_t n_batch, float radius, int32_t k_cap, double inv_h, uint32_t table_mask,
+                const int32_t *__restrict__ cell_start, const PointRec *__restrict__ table,
+                int32_t *__restrict__ row_len, const int32_t *__restrict__ row_ptr,
+                int32_t *__restrict__ col_idx, int64_t col_capacity) {
+    __shared__ int32_t s_start[kWaves][27];
+    __shared__ int32_t s_off[kWaves][27];
+    __shared__ float s_d2[kFill ? kWaves : 1][kFill ? kStage : 1];
+    __shared__ int32_t s_j[kFill ? kWaves : 1][kFill ? kStage : 1];
+    __shared__ int32_t s_keep[kFill ? kWaves : 1][kFill ? kStage : 1];
+
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    const int32_t i = blockIdx.x * kWaves + w;
+    if (i >= n_out) return;  // whole wave leaves together: no block barrier below
+
+    RowCtx c;
+    c.qx = x_out[3 * (int64_t)i];
+    c.qy = x_out[3 * (int64_t)i + 1];
+    c.qz = x_out[3 * (int64_t)i + 2];
+    const int32_t b = cloud_of(out_splits, n_batch, i);
+    c.j_lo = in_splits[b];
+    c.j_hi = in_splits[b + 1];
+    c.r2 = __fmul_rn(radius, radius);
+
+    const int32_t total = gather_buckets(c, b, inv_h, table_mask, cell_start, s_start[w], s_off[w]);
+    wave_lds_sync();
+
+    if (!kFill) {
+        int32_t n = 0;
+        for (int32_t base = 0; base < total; base += 64) {
+            int32_t cc = base + lane;
+            bool hit = false;
+            if (cc < total) {
+                PointRec p = table[candidate_pos(cc, s_start[w], s_off[w])];
+                float d2;
+                hit = in_ball(c, p, &d2);
+            }
+            n += __popcll(__ballot(hit));
+        }
+        if (lane == 0) row_len[i] = (k_cap > 0 && n > k_cap) ? k_cap : n;
+        return;
+    }
+
+    // ---- fill pass: stage the in-ball candidates
+    int32_t n = 0;
+    for (int32_t base = 0; base < total; base += 64) {
+        int32_t cc = base + lane;
+        bool hit = false;
+        float d2 = 0.f;
+        int32_t j = 0;
+        if (cc < total) {
+            PointRec p = table[candidate_pos(cc, s_start[w], s_off[w])];
+            hit = in_ball(c, p, &d2);
+            j = p.j;
+        }
+        uint64_t mask = __ballot(hit);
+        int32_t slot = n + __popcll(mask & ((1ull << lane) - 1ull));
+        if (hit && slot < kStage) {
+            s_d2[w][slot] = d2;
+            s_j[w][slot] = j;
+        }
+        n += __popcll(mask);
+    }
+    wave_lds_sync();
+    const int32_t out0 = row_ptr[i];
+    const bool capped = k_cap > 0 && n > k_cap;
+    const int32_t n_keep = capped ? k_cap : n;
+
+    if (n <= kStage) {
+        // keep flag: rank on (d2, j) below k_cap
+        for (int32_t a = lane; a < n; a += 64) {
+            int keep = 1;
+            if (capped) {
+                float da = s_d2[w][a];
+                int32_t ja = s_j[w][a];
+                int32_t rank = 0;
+                for (int32_t q = 0; q < n; ++q) rank += key_less(s_d2[w][q], s_j[w][q], da, ja);
+                keep = rank < k_cap;
+            }
+            s_keep[w][a] = keep;
+        }
+        wave_lds_sync();
+        for (int32_t a = lane; a < n; a += 64) {
+            if (!s_keep[w][a]) continue;
+            int32_t ja = s_j[w][a];
+            int32_t pos = 0;
+            for (int32_t q = 0; q < n; ++q) pos += (s_keep[w][q] && s_j[w][q] < ja) ? 1 : 0;
+            int64_t dst = (int64_t)out0 + pos;
+            if (dst < col_capacity) col_idx[dst] = ja;
+        }
+        return;
+    }
+
+    // ---- long rows (more in-ball candidates than the LDS stage holds).
+    // Keys (d2, j) are distinct; order them as the 64-bit integer
+    // (bits(d2) << 32) | j (d2 >= 0, so its bit pattern orders like its value).
+    uint64_t threshold = ~0ull;  // keep every in-ball key <= threshold
+    if (capped) {
+        // smallest K with #{key <= K} >= k_cap, by bisection on K
+        uint64_t lo = 0, hi = ~0ull;
+        while (lo < hi) {
+            const uint64_t mid = lo + ((hi - lo) >> 1);
+            int32_t cnt = 0;
+            for (int32_t base = 0; base < total; base += 64) {
+                int32_t cc = base + lane;
+                bool le = false;
+                if (cc < total) {
+                    PointRec p = table[candidate_pos(cc, s_start[w], s_off[w])];
+                    float d2;
+                    if (in_ball(c, p, &d2))
+                        le = (((uint64_t)__float_as_uint(d2) << 32) | (uint32_t)p.j) <= mid;
+                }
+                cnt += __popcll(__ballot(le));
+            }
+            if (cnt >= k_cap) hi = mid; else lo = mid + 1;
+        }
+        threshold = lo;
+    }
+    // stage the kept column indices when they fit, else rank against the cells
+    const bool staged = n_keep <= kStage;
+    int32_t m = 0;
+    for (int32_t base = 0; base < total; base += 64) {
+        int32_t cc = base + lane;
+        bool keep = false;
+        int32_t j = 0;
+        if (cc < total) {
+            PointRec p = table[candidate_pos(cc, s_start[w], s_off[w])];
+            float d2;
+            if (in_ball(c, p, &d2)) {
+                keep = (((uint64_t)__float_as_uint(d2) << 32) | (uint32_t)p.j) <= threshold;
+                j = p.j;
+            }
+        }
+        uint64_t mask = __ballot(keep);
+        if (staged) {
+            int32_t slot = m + __popcll(mask & ((1ull << lane) - 1ull));
+            if (keep) s_j[w][slot] = j;
+        } else if (keep) {
+            int32_t pos = 0;
+            for (int32_t q = 0; q < total; ++q) {
+                PointRec o = table[candidate_pos(q, s_start[w], s_off[w])];
+                float db;
+                if (in_ball(c, o, &db) && o.j < j &&
+                    (((uint64_t)__float_as_uint(db) << 32) | (uint32_t)o.j) <= threshold)
+                    ++pos;
+            }
+            int64_t dst = (int64_t)out0 + pos;
+            if (dst < col_capacity) col_idx[dst] = j;
+        }
+        m += __popcll(mask);
+    }
+    if (staged) {
+        wave_lds_sync();
+        for (int32_t a = lane; a < m; a += 64) {
+            int32_t ja = s_j[w][a];
+            int32_t pos = 0;
+            for (int32_t q = 0; q < m; ++q) pos += (s_j[w][q] < ja) ? 1 : 0;
+            int64_t dst = (int64_t)out0 + pos;
+            if (dst < col_capacity) col_idx[dst] = ja;
+        }
+    }
+}
+
+uint32_t table_size_for(int32_t n_in) {
+    uint32_t t = 1024;
+    while (t < 2u * (uint32_t)(n_in > 0 ? n_in : 1) && t < (1u << 30)) t <<= 1;
+    return t;
+}
+
+struct PointsWs {
+    uint32_t *keys;
+    int32_t *cell_count;
+    int32_t *cell_start;
+    int32_t *cursor;
+    PointRec *table;
+    int32_t *row_len;
+    int64_t *total;
+    uint32_t *status;
+    void *scan_ws;
+};
+
+PointsWs carve_points(void *base, int32_t n_in, int32_t n_out, int32_t /*n_batch*/, size_t *bytes) {
+    Carver cv(base);
+    const uint32_t T = table_size_for(n_in);
+    PointsWs w;
+    w.keys = cv.take<uint32_t>(n_in);
+    w.cell_count = cv.take<int32_t>(T);
+    w.cell_start = cv.take<int32_t>((size_t)T + 1);
+    w.cursor = cv.take<int32_t>((size_t)T + 1);
+    w.table = cv.take<PointRec>(n_in);
+    w.row_len = cv.take<int32_t>(n_out);
+    w.total = cv.take<int64_t>(2);
+    w.status = cv.take<uint32_t>(4);
+    int64_t m = (int64_t)T > (int64_t)n_out ? (int64_t)T : (int64_t)n_out;
+    w.scan_ws = cv.take<char>(scan_workspace_bytes(m));
+    if (bytes) *bytes = cv.used;
+    return w;
+}
+
+__global__ void copy_i32_kernel(const int32_t *src, int32_t *dst, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+
+}  // namespace
+}  // namespace sbc
+
+using namespace sbc;
+
+extern "C" size_t sbc_points_workspace_size(int32_t n_in, int32_t n_out, int32_t n_batch) {
+    size_t bytes = 0;
+    carve_points(nullptr, n_in < 0 ? 0 : n_in, n_out < 0 ? 0 : n_out, n_batch, &bytes);
+    return bytes;
+}
+
+extern "C" sbc_status sbc_neighbour_search_points(
+    const float *x_in, int32_t n_in, const int32_t *in_splits, const float *x_out, int32_t n_out,
+    const int32_t *out_splits, int32_t n_batch, float radius, int32_t k_cap, int32_t *row_ptr,
+    int32_t *col_idx, int64_t col_capacity, int64_t *nnz_host, void *workspace,
+    size_t workspace_bytes, hipStream_t stream) {
+    clear_error();
+    if (n_in < 0 || n_out < 0 || n_batch < 1)
+        return fail(SBC_ERR_INVALID_ARG, "n_in, n_out must be >= 0 and n_batch >= 1");
+    if (!(radius > 0.f) || !(radius < FLT_MAX))
+        return fail(SBC_ERR_INVALID_ARG, "radius must be finite and > 0");
+    if (!row_ptr || !in_splits || !out_splits || (n_in > 0 && !x_in) || (n_out > 0 && !x_out))
+        return fail(SBC_ERR_INVALID_ARG, "null pointer argument");
+    if (col_capacity < 0 || (col_capacity > 0 && !col_idx))
+        return fail(SBC_ERR_INVALID_ARG, "col_idx is null or col_capacity < 0");
+    size_t need = 0;
+    PointsWs ws = carve_points(workspace, n_in, n_out, n_batch, &need);
+    if (!workspace || workspace_bytes < need)
+        return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_points_workspace_size()");
+
+    const uint32_t T = table_size_for(n_in);
+    const double inv_h = 1.0 / ((double)radius * kCellMargin);
+
+    SBC_TRY(fill_i32(reinterpret_cast<int32_t *>(ws.status), 0, 1, stream));
+    hipLaunchKernelGGL(check_splits_kernel, dim3(grid_for(n_batch + 1, 256)), dim3(256), 0, stream,
+                       in_splits, out_splits, n_batch, n_in, n_out, ws.status);
+    SBC_LAUNCH_CHECK();
+    SBC_TRY(fill_i32(ws.cell_count, 0, T, stream));
+    if (n_in > 0) {
+        hipLaunchKernelGGL(key_kernel, dim3(grid_for(n_in, 256)), dim3(256), 0, stream, x_in, n_in,
+                           in_splits, n_batch, inv_h, T - 1, ws.keys, ws.cell_count);
+        SBC_LAUNCH_CHECK();
+    }
+    SBC_TRY(exclusive_scan_i32(ws.cell_count, ws.cell_start, T, ws.total + 1, ws.scan_ws, stream));
+    hipLaunchKernelGGL(copy_i32_kernel, dim3(grid_for(T, 256) > 4096 ? 4096 : grid_for(T, 256)),
+                       dim3(256), 0, stream, ws.cell_start, ws.cursor, (int64_t)T);
+    SBC_LAUNCH_CHECK();
+    if (n_in > 0) {
+        hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(n_in, 256)), dim3(256), 0, stream, x_in,
+                           n_in, ws.keys, ws.cursor, ws.table);
+        SBC_LAUNCH_CHECK();
+    }
+    const int row_blocks = grid_for(n_out, kWaves);
+    if (n_out > 0) {
+        trace_before("points_count", stream);
+        hipLaunchKernelGGL((rows_kernel<false>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
+                           x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
+                           T - 1, ws.cell_start, ws.table, ws.row_len, (const int32_t *)nullptr,
+                           (int32_t *)nullptr, (int64_t)0);
+        SBC_LAUNCH_CHECK();
+        trace_after("points_count", stream);
+    }
+    SBC_TRY(exclusive_scan_i32(ws.row_len, row_ptr, n_out, ws.total, ws.scan_ws, stream));
+
+    if (nnz_host) {
+        int64_t host[2];
+        uint32_t st = 0;
+        SBC_HIP_TRY(hipMemcpyAsync(host, ws.total, sizeof(host), hipMemcpyDeviceToHost, stream));
+        SBC_HIP_TRY(hipMemcpyAsync(&st, ws.status, sizeof(st), hipMemcpyDeviceToHost, stream));
+        SBC_HIP_TRY(hipStreamSynchronize(stream));
+        *nnz_host = host[0];
+        if (st & kFlagBadSplits)
+            return fail(SBC_ERR_OUT_OF_RANGE,
+                        "splits must be non-decreasing from 0 to n_in / n_out");
+        if (host[0] > (int64_t)INT32_MAX) return fail(SBC_ERR_OVERFLOW, "2^31 or more edges");
+        if (host[0] > col_capacity)
+            return fail(SBC_ERR_CAPACITY, "col_capacity " + std::to_string(col_capacity) +
+                                              " < E = " + std::to_string(host[0]));
+    }
+    if (n_out > 0 && col_capacity > 0) {
+        trace_before("points_fill", stream);
+        hipLaunchKernelGGL((rows_kernel<true>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
+                           x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
+                           T - 1, ws.cell_start, ws.table, ws.row_len, row_ptr, col_idx,
+                           col_capacity);
+        SBC_LAUNCH_CHECK();
+        trace_after("points_fill", stream);
+    }
+    return SBC_OK;
+}

@@ -1,0 +1,224 @@
+// Device-wide exclusive prefix sums, fills and small segmented sorts.
+//
+// Scan: a three-phase blocked scan.  Each block of 256 threads owns 1024
+// consecutive items (4 per thread); block totals are scanned recursively
+// (in int64, so edge totals beyond 2^31 are detected exactly), then every
+// block rescans its items with its offset added.
+#include <climits>
+
+#include "common.hpp"
+
+namespace sbc {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kItems = 4;
+constexpr int kPerBlock = kThreads * kItems;  // 1024
+
+// Inclusive scan of one int64 per thread across a 256-thread block.
+__device__ int64_t block_inclusive_scan(int64_t x, int64_t *lds /*[4]*/, int64_t *block_total) {
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        int64_t y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
+    }
+    if (lane == 63) lds[wave] = x;
+    __syncthreads();
+    int64_t before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) {
+        int64_t s = lds[w];
+        if (w < wave) before += s;
+        total += s;
+    }
+    __syncthreads();
+    *block_total = total;
+    return x + before;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(kThreads) block_sums_kernel(const T *in, int64_t n, int64_t *sums) {
+    __shared__ int64_t lds[kThreads / 64];
+    const int64_t base = (int64_t)blockIdx.x * kPerBlock + (int64_t)threadIdx.x * kItems;
+    int64_t s = 0;
+#pragma unroll
+    for (int k = 0; k < kItems; ++k)
+        if (base + k < n) s += (int64_t)in[base + k];
+    int64_t total;
+    block_inclusive_scan(s, lds, &total);
+    if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+// Exclusive scan of `in` with per-block offsets (offsets == nullptr: zero),
+// written to `out`.  OutT int32 saturates at INT_MAX.
+template <typename InT, typename OutT>
+__global__ void __launch_bounds__(kThreads)
+    block_scan_kernel(const InT *in, int64_t n, const int64_t *offsets, OutT *out,
+                      int64_t *total64, bool write_total) {
+    __shared__ int64_t lds[kThreads / 64];
+    const int64_t base = (int64_t)blockIdx.x * kPerBlock + (int64_t)threadIdx.x * kItems;
+    int64_t v[kItems];
+    int64_t s = 0;
+#pragma unroll
+    for (int k = 0; k < kItems; ++k) {
+        v[k] = (base + k < n) ? (int64_t)in[base + k] : 0;
+        s += v[k];
+    }
+    int64_t total;
+    int64_t incl = block_inclusive_scan(s, lds, &total);
+    int64_t run = incl - s + (offsets ? offsets[blockIdx.x] : 0);
+#pragma unroll
+    for (int k = 0; k < kItems; ++k) {
+        if (base + k < n) {
+            if (sizeof(OutT) == 4)
+                out[base + k] = (OutT)(run > (int64_t)INT_MAX ? (int64_t)INT_MAX : run);
+            else
+                out[base + k] = (OutT)run;
+        }
+        run += v[k];
+    }
+    // the thread holding item n-1 (or, past it, the block's last thread) knows
+    // the grand total
+    if (write_total && blockIdx.x == gridDim.x - 1 && threadIdx.x == kThreads - 1) {
+        int64_t grand = (offsets ? offsets[blockIdx.x] : 0) + total;
+        if (sizeof(OutT) == 4)
+            out[n] = (OutT)(grand > (int64_t)INT_MAX ? (int64_t)INT_MAX : grand);
+        else
+            out[n] = (OutT)grand;
+        if (total64) *total64 = grand;
+    }
+}
+
+// In-place exclusive scan of n int64 values; `ws` holds the recursion's sums.
+sbc_status scan_i64_inplace(int64_t *a, int64_t n, char *ws, hipStream_t stream) {
+    if (n <= 0) return SBC_OK;
+    const int64_t nb = (n + kPerBlock - 1) / kPerBlock;
+    if (nb == 1) {
+        hipLaunchKernelGGL((block_scan_kernel<int64_t, int64_t>), dim3(1), dim3(kThreads), 0,
+                           stream, a, n, (const int64_t *)nullptr, a, (int64_t *)nullptr, false);
+        SBC_LAUNCH_CHECK();
+        return SBC_OK;
+    }
+    int64_t *sums = reinterpret_cast<int64_t *>(ws);
+    char *rest = ws + align_up(nb * sizeof(int64_t));
+    hipLaunchKernelGGL((block_sums_kernel<int64_t>), dim3((unsigned)nb), dim3(kThreads), 0, stream,
+                       a, n, sums);
+    SBC_LAUNCH_CHECK();
+    SBC_TRY(scan_i64_inplace(sums, nb, rest, stream));
+    hipLaunchKernelGGL((block_scan_kernel<int64_t, int64_t>), dim3((unsigned)nb), dim3(kThreads),
+                       0, stream, a, n, (const int64_t *)sums, a, (int64_t *)nullptr, false);
+    SBC_LAUNCH_CHECK();
+    return SBC_OK;
+}
+
+size_t scan_i64_ws(int64_t n) {
+    size_t bytes = 0;
+    while (n > kPerBlock) {
+        int64_t nb = (n + kPerBlock - 1) / kPerBlock;
+        bytes += align_up(nb * sizeof(int64_t));
+        n = nb;
+    }
+    return bytes;
+}
+
+__global__ void fill_kernel(int32_t *p, int32_t value, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = value;
+}
+
+// One wave per segment.  Segments of up to 64 entries are ranked in
+// registers; longer ones rank every entry against the whole segment.
+__global__ void __launch_bounds__(256)
+    segsort_kernel(const int32_t *ptr, int32_t n_segments, const int32_t *key_in,
+                   const int32_t *val_in, int32_t *key_out, int32_t *val_out) {
+    const int lane = threadIdx.x & 63;
+    const int waves_per_block = blockDim.x >> 6;
+    int64_t wave = (int64_t)blockIdx.x * waves_per_block + (threadIdx.x >> 6);
+    const int64_t n_waves = (int64_t)gridDim.x * waves_per_block;
+    for (int64_t seg = wave; seg < n_segments; seg += n_waves) {
+        const int32_t s = ptr[seg];
+        const int32_t len = ptr[seg + 1] - s;
+        if (len <= 0) continue;
+        if (len <= 64) {
+            int32_t k = INT_MAX, v = 0;
+            if (lane < len) {
+                k = key_in[s + lane];
+                v = val_in[s + lane];
+            }
+            int rank = 0;
+            for (int q = 0; q < len; ++q) {
+                int32_t kq = __shfl(k, q, 64);
+                rank += (kq < k) ? 1 : 0;
+            }
+            if (lane < len) {
+                key_out[s + rank] = k;
+                val_out[s + rank] = v;
+            }
+        } else {
+            for (int32_t a = lane; a < len; a += 64) {
+                const int32_t k = key_in[s + a];
+                int32_t rank = 0;
+                for (int32_t b = 0; b < len; ++b) rank += (key_in[s + b] < k) ? 1 : 0;
+                key_out[s + rank] = k;
+                val_out[s + rank] = val_in[s + a];
+            }
+        }
+    }
+}
+
+}  // namespace
+
+size_t scan_workspace_bytes(int64_t n) {
+    int64_t nb = (n + kPerBlock - 1) / kPerBlock;
+    return align_up((nb > 0 ? nb : 1) * sizeof(int64_t)) + scan_i64_ws(nb);
+}
+
+sbc_status fill_i32(int32_t *p, int32_t value, int64_t n, hipStream_t stream) {
+    if (n <= 0) return SBC_OK;
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, p, value, n);
+    SBC_LAUNCH_CHECK();
+    return SBC_OK;
+}
+
+sbc_status exclusive_scan_i32(const int32_t *counts, int32_t *out, int64_t n, int64_t *total64,
+                              void *ws, hipStream_t stream) {
+    if (n <= 0) {
+        // out[0] = 0 and total = 0, written by a one-block scan of nothing
+        hipLaunchKernelGGL((block_scan_kernel<int32_t, int32_t>), dim3(1), dim3(kThreads), 0,
+                           stream, counts, (int64_t)0, (const int64_t *)nullptr, out, total64,
+                           true);
+        SBC_LAUNCH_CHECK();
+        return SBC_OK;
+    }
+    const int64_t nb = (n + kPerBlock - 1) / kPerBlock;
+    char *w = static_cast<char *>(ws);
+    int64_t *sums = reinterpret_cast<int64_t *>(w);
+    char *rest = w + align_up(nb * sizeof(int64_t));
+    hipLaunchKernelGGL((block_sums_kernel<int32_t>), dim3((unsigned)nb), dim3(kThreads), 0, stream,
+                       counts, n, sums);
+    SBC_LAUNCH_CHECK();
+    SBC_TRY(scan_i64_inplace(sums, nb, rest, stream));
+    hipLaunchKernelGGL((block_scan_kernel<int32_t, int32_t>), dim3((unsigned)nb), dim3(kThreads),
+                       0, stream, counts, n, (const int64_t *)sums, out, total64, true);
+    SBC_LAUNCH_CHECK();
+    return SBC_OK;
+}
+
+sbc_status segmented_sort_pairs(const int32_t *ptr, int32_t n_segments, const int32_t *key_in,
+                                const int32_t *val_in, int32_t *key_out, int32_t *val_out,
+                                hipStream_t stream) {
+    if (n_segments <= 0) return SBC_OK;
+    int64_t blocks = ((int64_t)n_segments + 3) / 4;
+    if (blocks > 16384) blocks = 16384;
+    hipLaunchKernelGGL(segsort_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, ptr,
+                       n_segments, key_in, val_in, key_out, val_out);
+    SBC_LAUNCH_CHECK();
+    return SBC_OK;
+}
+
+}  // namespace sbc

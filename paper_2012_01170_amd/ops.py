@@ -1,0 +1,273 @@
+"""Python binding of the sbconv C ABI on torch tensors.
+
+Argument marshalling only: every step runs in the HIP library.  torch supplies
+device memory (outputs and workspaces) and the current HIP stream.  Inputs
+must already be contiguous device tensors of the documented dtypes; nothing is
+converted or moved implicitly.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+from . import _lib as L
+
+ORDERS = {"auto": L.SBC_ORDER_AUTO, "spmm_first": L.SBC_ORDER_SPMM_FIRST,
+          "gemm_first": L.SBC_ORDER_GEMM_FIRST}
+BASES = {"mono4": L.SBC_BASIS_MONO4, "mono8": L.SBC_BASIS_MONO8, "event8": L.SBC_BASIS_EVENT8}
+BASIS_M = {"mono4": 4, "mono8": 8, "event8": 8}
+
+
+def _require(t: torch.Tensor, name: str, dtype, ndim=None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device (cuda/HIP) tensor, got {t.device}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must be {ndim}-D, got shape {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _p(t: Optional[torch.Tensor]):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+class _Workspace:
+    """A 256-byte aligned device buffer of at least `nbytes`."""
+
+    def __init__(self, nbytes: int, device):
+        self.buf = torch.empty(int(nbytes) + 256, dtype=torch.uint8, device=device)
+        base = self.buf.data_ptr()
+        self.ptr = ctypes.c_void_p(base + (-base) % 256)
+        self.nbytes = int(nbytes)
+
+
+@dataclass
+class CSR:
+    """Neighbourhood pattern: rows are outputs, columns inputs."""
+    row_ptr: torch.Tensor      # int32 [n_rows + 1]
+    col_idx: torch.Tensor      # int32 [>= nnz]
+    n_rows: int
+    n_cols: int
+    nnz: int                   # exact edge count (or an upper bound when not synchronised)
+
+    def c_struct(self) -> L.SbcCsr:
+        return L.SbcCsr(self.n_rows, self.n_cols, self.nnz, self.row_ptr.data_ptr(),
+                        self.col_idx.data_ptr())
+
+
+@dataclass
+class CSC:
+    col_ptr: torch.Tensor      # int32 [n_cols + 1]
+    row_idx: torch.Tensor      # int32 [nnz]
+    edge_perm: torch.Tensor    # int32 [nnz]
+    n_cols: int
+
+    def c_struct(self) -> L.SbcCsc:
+        return L.SbcCsc(self.n_cols, self.col_ptr.data_ptr(), self.row_idx.data_ptr(),
+                        self.edge_perm.data_ptr())
+
+
+@dataclass
+class Geometry:
+    """Coordinates the basis is evaluated from (points: x_in/x_out/radius; events: px/py/t/tau)."""
+    basis: str
+    radius: float = 0.0
+    tau: float = 0.0
+    x_in: Optional[torch.Tensor] = None
+    x_out: Optional[torch.Tensor] = None
+    px: Optional[torch.Tensor] = None
+    py: Optional[torch.Tensor] = None
+    t: Optional[torch.Tensor] = None
+
+    @property
+    def M(self) -> int:
+        return BASIS_M[self.basis]
+
+    def c_struct(self) -> L.SbcGeometry:
+        d = lambda x: x.data_ptr() if x is not None else 0
+        return L.SbcGeometry(BASES[self.basis], float(self.radius), float(self.tau), d(self.x_in),
+                             d(self.x_out), d(self.px), d(self.py), d(self.t))
+
+
+def neighbour_search_points(x_in, in_splits, x_out, out_splits, radius: float, k_cap: int,
+                            col_capacity: Optional[int] = None, sync: bool = True) -> CSR:
+    """Ball (k-capped) neighbourhoods of a ragged point batch -> CSR (sbc_neighbour_search_points).
+
+    sync=True reads E back (exact CSR, errors reported); sync=False never
+    synchronises and requires k_cap > 0 (the capacity is n_out * k_cap).
+    """
+    _require(x_in, "x_in", torch.float32, 2)
+    dev = x_in.device
+    _require(x_out, "x_out", torch.float32, 2, dev)
+    _require(in_splits, "in_splits", torch.int32, 1, dev)
+    _require(out_splits, "out_splits", torch.int32, 1, dev)
+    n_in, n_out = x_in.shape[0], x_out.shape[0]
+    n_batch = in_splits.numel() - 1
+    if out_splits.numel() != n_batch + 1:
+        raise ValueError("in_splits and out_splits must have the same length")
+    if col_capacity is None:
+        if k_cap > 0:
+            col_capacity = n_out * k_cap
+        elif not sync:
+            raise ValueError("an uncapped search without synchronisation needs col_capacity")
+        else:
+            col_capacity = max(1, 16 * n_out)
+    lib = L.lib()
+    ws = _Workspace(lib.sbc_points_workspace_size(n_in, n_out, n_batch), dev)
+    row_ptr = torch.empty(n_out + 1, dtype=torch.int32, device=dev)
+    stream = _stream(dev)
+    for _ in range(2):
+        col_idx = torch.empty(max(1, col_capacity), dtype=torch.int32, device=dev)
+        nnz = ctypes.c_int64(-1)
+        st = lib.sbc_neighbour_search_points(
+            _p(x_in), n_in, _p(in_splits), _p(x_out), n_out, _p(out_splits), n_batch,
+            ctypes.c_float(radius), int(k_cap), _p(row_ptr), _p(col_idx), int(col_capacity),
+            ctypes.byref(nnz) if sync else None, ws.ptr, ws.nbytes, stream)
+        if st == 2 and sync:          # capacity: retry once with the exact size
+            col_capacity = int(nnz.value)
+            continue
+        L.check(st)
+        E = int(nnz.value) if sync else int(col_capacity)
+        return CSR(row_ptr, col_idx, n_out, n_in, E)
+    raise RuntimeError("neighbour search did not converge on a capacity")
+
+
+def neighbour_search_events(px, py, t, width: int, height: int, window: int,
+                            half_extent: int = 1, col_capacity: Optional[int] = None,
+                            sync: bool = True) -> CSR:
+    """Backwards-in-time pixel-block neighbourhoods of an event stream (sbc_neighbour_search_events)."""
+    _require(px, "px", torch.int32, 1)
+    dev = px.device
+    _require(py, "py", torch.int32, 1, dev)
+    _require(t, "t", torch.int32, 1, dev)
+    n = px.numel()
+    if py.numel() != n or t.numel() != n:
+        raise ValueError("px, py, t must have the same length")
+    if col_capacity is None:
+        if not sync:
+            raise ValueError("sync=False needs col_capacity")
+        col_capacity = max(1, 16 * n)
+    lib = L.lib()
+    ws = _Workspace(lib.sbc_events_workspace_size(n, width, height), dev)
+    row_ptr = torch.empty(n + 1, dtype=torch.int32, device=dev)
+    stream = _stream(dev)
+    for _ in range(2):
+        col_idx = torch.empty(max(1, col_capacity), dtype=torch.int32, device=dev)
+        nnz = ctypes.c_int64(-1)
+        st = lib.sbc_neighbour_search_events(
+            _p(px), _p(py), _p(t), n, int(width), int(height), int(half_extent), int(window),
+            _p(row_ptr), _p(col_idx), int(col_capacity), ctypes.byref(nnz) if sync else None,
+            ws.ptr, ws.nbytes, stream)
+        if st == 2 and sync:
+            col_capacity = int(nnz.value)
+            continue
+        L.check(st)
+        E = int(nnz.value) if sync else int(col_capacity)
+        return CSR(row_ptr, col_idx, n, n, E)
+    raise RuntimeError("neighbour search did not converge on a capacity")
+
+
+def basis_eval(csr: CSR, geometry: Geometry) -> torch.Tensor:
+    """Per-edge basis values v [E, M] float32 (sbc_basis_eval)."""
+    dev = csr.row_ptr.device
+    v = torch.empty((max(csr.nnz, 0), geometry.M), dtype=torch.float32, device=dev)
+    c, g = csr.c_struct(), geometry.c_struct()
+    L.check(L.lib().sbc_basis_eval(ctypes.byref(c), ctypes.byref(g), _p(v), _stream(dev)))
+    return v
+
+
+def csr_transpose(csr: CSR) -> CSC:
+    """Stable transpose of the pattern (sbc_csr_transpose)."""
+    dev = csr.row_ptr.device
+    lib = L.lib()
+    ws = _Workspace(lib.sbc_transpose_workspace_size(csr.n_cols, csr.nnz), dev)
+    col_ptr = torch.empty(csr.n_cols + 1, dtype=torch.int32, device=dev)
+    row_idx = torch.empty(max(1, csr.nnz), dtype=torch.int32, device=dev)
+    perm = torch.empty(max(1, csr.nnz), dtype=torch.int32, device=dev)
+    c = csr.c_struct()
+    L.check(lib.sbc_csr_transpose(ctypes.byref(c), _p(col_ptr), _p(row_idx), _p(perm), ws.ptr,
+                                  ws.nbytes, _stream(dev)))
+    return CSC(col_ptr, row_idx, perm, csr.n_cols)
+
+
+def _dtype_code(F: torch.Tensor) -> int:
+    if F.dtype == torch.float32:
+        return L.SBC_F32
+    if F.dtype == torch.bfloat16:
+        return L.SBC_BF16
+    raise ValueError(f"features must be float32 or bfloat16, got {F.dtype}")
+
+
+def _conv_common(csr, F, W, v, geometry):
+    dev = csr.row_ptr.device
+    _require(F, "F", (torch.float32, torch.bfloat16), 2, dev)
+    _require(W, "W", F.dtype, 3, dev)
+    M, C_in, C_out = W.shape
+    if F.shape != (csr.n_cols, C_in):
+        raise ValueError(f"F must be [{csr.n_cols}, {C_in}], got {tuple(F.shape)}")
+    if v is not None:
+        _require(v, "v", torch.float32, 2, dev)
+        if v.shape[1] != M:
+            raise ValueError("v must be [E, M]")
+    elif geometry is None:
+        raise ValueError("either v or geometry is needed")
+    return dev, M, C_in, C_out
+
+
+def conv_workspace_size(csr: CSR, M, C_in, C_out, dtype_code, order) -> int:
+    return L.lib().sbc_conv_workspace_size(csr.n_rows, csr.n_cols, csr.nnz, M, C_in, C_out,
+                                           dtype_code, ORDERS[order])
+
+
+def conv_forward(csr: CSR, F, W, geometry: Optional[Geometry] = None, v=None,
+                 order: str = "auto") -> torch.Tensor:
+    """Y = sum_m N^(m) F W^(m), float32 [n_out, C_out] (sbc_conv_forward)."""
+    dev, M, C_in, C_out = _conv_common(csr, F, W, v, geometry)
+    dt = _dtype_code(F)
+    Y = torch.empty((csr.n_rows, C_out), dtype=torch.float32, device=dev)
+    ws = _Workspace(conv_workspace_size(csr, M, C_in, C_out, dt, order), dev)
+    c = csr.c_struct()
+    g = geometry.c_struct() if geometry is not None else None
+    L.check(L.lib().sbc_conv_forward(
+        ctypes.byref(c), _p(v), ctypes.byref(g) if g is not None else None, M, _p(F), _p(W), dt,
+        C_in, C_out, _p(Y), ORDERS[order], ws.ptr, ws.nbytes, _stream(dev)))
+    return Y
+
+
+def conv_backward(csr: CSR, csc: CSC, F, W, dY, geometry: Optional[Geometry] = None, v=None,
+                  order: str = "auto", need_dF: bool = True, need_dW: bool = True):
+    """(dF [n_in, C_in], dW [M, C_in, C_out]) float32 (sbc_conv_backward)."""
+    dev, M, C_in, C_out = _conv_common(csr, F, W, v, geometry)
+    _require(dY, "dY", F.dtype, 2, dev)
+    if dY.shape != (csr.n_rows, C_out):
+        raise ValueError(f"dY must be [{csr.n_rows}, {C_out}]")
+    dt = _dtype_code(F)
+    dF = torch.empty((csr.n_cols, C_in), dtype=torch.float32, device=dev) if need_dF else None
+    dW = torch.empty((M, C_in, C_out), dtype=torch.float32, device=dev) if need_dW else None
+    ws = _Workspace(conv_workspace_size(csr, M, C_in, C_out, dt, order), dev)
+    c, k = csr.c_struct(), csc.c_struct()
+    g = geometry.c_struct() if geometry is not None else None
+    L.check(L.lib().sbc_conv_backward(
+        ctypes.byref(c), ctypes.byref(k), _p(v), ctypes.byref(g) if g is not None else None, M,
+        _p(F), _p(W), _p(dY), dt, C_in, C_out, _p(dF), _p(dW), ORDERS[order], ws.ptr, ws.nbytes,
+        _stream(dev)))
+    return dF, dW
+
+
+def resolve_order(n_out, n_in, nnz, M, C_in, C_out, order="auto") -> str:
+    code = L.lib().sbc_resolve_order(n_out, n_in, nnz, M, C_in, C_out, ORDERS[order])
+    return {v: k for k, v in ORDERS.items()}[code]

@@ -1,0 +1,142 @@
+"""The C ABI without a GPU: exports, size queries, argument errors, order rule.
+
+Nothing here launches a kernel; every call returns before touching the device.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2012_01170_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(L.LIB_PATH):
+        from paper_2012_01170_amd import build
+        build.build()
+    return L.lib()
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "sbconv.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(sbc_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(L.EXPORTS) == names
+
+
+def test_workspace_queries(lib):
+    a = lib.sbc_points_workspace_size(32768, 32768, 32)
+    b = lib.sbc_points_workspace_size(1024, 256, 1)
+    assert a > b > 0 and a % 256 == 0
+    assert lib.sbc_events_workspace_size(300000, 128, 128) > 300000 * 4 * 5
+    assert lib.sbc_transpose_workspace_size(1000, 5000) >= 2 * 5000 * 4
+    s1 = lib.sbc_conv_workspace_size(1000, 1000, 8000, 8, 16, 16, L.SBC_F32, L.SBC_ORDER_SPMM_FIRST)
+    s2 = lib.sbc_conv_workspace_size(1000, 1000, 8000, 8, 16, 16, L.SBC_F32, L.SBC_ORDER_GEMM_FIRST)
+    assert s1 > 8000 * 8 * 4 and s2 > 8000 * 8 * 4
+    assert lib.sbc_conv_workspace_size(-1, 10, 10, 8, 1, 1, 0, 0) == 0
+
+
+def test_basis_sizes_and_strings(lib):
+    assert [lib.sbc_basis_size(b) for b in (0, 1, 2)] == [4, 8, 8]
+    assert lib.sbc_basis_size(7) == 0
+    assert lib.sbc_status_string(2) == b"insufficient col_idx capacity"
+
+
+def _search_points(lib, **kw):
+    args = dict(x_in=1, n_in=4, in_splits=1, x_out=1, n_out=2, out_splits=1, n_batch=1,
+                radius=0.1, k_cap=0, row_ptr=1, col_idx=1, cap=8, nnz=None, ws=1, ws_bytes=1 << 30,
+                stream=None)
+    args.update(kw)
+    return lib.sbc_neighbour_search_points(
+        args["x_in"], args["n_in"], args["in_splits"], args["x_out"], args["n_out"],
+        args["out_splits"], args["n_batch"], ctypes.c_float(args["radius"]), args["k_cap"],
+        args["row_ptr"], args["col_idx"], args["cap"], args["nnz"], args["ws"], args["ws_bytes"],
+        args["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_batch=0), 1), (dict(radius=0.0), 1), (dict(radius=float("nan")), 1),
+    (dict(radius=-1.0), 1), (dict(n_in=-1), 1), (dict(row_ptr=None), 1),
+    (dict(cap=-1), 1), (dict(col_idx=None), 1), (dict(ws_bytes=16), 6), (dict(ws=None), 6),
+])
+def test_point_search_argument_errors(lib, kw, status):
+    assert _search_points(lib, **kw) == status
+    assert lib.sbc_last_error() != b""
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(width=0), 1), (dict(half_extent=4), 8), (dict(window=-1), 1), (dict(px=None), 1),
+    (dict(ws_bytes=8), 6), (dict(width=1 << 16, height=1 << 16), 1),
+])
+def test_event_search_argument_errors(lib, kw, status):
+    a = dict(px=1, py=1, t=1, n=10, width=8, height=8, half_extent=1, window=5, row_ptr=1,
+             col_idx=1, cap=10, nnz=None, ws=1, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    st = lib.sbc_neighbour_search_events(a["px"], a["py"], a["t"], a["n"], a["width"],
+                                         a["height"], a["half_extent"], a["window"], a["row_ptr"],
+                                         a["col_idx"], a["cap"], a["nnz"], a["ws"], a["ws_bytes"],
+                                         a["stream"])
+    assert st == status
+
+
+def test_conv_argument_errors(lib):
+    csr = L.SbcCsr(10, 10, 40, 1, 1)
+    g = L.SbcGeometry(L.SBC_BASIS_MONO8, 0.1, 0.0, 1, 1, 0, 0, 0)
+    ok = dict(M=8, F=1, W=1, dt=0, ci=4, co=4, Y=1, order=0, ws=1, wsb=1 << 30)
+
+    def fwd(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return lib.sbc_conv_forward(ctypes.byref(csr), None, ctypes.byref(g), a["M"], a["F"],
+                                    a["W"], a["dt"], a["ci"], a["co"], a["Y"], a["order"], a["ws"],
+                                    a["wsb"], None)
+
+    assert fwd(M=6) == 8
+    assert fwd(M=4) == 1            # basis has M = 8
+    assert fwd(ci=0) == 1
+    assert fwd(dt=5) == 1
+    assert fwd(W=None) == 1
+    assert fwd(Y=None) == 1
+    assert fwd(wsb=8) == 6
+    bad = L.SbcCsr(10, 10, 1 << 31, 1, 1)
+    assert lib.sbc_conv_forward(ctypes.byref(bad), None, ctypes.byref(g), 8, 1, 1, 0, 4, 4, 1, 0,
+                                1, 1 << 30, None) == 3
+    ge = L.SbcGeometry(L.SBC_BASIS_EVENT8, 0.0, 0.0, 0, 0, 1, 1, 1)
+    assert lib.sbc_conv_forward(ctypes.byref(csr), None, ctypes.byref(ge), 8, 1, 1, 0, 4, 4, 1,
+                                0, 1, 1 << 30, None) == 1          # tau = 0
+    csc = L.SbcCsc(9, 1, 1, 1)                                      # n_cols mismatch
+    assert lib.sbc_conv_backward(ctypes.byref(csr), ctypes.byref(csc), None, ctypes.byref(g), 8,
+                                 1, 1, 1, 0, 4, 4, 1, 1, 0, 1, 1 << 30, None) == 1
+
+
+@pytest.mark.parametrize("shape", [
+    (256, 1024, 2800, 4, 16, 32), (32768, 32768, 194456, 8, 64, 64),
+    (8192, 32768, 159867, 8, 64, 128), (32768, 8192, 159867, 8, 128, 64),
+    (1000, 1000, 10, 8, 64, 8), (1000, 1000, 10, 8, 8, 64)])
+def test_order_rule_is_the_cost_table(lib, shape):
+    """AUTO picks the order with fewer multiply-adds (the paper's cost table)."""
+    n_out, n_in, E, M, ci, co = shape
+    spmm_first = M * ci * (E + n_out * co)
+    gemm_first = M * co * (E + n_in * ci)
+    want = L.SBC_ORDER_SPMM_FIRST if spmm_first <= gemm_first else L.SBC_ORDER_GEMM_FIRST
+    assert lib.sbc_resolve_order(n_out, n_in, E, M, ci, co, L.SBC_ORDER_AUTO) == want
+    assert lib.sbc_resolve_order(n_out, n_in, E, M, ci, co, L.SBC_ORDER_GEMM_FIRST) == 2
+
+
+def test_trace_registry_without_events(lib):
+    names = lib.sbc_kernel_names().decode().split(",")
+    assert "fwd_gemm" in names and "points_fill" in names
+    assert lib.sbc_trace_kernel(b"fwd_gemm", None, None) == 0     # removing is always fine
+    assert lib.sbc_trace_kernel(None, None, None) == 1
+    lib.sbc_trace_clear()

@@ -1,0 +1,250 @@
+"""HIP path vs the CPU oracle, element by element, through the C ABI.
+
+Neighbour CSRs and transposes must be bit-exact; basis values, outputs and
+gradients must match to the float32 tolerance (bf16 inputs: the bf16 one),
+row-normwise (gpu_common.row_error); rows that are exactly zero in the oracle
+must be exactly zero.  Small cases span several tiles and a ragged tail;
+the five full-size workloads are checked on every CSR entry and on sampled
+rows of the outputs.
+"""
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from tests import gpu_common as G
+
+pytestmark = pytest.mark.gpu
+
+SMALL = {
+    "pts_inplace": lambda: workloads.small_points(seed=0),
+    "pts_down": lambda: workloads.small_points(seed=1, n_out=60),
+    "pts_uncapped": lambda: workloads.small_points(seed=2, k_cap=0),
+    "pts_cap1": lambda: workloads.small_points(seed=3, k_cap=1),
+    "pts_mono4_odd": lambda: workloads.small_points(seed=4, basis=workloads.BASIS_MONO4, c_in=5,
+                                                    c_out=7, n_out=45),
+    "pts_wide": lambda: workloads.small_points(seed=5, n_clouds=2, c_in=96, c_out=80),
+    "pts_bf16": lambda: workloads.small_points(seed=6, dtype="bf16", c_in=32, c_out=48),
+    "ev_small": lambda: workloads.small_events(seed=0),
+    "ev_odd": lambda: workloads.small_events(seed=1, c=13, n=3001),
+    "ev_bf16": lambda: workloads.small_events(seed=2, dtype="bf16", c=24),
+}
+FULL = list(workloads.WORKLOADS)
+ORDERS = ["spmm_first", "gemm_first"]
+
+
+@functools.lru_cache(maxsize=None)
+def case(name):
+    w = SMALL[name]() if name in SMALL else workloads.WORKLOADS[name]()
+    if w["kind"] == "points":
+        rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
+                                   w["radius"], w["k_cap"])
+        v = oracle.basis.point_basis(w["x_in"], w["x_out"], rp, ci, w["radius"], w["M"])
+    else:
+        rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"],
+                                   w["height"])
+        v = oracle.basis.event_basis(w["px"], w["py"], w["t"], rp, ci, w["tau"])
+    return w, rp, ci, v
+
+
+@functools.lru_cache(maxsize=None)
+def gpu_case(name):
+    w, rp, ci, v = case(name)
+    t = G.to_device(w)
+    csr = G.search(w, t)
+    return t, csr
+
+
+def sample_rows(n, rp=None, k=1500, seed=0):
+    rng = np.random.default_rng(seed)
+    rows = set(range(min(50, n))) | set(range(max(0, n - 50), n))
+    rows |= set(rng.choice(n, size=min(k, n), replace=False).tolist())
+    if rp is not None:      # include some empty rows
+        empty = np.nonzero(np.diff(rp) == 0)[0]
+        rows |= set(empty[:20].tolist())
+    return np.array(sorted(rows), dtype=np.int64)
+
+
+def is_full(name):
+    return name in FULL
+
+
+def tol(w):
+    return G.TOL_BF16 if w["dtype"] == "bf16" else G.TOL_F32
+
+
+# ---------------------------------------------------------------- neighbours
+@pytest.mark.parametrize("name", list(SMALL) + FULL)
+def test_csr_bit_exact(name):
+    print(f"[csr] {name}", flush=True)
+    w, rp, ci, _ = case(name)
+    t, csr = gpu_case(name)
+    assert csr.nnz == len(ci)
+    assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
+    assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+
+
+@pytest.mark.parametrize("name", ["pts_inplace", "pts_down", "ellipsoids_inplace"])
+def test_csr_without_sync(name):
+    print(f"[csr nosync] {name}", flush=True)
+    w, rp, ci, _ = case(name)
+    t = G.to_device(w)
+    csr = G.search(w, t, sync=False)
+    torch.cuda.synchronize()
+    got_rp = csr.row_ptr.cpu().numpy()
+    assert np.array_equal(got_rp, rp)
+    assert np.array_equal(csr.col_idx[:got_rp[-1]].cpu().numpy(), ci)
+
+
+def test_csr_transpose_bit_exact():
+    for name in ["pts_down", "pts_uncapped", "ev_small", "ellipsoids_down", "events_300k"]:
+        print(f"[transpose] {name}", flush=True)
+        w, rp, ci, _ = case(name)
+        t, csr = gpu_case(name)
+        csc = G.sbc.csr_transpose(csr)
+        cp, ri, perm = oracle.csr_transpose(rp, ci, w["n_in"])
+        assert np.array_equal(csc.col_ptr.cpu().numpy(), cp)
+        assert np.array_equal(csc.row_idx[:len(ci)].cpu().numpy(), ri)
+        assert np.array_equal(csc.edge_perm[:len(ci)].cpu().numpy(), perm)
+
+
+# ---------------------------------------------------------------- basis
+@pytest.mark.parametrize("name", list(SMALL) + FULL)
+def test_basis_values(name):
+    print(f"[basis] {name}", flush=True)
+    w, rp, ci, v_ref = case(name)
+    t, csr = gpu_case(name)
+    v = G.sbc.basis_eval(csr, G.geometry(w, t)).cpu().numpy()
+    assert v.shape == v_ref.shape
+    # all basis values are bounded by 1 in magnitude: absolute float32 error
+    assert np.max(np.abs(v - v_ref)) < 2e-6
+    assert np.all(v[v_ref == 0] == 0) or w["kind"] == "points"
+
+
+# ---------------------------------------------------------------- forward
+@pytest.mark.parametrize("order", ORDERS)
+@pytest.mark.parametrize("name", list(SMALL) + FULL)
+def test_forward(name, order):
+    print(f"[forward] {name} {order}", flush=True)
+    w, rp, ci, v = case(name)
+    t, csr = gpu_case(name)
+    Y = G.sbc.conv_forward(csr, t["F"], t["W"], geometry=G.geometry(w, t), order=order)
+    rows = sample_rows(w["n_out"], rp) if w["kind"] == "events" and is_full(name) else None
+    Y_ref = oracle.conv.forward(rp, ci, v, w["F"], w["W"], rows=rows)
+    got = Y.cpu().numpy() if rows is None else Y.cpu().numpy()[rows]
+    err = G.row_error(got, Y_ref)
+    print(f"    row error {err:.3e}", flush=True)
+    assert err < tol(w)
+
+
+@pytest.mark.parametrize("name", ["pts_down", "ev_odd", "sphere_1024"])
+def test_forward_with_materialised_basis(name):
+    w, rp, ci, v = case(name)
+    t, csr = gpu_case(name)
+    vv = G.sbc.basis_eval(csr, G.geometry(w, t))
+    for order in ORDERS:
+        Y = G.sbc.conv_forward(csr, t["F"], t["W"], v=vv, order=order)
+        Y_ref = oracle.conv.forward(rp, ci, v, w["F"], w["W"])
+        assert G.row_error(Y.cpu().numpy(), Y_ref) < tol(w)
+
+
+# ---------------------------------------------------------------- backward
+@pytest.mark.parametrize("order", ORDERS)
+@pytest.mark.parametrize("name", list(SMALL) + FULL)
+def test_backward(name, order):
+    print(f"[backward] {name} {order}", flush=True)
+    w, rp, ci, v = case(name)
+    t, csr = gpu_case(name)
+    csc = G.sbc.csr_transpose(csr)
+    dF, dW = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"], geometry=G.geometry(w, t),
+                                 order=order)
+    cols = sample_rows(w["n_in"]) if w["kind"] == "events" and is_full(name) else None
+    dF_ref, dW_ref = oracle.conv.backward(rp, ci, v, w["F"], w["W"], w["dY"], w["n_in"],
+                                          cols_subset=cols)
+    got = dF.cpu().numpy() if cols is None else dF.cpu().numpy()[cols]
+    e1 = G.row_error(got, dF_ref)
+    e2 = G.norm_error(dW.cpu().numpy(), dW_ref)
+    print(f"    dF row error {e1:.3e}  dW error {e2:.3e}", flush=True)
+    assert e1 < tol(w) and e2 < tol(w)
+
+
+def test_runs_are_bitwise_reproducible():
+    for name in ["ev_small", "pts_down"]:
+        w, rp, ci, v = case(name)
+        t, csr = gpu_case(name)
+        csc = G.sbc.csr_transpose(csr)
+        g = G.geometry(w, t)
+        outs = []
+        for _ in range(2):
+            Y = G.sbc.conv_forward(csr, t["F"], t["W"], geometry=g)
+            dF, dW = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"], geometry=g)
+            outs.append([x.cpu().numpy() for x in (Y, dF, dW)])
+        for a, b in zip(*outs):
+            assert np.array_equal(a, b)
+
+
+# ---------------------------------------------------------------- edge cases
+def test_isolated_and_empty_outputs_are_exact_zero():
+    w = workloads.small_points(seed=8, n_out=30, n_clouds=2)
+    # an output far from everything, and a last cloud with no inputs
+    w["x_out"] = np.concatenate([w["x_out"], np.array([[9, 9, 9]], np.float32)])
+    w["out_splits"] = w["out_splits"].copy()
+    w["out_splits"][-1] += 1
+    w["dY"] = np.concatenate([w["dY"], np.ones((1, w["C_out"]), np.float32)])
+    w["n_out"] += 1
+    t = G.to_device(w)
+    csr = G.search(w, t)
+    Y = G.sbc.conv_forward(csr, t["F"], t["W"], geometry=G.geometry(w, t)).cpu().numpy()
+    assert np.all(Y[-1] == 0.0)
+    rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
+                               w["radius"], w["k_cap"])
+    assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
+
+
+def test_empty_stream_and_cloud():
+    z = torch.zeros(0, dtype=torch.int32, device=G.DEV)
+    csr = G.sbc.neighbour_search_events(z, z, z, 8, 8, 100)
+    assert csr.nnz == 0 and csr.row_ptr.cpu().tolist() == [0]
+    x = torch.zeros((0, 3), dtype=torch.float32, device=G.DEV)
+    s = torch.zeros(2, dtype=torch.int32, device=G.DEV)
+    csr = G.sbc.neighbour_search_points(x, s, x, s, 0.1, 4)
+    assert csr.nnz == 0 and csr.row_ptr.cpu().tolist() == [0]
+
+
+@pytest.mark.parametrize("k_cap", [0, 7, 300, 700])
+def test_rows_longer_than_the_lds_stage(k_cap):
+    """A dense cloud whose in-ball rows exceed the kernel's LDS stage (512)."""
+    rng = np.random.default_rng(3)
+    x = (rng.random((1500, 3)) * 0.1).astype(np.float32)
+    y = x[:40]
+    w = workloads.points_workload(rng, [(x, y)], workloads.BASIS_MONO8, 0.3, k_cap, 4, 4)
+    rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
+                               w["radius"], k_cap)
+    assert np.diff(rp).max() == (k_cap if k_cap else 1500)
+    t = G.to_device(w)
+    csr = G.search(w, t)
+    assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
+    assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+
+
+def test_unsorted_and_out_of_range_events_are_reported():
+    px = torch.tensor([1, 2, 3, 1], dtype=torch.int32, device=G.DEV)
+    py = torch.tensor([1, 1, 1, 1], dtype=torch.int32, device=G.DEV)
+    t = torch.tensor([0, 10, 5, 20], dtype=torch.int32, device=G.DEV)
+    with pytest.raises(G.sbc.ops.L.SbcError, match="UNSORTED"):
+        G.sbc.neighbour_search_events(px, py, t, 8, 8, 100)
+    t2 = torch.tensor([0, 10, 15, 20], dtype=torch.int32, device=G.DEV)
+    px2 = torch.tensor([1, 2, 8, 1], dtype=torch.int32, device=G.DEV)
+    with pytest.raises(G.sbc.ops.L.SbcError, match="OUT_OF_RANGE"):
+        G.sbc.neighbour_search_events(px2, py, t2, 8, 8, 100)
+
+
+def test_malformed_splits_are_reported():
+    x = torch.zeros((4, 3), dtype=torch.float32, device=G.DEV)
+    good = torch.tensor([0, 4], dtype=torch.int32, device=G.DEV)
+    bad = torch.tensor([0, 5], dtype=torch.int32, device=G.DEV)
+    with pytest.raises(G.sbc.ops.L.SbcError, match="OUT_OF_RANGE"):
+        G.sbc.neighbour_search_points(x, bad, x, good, 0.1, 2)
