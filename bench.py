@@ -44,8 +44,13 @@ DESCRIPTIONS = {
 }
 
 
-def kernel_table(kind, order, n_in, n_out, E, M, ci, co, sf):
-    """Kernels of one step: name -> (launches per step, algorithmic bytes, flops, mfma?)."""
+def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256):
+    """Kernels of one step: name -> (launches per step, algorithmic bytes, flops, on MFMA).
+
+    Bytes count every array the kernel must touch once (gathered rows once per
+    row, not once per edge); flops count the multiply-adds x 2 of the
+    contraction (MFMA) or of the gather (vector ALU, reported but not a roof).
+    """
     geo = 12 * (n_in + n_out) if kind == "points" else 12 * n_in
     W = M * ci * co * sf
     t = {}
@@ -55,27 +60,45 @@ def kernel_table(kind, order, n_in, n_out, E, M, ci, co, sf):
     else:
         t["events_count"] = (1, 24 * n_in, 0, False)
         t["events_fill"] = (1, 28 * n_in + 4 * E, 0, False)
-    t["basis"] = (2, 4 * (n_out + 1) + 4 * E + geo + 4 * E * M, 0, False)
     t["transpose_sort"] = (1, 4 * (n_in + 1) + 16 * E, 0, False)
+    basis_launches = 0
     csr_b = 4 * (n_out + 1) + 4 * E + 4 * E * M
     csc_b = 4 * (n_in + 1) + 8 * E + 4 * E * M
-    if order == "spmm_first":
+    if plan["forward_fused"]:
+        t["fwd_fused"] = (1, 4 * (n_out + 1) + 4 * E + geo + n_in * ci * sf + W + 4 * n_out * co,
+                          2 * n_out * M * ci * co, True)
+    elif plan["forward_order"] == "spmm_first":
+        basis_launches += 1
         G = 4 * n_out * M * ci
         t["fwd_spmm"] = (1, csr_b + n_in * ci * sf + G, 2 * E * M * ci, False)
         t["fwd_gemm"] = (1, G + W + 4 * n_out * co, 2 * n_out * M * ci * co, True)
-        t["bwd_spmm"] = t["fwd_spmm"]
+    else:
+        basis_launches += 1
+        H = 4 * n_in * M * co
+        t["fwd_gemm_h"] = (1, n_in * ci * sf + W + H, 2 * n_in * ci * M * co, True)
+        t["fwd_spmm_contract"] = (1, csr_b + H + 4 * n_out * co, 2 * E * M * co, False)
+    if plan["backward_fused"]:
+        part = 4 * blocks_bwd * ci * M * co
+        t["bwd_fused"] = (1, 4 * (n_in + 1) + 4 * E + geo + n_out * co * sf + n_in * ci * sf
+                          + W + 4 * n_in * ci + part, 4 * n_in * M * ci * co, True)
+        t["bwd_dw_reduce"] = (1, part + 4 * M * ci * co, 0, False)
+    elif plan["backward_order"] == "spmm_first":
+        basis_launches += 1
+        D = 4 * n_in * M * co
+        t["bwd_spmm_t_expand"] = (1, csc_b + n_out * co * sf + D, 2 * E * M * co, False)
+        t["bwd_gemm_df"] = (1, D + W + 4 * n_in * ci, 2 * n_in * M * co * ci, True)
+        t["bwd_gemm_dw_t"] = (1, n_in * ci * sf + D + 4 * M * ci * co, 2 * n_in * ci * M * co,
+                              True)
+    else:
+        basis_launches += 1
+        G = 4 * n_out * M * ci
+        t["bwd_spmm"] = (1, csr_b + n_in * ci * sf + G, 2 * E * M * ci, False)
         t["bwd_gemm_dw"] = (1, G + n_out * co * sf + 4 * M * ci * co, 2 * n_out * M * ci * co,
                             True)
         t["bwd_gemm_dg"] = (1, n_out * co * sf + W + G, 2 * n_out * M * ci * co, True)
         t["bwd_spmm_t"] = (1, csc_b + G + 4 * n_in * ci, 2 * E * M * ci, False)
-    else:
-        H = 4 * n_in * M * co
-        t["fwd_gemm_h"] = (1, n_in * ci * sf + W + H, 2 * n_in * ci * M * co, True)
-        t["fwd_spmm_contract"] = (1, csr_b + H + 4 * n_out * co, 2 * E * M * co, False)
-        t["bwd_spmm_t_expand"] = (1, csc_b + n_out * co * sf + H, 2 * E * M * co, False)
-        t["bwd_gemm_df"] = (1, H + W + 4 * n_in * ci, 2 * n_in * M * co * ci, True)
-        t["bwd_gemm_dw_t"] = (1, n_in * ci * sf + H + 4 * M * ci * co, 2 * n_in * ci * M * co,
-                              True)
+    if basis_launches:
+        t["basis"] = (basis_launches, 4 * (n_out + 1) + 4 * E + geo + 4 * E * M, 0, False)
     return t
 
 
@@ -166,16 +189,19 @@ def main(argv=None):
     csr0 = search()
     torch.cuda.synchronize()
     E = int(csr0.row_ptr[-1].item())
-    order = sbc.resolve_order(n_out, n_in, E, M, ci, co, a.order)
+    plan = sbc.conv_plan(n_out, n_in, csr0.nnz, M, ci, co, F.dtype, a.order)
 
     def step():
         csr = search()
-        Y = sbc.conv_forward(csr, F, W, geometry=geo, order=order)
+        Y = sbc.conv_forward(csr, F, W, geometry=geo, order=a.order)
         csc = sbc.csr_transpose(csr)
-        dF, dW = sbc.conv_backward(csr, csc, F, W, dY, geometry=geo, order=order)
+        dF, dW = sbc.conv_backward(csr, csc, F, W, dY, geometry=geo, order=a.order)
         return Y, dF, dW
 
-    table = kernel_table(w["kind"], order, n_in, n_out, E, M, ci, co, sf)
+    n_cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    tr_bwd = 64 if M * co * sf * 64 <= 65536 else 32     # the fused backward's tile rows
+    blocks_bwd = max(1, min(256, n_cus, (n_in + tr_bwd - 1) // tr_bwd))
+    table = kernel_table(w["kind"], plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd)
     L = _lib.lib()
     # one (start, stop) event pair per kernel per timed step; record once so the
     # underlying HIP events exist before the library records them again
@@ -189,9 +215,10 @@ def main(argv=None):
     for _ in range(a.warmup):
         step()
     torch.cuda.synchronize()
+
+    # (1) eager steps with every kernel bracketed by HIP events (trace hook)
     t_start = torch.cuda.Event(enable_timing=True)
     t_stop = torch.cuda.Event(enable_timing=True)
-    wall0 = time.perf_counter()
     t_start.record()
     for s in range(a.steps):
         for k, (s0, s1) in ev[s].items():
@@ -199,8 +226,30 @@ def main(argv=None):
         step()
     t_stop.record()
     torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
     L.sbc_trace_clear()
+    eager_ms = t_start.elapsed_time(t_stop) / a.steps
+
+    # (2) the same step captured once in a HIP graph (it never synchronises
+    # with the host), then replayed: the timed region
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(2):
+            step()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(a.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record()
+    for _ in range(a.steps):
+        graph.replay()
+    t_stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
     ms = t_start.elapsed_time(t_stop) / a.steps
 
     kernels = {}
@@ -227,7 +276,8 @@ def main(argv=None):
            "data": "synthetic (seeded generators; inputs resident in HBM)",
            "config": {"workload": f"{a.workload}: {DESCRIPTIONS[a.workload]}", "n_in": n_in,
                       "n_out": n_out, "edges": E, "M": M, "C_in": ci, "C_out": co,
-                      "order": order, "wall_s": round(wall, 3)},
+                      "plan": plan, "timing": "HIP graph replays of the captured step",
+                      "eager_ms_per_step": round(eager_ms, 4), "wall_s": round(wall, 3)},
            "roofline": roof, "kernels": kernels}
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, a.cpu_reps)

@@ -260,6 +260,27 @@ sbc_status sbc_trace_kernel(const char *name, hipEvent_t start, hipEvent_t stop)
 void sbc_trace_clear(void);
 const char *sbc_kernel_names(void);
 
+/*
+ * The plan sbc_conv_forward / sbc_conv_backward follow for a shape.
+ *   forward_order   SPMM_FIRST: (N F) W;  GEMM_FIRST: N (F W)
+ *   backward_order  SPMM_FIRST: D = N^T dY first (dF = D Wt, dW = F^T D);
+ *                   GEMM_FIRST: dG = dY W^T first (dF = N^T dG, dW = G^T dY)
+ *   *_fused         1 when that pass runs as one fused kernel (gather into
+ *                   LDS, basis evaluated inside, MFMA contraction), 0 when it
+ *                   runs as separate gather and contraction kernels.
+ * AUTO picks the order with fewer multiply-adds (the paper's cost table);
+ * for the backward the rule is applied to the transposed problem.
+ */
+typedef struct {
+    sbc_order forward_order;
+    sbc_order backward_order;
+    int32_t forward_fused;
+    int32_t backward_fused;
+} sbc_conv_plan_t;
+sbc_status sbc_conv_plan(int32_t n_out, int32_t n_in, int64_t nnz_bound, int32_t M,
+                         int32_t C_in, int32_t C_out, sbc_dtype dtype, sbc_order order,
+                         sbc_conv_plan_t *plan);
+
 /* Order AUTO resolves to (SBC_ORDER_SPMM_FIRST or SBC_ORDER_GEMM_FIRST). */
 sbc_order sbc_resolve_order(int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t C_in,
                             int32_t C_out, sbc_order order);

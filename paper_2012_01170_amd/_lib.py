@@ -27,6 +27,7 @@ EXPORTS = [
     "sbc_transpose_workspace_size", "sbc_csr_transpose",
     "sbc_conv_workspace_size", "sbc_conv_forward", "sbc_conv_backward",
     "sbc_resolve_order", "sbc_trace_kernel", "sbc_trace_clear", "sbc_kernel_names",
+    "sbc_conv_plan",
 ]
 
 
@@ -45,6 +46,11 @@ class SbcGeometry(ctypes.Structure):
     _fields_ = [("basis", ctypes.c_int), ("radius", ctypes.c_float), ("tau", ctypes.c_float),
                 ("x_in", ctypes.c_void_p), ("x_out", ctypes.c_void_p), ("px", ctypes.c_void_p),
                 ("py", ctypes.c_void_p), ("t", ctypes.c_void_p)]
+
+
+class SbcConvPlan(ctypes.Structure):
+    _fields_ = [("forward_order", ctypes.c_int), ("backward_order", ctypes.c_int),
+                ("forward_fused", ctypes.c_int32), ("backward_fused", ctypes.c_int32)]
 
 
 class SbcError(RuntimeError):
@@ -86,6 +92,8 @@ _SIGS = {
     "sbc_trace_kernel": (ctypes.c_int, [ctypes.c_char_p, _vp, _vp]),
     "sbc_trace_clear": (None, []),
     "sbc_kernel_names": (ctypes.c_char_p, []),
+    "sbc_conv_plan": (ctypes.c_int, [_i32, _i32, _i64, _i32, _i32, _i32, ctypes.c_int, ctypes.c_int,
+                                     ctypes.POINTER(SbcConvPlan)]),
 }
 
 

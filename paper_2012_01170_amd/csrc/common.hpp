@@ -75,11 +75,12 @@ enum : uint32_t {
 
 // ---------------------------------------------------------------- primitives (scan.hip)
 // Exclusive prefix sum of `n` int32 counts into out[0..n]; out[n] is the total.
-// The total is also stored, as int64, to *total64 (device).  Sums of 2^31 or
-// more are saturated in `out` and still exact in *total64.
+// The total is also stored, as int64, to *total64 (device, may be null).  Sums
+// of 2^31 or more are saturated in `out` and still exact in *total64.  out2
+// (may be null) receives a second copy of out.  Short arrays take one kernel.
 size_t scan_workspace_bytes(int64_t n);
 sbc_status exclusive_scan_i32(const int32_t *counts, int32_t *out, int64_t n, int64_t *total64,
-                              void *ws, hipStream_t stream);
+                              void *ws, hipStream_t stream, int32_t *out2 = nullptr);
 
 // Fill n int32 words with a value (a kernel, not a memset node).
 sbc_status fill_i32(int32_t *p, int32_t value, int64_t n, hipStream_t stream);

@@ -2,17 +2,17 @@
 // gradients (Section 3.1, the matrix-product form; its down- and up-sampling
 // evaluation orders and their multiply-add counts).
 //
-// SpMM-first ((N F) W):  G = [N^(m) F]_m  [n_out, M*C_in]   (gather, expand)
-//                        Y = G W_flat                        (MFMA)
-//   backward:  dW = G^T dY (split K over n_out), dG = dY W_flat^T (MFMA),
-//              dF = sum_m N^(m)T dG_m                        (gather, contract, CSC)
-// GEMM-first (N (F W)):  H = F [W^(m)]_m  [n_in, M*C_out]   (MFMA)
-//                        Y = sum_m N^(m) H_m                 (gather, contract)
-//   backward:  D = [N^(m)T dY]_m [n_in, M*C_out]            (gather, expand, CSC)
-//              dF = D Wt, dW = F^T D (split K over n_in)     (MFMA)
-// When v is NULL the basis values are evaluated into the workspace first.
+// Forward, SpMM-first ((N F) W):  G = [N^(m) F]_m [n_out, M*C_in] (gather), Y = G W_flat (MFMA)
+// Forward, GEMM-first (N (F W)):  H = F [W^(m)]_m [n_in, M*C_out] (MFMA), Y = sum_m N^(m) H_m
+// Backward, D-route (gather first):  D = [N^(m)T dY]_m [n_in, M*C_out], dF = D Wt, dW = F^T D
+// Backward, G-route (GEMM first):    dG = dY W_flat^T, dF = N^T dG; dW = G^T dY with G = N F
+// Shapes listed in fused.hip run SpMM-first forward and the D-route as fused
+// kernels (basis evaluated inside); other shapes and orders use the generic
+// kernels below, which evaluate the basis into the workspace first when v is
+// NULL.
 #include "basis.hpp"
 #include "common.hpp"
+#include "fused.hpp"
 #include "gemm.hpp"
 #include "spmm.hpp"
 
@@ -77,41 +77,86 @@ sbc_status permute_w_back(const float *dwp, int32_t M, int32_t Ci, int32_t Co, f
     return SBC_OK;
 }
 
+// Routes of the four products.  Forward: SpMM-first gathers G = N F then
+// contracts with W; GEMM-first contracts H = F W then gathers over H.
+// Backward: the D-route gathers D = N^T dY first (dF = D Wt, dW = F^T D), the
+// G-route contracts dG = dY W^T first (dF = N^T dG) with dW = G^T dY.
+enum Route { kFwdSpmm, kFwdGemm, kBwdD, kBwdG };
+
 struct ConvWs {
-    float *v;        // [nnz, M]
+    float *v;        // [nnz, M] basis values (when not supplied)
     float *inter;    // G / H / D
-    float *inter2;   // dG
-    float *wperm;    // permuted weights (GEMM-first)
+    float *inter2;   // dG (G-route)
+    float *wperm;    // permuted weights
     float *dwperm;   // dW in [C_in, M, C_out] (D-route)
     float *partial;  // split-K partial tiles
 };
 
-ConvWs carve_conv(void *base, int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t Ci,
-                  int32_t Co, sbc_order order, size_t *bytes) {
+ConvWs carve_route(void *base, Route r, int32_t n_out, int32_t n_in, int64_t nnz, int32_t M,
+                   int32_t Ci, int32_t Co, size_t *bytes) {
     Carver cv(base);
     ConvWs w{};
     w.v = cv.take<float>((size_t)nnz * M);
     const int64_t wsz = (int64_t)M * Ci * Co;
-    if (order == SBC_ORDER_SPMM_FIRST) {
-        w.inter = cv.take<float>((size_t)n_out * M * Ci);
-        w.inter2 = cv.take<float>((size_t)n_out * M * Ci);
-        size_t p1 = gemm_workspace_floats(M * Ci, Co, n_out);      // dW = G^T dY
-        size_t p2 = gemm_workspace_floats(n_out, Co, (int64_t)M * Ci);  // Y = G W
-        size_t p3 = gemm_workspace_floats(n_out, M * Ci, Co);      // dG = dY W^T
-        size_t p = p1 > p2 ? p1 : p2;
-        w.partial = cv.take<float>(p > p3 ? p : p3);
-    } else {
-        w.inter = cv.take<float>((size_t)n_in * M * Co);
-        w.wperm = cv.take<float>((size_t)wsz);
-        w.dwperm = cv.take<float>((size_t)wsz);
-        size_t p1 = gemm_workspace_floats(n_in, M * Co, Ci);       // H = F Wp
-        size_t p2 = gemm_workspace_floats(n_in, Ci, (int64_t)M * Co);  // dF = D Wt
-        size_t p3 = gemm_workspace_floats(Ci, M * Co, n_in);       // dW' = F^T D
-        size_t p = p1 > p2 ? p1 : p2;
-        w.partial = cv.take<float>(p > p3 ? p : p3);
+    size_t p = 0;
+    auto upd = [&p](size_t q) { p = q > p ? q : p; };
+    switch (r) {
+        case kFwdSpmm:
+            w.inter = cv.take<float>((size_t)n_out * M * Ci);
+            upd(gemm_workspace_floats(n_out, Co, (int64_t)M * Ci));
+            break;
+        case kFwdGemm:
+            w.inter = cv.take<float>((size_t)n_in * M * Co);
+            w.wperm = cv.take<float>((size_t)wsz);
+            upd(gemm_workspace_floats(n_in, M * Co, Ci));
+            break;
+        case kBwdD:
+            w.inter = cv.take<float>((size_t)n_in * M * Co);
+            w.wperm = cv.take<float>((size_t)wsz);
+            w.dwperm = cv.take<float>((size_t)wsz);
+            upd(gemm_workspace_floats(n_in, Ci, (int64_t)M * Co));
+            upd(gemm_workspace_floats(Ci, M * Co, n_in));
+            break;
+        case kBwdG:
+            w.inter = cv.take<float>((size_t)n_out * M * Ci);
+            w.inter2 = cv.take<float>((size_t)n_out * M * Ci);
+            upd(gemm_workspace_floats(M * Ci, Co, n_out));
+            upd(gemm_workspace_floats(n_out, M * Ci, Co));
+            break;
     }
+    w.partial = cv.take<float>(p);
     if (bytes) *bytes = cv.used;
     return w;
+}
+
+bool route_fused(Route r, int32_t M, int32_t Ci, int32_t Co, bool bf) {
+    if (r == kFwdSpmm) return fused_forward_available(M, Ci, Co, bf);
+    if (r == kBwdD) return fused_backward_available(M, Ci, Co, bf);
+    return false;
+}
+
+size_t route_bytes(Route r, int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t Ci,
+                   int32_t Co, bool bf) {
+    if (route_fused(r, M, Ci, Co, bf)) return fused_workspace_bytes(M, Ci, Co);
+    size_t b = 0;
+    carve_route(nullptr, r, n_out, n_in, nnz, M, Ci, Co, &b);
+    return b;
+}
+
+Route forward_route(int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t Ci, int32_t Co,
+                    sbc_order order) {
+    return sbc_resolve_order(n_out, n_in, nnz, M, Ci, Co, order) == SBC_ORDER_SPMM_FIRST
+               ? kFwdSpmm
+               : kFwdGemm;
+}
+
+// The backward is itself a convolution from the outputs back to the inputs
+// (N^T, channels C_out -> C_in); AUTO applies the same cost rule to it.
+// Explicit orders name what is done first: SPMM_FIRST = D-route, GEMM_FIRST = G-route.
+Route backward_route(int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t Ci, int32_t Co,
+                     sbc_order order) {
+    return sbc_resolve_order(n_in, n_out, nnz, M, Co, Ci, order) == SBC_ORDER_SPMM_FIRST ? kBwdD
+                                                                                       : kBwdG;
 }
 
 sbc_status check_conv_args(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,
@@ -126,6 +171,12 @@ sbc_status check_conv_args(const sbc_csr *csr, const float *v, const sbc_geometr
         const int32_t gm = g->basis == SBC_BASIS_MONO4 ? 4 : 8;
         if (gm != M) return fail(SBC_ERR_INVALID_ARG, "M does not match the geometry's basis");
     }
+    return SBC_OK;
+}
+
+sbc_status check_order(sbc_order order) {
+    if (order != SBC_ORDER_AUTO && order != SBC_ORDER_SPMM_FIRST && order != SBC_ORDER_GEMM_FIRST)
+        return fail(SBC_ERR_INVALID_ARG, "unknown order");
     return SBC_OK;
 }
 
@@ -145,14 +196,34 @@ extern "C" sbc_order sbc_resolve_order(int32_t n_out, int32_t n_in, int64_t nnz,
     return spmm_first <= gemm_first ? SBC_ORDER_SPMM_FIRST : SBC_ORDER_GEMM_FIRST;
 }
 
+extern "C" sbc_status sbc_conv_plan(int32_t n_out, int32_t n_in, int64_t nnz_bound, int32_t M,
+                                    int32_t C_in, int32_t C_out, sbc_dtype dtype, sbc_order order,
+                                    sbc_conv_plan_t *plan) {
+    clear_error();
+    if (!plan) return fail(SBC_ERR_INVALID_ARG, "plan is null");
+    if (n_out < 0 || n_in < 0 || nnz_bound < 0 || M <= 0 || C_in <= 0 || C_out <= 0)
+        return fail(SBC_ERR_INVALID_ARG, "negative or zero size");
+    SBC_TRY(check_order(order));
+    const bool bf = dtype == SBC_BF16;
+    const Route f = forward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order);
+    const Route b = backward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order);
+    plan->forward_order = f == kFwdSpmm ? SBC_ORDER_SPMM_FIRST : SBC_ORDER_GEMM_FIRST;
+    plan->backward_order = b == kBwdD ? SBC_ORDER_SPMM_FIRST : SBC_ORDER_GEMM_FIRST;
+    plan->forward_fused = route_fused(f, M, C_in, C_out, bf) ? 1 : 0;
+    plan->backward_fused = route_fused(b, M, C_in, C_out, bf) ? 1 : 0;
+    return SBC_OK;
+}
+
 extern "C" size_t sbc_conv_workspace_size(int32_t n_out, int32_t n_in, int64_t nnz_bound,
                                           int32_t M, int32_t C_in, int32_t C_out,
-                                          sbc_dtype /*dtype*/, sbc_order order) {
+                                          sbc_dtype dtype, sbc_order order) {
     if (n_out < 0 || n_in < 0 || nnz_bound < 0 || M <= 0 || C_in <= 0 || C_out <= 0) return 0;
-    order = sbc_resolve_order(n_out, n_in, nnz_bound, M, C_in, C_out, order);
-    size_t bytes = 0;
-    carve_conv(nullptr, n_out, n_in, nnz_bound, M, C_in, C_out, order, &bytes);
-    return bytes;
+    const bool bf = dtype == SBC_BF16;
+    const Route f = forward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order);
+    const Route b = backward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order);
+    const size_t a = route_bytes(f, n_out, n_in, nnz_bound, M, C_in, C_out, bf);
+    const size_t c = route_bytes(b, n_out, n_in, nnz_bound, M, C_in, C_out, bf);
+    return a > c ? a : c;
 }
 
 extern "C" sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v,
@@ -162,20 +233,24 @@ extern "C" sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v,
                                        size_t workspace_bytes, hipStream_t stream) {
     clear_error();
     SBC_TRY(check_conv_args(csr, v, geometry, M, F, W, dtype, C_in, C_out));
+    SBC_TRY(check_order(order));
     if (!Y && csr->n_rows > 0) return fail(SBC_ERR_INVALID_ARG, "Y is null");
     const int32_t n_out = csr->n_rows, n_in = csr->n_cols;
-    order = sbc_resolve_order(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order);
-    size_t need = 0;
-    ConvWs ws = carve_conv(workspace, n_out, n_in, csr->nnz_bound, M, C_in, C_out, order, &need);
+    const bool bf = dtype == SBC_BF16;
+    const Route r = forward_route(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order);
+    const size_t need = route_bytes(r, n_out, n_in, csr->nnz_bound, M, C_in, C_out, bf);
     if (!workspace || workspace_bytes < need)
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_conv_workspace_size()");
-    const bool bf = dtype == SBC_BF16;
+    if (route_fused(r, M, C_in, C_out, bf))
+        return fused_forward(csr, v, geometry, M, F, W, bf, C_in, C_out, Y, workspace, stream);
+
+    ConvWs ws = carve_route(workspace, r, n_out, n_in, csr->nnz_bound, M, C_in, C_out, nullptr);
     const float *vv = v;
     if (!vv) {
         SBC_TRY(basis_eval_launch(csr, geometry, ws.v, stream));
         vv = ws.v;
     }
-    if (order == SBC_ORDER_SPMM_FIRST) {
+    if (r == kFwdSpmm) {
         SBC_TRY(spmm(n_out, csr->row_ptr, csr->col_idx, nullptr, vv, M, F, bf, C_in, false,
                      ws.inter, stream, "fwd_spmm"));
         SBC_TRY(gemm(ws.inter, false, (int64_t)M * C_in, 1, W, bf, C_out, 1, Y, C_out, 1, n_out,
@@ -200,24 +275,30 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
                                         hipStream_t stream) {
     clear_error();
     SBC_TRY(check_conv_args(csr, v, geometry, M, F, W, dtype, C_in, C_out));
+    SBC_TRY(check_order(order));
     if (!csc || !csc->col_ptr || csc->n_cols != csr->n_cols ||
         (csr->nnz_bound > 0 && (!csc->row_idx || !csc->edge_perm)))
         return fail(SBC_ERR_INVALID_ARG, "csc is null or does not match csr");
     if (!dY && csr->n_rows > 0) return fail(SBC_ERR_INVALID_ARG, "dY is null");
+    if (!dF && !dW) return SBC_OK;
     const int32_t n_out = csr->n_rows, n_in = csr->n_cols;
-    order = sbc_resolve_order(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order);
-    size_t need = 0;
-    ConvWs ws = carve_conv(workspace, n_out, n_in, csr->nnz_bound, M, C_in, C_out, order, &need);
+    const bool bf = dtype == SBC_BF16;
+    const Route r = backward_route(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order);
+    const size_t need = route_bytes(r, n_out, n_in, csr->nnz_bound, M, C_in, C_out, bf);
     if (!workspace || workspace_bytes < need)
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_conv_workspace_size()");
-    const bool bf = dtype == SBC_BF16;
+    if (route_fused(r, M, C_in, C_out, bf))
+        return fused_backward(csr, csc, v, geometry, M, F, W, dY, bf, C_in, C_out, dF, dW,
+                              workspace, stream);
+
+    ConvWs ws = carve_route(workspace, r, n_out, n_in, csr->nnz_bound, M, C_in, C_out, nullptr);
     const float *vv = v;
     if (!vv) {
         SBC_TRY(basis_eval_launch(csr, geometry, ws.v, stream));
         vv = ws.v;
     }
     const int64_t K1 = (int64_t)M * C_in, K2 = (int64_t)M * C_out;
-    if (order == SBC_ORDER_SPMM_FIRST) {
+    if (r == kBwdG) {
         SBC_TRY(spmm(n_out, csr->row_ptr, csr->col_idx, nullptr, vv, M, F, bf, C_in, false,
                      ws.inter, stream, "bwd_spmm"));
         if (dW)  // dW [M*C_in, C_out] = G^T dY
@@ -241,7 +322,6 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
         if (dW) {  // dW' [C_in, M*C_out] = F^T D, then back to [M, C_in, C_out]
             SBC_TRY(gemm(F, bf, 1, C_in, ws.inter, false, K2, 1, ws.dwperm, K2, 1, C_in,
                          (int32_t)K2, n_in, ws.partial, stream, "bwd_gemm_dw_t"));
-            // dwperm element (c, m, p) at c*M*C_out + m*C_out + p -> dW (m, c, p)
             SBC_TRY(permute_w_back(ws.dwperm, M, C_in, C_out, dW, stream));
         }
     }

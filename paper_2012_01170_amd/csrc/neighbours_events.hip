@@ -185,10 +185,11 @@ EventsWs carve_events(void *base, int32_t n, int64_t npix, size_t *bytes) {
     return w;
 }
 
-__global__ void copy_kernel(const int32_t *src, int32_t *dst, int64_t n) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x)
-        dst[i] = src[i];
+// Zeroes the pixel counts and the status word.
+__global__ void init_kernel(int32_t *__restrict__ pix_count, int64_t npix, uint32_t *status) {
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (int64_t x = gid; x < npix; x += (int64_t)gridDim.x * blockDim.x) pix_count[x] = 0;
+    if (gid == 0) *status = 0u;
 }
 
 template <int kSide>
@@ -255,19 +256,20 @@ extern "C" sbc_status sbc_neighbour_search_events(const int32_t *px, const int32
     if (!workspace || workspace_bytes < need)
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_events_workspace_size()");
 
-    SBC_TRY(fill_i32(reinterpret_cast<int32_t *>(ws.status), 0, 1, stream));
-    SBC_TRY(fill_i32(ws.pix_count, 0, npix, stream));
+    {
+        const int g = grid_for(npix, 256) < 1024 ? grid_for(npix, 256) : 1024;
+        hipLaunchKernelGGL(init_kernel, dim3(g), dim3(256), 0, stream, ws.pix_count, npix,
+                           ws.status);
+        SBC_LAUNCH_CHECK();
+    }
     if (n > 0) {
         hipLaunchKernelGGL(pixel_count_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream, px, py,
                            t, n, width, height, ws.pix_count, ws.status);
         SBC_LAUNCH_CHECK();
     }
-    SBC_TRY(exclusive_scan_i32(ws.pix_count, ws.pix_start, npix, ws.total + 1, ws.scan_ws, stream));
+    SBC_TRY(exclusive_scan_i32(ws.pix_count, ws.pix_start, npix, ws.total + 1, ws.scan_ws, stream,
+                               ws.cursor));
     if (n > 0) {
-        int g = grid_for(npix + 1, 256);
-        hipLaunchKernelGGL(copy_kernel, dim3(g > 4096 ? 4096 : g), dim3(256), 0, stream,
-                           ws.pix_start, ws.cursor, npix + 1);
-        SBC_LAUNCH_CHECK();
         hipLaunchKernelGGL(pixel_scatter_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream, px,
                            py, n, width, height, ws.cursor, ws.list_unsorted);
         SBC_LAUNCH_CHECK();

@@ -80,23 +80,31 @@ __device__ __forceinline__ float sq_dist(float ax, float ay, float az, float bx,
     return __fadd_rn(__fadd_rn(__fmul_rn(dx, dx), __fmul_rn(dy, dy)), __fmul_rn(dz, dz));
 }
 
-__global__ void check_splits_kernel(const int32_t *in_splits, const int32_t *out_splits,
-                                    int32_t n_batch, int32_t n_in, int32_t n_out,
-                                    uint32_t *status) {
-    int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b > n_batch) return;
-    bool bad = false;
-    if (b == 0) bad = in_splits[0] != 0 || out_splits[0] != 0;
-    if (b == n_batch) bad = bad || in_splits[b] != n_in || out_splits[b] != n_out;
-    if (b > 0) bad = bad || in_splits[b] < in_splits[b - 1] || out_splits[b] < out_splits[b - 1];
-    if (bad) atomicOr(status, (uint32_t)kFlagBadSplits);
+// Zeroes the cell counts and the status word.
+__global__ void init_kernel(int32_t *__restrict__ cell_count, uint32_t table_size,
+                            uint32_t *status) {
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (int64_t x = gid; x < table_size; x += (int64_t)gridDim.x * blockDim.x) cell_count[x] = 0;
+    if (gid == 0) *status = 0u;
 }
 
+// Cell key of every input point (and, in the first n_batch + 1 threads, the
+// check that the splits run from 0 to n_in / n_out without decreasing).
 __global__ void key_kernel(const float *__restrict__ x_in, int32_t n_in,
-                           const int32_t *__restrict__ in_splits, int32_t n_batch, double inv_h,
-                           uint32_t table_mask, uint32_t *__restrict__ keys,
-                           int32_t *__restrict__ counts) {
+                           const int32_t *__restrict__ in_splits,
+                           const int32_t *__restrict__ out_splits, int32_t n_out, int32_t n_batch,
+                           double inv_h, uint32_t table_mask, uint32_t *__restrict__ keys,
+                           int32_t *__restrict__ counts, uint32_t *status) {
     int32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+    if (j <= n_batch) {
+        const int32_t b = j;
+        bool bad = false;
+        if (b == 0) bad = in_splits[0] != 0 || out_splits[0] != 0;
+        if (b == n_batch) bad = bad || in_splits[b] != n_in || out_splits[b] != n_out;
+        if (b > 0)
+            bad = bad || in_splits[b] < in_splits[b - 1] || out_splits[b] < out_splits[b - 1];
+        if (bad) atomicOr(status, (uint32_t)kFlagBadSplits);
+    }
     if (j >= n_in) return;
     int32_t b = cloud_of(in_splits, n_batch, j);
     float x = x_in[3 * (int64_t)j], y = x_in[3 * (int64_t)j + 1], z = x_in[3 * (int64_t)j + 2];
@@ -390,12 +398,6 @@ PointsWs carve_points(void *base, int32_t n_in, int32_t n_out, int32_t /*n_batch
     return w;
 }
 
-__global__ void copy_i32_kernel(const int32_t *src, int32_t *dst, int64_t n) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x)
-        dst[i] = src[i];
-}
-
 }  // namespace
 }  // namespace sbc
 
@@ -429,20 +431,19 @@ extern "C" sbc_status sbc_neighbour_search_points(
     const uint32_t T = table_size_for(n_in);
     const double inv_h = 1.0 / ((double)radius * kCellMargin);
 
-    SBC_TRY(fill_i32(reinterpret_cast<int32_t *>(ws.status), 0, 1, stream));
-    hipLaunchKernelGGL(check_splits_kernel, dim3(grid_for(n_batch + 1, 256)), dim3(256), 0, stream,
-                       in_splits, out_splits, n_batch, n_in, n_out, ws.status);
-    SBC_LAUNCH_CHECK();
-    SBC_TRY(fill_i32(ws.cell_count, 0, T, stream));
-    if (n_in > 0) {
-        hipLaunchKernelGGL(key_kernel, dim3(grid_for(n_in, 256)), dim3(256), 0, stream, x_in, n_in,
-                           in_splits, n_batch, inv_h, T - 1, ws.keys, ws.cell_count);
+    {
+        const int g = grid_for(T, 256) < 1024 ? grid_for(T, 256) : 1024;
+        hipLaunchKernelGGL(init_kernel, dim3(g), dim3(256), 0, stream, ws.cell_count, T,
+                           ws.status);
+        SBC_LAUNCH_CHECK();
+        const int64_t kn = (int64_t)n_in > (int64_t)n_batch + 1 ? n_in : (int64_t)n_batch + 1;
+        hipLaunchKernelGGL(key_kernel, dim3(grid_for(kn, 256)), dim3(256), 0, stream, x_in, n_in,
+                           in_splits, out_splits, n_out, n_batch, inv_h, T - 1, ws.keys,
+                           ws.cell_count, ws.status);
         SBC_LAUNCH_CHECK();
     }
-    SBC_TRY(exclusive_scan_i32(ws.cell_count, ws.cell_start, T, ws.total + 1, ws.scan_ws, stream));
-    hipLaunchKernelGGL(copy_i32_kernel, dim3(grid_for(T, 256) > 4096 ? 4096 : grid_for(T, 256)),
-                       dim3(256), 0, stream, ws.cell_start, ws.cursor, (int64_t)T);
-    SBC_LAUNCH_CHECK();
+    SBC_TRY(exclusive_scan_i32(ws.cell_count, ws.cell_start, T, ws.total + 1, ws.scan_ws, stream,
+                               ws.cursor));
     if (n_in > 0) {
         hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(n_in, 256)), dim3(256), 0, stream, x_in,
                            n_in, ws.keys, ws.cursor, ws.table);

@@ -1,9 +1,11 @@
 // Device-wide exclusive prefix sums, fills and small segmented sorts.
 //
-// Scan: a three-phase blocked scan.  Each block of 256 threads owns 1024
-// consecutive items (4 per thread); block totals are scanned recursively
-// (in int64, so edge totals beyond 2^31 are detected exactly), then every
-// block rescans its items with its offset added.
+// Scan: up to 8192 items, one block walks the array.  Beyond, a blocked
+// scan: each block of 256 threads owns 1024 consecutive items (4 per thread)
+// and publishes its total (int64, so edge totals beyond 2^31 are detected
+// exactly); a second kernel's blocks each add up the preceding totals
+// themselves and rescan their items (for very long arrays the totals are
+// scanned recursively instead).
 #include <climits>
 
 #include "common.hpp"
@@ -56,7 +58,7 @@ __global__ void __launch_bounds__(kThreads) block_sums_kernel(const T *in, int64
 template <typename InT, typename OutT>
 __global__ void __launch_bounds__(kThreads)
     block_scan_kernel(const InT *in, int64_t n, const int64_t *offsets, OutT *out,
-                      int64_t *total64, bool write_total) {
+                      int64_t *total64, bool write_total, OutT *out2) {
     __shared__ int64_t lds[kThreads / 64];
     const int64_t base = (int64_t)blockIdx.x * kPerBlock + (int64_t)threadIdx.x * kItems;
     int64_t v[kItems];
@@ -72,10 +74,13 @@ __global__ void __launch_bounds__(kThreads)
 #pragma unroll
     for (int k = 0; k < kItems; ++k) {
         if (base + k < n) {
+            OutT o;
             if (sizeof(OutT) == 4)
-                out[base + k] = (OutT)(run > (int64_t)INT_MAX ? (int64_t)INT_MAX : run);
+                o = (OutT)(run > (int64_t)INT_MAX ? (int64_t)INT_MAX : run);
             else
-                out[base + k] = (OutT)run;
+                o = (OutT)run;
+            out[base + k] = o;
+            if (out2) out2[base + k] = o;
         }
         run += v[k];
     }
@@ -83,10 +88,128 @@ __global__ void __launch_bounds__(kThreads)
     // the grand total
     if (write_total && blockIdx.x == gridDim.x - 1 && threadIdx.x == kThreads - 1) {
         int64_t grand = (offsets ? offsets[blockIdx.x] : 0) + total;
+        OutT o;
         if (sizeof(OutT) == 4)
-            out[n] = (OutT)(grand > (int64_t)INT_MAX ? (int64_t)INT_MAX : grand);
+            o = (OutT)(grand > (int64_t)INT_MAX ? (int64_t)INT_MAX : grand);
         else
-            out[n] = (OutT)grand;
+            o = (OutT)grand;
+        out[n] = o;
+        if (out2) out2[n] = o;
+        if (total64) *total64 = grand;
+    }
+}
+
+// Single-block scan for short arrays: 1024 threads walk the array in chunks
+// of 1024 x kSmallItems, carrying the running total; the next chunk is loaded
+// while the current one is scanned.  out2 (optional) receives a copy.
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallItems = 8;
+constexpr int64_t kSmallMax = 8192;
+// Up to this many blocks, each block sums the preceding block totals itself.
+constexpr int64_t kSelfOffsetBlocks = 4096;
+
+__global__ void __launch_bounds__(kSmallThreads)
+    small_scan_kernel(const int32_t *__restrict__ in, int64_t n, int32_t *__restrict__ out,
+                      int32_t *__restrict__ out2, int64_t *__restrict__ total64) {
+    __shared__ int64_t wsum[kSmallThreads / 64];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    constexpr int64_t chunk = (int64_t)kSmallThreads * kSmallItems;
+    int64_t carry = 0;
+    int32_t cur[kSmallItems];
+    int64_t base = (int64_t)threadIdx.x * kSmallItems;
+#pragma unroll
+    for (int k = 0; k < kSmallItems; ++k) cur[k] = (base + k < n) ? in[base + k] : 0;
+    for (int64_t c0 = 0; c0 < n; c0 += chunk) {
+        int32_t nxt[kSmallItems];
+        const int64_t nb = c0 + chunk + (int64_t)threadIdx.x * kSmallItems;
+#pragma unroll
+        for (int k = 0; k < kSmallItems; ++k) nxt[k] = (nb + k < n) ? in[nb + k] : 0;
+        int64_t s = 0;
+#pragma unroll
+        for (int k = 0; k < kSmallItems; ++k) s += cur[k];
+        int64_t x = s;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            int64_t y = __shfl_up(x, d, 64);
+            if (lane >= d) x += y;
+        }
+        if (lane == 63) wsum[wave] = x;
+        __syncthreads();
+        int64_t before = 0, tot = 0;
+#pragma unroll
+        for (int w = 0; w < kSmallThreads / 64; ++w) {
+            const int64_t v = wsum[w];
+            before += (w < wave) ? v : 0;
+            tot += v;
+        }
+        __syncthreads();
+        int64_t run = carry + before + x - s;
+        const int64_t b0 = c0 + (int64_t)threadIdx.x * kSmallItems;
+#pragma unroll
+        for (int k = 0; k < kSmallItems; ++k) {
+            if (b0 + k < n) {
+                const int32_t o = (int32_t)(run > (int64_t)INT_MAX ? (int64_t)INT_MAX : run);
+                out[b0 + k] = o;
+                if (out2) out2[b0 + k] = o;
+            }
+            run += cur[k];
+        }
+        carry += tot;
+#pragma unroll
+        for (int k = 0; k < kSmallItems; ++k) cur[k] = nxt[k];
+    }
+    if (threadIdx.x == 0) {
+        const int32_t o = (int32_t)(carry > (int64_t)INT_MAX ? (int64_t)INT_MAX : carry);
+        out[n] = o;
+        if (out2) out2[n] = o;
+        if (total64) *total64 = carry;
+    }
+}
+
+// Second pass of the two-kernel scan: block b first adds up the totals of
+// blocks 0..b-1 (all 256 threads, then a block reduction; the order is fixed),
+// then scans its own items with that offset.
+__global__ void __launch_bounds__(kThreads)
+    self_offset_scan_kernel(const int32_t *__restrict__ in, int64_t n,
+                            const int64_t *__restrict__ sums, int32_t *__restrict__ out,
+                            int32_t *__restrict__ out2, int64_t *__restrict__ total64) {
+    __shared__ int64_t lds[kThreads / 64];
+    __shared__ int64_t red[kThreads];
+    int64_t part = 0;
+    for (int64_t q = threadIdx.x; q < (int64_t)blockIdx.x; q += kThreads) part += sums[q];
+    red[threadIdx.x] = part;
+    __syncthreads();
+    for (int w = kThreads / 2; w > 0; w >>= 1) {
+        if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    const int64_t offset = red[0];
+    const int64_t base = (int64_t)blockIdx.x * kPerBlock + (int64_t)threadIdx.x * kItems;
+    int64_t v[kItems];
+    int64_t s = 0;
+#pragma unroll
+    for (int k = 0; k < kItems; ++k) {
+        v[k] = (base + k < n) ? (int64_t)in[base + k] : 0;
+        s += v[k];
+    }
+    int64_t total;
+    const int64_t incl = block_inclusive_scan(s, lds, &total);
+    int64_t run = incl - s + offset;
+#pragma unroll
+    for (int k = 0; k < kItems; ++k) {
+        if (base + k < n) {
+            const int32_t o = (int32_t)(run > (int64_t)INT_MAX ? (int64_t)INT_MAX : run);
+            out[base + k] = o;
+            if (out2) out2[base + k] = o;
+        }
+        run += v[k];
+    }
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == kThreads - 1) {
+        const int64_t grand = offset + total;
+        const int32_t o = (int32_t)(grand > (int64_t)INT_MAX ? (int64_t)INT_MAX : grand);
+        out[n] = o;
+        if (out2) out2[n] = o;
         if (total64) *total64 = grand;
     }
 }
@@ -97,7 +220,8 @@ sbc_status scan_i64_inplace(int64_t *a, int64_t n, char *ws, hipStream_t stream)
     const int64_t nb = (n + kPerBlock - 1) / kPerBlock;
     if (nb == 1) {
         hipLaunchKernelGGL((block_scan_kernel<int64_t, int64_t>), dim3(1), dim3(kThreads), 0,
-                           stream, a, n, (const int64_t *)nullptr, a, (int64_t *)nullptr, false);
+                           stream, a, n, (const int64_t *)nullptr, a, (int64_t *)nullptr, false,
+                           (int64_t *)nullptr);
         SBC_LAUNCH_CHECK();
         return SBC_OK;
     }
@@ -108,7 +232,8 @@ sbc_status scan_i64_inplace(int64_t *a, int64_t n, char *ws, hipStream_t stream)
     SBC_LAUNCH_CHECK();
     SBC_TRY(scan_i64_inplace(sums, nb, rest, stream));
     hipLaunchKernelGGL((block_scan_kernel<int64_t, int64_t>), dim3((unsigned)nb), dim3(kThreads),
-                       0, stream, a, n, (const int64_t *)sums, a, (int64_t *)nullptr, false);
+                       0, stream, a, n, (const int64_t *)sums, a, (int64_t *)nullptr, false,
+                       (int64_t *)nullptr);
     SBC_LAUNCH_CHECK();
     return SBC_OK;
 }
@@ -186,12 +311,10 @@ sbc_status fill_i32(int32_t *p, int32_t value, int64_t n, hipStream_t stream) {
 }
 
 sbc_status exclusive_scan_i32(const int32_t *counts, int32_t *out, int64_t n, int64_t *total64,
-                              void *ws, hipStream_t stream) {
-    if (n <= 0) {
-        // out[0] = 0 and total = 0, written by a one-block scan of nothing
-        hipLaunchKernelGGL((block_scan_kernel<int32_t, int32_t>), dim3(1), dim3(kThreads), 0,
-                           stream, counts, (int64_t)0, (const int64_t *)nullptr, out, total64,
-                           true);
+                              void *ws, hipStream_t stream, int32_t *out2) {
+    if (n <= kSmallMax) {
+        hipLaunchKernelGGL(small_scan_kernel, dim3(1), dim3(kSmallThreads), 0, stream, counts,
+                           n > 0 ? n : 0, out, out2, total64);
         SBC_LAUNCH_CHECK();
         return SBC_OK;
     }
@@ -202,9 +325,15 @@ sbc_status exclusive_scan_i32(const int32_t *counts, int32_t *out, int64_t n, in
     hipLaunchKernelGGL((block_sums_kernel<int32_t>), dim3((unsigned)nb), dim3(kThreads), 0, stream,
                        counts, n, sums);
     SBC_LAUNCH_CHECK();
+    if (nb <= kSelfOffsetBlocks) {
+        hipLaunchKernelGGL(self_offset_scan_kernel, dim3((unsigned)nb), dim3(kThreads), 0, stream,
+                           counts, n, (const int64_t *)sums, out, out2, total64);
+        SBC_LAUNCH_CHECK();
+        return SBC_OK;
+    }
     SBC_TRY(scan_i64_inplace(sums, nb, rest, stream));
     hipLaunchKernelGGL((block_scan_kernel<int32_t, int32_t>), dim3((unsigned)nb), dim3(kThreads),
-                       0, stream, counts, n, (const int64_t *)sums, out, total64, true);
+                       0, stream, counts, n, (const int64_t *)sums, out, total64, true, out2);
     SBC_LAUNCH_CHECK();
     return SBC_OK;
 }

@@ -35,12 +35,6 @@ __global__ void col_scatter_kernel(int32_t n_rows, int32_t n_cols,
     }
 }
 
-__global__ void copy_kernel(const int32_t *src, int32_t *dst, int64_t n) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x)
-        dst[i] = src[i];
-}
-
 struct TransposeWs {
     int32_t *count;
     int32_t *cursor;
@@ -95,12 +89,8 @@ extern "C" sbc_status sbc_csr_transpose(const sbc_csr *csr, int32_t *col_ptr, in
                            csr->row_ptr, csr->col_idx, ws.count);
         SBC_LAUNCH_CHECK();
     }
-    SBC_TRY(exclusive_scan_i32(ws.count, col_ptr, C, ws.total, ws.scan_ws, stream));
+    SBC_TRY(exclusive_scan_i32(ws.count, col_ptr, C, ws.total, ws.scan_ws, stream, ws.cursor));
     if (R > 0 && C > 0) {
-        int g = grid_for((int64_t)C + 1, 256);
-        hipLaunchKernelGGL(copy_kernel, dim3(g > 4096 ? 4096 : g), dim3(256), 0, stream, col_ptr,
-                           ws.cursor, (int64_t)C + 1);
-        SBC_LAUNCH_CHECK();
         hipLaunchKernelGGL(col_scatter_kernel, dim3(grid_for(R, 256)), dim3(256), 0, stream, R, C,
                            csr->row_ptr, csr->col_idx, ws.cursor, ws.rows_tmp, ws.perm_tmp);
         SBC_LAUNCH_CHECK();

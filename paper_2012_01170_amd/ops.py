@@ -268,6 +268,17 @@ def conv_backward(csr: CSR, csc: CSC, F, W, dY, geometry: Optional[Geometry] = N
     return dF, dW
 
 
+def conv_plan(n_out, n_in, nnz, M, C_in, C_out, dtype=torch.float32, order="auto") -> dict:
+    """Route and fusion of forward and backward for a shape (sbc_conv_plan)."""
+    plan = L.SbcConvPlan()
+    code = L.SBC_BF16 if dtype == torch.bfloat16 else L.SBC_F32
+    L.check(L.lib().sbc_conv_plan(n_out, n_in, nnz, M, C_in, C_out, code, ORDERS[order],
+                                  ctypes.byref(plan)))
+    names = {v: k for k, v in ORDERS.items()}
+    return {"forward_order": names[plan.forward_order], "backward_order": names[plan.backward_order],
+            "forward_fused": bool(plan.forward_fused), "backward_fused": bool(plan.backward_fused)}
+
+
 def resolve_order(n_out, n_in, nnz, M, C_in, C_out, order="auto") -> str:
     code = L.lib().sbc_resolve_order(n_out, n_in, nnz, M, C_in, C_out, ORDERS[order])
     return {v: k for k, v in ORDERS.items()}[code]

@@ -140,3 +140,19 @@ def test_trace_registry_without_events(lib):
     assert lib.sbc_trace_kernel(b"fwd_gemm", None, None) == 0     # removing is always fine
     assert lib.sbc_trace_kernel(None, None, None) == 1
     lib.sbc_trace_clear()
+
+
+def test_conv_plan(lib):
+    from paper_2012_01170_amd import ops
+    p = ops.conv_plan(32768, 32768, 194456, 8, 64, 64)
+    assert p == {"forward_order": "spmm_first", "backward_order": "spmm_first",
+                 "forward_fused": True, "backward_fused": True}
+    # down-sampling: gather first forward; the backward's cost rule picks dG first
+    p = ops.conv_plan(8192, 32768, 159867, 8, 64, 128)
+    assert p["forward_order"] == "spmm_first" and p["backward_order"] == "gemm_first"
+    assert p["forward_fused"] and not p["backward_fused"]
+    p = ops.conv_plan(100, 100, 500, 8, 5, 7)
+    assert not p["forward_fused"] and not p["backward_fused"]
+    p = ops.conv_plan(100, 100, 500, 8, 64, 64, order="gemm_first")
+    assert p["forward_order"] == "gemm_first" and not p["forward_fused"]
+    assert p["backward_order"] == "gemm_first" and not p["backward_fused"]

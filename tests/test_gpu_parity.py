@@ -31,6 +31,14 @@ SMALL = {
     "ev_small": lambda: workloads.small_events(seed=0),
     "ev_odd": lambda: workloads.small_events(seed=1, c=13, n=3001),
     "ev_bf16": lambda: workloads.small_events(seed=2, dtype="bf16", c=24),
+    # shapes with fused kernels, at sizes spanning several tiles and a ragged tail
+    "fz_pts64": lambda: workloads.small_points(seed=7, c_in=64, c_out=64),
+    "fz_pts_down128": lambda: workloads.small_points(seed=8, n_out=61, c_in=64, c_out=128),
+    "fz_pts_m4": lambda: workloads.small_points(seed=9, basis=workloads.BASIS_MONO4, n_out=70,
+                                                c_in=16, c_out=32),
+    "fz_pts_bf16": lambda: workloads.small_points(seed=10, dtype="bf16", c_in=32, c_out=32),
+    "fz_ev32": lambda: workloads.small_events(seed=3, c=32, n=5003),
+    "fz_ev_bf16": lambda: workloads.small_events(seed=4, c=64, dtype="bf16", n=4099),
 }
 FULL = list(workloads.WORKLOADS)
 ORDERS = ["spmm_first", "gemm_first"]
@@ -140,7 +148,7 @@ def test_forward(name, order):
     assert err < tol(w)
 
 
-@pytest.mark.parametrize("name", ["pts_down", "ev_odd", "sphere_1024"])
+@pytest.mark.parametrize("name", ["pts_down", "ev_odd", "sphere_1024", "fz_pts64", "fz_ev32"])
 def test_forward_with_materialised_basis(name):
     w, rp, ci, v = case(name)
     t, csr = gpu_case(name)
@@ -171,8 +179,28 @@ def test_backward(name, order):
     assert e1 < tol(w) and e2 < tol(w)
 
 
+@pytest.mark.parametrize("name", ["pts_mono4_odd", "fz_pts64", "fz_ev_bf16"])
+def test_backward_with_materialised_basis_and_partial_outputs(name):
+    w, rp, ci, v = case(name)
+    t, csr = gpu_case(name)
+    csc = G.sbc.csr_transpose(csr)
+    vv = G.sbc.basis_eval(csr, G.geometry(w, t))
+    dF_ref, dW_ref = oracle.conv.backward(rp, ci, v, w["F"], w["W"], w["dY"], w["n_in"])
+    for order in ORDERS:
+        dF, dW = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"], v=vv, order=order)
+        assert G.row_error(dF.cpu().numpy(), dF_ref) < tol(w)
+        assert G.norm_error(dW.cpu().numpy(), dW_ref) < tol(w)
+        dF1, none = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"], v=vv, order=order,
+                                        need_dW=False)
+        none2, dW1 = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"], v=vv, order=order,
+                                         need_dF=False)
+        assert none is None and none2 is None
+        assert np.array_equal(dF1.cpu().numpy(), dF.cpu().numpy())
+        assert np.array_equal(dW1.cpu().numpy(), dW.cpu().numpy())
+
+
 def test_runs_are_bitwise_reproducible():
-    for name in ["ev_small", "pts_down"]:
+    for name in ["ev_small", "pts_down", "fz_pts64", "fz_ev_bf16"]:
         w, rp, ci, v = case(name)
         t, csr = gpu_case(name)
         csc = G.sbc.csr_transpose(csr)
@@ -248,3 +276,20 @@ def test_malformed_splits_are_reported():
     bad = torch.tensor([0, 5], dtype=torch.int32, device=G.DEV)
     with pytest.raises(G.sbc.ops.L.SbcError, match="OUT_OF_RANGE"):
         G.sbc.neighbour_search_points(x, bad, x, good, 0.1, 2)
+
+
+@pytest.mark.parametrize("n_cols", [5_000_000, 8192, 8193])
+def test_transpose_of_wide_patterns(n_cols):
+    """Column counts of 5M entries take the scan's recursive path; 8192/8193 its boundaries."""
+    rng = np.random.default_rng(n_cols)
+    n_rows = 3000
+    lens = rng.integers(0, 9, size=n_rows)
+    rp = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    ci = np.concatenate([np.sort(rng.choice(n_cols, size=k, replace=False)) for k in lens])
+    ci = ci.astype(np.int32)
+    csr = G.sbc.CSR(G.dev(rp), G.dev(ci), n_rows, n_cols, len(ci))
+    csc = G.sbc.csr_transpose(csr)
+    cp, ri, perm = oracle.csr_transpose(rp, ci, n_cols)
+    assert np.array_equal(csc.col_ptr.cpu().numpy(), cp)
+    assert np.array_equal(csc.row_idx[:len(ci)].cpu().numpy(), ri)
+    assert np.array_equal(csc.edge_perm[:len(ci)].cpu().numpy(), perm)
