@@ -133,6 +133,31 @@ def cpu_baseline(w, reps):
                       f"backward in float64; median of {reps} passes, {med:.2f} s each"}
 
 
+def graph_timing(step, a, torch):
+    """ms per step of HIP-graph replays of one captured step, and the wall time."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(2):
+            step()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(a.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    t_start.record()
+    for _ in range(a.steps):
+        graph.replay()
+    t_stop.record()
+    torch.cuda.synchronize()
+    return t_start.elapsed_time(t_stop) / a.steps, time.perf_counter() - wall0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -142,6 +167,11 @@ def main(argv=None):
     ap.add_argument("--order", default="auto", choices=["auto", "spmm_first", "gemm_first"])
     ap.add_argument("--cpu-reps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="time eager steps only (for counter collection, which serialises)")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="after timing, run one plain device copy of this many MiB "
+                         "(calibrates profiler byte counters)")
     a = ap.parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if a.gpus != 1 or world != 1:
@@ -231,26 +261,16 @@ def main(argv=None):
 
     # (2) the same step captured once in a HIP graph (it never synchronises
     # with the host), then replayed: the timed region
-    side = torch.cuda.Stream()
-    side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        for _ in range(2):
-            step()
-    torch.cuda.current_stream().wait_stream(side)
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        step()
-    for _ in range(a.warmup):
-        graph.replay()
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    t_start.record()
-    for _ in range(a.steps):
-        graph.replay()
-    t_stop.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms = t_start.elapsed_time(t_stop) / a.steps
+    if a.no_graph:
+        ms, wall = eager_ms, float("nan")
+    else:
+        ms, wall = graph_timing(step, a, torch)
+    if a.copy_probe_mb > 0:
+        src = torch.ones(a.copy_probe_mb << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     kernels = {}
     for k, (launches, nbytes, flops, mfma) in table.items():
@@ -276,7 +296,8 @@ def main(argv=None):
            "data": "synthetic (seeded generators; inputs resident in HBM)",
            "config": {"workload": f"{a.workload}: {DESCRIPTIONS[a.workload]}", "n_in": n_in,
                       "n_out": n_out, "edges": E, "M": M, "C_in": ci, "C_out": co,
-                      "plan": plan, "timing": "HIP graph replays of the captured step",
+                      "plan": plan,
+                      "timing": "eager steps" if a.no_graph else "HIP graph replays of the captured step",
                       "eager_ms_per_step": round(eager_ms, 4), "wall_s": round(wall, 3)},
            "roofline": roof, "kernels": kernels}
     if not a.no_cpu_baseline:

@@ -14,6 +14,9 @@
 //   contract Y_tile = G_tile W on the matrix cores (float32: 16x16x4 f32
 //            MFMA with W read from L2; bf16: G rounded to bf16 in LDS and
 //            16x16x32 bf16 MFMA against a [C_out, M*C_in] copy of W).
+// Forward for narrow inputs (C_in <= 32), persistent blocks of 8 waves: each
+//            wave owns 16-row tiles and keeps G in registers as the MFMA A
+//            operand; W stays in LDS for the life of the block.
 // Backward (D-route), persistent blocks over tiles of TR input rows:
 //   gather   D[j, m*C_out + p] = sum_{e=(i,j)} v[e, m] dY[i, p] through the
 //            transposed pattern, into LDS (F's tile rows are staged too);
@@ -74,10 +77,12 @@ __device__ __forceinline__ void edge_basis(const sbc_geometry &g, const float *_
 
 // Per-wave LDS stage of up to 64 edges: neighbour index and basis values,
 // plus the row bounds of the wave's rows.
+// Entry 64 is a padding edge of weight zero (its neighbour index is any valid
+// row), so groups of edges can be processed without predication.
 template <int M>
 struct EdgeStage {
-    int32_t nb[64];
-    float v[64][M + 1];
+    int32_t nb[65];
+    float v[65][M];
     int32_t bounds[17];
 };
 
@@ -119,7 +124,8 @@ __device__ __forceinline__ void gather_rows(int32_t row_begin, int32_t n_rows,
                                             const float *__restrict__ v, const sbc_geometry &g,
                                             const void *__restrict__ Xv, void *out_tile, int S,
                                             int local_row0, EdgeStage<M> &st, double inv_r,
-                                            float inv_tau) {
+                                            float inv_tau, uint16_t *out_t = nullptr,
+                                            int ST = 0) {
     constexpr int VEC = kXbf ? 8 : 4;
     static_assert(C % VEC == 0, "channels must be a multiple of the vector width");
     constexpr int LPR = C / VEC;                   // lanes per row
@@ -176,6 +182,11 @@ __device__ __forceinline__ void gather_rows(int32_t row_begin, int32_t n_rows,
             st.nb[lane] = other;
 #pragma unroll
             for (int m = 0; m < M; ++m) st.v[lane][m] = bv[m];
+            if (lane == 0) {  // padding edge: first neighbour of the chunk, weight 0
+                st.nb[64] = other;
+#pragma unroll
+                for (int m = 0; m < M; ++m) st.v[64][m] = 0.f;
+            }
         }
         wave_lds_sync();
 #pragma unroll
@@ -186,18 +197,16 @@ __device__ __forceinline__ void gather_rows(int32_t row_begin, int32_t n_rows,
             for (int32_t e2 = lo; e2 < hi; e2 += U) {
                 float f[U][VEC];
                 int q[U];
-                bool ok[U];
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
-                    ok[u] = e2 + u < hi;
-                    q[u] = (ok[u] ? e2 + u : lo) - c0;
+                    q[u] = e2 + u < hi ? e2 + u - c0 : 64;
                     load_row_vec<C, VEC, kXbf>(Xv, st.nb[q[u]], cg, f[u]);
                 }
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
 #pragma unroll
                     for (int m = 0; m < M; ++m) {
-                        const float vm = ok[u] ? st.v[q[u]][m] : 0.f;
+                        const float vm = st.v[q[u]][m];
 #pragma unroll
                         for (int k = 0; k < VEC; ++k) acc[b][m][k] += vm * f[u][k];
                     }
@@ -217,6 +226,11 @@ __device__ __forceinline__ void gather_rows(int32_t row_begin, int32_t n_rows,
                                   (int64_t)(local_row0 + lr) * S + m * C + cg * VEC;
 #pragma unroll
                     for (int k = 0; k < VEC; ++k) o[k] = f2bf(acc[b][m][k]);
+                    if (out_t) {  // transposed copy: column (m*C + c), row lr
+#pragma unroll
+                        for (int k = 0; k < VEC; ++k)
+                            out_t[(m * C + cg * VEC + k) * ST + local_row0 + lr] = o[k];
+                    }
                 } else {
                     float *o = static_cast<float *>(out_tile) + (int64_t)(local_row0 + lr) * S +
                                m * C + cg * VEC;
@@ -231,44 +245,84 @@ __device__ __forceinline__ void gather_rows(int32_t row_begin, int32_t n_rows,
 // acc[u][t] += A_tile[16 rb_u .., :] x B[:, 16 cb_t ..] for the 16x16 blocks of
 // one wave (rb_u = wr + NRG u, cb_t = wc + NCBW t).  A sits in LDS (row stride
 // S elements), B [K, NCOL] in global memory (float32) or, for bf16, as
-// B^T [NCOL, K]; the B fragments of the next k-group are loaded while the
-// current group is multiplied.
+// B^T [NCOL, K].  The B fragments of k-groups alternate between two register
+// sets, so the loads of the next group are in flight while the current group
+// is multiplied (no copies between the sets, which would force a wait).
+template <int NCOL, int WCB, int NCBW>
+__device__ __forceinline__ void load_b_f32(const float *__restrict__ B, int k0, int wc, int lr,
+                                           int lc, float (&b)[8][WCB]) {
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+#pragma unroll
+        for (int t = 0; t < WCB; ++t) b[s][t] = B[(k0 + 4 * s + lr) * NCOL + 16 * (wc + NCBW * t) + lc];
+}
+
+template <int S, int WRB, int WCB, int NRG>
+__device__ __forceinline__ void mma_group_f32(const float *As, int k0, int wr, int lr, int lc,
+                                              const float (&b)[8][WCB], floatx4 (&acc)[WRB][WCB]) {
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        float a[WRB];
+#pragma unroll
+        for (int u = 0; u < WRB; ++u) a[u] = As[(16 * (wr + NRG * u) + lc) * S + k0 + 4 * s + lr];
+#pragma unroll
+        for (int u = 0; u < WRB; ++u)
+#pragma unroll
+            for (int t = 0; t < WCB; ++t)
+                acc[u][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u], b[s][t], acc[u][t], 0, 0, 0);
+    }
+}
+
 template <int K, int NCOL, int S, int WRB, int WCB, int NCBW, int NRG>
 __device__ __forceinline__ void mfma_lds_x_global_f32(const float *As, const float *__restrict__ B,
                                                       int wr, int wc,
                                                       floatx4 (&acc)[WRB][WCB]) {
     constexpr int KG = 32;  // 8 MFMA k-steps of 4
-    static_assert(K % KG == 0, "K must be a multiple of 32");
+    static_assert(K % (2 * KG) == 0, "K must be a multiple of 64");
     const int lane = threadIdx.x & 63;
     const int lr = lane >> 4, lc = lane & 15;
-    float bc[8][WCB], bn[8][WCB];
-#pragma unroll
-    for (int s = 0; s < 8; ++s)
-#pragma unroll
-        for (int t = 0; t < WCB; ++t) bc[s][t] = B[(4 * s + lr) * NCOL + 16 * (wc + NCBW * t) + lc];
+    float b0[8][WCB], b1[8][WCB];
+    load_b_f32<NCOL, WCB, NCBW>(B, 0, wc, lr, lc, b0);
 #pragma unroll 1
-    for (int k0 = 0; k0 < K; k0 += KG) {
-        const int kn = k0 + KG < K ? k0 + KG : k0;
+    for (int k0 = 0; k0 < K; k0 += 2 * KG) {
+        load_b_f32<NCOL, WCB, NCBW>(B, k0 + KG, wc, lr, lc, b1);
+        __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the MFMAs
+        mma_group_f32<S, WRB, WCB, NRG>(As, k0, wr, lr, lc, b0, acc);
+        // the last iteration reloads the final group (harmless, no branch)
+        const int kn = k0 + 2 * KG < K ? k0 + 2 * KG : K - KG;
+        load_b_f32<NCOL, WCB, NCBW>(B, kn, wc, lr, lc, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_group_f32<S, WRB, WCB, NRG>(As, k0 + KG, wr, lr, lc, b1, acc);
+    }
+}
+
+template <int K, int WCB, int NCBW>
+__device__ __forceinline__ void load_b_bf16(const uint16_t *__restrict__ Bt, int k0, int wc,
+                                            int lk, int lc, bf16x8 (&b)[4][WCB]) {
 #pragma unroll
-        for (int s = 0; s < 8; ++s)
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int t = 0; t < WCB; ++t)
+            b[s][t] = *reinterpret_cast<const bf16x8 *>(
+                Bt + (int64_t)(16 * (wc + NCBW * t) + lc) * K + k0 + 32 * s + lk);
+}
+
+template <int S, int WRB, int WCB, int NRG>
+__device__ __forceinline__ void mma_group_bf16(const uint16_t *As, int k0, int wr, int lk, int lc,
+                                               const bf16x8 (&b)[4][WCB],
+                                               floatx4 (&acc)[WRB][WCB]) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        bf16x8 a[WRB];
+#pragma unroll
+        for (int u = 0; u < WRB; ++u)
+            a[u] = *reinterpret_cast<const bf16x8 *>(
+                &As[(16 * (wr + NRG * u) + lc) * S + k0 + 32 * s + lk]);
+#pragma unroll
+        for (int u = 0; u < WRB; ++u)
 #pragma unroll
             for (int t = 0; t < WCB; ++t)
-                bn[s][t] = B[(kn + 4 * s + lr) * NCOL + 16 * (wc + NCBW * t) + lc];
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-            float a[WRB];
-#pragma unroll
-            for (int u = 0; u < WRB; ++u) a[u] = As[(16 * (wr + NRG * u) + lc) * S + k0 + 4 * s + lr];
-#pragma unroll
-            for (int u = 0; u < WRB; ++u)
-#pragma unroll
-                for (int t = 0; t < WCB; ++t)
-                    acc[u][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u], bc[s][t], acc[u][t], 0, 0, 0);
-        }
-#pragma unroll
-        for (int s = 0; s < 8; ++s)
-#pragma unroll
-            for (int t = 0; t < WCB; ++t) bc[s][t] = bn[s][t];
+                acc[u][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u], b[s][t], acc[u][t], 0, 0, 0);
     }
 }
 
@@ -277,42 +331,20 @@ __device__ __forceinline__ void mfma_lds_x_global_bf16(const uint16_t *As,
                                                        const uint16_t *__restrict__ Bt, int wr,
                                                        int wc, floatx4 (&acc)[WRB][WCB]) {
     constexpr int KG = 128;  // 4 MFMA k-steps of 32
-    static_assert(K % KG == 0, "K must be a multiple of 128");
+    static_assert(K % (2 * KG) == 0, "K must be a multiple of 256");
     const int lane = threadIdx.x & 63;
     const int lk = 8 * (lane >> 4), lc = lane & 15;
-    bf16x8 bc[4][WCB], bn[4][WCB];
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int t = 0; t < WCB; ++t)
-            bc[s][t] = *reinterpret_cast<const bf16x8 *>(
-                Bt + (int64_t)(16 * (wc + NCBW * t) + lc) * K + 32 * s + lk);
+    bf16x8 b0[4][WCB], b1[4][WCB];
+    load_b_bf16<K, WCB, NCBW>(Bt, 0, wc, lk, lc, b0);
 #pragma unroll 1
-    for (int k0 = 0; k0 < K; k0 += KG) {
-        const int kn = k0 + KG < K ? k0 + KG : k0;
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-            for (int t = 0; t < WCB; ++t)
-                bn[s][t] = *reinterpret_cast<const bf16x8 *>(
-                    Bt + (int64_t)(16 * (wc + NCBW * t) + lc) * K + kn + 32 * s + lk);
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            bf16x8 a[WRB];
-#pragma unroll
-            for (int u = 0; u < WRB; ++u)
-                a[u] = *reinterpret_cast<const bf16x8 *>(
-                    &As[(16 * (wr + NRG * u) + lc) * S + k0 + 32 * s + lk]);
-#pragma unroll
-            for (int u = 0; u < WRB; ++u)
-#pragma unroll
-                for (int t = 0; t < WCB; ++t)
-                    acc[u][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u], bc[s][t], acc[u][t], 0, 0, 0);
-        }
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-            for (int t = 0; t < WCB; ++t) bc[s][t] = bn[s][t];
+    for (int k0 = 0; k0 < K; k0 += 2 * KG) {
+        load_b_bf16<K, WCB, NCBW>(Bt, k0 + KG, wc, lk, lc, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_group_bf16<S, WRB, WCB, NRG>(As, k0, wr, lk, lc, b0, acc);
+        const int kn = k0 + 2 * KG < K ? k0 + 2 * KG : K - KG;
+        load_b_bf16<K, WCB, NCBW>(Bt, kn, wc, lk, lc, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_group_bf16<S, WRB, WCB, NRG>(As, k0 + KG, wr, lk, lc, b1, acc);
     }
 }
 
@@ -322,36 +354,49 @@ constexpr int tile_rows() {
     return (K * (kBf ? 2 : 4) * 64 <= 65536) ? 64 : 32;
 }
 
+// Logical tile of physical block b of n: consecutive blocks are dispatched to
+// the 8 XCDs in turn, so this gives each XCD one contiguous range of tiles and
+// keeps the rows an XCD gathers local to its L2.
+__device__ __forceinline__ int32_t xcd_tile(int32_t b, int32_t n) {
+    const int32_t per = n / 8, rem = n % 8;
+    const int32_t x = b % 8, l = b / 8;
+    return x < rem ? x * (per + 1) + l : rem * (per + 1) + (x - rem) * per + l;
+}
+
 // ================================================================ forward
+constexpr int kFwdWaves = 4;
+
 template <int M, int CI, int CO, int kBasis, bool kBf>
-__global__ void __launch_bounds__(256, 2)
+__global__ void __launch_bounds__(kFwdWaves * 64, 2)
     fwd_fused_kernel(int32_t n_out, const int32_t *__restrict__ row_ptr,
                      const int32_t *__restrict__ col_idx, const float *__restrict__ v,
                      sbc_geometry g, const void *__restrict__ F, const void *__restrict__ Wop,
                      float *__restrict__ Y) {
+    constexpr int NW = kFwdWaves;
     constexpr int K = M * CI;
     constexpr int TR = tile_rows<K, kBf>();
     constexpr int S = K + (kBf ? 8 : 4);           // padded LDS row (elements)
     constexpr int NRB = TR / 16, NCB = CO / 16;
     static_assert(CO % 16 == 0 && CI % 4 == 0, "shape");
-    constexpr int NCBW = NCB < 4 ? NCB : 4;        // column groups of waves
-    constexpr int NRG = 4 / NCBW;                  // row groups of waves
+    constexpr int NCBW = NCB < NW ? NCB : NW;      // column groups of waves
+    constexpr int NRG = NW / NCBW;                 // row groups of waves
     static_assert(NCB % NCBW == 0 && NRB % NRG == 0, "tile split");
     constexpr int WCB = NCB / NCBW, WRB = NRB / NRG;
+    constexpr int RPW = TR / NW;
 
     using GT = typename std::conditional<kBf, uint16_t, float>::type;
     __shared__ __attribute__((aligned(16))) GT Gs[TR * S];
-    __shared__ EdgeStage<M> stage[4];
+    __shared__ EdgeStage<M> stage[NW];
 
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
-    const int32_t row0 = blockIdx.x * TR;
+    const int32_t row0 = xcd_tile(blockIdx.x, gridDim.x) * TR;
     const double inv_r = 1.0 / (double)g.radius;
     const float inv_tau = 1.0f / g.tau;
 
-    gather_rows<M, CI, kBasis, kBf, kBf, false, TR / 4>(row0 + w * (TR / 4), n_out, row_ptr,
-                                                         col_idx, nullptr, v, g, F, Gs, S,
-                                                         w * (TR / 4), stage[w], inv_r, inv_tau);
+    gather_rows<M, CI, kBasis, kBf, kBf, false, RPW>(row0 + w * RPW, n_out, row_ptr, col_idx,
+                                                     nullptr, v, g, F, Gs, S, w * RPW, stage[w],
+                                                     inv_r, inv_tau);
     __syncthreads();
 
     const int wc = w % NCBW, wr = w / NCBW;
@@ -378,40 +423,248 @@ __global__ void __launch_bounds__(256, 2)
             }
 }
 
-// ================================================================ backward (D-route)
-template <int K2, bool kBf>
-constexpr int bwd_tile_rows() {
-    return (K2 * (kBf ? 2 : 4) * 64 <= 65536) ? 64 : 32;
+// ================================================================ forward, G in registers
+// Each wave owns tiles of 16 output rows: lane l serves row (l & 15) and
+// channel group g = l >> 4, i.e. channels [g*CI/4, (g+1)*CI/4) of every basis
+// function.  G accumulates in registers and is the MFMA A operand as is: at
+// k-step s lane group g contributes G[row, m(s), g*CI/4 + t(s)], so the
+// contraction index is a permutation of (m, c) that the W operand follows.
+// W sits in LDS, staged once per persistent block; waves then run their
+// tiles independently, so one wave's gather overlaps another's MFMAs.
+constexpr int kRegWaves = 8;
+
+// bytes of W in LDS for the register-resident forward
+template <int M, int CI, int CO, bool kBf>
+constexpr int reg_w_bytes() {
+    return M * CI * CO * (kBf ? 2 : 4) + (kBf ? CO * 16 : 0);
+}
+
+template <int M, int CI, int CO, bool kBf>
+constexpr bool reg_forward_fits() {
+    // CI <= 32: wider inputs hold M*CI/4 gather accumulators per lane, which
+    // leaves too few waves per CU to hide the gather; the LDS-tile kernel wins
+    return reg_w_bytes<M, CI, CO, kBf>() <= 131072 && CI % 16 == 0 && CI <= 32 &&
+           CO % 16 == 0 && (!kBf || (CI / 4) % 8 == 0);
 }
 
 template <int M, int CI, int CO, int kBasis, bool kBf>
-__global__ void __launch_bounds__(256, 1)
+__global__ void __launch_bounds__(kRegWaves * 64, 1)
+    fwd_reg_kernel(int32_t n_out, int32_t n_tiles, const int32_t *__restrict__ row_ptr,
+                   const int32_t *__restrict__ col_idx, const float *__restrict__ v,
+                   sbc_geometry g, const void *__restrict__ Fv, const void *__restrict__ Wv,
+                   float *__restrict__ Y) {
+    constexpr int K = M * CI;
+    constexpr int CG = CI / 4;          // channels per lane group
+    constexpr int NCB = CO / 16;        // 16-column blocks of Y
+    constexpr int NT = kRegWaves * 64;
+    static_assert(reg_forward_fits<M, CI, CO, kBf>(), "shape");
+    // W in LDS.  float32: [K][16][NCB] (b for all column blocks of one (k, n)
+    // contiguous);  bf16: [NCB][16][K + 8] (8 consecutive k of one n contiguous)
+    constexpr int SWB = K + 8;
+    constexpr int WLDS = kBf ? NCB * 16 * SWB * 2 : K * CO * 4;
+    __shared__ __attribute__((aligned(16))) char Wl[WLDS];
+
+    if constexpr (!kBf) {
+        const float *W = static_cast<const float *>(Wv);  // [K, CO]
+        float *Wf = reinterpret_cast<float *>(Wl);
+        for (int q = threadIdx.x; q < K * CO; q += NT) {
+            const int k = q / CO, n = q % CO;
+            Wf[(k * 16 + (n & 15)) * NCB + (n >> 4)] = W[q];
+        }
+    } else {
+        const uint16_t *W = static_cast<const uint16_t *>(Wv);  // [K, CO] bf16
+        uint16_t *Wb = reinterpret_cast<uint16_t *>(Wl);
+        for (int q = threadIdx.x; q < K * CO; q += NT) {
+            const int k = q / CO, n = q % CO;
+            Wb[((n >> 4) * 16 + (n & 15)) * SWB + k] = W[q];
+        }
+    }
+    __syncthreads();
+
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    const int rl = lane & 15;        // row within the tile
+    const int gq = lane >> 4;        // channel group
+    const double inv_r = 1.0 / (double)g.radius;
+    const float inv_tau = 1.0f / g.tau;
+
+    // tiles of this wave: the block's XCD owns a contiguous range, its waves
+    // interleave (with fewer than 8 blocks, one range per block)
+    const int32_t G = gridDim.x, X = G < 8 ? G : 8;
+    const int32_t x = blockIdx.x % X;
+    const int32_t gx = G / X + (x < G % X ? 1 : 0);
+    const int32_t waves_x = gx * kRegWaves;
+    const int32_t lw = (blockIdx.x / X) * kRegWaves + w;
+    const int32_t t_begin = (int32_t)((int64_t)x * n_tiles / X);
+    const int32_t t_end = (int32_t)((int64_t)(x + 1) * n_tiles / X);
+
+#pragma unroll 1
+    for (int32_t tile = t_begin + lw; tile < t_end; tile += waves_x) {
+        const int32_t row = tile * 16 + rl;
+        int32_t e0 = 0, e1 = 0;
+        if (row < n_out) {
+            e0 = row_ptr[row];
+            e1 = row_ptr[row + 1];
+        }
+        int32_t len = e1 - e0;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int32_t o = __shfl_xor(len, d, 64);
+            len = o > len ? o : len;
+        }
+        float acc[M][CG];
+#pragma unroll
+        for (int m = 0; m < M; ++m)
+#pragma unroll
+            for (int t = 0; t < CG; ++t) acc[m][t] = 0.f;
+
+        // edges in flight per lane: two while the accumulators leave room
+        constexpr int U = M * CG >= 128 ? 1 : 2;
+#pragma unroll 1
+        for (int32_t q = 0; q < len; q += U) {
+            float f[U][CG];
+            float bv[U][M];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t e = e0 + q + u;
+                if (e < e1) {
+                    const int32_t j = col_idx[e];
+                    edge_basis<M, kBasis>(g, v, row, j, e, inv_r, inv_tau, bv[u]);
+                    if constexpr (kBf) {
+                        const uint16_t *src = static_cast<const uint16_t *>(Fv) + (int64_t)j * CI + gq * CG;
+#pragma unroll
+                        for (int c = 0; c < CG; c += 8) {
+                            const uint4 raw = *reinterpret_cast<const uint4 *>(src + c);
+                            const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+                            for (int k = 0; k < 4; ++k) {
+                                f[u][c + 2 * k] = __uint_as_float(w4[k] << 16);
+                                f[u][c + 2 * k + 1] = __uint_as_float(w4[k] & 0xFFFF0000u);
+                            }
+                        }
+                    } else {
+                        const float *src = static_cast<const float *>(Fv) + (int64_t)j * CI + gq * CG;
+#pragma unroll
+                        for (int c = 0; c < CG; c += 4) {
+                            const float4 raw = *reinterpret_cast<const float4 *>(src + c);
+                            f[u][c] = raw.x;
+                            f[u][c + 1] = raw.y;
+                            f[u][c + 2] = raw.z;
+                            f[u][c + 3] = raw.w;
+                        }
+                    }
+                } else {
+#pragma unroll
+                    for (int m = 0; m < M; ++m) bv[u][m] = 0.f;
+#pragma unroll
+                    for (int c = 0; c < CG; ++c) f[u][c] = 0.f;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int m = 0; m < M; ++m)
+#pragma unroll
+                    for (int t = 0; t < CG; ++t) acc[m][t] += bv[u][m] * f[u][t];
+        }
+
+        // ---- Y rows of the tile = G W on the matrix cores
+        floatx4 ay[NCB];
+#pragma unroll
+        for (int nb = 0; nb < NCB; ++nb) ay[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (!kBf) {
+            const float *Wf = reinterpret_cast<const float *>(Wl);
+#pragma unroll
+            for (int m = 0; m < M; ++m)
+#pragma unroll
+                for (int t = 0; t < CG; ++t) {
+                    const int kB = m * CI + gq * CG + t;
+                    float b[NCB];
+#pragma unroll
+                    for (int nb = 0; nb < NCB; ++nb) b[nb] = Wf[(kB * 16 + rl) * NCB + nb];
+#pragma unroll
+                    for (int nb = 0; nb < NCB; ++nb)
+                        ay[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[m][t], b[nb], ay[nb], 0, 0, 0);
+                    if ((t & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+                }
+        } else {
+            const uint16_t *Wb = reinterpret_cast<const uint16_t *>(Wl);
+#pragma unroll
+            for (int m = 0; m < M; ++m)
+#pragma unroll
+                for (int t0 = 0; t0 < CG; t0 += 8) {
+                    bf16x8 a;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const uint16_t hb = f2bf(acc[m][t0 + j]);
+                        a[j] = __builtin_bit_cast(__bf16, hb);
+                    }
+                    const int kB = m * CI + gq * CG + t0;
+#pragma unroll
+                    for (int nb = 0; nb < NCB; ++nb) {
+                        const bf16x8 b = *reinterpret_cast<const bf16x8 *>(&Wb[(nb * 16 + rl) * SWB + kB]);
+                        ay[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, ay[nb], 0, 0, 0);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+        }
+        // D layout: lane holds rows 4*(l >> 4) + r, column l & 15 of each block
+#pragma unroll
+        for (int nb = 0; nb < NCB; ++nb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int32_t yr = tile * 16 + 4 * gq + r;
+                if (yr < n_out) Y[(int64_t)yr * CO + 16 * nb + rl] = ay[nb][r];
+            }
+    }
+}
+
+// ================================================================ backward (D-route)
+template <int K2, bool kBf>
+constexpr int bwd_tile_rows() {
+    return kBf ? 32 : ((K2 * 4 * 64 <= 65536) ? 64 : 32);
+}
+
+// Waves per backward block: eight when the dF tile has at least eight 16x16 blocks.
+template <int M, int CI, int CO, bool kBf>
+constexpr int bwd_waves() {
+    return (bwd_tile_rows<M * CO, kBf>() / 16) * (CI / 16) >= 8 ? 8 : 4;
+}
+
+template <int M, int CI, int CO, int kBasis, bool kBf>
+__global__ void __launch_bounds__((bwd_waves<M, CI, CO, kBf>() * 64), 1)
     bwd_fused_kernel(int32_t n_in, int32_t n_tiles, const int32_t *__restrict__ col_ptr,
                      const int32_t *__restrict__ row_idx, const int32_t *__restrict__ perm,
                      const float *__restrict__ v, sbc_geometry g, const void *__restrict__ Fv,
                      const void *__restrict__ dY, const void *__restrict__ Wop,
                      float *__restrict__ dF, float *__restrict__ dW_part) {
     // dF == nullptr: no input gradient; dW_part == nullptr: no weight gradient
+    constexpr int NW = bwd_waves<M, CI, CO, kBf>();
+    constexpr int NT = NW * 64;
     constexpr int K2 = M * CO;
     constexpr int TR = bwd_tile_rows<K2, kBf>();
+    constexpr int RPW = TR / NW;
     constexpr int SD = K2 + (kBf ? 8 : 4);
-    constexpr int SF = CI + 4;
+    constexpr int SF = CI + 4;        // float32 F tile row
+    constexpr int ST = TR + 8;        // bf16 transposed tiles (D^T, F^T) row
     static_assert(CI % 16 == 0 && CO % 16 == 0, "shape");
     // dF tile [TR, CI]: 16x16 blocks over waves
     constexpr int NRB = TR / 16, NCB = CI / 16;
-    constexpr int NCBW = NCB < 4 ? NCB : 4;
-    constexpr int NRG = 4 / NCBW;
+    constexpr int NCBW = NCB < NW ? NCB : NW;
+    constexpr int NRG = NW / NCBW;
     static_assert(NCB % NCBW == 0 && NRB % NRG == 0, "dF split");
     constexpr int WCB = NCB / NCBW, WRB = NRB / NRG;
-    // dW [CI, K2]: each wave owns K2/4 columns, all CI rows
-    constexpr int NWB = (K2 / 16) / 4;                 // column blocks per wave
+    // dW [CI, K2]: each wave owns K2/NW columns, all CI rows
+    constexpr int NWB = (K2 / 16) / NW;                // column blocks per wave
     constexpr int NIB = CI / 16;                       // row blocks
-    static_assert((K2 / 16) % 4 == 0, "dW split");
+    static_assert((K2 / 16) % NW == 0, "dW split");
 
     using DT = typename std::conditional<kBf, uint16_t, float>::type;
     __shared__ __attribute__((aligned(16))) DT Ds[TR * SD];
-    __shared__ __attribute__((aligned(16))) float Fs[TR * SF];
-    __shared__ EdgeStage<M> stage[4];
+    __shared__ __attribute__((aligned(16))) float Fs[kBf ? 1 : TR * SF];
+    __shared__ __attribute__((aligned(16))) uint16_t DsT[kBf ? K2 * ST : 1];
+    __shared__ __attribute__((aligned(16))) uint16_t FsT[kBf ? CI * ST : 1];
+    __shared__ EdgeStage<M> stage[NW];
 
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
@@ -425,26 +678,35 @@ __global__ void __launch_bounds__(256, 1)
 #pragma unroll
         for (int b = 0; b < NWB; ++b) accw[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+    // tiles of this block: its XCD's contiguous range, interleaved over the
+    // XCD's blocks (with fewer than 8 blocks, one range per block)
+    const int32_t G = gridDim.x, X = G < 8 ? G : 8;
+    const int32_t x = blockIdx.x % X, l = blockIdx.x / X;
+    const int32_t gx = G / X + (x < G % X ? 1 : 0);
+    const int32_t t_begin = (int32_t)((int64_t)x * n_tiles / X);
+    const int32_t t_end = (int32_t)((int64_t)(x + 1) * n_tiles / X);
+
 #pragma unroll 1
-    for (int32_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    for (int32_t tile = t_begin + l; tile < t_end; tile += gx) {
         const int32_t row0 = tile * TR;
-        // F rows of the tile -> Fs (float32), zero past n_in
-        for (int x = threadIdx.x; x < TR * CI; x += 256) {
-            const int r = x / CI, c = x % CI;
+        // F rows of the tile: float32 row-major, or bf16 transposed
+        for (int q = threadIdx.x; q < TR * CI; q += NT) {
+            const int r = q / CI, c = q % CI;
             const int32_t row = row0 + r;
-            float f = 0.f;
-            if (row < n_in) {
-                if constexpr (kBf)
-                    f = bf2f(static_cast<const uint16_t *>(Fv)[(int64_t)row * CI + c]);
-                else
-                    f = static_cast<const float *>(Fv)[(int64_t)row * CI + c];
+            if constexpr (kBf) {
+                uint16_t f = 0;
+                if (row < n_in) f = static_cast<const uint16_t *>(Fv)[(int64_t)row * CI + c];
+                FsT[c * ST + r] = f;
+            } else {
+                float f = 0.f;
+                if (row < n_in) f = static_cast<const float *>(Fv)[(int64_t)row * CI + c];
+                Fs[r * SF + c] = f;
             }
-            Fs[r * SF + c] = f;
         }
-        gather_rows<M, CO, kBasis, kBf, kBf, true, TR / 4>(row0 + w * (TR / 4), n_in, col_ptr,
-                                                            row_idx, perm, v, g, dY, Ds, SD,
-                                                            w * (TR / 4), stage[w], inv_r,
-                                                            inv_tau);
+        gather_rows<M, CO, kBasis, kBf, kBf, true, RPW>(row0 + w * RPW, n_in, col_ptr, row_idx,
+                                                         perm, v, g, dY, Ds, SD, w * RPW,
+                                                         stage[w], inv_r, inv_tau,
+                                                         kBf ? DsT : nullptr, ST);
         __syncthreads();
 
         // ---- dF_tile = D_tile Wt  ([TR, K2] x [K2, CI])
@@ -472,27 +734,42 @@ __global__ void __launch_bounds__(256, 1)
                 }
         }
 
-        // ---- dW += F_tile^T D_tile  ([CI, TR] x [TR, K2]), float32 MFMA over the tile rows
+        // ---- dW += F_tile^T D_tile  ([CI, TR] x [TR, K2]) over the tile rows
         if (dW_part) {
+            if constexpr (!kBf) {
 #pragma unroll 2
-        for (int k0 = 0; k0 < TR; k0 += 4) {
-            const int kk = k0 + (lane >> 4);
-            float a[NIB];
+                for (int k0 = 0; k0 < TR; k0 += 4) {
+                    const int kk = k0 + (lane >> 4);
+                    float a[NIB];
 #pragma unroll
-            for (int ib = 0; ib < NIB; ++ib) a[ib] = Fs[kk * SF + 16 * ib + (lane & 15)];
+                    for (int ib = 0; ib < NIB; ++ib) a[ib] = Fs[kk * SF + 16 * ib + (lane & 15)];
 #pragma unroll
-            for (int nb = 0; nb < NWB; ++nb) {
-                const int col = 16 * (w * NWB + nb) + (lane & 15);
-                float bb;
-                if constexpr (kBf)
-                    bb = bf2f(Ds[kk * SD + col]);
-                else
-                    bb = Ds[kk * SD + col];
+                    for (int nb = 0; nb < NWB; ++nb) {
+                        const float bb = Ds[kk * SD + 16 * (w * NWB + nb) + (lane & 15)];
 #pragma unroll
-                for (int ib = 0; ib < NIB; ++ib)
-                    accw[ib][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ib], bb, accw[ib][nb], 0, 0, 0);
+                        for (int ib = 0; ib < NIB; ++ib)
+                            accw[ib][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ib], bb, accw[ib][nb], 0, 0, 0);
+                    }
+                }
+            } else {
+                // bf16 MFMA: 8 consecutive tile rows per lane from the transposed tiles
+#pragma unroll
+                for (int k0 = 0; k0 < TR; k0 += 32) {
+                    const int kk = k0 + 8 * (lane >> 4);
+                    bf16x8 a[NIB];
+#pragma unroll
+                    for (int ib = 0; ib < NIB; ++ib)
+                        a[ib] = *reinterpret_cast<const bf16x8 *>(&FsT[(16 * ib + (lane & 15)) * ST + kk]);
+#pragma unroll
+                    for (int nb = 0; nb < NWB; ++nb) {
+                        const bf16x8 bb = *reinterpret_cast<const bf16x8 *>(
+                            &DsT[(16 * (w * NWB + nb) + (lane & 15)) * ST + kk]);
+#pragma unroll
+                        for (int ib = 0; ib < NIB; ++ib)
+                            accw[ib][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ib], bb, accw[ib][nb], 0, 0, 0);
+                    }
+                }
             }
-        }
         }
         __syncthreads();
     }
@@ -574,6 +851,8 @@ __global__ void w_perm_f32_kernel(const float *__restrict__ W, int32_t M, int32_
 // ---------------------------------------------------------------- dispatch tables
 using FwdFn = void (*)(int32_t, const int32_t *, const int32_t *, const float *, sbc_geometry,
                        const void *, const void *, float *);
+using RegFn = void (*)(int32_t, int32_t, const int32_t *, const int32_t *, const float *,
+                       sbc_geometry, const void *, const void *, float *);
 using BwdFn = void (*)(int32_t, int32_t, const int32_t *, const int32_t *, const int32_t *,
                        const float *, sbc_geometry, const void *, const void *, const void *,
                        float *, float *);
@@ -598,6 +877,27 @@ FwdFn fwd_for(int basis_mode) {
             return nullptr;
     }
     return nullptr;
+}
+
+template <int M, int CI, int CO, bool kBf>
+RegFn reg_for(int basis_mode) {
+    if constexpr (!reg_forward_fits<M, CI, CO, kBf>()) {
+        return nullptr;
+    } else {
+        switch (basis_mode) {
+            case 0: return fwd_reg_kernel<M, CI, CO, 0, kBf>;
+            case SBC_BASIS_MONO4 + 1:
+                if constexpr (M == 4) return fwd_reg_kernel<M, CI, CO, SBC_BASIS_MONO4 + 1, kBf>;
+                return nullptr;
+            case SBC_BASIS_MONO8 + 1:
+                if constexpr (M == 8) return fwd_reg_kernel<M, CI, CO, SBC_BASIS_MONO8 + 1, kBf>;
+                return nullptr;
+            case SBC_BASIS_EVENT8 + 1:
+                if constexpr (M == 8) return fwd_reg_kernel<M, CI, CO, SBC_BASIS_EVENT8 + 1, kBf>;
+                return nullptr;
+        }
+        return nullptr;
+    }
 }
 
 template <int M, int CI, int CO, bool kBf>
@@ -637,6 +937,14 @@ BwdFn bwd_for(int basis_mode) {
 FwdFn find_fwd(const Shape &s, int basis_mode) {
 #define SBC_X(m_, ci_, co_, bf_) \
     if (s.M == m_ && s.CI == ci_ && s.CO == co_ && s.bf == bf_) return fwd_for<m_, ci_, co_, bf_>(basis_mode);
+    SBC_FWD_SHAPES(SBC_X)
+#undef SBC_X
+    return nullptr;
+}
+
+RegFn find_reg(const Shape &s, int basis_mode) {
+#define SBC_X(m_, ci_, co_, bf_) \
+    if (s.M == m_ && s.CI == ci_ && s.CO == co_ && s.bf == bf_) return reg_for<m_, ci_, co_, bf_>(basis_mode);
     SBC_FWD_SHAPES(SBC_X)
 #undef SBC_X
     return nullptr;
@@ -713,6 +1021,23 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
     FwdFn fn = find_fwd(Shape{M, CI, CO, bf}, basis_mode_of(v, g));
     if (!fn) return fail(SBC_ERR_UNSUPPORTED, "no fused forward for this shape");
     if (csr->n_rows == 0) return SBC_OK;
+    sbc_geometry gr = g ? *g : sbc_geometry{};
+    if (RegFn rf = find_reg(Shape{M, CI, CO, bf}, basis_mode_of(v, g))) {
+        const int32_t n_tiles = (csr->n_rows + 15) / 16;
+        int per_cu = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(rf),
+                                                         kRegWaves * 64, 0) != hipSuccess ||
+            per_cu < 1)
+            per_cu = 1;
+        int blocks = (n_tiles + kRegWaves - 1) / kRegWaves;
+        if (blocks > device_cus() * per_cu) blocks = device_cus() * per_cu;
+        trace_before("fwd_fused", stream);
+        hipLaunchKernelGGL(rf, dim3(blocks), dim3(kRegWaves * 64), 0, stream, csr->n_rows,
+                           n_tiles, csr->row_ptr, csr->col_idx, v, gr, F, W, Y);
+        SBC_LAUNCH_CHECK();
+        trace_after("fwd_fused", stream);
+        return SBC_OK;
+    }
     const void *Wop = W;
     if (bf) {  // [CO, K] bf16: element (m, c, p) at p*K + m*CI + c
         const int64_t K = (int64_t)M * CI;
@@ -723,8 +1048,8 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
     const int TR = (K * (bf ? 2 : 4) * 64 <= 65536) ? 64 : 32;
     sbc_geometry gg = g ? *g : sbc_geometry{};
     trace_before("fwd_fused", stream);
-    hipLaunchKernelGGL(fn, dim3(grid_for(csr->n_rows, TR)), dim3(256), 0, stream, csr->n_rows,
-                       csr->row_ptr, csr->col_idx, v, gg, F, Wop, Y);
+    hipLaunchKernelGGL(fn, dim3(grid_for(csr->n_rows, TR)), dim3(kFwdWaves * 64), 0, stream,
+                       csr->n_rows, csr->row_ptr, csr->col_idx, v, gg, F, Wop, Y);
     SBC_LAUNCH_CHECK();
     trace_after("fwd_fused", stream);
     return SBC_OK;
@@ -746,8 +1071,9 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
         SBC_TRY(launch_perm(W, true, true, M, CI, CO, CO, K2, 1, wt, stream));
     else
         SBC_TRY(launch_perm(W, false, false, M, CI, CO, (int64_t)CO * CI, 1, CI, wt, stream));
-    const int TR = (K2 * (bf ? 2 : 4) * 64 <= 65536) ? 64 : 32;
+    const int TR = bf ? 32 : ((K2 * 4 * 64 <= 65536) ? 64 : 32);
     const int32_t n_tiles = (n_in + TR - 1) / TR;
+    const int nw = (TR / 16) * (CI / 16) >= 8 ? 8 : 4;
     int blocks = device_cus();
     if (blocks > kMaxBlocksBwd) blocks = kMaxBlocksBwd;
     if (blocks > n_tiles) blocks = n_tiles;
@@ -755,7 +1081,7 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
     sbc_geometry gg = g ? *g : sbc_geometry{};
     if (n_in > 0 && (dF || dW)) {
         trace_before("bwd_fused", stream);
-        hipLaunchKernelGGL(fn, dim3(blocks), dim3(256), 0, stream, n_in, n_tiles, csc->col_ptr,
+        hipLaunchKernelGGL(fn, dim3(blocks), dim3(nw * 64), 0, stream, n_in, n_tiles, csc->col_ptr,
                            csc->row_idx, csc->edge_perm, v, gg, F, dY, wt, dF,
                            dW ? part : nullptr);
         SBC_LAUNCH_CHECK();

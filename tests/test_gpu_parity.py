@@ -39,6 +39,11 @@ SMALL = {
     "fz_pts_bf16": lambda: workloads.small_points(seed=10, dtype="bf16", c_in=32, c_out=32),
     "fz_ev32": lambda: workloads.small_events(seed=3, c=32, n=5003),
     "fz_ev_bf16": lambda: workloads.small_events(seed=4, c=64, dtype="bf16", n=4099),
+    # fewer tiles than XCDs / persistent blocks
+    "fz_tiny_ev": lambda: workloads.small_events(seed=5, c=32, n=150),
+    "fz_tiny_pts": lambda: workloads.small_points(seed=12, n_clouds=1, n=90, c_in=64, c_out=64),
+    "fz_tiny_bf16": lambda: workloads.small_events(seed=6, c=64, dtype="bf16", n=70),
+    "fz_tiny_bf16_32": lambda: workloads.small_events(seed=13, c=32, dtype="bf16", n=70),
 }
 FULL = list(workloads.WORKLOADS)
 ORDERS = ["spmm_first", "gemm_first"]
