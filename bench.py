@@ -16,8 +16,12 @@ on the same workload, outside the timed region.
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
+import re
 import statistics
 import sys
 import time
@@ -42,6 +46,144 @@ DESCRIPTIONS = {
     "events_1m_bf16": "1M bursty events, 346x260 pixels, 200 ms; 3x3 block, 5 ms window; M 8; "
                       "64 -> 64 channels bf16 in, fp32 accumulate",
 }
+
+
+SRC_DIR = os.path.join(ROOT, "paper_2012_01170_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+# device function -> the name the library's trace hook gives its launch
+TRACE_NAME = {"bwd_fused_kernel": "bwd_fused", "fwd_fused_kernel": "fwd_fused",
+              "fwd_reg_kernel": "fwd_fused", "dw_reduce_kernel": "bwd_dw_reduce"}
+
+
+def source_fingerprint():
+    """Hash of the HIP sources: byte counts taken on other sources do not apply."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(SRC_DIR)):
+        if name.endswith((".hip", ".hpp")):
+            h.update(name.encode())
+            with open(os.path.join(SRC_DIR, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def short_kernel_name(name):
+    """'void ns::(anonymous namespace)::f<...>(args)' -> 'f<...>'."""
+    name = name.replace("(anonymous namespace)::", "")
+    if name.startswith("void "):
+        name = name[5:]
+    depth, cut = 0, len(name)
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            cut = i
+            break
+    return name[:cut].split("::")[-1] if "<" not in name[:cut] else \
+        name[:cut][name[:cut].rfind("::", 0, name[:cut].find("<")) + 2:]
+
+
+def read_traffic(workload):
+    """HBM bytes per dispatch of each traced kernel from a committed counter summary.
+
+    Returns (table, note): table maps trace name -> bytes per launch, or is None
+    when there is no summary or the sources changed since it was taken.
+    """
+    path = os.path.join(PROFILES, f"hbm_traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    table, fp = {}, None
+    with open(path) as f:
+        for line in f:
+            parts = line.split()
+            if len(parts) >= 2 and parts[0] == "source_fingerprint:":
+                fp = parts[1]
+            elif len(parts) >= 6 and parts[0] == "traffic":
+                table[parts[1]] = float(parts[5])
+    if fp != source_fingerprint():
+        return None, f"{os.path.basename(path)} was taken on other sources"
+    return table, os.path.basename(path)
+
+
+def _counter_rows(directory):
+    files = glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {directory}")
+    with open(files[0]) as f:
+        return list(csv.DictReader(f))
+
+
+def summarize_traffic(fetch_dir, write_dir, probe_mb, command):
+    """Text summary of FETCH_SIZE / WRITE_SIZE per dispatch, scaled by a copy probe.
+
+    The probe is one plain device-to-device copy of probe_mb MiB run by the
+    profiled command after its steps: it reads and writes exactly that many
+    bytes, so true bytes / counter bytes calibrates each counter.
+    """
+    probe_kib = probe_mb * 1024.0
+    out = [f"# HBM traffic per dispatch from rocprofv3 byte counters", f"# command: {command}",
+           f"source_fingerprint: {source_fingerprint()}"]
+    per = {}
+    factors = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = [r for r in _counter_rows(d) if r["Counter_Name"] == counter]
+        copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        probe = max(copies) if copies else 0.0
+        if probe <= 0.0:
+            raise SystemExit(f"{counter}: no copy-probe dispatch found in {d}")
+        factors[counter] = probe_kib / probe
+        out.append(f"{counter.lower()}_factor: {factors[counter]:.4f}  "
+                   f"(copy probe {probe_mb} MiB; counter read {probe:.0f} KiB)")
+        for r in rows:
+            k = short_kernel_name(r["Kernel_Name"])
+            per.setdefault(k, {}).setdefault(counter, []).append(float(r["Counter_Value"]))
+    out.append("# kernel  dispatches  FETCH_KiB/dispatch  WRITE_KiB/dispatch  "
+               "scaled bytes/dispatch")
+    rows_out = []
+    for k, c in per.items():
+        if "FETCH_SIZE" not in c or "WRITE_SIZE" not in c:
+            continue
+        fk = statistics.mean(c["FETCH_SIZE"])
+        wk = statistics.mean(c["WRITE_SIZE"])
+        b = (fk * factors["FETCH_SIZE"] + wk * factors["WRITE_SIZE"]) * 1024.0
+        rows_out.append((b, k, len(c["FETCH_SIZE"]), fk, wk))
+    for b, k, n, fk, wk in sorted(rows_out, reverse=True):
+        out.append(f"kernel {k}  {n}  {fk:.1f}  {wk:.1f}  {b:.0f}")
+    # one line per traced launch name, the form bench.py reads back
+    for b, k, n, fk, wk in sorted(rows_out, reverse=True):
+        base = k.split("<")[0]
+        if base in TRACE_NAME:
+            out.append(f"traffic {TRACE_NAME[base]} {base} {fk:.1f} {wk:.1f} {b:.0f}")
+    return "\n".join(out) + "\n"
+
+
+def summarize_trace(trace_dir, command, bench_json=None):
+    """Text summary of a rocprofv3 --kernel-trace --stats run (top kernels by time)."""
+    files = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_stats.csv under {trace_dir}")
+    with open(files[0]) as f:
+        rows = list(csv.DictReader(f))
+    out = ["# rocprofv3 kernel statistics", f"# command: {command}",
+           f"source_fingerprint: {source_fingerprint()}",
+           "# calls  total_us  avg_us  min_us  max_us  share%  kernel"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        out.append(f"{int(r['Calls']):6d}  {float(r['TotalDurationNs']) / 1e3:10.1f}  "
+                   f"{float(r['AverageNs']) / 1e3:8.2f}  {float(r['MinNs']) / 1e3:8.2f}  "
+                   f"{float(r['MaxNs']) / 1e3:8.2f}  {float(r['Percentage']):5.2f}  "
+                   f"{short_kernel_name(r['Name'])}")
+    if bench_json:
+        with open(bench_json) as f:
+            line = [l for l in f if l.startswith("{")][-1]
+        b = json.loads(line)
+        out.append("# the same run's bench line: HIP-event time per launch (trace hook)")
+        for k, v in b["kernels"].items():
+            out.append(f"bench {k} {v['us']} us")
+        r = b["roofline"]
+        out.append(f"bench roofline {r['kernel']} {r['bound']} achieved {r['achieved']} "
+                   f"{r['unit']} frac {r['frac']}")
+    return "\n".join(out) + "\n"
 
 
 def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256):
@@ -172,7 +314,21 @@ def main(argv=None):
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB "
                          "(calibrates profiler byte counters)")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="print a summary of a rocprofv3 --kernel-trace --stats output and exit")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print per-dispatch HBM bytes from two rocprofv3 --pmc outputs and exit")
+    ap.add_argument("--bench-json", help="with --summarize-trace: the profiled run's bench line")
+    ap.add_argument("--command", default="", help="the profiled command, quoted in a summary")
     a = ap.parse_args(argv)
+    if a.summarize_trace:
+        sys.stdout.write(summarize_trace(a.summarize_trace, a.command, a.bench_json))
+        return 0
+    if a.summarize_traffic:
+        if a.copy_probe_mb <= 0:
+            ap.error("--summarize-traffic needs --copy-probe-mb (the probe size of the run)")
+        sys.stdout.write(summarize_traffic(*a.summarize_traffic, a.copy_probe_mb, a.command))
+        return 0
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if a.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the hot path is built and timed on a single MI355X; "
@@ -286,9 +442,13 @@ def main(argv=None):
         achieved, peak, unit, bound = flops / (us * 1e-6) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s", "mfma"
     else:
         achieved, peak, unit, bound = nbytes / (us * 1e-6) / 1e9, HBM_PEAK_GBS, "GB/s", "hbm"
+    traffic, traffic_src = read_traffic(a.workload)
+    traffic = traffic.get(dom) if traffic else None
     roof = {"bound": bound, "kernel": dom, "achieved": round(achieved, 3), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
-            "per_launch": {"bytes": nbytes, "flops": flops, "us": us}}
+            "unit": unit, "frac": round(achieved / peak, 4),
+            "traffic": round(traffic) if traffic is not None else None,
+            "per_launch": {"bytes": nbytes, "flops": flops, "us": us,
+                           "traffic_source": traffic_src}}
 
     out = {"metric": METRIC, "value": E / (ms * 1e-3), "unit": "edges/s", "n_gpus": 1,
            "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 4),
