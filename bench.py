@@ -202,7 +202,11 @@ def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256):
     else:
         t["events_count"] = (1, 24 * n_in, 0, False)
         t["events_fill"] = (1, 28 * n_in + 4 * E, 0, False)
-    t["transpose_sort"] = (1, 4 * (n_in + 1) + 16 * E, 0, False)
+    t["transpose_count"] = (1, 4 * (n_out + 1) + 4 * E + 4 * n_in, 0, False)
+    t["transpose_scatter"] = (1, 4 * (n_out + 1) + 4 * E + 4 * n_in + 12 * E, 0, False)
+    # rank sort of the scattered (column, edge, row) triples: column bounds,
+    # three input arrays, two outputs
+    t["transpose_sort"] = (1, 8 * (n_in + 1) + 20 * E, 0, False)
     basis_launches = 0
     csr_b = 4 * (n_out + 1) + 4 * E + 4 * E * M
     csc_b = 4 * (n_in + 1) + 8 * E + 4 * E * M

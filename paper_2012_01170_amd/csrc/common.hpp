@@ -87,9 +87,11 @@ sbc_status fill_i32(int32_t *p, int32_t value, int64_t n, hipStream_t stream);
 
 // Sort the entries of each segment [ptr[s], ptr[s+1]) of (key, payload) pairs by
 // key ascending (keys distinct within a segment), writing to the *_out arrays.
-sbc_status segmented_sort_pairs(const int32_t *ptr, int32_t n_segments, const int32_t *key_in,
-                                const int32_t *val_in, int32_t *key_out, int32_t *val_out,
-                                hipStream_t stream);
+// seg_of[p] is the segment of entry p; only entries p < min(ptr[n_segments],
+// n_bound) are sorted.  val_in / val_out may be null (keys only).
+sbc_status segmented_sort_pairs(const int32_t *ptr, int32_t n_segments, const int32_t *seg_of,
+                                int64_t n_bound, const int32_t *key_in, const int32_t *val_in,
+                                int32_t *key_out, int32_t *val_out, hipStream_t stream);
 
 inline int grid_for(int64_t n, int block) {
     int64_t g = (n + block - 1) / block;

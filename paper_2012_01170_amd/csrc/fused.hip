@@ -5,25 +5,27 @@
 // indices), or read from a materialised [E, M] array.
 //
 // Forward, one block per tile of TR output rows:
-//   gather   G[r, m*C_in + c] = sum_e v[e, m] F[j(e), c] into LDS.  A wave
-//            handles its rows in batches: the batch's edges are staged 64 at a
-//            time (index and basis values, one edge per lane) in LDS, then
-//            every row of the batch is owned by LPR lanes that accumulate
-//            M x VEC values while walking the row's edges, loading VEC
-//            contiguous channels of F[j] per edge (16-byte loads);
+//   gather   G[r, m*C_in + c] = sum_e v[e, m] F[j(e), c] into LDS.  The
+//            wave's edges are staged 64 at a time (index and basis values,
+//            one edge per lane) in LDS; every row is owned by LPR lanes that
+//            accumulate M x VEC values while walking the row's edges, loading
+//            VEC contiguous channels of F[j] per edge (16-byte loads);
 //   contract Y_tile = G_tile W on the matrix cores (float32: 16x16x4 f32
 //            MFMA with W read from L2; bf16: G rounded to bf16 in LDS and
 //            16x16x32 bf16 MFMA against a [C_out, M*C_in] copy of W).
 // Forward for narrow inputs (C_in <= 32), persistent blocks of 8 waves: each
 //            wave owns 16-row tiles and keeps G in registers as the MFMA A
-//            operand; W stays in LDS for the life of the block.
-// Backward (D-route), persistent blocks over tiles of TR input rows:
-//   gather   D[j, m*C_out + p] = sum_{e=(i,j)} v[e, m] dY[i, p] through the
-//            transposed pattern, into LDS (F's tile rows are staged too);
-//   dF       dF_tile = D_tile Wt (Wt[(m, p), c] = W[m, c, p]) on MFMA;
-//   dW       every block accumulates F_tile^T D_tile over its tiles in
-//            registers; the per-block partials are summed afterwards in
-//            block order, so dW does not depend on scheduling.
+//            operand; W stays in LDS for the life of the block.  A row's four
+//            lanes take four edges per step, with the next step's neighbour
+//            indices already loaded.
+// Backward (D-route), persistent blocks over tiles of 32 input rows, with
+// the waves split in two roles and the tiles double-buffered in LDS:
+//   gather waves   D[j, m*C_out + p] = sum_{e=(i,j)} v[e, m] dY[i, p] through
+//                  the transposed pattern (and F's tile rows) for tile s+1;
+//   matrix waves   dF_tile = D_tile Wt (Wt[(m, p), c] = W[m, c, p]) and
+//                  dW += F_tile^T D_tile for tile s; the dW partials stay in
+//                  registers and are summed afterwards in block order, so dW
+//                  does not depend on scheduling.
 // Sums over edges run in pattern order inside a lane; no floating-point
 // atomics are used anywhere.
 #include <type_traits>
@@ -53,19 +55,49 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
     return (uint16_t)(u >> 16);
 }
 
+// Eight bf16 values p[0], p[s], ..., p[7 s] of a row-major LDS tile, as one
+// MFMA operand of eight consecutive k (the k index runs down a column).
+__device__ __forceinline__ bf16x8 lds_column8(const uint16_t *p, int s) {
+    typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+    u16x8 r;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) r[q] = p[q * s];
+    return __builtin_bit_cast(bf16x8, r);
+}
+
+// ---------------------------------------------------------------- geometry
+// Geometry as the fused kernels read it: the caller's point coordinates, and
+// for event streams a packed copy (px, py, t, 0) per event, so that one
+// 16-byte load brings all three coordinates of an edge's far end (three
+// separate arrays would cost three cache lines per edge).
+struct KGeo {
+    double inv_r;
+    float inv_tau;
+    const float *x_in, *x_out;
+    const int4 *ev;
+};
+
+__global__ void pack_events_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
+                                   const int32_t *__restrict__ t, int32_t n,
+                                   int4 *__restrict__ out) {
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+        out[i] = make_int4(px[i], py[i], t[i], 0);
+}
+
 // ---------------------------------------------------------------- basis per edge
 // kBasis: 0 = read v[ev, :], SBC_BASIS_MONO4 + 1, SBC_BASIS_MONO8 + 1, SBC_BASIS_EVENT8 + 1
 // (i = output index, j = input index of the edge, ev = its CSR position).
 template <int M, int kBasis>
-__device__ __forceinline__ void edge_basis(const sbc_geometry &g, const float *__restrict__ v,
+__device__ __forceinline__ void edge_basis(const KGeo &g, const float *__restrict__ v,
                                            int32_t i, int32_t j, int64_t ev, double inv_r,
                                            float inv_tau, float *out) {
     if constexpr (kBasis == 0) {
 #pragma unroll
         for (int m = 0; m < M; ++m) out[m] = v[ev * M + m];
     } else if constexpr (kBasis == SBC_BASIS_EVENT8 + 1) {
-        const int k = event_index(g.px[i] - g.px[j], g.py[i] - g.py[j]);
-        const float d = event_decay(g.t[i], g.t[j], inv_tau);
+        const int4 a = g.ev[i], b = g.ev[j];
+        const int k = event_index(a.x - b.x, a.y - b.y);
+        const float d = event_decay(a.z, b.z, inv_tau);
 #pragma unroll
         for (int m = 0; m < M; ++m) out[m] = (m == k) ? d : 0.f;
     } else {
@@ -109,23 +141,45 @@ __device__ __forceinline__ void load_row_vec(const void *__restrict__ Xv, int32_
     }
 }
 
+// Row bound ptr[row_begin + lane] (clamped to [0, n_rows]) for lanes 0..RPW:
+// what gather_rows needs to start, loadable one call ahead.
+template <int RPW>
+__device__ __forceinline__ int32_t load_bound(const int32_t *__restrict__ ptr, int32_t n_rows,
+                                              int32_t row_begin) {
+    const int lane = threadIdx.x & 63;
+    if (lane > RPW) return 0;
+    int32_t r = row_begin + lane;
+    r = r < n_rows ? r : n_rows;
+    r = r > 0 ? r : 0;
+    return ptr[r];
+}
+
 // Gather of one wave's RPW consecutive rows into an LDS tile.
 //   kT: the pattern is transposed (rows are inputs j, idx gives outputs i).
 //   X [*, C] features gathered along the pattern; out tile row stride S
 //   (elements), row r_local at out + r_local * S, column m*C + c.
+//   my_bound: load_bound<RPW>(ptr, n_rows, row_begin) of this lane.
+//   next_row_begin >= 0: the bound of the next call's rows is loaded while
+//   this one runs and returned.
 // The wave's edges are staged 64 at a time; the rows are owned by groups of
-// LPR lanes (RPB rows at once, NB rounds, all accumulators live across the
-// staging chunks), and each group loads the features of 4 edges at once.
-template <int M, int C, int kBasis, bool kXbf, bool kOutBf, bool kT, int RPW>
-__device__ __forceinline__ void gather_rows(int32_t row_begin, int32_t n_rows,
-                                            const int32_t *__restrict__ ptr,
-                                            const int32_t *__restrict__ idx,
-                                            const int32_t *__restrict__ perm,
-                                            const float *__restrict__ v, const sbc_geometry &g,
-                                            const void *__restrict__ Xv, void *out_tile, int S,
-                                            int local_row0, EdgeStage<M> &st, double inv_r,
-                                            float inv_tau, uint16_t *out_t = nullptr,
-                                            int ST = 0) {
+// LPR lanes (each group owns NB rows, all accumulators live across the
+// staging chunks).  kPipelined: the group's NB rows advance together with
+// NB * U feature loads in flight, and the first feature loads of a chunk are
+// issued together with the coordinate loads of the chunk's basis values, so
+// they share one memory round trip (for persistent waves that gather while
+// other waves multiply).  Otherwise the rows are taken one after another,
+// four edges at a time, after the basis values (for blocks that gather and
+// then multiply, where the co-resident block hides the latency).
+template <int M, int C, int kBasis, bool kXbf, bool kOutBf, bool kT, int RPW, bool kPipelined>
+__device__ __forceinline__ int32_t gather_rows(int32_t row_begin, int32_t n_rows,
+                                               const int32_t *__restrict__ ptr,
+                                               const int32_t *__restrict__ idx,
+                                               const int32_t *__restrict__ perm,
+                                               const float *__restrict__ v, const KGeo &g,
+                                               const void *__restrict__ Xv, void *out_tile, int S,
+                                               int local_row0, EdgeStage<M> &st, double inv_r,
+                                               float inv_tau, int32_t my_bound,
+                                               int32_t next_row_begin) {
     constexpr int VEC = kXbf ? 8 : 4;
     static_assert(C % VEC == 0, "channels must be a multiple of the vector width");
     constexpr int LPR = C / VEC;                   // lanes per row
@@ -133,18 +187,18 @@ __device__ __forceinline__ void gather_rows(int32_t row_begin, int32_t n_rows,
     static_assert(RPW <= 16, "row bounds stage holds 17 entries");
     constexpr int RPB_ = 64 / LPR;
     constexpr int RPB = RPB_ < RPW ? RPB_ : RPW;   // rows in flight at once
-    constexpr int NB = (RPW + RPB - 1) / RPB;      // rounds over the wave's rows
-    constexpr int U = 4;                           // edges loaded together
+    constexpr int NB = (RPW + RPB - 1) / RPB;      // rows per lane group
+    // edges per row loaded together: NB * U feature loads in flight per lane
+    // (pipelined), or 4 per row with the rows taken one after another
+    constexpr int UP = 32 / (NB * VEC) > 1 ? 32 / (NB * VEC) : 1;
+    constexpr int U = kPipelined ? UP : 4;
     const int lane = threadIdx.x & 63;
     const int slot = lane / LPR;
     const int cg = lane % LPR;
 
-    if (lane <= RPW) {
-        int32_t r = row_begin + lane;
-        r = r < n_rows ? r : n_rows;
-        r = r > 0 ? r : 0;
-        st.bounds[lane] = ptr[r];
-    }
+    if (lane <= RPW) st.bounds[lane] = my_bound;
+    const int32_t next_bound =
+        next_row_begin >= 0 ? load_bound<RPW>(ptr, n_rows, next_row_begin) : 0;
     wave_lds_sync();
     const int32_t wb = st.bounds[0], we = st.bounds[RPW];
     int32_t rs[NB], re[NB];
@@ -166,51 +220,114 @@ __device__ __forceinline__ void gather_rows(int32_t row_begin, int32_t n_rows,
 #pragma unroll 1
     for (int32_t c0 = wb; c0 < we; c0 += 64) {
         const int32_t e = c0 + lane;
+        int32_t row = 0, other = 0;
+        int64_t ev = 0;
         if (e < we) {
             int s = 0;
 #pragma unroll
             for (int q = 1; q < RPW; ++q)
                 if (st.bounds[q] <= e) s = q;
-            const int32_t row = row_begin + s;
-            const int32_t other = idx[e];
-            const int64_t ev = (kBasis == 0) ? (perm ? (int64_t)perm[e] : (int64_t)e) : 0;
+            row = row_begin + s;
+            other = idx[e];
+            ev = (kBasis == 0) ? (perm ? (int64_t)perm[e] : (int64_t)e) : 0;
+            st.nb[lane] = other;
+            if (lane == 0) st.nb[64] = other;  // padding edge: a valid row, weight 0
+        }
+        if constexpr (!kPipelined) {
+            // basis values first, then each row of the lane group in turn
+            if (e < we) {
+                float bv[M];
+                if (kT)
+                    edge_basis<M, kBasis>(g, v, other, row, ev, inv_r, inv_tau, bv);
+                else
+                    edge_basis<M, kBasis>(g, v, row, other, ev, inv_r, inv_tau, bv);
+#pragma unroll
+                for (int m = 0; m < M; ++m) st.v[lane][m] = bv[m];
+                if (lane == 0) {
+#pragma unroll
+                    for (int m = 0; m < M; ++m) st.v[64][m] = 0.f;
+                }
+            }
+            wave_lds_sync();
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const int32_t lo = rs[b] > c0 ? rs[b] : c0;
+                const int32_t hi = re[b] < c0 + 64 ? re[b] : c0 + 64;
+#pragma unroll 1
+                for (int32_t e2 = lo; e2 < hi; e2 += U) {
+                    float f[U][VEC];
+                    int q[U];
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        q[u] = e2 + u < hi ? e2 + u - c0 : 64;
+                        load_row_vec<C, VEC, kXbf>(Xv, st.nb[q[u]], cg, f[u]);
+                    }
+#pragma unroll
+                    for (int u = 0; u < U; ++u)
+#pragma unroll
+                        for (int m = 0; m < M; ++m) {
+                            const float vm = st.v[q[u]][m];
+#pragma unroll
+                            for (int k = 0; k < VEC; ++k) acc[b][m][k] += vm * f[u][k];
+                        }
+                }
+            }
+            wave_lds_sync();
+            continue;
+        }
+        wave_lds_sync();
+        // the lane group's NB rows advance together, U edges each per step
+        int32_t pos[NB], hi[NB];
+        int32_t steps = 0;
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            pos[b] = rs[b] > c0 ? rs[b] : c0;
+            hi[b] = re[b] < c0 + 64 ? re[b] : c0 + 64;
+            const int32_t n = hi[b] > pos[b] ? (hi[b] - pos[b] + U - 1) / U : 0;
+            steps = n > steps ? n : steps;
+        }
+        float f[NB][U][VEC];
+        int q[NB][U];
+        auto issue = [&]() {
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    q[b][u] = pos[b] + u < hi[b] ? pos[b] + u - c0 : 64;
+                    load_row_vec<C, VEC, kXbf>(Xv, st.nb[q[b][u]], cg, f[b][u]);
+                }
+        };
+        if (steps > 0) issue();
+        // basis values of this lane's edge; their coordinate loads overlap the
+        // feature loads just issued
+        if (e < we) {
             float bv[M];
             if (kT)
                 edge_basis<M, kBasis>(g, v, other, row, ev, inv_r, inv_tau, bv);
             else
                 edge_basis<M, kBasis>(g, v, row, other, ev, inv_r, inv_tau, bv);
-            st.nb[lane] = other;
 #pragma unroll
             for (int m = 0; m < M; ++m) st.v[lane][m] = bv[m];
-            if (lane == 0) {  // padding edge: first neighbour of the chunk, weight 0
-                st.nb[64] = other;
+            if (lane == 0) {
 #pragma unroll
                 for (int m = 0; m < M; ++m) st.v[64][m] = 0.f;
             }
         }
         wave_lds_sync();
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            const int32_t lo = rs[b] > c0 ? rs[b] : c0;
-            const int32_t hi = re[b] < c0 + 64 ? re[b] : c0 + 64;
 #pragma unroll 1
-            for (int32_t e2 = lo; e2 < hi; e2 += U) {
-                float f[U][VEC];
-                int q[U];
+        for (int32_t it = 0; it < steps; ++it) {
+            if (it > 0) issue();
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    q[u] = e2 + u < hi ? e2 + u - c0 : 64;
-                    load_row_vec<C, VEC, kXbf>(Xv, st.nb[q[u]], cg, f[u]);
-                }
+            for (int b = 0; b < NB; ++b) {
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
+                for (int u = 0; u < U; ++u)
 #pragma unroll
                     for (int m = 0; m < M; ++m) {
-                        const float vm = st.v[q[u]][m];
+                        const float vm = st.v[q[b][u]][m];
 #pragma unroll
-                        for (int k = 0; k < VEC; ++k) acc[b][m][k] += vm * f[u][k];
+                        for (int k = 0; k < VEC; ++k) acc[b][m][k] += vm * f[b][u][k];
                     }
-                }
+                pos[b] += U;
             }
         }
         wave_lds_sync();
@@ -222,15 +339,14 @@ __device__ __forceinline__ void gather_rows(int32_t row_begin, int32_t n_rows,
 #pragma unroll
             for (int m = 0; m < M; ++m) {
                 if constexpr (kOutBf) {
-                    uint16_t *o = static_cast<uint16_t *>(out_tile) +
-                                  (int64_t)(local_row0 + lr) * S + m * C + cg * VEC;
+                    static_assert(VEC == 8, "bf16 rows are written 16 bytes at a time");
+                    typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+                    u16x8 packed;
 #pragma unroll
-                    for (int k = 0; k < VEC; ++k) o[k] = f2bf(acc[b][m][k]);
-                    if (out_t) {  // transposed copy: column (m*C + c), row lr
-#pragma unroll
-                        for (int k = 0; k < VEC; ++k)
-                            out_t[(m * C + cg * VEC + k) * ST + local_row0 + lr] = o[k];
-                    }
+                    for (int k = 0; k < VEC; ++k) packed[k] = f2bf(acc[b][m][k]);
+                    *reinterpret_cast<u16x8 *>(static_cast<uint16_t *>(out_tile) +
+                                               (int64_t)(local_row0 + lr) * S + m * C +
+                                               cg * VEC) = packed;
                 } else {
                     float *o = static_cast<float *>(out_tile) + (int64_t)(local_row0 + lr) * S +
                                m * C + cg * VEC;
@@ -240,6 +356,7 @@ __device__ __forceinline__ void gather_rows(int32_t row_begin, int32_t n_rows,
             }
         }
     }
+    return next_bound;
 }
 
 // acc[u][t] += A_tile[16 rb_u .., :] x B[:, 16 cb_t ..] for the 16x16 blocks of
@@ -370,7 +487,7 @@ template <int M, int CI, int CO, int kBasis, bool kBf>
 __global__ void __launch_bounds__(kFwdWaves * 64, 2)
     fwd_fused_kernel(int32_t n_out, const int32_t *__restrict__ row_ptr,
                      const int32_t *__restrict__ col_idx, const float *__restrict__ v,
-                     sbc_geometry g, const void *__restrict__ F, const void *__restrict__ Wop,
+                     KGeo g, const void *__restrict__ F, const void *__restrict__ Wop,
                      float *__restrict__ Y) {
     constexpr int NW = kFwdWaves;
     constexpr int K = M * CI;
@@ -391,12 +508,12 @@ __global__ void __launch_bounds__(kFwdWaves * 64, 2)
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
     const int32_t row0 = xcd_tile(blockIdx.x, gridDim.x) * TR;
-    const double inv_r = 1.0 / (double)g.radius;
-    const float inv_tau = 1.0f / g.tau;
+    const double inv_r = g.inv_r;
+    const float inv_tau = g.inv_tau;
 
-    gather_rows<M, CI, kBasis, kBf, kBf, false, RPW>(row0 + w * RPW, n_out, row_ptr, col_idx,
-                                                     nullptr, v, g, F, Gs, S, w * RPW, stage[w],
-                                                     inv_r, inv_tau);
+    gather_rows<M, CI, kBasis, kBf, kBf, false, RPW, false>(
+        row0 + w * RPW, n_out, row_ptr, col_idx, nullptr, v, g, F, Gs, S, w * RPW, stage[w],
+        inv_r, inv_tau, load_bound<RPW>(row_ptr, n_out, row0 + w * RPW), -1);
     __syncthreads();
 
     const int wc = w % NCBW, wr = w / NCBW;
@@ -448,10 +565,10 @@ constexpr bool reg_forward_fits() {
 }
 
 template <int M, int CI, int CO, int kBasis, bool kBf>
-__global__ void __launch_bounds__(kRegWaves * 64, 1)
+__global__ void __launch_bounds__(kRegWaves * 64) __attribute__((amdgpu_waves_per_eu(4)))
     fwd_reg_kernel(int32_t n_out, int32_t n_tiles, const int32_t *__restrict__ row_ptr,
                    const int32_t *__restrict__ col_idx, const float *__restrict__ v,
-                   sbc_geometry g, const void *__restrict__ Fv, const void *__restrict__ Wv,
+                   KGeo g, const void *__restrict__ Fv, const void *__restrict__ Wv,
                    float *__restrict__ Y) {
     constexpr int K = M * CI;
     constexpr int CG = CI / 4;          // channels per lane group
@@ -485,8 +602,8 @@ __global__ void __launch_bounds__(kRegWaves * 64, 1)
     const int w = threadIdx.x >> 6;
     const int rl = lane & 15;        // row within the tile
     const int gq = lane >> 4;        // channel group
-    const double inv_r = 1.0 / (double)g.radius;
-    const float inv_tau = 1.0f / g.tau;
+    const double inv_r = g.inv_r;
+    const float inv_tau = g.inv_tau;
 
     // tiles of this wave: the block's XCD owns a contiguous range, its waves
     // interleave (with fewer than 8 blocks, one range per block)
@@ -518,54 +635,62 @@ __global__ void __launch_bounds__(kRegWaves * 64, 1)
 #pragma unroll
             for (int t = 0; t < CG; ++t) acc[m][t] = 0.f;
 
-        // edges in flight per lane: two while the accumulators leave room
-        constexpr int U = M * CG >= 128 ? 1 : 2;
+        // Four edges of the row per step, one per lane of the row's group:
+        // lane gq loads the neighbour index of edge q + gq one step ahead and
+        // evaluates that edge's basis; the group shares indices and basis
+        // values through cross-lane reads, and every lane loads its channels
+        // of all four neighbours' features.
+        int32_t jn = (e0 + gq < e1) ? col_idx[e0 + gq] : 0;
 #pragma unroll 1
-        for (int32_t q = 0; q < len; q += U) {
-            float f[U][CG];
-            float bv[U][M];
+        for (int32_t q = 0; q < len; q += 4) {
+            const int32_t eo = e0 + q + gq;          // this lane's edge
+            const int32_t jo = jn;
+            jn = (eo + 4 < e1) ? col_idx[eo + 4] : 0;
+            float f[4][CG];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int32_t e = e0 + q + u;
-                if (e < e1) {
-                    const int32_t j = col_idx[e];
-                    edge_basis<M, kBasis>(g, v, row, j, e, inv_r, inv_tau, bv[u]);
-                    if constexpr (kBf) {
-                        const uint16_t *src = static_cast<const uint16_t *>(Fv) + (int64_t)j * CI + gq * CG;
+            for (int u = 0; u < 4; ++u) {
+                const int32_t j = __shfl(jo, rl + 16 * u, 64);
+                if constexpr (kBf) {
+                    const uint16_t *src = static_cast<const uint16_t *>(Fv) + (int64_t)j * CI + gq * CG;
 #pragma unroll
-                        for (int c = 0; c < CG; c += 8) {
-                            const uint4 raw = *reinterpret_cast<const uint4 *>(src + c);
-                            const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
+                    for (int c = 0; c < CG; c += 8) {
+                        const uint4 raw = *reinterpret_cast<const uint4 *>(src + c);
+                        const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
-                            for (int k = 0; k < 4; ++k) {
-                                f[u][c + 2 * k] = __uint_as_float(w4[k] << 16);
-                                f[u][c + 2 * k + 1] = __uint_as_float(w4[k] & 0xFFFF0000u);
-                            }
-                        }
-                    } else {
-                        const float *src = static_cast<const float *>(Fv) + (int64_t)j * CI + gq * CG;
-#pragma unroll
-                        for (int c = 0; c < CG; c += 4) {
-                            const float4 raw = *reinterpret_cast<const float4 *>(src + c);
-                            f[u][c] = raw.x;
-                            f[u][c + 1] = raw.y;
-                            f[u][c + 2] = raw.z;
-                            f[u][c + 3] = raw.w;
+                        for (int k = 0; k < 4; ++k) {
+                            f[u][c + 2 * k] = __uint_as_float(w4[k] << 16);
+                            f[u][c + 2 * k + 1] = __uint_as_float(w4[k] & 0xFFFF0000u);
                         }
                     }
                 } else {
+                    const float *src = static_cast<const float *>(Fv) + (int64_t)j * CI + gq * CG;
 #pragma unroll
-                    for (int m = 0; m < M; ++m) bv[u][m] = 0.f;
-#pragma unroll
-                    for (int c = 0; c < CG; ++c) f[u][c] = 0.f;
+                    for (int c = 0; c < CG; c += 4) {
+                        const float4 raw = *reinterpret_cast<const float4 *>(src + c);
+                        f[u][c] = raw.x;
+                        f[u][c + 1] = raw.y;
+                        f[u][c + 2] = raw.z;
+                        f[u][c + 3] = raw.w;
+                    }
                 }
             }
+            // this lane's edge basis (zero past the row's end: those lanes
+            // loaded row 0's features, which then carry no weight)
+            float bo[M];
+            if (eo < e1) {
+                edge_basis<M, kBasis>(g, v, row, jo, eo, inv_r, inv_tau, bo);
+            } else {
 #pragma unroll
-            for (int u = 0; u < U; ++u)
+                for (int m = 0; m < M; ++m) bo[m] = 0.f;
+            }
 #pragma unroll
-                for (int m = 0; m < M; ++m)
+            for (int u = 0; u < 4; ++u)
 #pragma unroll
-                    for (int t = 0; t < CG; ++t) acc[m][t] += bv[u][m] * f[u][t];
+                for (int m = 0; m < M; ++m) {
+                    const float bm = __shfl(bo[m], rl + 16 * u, 64);
+#pragma unroll
+                    for (int t = 0; t < CG; ++t) acc[m][t] += bm * f[u][t];
+                }
         }
 
         // ---- Y rows of the tile = G W on the matrix cores
@@ -619,154 +744,237 @@ __global__ void __launch_bounds__(kRegWaves * 64, 1)
     }
 }
 
-// ================================================================ backward (D-route)
-template <int K2, bool kBf>
-constexpr int bwd_tile_rows() {
-    return kBf ? 32 : ((K2 * 4 * 64 <= 65536) ? 64 : 32);
-}
+// ================================================================ backward, wave-specialised
+// Persistent blocks of eight waves over tiles of 32 input rows.  Waves 0-3
+// gather tile s+1 (D rows through the transposed pattern, and F rows) into
+// one half of a double-buffered LDS tile while waves 4-7 run the matrix work
+// of tile s on the other half (dF = D Wt, dW += F^T D); one block barrier per
+// step hands the halves over, so the gathers' memory latency overlaps the
+// matrix cores' work.
+constexpr int kWsMma = 4;
+constexpr int kWsTR = 32;
 
-// Waves per backward block: eight when the dF tile has at least eight 16x16 blocks.
+// Gather waves of the wave-specialised kernels: eight where the kernel's
+// registers allow twelve waves per CU (narrow float32 rows), else four.
 template <int M, int CI, int CO, bool kBf>
-constexpr int bwd_waves() {
-    return (bwd_tile_rows<M * CO, kBf>() / 16) * (CI / 16) >= 8 ? 8 : 4;
+constexpr int ws_gather_waves() {
+    return (!kBf && CI <= 32 && CO <= 32) ? 8 : 4;
 }
 
-template <int M, int CI, int CO, int kBasis, bool kBf>
-__global__ void __launch_bounds__((bwd_waves<M, CI, CO, kBf>() * 64), 1)
-    bwd_fused_kernel(int32_t n_in, int32_t n_tiles, const int32_t *__restrict__ col_ptr,
-                     const int32_t *__restrict__ row_idx, const int32_t *__restrict__ perm,
-                     const float *__restrict__ v, sbc_geometry g, const void *__restrict__ Fv,
-                     const void *__restrict__ dY, const void *__restrict__ Wop,
-                     float *__restrict__ dF, float *__restrict__ dW_part) {
+template <int M, int CI, int CO, int kBasis, bool kBf,
+          int kWsGather = ws_gather_waves<M, CI, CO, kBf>()>
+__global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
+    bwd_ws_kernel(int32_t n_in, int32_t n_tiles, const int32_t *__restrict__ col_ptr,
+                  const int32_t *__restrict__ row_idx, const int32_t *__restrict__ perm,
+                  const float *__restrict__ v, KGeo g, const void *__restrict__ Fv,
+                  const void *__restrict__ dY, const void *__restrict__ Wop,
+                  float *__restrict__ dF, float *__restrict__ dW_part) {
     // dF == nullptr: no input gradient; dW_part == nullptr: no weight gradient
-    constexpr int NW = bwd_waves<M, CI, CO, kBf>();
-    constexpr int NT = NW * 64;
+    constexpr int TR = kWsTR;
     constexpr int K2 = M * CO;
-    constexpr int TR = bwd_tile_rows<K2, kBf>();
-    constexpr int RPW = TR / NW;
     constexpr int SD = K2 + (kBf ? 8 : 4);
-    constexpr int SF = CI + 4;        // float32 F tile row
-    constexpr int ST = TR + 8;        // bf16 transposed tiles (D^T, F^T) row
+    constexpr int SF = CI + (kBf ? 8 : 4);
+    constexpr int RPW = TR / kWsGather;
     static_assert(CI % 16 == 0 && CO % 16 == 0, "shape");
-    // dF tile [TR, CI]: 16x16 blocks over waves
+    // dF tile [TR, CI]: 16x16 blocks over the matrix waves
     constexpr int NRB = TR / 16, NCB = CI / 16;
-    constexpr int NCBW = NCB < NW ? NCB : NW;
-    constexpr int NRG = NW / NCBW;
+    constexpr int NCBW = NCB < kWsMma ? NCB : kWsMma;
+    constexpr int NRG_ = kWsMma / NCBW;
+    constexpr int NRG = NRG_ < NRB ? NRG_ : NRB;  // waves past NCBW * NRG have no dF block
     static_assert(NCB % NCBW == 0 && NRB % NRG == 0, "dF split");
     constexpr int WCB = NCB / NCBW, WRB = NRB / NRG;
-    // dW [CI, K2]: each wave owns K2/NW columns, all CI rows
-    constexpr int NWB = (K2 / 16) / NW;                // column blocks per wave
-    constexpr int NIB = CI / 16;                       // row blocks
-    static_assert((K2 / 16) % NW == 0, "dW split");
+    // dW [CI, K2]: each matrix wave owns K2/4 columns, all CI rows
+    constexpr int NWB = (K2 / 16) / kWsMma;
+    constexpr int NIB = CI / 16;
+    static_assert((K2 / 16) % kWsMma == 0, "dW split");
 
     using DT = typename std::conditional<kBf, uint16_t, float>::type;
-    __shared__ __attribute__((aligned(16))) DT Ds[TR * SD];
-    __shared__ __attribute__((aligned(16))) float Fs[kBf ? 1 : TR * SF];
-    __shared__ __attribute__((aligned(16))) uint16_t DsT[kBf ? K2 * ST : 1];
-    __shared__ __attribute__((aligned(16))) uint16_t FsT[kBf ? CI * ST : 1];
-    __shared__ EdgeStage<M> stage[NW];
+    __shared__ __attribute__((aligned(16))) DT Ds[2][TR * SD];
+    __shared__ __attribute__((aligned(16))) DT Fs[2][TR * SF];
+    __shared__ EdgeStage<M> stage[kWsGather];
 
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
-    const double inv_r = 1.0 / (double)g.radius;
-    const float inv_tau = 1.0f / g.tau;
-    const int wc = w % NCBW, wr = w / NCBW;
-
-    floatx4 accw[NIB][NWB];
-#pragma unroll
-    for (int a = 0; a < NIB; ++a)
-#pragma unroll
-        for (int b = 0; b < NWB; ++b) accw[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const bool gatherer = w < kWsGather;
+    const int mw = w - kWsGather;
+    const int wc = mw % NCBW, wr = mw / NCBW;
+    const double inv_r = g.inv_r;
+    const float inv_tau = g.inv_tau;
 
     // tiles of this block: its XCD's contiguous range, interleaved over the
     // XCD's blocks (with fewer than 8 blocks, one range per block)
     const int32_t G = gridDim.x, X = G < 8 ? G : 8;
     const int32_t x = blockIdx.x % X, l = blockIdx.x / X;
     const int32_t gx = G / X + (x < G % X ? 1 : 0);
-    const int32_t t_begin = (int32_t)((int64_t)x * n_tiles / X);
+    const int32_t t_first = (int32_t)((int64_t)x * n_tiles / X) + l;
     const int32_t t_end = (int32_t)((int64_t)(x + 1) * n_tiles / X);
+    const int32_t n_my = t_first < t_end ? (t_end - t_first + gx - 1) / gx : 0;
 
-#pragma unroll 1
-    for (int32_t tile = t_begin + l; tile < t_end; tile += gx) {
-        const int32_t row0 = tile * TR;
-        // F rows of the tile: float32 row-major, or bf16 transposed
-        for (int q = threadIdx.x; q < TR * CI; q += NT) {
-            const int r = q / CI, c = q % CI;
-            const int32_t row = row0 + r;
-            if constexpr (kBf) {
-                uint16_t f = 0;
-                if (row < n_in) f = static_cast<const uint16_t *>(Fv)[(int64_t)row * CI + c];
-                FsT[c * ST + r] = f;
-            } else {
-                float f = 0.f;
-                if (row < n_in) f = static_cast<const float *>(Fv)[(int64_t)row * CI + c];
-                Fs[r * SF + c] = f;
+    // row bounds of the gather's next tile, loaded one tile ahead
+    int32_t bound = n_my > 0 ? load_bound<RPW>(col_ptr, n_in, t_first * TR + w * RPW) : 0;
+    auto load_tile = [&](int32_t s, int buf) {
+        const int32_t row0 = (t_first + s * gx) * TR;
+        if (dW_part) {  // F rows of the tile, row-major (zero past the last row), 16 B per load
+            constexpr int CPR = CI * (int)sizeof(DT) / 16;
+            constexpr int NQ = (TR * CPR + kWsGather * 64 - 1) / (kWsGather * 64);
+            uint4 val[NQ];
+#pragma unroll
+            for (int k = 0; k < NQ; ++k) {
+                const int q = threadIdx.x + k * kWsGather * 64;
+                const int r = q / CPR, c16 = q % CPR;
+                val[k] = uint4{0u, 0u, 0u, 0u};
+                if (q < TR * CPR && row0 + r < n_in)
+                    val[k] = *reinterpret_cast<const uint4 *>(
+                        static_cast<const char *>(Fv) + (int64_t)(row0 + r) * CI * sizeof(DT) +
+                        16 * c16);
+            }
+#pragma unroll
+            for (int k = 0; k < NQ; ++k) {
+                const int q = threadIdx.x + k * kWsGather * 64;
+                const int r = q / CPR, c16 = q % CPR;
+                if (q < TR * CPR)
+                    *reinterpret_cast<uint4 *>(reinterpret_cast<char *>(&Fs[buf][r * SF]) +
+                                               16 * c16) = val[k];
             }
         }
-        gather_rows<M, CO, kBasis, kBf, kBf, true, RPW>(row0 + w * RPW, n_in, col_ptr, row_idx,
-                                                         perm, v, g, dY, Ds, SD, w * RPW,
-                                                         stage[w], inv_r, inv_tau,
-                                                         kBf ? DsT : nullptr, ST);
+        const int32_t next = s + 1 < n_my ? (t_first + (s + 1) * gx) * TR + w * RPW : -1;
+        bound = gather_rows<M, CO, kBasis, kBf, kBf, true, RPW, true>(
+            row0 + w * RPW, n_in, col_ptr, row_idx, perm, v, g, dY, Ds[buf], SD, w * RPW,
+            stage[w], inv_r, inv_tau, bound, next);
+    };
+
+    // The two roles run separate loops (so the matrix waves' dW accumulators
+    // are not live in the gather code); each role passes the block barrier
+    // exactly n_my + 1 times, in the same steps.
+    if (gatherer) {
+        if (n_my > 0) load_tile(0, 0);
         __syncthreads();
-
-        // ---- dF_tile = D_tile Wt  ([TR, K2] x [K2, CI])
-        if (dF) {
-        floatx4 acc[WRB][WCB];
-#pragma unroll
-        for (int u = 0; u < WRB; ++u)
-#pragma unroll
-            for (int t = 0; t < WCB; ++t) acc[u][t] = floatx4{0.f, 0.f, 0.f, 0.f};
-        if constexpr (!kBf)
-            mfma_lds_x_global_f32<K2, CI, SD, WRB, WCB, NCBW, NRG>(
-                Ds, static_cast<const float *>(Wop), wr, wc, acc);
-        else
-            mfma_lds_x_global_bf16<K2, SD, WRB, WCB, NCBW, NRG>(
-                Ds, static_cast<const uint16_t *>(Wop), wr, wc, acc);
-#pragma unroll
-        for (int u = 0; u < WRB; ++u)
-#pragma unroll
-            for (int t = 0; t < WCB; ++t)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int32_t row = row0 + 16 * (wr + NRG * u) + 4 * (lane >> 4) + r;
-                    if (row < n_in)
-                        dF[(int64_t)row * CI + 16 * (wc + NCBW * t) + (lane & 15)] = acc[u][t][r];
-                }
+#pragma unroll 1
+        for (int32_t s = 0; s < n_my; ++s) {
+            if (s + 1 < n_my) load_tile(s + 1, (s & 1) ^ 1);
+            __syncthreads();
         }
+        return;
+    }
 
-        // ---- dW += F_tile^T D_tile  ([CI, TR] x [TR, K2]) over the tile rows
-        if (dW_part) {
-            if constexpr (!kBf) {
-#pragma unroll 2
-                for (int k0 = 0; k0 < TR; k0 += 4) {
-                    const int kk = k0 + (lane >> 4);
-                    float a[NIB];
+    floatx4 accw[NIB][NWB];
 #pragma unroll
-                    for (int ib = 0; ib < NIB; ++ib) a[ib] = Fs[kk * SF + 16 * ib + (lane & 15)];
+    for (int a = 0; a < NIB; ++a)
 #pragma unroll
-                    for (int nb = 0; nb < NWB; ++nb) {
-                        const float bb = Ds[kk * SD + 16 * (w * NWB + nb) + (lane & 15)];
+        for (int b = 0; b < NWB; ++b) accw[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // the wave's slice of Wt for dF, held in registers for the whole kernel
+    // when it takes at most 64 of them (it is the same for every tile)
+    constexpr bool kWreg = kBf ? (K2 * WCB <= 512) : (K2 * WCB <= 256);
+    constexpr int KS = kBf ? K2 / 32 : K2 / 4;  // MFMA k-steps of the dF product
+    using BT = typename std::conditional<kBf, bf16x8, float>::type;
+    BT bw[kWreg ? KS : 1][WCB];
+    if constexpr (kWreg) {
+        const int lr = lane >> 4, lc = lane & 15;
 #pragma unroll
-                        for (int ib = 0; ib < NIB; ++ib)
-                            accw[ib][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ib], bb, accw[ib][nb], 0, 0, 0);
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int t = 0; t < WCB; ++t) {
+                if constexpr (kBf)
+                    bw[ks][t] = *reinterpret_cast<const bf16x8 *>(
+                        static_cast<const uint16_t *>(Wop) +
+                        (int64_t)(16 * (wc + NCBW * t) + lc) * K2 + 32 * ks + 8 * lr);
+                else
+                    bw[ks][t] = static_cast<const float *>(Wop)[(4 * ks + lr) * CI +
+                                                                16 * (wc + NCBW * t) + lc];
+            }
+    }
+    __syncthreads();
+#pragma unroll 1
+    for (int32_t s = 0; s < n_my; ++s) {
+        const int buf = s & 1;
+        {
+            const int32_t row0 = (t_first + s * gx) * TR;
+            const DT *D = Ds[buf];
+            // ---- dF_tile = D_tile Wt  ([TR, K2] x [K2, CI])
+            if (dF && mw < NCBW * NRG) {
+                floatx4 acc[WRB][WCB];
+#pragma unroll
+                for (int u = 0; u < WRB; ++u)
+#pragma unroll
+                    for (int t = 0; t < WCB; ++t) acc[u][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+                if constexpr (kWreg) {
+                    const int lr = lane >> 4, lc = lane & 15;
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+                        for (int u = 0; u < WRB; ++u) {
+                            const int arow = 16 * (wr + NRG * u) + lc;
+                            if constexpr (kBf) {
+                                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
+                                    &D[arow * SD + 32 * ks + 8 * lr]);
+#pragma unroll
+                                for (int t = 0; t < WCB; ++t)
+                                    acc[u][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                        a, bw[ks][t], acc[u][t], 0, 0, 0);
+                            } else {
+                                const float a = D[arow * SD + 4 * ks + lr];
+#pragma unroll
+                                for (int t = 0; t < WCB; ++t)
+                                    acc[u][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                        a, bw[ks][t], acc[u][t], 0, 0, 0);
+                            }
+                        }
                     }
+                } else if constexpr (!kBf) {
+                    mfma_lds_x_global_f32<K2, CI, SD, WRB, WCB, NCBW, NRG>(
+                        D, static_cast<const float *>(Wop), wr, wc, acc);
+                } else {
+                    mfma_lds_x_global_bf16<K2, SD, WRB, WCB, NCBW, NRG>(
+                        D, static_cast<const uint16_t *>(Wop), wr, wc, acc);
                 }
-            } else {
-                // bf16 MFMA: 8 consecutive tile rows per lane from the transposed tiles
 #pragma unroll
-                for (int k0 = 0; k0 < TR; k0 += 32) {
-                    const int kk = k0 + 8 * (lane >> 4);
-                    bf16x8 a[NIB];
+                for (int u = 0; u < WRB; ++u)
 #pragma unroll
-                    for (int ib = 0; ib < NIB; ++ib)
-                        a[ib] = *reinterpret_cast<const bf16x8 *>(&FsT[(16 * ib + (lane & 15)) * ST + kk]);
+                    for (int t = 0; t < WCB; ++t)
 #pragma unroll
-                    for (int nb = 0; nb < NWB; ++nb) {
-                        const bf16x8 bb = *reinterpret_cast<const bf16x8 *>(
-                            &DsT[(16 * (w * NWB + nb) + (lane & 15)) * ST + kk]);
+                        for (int r = 0; r < 4; ++r) {
+                            const int32_t row = row0 + 16 * (wr + NRG * u) + 4 * (lane >> 4) + r;
+                            if (row < n_in)
+                                dF[(int64_t)row * CI + 16 * (wc + NCBW * t) + (lane & 15)] =
+                                    acc[u][t][r];
+                        }
+            }
+            // ---- dW += F_tile^T D_tile  ([CI, TR] x [TR, K2]) over the tile rows
+            if (dW_part) {
+                const DT *Fb = Fs[buf];
+                if constexpr (!kBf) {
+#pragma unroll 2
+                    for (int k0 = 0; k0 < TR; k0 += 4) {
+                        const int kk = k0 + (lane >> 4);
+                        float a[NIB];
+#pragma unroll
+                        for (int ib = 0; ib < NIB; ++ib) a[ib] = Fb[kk * SF + 16 * ib + (lane & 15)];
+#pragma unroll
+                        for (int nb = 0; nb < NWB; ++nb) {
+                            const float bb = D[kk * SD + 16 * (mw * NWB + nb) + (lane & 15)];
+#pragma unroll
+                            for (int ib = 0; ib < NIB; ++ib)
+                                accw[ib][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                    a[ib], bb, accw[ib][nb], 0, 0, 0);
+                        }
+                    }
+                } else {
+#pragma unroll
+                    for (int k0 = 0; k0 < TR; k0 += 32) {
+                        const int kk = k0 + 8 * (lane >> 4);
+                        bf16x8 a[NIB];
 #pragma unroll
                         for (int ib = 0; ib < NIB; ++ib)
-                            accw[ib][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ib], bb, accw[ib][nb], 0, 0, 0);
+                            a[ib] = lds_column8(&Fb[kk * SF + 16 * ib + (lane & 15)], SF);
+#pragma unroll
+                        for (int nb = 0; nb < NWB; ++nb) {
+                            const bf16x8 bb =
+                                lds_column8(&D[kk * SD + 16 * (mw * NWB + nb) + (lane & 15)], SD);
+#pragma unroll
+                            for (int ib = 0; ib < NIB; ++ib)
+                                accw[ib][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                    a[ib], bb, accw[ib][nb], 0, 0, 0);
+                        }
                     }
                 }
             }
@@ -782,7 +990,7 @@ __global__ void __launch_bounds__((bwd_waves<M, CI, CO, kBf>() * 64), 1)
         for (int nb = 0; nb < NWB; ++nb)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                out[(16 * ib + 4 * (lane >> 4) + r) * K2 + 16 * (w * NWB + nb) + (lane & 15)] =
+                out[(16 * ib + 4 * (lane >> 4) + r) * K2 + 16 * (mw * NWB + nb) + (lane & 15)] =
                     accw[ib][nb][r];
 }
 
@@ -849,12 +1057,12 @@ __global__ void w_perm_f32_kernel(const float *__restrict__ W, int32_t M, int32_
 }
 
 // ---------------------------------------------------------------- dispatch tables
-using FwdFn = void (*)(int32_t, const int32_t *, const int32_t *, const float *, sbc_geometry,
+using FwdFn = void (*)(int32_t, const int32_t *, const int32_t *, const float *, KGeo,
                        const void *, const void *, float *);
 using RegFn = void (*)(int32_t, int32_t, const int32_t *, const int32_t *, const float *,
-                       sbc_geometry, const void *, const void *, float *);
+                       KGeo, const void *, const void *, float *);
 using BwdFn = void (*)(int32_t, int32_t, const int32_t *, const int32_t *, const int32_t *,
-                       const float *, sbc_geometry, const void *, const void *, const void *,
+                       const float *, KGeo, const void *, const void *, const void *,
                        float *, float *);
 
 struct Shape {
@@ -903,15 +1111,15 @@ RegFn reg_for(int basis_mode) {
 template <int M, int CI, int CO, bool kBf>
 BwdFn bwd_for(int basis_mode) {
     switch (basis_mode) {
-        case 0: return bwd_fused_kernel<M, CI, CO, 0, kBf>;
+        case 0: return bwd_ws_kernel<M, CI, CO, 0, kBf>;
         case SBC_BASIS_MONO4 + 1:
-            if constexpr (M == 4) return bwd_fused_kernel<M, CI, CO, SBC_BASIS_MONO4 + 1, kBf>;
+            if constexpr (M == 4) return bwd_ws_kernel<M, CI, CO, SBC_BASIS_MONO4 + 1, kBf>;
             return nullptr;
         case SBC_BASIS_MONO8 + 1:
-            if constexpr (M == 8) return bwd_fused_kernel<M, CI, CO, SBC_BASIS_MONO8 + 1, kBf>;
+            if constexpr (M == 8) return bwd_ws_kernel<M, CI, CO, SBC_BASIS_MONO8 + 1, kBf>;
             return nullptr;
         case SBC_BASIS_EVENT8 + 1:
-            if constexpr (M == 8) return bwd_fused_kernel<M, CI, CO, SBC_BASIS_EVENT8 + 1, kBf>;
+            if constexpr (M == 8) return bwd_ws_kernel<M, CI, CO, SBC_BASIS_EVENT8 + 1, kBf>;
             return nullptr;
     }
     return nullptr;
@@ -956,6 +1164,11 @@ BwdFn find_bwd(const Shape &s, int basis_mode) {
     SBC_BWD_SHAPES(SBC_X)
 #undef SBC_X
     return nullptr;
+}
+
+int ws_gather_waves_rt(int32_t M, int32_t CI, int32_t CO, bool bf) {
+    (void)M;
+    return (!bf && CI <= 32 && CO <= 32) ? 8 : 4;
 }
 
 int basis_mode_of(const float *v, const sbc_geometry *g) {
@@ -1009,11 +1222,46 @@ bool fused_backward_available(int32_t M, int32_t CI, int32_t CO, bool bf) {
     return find_bwd(Shape{M, CI, CO, bf}, 0) != nullptr;
 }
 
-size_t fused_workspace_bytes(int32_t M, int32_t CI, int32_t CO) {
-    // a permuted copy of W plus the per-block dW partials
+// Workspace of the fused kernels: a permuted copy of W, the per-block dW
+// partials, and the packed event coordinates.
+size_t fused_workspace_bytes(int32_t M, int32_t CI, int32_t CO, int32_t n_points) {
     return align_up((size_t)M * CI * CO * 4) +
-           align_up((size_t)kMaxBlocksBwd * (size_t)CI * M * CO * 4);
+           align_up((size_t)kMaxBlocksBwd * (size_t)CI * M * CO * 4) +
+           align_up((size_t)(n_points > 0 ? n_points : 0) * sizeof(int4));
 }
+
+namespace {
+
+// Kernel geometry for a call: packs the event coordinates into the workspace
+// (after the weight copy and the dW partials) when the basis is evaluated
+// from an event stream.
+sbc_status make_kgeo(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,
+                     int32_t CI, int32_t CO, void *ws, hipStream_t stream, KGeo *kg) {
+    *kg = KGeo{};
+    if (v || !g) return SBC_OK;
+    kg->inv_r = 1.0 / (double)g->radius;
+    kg->inv_tau = 1.0f / g->tau;
+    kg->x_in = g->x_in;
+    kg->x_out = g->x_out;
+    if (g->basis == SBC_BASIS_EVENT8) {
+        // event streams are in place: rows and columns index the same events
+        const int32_t n = csr->n_cols > csr->n_rows ? csr->n_cols : csr->n_rows;
+        int4 *pk = reinterpret_cast<int4 *>(static_cast<char *>(ws) +
+                                            align_up((size_t)M * CI * CO * 4) +
+                                            align_up((size_t)kMaxBlocksBwd * (size_t)CI * M * CO * 4));
+        if (n > 0) {
+            int blocks = grid_for(n, 256);
+            if (blocks > 2048) blocks = 2048;
+            hipLaunchKernelGGL(pack_events_kernel, dim3(blocks), dim3(256), 0, stream, g->px, g->py,
+                               g->t, n, pk);
+            SBC_LAUNCH_CHECK();
+        }
+        kg->ev = pk;
+    }
+    return SBC_OK;
+}
+
+}  // namespace
 
 sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,
                          const void *F, const void *W, bool bf, int32_t CI, int32_t CO, float *Y,
@@ -1021,7 +1269,8 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
     FwdFn fn = find_fwd(Shape{M, CI, CO, bf}, basis_mode_of(v, g));
     if (!fn) return fail(SBC_ERR_UNSUPPORTED, "no fused forward for this shape");
     if (csr->n_rows == 0) return SBC_OK;
-    sbc_geometry gr = g ? *g : sbc_geometry{};
+    KGeo gr;
+    SBC_TRY(make_kgeo(csr, v, g, M, CI, CO, ws, stream, &gr));
     if (RegFn rf = find_reg(Shape{M, CI, CO, bf}, basis_mode_of(v, g))) {
         const int32_t n_tiles = (csr->n_rows + 15) / 16;
         int per_cu = 0;
@@ -1046,10 +1295,9 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
     }
     const int K = M * CI;
     const int TR = (K * (bf ? 2 : 4) * 64 <= 65536) ? 64 : 32;
-    sbc_geometry gg = g ? *g : sbc_geometry{};
     trace_before("fwd_fused", stream);
     hipLaunchKernelGGL(fn, dim3(grid_for(csr->n_rows, TR)), dim3(kFwdWaves * 64), 0, stream,
-                       csr->n_rows, csr->row_ptr, csr->col_idx, v, gg, F, Wop, Y);
+                       csr->n_rows, csr->row_ptr, csr->col_idx, v, gr, F, Wop, Y);
     SBC_LAUNCH_CHECK();
     trace_after("fwd_fused", stream);
     return SBC_OK;
@@ -1071,14 +1319,15 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
         SBC_TRY(launch_perm(W, true, true, M, CI, CO, CO, K2, 1, wt, stream));
     else
         SBC_TRY(launch_perm(W, false, false, M, CI, CO, (int64_t)CO * CI, 1, CI, wt, stream));
-    const int TR = bf ? 32 : ((K2 * 4 * 64 <= 65536) ? 64 : 32);
+    const int TR = kWsTR;
     const int32_t n_tiles = (n_in + TR - 1) / TR;
-    const int nw = (TR / 16) * (CI / 16) >= 8 ? 8 : 4;
+    const int nw = ws_gather_waves_rt(M, CI, CO, bf) + kWsMma;
     int blocks = device_cus();
     if (blocks > kMaxBlocksBwd) blocks = kMaxBlocksBwd;
     if (blocks > n_tiles) blocks = n_tiles;
     if (blocks < 1) blocks = 1;
-    sbc_geometry gg = g ? *g : sbc_geometry{};
+    KGeo gg;
+    SBC_TRY(make_kgeo(csr, v, g, M, CI, CO, ws, stream, &gg));
     if (n_in > 0 && (dF || dW)) {
         trace_before("bwd_fused", stream);
         hipLaunchKernelGGL(fn, dim3(blocks), dim3(nw * 64), 0, stream, n_in, n_tiles, csc->col_ptr,

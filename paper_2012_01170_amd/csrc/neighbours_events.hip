@@ -43,13 +43,16 @@ __global__ void pixel_count_kernel(const int32_t *__restrict__ px, const int32_t
 
 __global__ void pixel_scatter_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
                                      int32_t n, int32_t W, int32_t H, int32_t *__restrict__ cursor,
-                                     int32_t *__restrict__ list_unsorted) {
+                                     int32_t *__restrict__ list_unsorted,
+                                     int32_t *__restrict__ pixel_of) {
     int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
     int32_t x = px[i], y = py[i];
     if (!valid_pixel(x, y, W, H)) return;
-    int32_t pos = atomicAdd(&cursor[(int64_t)y * W + x], 1);
+    const int32_t q = y * W + x;  // < W * H < 2^31
+    int32_t pos = atomicAdd(&cursor[q], 1);
     list_unsorted[pos] = i;
+    pixel_of[pos] = q;
 }
 
 // Timestamps alongside the sorted lists.  Only the first pix_start[npix]
@@ -271,11 +274,11 @@ extern "C" sbc_status sbc_neighbour_search_events(const int32_t *px, const int32
                                ws.cursor));
     if (n > 0) {
         hipLaunchKernelGGL(pixel_scatter_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream, px,
-                           py, n, width, height, ws.cursor, ws.list_unsorted);
+                           py, n, width, height, ws.cursor, ws.list_unsorted, ws.scratch);
         SBC_LAUNCH_CHECK();
-        // order each pixel's list by event index; the payload is unused
-        SBC_TRY(segmented_sort_pairs(ws.pix_start, (int32_t)npix, ws.list_unsorted,
-                                     ws.list_unsorted, ws.list, ws.scratch, stream));
+        // order each pixel's list by event index (scratch holds each entry's pixel)
+        SBC_TRY(segmented_sort_pairs(ws.pix_start, (int32_t)npix, ws.scratch, n,
+                                     ws.list_unsorted, nullptr, ws.list, nullptr, stream));
         // listed events = pix_start[npix] <= n; the kernel is sized by n and
         // reads the true count from the end of the scan
         hipLaunchKernelGGL(list_times_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream,

@@ -254,43 +254,29 @@ __global__ void fill_kernel(int32_t *p, int32_t value, int64_t n) {
         p[i] = value;
 }
 
-// One wave per segment.  Segments of up to 64 entries are ranked in
-// registers; longer ones rank every entry against the whole segment.
+// One thread per entry p < min(ptr[n_segments], n_bound): its segment is
+// seg_of[p], and its rank is the number of keys of that segment below its own
+// (keys are distinct within a segment), so it moves to ptr[seg] + rank.  A
+// segment of length L costs L^2 key reads in all, spread over L threads; the
+// segments here are neighbourhood columns and pixel lists, a few tens long.
+// Ranks stay inside the segment even for repeated keys (an entry is never
+// counted below itself), so every write is in bounds.
 __global__ void __launch_bounds__(256)
-    segsort_kernel(const int32_t *ptr, int32_t n_segments, const int32_t *key_in,
-                   const int32_t *val_in, int32_t *key_out, int32_t *val_out) {
-    const int lane = threadIdx.x & 63;
-    const int waves_per_block = blockDim.x >> 6;
-    int64_t wave = (int64_t)blockIdx.x * waves_per_block + (threadIdx.x >> 6);
-    const int64_t n_waves = (int64_t)gridDim.x * waves_per_block;
-    for (int64_t seg = wave; seg < n_segments; seg += n_waves) {
-        const int32_t s = ptr[seg];
-        const int32_t len = ptr[seg + 1] - s;
-        if (len <= 0) continue;
-        if (len <= 64) {
-            int32_t k = INT_MAX, v = 0;
-            if (lane < len) {
-                k = key_in[s + lane];
-                v = val_in[s + lane];
-            }
-            int rank = 0;
-            for (int q = 0; q < len; ++q) {
-                int32_t kq = __shfl(k, q, 64);
-                rank += (kq < k) ? 1 : 0;
-            }
-            if (lane < len) {
-                key_out[s + rank] = k;
-                val_out[s + rank] = v;
-            }
-        } else {
-            for (int32_t a = lane; a < len; a += 64) {
-                const int32_t k = key_in[s + a];
-                int32_t rank = 0;
-                for (int32_t b = 0; b < len; ++b) rank += (key_in[s + b] < k) ? 1 : 0;
-                key_out[s + rank] = k;
-                val_out[s + rank] = val_in[s + a];
-            }
-        }
+    rank_sort_kernel(const int32_t *__restrict__ ptr, int32_t n_segments,
+                     const int32_t *__restrict__ seg_of, int64_t n_bound,
+                     const int32_t *__restrict__ key_in, const int32_t *__restrict__ val_in,
+                     int32_t *__restrict__ key_out, int32_t *__restrict__ val_out) {
+    int64_t n = ptr[n_segments];
+    n = n < n_bound ? n : n_bound;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n;
+         p += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t sg = seg_of[p];
+        const int32_t s = ptr[sg], t = ptr[sg + 1];
+        const int32_t k = key_in[p];
+        int32_t rank = 0;
+        for (int32_t b = s; b < t; ++b) rank += key_in[b] < k ? 1 : 0;
+        key_out[s + rank] = k;
+        if (val_out) val_out[s + rank] = val_in[p];
     }
 }
 
@@ -338,14 +324,14 @@ sbc_status exclusive_scan_i32(const int32_t *counts, int32_t *out, int64_t n, in
     return SBC_OK;
 }
 
-sbc_status segmented_sort_pairs(const int32_t *ptr, int32_t n_segments, const int32_t *key_in,
-                                const int32_t *val_in, int32_t *key_out, int32_t *val_out,
-                                hipStream_t stream) {
-    if (n_segments <= 0) return SBC_OK;
-    int64_t blocks = ((int64_t)n_segments + 3) / 4;
-    if (blocks > 16384) blocks = 16384;
-    hipLaunchKernelGGL(segsort_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, ptr,
-                       n_segments, key_in, val_in, key_out, val_out);
+sbc_status segmented_sort_pairs(const int32_t *ptr, int32_t n_segments, const int32_t *seg_of,
+                                int64_t n_bound, const int32_t *key_in, const int32_t *val_in,
+                                int32_t *key_out, int32_t *val_out, hipStream_t stream) {
+    if (n_segments <= 0 || n_bound <= 0) return SBC_OK;
+    int64_t blocks = (n_bound + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(rank_sort_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, ptr,
+                       n_segments, seg_of, n_bound, key_in, val_in, key_out, val_out);
     SBC_LAUNCH_CHECK();
     return SBC_OK;
 }
