@@ -93,6 +93,18 @@ sbc_status segmented_sort_pairs(const int32_t *ptr, int32_t n_segments, const in
                                 int64_t n_bound, const int32_t *key_in, const int32_t *val_in,
                                 int32_t *key_out, int32_t *val_out, hipStream_t stream);
 
+// Stable radix sort (sort.hip) of n (key, value) pairs, keys in [0, key_bound);
+// n = *n_dev clamped to [0, n_bound] (n_dev may be null: n = n_bound).
+// vals == nullptr: the values are the item indices.  No global atomics.
+size_t radix_sort_workspace_bytes(int64_t n_bound);
+sbc_status radix_sort_pairs(const int32_t *keys, const int32_t *vals, const int64_t *n_dev,
+                            int64_t n_bound, int32_t key_bound, int32_t *keys_out,
+                            int32_t *vals_out, void *ws, hipStream_t stream);
+// ptr[k] = first position of the sorted keys with key >= k, for k in
+// [0, key_bound]; keys must lie in [0, key_bound].
+sbc_status segment_bounds(const int32_t *sorted, const int64_t *n_dev, int64_t n_bound,
+                          int32_t key_bound, int32_t *ptr, hipStream_t stream);
+
 inline int grid_for(int64_t n, int block) {
     int64_t g = (n + block - 1) / block;
     return static_cast<int>(g < 1 ? 1 : g);

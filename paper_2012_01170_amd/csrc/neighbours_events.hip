@@ -2,9 +2,10 @@
 // (Section 3.2: a small spatial neighbourhood extending backwards in time).
 //
 // Pipeline (all on the caller's stream):
-//   1. per-pixel event lists in stream order: count per pixel, scan, scatter,
-//      then each pixel's list is sorted by event index (lists are short);
-//      the lists carry the event timestamps alongside the indices;
+//   1. per-pixel event lists in stream order: the events are sorted by pixel
+//      with a stable radix sort (equal pixels keep their event order), and
+//      the list bounds are where each pixel's run starts; the lists carry the
+//      event timestamps alongside the indices;
 //   2. count pass, one thread per event i: for each pixel q of its block, the
 //      events of q with index < i and t >= t_i - window form one contiguous
 //      run of q's list (indices and times both ascend along it), found by two
@@ -27,32 +28,21 @@ __device__ __forceinline__ bool valid_pixel(int32_t x, int32_t y, int32_t W, int
     return x >= 0 && x < W && y >= 0 && y < H;
 }
 
-__global__ void pixel_count_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
-                                   const int32_t *__restrict__ t, int32_t n, int32_t W, int32_t H,
-                                   int32_t *__restrict__ pix_count, uint32_t *status) {
-    int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+// Sort key of each event: its pixel, or npix (behind every pixel) for an
+// event off the sensor; raises the out-of-range and unsorted flags.
+__global__ void pixel_key_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
+                                 const int32_t *__restrict__ t, int32_t n, int32_t W, int32_t H,
+                                 int32_t *__restrict__ keys, uint32_t *status) {
+    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
-    int32_t x = px[i], y = py[i];
+    const int32_t x = px[i], y = py[i];
+    if (i > 0 && t[i] < t[i - 1]) atomicOr(status, (uint32_t)kFlagUnsorted);
     if (!valid_pixel(x, y, W, H)) {
         atomicOr(status, (uint32_t)kFlagOutOfRange);
+        keys[i] = W * H;
         return;
     }
-    if (i > 0 && t[i] < t[i - 1]) atomicOr(status, (uint32_t)kFlagUnsorted);
-    atomicAdd(&pix_count[(int64_t)y * W + x], 1);
-}
-
-__global__ void pixel_scatter_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
-                                     int32_t n, int32_t W, int32_t H, int32_t *__restrict__ cursor,
-                                     int32_t *__restrict__ list_unsorted,
-                                     int32_t *__restrict__ pixel_of) {
-    int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    int32_t x = px[i], y = py[i];
-    if (!valid_pixel(x, y, W, H)) return;
-    const int32_t q = y * W + x;  // < W * H < 2^31
-    int32_t pos = atomicAdd(&cursor[q], 1);
-    list_unsorted[pos] = i;
-    pixel_of[pos] = q;
+    keys[i] = y * W + x;  // < W * H < 2^31 - 1
 }
 
 // Timestamps alongside the sorted lists.  Only the first pix_start[npix]
@@ -157,42 +147,33 @@ __global__ void __launch_bounds__(256)
 }
 
 struct EventsWs {
-    int32_t *pix_count;
     int32_t *pix_start;
-    int32_t *cursor;
-    int32_t *list_unsorted;
+    int32_t *keys;
+    int32_t *sorted;
     int32_t *list;
     int32_t *list_t;
-    int32_t *scratch;
     int32_t *row_len;
     int64_t *total;
     uint32_t *status;
     void *scan_ws;
+    void *sort_ws;
 };
 
 EventsWs carve_events(void *base, int32_t n, int64_t npix, size_t *bytes) {
     Carver cv(base);
     EventsWs w;
-    w.pix_count = cv.take<int32_t>(npix);
     w.pix_start = cv.take<int32_t>(npix + 1);
-    w.cursor = cv.take<int32_t>(npix + 1);
-    w.list_unsorted = cv.take<int32_t>(n);
+    w.keys = cv.take<int32_t>(n);
+    w.sorted = cv.take<int32_t>(n);
     w.list = cv.take<int32_t>(n);
     w.list_t = cv.take<int32_t>(n);
-    w.scratch = cv.take<int32_t>(n);
     w.row_len = cv.take<int32_t>(n);
     w.total = cv.take<int64_t>(2);
     w.status = cv.take<uint32_t>(4);
-    w.scan_ws = cv.take<char>(scan_workspace_bytes(npix > n ? npix : n));
+    w.scan_ws = cv.take<char>(scan_workspace_bytes(n));
+    w.sort_ws = cv.take<char>(radix_sort_workspace_bytes(n));
     if (bytes) *bytes = cv.used;
     return w;
-}
-
-// Zeroes the pixel counts and the status word.
-__global__ void init_kernel(int32_t *__restrict__ pix_count, int64_t npix, uint32_t *status) {
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    for (int64_t x = gid; x < npix; x += (int64_t)gridDim.x * blockDim.x) pix_count[x] = 0;
-    if (gid == 0) *status = 0u;
 }
 
 template <int kSide>
@@ -244,8 +225,8 @@ extern "C" sbc_status sbc_neighbour_search_events(const int32_t *px, const int32
     clear_error();
     if (n < 0 || width <= 0 || height <= 0)
         return fail(SBC_ERR_INVALID_ARG, "n must be >= 0, width and height > 0");
-    if ((int64_t)width * height > (int64_t)INT32_MAX)
-        return fail(SBC_ERR_INVALID_ARG, "width * height must be < 2^31");
+    if ((int64_t)width * height >= (int64_t)INT32_MAX)
+        return fail(SBC_ERR_INVALID_ARG, "width * height must be < 2^31 - 1");
     if (half_extent < 0 || half_extent > 3)
         return fail(SBC_ERR_UNSUPPORTED, "half_extent must be 0..3");
     if (window < 0) return fail(SBC_ERR_INVALID_ARG, "window must be >= 0");
@@ -259,26 +240,16 @@ extern "C" sbc_status sbc_neighbour_search_events(const int32_t *px, const int32
     if (!workspace || workspace_bytes < need)
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_events_workspace_size()");
 
-    {
-        const int g = grid_for(npix, 256) < 1024 ? grid_for(npix, 256) : 1024;
-        hipLaunchKernelGGL(init_kernel, dim3(g), dim3(256), 0, stream, ws.pix_count, npix,
-                           ws.status);
-        SBC_LAUNCH_CHECK();
-    }
+    SBC_TRY(fill_i32(reinterpret_cast<int32_t *>(ws.status), 0, 1, stream));
+    if (n == 0) SBC_TRY(fill_i32(ws.pix_start, 0, npix + 1, stream));
     if (n > 0) {
-        hipLaunchKernelGGL(pixel_count_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream, px, py,
-                           t, n, width, height, ws.pix_count, ws.status);
+        hipLaunchKernelGGL(pixel_key_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream, px, py,
+                           t, n, width, height, ws.keys, ws.status);
         SBC_LAUNCH_CHECK();
-    }
-    SBC_TRY(exclusive_scan_i32(ws.pix_count, ws.pix_start, npix, ws.total + 1, ws.scan_ws, stream,
-                               ws.cursor));
-    if (n > 0) {
-        hipLaunchKernelGGL(pixel_scatter_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream, px,
-                           py, n, width, height, ws.cursor, ws.list_unsorted, ws.scratch);
-        SBC_LAUNCH_CHECK();
-        // order each pixel's list by event index (scratch holds each entry's pixel)
-        SBC_TRY(segmented_sort_pairs(ws.pix_start, (int32_t)npix, ws.scratch, n,
-                                     ws.list_unsorted, nullptr, ws.list, nullptr, stream));
+        // stable: each pixel's events stay in stream order
+        SBC_TRY(radix_sort_pairs(ws.keys, nullptr, nullptr, n, (int32_t)npix + 1, ws.sorted,
+                                 ws.list, ws.sort_ws, stream));
+        SBC_TRY(segment_bounds(ws.sorted, nullptr, n, (int32_t)npix, ws.pix_start, stream));
         // listed events = pix_start[npix] <= n; the kernel is sized by n and
         // reads the true count from the end of the scan
         hipLaunchKernelGGL(list_times_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream,

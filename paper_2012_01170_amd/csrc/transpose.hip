@@ -1,21 +1,24 @@
 // sbc_csr_transpose: stable transpose of the neighbourhood pattern
 // (Section 3.1, "Symmetry": the reverse neighbourhood is the transposed
-// matrix).  Counting sort by column, edge-parallel: per-column counts
-// (integer atomics), scan, scatter of (row, edge, column) through per-column
-// cursors, then every column is ordered by edge index (equivalently by row,
-// since edge indices ascend with the row), which makes the result independent
-// of the order in which the atomics were served.
+// matrix): each column lists its rows in ascending order, with edge_perm
+// giving every entry's CSR position.  Two ways, chosen by size, both
+// independent of scheduling:
+//   - up to kRadixMin edges, a counting sort: per-column counts and
+//     per-column cursors with integer atomics, then every column ordered by
+//     edge index with a per-entry rank sort (few launches);
+//   - beyond, a stable radix sort of the edges by column (values: the edge
+//     indices), with no atomics, whose passes read and write in runs (global
+//     atomics are served past the L2 cache here, one at a time per address,
+//     which is what limits the counting sort on millions of edges).
 //
-// Edges are e in [0, min(row_ptr[n_rows], nnz_bound)), so a malformed row_ptr
-// can never move a read or write outside the caller's arrays.
+// Edges are e in [0, min(row_ptr[n_rows], nnz_bound)); column indices outside
+// [0, n_cols) are left out (counting sort) or sorted behind every column
+// (radix sort), so a malformed pattern can never move a read or write
+// outside the caller's arrays.
 #include "common.hpp"
 
 namespace sbc {
 namespace {
-
-constexpr int kScatterThreads = 256;
-constexpr int kScatterItems = 4;
-constexpr int kScatterChunk = kScatterThreads * kScatterItems;  // edges per block
 
 __device__ __forceinline__ int64_t edge_count(const int32_t *row_ptr, int32_t n_rows,
                                               int64_t nnz_bound) {
@@ -32,6 +35,12 @@ __device__ __forceinline__ int32_t row_of(const int32_t *__restrict__ row_ptr, i
     }
     return lo;
 }
+
+constexpr int kScatterThreads = 256;
+constexpr int kScatterItems = 4;
+constexpr int kScatterChunk = kScatterThreads * kScatterItems;  // edges per block
+
+
 
 __global__ void col_count_kernel(const int32_t *__restrict__ row_ptr, int32_t n_rows,
                                  int64_t nnz_bound, int32_t n_cols,
@@ -74,28 +83,88 @@ __global__ void __launch_bounds__(kScatterThreads)
     }
 }
 
+// Sort keys (column, or n_cols for an invalid one) per edge, and the edge count.
+__global__ void col_keys_kernel(const int32_t *__restrict__ row_ptr, int32_t n_rows,
+                                int64_t nnz_bound, int32_t n_cols,
+                                const int32_t *__restrict__ col_idx, int32_t *__restrict__ keys,
+                                int64_t *__restrict__ n_edges) {
+    const int64_t E = edge_count(row_ptr, n_rows, nnz_bound);
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (tid == 0) *n_edges = E;
+    for (int64_t e = tid; e < E; e += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t c = col_idx[e];
+        keys[e] = (c >= 0 && c < n_cols) ? c : n_cols;
+    }
+}
+
+
+// rowof[e] = the row holding edge e.  Each block takes 1024 consecutive
+// edges: two threads locate the rows of its first and last edge, and every
+// edge then bisects between those two.
+__global__ void __launch_bounds__(256)
+    edge_rows_kernel(const int32_t *__restrict__ row_ptr, int32_t n_rows, int64_t nnz_bound,
+                     int32_t *__restrict__ rowof) {
+    __shared__ int32_t span[2];
+    const int64_t E = edge_count(row_ptr, n_rows, nnz_bound);
+    const int64_t e0 = (int64_t)blockIdx.x * 1024;
+    if (e0 >= E) return;  // the whole block leaves together
+    const int64_t e1 = e0 + 1024 < E ? e0 + 1024 : E;
+    if (threadIdx.x < 2) span[threadIdx.x] = row_of(row_ptr, 0, n_rows - 1, threadIdx.x ? e1 - 1 : e0);
+    __syncthreads();
+    const int32_t r0 = span[0], r1 = span[1];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int64_t e = e0 + q * 256 + threadIdx.x;
+        if (e < e1) rowof[e] = row_of(row_ptr, r0, r1, e);
+    }
+}
+
+// row_idx[p] = rowof[edge_perm[p]] for the sorted positions p
+__global__ void gather_rows_kernel(const int32_t *__restrict__ edge_perm,
+                                   const int64_t *__restrict__ n_edges,
+                                   const int32_t *__restrict__ rowof,
+                                   int32_t *__restrict__ row_idx) {
+    const int64_t E = *n_edges;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < E;
+         p += (int64_t)gridDim.x * blockDim.x)
+        row_idx[p] = rowof[edge_perm[p]];
+}
+
+// Rows of the transpose workspace; the counting sort uses count, cursor and
+// the three tmp arrays, the radix sort keys, sorted, rowof and sort_ws.
+constexpr int64_t kRadixMin = 1 << 21;
+
 struct TransposeWs {
-    int32_t *count;
-    int32_t *cursor;
-    int32_t *rows_tmp;
-    int32_t *perm_tmp;
-    int32_t *cols_tmp;
-    int64_t *total;
-    void *scan_ws;
+    int32_t *count, *cursor, *rows_tmp, *perm_tmp, *cols_tmp;   // counting sort
+    int32_t *keys, *sorted, *rowof;                               // radix sort
+    int64_t *n_edges;
+    void *scan_ws, *sort_ws;
 };
 
 TransposeWs carve_transpose(void *base, int32_t n_cols, int64_t nnz, size_t *bytes) {
     Carver cv(base);
-    TransposeWs w;
-    w.count = cv.take<int32_t>(n_cols);
-    w.cursor = cv.take<int32_t>((size_t)n_cols + 1);
-    w.rows_tmp = cv.take<int32_t>(nnz);
-    w.perm_tmp = cv.take<int32_t>(nnz);
-    w.cols_tmp = cv.take<int32_t>(nnz);
-    w.total = cv.take<int64_t>(1);
-    w.scan_ws = cv.take<char>(scan_workspace_bytes(n_cols));
+    TransposeWs w{};
+    w.n_edges = cv.take<int64_t>(1);
+    if (nnz < kRadixMin) {
+        w.count = cv.take<int32_t>(n_cols);
+        w.cursor = cv.take<int32_t>((size_t)n_cols + 1);
+        w.rows_tmp = cv.take<int32_t>(nnz);
+        w.perm_tmp = cv.take<int32_t>(nnz);
+        w.cols_tmp = cv.take<int32_t>(nnz);
+        w.scan_ws = cv.take<char>(scan_workspace_bytes(n_cols));
+    } else {
+        w.keys = cv.take<int32_t>(nnz);
+        w.sorted = cv.take<int32_t>(nnz);
+        w.rowof = cv.take<int32_t>(nnz);
+        w.sort_ws = cv.take<char>(radix_sort_workspace_bytes(nnz));
+    }
     if (bytes) *bytes = cv.used;
     return w;
+}
+
+int grid_cap(int64_t n, int cap) {
+    int64_t g = (n + 255) / 256;
+    return (int)(g < 1 ? 1 : (g > cap ? cap : g));
 }
 
 }  // namespace
@@ -125,23 +194,21 @@ extern "C" sbc_status sbc_csr_transpose(const sbc_csr *csr, int32_t *col_ptr, in
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_transpose_workspace_size()");
     const int32_t R = csr->n_rows, C = csr->n_cols;
     const int64_t nnz = csr->nnz_bound;
-    SBC_TRY(fill_i32(ws.count, 0, C, stream));
-    if (R > 0 && nnz > 0) {
-        int64_t g = (nnz + 255) / 256;
-        if (g > 8192) g = 8192;
+    if (R == 0 || nnz == 0) return fill_i32(col_ptr, 0, (int64_t)C + 1, stream);
+    if (C == INT32_MAX) return fail(SBC_ERR_INVALID_ARG, "n_cols must be < 2^31 - 1");
+    if (nnz < kRadixMin) {
+        SBC_TRY(fill_i32(ws.count, 0, C, stream));
         trace_before("transpose_count", stream);
-        hipLaunchKernelGGL(col_count_kernel, dim3((unsigned)g), dim3(256), 0, stream, csr->row_ptr,
-                           R, nnz, C, csr->col_idx, ws.count);
+        hipLaunchKernelGGL(col_count_kernel, dim3(grid_cap(nnz, 8192)), dim3(256), 0, stream,
+                           csr->row_ptr, R, nnz, C, csr->col_idx, ws.count);
         SBC_LAUNCH_CHECK();
         trace_after("transpose_count", stream);
-    }
-    SBC_TRY(exclusive_scan_i32(ws.count, col_ptr, C, ws.total, ws.scan_ws, stream, ws.cursor));
-    if (R > 0 && C > 0 && nnz > 0) {
-        const int64_t g = (nnz + kScatterChunk - 1) / kScatterChunk;
+        SBC_TRY(exclusive_scan_i32(ws.count, col_ptr, C, ws.n_edges, ws.scan_ws, stream,
+                                   ws.cursor));
         trace_before("transpose_scatter", stream);
-        hipLaunchKernelGGL(col_scatter_kernel, dim3((unsigned)g), dim3(kScatterThreads), 0, stream,
-                           csr->row_ptr, R, nnz, C, csr->col_idx, ws.cursor, ws.rows_tmp,
-                           ws.perm_tmp, ws.cols_tmp);
+        hipLaunchKernelGGL(col_scatter_kernel, dim3((unsigned)((nnz + kScatterChunk - 1) / kScatterChunk)),
+                           dim3(kScatterThreads), 0, stream, csr->row_ptr, R, nnz, C,
+                           csr->col_idx, ws.cursor, ws.rows_tmp, ws.perm_tmp, ws.cols_tmp);
         SBC_LAUNCH_CHECK();
         trace_after("transpose_scatter", stream);
         trace_before("transpose_sort", stream);
@@ -149,6 +216,26 @@ extern "C" sbc_status sbc_csr_transpose(const sbc_csr *csr, int32_t *col_ptr, in
         SBC_TRY(segmented_sort_pairs(col_ptr, C, ws.cols_tmp, nnz, ws.perm_tmp, ws.rows_tmp,
                                      edge_perm, row_idx, stream));
         trace_after("transpose_sort", stream);
+        return SBC_OK;
     }
+    trace_before("transpose_count", stream);
+    hipLaunchKernelGGL(col_keys_kernel, dim3(grid_cap(nnz, 8192)), dim3(256), 0, stream,
+                       csr->row_ptr, R, nnz, C, csr->col_idx, ws.keys, ws.n_edges);
+    SBC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(edge_rows_kernel, dim3((unsigned)((nnz + 1023) / 1024)), dim3(256), 0,
+                       stream, csr->row_ptr, R, nnz, ws.rowof);
+    SBC_LAUNCH_CHECK();
+    trace_after("transpose_count", stream);
+    trace_before("transpose_scatter", stream);
+    // values are the edge indices: they become edge_perm
+    SBC_TRY(radix_sort_pairs(ws.keys, nullptr, ws.n_edges, nnz, C + 1, ws.sorted, edge_perm,
+                             ws.sort_ws, stream));
+    trace_after("transpose_scatter", stream);
+    trace_before("transpose_sort", stream);
+    SBC_TRY(segment_bounds(ws.sorted, ws.n_edges, nnz, C, col_ptr, stream));
+    hipLaunchKernelGGL(gather_rows_kernel, dim3(grid_cap(nnz, 8192)), dim3(256), 0, stream,
+                       edge_perm, ws.n_edges, ws.rowof, row_idx);
+    SBC_LAUNCH_CHECK();
+    trace_after("transpose_sort", stream);
     return SBC_OK;
 }
