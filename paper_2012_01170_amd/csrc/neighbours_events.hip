@@ -6,10 +6,12 @@
 //      with a stable radix sort (equal pixels keep their event order), and
 //      the list bounds are where each pixel's run starts; the lists carry the
 //      event timestamps alongside the indices;
-//   2. count pass, one thread per event i: for each pixel q of its block, the
-//      events of q with index < i and t >= t_i - window form one contiguous
-//      run of q's list (indices and times both ascend along it), found by two
-//      binary searches; the row length is the sum of the run lengths;
+//   2. runs: for each pixel q of an event i's block, the events of q with
+//      index < i and t >= t_i - window form one contiguous run of q's list
+//      (indices and times both ascend along it); for blocks up to 3x3 the
+//      runs of all events come from one two-pointer sweep per (pixel,
+//      offset) pair and are stored, for larger blocks each event bisects;
+//      the count pass sums the run lengths per event;
 //   3. scan -> row_ptr;
 //   4. fill pass: the (2h+1)^2 runs are merged by index into the row.
 // Events with a pixel outside the sensor get no neighbours and are in no
@@ -98,14 +100,58 @@ __device__ __forceinline__ int32_t find_runs(int32_t i, int32_t x, int32_t y, in
     return count;
 }
 
+// Runs of every event in the lists of its block's pixels, by a two-pointer
+// sweep: one thread per (pixel p, offset k) walks the events of p in stream
+// order.  For event i the run in the list of q = p + offset is [lo, hi): hi
+// is the first entry with index >= i and lo the first with t >= t_i - window;
+// both only move forward as i grows (indices and times ascend along every
+// list), so each list is read once per thread instead of bisected per event.
+// runs[i * kRunsK + k] = (lo, hi); offsets past the sensor give (0, 0).
+constexpr int kRunsK = 9;  // stored runs per event: blocks up to 3x3
+
 template <int kSide>
+__global__ void pixel_runs_kernel(int64_t npix, int32_t W, int32_t H, int32_t window,
+                                  const int32_t *__restrict__ pix_start,
+                                  const int32_t *__restrict__ list,
+                                  const int32_t *__restrict__ list_t, int2 *__restrict__ runs) {
+    constexpr int K = kSide * kSide;
+    constexpr int h = kSide / 2;
+    static_assert(K <= kRunsK, "runs are stored for blocks up to 3x3");
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (tid >= npix * K) return;
+    const int64_t p = tid / K;
+    const int k = (int)(tid % K);
+    const int32_t x = (int32_t)(p % W), y = (int32_t)(p / W);
+    const int32_t qx = x + (k % kSide) - h, qy = y + (k / kSide) - h;
+    const int32_t ps = pix_start[p], pe = pix_start[p + 1];
+    if (!valid_pixel(qx, qy, W, H)) {
+        for (int32_t a = ps; a < pe; ++a) runs[(int64_t)list[a] * kRunsK + k] = make_int2(0, 0);
+        return;
+    }
+    const int64_t q = (int64_t)qy * W + qx;
+    const int32_t qe = pix_start[q + 1];
+    int32_t lo = pix_start[q], hi = lo;
+    for (int32_t a = ps; a < pe; ++a) {
+        const int32_t i = list[a];
+        // t_j >= t_i - window, computed without int32 overflow
+        const int64_t tmin64 = (int64_t)list_t[a] - window;
+        const int32_t tmin = tmin64 < (int64_t)INT_MIN ? INT_MIN : (int32_t)tmin64;
+        while (hi < qe && list[hi] < i) ++hi;
+        while (lo < hi && list_t[lo] < tmin) ++lo;
+        runs[(int64_t)i * kRunsK + k] = make_int2(lo, hi);
+    }
+}
+
+// kStored: runs read from pixel_runs_kernel's output, else found by bisection.
+template <int kSide, bool kStored>
 __global__ void __launch_bounds__(256)
     event_rows_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
                       const int32_t *__restrict__ t, int32_t n, int32_t W, int32_t H,
                       int32_t window, const int32_t *__restrict__ pix_start,
                       const int32_t *__restrict__ list, const int32_t *__restrict__ list_t,
                       int32_t *__restrict__ row_len, const int32_t *__restrict__ row_ptr,
-                      int32_t *__restrict__ col_idx, int64_t col_capacity) {
+                      int32_t *__restrict__ col_idx, int64_t col_capacity,
+                      const int2 *__restrict__ runs) {
     const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
     const int32_t x = px[i], y = py[i];
@@ -114,8 +160,18 @@ __global__ void __launch_bounds__(256)
         return;
     }
     Runs r;
-    const int32_t cnt = find_runs<kSide>(i, x, y, t[i], W, H, (int64_t)window, pix_start, list,
-                                         list_t, r);
+    int32_t cnt = 0;
+    if constexpr (kStored) {
+#pragma unroll
+        for (int k = 0; k < kSide * kSide; ++k) {
+            const int2 lh = runs[(int64_t)i * kRunsK + k];
+            r.lo[k] = lh.x;
+            r.hi[k] = lh.y;
+            cnt += lh.y - lh.x;
+        }
+    } else {
+        cnt = find_runs<kSide>(i, x, y, t[i], W, H, (int64_t)window, pix_start, list, list_t, r);
+    }
     if (row_len) {
         row_len[i] = cnt;
         return;
@@ -153,6 +209,7 @@ struct EventsWs {
     int32_t *list;
     int32_t *list_t;
     int32_t *row_len;
+    int2 *runs;
     int64_t *total;
     uint32_t *status;
     void *scan_ws;
@@ -168,6 +225,7 @@ EventsWs carve_events(void *base, int32_t n, int64_t npix, size_t *bytes) {
     w.list = cv.take<int32_t>(n);
     w.list_t = cv.take<int32_t>(n);
     w.row_len = cv.take<int32_t>(n);
+    w.runs = cv.take<int2>((size_t)n * kRunsK);
     w.total = cv.take<int64_t>(2);
     w.status = cv.take<uint32_t>(4);
     w.scan_ws = cv.take<char>(scan_workspace_bytes(n));
@@ -180,17 +238,43 @@ template <int kSide>
 void launch_rows(int32_t n, const int32_t *px, const int32_t *py, const int32_t *t, int32_t W,
                  int32_t H, int32_t window, const EventsWs &ws, int32_t *row_len,
                  const int32_t *row_ptr, int32_t *col_idx, int64_t cap, hipStream_t stream) {
-    hipLaunchKernelGGL((event_rows_kernel<kSide>), dim3(grid_for(n, 256)), dim3(256), 0, stream,
-                       px, py, t, n, W, H, window, ws.pix_start, ws.list, ws.list_t, row_len,
-                       row_ptr, col_idx, cap);
+    constexpr bool kStored = kSide * kSide <= kRunsK;
+    hipLaunchKernelGGL((event_rows_kernel<kSide, kStored>), dim3(grid_for(n, 256)), dim3(256), 0,
+                       stream, px, py, t, n, W, H, window, ws.pix_start, ws.list, ws.list_t,
+                       row_len, row_ptr, col_idx, cap, ws.runs);
 }
 
-sbc_status rows_dispatch(int32_t half_extent, int32_t n, const int32_t *px, const int32_t *py,
-                         const int32_t *t, int32_t W, int32_t H, int32_t window,
-                         const EventsWs &ws, int32_t *row_len, const int32_t *row_ptr,
-                         int32_t *col_idx, int64_t cap, hipStream_t stream) {
+template <int kSide>
+void launch_runs(int64_t npix, int32_t W, int32_t H, int32_t window, const EventsWs &ws,
+                 hipStream_t stream) {
+    if constexpr (kSide * kSide <= kRunsK) {
+        const int64_t threads = npix * kSide * kSide;
+        hipLaunchKernelGGL(pixel_runs_kernel<kSide>, dim3((unsigned)((threads + 255) / 256)),
+                           dim3(256), 0, stream, npix, W, H, window, ws.pix_start, ws.list,
+                           ws.list_t, ws.runs);
+    }
+}
+
+sbc_status runs_dispatch(int32_t half_extent, int64_t npix, int32_t W, int32_t H, int32_t window,
+                         const EventsWs &ws, hipStream_t stream) {
+    switch (half_extent) {
+        case 0: launch_runs<1>(npix, W, H, window, ws, stream); break;
+        case 1: launch_runs<3>(npix, W, H, window, ws, stream); break;
+        default: return SBC_OK;  // larger blocks bisect per event
+    }
+    SBC_LAUNCH_CHECK();
+    return SBC_OK;
+}
+
+// Count pass (row_len != null; computes the runs first) or fill pass.
+sbc_status rows_dispatch(int32_t half_extent, int64_t npix, int32_t n, const int32_t *px,
+                         const int32_t *py, const int32_t *t, int32_t W, int32_t H,
+                         int32_t window, const EventsWs &ws, int32_t *row_len,
+                         const int32_t *row_ptr, int32_t *col_idx, int64_t cap,
+                         hipStream_t stream) {
     const char *name = row_len ? "events_count" : "events_fill";
     trace_before(name, stream);
+    if (row_len) SBC_TRY(runs_dispatch(half_extent, npix, W, H, window, ws, stream));
     switch (half_extent) {
         case 0: launch_rows<1>(n, px, py, t, W, H, window, ws, row_len, row_ptr, col_idx, cap, stream); break;
         case 1: launch_rows<3>(n, px, py, t, W, H, window, ws, row_len, row_ptr, col_idx, cap, stream); break;
@@ -255,8 +339,8 @@ extern "C" sbc_status sbc_neighbour_search_events(const int32_t *px, const int32
         hipLaunchKernelGGL(list_times_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream,
                            ws.list, t, ws.pix_start, npix, ws.list_t);
         SBC_LAUNCH_CHECK();
-        SBC_TRY(rows_dispatch(half_extent, n, px, py, t, width, height, window, ws, ws.row_len,
-                              nullptr, nullptr, 0, stream));
+        SBC_TRY(rows_dispatch(half_extent, npix, n, px, py, t, width, height, window, ws,
+                              ws.row_len, nullptr, nullptr, 0, stream));
     }
     SBC_TRY(exclusive_scan_i32(ws.row_len, row_ptr, n, ws.total, ws.scan_ws, stream));
     if (nnz_host) {
@@ -274,7 +358,7 @@ extern "C" sbc_status sbc_neighbour_search_events(const int32_t *px, const int32
                                               " < E = " + std::to_string(host[0]));
     }
     if (n > 0 && col_capacity > 0)
-        SBC_TRY(rows_dispatch(half_extent, n, px, py, t, width, height, window, ws, nullptr,
-                              row_ptr, col_idx, col_capacity, stream));
+        SBC_TRY(rows_dispatch(half_extent, npix, n, px, py, t, width, height, window, ws,
+                              nullptr, row_ptr, col_idx, col_capacity, stream));
     return SBC_OK;
 }
