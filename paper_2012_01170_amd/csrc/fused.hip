@@ -13,7 +13,7 @@
 //   contract Y_tile = G_tile W on the matrix cores (float32: 16x16x4 f32
 //            MFMA with W read from L2; bf16: G rounded to bf16 in LDS and
 //            16x16x32 bf16 MFMA against a [C_out, M*C_in] copy of W).
-// Forward for narrow inputs (C_in <= 32), persistent blocks of 8 waves: each
+// Forward for narrow inputs (C_in <= 32, or 64 in bf16), persistent blocks of 8 waves: each
 //            wave owns 16-row tiles and keeps G in registers as the MFMA A
 //            operand; W stays in LDS for the life of the block.  A row's four
 //            lanes take four edges per step, with the next step's neighbour
@@ -158,9 +158,10 @@ __device__ __forceinline__ int32_t load_bound(const int32_t *__restrict__ ptr, i
 //   kT: the pattern is transposed (rows are inputs j, idx gives outputs i).
 //   X [*, C] features gathered along the pattern; out tile row stride S
 //   (elements), row r_local at out + r_local * S, column m*C + c.
-//   my_bound: load_bound<RPW>(ptr, n_rows, row_begin) of this lane.
-//   next_row_begin >= 0: the bound of the next call's rows is loaded while
-//   this one runs and returned.
+//   pre.bound: load_bound<RPW>(ptr, n_rows, row_begin) of this lane;
+//   pre.idx0 (pre.have_idx, pipelined only): idx[first edge + lane].
+//   next_row_begin >= 0: the bound of the next call's rows (and, pipelined,
+//   its first neighbour indices) is loaded while this one runs and returned.
 // The wave's edges are staged 64 at a time; the rows are owned by groups of
 // LPR lanes (each group owns NB rows, all accumulators live across the
 // staging chunks).  kPipelined: the group's NB rows advance together with
@@ -170,16 +171,25 @@ __device__ __forceinline__ int32_t load_bound(const int32_t *__restrict__ ptr, i
 // other waves multiply).  Otherwise the rows are taken one after another,
 // four edges at a time, after the basis values (for blocks that gather and
 // then multiply, where the co-resident block hides the latency).
+// What a gather call hands to the next one: the next rows' bound for this
+// lane and, when known, the neighbour index of the lane's edge in the next
+// rows' first chunk.
+struct GatherAhead {
+    int32_t bound;
+    int32_t idx0;
+    bool have_idx;
+};
+
 template <int M, int C, int kBasis, bool kXbf, bool kOutBf, bool kT, int RPW, bool kPipelined>
-__device__ __forceinline__ int32_t gather_rows(int32_t row_begin, int32_t n_rows,
-                                               const int32_t *__restrict__ ptr,
-                                               const int32_t *__restrict__ idx,
-                                               const int32_t *__restrict__ perm,
-                                               const float *__restrict__ v, const KGeo &g,
-                                               const void *__restrict__ Xv, void *out_tile, int S,
-                                               int local_row0, EdgeStage<M> &st, double inv_r,
-                                               float inv_tau, int32_t my_bound,
-                                               int32_t next_row_begin) {
+__device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_rows,
+                                                   const int32_t *__restrict__ ptr,
+                                                   const int32_t *__restrict__ idx,
+                                                   const int32_t *__restrict__ perm,
+                                                   const float *__restrict__ v, const KGeo &g,
+                                                   const void *__restrict__ Xv, void *out_tile,
+                                                   int S, int local_row0, EdgeStage<M> &st,
+                                                   double inv_r, float inv_tau, GatherAhead pre,
+                                                   int32_t next_row_begin) {
     constexpr int VEC = kXbf ? 8 : 4;
     static_assert(C % VEC == 0, "channels must be a multiple of the vector width");
     constexpr int LPR = C / VEC;                   // lanes per row
@@ -196,7 +206,7 @@ __device__ __forceinline__ int32_t gather_rows(int32_t row_begin, int32_t n_rows
     const int slot = lane / LPR;
     const int cg = lane % LPR;
 
-    if (lane <= RPW) st.bounds[lane] = my_bound;
+    if (lane <= RPW) st.bounds[lane] = pre.bound;
     const int32_t next_bound =
         next_row_begin >= 0 ? load_bound<RPW>(ptr, n_rows, next_row_begin) : 0;
     wave_lds_sync();
@@ -228,7 +238,7 @@ __device__ __forceinline__ int32_t gather_rows(int32_t row_begin, int32_t n_rows
             for (int q = 1; q < RPW; ++q)
                 if (st.bounds[q] <= e) s = q;
             row = row_begin + s;
-            other = idx[e];
+            other = (kPipelined && pre.have_idx && c0 == wb) ? pre.idx0 : idx[e];
             ev = (kBasis == 0) ? (perm ? (int64_t)perm[e] : (int64_t)e) : 0;
             st.nb[lane] = other;
             if (lane == 0) st.nb[64] = other;  // padding edge: a valid row, weight 0
@@ -356,7 +366,13 @@ __device__ __forceinline__ int32_t gather_rows(int32_t row_begin, int32_t n_rows
             }
         }
     }
-    return next_bound;
+    GatherAhead ahead{next_bound, 0, false};
+    if (kPipelined && next_row_begin >= 0) {
+        const int32_t nb0 = __shfl(next_bound, 0, 64), nb1 = __shfl(next_bound, RPW, 64);
+        ahead.idx0 = nb0 + lane < nb1 ? idx[nb0 + lane] : 0;
+        ahead.have_idx = true;
+    }
+    return ahead;
 }
 
 // acc[u][t] += A_tile[16 rb_u .., :] x B[:, 16 cb_t ..] for the 16x16 blocks of
@@ -513,7 +529,8 @@ __global__ void __launch_bounds__(kFwdWaves * 64, 2)
 
     gather_rows<M, CI, kBasis, kBf, kBf, false, RPW, false>(
         row0 + w * RPW, n_out, row_ptr, col_idx, nullptr, v, g, F, Gs, S, w * RPW, stage[w],
-        inv_r, inv_tau, load_bound<RPW>(row_ptr, n_out, row0 + w * RPW), -1);
+        inv_r, inv_tau, GatherAhead{load_bound<RPW>(row_ptr, n_out, row0 + w * RPW), 0, false},
+        -1);
     __syncthreads();
 
     const int wc = w % NCBW, wr = w / NCBW;
@@ -558,14 +575,23 @@ constexpr int reg_w_bytes() {
 
 template <int M, int CI, int CO, bool kBf>
 constexpr bool reg_forward_fits() {
-    // CI <= 32: wider inputs hold M*CI/4 gather accumulators per lane, which
-    // leaves too few waves per CU to hide the gather; the LDS-tile kernel wins
-    return reg_w_bytes<M, CI, CO, kBf>() <= 131072 && CI % 16 == 0 && CI <= 32 &&
-           CO % 16 == 0 && (!kBf || (CI / 4) % 8 == 0);
+    // float32 rows wider than 32 channels hold M*CI/4 gather accumulators per
+    // lane and spend long on float32 MFMAs with two waves per SIMD; there the
+    // LDS-tile kernel is faster.  bf16 rows of 64 channels still gain.
+    return reg_w_bytes<M, CI, CO, kBf>() <= 131072 && CI % 16 == 0 &&
+           (CI <= 32 || (kBf && CI <= 64)) && CO % 16 == 0 && (!kBf || (CI / 4) % 8 == 0);
+}
+
+// Waves per SIMD the register-resident forward is compiled for: four while
+// the gather accumulators (M * CI / 4 per lane) leave room, else two.
+template <int M, int CI>
+constexpr int reg_waves_per_eu() {
+    return M * CI / 4 <= 64 ? 4 : 2;
 }
 
 template <int M, int CI, int CO, int kBasis, bool kBf>
-__global__ void __launch_bounds__(kRegWaves * 64) __attribute__((amdgpu_waves_per_eu(4)))
+__global__ void __launch_bounds__(kRegWaves * 64)
+    __attribute__((amdgpu_waves_per_eu(reg_waves_per_eu<M, CI>())))
     fwd_reg_kernel(int32_t n_out, int32_t n_tiles, const int32_t *__restrict__ row_ptr,
                    const int32_t *__restrict__ col_idx, const float *__restrict__ v,
                    KGeo g, const void *__restrict__ Fv, const void *__restrict__ Wv,
@@ -646,9 +672,16 @@ __global__ void __launch_bounds__(kRegWaves * 64) __attribute__((amdgpu_waves_pe
             const int32_t eo = e0 + q + gq;          // this lane's edge
             const int32_t jo = jn;
             jn = (eo + 4 < e1) ? col_idx[eo + 4] : 0;
-            float f[4][CG];
+            // features of the four edges, SB at a time (fewer registers for wide rows)
+            constexpr int SB = CG <= 8 ? 4 : 2;
+            float bo[M];
+            bool have_basis = false;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u0 = 0; u0 < 4; u0 += SB) {
+            float f[SB][CG];
+#pragma unroll
+            for (int us = 0; us < SB; ++us) {
+                const int u = u0 + us;
                 const int32_t j = __shfl(jo, rl + 16 * u, 64);
                 if constexpr (kBf) {
                     const uint16_t *src = static_cast<const uint16_t *>(Fv) + (int64_t)j * CI + gq * CG;
@@ -658,8 +691,8 @@ __global__ void __launch_bounds__(kRegWaves * 64) __attribute__((amdgpu_waves_pe
                         const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
                         for (int k = 0; k < 4; ++k) {
-                            f[u][c + 2 * k] = __uint_as_float(w4[k] << 16);
-                            f[u][c + 2 * k + 1] = __uint_as_float(w4[k] & 0xFFFF0000u);
+                            f[us][c + 2 * k] = __uint_as_float(w4[k] << 16);
+                            f[us][c + 2 * k + 1] = __uint_as_float(w4[k] & 0xFFFF0000u);
                         }
                     }
                 } else {
@@ -667,30 +700,33 @@ __global__ void __launch_bounds__(kRegWaves * 64) __attribute__((amdgpu_waves_pe
 #pragma unroll
                     for (int c = 0; c < CG; c += 4) {
                         const float4 raw = *reinterpret_cast<const float4 *>(src + c);
-                        f[u][c] = raw.x;
-                        f[u][c + 1] = raw.y;
-                        f[u][c + 2] = raw.z;
-                        f[u][c + 3] = raw.w;
+                        f[us][c] = raw.x;
+                        f[us][c + 1] = raw.y;
+                        f[us][c + 2] = raw.z;
+                        f[us][c + 3] = raw.w;
                     }
                 }
             }
-            // this lane's edge basis (zero past the row's end: those lanes
-            // loaded row 0's features, which then carry no weight)
-            float bo[M];
-            if (eo < e1) {
-                edge_basis<M, kBasis>(g, v, row, jo, eo, inv_r, inv_tau, bo);
-            } else {
+            // this lane's edge basis, once per step (zero past the row's end:
+            // those lanes loaded row 0's features, which then carry no weight)
+            if (!have_basis) {
+                have_basis = true;
+                if (eo < e1) {
+                    edge_basis<M, kBasis>(g, v, row, jo, eo, inv_r, inv_tau, bo);
+                } else {
 #pragma unroll
-                for (int m = 0; m < M; ++m) bo[m] = 0.f;
+                    for (int m = 0; m < M; ++m) bo[m] = 0.f;
+                }
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int us = 0; us < SB; ++us)
 #pragma unroll
                 for (int m = 0; m < M; ++m) {
-                    const float bm = __shfl(bo[m], rl + 16 * u, 64);
+                    const float bm = __shfl(bo[m], rl + 16 * (u0 + us), 64);
 #pragma unroll
-                    for (int t = 0; t < CG; ++t) acc[m][t] += bm * f[u][t];
+                    for (int t = 0; t < CG; ++t) acc[m][t] += bm * f[us][t];
                 }
+            }
         }
 
         // ---- Y rows of the tile = G W on the matrix cores
@@ -810,8 +846,10 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     const int32_t t_end = (int32_t)((int64_t)(x + 1) * n_tiles / X);
     const int32_t n_my = t_first < t_end ? (t_end - t_first + gx - 1) / gx : 0;
 
-    // row bounds of the gather's next tile, loaded one tile ahead
-    int32_t bound = n_my > 0 ? load_bound<RPW>(col_ptr, n_in, t_first * TR + w * RPW) : 0;
+    // row bounds (and first neighbour indices) of the gather's next tile,
+    // loaded one tile ahead
+    GatherAhead ahead{n_my > 0 ? load_bound<RPW>(col_ptr, n_in, t_first * TR + w * RPW) : 0, 0,
+                      false};
     auto load_tile = [&](int32_t s, int buf) {
         const int32_t row0 = (t_first + s * gx) * TR;
         if (dW_part) {  // F rows of the tile, row-major (zero past the last row), 16 B per load
@@ -838,9 +876,9 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
             }
         }
         const int32_t next = s + 1 < n_my ? (t_first + (s + 1) * gx) * TR + w * RPW : -1;
-        bound = gather_rows<M, CO, kBasis, kBf, kBf, true, RPW, true>(
+        ahead = gather_rows<M, CO, kBasis, kBf, kBf, true, RPW, true>(
             row0 + w * RPW, n_in, col_ptr, row_idx, perm, v, g, dY, Ds[buf], SD, w * RPW,
-            stage[w], inv_r, inv_tau, bound, next);
+            stage[w], inv_r, inv_tau, ahead, next);
     };
 
     // The two roles run separate loops (so the matrix waves' dW accumulators
