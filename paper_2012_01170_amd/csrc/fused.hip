@@ -198,6 +198,10 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
     constexpr int RPB_ = 64 / LPR;
     constexpr int RPB = RPB_ < RPW ? RPB_ : RPW;   // rows in flight at once
     constexpr int NB = (RPW + RPB - 1) / RPB;      // rows per lane group
+    // pipelined, with fewer rows than lane groups: SPL groups share a row,
+    // group part p taking its edges rs + p, rs + p + SPL, ...; the partial
+    // sums are added across the groups at the end
+    constexpr int SPL = (kPipelined && RPB_ > RPW) ? RPB_ / RPW : 1;
     // edges per row loaded together: NB * U feature loads in flight per lane
     // (pipelined), or 4 per row with the rows taken one after another
     constexpr int UP = 32 / (NB * VEC) > 1 ? 32 / (NB * VEC) : 1;
@@ -205,6 +209,8 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
     const int lane = threadIdx.x & 63;
     const int slot = lane / LPR;
     const int cg = lane % LPR;
+    const int part = slot / RPB;                   // < SPL
+    const int rslot = slot % RPB;
 
     if (lane <= RPW) st.bounds[lane] = pre.bound;
     const int32_t next_bound =
@@ -214,8 +220,8 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
     int32_t rs[NB], re[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-        const int lr = b * RPB + slot;
-        const bool own = slot < RPB && lr < RPW;
+        const int lr = b * RPB + rslot;
+        const bool own = slot < RPB * SPL && lr < RPW;
         rs[b] = own ? st.bounds[lr] : 0;
         re[b] = own ? st.bounds[lr + 1] : 0;
     }
@@ -291,9 +297,13 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
         int32_t steps = 0;
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
-            pos[b] = rs[b] > c0 ? rs[b] : c0;
+            // this part's first edge at or after the chunk start
+            const int32_t lo = rs[b] > c0 ? rs[b] : c0;
+            const int32_t d = lo - (rs[b] + part);
+            pos[b] = rs[b] + part + (d > 0 ? (d + SPL - 1) / SPL : 0) * SPL;
             hi[b] = re[b] < c0 + 64 ? re[b] : c0 + 64;
-            const int32_t n = hi[b] > pos[b] ? (hi[b] - pos[b] + U - 1) / U : 0;
+            const int32_t mine = hi[b] > pos[b] ? (hi[b] - pos[b] + SPL - 1) / SPL : 0;
+            const int32_t n = (mine + U - 1) / U;
             steps = n > steps ? n : steps;
         }
         float f[NB][U][VEC];
@@ -303,7 +313,7 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
             for (int b = 0; b < NB; ++b)
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
-                    q[b][u] = pos[b] + u < hi[b] ? pos[b] + u - c0 : 64;
+                    q[b][u] = pos[b] + u * SPL < hi[b] ? pos[b] + u * SPL - c0 : 64;
                     load_row_vec<C, VEC, kXbf>(Xv, st.nb[q[b][u]], cg, f[b][u]);
                 }
         };
@@ -337,10 +347,19 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
 #pragma unroll
                         for (int k = 0; k < VEC; ++k) acc[b][m][k] += vm * f[b][u][k];
                     }
-                pos[b] += U;
+                pos[b] += U * SPL;
             }
         }
         wave_lds_sync();
+    }
+    if constexpr (SPL > 1) {
+        // add the parts of each row (every lane of the row ends with the same sum)
+#pragma unroll
+        for (int d = RPB * LPR; d < RPB * LPR * SPL; d <<= 1)
+#pragma unroll
+            for (int m = 0; m < M; ++m)
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) acc[0][m][k] += __shfl_xor(acc[0][m][k], d, 64);
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
