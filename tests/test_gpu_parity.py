@@ -298,3 +298,46 @@ def test_transpose_of_wide_patterns(n_cols):
     assert np.array_equal(csc.col_ptr.cpu().numpy(), cp)
     assert np.array_equal(csc.row_idx[:len(ci)].cpu().numpy(), ri)
     assert np.array_equal(csc.edge_perm[:len(ci)].cpu().numpy(), perm)
+
+
+@pytest.mark.parametrize("half_extent", [0, 1, 2, 3])
+def test_event_search_block_sizes(half_extent):
+    """1x1 and 3x3 blocks take the stored-run sweep, 5x5 and 7x7 the per-event bisection.
+
+    A small sensor with a hot pixel gives long per-pixel lists and rows.
+    """
+    print(f"[events h={half_extent}]", flush=True)
+    rng = np.random.default_rng(40 + half_extent)
+    n, W, H = 6000, 9, 7
+    px = rng.integers(0, W, size=n).astype(np.int32)
+    py = rng.integers(0, H, size=n).astype(np.int32)
+    hot = rng.random(n) < 0.2
+    px[hot], py[hot] = 4, 3
+    t = np.sort(rng.integers(0, 40_000, size=n)).astype(np.int32)
+    window = 900
+    rp, ci = oracle.events_csr(px, py, t, window, half_extent, W, H)
+    csr = G.sbc.neighbour_search_events(G.dev(px), G.dev(py), G.dev(t), W, H, window,
+                                        half_extent=half_extent)
+    assert csr.nnz == len(ci)
+    assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
+    assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+
+
+def test_transpose_by_radix_sort():
+    """Patterns of 2^21 edges or more are transposed by the radix sort; trailing
+    columns without edges must still get their (empty) ranges."""
+    rng = np.random.default_rng(77)
+    n_rows, n_cols = 300_000, 160_000
+    lens = rng.integers(4, 11, size=n_rows)
+    rp = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    assert rp[-1] >= 1 << 21
+    # columns drawn from the first 120k only: the last 40k columns stay empty
+    starts = rng.integers(0, 120_000 - 12, size=n_rows)
+    ci = np.concatenate([s + np.sort(rng.choice(12, size=k, replace=False))
+                         for s, k in zip(starts, lens)]).astype(np.int32)
+    csr = G.sbc.CSR(G.dev(rp), G.dev(ci), n_rows, n_cols, len(ci))
+    csc = G.sbc.csr_transpose(csr)
+    cp, ri, perm = oracle.csr_transpose(rp, ci, n_cols)
+    assert np.array_equal(csc.col_ptr.cpu().numpy(), cp)
+    assert np.array_equal(csc.row_idx[:len(ci)].cpu().numpy(), ri)
+    assert np.array_equal(csc.edge_perm[:len(ci)].cpu().numpy(), perm)
