@@ -800,24 +800,38 @@ __global__ void __launch_bounds__(kRegWaves * 64)
 }
 
 // ================================================================ backward, wave-specialised
-// Persistent blocks of eight waves over tiles of 32 input rows.  Waves 0-3
-// gather tile s+1 (D rows through the transposed pattern, and F rows) into
-// one half of a double-buffered LDS tile while waves 4-7 run the matrix work
-// of tile s on the other half (dF = D Wt, dW += F^T D); one block barrier per
-// step hands the halves over, so the gathers' memory latency overlaps the
-// matrix cores' work.
-constexpr int kWsMma = 4;
-constexpr int kWsTR = 32;
+// Persistent blocks over tiles of TR input rows, with the waves in two roles:
+// NG gather waves build tile s+1 (D rows through the transposed pattern, and
+// F rows) in one half of a double-buffered LDS tile while NM matrix waves run
+// the matrix work of tile s on the other half (dF = D Wt, dW += F^T D); one
+// block barrier per step hands the halves over, so the gathers' memory
+// latency overlaps the matrix cores' work.  The matrix waves read Wt from
+// memory or from registers (their slice, loaded once).
+enum WLoc { kWGlobal = 0, kWRegs = 1 };
 
-// Gather waves of the wave-specialised kernels: eight where the kernel's
-// registers allow twelve waves per CU (narrow float32 rows), else four.
+// Per shape: waves of each role, tile rows and where Wt lives, sized so that
+// the registers allow all waves on one CU and the LDS tiles fit:
+//   narrow float32 rows   8 + 4 waves, 32 rows, Wt slice in registers;
+//   otherwise             4 + 4 waves, 32 rows, Wt slice in registers if it
+//                         takes at most 64 of them, else from memory.
+// (Measured on the 64-channel shapes: 8 + 8 waves with 16-row float32 tiles,
+// or with Wt in LDS for bf16, ran slower than 4 + 4.)
+struct WsCfg {
+    int ng, nm, tr, wloc;
+};
+
 template <int M, int CI, int CO, bool kBf>
-constexpr int ws_gather_waves() {
-    return (!kBf && CI <= 32 && CO <= 32) ? 8 : 4;
+constexpr WsCfg ws_cfg() {
+    if (!kBf && CI <= 32 && CO <= 32) return WsCfg{8, 4, 32, kWRegs};
+    // 16 columns of Wt per matrix wave (one dF column block), K2 = M*CO rows
+    return WsCfg{4, 4, 32, (kBf ? M * CO <= 512 : M * CO <= 256) ? kWRegs : kWGlobal};
 }
 
 template <int M, int CI, int CO, int kBasis, bool kBf,
-          int kWsGather = ws_gather_waves<M, CI, CO, kBf>()>
+          int kWsGather = ws_cfg<M, CI, CO, kBf>().ng,
+          int kWsMma = ws_cfg<M, CI, CO, kBf>().nm,
+          int kTR = ws_cfg<M, CI, CO, kBf>().tr,
+          int kWLoc = ws_cfg<M, CI, CO, kBf>().wloc>
 __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     bwd_ws_kernel(int32_t n_in, int32_t n_tiles, const int32_t *__restrict__ col_ptr,
                   const int32_t *__restrict__ row_idx, const int32_t *__restrict__ perm,
@@ -825,12 +839,13 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
                   const void *__restrict__ dY, const void *__restrict__ Wop,
                   float *__restrict__ dF, float *__restrict__ dW_part) {
     // dF == nullptr: no input gradient; dW_part == nullptr: no weight gradient
-    constexpr int TR = kWsTR;
+    constexpr int TR = kTR;
     constexpr int K2 = M * CO;
     constexpr int SD = K2 + (kBf ? 8 : 4);
     constexpr int SF = CI + (kBf ? 8 : 4);
     constexpr int RPW = TR / kWsGather;
-    static_assert(CI % 16 == 0 && CO % 16 == 0, "shape");
+    static_assert(CI % 16 == 0 && CO % 16 == 0 && TR % kWsGather == 0, "shape");
+    static_assert(!kBf || TR % 32 == 0, "bf16 dW takes 32 rows per MFMA k-step");
     // dF tile [TR, CI]: 16x16 blocks over the matrix waves
     constexpr int NRB = TR / 16, NCB = CI / 16;
     constexpr int NCBW = NCB < kWsMma ? NCB : kWsMma;
@@ -838,7 +853,7 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     constexpr int NRG = NRG_ < NRB ? NRG_ : NRB;  // waves past NCBW * NRG have no dF block
     static_assert(NCB % NCBW == 0 && NRB % NRG == 0, "dF split");
     constexpr int WCB = NCB / NCBW, WRB = NRB / NRG;
-    // dW [CI, K2]: each matrix wave owns K2/4 columns, all CI rows
+    // dW [CI, K2]: each matrix wave owns K2/NM columns, all CI rows
     constexpr int NWB = (K2 / 16) / kWsMma;
     constexpr int NIB = CI / 16;
     static_assert((K2 / 16) % kWsMma == 0, "dW split");
@@ -920,8 +935,9 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
 #pragma unroll
         for (int b = 0; b < NWB; ++b) accw[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
     // the wave's slice of Wt for dF, held in registers for the whole kernel
-    // when it takes at most 64 of them (it is the same for every tile)
-    constexpr bool kWreg = kBf ? (K2 * WCB <= 512) : (K2 * WCB <= 256);
+    // (it is the same for every tile)
+    constexpr bool kWreg = kWLoc == kWRegs;
+    static_assert(!kWreg || (kBf ? K2 * WCB <= 512 : K2 * WCB <= 256), "Wt slice too large");
     constexpr int KS = kBf ? K2 / 32 : K2 / 4;  // MFMA k-steps of the dF product
     using BT = typename std::conditional<kBf, bf16x8, float>::type;
     BT bw[kWreg ? KS : 1][WCB];
@@ -1223,9 +1239,13 @@ BwdFn find_bwd(const Shape &s, int basis_mode) {
     return nullptr;
 }
 
-int ws_gather_waves_rt(int32_t M, int32_t CI, int32_t CO, bool bf) {
-    (void)M;
-    return (!bf && CI <= 32 && CO <= 32) ? 8 : 4;
+// ws_cfg() of a shape listed for the fused kernels
+WsCfg ws_cfg_rt(int32_t M, int32_t CI, int32_t CO, bool bf) {
+#define SBC_X(m_, ci_, co_, bf_) \
+    if (M == m_ && CI == ci_ && CO == co_ && bf == bf_) return ws_cfg<m_, ci_, co_, bf_>();
+    SBC_BWD_SHAPES(SBC_X)
+#undef SBC_X
+    return WsCfg{4, 4, 32, kWGlobal};
 }
 
 int basis_mode_of(const float *v, const sbc_geometry *g) {
@@ -1376,9 +1396,10 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
         SBC_TRY(launch_perm(W, true, true, M, CI, CO, CO, K2, 1, wt, stream));
     else
         SBC_TRY(launch_perm(W, false, false, M, CI, CO, (int64_t)CO * CI, 1, CI, wt, stream));
-    const int TR = kWsTR;
+    const WsCfg cfg = ws_cfg_rt(M, CI, CO, bf);
+    const int TR = cfg.tr;
     const int32_t n_tiles = (n_in + TR - 1) / TR;
-    const int nw = ws_gather_waves_rt(M, CI, CO, bf) + kWsMma;
+    const int nw = cfg.ng + cfg.nm;
     int blocks = device_cus();
     if (blocks > kMaxBlocksBwd) blocks = kMaxBlocksBwd;
     if (blocks > n_tiles) blocks = n_tiles;
