@@ -51,7 +51,7 @@ DESCRIPTIONS = {
 SRC_DIR = os.path.join(ROOT, "paper_2012_01170_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
 # device function -> the name the library's trace hook gives its launch
-TRACE_NAME = {"bwd_fused_kernel": "bwd_fused", "fwd_fused_kernel": "fwd_fused",
+TRACE_NAME = {"bwd_ws_kernel": "bwd_fused", "fwd_fused_kernel": "fwd_fused",
               "fwd_reg_kernel": "fwd_fused", "dw_reduce_kernel": "bwd_dw_reduce"}
 
 
