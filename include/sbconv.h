@@ -169,7 +169,10 @@ int32_t sbc_basis_size(sbc_basis basis);
  *                                        caller checks row_ptr[n_out] <=
  *                                        col_capacity before using col_idx.
  * ------------------------------------------------------------------------ */
-size_t sbc_points_workspace_size(int32_t n_in, int32_t n_out, int32_t n_batch);
+/* Workspace of a point search with these sizes and this k_cap (a capped
+ * search with 1 <= k_cap <= 512 visits the candidates once, into n_out rows of
+ * k_cap entries held in the workspace). */
+size_t sbc_points_workspace_size(int32_t n_in, int32_t n_out, int32_t n_batch, int32_t k_cap);
 sbc_status sbc_neighbour_search_points(const float *x_in, int32_t n_in, const int32_t *in_splits,
                                        const float *x_out, int32_t n_out,
                                        const int32_t *out_splits, int32_t n_batch, float radius,

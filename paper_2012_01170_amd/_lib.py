@@ -72,7 +72,7 @@ _SIGS = {
     "sbc_last_error": (ctypes.c_char_p, []),
     "sbc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "sbc_basis_size": (_i32, [ctypes.c_int]),
-    "sbc_points_workspace_size": (_sz, [_i32, _i32, _i32]),
+    "sbc_points_workspace_size": (_sz, [_i32, _i32, _i32, _i32]),
     "sbc_neighbour_search_points": (ctypes.c_int, [_vp, _i32, _vp, _vp, _i32, _vp, _i32, _f32, _i32,
                                                    _vp, _vp, _i64, _i64_p, _vp, _sz, _vp]),
     "sbc_events_workspace_size": (_sz, [_i32, _i32, _i32]),

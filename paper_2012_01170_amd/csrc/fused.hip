@@ -396,55 +396,69 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
 
 // acc[u][t] += A_tile[16 rb_u .., :] x B[:, 16 cb_t ..] for the 16x16 blocks of
 // one wave (rb_u = wr + NRG u, cb_t = wc + NCBW t).  A sits in LDS (row stride
-// S elements), B [K, NCOL] in global memory (float32) or, for bf16, as
-// B^T [NCOL, K].  The B fragments of k-groups alternate between two register
-// sets, so the loads of the next group are in flight while the current group
-// is multiplied (no copies between the sets, which would force a wait).
-template <int NCOL, int WCB, int NCBW>
-__device__ __forceinline__ void load_b_f32(const float *__restrict__ B, int k0, int wc, int lr,
-                                           int lc, float (&b)[8][WCB]) {
+// S elements), B in global memory as B^T [NCOL, K].  The B fragments of
+// k-groups alternate between two register sets, so the loads of the next
+// group are in flight while the current group is multiplied (no copies
+// between the sets, which would force a wait).
+//
+// float32 variant with B given transposed (Bt [NCOL][K]): within each group of
+// 32 k, lane group lr takes k0 + 8 lr + s (s = 0..7), a permutation of the
+// contraction index under which a lane's eight A values and eight B values
+// are consecutive floats, loaded 16 bytes at a time.  The groups' B values
+// alternate between two register sets as above.
+template <int K, int WCB, int NCBW>
+__device__ __forceinline__ void load_bt_f32(const float *__restrict__ Bt, int k0, int wc, int lr,
+                                            int lc, float4 (&b)[2][WCB]) {
 #pragma unroll
-    for (int s = 0; s < 8; ++s)
-#pragma unroll
-        for (int t = 0; t < WCB; ++t) b[s][t] = B[(k0 + 4 * s + lr) * NCOL + 16 * (wc + NCBW * t) + lc];
-}
-
-template <int S, int WRB, int WCB, int NRG>
-__device__ __forceinline__ void mma_group_f32(const float *As, int k0, int wr, int lr, int lc,
-                                              const float (&b)[8][WCB], floatx4 (&acc)[WRB][WCB]) {
-#pragma unroll
-    for (int s = 0; s < 8; ++s) {
-        float a[WRB];
-#pragma unroll
-        for (int u = 0; u < WRB; ++u) a[u] = As[(16 * (wr + NRG * u) + lc) * S + k0 + 4 * s + lr];
-#pragma unroll
-        for (int u = 0; u < WRB; ++u)
-#pragma unroll
-            for (int t = 0; t < WCB; ++t)
-                acc[u][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u], b[s][t], acc[u][t], 0, 0, 0);
+    for (int t = 0; t < WCB; ++t) {
+        const float *p = Bt + (int64_t)(16 * (wc + NCBW * t) + lc) * K + k0 + 8 * lr;
+        b[0][t] = *reinterpret_cast<const float4 *>(p);
+        b[1][t] = *reinterpret_cast<const float4 *>(p + 4);
     }
 }
 
-template <int K, int NCOL, int S, int WRB, int WCB, int NCBW, int NRG>
-__device__ __forceinline__ void mfma_lds_x_global_f32(const float *As, const float *__restrict__ B,
-                                                      int wr, int wc,
-                                                      floatx4 (&acc)[WRB][WCB]) {
-    constexpr int KG = 32;  // 8 MFMA k-steps of 4
+template <int S, int WRB, int WCB, int NRG>
+__device__ __forceinline__ void mma_group_f32t(const float *As, int k0, int wr, int lr, int lc,
+                                               const float4 (&b)[2][WCB],
+                                               floatx4 (&acc)[WRB][WCB]) {
+    float4 a[WRB][2];
+#pragma unroll
+    for (int u = 0; u < WRB; ++u) {
+        const float *p = As + (16 * (wr + NRG * u) + lc) * S + k0 + 8 * lr;
+        a[u][0] = *reinterpret_cast<const float4 *>(p);
+        a[u][1] = *reinterpret_cast<const float4 *>(p + 4);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int u = 0; u < WRB; ++u)
+#pragma unroll
+                for (int t = 0; t < WCB; ++t)
+                    acc[u][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][h][q], b[h][t][q],
+                                                                      acc[u][t], 0, 0, 0);
+}
+
+template <int K, int S, int WRB, int WCB, int NCBW, int NRG>
+__device__ __forceinline__ void mfma_lds_x_global_f32t(const float *As,
+                                                       const float *__restrict__ Bt, int wr,
+                                                       int wc, floatx4 (&acc)[WRB][WCB]) {
+    constexpr int KG = 32;
     static_assert(K % (2 * KG) == 0, "K must be a multiple of 64");
     const int lane = threadIdx.x & 63;
     const int lr = lane >> 4, lc = lane & 15;
-    float b0[8][WCB], b1[8][WCB];
-    load_b_f32<NCOL, WCB, NCBW>(B, 0, wc, lr, lc, b0);
+    float4 b0[2][WCB], b1[2][WCB];
+    load_bt_f32<K, WCB, NCBW>(Bt, 0, wc, lr, lc, b0);
 #pragma unroll 1
     for (int k0 = 0; k0 < K; k0 += 2 * KG) {
-        load_b_f32<NCOL, WCB, NCBW>(B, k0 + KG, wc, lr, lc, b1);
-        __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the MFMAs
-        mma_group_f32<S, WRB, WCB, NRG>(As, k0, wr, lr, lc, b0, acc);
-        // the last iteration reloads the final group (harmless, no branch)
-        const int kn = k0 + 2 * KG < K ? k0 + 2 * KG : K - KG;
-        load_b_f32<NCOL, WCB, NCBW>(B, kn, wc, lr, lc, b0);
+        load_bt_f32<K, WCB, NCBW>(Bt, k0 + KG, wc, lr, lc, b1);
         __builtin_amdgcn_sched_barrier(0);
-        mma_group_f32<S, WRB, WCB, NRG>(As, k0 + KG, wr, lr, lc, b1, acc);
+        mma_group_f32t<S, WRB, WCB, NRG>(As, k0, wr, lr, lc, b0, acc);
+        const int kn = k0 + 2 * KG < K ? k0 + 2 * KG : K - KG;
+        load_bt_f32<K, WCB, NCBW>(Bt, kn, wc, lr, lc, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_group_f32t<S, WRB, WCB, NRG>(As, k0 + KG, wr, lr, lc, b1, acc);
     }
 }
 
@@ -560,7 +574,7 @@ __global__ void __launch_bounds__(kFwdWaves * 64, 2)
         for (int t = 0; t < WCB; ++t) acc[u][t] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     if constexpr (!kBf)
-        mfma_lds_x_global_f32<K, CO, S, WRB, WCB, NCBW, NRG>(
+        mfma_lds_x_global_f32t<K, S, WRB, WCB, NCBW, NRG>(
             Gs, static_cast<const float *>(Wop), wr, wc, acc);
     else
         mfma_lds_x_global_bf16<K, S, WRB, WCB, NCBW, NRG>(
@@ -952,8 +966,8 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
                         static_cast<const uint16_t *>(Wop) +
                         (int64_t)(16 * (wc + NCBW * t) + lc) * K2 + 32 * ks + 8 * lr);
                 else
-                    bw[ks][t] = static_cast<const float *>(Wop)[(4 * ks + lr) * CI +
-                                                                16 * (wc + NCBW * t) + lc];
+                    bw[ks][t] = static_cast<const float *>(
+                        Wop)[(int64_t)(16 * (wc + NCBW * t) + lc) * K2 + 4 * ks + lr];
             }
     }
     __syncthreads();
@@ -994,7 +1008,7 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
                         }
                     }
                 } else if constexpr (!kBf) {
-                    mfma_lds_x_global_f32<K2, CI, SD, WRB, WCB, NCBW, NRG>(
+                    mfma_lds_x_global_f32t<K2, SD, WRB, WCB, NCBW, NRG>(
                         D, static_cast<const float *>(Wop), wr, wc, acc);
                 } else {
                     mfma_lds_x_global_bf16<K2, SD, WRB, WCB, NCBW, NRG>(
@@ -1364,12 +1378,9 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
         trace_after("fwd_fused", stream);
         return SBC_OK;
     }
-    const void *Wop = W;
-    if (bf) {  // [CO, K] bf16: element (m, c, p) at p*K + m*CI + c
-        const int64_t K = (int64_t)M * CI;
-        SBC_TRY(launch_perm(W, true, true, M, CI, CO, CI, 1, K, ws, stream));
-        Wop = ws;
-    }
+    // W transposed, [CO, K]: element (m, c, p) at p*K + m*CI + c (float32 or bf16)
+    SBC_TRY(launch_perm(W, bf, bf, M, CI, CO, CI, 1, (int64_t)M * CI, ws, stream));
+    const void *Wop = ws;
     const int K = M * CI;
     const int TR = (K * (bf ? 2 : 4) * 64 <= 65536) ? 64 : 32;
     trace_before("fwd_fused", stream);
@@ -1391,11 +1402,8 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
     char *base = static_cast<char *>(ws);
     void *wt = base;
     float *part = reinterpret_cast<float *>(base + align_up((size_t)M * CI * CO * 4));
-    // Wt: float32 [K2, CI] (element (m,c,p) at (m*CO + p)*CI + c), or bf16 [CI, K2]
-    if (bf)
-        SBC_TRY(launch_perm(W, true, true, M, CI, CO, CO, K2, 1, wt, stream));
-    else
-        SBC_TRY(launch_perm(W, false, false, M, CI, CO, (int64_t)CO * CI, 1, CI, wt, stream));
+    // Wt [CI, K2], element (m, c, p) at c*K2 + m*CO + p (float32 or bf16)
+    SBC_TRY(launch_perm(W, bf, bf, M, CI, CO, CO, K2, 1, wt, stream));
     const WsCfg cfg = ws_cfg_rt(M, CI, CO, bf);
     const int TR = cfg.tr;
     const int32_t n_tiles = (n_in + TR - 1) / TR;

@@ -15,6 +15,10 @@
 //      truncated to the k_cap smallest by rank on (d2, j), and written in
 //      ascending j by rank on j.  Rows longer than the LDS stage rank against
 //      the candidate cells directly (same result, slower).
+// A capped search (1 <= k_cap <= kStage) instead runs the fill pass once,
+// before the scan, into rows of stride k_cap in the workspace (it also
+// writes the row lengths), and copies the rows into place after the scan, so
+// the candidates are visited once rather than twice.
 // The hash only prunes: buckets shared by distinct cells or clouds add
 // candidates that the exact distance and cloud-range tests reject.
 #include <cfloat>
@@ -195,7 +199,10 @@ __device__ __forceinline__ bool key_less(float da, int32_t ja, float db, int32_t
     return da < db || (da == db && ja < jb);
 }
 
-template <bool kFill>
+// kMode: 0 count pass; 1 fill pass into the CSR (row i at row_ptr[i]);
+// 2 fill pass into rows of stride k_cap (row i at i * k_cap, col_capacity =
+// n_out * k_cap), writing the row lengths too.
+template <int kMode>
 __global__ void __launch_bounds__(kWaves * 64)
     rows_kernel(const float *__restrict__ x_out, int32_t n_out,
                 const int32_t *__restrict__ in_splits, const int32_t *__restrict__ out_splits,
@@ -205,6 +212,7 @@ __global__ void __launch_bounds__(kWaves * 64)
                 int32_t *__restrict__ col_idx, int64_t col_capacity) {
     __shared__ int32_t s_start[kWaves][27];
     __shared__ int32_t s_off[kWaves][27];
+    constexpr bool kFill = kMode != 0;
     __shared__ float s_d2[kFill ? kWaves : 1][kFill ? kStage : 1];
     __shared__ int32_t s_j[kFill ? kWaves : 1][kFill ? kStage : 1];
     __shared__ int32_t s_keep[kFill ? kWaves : 1][kFill ? kStage : 1];
@@ -263,9 +271,10 @@ __global__ void __launch_bounds__(kWaves * 64)
         n += __popcll(mask);
     }
     wave_lds_sync();
-    const int32_t out0 = row_ptr[i];
+    const int32_t out0 = kMode == 2 ? i * k_cap : row_ptr[i];
     const bool capped = k_cap > 0 && n > k_cap;
     const int32_t n_keep = capped ? k_cap : n;
+    if (kMode == 2 && lane == 0) row_len[i] = n_keep;
 
     if (n <= kStage) {
         // keep flag: rank on (d2, j) below k_cap
@@ -362,6 +371,25 @@ __global__ void __launch_bounds__(kWaves * 64)
     }
 }
 
+// col_idx[row_ptr[i] + s] = rows[i * k_cap + s] for s < row_len[i]
+__global__ void compact_rows_kernel(const int32_t *__restrict__ rows,
+                                    const int32_t *__restrict__ row_len,
+                                    const int32_t *__restrict__ row_ptr, int32_t n_out,
+                                    int32_t k_cap, int32_t *__restrict__ col_idx,
+                                    int64_t col_capacity) {
+    const int64_t total = (int64_t)n_out * k_cap;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t i = (int32_t)(q / k_cap), sl = (int32_t)(q % k_cap);
+        if (sl < row_len[i]) {
+            const int64_t dst = (int64_t)row_ptr[i] + sl;
+            if (dst < col_capacity) col_idx[dst] = rows[q];
+        }
+    }
+}
+
+bool one_pass(int32_t k_cap) { return k_cap >= 1 && k_cap <= kStage; }
+
 uint32_t table_size_for(int32_t n_in) {
     uint32_t t = 1024;
     while (t < 2u * (uint32_t)(n_in > 0 ? n_in : 1) && t < (1u << 30)) t <<= 1;
@@ -375,12 +403,14 @@ struct PointsWs {
     int32_t *cursor;
     PointRec *table;
     int32_t *row_len;
+    int32_t *rows;  // capped one-pass search: n_out rows of stride k_cap
     int64_t *total;
     uint32_t *status;
     void *scan_ws;
 };
 
-PointsWs carve_points(void *base, int32_t n_in, int32_t n_out, int32_t /*n_batch*/, size_t *bytes) {
+PointsWs carve_points(void *base, int32_t n_in, int32_t n_out, int32_t /*n_batch*/,
+                      int32_t k_cap, size_t *bytes) {
     Carver cv(base);
     const uint32_t T = table_size_for(n_in);
     PointsWs w;
@@ -390,6 +420,7 @@ PointsWs carve_points(void *base, int32_t n_in, int32_t n_out, int32_t /*n_batch
     w.cursor = cv.take<int32_t>((size_t)T + 1);
     w.table = cv.take<PointRec>(n_in);
     w.row_len = cv.take<int32_t>(n_out);
+    w.rows = cv.take<int32_t>(one_pass(k_cap) ? (size_t)n_out * k_cap : 0);
     w.total = cv.take<int64_t>(2);
     w.status = cv.take<uint32_t>(4);
     int64_t m = (int64_t)T > (int64_t)n_out ? (int64_t)T : (int64_t)n_out;
@@ -403,9 +434,10 @@ PointsWs carve_points(void *base, int32_t n_in, int32_t n_out, int32_t /*n_batch
 
 using namespace sbc;
 
-extern "C" size_t sbc_points_workspace_size(int32_t n_in, int32_t n_out, int32_t n_batch) {
+extern "C" size_t sbc_points_workspace_size(int32_t n_in, int32_t n_out, int32_t n_batch,
+                                            int32_t k_cap) {
     size_t bytes = 0;
-    carve_points(nullptr, n_in < 0 ? 0 : n_in, n_out < 0 ? 0 : n_out, n_batch, &bytes);
+    carve_points(nullptr, n_in < 0 ? 0 : n_in, n_out < 0 ? 0 : n_out, n_batch, k_cap, &bytes);
     return bytes;
 }
 
@@ -424,7 +456,7 @@ extern "C" sbc_status sbc_neighbour_search_points(
     if (col_capacity < 0 || (col_capacity > 0 && !col_idx))
         return fail(SBC_ERR_INVALID_ARG, "col_idx is null or col_capacity < 0");
     size_t need = 0;
-    PointsWs ws = carve_points(workspace, n_in, n_out, n_batch, &need);
+    PointsWs ws = carve_points(workspace, n_in, n_out, n_batch, k_cap, &need);
     if (!workspace || workspace_bytes < need)
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_points_workspace_size()");
 
@@ -450,12 +482,19 @@ extern "C" sbc_status sbc_neighbour_search_points(
         SBC_LAUNCH_CHECK();
     }
     const int row_blocks = grid_for(n_out, kWaves);
+    const bool single = one_pass(k_cap);
     if (n_out > 0) {
         trace_before("points_count", stream);
-        hipLaunchKernelGGL((rows_kernel<false>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
-                           x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
-                           T - 1, ws.cell_start, ws.table, ws.row_len, (const int32_t *)nullptr,
-                           (int32_t *)nullptr, (int64_t)0);
+        if (single)
+            hipLaunchKernelGGL((rows_kernel<2>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
+                               x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
+                               T - 1, ws.cell_start, ws.table, ws.row_len,
+                               (const int32_t *)nullptr, ws.rows, (int64_t)n_out * k_cap);
+        else
+            hipLaunchKernelGGL((rows_kernel<0>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
+                               x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
+                               T - 1, ws.cell_start, ws.table, ws.row_len,
+                               (const int32_t *)nullptr, (int32_t *)nullptr, (int64_t)0);
         SBC_LAUNCH_CHECK();
         trace_after("points_count", stream);
     }
@@ -478,10 +517,19 @@ extern "C" sbc_status sbc_neighbour_search_points(
     }
     if (n_out > 0 && col_capacity > 0) {
         trace_before("points_fill", stream);
-        hipLaunchKernelGGL((rows_kernel<true>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
-                           x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
-                           T - 1, ws.cell_start, ws.table, ws.row_len, row_ptr, col_idx,
-                           col_capacity);
+        if (single) {
+            const int64_t total = (int64_t)n_out * k_cap;
+            int64_t g = (total + 255) / 256;
+            if (g > 8192) g = 8192;
+            hipLaunchKernelGGL(compact_rows_kernel, dim3((unsigned)g), dim3(256), 0, stream,
+                               ws.rows, ws.row_len, row_ptr, n_out, k_cap, col_idx,
+                               col_capacity);
+        } else {
+            hipLaunchKernelGGL((rows_kernel<1>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
+                               x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap,
+                               inv_h, T - 1, ws.cell_start, ws.table, ws.row_len, row_ptr,
+                               col_idx, col_capacity);
+        }
         SBC_LAUNCH_CHECK();
         trace_after("points_fill", stream);
     }

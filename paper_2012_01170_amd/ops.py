@@ -127,7 +127,7 @@ def neighbour_search_points(x_in, in_splits, x_out, out_splits, radius: float, k
         else:
             col_capacity = max(1, 16 * n_out)
     lib = L.lib()
-    ws = _Workspace(lib.sbc_points_workspace_size(n_in, n_out, n_batch), dev)
+    ws = _Workspace(lib.sbc_points_workspace_size(n_in, n_out, n_batch, int(k_cap)), dev)
     row_ptr = torch.empty(n_out + 1, dtype=torch.int32, device=dev)
     stream = _stream(dev)
     for _ in range(2):

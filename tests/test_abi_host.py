@@ -36,9 +36,11 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_workspace_queries(lib):
-    a = lib.sbc_points_workspace_size(32768, 32768, 32)
-    b = lib.sbc_points_workspace_size(1024, 256, 1)
+    a = lib.sbc_points_workspace_size(32768, 32768, 32, 0)
+    b = lib.sbc_points_workspace_size(1024, 256, 1, 0)
     assert a > b > 0 and a % 256 == 0
+    # a capped search keeps n_out rows of k_cap entries
+    assert lib.sbc_points_workspace_size(32768, 32768, 32, 32) >= a + 32768 * 32 * 4
     assert lib.sbc_events_workspace_size(300000, 128, 128) > 300000 * 4 * 5
     assert lib.sbc_transpose_workspace_size(1000, 5000) >= 2 * 5000 * 4
     s1 = lib.sbc_conv_workspace_size(1000, 1000, 8000, 8, 16, 16, L.SBC_F32, L.SBC_ORDER_SPMM_FIRST)
