@@ -404,8 +404,12 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
 // float32 variant with B given transposed (Bt [NCOL][K]): within each group of
 // 32 k, lane group lr takes k0 + 8 lr + s (s = 0..7), a permutation of the
 // contraction index under which a lane's eight A values and eight B values
-// are consecutive floats, loaded 16 bytes at a time.  The groups' B values
-// alternate between two register sets as above.
+// are consecutive floats, loaded 16 bytes at a time.  The k loop is unrolled
+// in full with the loads software-pipelined: the B fragments of group g + 2
+// (from global memory, one L2 round trip) and the A fragments of group g + 1
+// (from LDS) are issued before the 16 x WRB x WCB products of group g, in
+// register sets of their own, so no product waits on a load issued just
+// before it.
 template <int K, int WCB, int NCBW>
 __device__ __forceinline__ void load_bt_f32(const float *__restrict__ Bt, int k0, int wc, int lr,
                                             int lc, float4 (&b)[2][WCB]) {
@@ -417,17 +421,21 @@ __device__ __forceinline__ void load_bt_f32(const float *__restrict__ Bt, int k0
     }
 }
 
-template <int S, int WRB, int WCB, int NRG>
-__device__ __forceinline__ void mma_group_f32t(const float *As, int k0, int wr, int lr, int lc,
-                                               const float4 (&b)[2][WCB],
-                                               floatx4 (&acc)[WRB][WCB]) {
-    float4 a[WRB][2];
+template <int S, int WRB, int NRG>
+__device__ __forceinline__ void load_a_f32(const float *As, int k0, int wr, int lr, int lc,
+                                           float4 (&a)[WRB][2]) {
 #pragma unroll
     for (int u = 0; u < WRB; ++u) {
         const float *p = As + (16 * (wr + NRG * u) + lc) * S + k0 + 8 * lr;
         a[u][0] = *reinterpret_cast<const float4 *>(p);
         a[u][1] = *reinterpret_cast<const float4 *>(p + 4);
     }
+}
+
+template <int WRB, int WCB>
+__device__ __forceinline__ void mma_group_f32t(const float4 (&a)[WRB][2],
+                                               const float4 (&b)[2][WCB],
+                                               floatx4 (&acc)[WRB][WCB]) {
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -445,20 +453,22 @@ __device__ __forceinline__ void mfma_lds_x_global_f32t(const float *As,
                                                        const float *__restrict__ Bt, int wr,
                                                        int wc, floatx4 (&acc)[WRB][WCB]) {
     constexpr int KG = 32;
-    static_assert(K % (2 * KG) == 0, "K must be a multiple of 64");
+    constexpr int NG = K / KG;
+    static_assert(K % KG == 0 && NG >= 2, "K must be a multiple of 32, at least 64");
     const int lane = threadIdx.x & 63;
     const int lr = lane >> 4, lc = lane & 15;
-    float4 b0[2][WCB], b1[2][WCB];
-    load_bt_f32<K, WCB, NCBW>(Bt, 0, wc, lr, lc, b0);
-#pragma unroll 1
-    for (int k0 = 0; k0 < K; k0 += 2 * KG) {
-        load_bt_f32<K, WCB, NCBW>(Bt, k0 + KG, wc, lr, lc, b1);
+    float4 b[3][2][WCB];
+    float4 a[2][WRB][2];
+    load_bt_f32<K, WCB, NCBW>(Bt, 0, wc, lr, lc, b[0]);
+    load_bt_f32<K, WCB, NCBW>(Bt, KG, wc, lr, lc, b[1]);
+    load_a_f32<S, WRB, NRG>(As, 0, wr, lr, lc, a[0]);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+        if (g + 2 < NG) load_bt_f32<K, WCB, NCBW>(Bt, (g + 2) * KG, wc, lr, lc, b[(g + 2) % 3]);
+        if (g + 1 < NG) load_a_f32<S, WRB, NRG>(As, (g + 1) * KG, wr, lr, lc, a[(g + 1) % 2]);
         __builtin_amdgcn_sched_barrier(0);
-        mma_group_f32t<S, WRB, WCB, NRG>(As, k0, wr, lr, lc, b0, acc);
-        const int kn = k0 + 2 * KG < K ? k0 + 2 * KG : K - KG;
-        load_bt_f32<K, WCB, NCBW>(Bt, kn, wc, lr, lc, b0);
+        mma_group_f32t<WRB, WCB>(a[g % 2], b[g % 3], acc);
         __builtin_amdgcn_sched_barrier(0);
-        mma_group_f32t<S, WRB, WCB, NRG>(As, k0 + KG, wr, lr, lc, b1, acc);
     }
 }
 
@@ -1030,20 +1040,34 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
             if (dW_part) {
                 const DT *Fb = Fs[buf];
                 if constexpr (!kBf) {
-#pragma unroll 2
-                    for (int k0 = 0; k0 < TR; k0 += 4) {
-                        const int kk = k0 + (lane >> 4);
-                        float a[NIB];
+                    // k-steps of 4 tile rows: in step k lane group lr takes
+                    // row (k & 3) + 16 (k >> 2) + 4 lr, so the four rows of
+                    // one read sit 4 row strides apart (16 banks apart for
+                    // the padded strides); the operands of step k + 1 are
+                    // read from LDS while the products of step k run
+                    static_assert(TR % 16 == 0, "row permutation covers 16-row blocks");
+                    const float *Fp = Fb + 4 * (lane >> 4) * SF + (lane & 15);
+                    const float *Dp = D + 4 * (lane >> 4) * SD + 16 * mw * NWB + (lane & 15);
+                    float a[2][NIB], bb[2][NWB];
+                    auto load_step = [&](int r0, float(&aa)[NIB], float(&bq)[NWB]) {
 #pragma unroll
-                        for (int ib = 0; ib < NIB; ++ib) a[ib] = Fb[kk * SF + 16 * ib + (lane & 15)];
+                        for (int ib = 0; ib < NIB; ++ib) aa[ib] = Fp[r0 * SF + 16 * ib];
 #pragma unroll
-                        for (int nb = 0; nb < NWB; ++nb) {
-                            const float bb = D[kk * SD + 16 * (mw * NWB + nb) + (lane & 15)];
+                        for (int nb = 0; nb < NWB; ++nb) bq[nb] = Dp[r0 * SD + 16 * nb];
+                    };
+                    auto row0_of = [](int k) { return (k & 3) + 16 * (k >> 2); };
+                    load_step(0, a[0], bb[0]);
+#pragma unroll
+                    for (int k = 0; k < TR / 4; ++k) {
+                        if (k + 1 < TR / 4) load_step(row0_of(k + 1), a[(k + 1) & 1], bb[(k + 1) & 1]);
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int nb = 0; nb < NWB; ++nb)
 #pragma unroll
                             for (int ib = 0; ib < NIB; ++ib)
                                 accw[ib][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                                    a[ib], bb, accw[ib][nb], 0, 0, 0);
-                        }
+                                    a[k & 1][ib], bb[k & 1][nb], accw[ib][nb], 0, 0, 0);
+                        __builtin_amdgcn_sched_barrier(0);
                     }
                 } else {
 #pragma unroll

@@ -75,6 +75,35 @@ __device__ __forceinline__ int32_t cloud_of(const int32_t *splits, int32_t n_bat
     return lo;
 }
 
+// Cloud b of the output index i, the same on every lane of the wave, and the
+// input range [*j_lo, *j_hi) of that cloud.  The splits are read across the
+// wave, 64 at a time, and b counts the interior splits at or below i, which
+// for non-decreasing splits is the bisection's answer.  With fewer than 64
+// clouds the input splits are read in the same round trip and picked out by
+// lane.
+__device__ __forceinline__ int32_t wave_cloud(const int32_t *__restrict__ out_splits,
+                                              const int32_t *__restrict__ in_splits,
+                                              int32_t n_batch, int32_t i, int32_t *j_lo,
+                                              int32_t *j_hi) {
+    const int lane = threadIdx.x & 63;
+    if (n_batch < 64) {
+        const int32_t so = lane <= n_batch ? out_splits[lane] : 0;
+        const int32_t si = lane <= n_batch ? in_splits[lane] : 0;
+        const int32_t b = __popcll(__ballot(lane >= 1 && lane < n_batch && so <= i));
+        *j_lo = __shfl(si, b, 64);
+        *j_hi = __shfl(si, b + 1, 64);
+        return b;
+    }
+    int32_t b = 0;
+    for (int32_t base = 1; base < n_batch; base += 64) {
+        const int32_t k = base + lane;
+        b += __popcll(__ballot(k < n_batch && out_splits[k] <= i));
+    }
+    *j_lo = in_splits[b];
+    *j_hi = in_splits[b + 1];
+    return b;
+}
+
 // Canonical float32 squared distance: no contraction, fixed association.
 __device__ __forceinline__ float sq_dist(float ax, float ay, float az, float bx, float by,
                                          float bz) {
@@ -94,11 +123,19 @@ __global__ void init_kernel(int32_t *__restrict__ cell_count, uint32_t table_siz
 
 // Cell key of every input point (and, in the first n_batch + 1 threads, the
 // check that the splits run from 0 to n_in / n_out without decreasing).
-__global__ void key_kernel(const float *__restrict__ x_in, int32_t n_in,
-                           const int32_t *__restrict__ in_splits,
-                           const int32_t *__restrict__ out_splits, int32_t n_out, int32_t n_batch,
-                           double inv_h, uint32_t table_mask, uint32_t *__restrict__ keys,
-                           int32_t *__restrict__ counts, uint32_t *status) {
+constexpr int kKeyThreads = 256;
+constexpr int kSplitsInLds = 1024;     // key pass: splits bisected in LDS up to this many
+
+__global__ void __launch_bounds__(kKeyThreads)
+    key_kernel(const float *__restrict__ x_in, int32_t n_in,
+               const int32_t *__restrict__ in_splits, const int32_t *__restrict__ out_splits,
+               int32_t n_out, int32_t n_batch, double inv_h, uint32_t table_mask,
+               uint32_t *__restrict__ keys, int32_t *__restrict__ counts, uint32_t *status) {
+    __shared__ int32_t s_splits[kSplitsInLds];
+    const bool lds = n_batch < kSplitsInLds;
+    if (lds)
+        for (int k = threadIdx.x; k <= n_batch; k += kKeyThreads) s_splits[k] = in_splits[k];
+    __syncthreads();
     int32_t j = blockIdx.x * blockDim.x + threadIdx.x;
     if (j <= n_batch) {
         const int32_t b = j;
@@ -110,7 +147,7 @@ __global__ void key_kernel(const float *__restrict__ x_in, int32_t n_in,
         if (bad) atomicOr(status, (uint32_t)kFlagBadSplits);
     }
     if (j >= n_in) return;
-    int32_t b = cloud_of(in_splits, n_batch, j);
+    int32_t b = cloud_of(lds ? s_splits : in_splits, n_batch, j);
     float x = x_in[3 * (int64_t)j], y = x_in[3 * (int64_t)j + 1], z = x_in[3 * (int64_t)j + 2];
     uint32_t key = hash_cell(b, cell_coord(x, inv_h), cell_coord(y, inv_h), cell_coord(z, inv_h)) &
                    table_mask;
@@ -215,7 +252,6 @@ __global__ void __launch_bounds__(kWaves * 64)
     constexpr bool kFill = kMode != 0;
     __shared__ float s_d2[kFill ? kWaves : 1][kFill ? kStage : 1];
     __shared__ int32_t s_j[kFill ? kWaves : 1][kFill ? kStage : 1];
-    __shared__ int32_t s_keep[kFill ? kWaves : 1][kFill ? kStage : 1];
 
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
@@ -226,9 +262,7 @@ __global__ void __launch_bounds__(kWaves * 64)
     c.qx = x_out[3 * (int64_t)i];
     c.qy = x_out[3 * (int64_t)i + 1];
     c.qz = x_out[3 * (int64_t)i + 2];
-    const int32_t b = cloud_of(out_splits, n_batch, i);
-    c.j_lo = in_splits[b];
-    c.j_hi = in_splits[b + 1];
+    const int32_t b = wave_cloud(out_splits, in_splits, n_batch, i, &c.j_lo, &c.j_hi);
     c.r2 = __fmul_rn(radius, radius);
 
     const int32_t total = gather_buckets(c, b, inv_h, table_mask, cell_start, s_start[w], s_off[w]);
@@ -277,26 +311,38 @@ __global__ void __launch_bounds__(kWaves * 64)
     if (kMode == 2 && lane == 0) row_len[i] = n_keep;
 
     if (n <= kStage) {
-        // keep flag: rank on (d2, j) below k_cap
-        for (int32_t a = lane; a < n; a += 64) {
-            int keep = 1;
-            if (capped) {
-                float da = s_d2[w][a];
-                int32_t ja = s_j[w][a];
-                int32_t rank = 0;
-                for (int32_t q = 0; q < n; ++q) rank += key_less(s_d2[w][q], s_j[w][q], da, ja);
-                keep = rank < k_cap;
+        if (capped) {
+            // keep the entries whose rank on (d2, j) is below k_cap; a dropped
+            // entry gets bit 31 set in its staged j, which orders it (as an
+            // unsigned number) after every kept one
+            constexpr int kPerLane = kStage / 64;
+            bool drop[kPerLane];
+#pragma unroll
+            for (int u = 0; u < kPerLane; ++u) {
+                const int32_t a = lane + 64 * u;
+                drop[u] = false;
+                if (a < n) {
+                    const float da = s_d2[w][a];
+                    const int32_t ja = s_j[w][a];
+                    int32_t rank = 0;
+                    for (int32_t q = 0; q < n; ++q) rank += key_less(s_d2[w][q], s_j[w][q], da, ja);
+                    drop[u] = rank >= k_cap;
+                }
             }
-            s_keep[w][a] = keep;
+            wave_lds_sync();
+#pragma unroll
+            for (int u = 0; u < kPerLane; ++u)
+                if (drop[u]) s_j[w][lane + 64 * u] |= INT32_MIN;
+            wave_lds_sync();
         }
-        wave_lds_sync();
+        // position among the kept entries by rank on j
         for (int32_t a = lane; a < n; a += 64) {
-            if (!s_keep[w][a]) continue;
-            int32_t ja = s_j[w][a];
+            const uint32_t ja = (uint32_t)s_j[w][a];
+            if (ja & 0x80000000u) continue;
             int32_t pos = 0;
-            for (int32_t q = 0; q < n; ++q) pos += (s_keep[w][q] && s_j[w][q] < ja) ? 1 : 0;
+            for (int32_t q = 0; q < n; ++q) pos += ((uint32_t)s_j[w][q] < ja) ? 1 : 0;
             int64_t dst = (int64_t)out0 + pos;
-            if (dst < col_capacity) col_idx[dst] = ja;
+            if (dst < col_capacity) col_idx[dst] = (int32_t)ja;
         }
         return;
     }
@@ -469,7 +515,8 @@ extern "C" sbc_status sbc_neighbour_search_points(
                            ws.status);
         SBC_LAUNCH_CHECK();
         const int64_t kn = (int64_t)n_in > (int64_t)n_batch + 1 ? n_in : (int64_t)n_batch + 1;
-        hipLaunchKernelGGL(key_kernel, dim3(grid_for(kn, 256)), dim3(256), 0, stream, x_in, n_in,
+        hipLaunchKernelGGL(key_kernel, dim3(grid_for(kn, kKeyThreads)), dim3(kKeyThreads), 0,
+                           stream, x_in, n_in,
                            in_splits, out_splits, n_out, n_batch, inv_h, T - 1, ws.keys,
                            ws.cell_count, ws.status);
         SBC_LAUNCH_CHECK();

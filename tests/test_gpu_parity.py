@@ -237,6 +237,27 @@ def test_isolated_and_empty_outputs_are_exact_zero():
     assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
 
 
+@pytest.mark.parametrize("n_batch,k_cap,radius", [(70, 12, 0.35), (130, 0, 0.2), (63, 5, 0.3)])
+def test_many_clouds(n_batch, k_cap, radius):
+    """Batches of 63 to 130 clouds (the splits are read by the wave 64 at a
+    time), with empty clouds among them."""
+    print(f"[many clouds] {n_batch} k_cap {k_cap}", flush=True)
+    rng = np.random.default_rng(n_batch)
+    x = workloads.ellipsoid_surface_points(rng, 2400, np.array([1.0, 0.7, 0.5]))
+    cuts = np.sort(rng.integers(0, len(x) + 1, size=n_batch - 1))
+    cuts[:3] = cuts[3]            # a few empty clouds in a row
+    splits = np.concatenate([[0], cuts, [len(x)]]).astype(np.int32)
+    w = workloads.points_workload(rng, [(x, x)], workloads.BASIS_MONO8, radius, k_cap, 4, 4)
+    w["in_splits"] = splits
+    w["out_splits"] = splits.copy()
+    rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
+                               w["radius"], k_cap)
+    t = G.to_device(w)
+    csr = G.search(w, t)
+    assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
+    assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+
+
 def test_empty_stream_and_cloud():
     z = torch.zeros(0, dtype=torch.int32, device=G.DEV)
     csr = G.sbc.neighbour_search_events(z, z, z, 8, 8, 100)
