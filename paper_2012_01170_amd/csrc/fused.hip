@@ -22,8 +22,9 @@
 // the waves split in two roles and the tiles double-buffered in LDS:
 //   gather waves   D[j, m*C_out + p] = sum_{e=(i,j)} v[e, m] dY[i, p] through
 //                  the transposed pattern (and F's tile rows) for tile s+1;
-//   matrix waves   dF_tile = D_tile Wt (Wt[(m, p), c] = W[m, c, p]) and
-//                  dW += F_tile^T D_tile for tile s; the dW partials stay in
+//   matrix waves   dF_tile = D_tile Wt (Wt[(m, p), c] = W[m, c, p], read in
+//                  place: 8 consecutive (m, p) are 8 consecutive floats of W)
+//                  and dW += F_tile^T D_tile for tile s; the dW partials stay in
 //                  registers and are summed afterwards in block order, so dW
 //                  does not depend on scheduling.
 // Sums over edges run in pattern order inside a lane; no floating-point
@@ -410,12 +411,25 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
 // (from LDS) are issued before the 16 x WRB x WCB products of group g, in
 // register sets of their own, so no product waits on a load issued just
 // before it.
-template <int K, int WCB, int NCBW>
+// Offset of B^T element (n, k): a plain [NCOL][K] array (P == 0), or a weight
+// tensor W[K / P][NCOL][P] read in place (k = m P + p), where every run of 8
+// consecutive k starting at a multiple of 8 stays within one m (P % 8 == 0).
+template <int K, int NCOL, int P>
+__device__ __forceinline__ int64_t bt_offset(int n, int k) {
+    if constexpr (P == 0) {
+        return (int64_t)n * K + k;
+    } else {
+        static_assert(P % 8 == 0 && K % P == 0, "runs of 8 k within one block of W");
+        return ((int64_t)(k / P) * NCOL + n) * P + k % P;
+    }
+}
+
+template <int K, int WCB, int NCBW, int NCOL = 0, int P = 0>
 __device__ __forceinline__ void load_bt_f32(const float *__restrict__ Bt, int k0, int wc, int lr,
                                             int lc, float4 (&b)[2][WCB]) {
 #pragma unroll
     for (int t = 0; t < WCB; ++t) {
-        const float *p = Bt + (int64_t)(16 * (wc + NCBW * t) + lc) * K + k0 + 8 * lr;
+        const float *p = Bt + bt_offset<K, NCOL, P>(16 * (wc + NCBW * t) + lc, k0 + 8 * lr);
         b[0][t] = *reinterpret_cast<const float4 *>(p);
         b[1][t] = *reinterpret_cast<const float4 *>(p + 4);
     }
@@ -448,7 +462,7 @@ __device__ __forceinline__ void mma_group_f32t(const float4 (&a)[WRB][2],
                                                                       acc[u][t], 0, 0, 0);
 }
 
-template <int K, int S, int WRB, int WCB, int NCBW, int NRG>
+template <int K, int S, int WRB, int WCB, int NCBW, int NRG, int NCOL = 0, int P = 0>
 __device__ __forceinline__ void mfma_lds_x_global_f32t(const float *As,
                                                        const float *__restrict__ Bt, int wr,
                                                        int wc, floatx4 (&acc)[WRB][WCB]) {
@@ -459,12 +473,13 @@ __device__ __forceinline__ void mfma_lds_x_global_f32t(const float *As,
     const int lr = lane >> 4, lc = lane & 15;
     float4 b[3][2][WCB];
     float4 a[2][WRB][2];
-    load_bt_f32<K, WCB, NCBW>(Bt, 0, wc, lr, lc, b[0]);
-    load_bt_f32<K, WCB, NCBW>(Bt, KG, wc, lr, lc, b[1]);
+    load_bt_f32<K, WCB, NCBW, NCOL, P>(Bt, 0, wc, lr, lc, b[0]);
+    load_bt_f32<K, WCB, NCBW, NCOL, P>(Bt, KG, wc, lr, lc, b[1]);
     load_a_f32<S, WRB, NRG>(As, 0, wr, lr, lc, a[0]);
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-        if (g + 2 < NG) load_bt_f32<K, WCB, NCBW>(Bt, (g + 2) * KG, wc, lr, lc, b[(g + 2) % 3]);
+        if (g + 2 < NG)
+            load_bt_f32<K, WCB, NCBW, NCOL, P>(Bt, (g + 2) * KG, wc, lr, lc, b[(g + 2) % 3]);
         if (g + 1 < NG) load_a_f32<S, WRB, NRG>(As, (g + 1) * KG, wr, lr, lc, a[(g + 1) % 2]);
         __builtin_amdgcn_sched_barrier(0);
         mma_group_f32t<WRB, WCB>(a[g % 2], b[g % 3], acc);
@@ -472,7 +487,7 @@ __device__ __forceinline__ void mfma_lds_x_global_f32t(const float *As,
     }
 }
 
-template <int K, int WCB, int NCBW>
+template <int K, int WCB, int NCBW, int NCOL = 0, int P = 0>
 __device__ __forceinline__ void load_b_bf16(const uint16_t *__restrict__ Bt, int k0, int wc,
                                             int lk, int lc, bf16x8 (&b)[4][WCB]) {
 #pragma unroll
@@ -480,7 +495,7 @@ __device__ __forceinline__ void load_b_bf16(const uint16_t *__restrict__ Bt, int
 #pragma unroll
         for (int t = 0; t < WCB; ++t)
             b[s][t] = *reinterpret_cast<const bf16x8 *>(
-                Bt + (int64_t)(16 * (wc + NCBW * t) + lc) * K + k0 + 32 * s + lk);
+                Bt + bt_offset<K, NCOL, P>(16 * (wc + NCBW * t) + lc, k0 + 32 * s + lk));
 }
 
 template <int S, int WRB, int WCB, int NRG>
@@ -502,7 +517,7 @@ __device__ __forceinline__ void mma_group_bf16(const uint16_t *As, int k0, int w
     }
 }
 
-template <int K, int S, int WRB, int WCB, int NCBW, int NRG>
+template <int K, int S, int WRB, int WCB, int NCBW, int NRG, int NCOL = 0, int P = 0>
 __device__ __forceinline__ void mfma_lds_x_global_bf16(const uint16_t *As,
                                                        const uint16_t *__restrict__ Bt, int wr,
                                                        int wc, floatx4 (&acc)[WRB][WCB]) {
@@ -511,14 +526,14 @@ __device__ __forceinline__ void mfma_lds_x_global_bf16(const uint16_t *As,
     const int lane = threadIdx.x & 63;
     const int lk = 8 * (lane >> 4), lc = lane & 15;
     bf16x8 b0[4][WCB], b1[4][WCB];
-    load_b_bf16<K, WCB, NCBW>(Bt, 0, wc, lk, lc, b0);
+    load_b_bf16<K, WCB, NCBW, NCOL, P>(Bt, 0, wc, lk, lc, b0);
 #pragma unroll 1
     for (int k0 = 0; k0 < K; k0 += 2 * KG) {
-        load_b_bf16<K, WCB, NCBW>(Bt, k0 + KG, wc, lk, lc, b1);
+        load_b_bf16<K, WCB, NCBW, NCOL, P>(Bt, k0 + KG, wc, lk, lc, b1);
         __builtin_amdgcn_sched_barrier(0);
         mma_group_bf16<S, WRB, WCB, NRG>(As, k0, wr, lk, lc, b0, acc);
         const int kn = k0 + 2 * KG < K ? k0 + 2 * KG : K - KG;
-        load_b_bf16<K, WCB, NCBW>(Bt, kn, wc, lk, lc, b0);
+        load_b_bf16<K, WCB, NCBW, NCOL, P>(Bt, kn, wc, lk, lc, b0);
         __builtin_amdgcn_sched_barrier(0);
         mma_group_bf16<S, WRB, WCB, NRG>(As, k0 + KG, wr, lk, lc, b1, acc);
     }
@@ -974,10 +989,10 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
                 if constexpr (kBf)
                     bw[ks][t] = *reinterpret_cast<const bf16x8 *>(
                         static_cast<const uint16_t *>(Wop) +
-                        (int64_t)(16 * (wc + NCBW * t) + lc) * K2 + 32 * ks + 8 * lr);
+                        bt_offset<K2, CI, CO>(16 * (wc + NCBW * t) + lc, 32 * ks + 8 * lr));
                 else
                     bw[ks][t] = static_cast<const float *>(
-                        Wop)[(int64_t)(16 * (wc + NCBW * t) + lc) * K2 + 4 * ks + lr];
+                        Wop)[bt_offset<K2, CI, CO>(16 * (wc + NCBW * t) + lc, 4 * ks + lr)];
             }
     }
     __syncthreads();
@@ -1018,10 +1033,10 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
                         }
                     }
                 } else if constexpr (!kBf) {
-                    mfma_lds_x_global_f32t<K2, SD, WRB, WCB, NCBW, NRG>(
+                    mfma_lds_x_global_f32t<K2, SD, WRB, WCB, NCBW, NRG, CI, CO>(
                         D, static_cast<const float *>(Wop), wr, wc, acc);
                 } else {
-                    mfma_lds_x_global_bf16<K2, SD, WRB, WCB, NCBW, NRG>(
+                    mfma_lds_x_global_bf16<K2, SD, WRB, WCB, NCBW, NRG, CI, CO>(
                         D, static_cast<const uint16_t *>(Wop), wr, wc, acc);
                 }
 #pragma unroll
@@ -1422,12 +1437,9 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
     BwdFn fn = find_bwd(Shape{M, CI, CO, bf}, basis_mode_of(v, g));
     if (!fn) return fail(SBC_ERR_UNSUPPORTED, "no fused backward for this shape");
     const int32_t n_in = csr->n_cols;
-    const int64_t K2 = (int64_t)M * CO;
     char *base = static_cast<char *>(ws);
-    void *wt = base;
     float *part = reinterpret_cast<float *>(base + align_up((size_t)M * CI * CO * 4));
-    // Wt [CI, K2], element (m, c, p) at c*K2 + m*CO + p (float32 or bf16)
-    SBC_TRY(launch_perm(W, bf, bf, M, CI, CO, CO, K2, 1, wt, stream));
+    // the kernel reads W [M, CI, CO] in place as Wt [CI, M*CO]
     const WsCfg cfg = ws_cfg_rt(M, CI, CO, bf);
     const int TR = cfg.tr;
     const int32_t n_tiles = (n_in + TR - 1) / TR;
@@ -1441,7 +1453,7 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
     if (n_in > 0 && (dF || dW)) {
         trace_before("bwd_fused", stream);
         hipLaunchKernelGGL(fn, dim3(blocks), dim3(nw * 64), 0, stream, n_in, n_tiles, csc->col_ptr,
-                           csc->row_idx, csc->edge_perm, v, gg, F, dY, wt, dF,
+                           csc->row_idx, csc->edge_perm, v, gg, F, dY, W, dF,
                            dW ? part : nullptr);
         SBC_LAUNCH_CHECK();
         trace_after("bwd_fused", stream);
