@@ -30,6 +30,7 @@
 // Sums over edges run in pattern order inside a lane; no floating-point
 // atomics are used anywhere.
 #include <type_traits>
+#include <utility>
 
 #include "basis.hpp"
 #include "common.hpp"
@@ -142,6 +143,40 @@ __device__ __forceinline__ void load_row_vec(const void *__restrict__ Xv, int32_
     }
 }
 
+// The same 16 bytes kept as loaded (four registers for 8 bf16 or 4 float32
+// channels), converted where they are used: twice the bf16 edges in flight
+// for the registers of the converted form.
+template <bool kXbf>
+using RawVec = typename std::conditional<kXbf, uint4, float4>::type;
+
+template <int C, int VEC, bool kXbf>
+__device__ __forceinline__ RawVec<kXbf> load_row_raw(const void *__restrict__ Xv, int32_t r,
+                                                     int cg) {
+    if constexpr (kXbf)
+        return *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(Xv) +
+                                                (int64_t)r * C + cg * VEC);
+    else
+        return *reinterpret_cast<const float4 *>(static_cast<const float *>(Xv) +
+                                                 (int64_t)r * C + cg * VEC);
+}
+
+// channel k (compile-time) of a raw row vector, as float32
+template <bool kXbf, int k>
+__device__ __forceinline__ float raw_elem(const RawVec<kXbf> &v) {
+    if constexpr (kXbf) {
+        const uint32_t wd = k / 2 == 0 ? v.x : k / 2 == 1 ? v.y : k / 2 == 2 ? v.z : v.w;
+        return __uint_as_float((k & 1) ? (wd & 0xFFFF0000u) : (wd << 16));
+    } else {
+        return k == 0 ? v.x : k == 1 ? v.y : k == 2 ? v.z : v.w;
+    }
+}
+
+template <bool kXbf, int VEC, int M, int... K>
+__device__ __forceinline__ void fma_row(float (&acc)[M][VEC], const RawVec<kXbf> &f, float vm,
+                                        int m, std::integer_sequence<int, K...>) {
+    ((acc[m][K] += vm * raw_elem<kXbf, K>(f)), ...);
+}
+
 // Row bound ptr[row_begin + lane] (clamped to [0, n_rows]) for lanes 0..RPW:
 // what gather_rows needs to start, loadable one call ahead.
 template <int RPW>
@@ -203,9 +238,10 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
     // group part p taking its edges rs + p, rs + p + SPL, ...; the partial
     // sums are added across the groups at the end
     constexpr int SPL = (kPipelined && RPB_ > RPW) ? RPB_ / RPW : 1;
-    // edges per row loaded together: NB * U feature loads in flight per lane
-    // (pipelined), or 4 per row with the rows taken one after another
-    constexpr int UP = 32 / (NB * VEC) > 1 ? 32 / (NB * VEC) : 1;
+    // edges per row loaded together: NB * U feature loads (16 bytes each, 32
+    // registers in all) in flight per lane (pipelined), or 4 per row with the
+    // rows taken one after another
+    constexpr int UP = 8 / NB > 1 ? 8 / NB : 1;
     constexpr int U = kPipelined ? UP : 4;
     const int lane = threadIdx.x & 63;
     const int slot = lane / LPR;
@@ -307,7 +343,7 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
             const int32_t n = (mine + U - 1) / U;
             steps = n > steps ? n : steps;
         }
-        float f[NB][U][VEC];
+        RawVec<kXbf> f[NB][U];
         int q[NB][U];
         auto issue = [&]() {
 #pragma unroll
@@ -315,7 +351,7 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     q[b][u] = pos[b] + u * SPL < hi[b] ? pos[b] + u * SPL - c0 : 64;
-                    load_row_vec<C, VEC, kXbf>(Xv, st.nb[q[b][u]], cg, f[b][u]);
+                    f[b][u] = load_row_raw<C, VEC, kXbf>(Xv, st.nb[q[b][u]], cg);
                 }
         };
         if (steps > 0) issue();
@@ -343,11 +379,9 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
 #pragma unroll
                 for (int u = 0; u < U; ++u)
 #pragma unroll
-                    for (int m = 0; m < M; ++m) {
-                        const float vm = st.v[q[b][u]][m];
-#pragma unroll
-                        for (int k = 0; k < VEC; ++k) acc[b][m][k] += vm * f[b][u][k];
-                    }
+                    for (int m = 0; m < M; ++m)
+                        fma_row<kXbf, VEC>(acc[b], f[b][u], st.v[q[b][u]][m], m,
+                                           std::make_integer_sequence<int, VEC>{});
                 pos[b] += U * SPL;
             }
         }
