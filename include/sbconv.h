@@ -20,7 +20,8 @@
  *     caller; the library keeps no pointer after a call returns and allocates
  *     no device memory: temporary space comes from the `workspace` argument,
  *     whose required size a *_workspace_size query gives.  workspace must be
- *     256-byte aligned.
+ *     256-byte aligned; the feature, weight, output and gradient arrays of the
+ *     convolution calls 16-byte aligned (rows move 16 bytes at a time).
  *   - Work is enqueued on `stream` and runs asynchronously; only a neighbour
  *     search given a non-NULL nnz_host synchronises the stream (once).
  *   - Outputs are overwritten, never accumulated into.

@@ -160,6 +160,9 @@ Route backward_route(int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_
                                                                                        : kBwdG;
 }
 
+// feature, weight and gradient rows are moved 16 bytes at a time
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
 sbc_status check_conv_args(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,
                            const void *F, const void *W, sbc_dtype dtype, int32_t Ci, int32_t Co) {
     SBC_TRY(check_csr(csr));
@@ -167,6 +170,8 @@ sbc_status check_conv_args(const sbc_csr *csr, const float *v, const sbc_geometr
     if (Ci <= 0 || Co <= 0) return fail(SBC_ERR_INVALID_ARG, "C_in and C_out must be > 0");
     if (dtype != SBC_F32 && dtype != SBC_BF16) return fail(SBC_ERR_INVALID_ARG, "unknown dtype");
     if (!W || (csr->n_cols > 0 && !F)) return fail(SBC_ERR_INVALID_ARG, "F or W is null");
+    if (!aligned16(F) || !aligned16(W))
+        return fail(SBC_ERR_INVALID_ARG, "F and W must be 16-byte aligned");
     if (!v) {
         SBC_TRY(check_geometry(g, csr->n_rows, csr->n_cols));
         const int32_t gm = g->basis == SBC_BASIS_MONO4 ? 4 : 8;
@@ -236,6 +241,7 @@ extern "C" sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v,
     SBC_TRY(check_conv_args(csr, v, geometry, M, F, W, dtype, C_in, C_out));
     SBC_TRY(check_order(order));
     if (!Y && csr->n_rows > 0) return fail(SBC_ERR_INVALID_ARG, "Y is null");
+    if (!aligned16(Y)) return fail(SBC_ERR_INVALID_ARG, "Y must be 16-byte aligned");
     const int32_t n_out = csr->n_rows, n_in = csr->n_cols;
     const bool bf = dtype == SBC_BF16;
     const Route r = forward_route(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order);
@@ -281,6 +287,8 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
         (csr->nnz_bound > 0 && (!csc->row_idx || !csc->edge_perm)))
         return fail(SBC_ERR_INVALID_ARG, "csc is null or does not match csr");
     if (!dY && csr->n_rows > 0) return fail(SBC_ERR_INVALID_ARG, "dY is null");
+    if (!aligned16(dY) || !aligned16(dF) || !aligned16(dW))
+        return fail(SBC_ERR_INVALID_ARG, "dY, dF and dW must be 16-byte aligned");
     if (!dF && !dW) return SBC_OK;
     const int32_t n_out = csr->n_rows, n_in = csr->n_cols;
     const bool bf = dtype == SBC_BF16;

@@ -1154,36 +1154,60 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
                     accw[ib][nb][r];
 }
 
-// dW[m, c, p] = sum_b part[b, c, m*CO + p].  A block of 256 threads owns 32
-// consecutive partial positions; its 8 thread groups each sum a fixed,
-// contiguous range of blocks in order, and the 8 group sums are then added in
-// group order, so the result is independent of scheduling.
-constexpr int kReduceGroups = 8;
+// dW[m, c, p] = sum_b part[b, c, m*CO + p].  A block of 256 threads owns
+// kReducePos consecutive partial positions, four per thread (16-byte loads);
+// its kReduceGroups thread groups each sum a fixed, contiguous range of
+// blocks in order (eight loads in flight per thread), and the group sums are
+// then added in group order, so the result is independent of scheduling.
+constexpr int kReduceGroups = 16;
+constexpr int kReducePos = 64;  // 16 threads x 4 positions per group
 
 __global__ void __launch_bounds__(256)
     dw_reduce_kernel(const float *__restrict__ part, int32_t n_parts, int32_t M, int32_t CI,
                      int32_t CO, float *__restrict__ dW) {
-    __shared__ float sums[kReduceGroups][32];
+    __shared__ float4 sums[kReduceGroups][kReducePos / 4];
     const int64_t K2 = (int64_t)M * CO;
-    const int64_t total = (int64_t)CI * K2;
-    const int g = threadIdx.x >> 5;
-    const int64_t off = (int64_t)blockIdx.x * 32 + (threadIdx.x & 31);
+    const int64_t total = (int64_t)CI * K2;  // a multiple of 4 (CO % 16 == 0)
+    const int g = threadIdx.x / (kReducePos / 4);
+    const int tq = threadIdx.x % (kReducePos / 4);
+    const int64_t off = (int64_t)blockIdx.x * kReducePos + 4 * tq;
     const int32_t per = (n_parts + kReduceGroups - 1) / kReduceGroups;
     const int32_t b0 = g * per;
     const int32_t b1 = b0 + per < n_parts ? b0 + per : n_parts;
-    float s = 0.f;
-    if (off < total)
-        for (int32_t b = b0; b < b1; ++b) s += part[(int64_t)b * total + off];
-    sums[g][threadIdx.x & 31] = s;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (off < total) {
+        for (int32_t bb = b0; bb < b1; bb += 8) {
+            float4 v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                v[j] = bb + j < b1 ? *reinterpret_cast<const float4 *>(
+                                         part + (int64_t)(bb + j) * total + off)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                s.x += v[j].x;
+                s.y += v[j].y;
+                s.z += v[j].z;
+                s.w += v[j].w;
+            }
+        }
+    }
+    sums[g][tq] = s;
     __syncthreads();
     if (g == 0 && off < total) {
-        float t = 0.f;
+        float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int q = 0; q < kReduceGroups; ++q) t += sums[q][threadIdx.x & 31];
-        // off = c*K2 + m*CO + p  ->  dW[(m*CI + c)*CO + p]
+        for (int q = 0; q < kReduceGroups; ++q) {
+            const float4 u = sums[q][tq];
+            t.x += u.x;
+            t.y += u.y;
+            t.z += u.z;
+            t.w += u.w;
+        }
+        // off = c*K2 + m*CO + p  ->  dW[(m*CI + c)*CO + p]; p..p+3 share m
         const int64_t c = off / K2, mp = off % K2;
         const int64_t m = mp / CO, p = mp % CO;
-        dW[(m * CI + c) * CO + p] = t;
+        *reinterpret_cast<float4 *>(dW + (m * CI + c) * CO + p) = t;
     }
 }
 
@@ -1494,7 +1518,7 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
     }
     if (!dW) return SBC_OK;
     const int64_t total = (int64_t)M * CI * CO;
-    const int64_t rb = (total + 31) / 32;
+    const int64_t rb = (total + kReducePos - 1) / kReducePos;
     trace_before("bwd_dw_reduce", stream);
     hipLaunchKernelGGL(dw_reduce_kernel, dim3((unsigned)rb), dim3(256), 0, stream, part,
                        n_in > 0 ? blocks : 0, M, CI, CO, dW);
