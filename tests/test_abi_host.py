@@ -95,7 +95,10 @@ def test_event_search_argument_errors(lib, kw, status):
 def test_conv_argument_errors(lib):
     csr = L.SbcCsr(10, 10, 40, 1, 1)
     g = L.SbcGeometry(L.SBC_BASIS_MONO8, 0.1, 0.0, 1, 1, 0, 0, 0)
-    ok = dict(M=8, F=1, W=1, dt=0, ci=4, co=4, Y=1, order=0, ws=1, wsb=1 << 30)
+    # stand-in device addresses (never dereferenced: every call below fails
+    # its argument checks first), 16-byte aligned like real arrays
+    A = 1 << 20
+    ok = dict(M=8, F=A, W=A, dt=0, ci=4, co=4, Y=A, order=0, ws=A, wsb=1 << 30)
 
     def fwd(**kw):
         a = dict(ok)
@@ -111,15 +114,23 @@ def test_conv_argument_errors(lib):
     assert fwd(W=None) == 1
     assert fwd(Y=None) == 1
     assert fwd(wsb=8) == 6
+    # rows move 16 bytes at a time: unaligned arrays are argument errors
+    assert fwd(F=A + 4) == 1
+    assert fwd(W=A + 8) == 1
+    assert fwd(Y=A + 12) == 1
     bad = L.SbcCsr(10, 10, 1 << 31, 1, 1)
-    assert lib.sbc_conv_forward(ctypes.byref(bad), None, ctypes.byref(g), 8, 1, 1, 0, 4, 4, 1, 0,
-                                1, 1 << 30, None) == 3
+    assert lib.sbc_conv_forward(ctypes.byref(bad), None, ctypes.byref(g), 8, A, A, 0, 4, 4, A, 0,
+                                A, 1 << 30, None) == 3
     ge = L.SbcGeometry(L.SBC_BASIS_EVENT8, 0.0, 0.0, 0, 0, 1, 1, 1)
-    assert lib.sbc_conv_forward(ctypes.byref(csr), None, ctypes.byref(ge), 8, 1, 1, 0, 4, 4, 1,
-                                0, 1, 1 << 30, None) == 1          # tau = 0
+    assert lib.sbc_conv_forward(ctypes.byref(csr), None, ctypes.byref(ge), 8, A, A, 0, 4, 4, A,
+                                0, A, 1 << 30, None) == 1          # tau = 0
     csc = L.SbcCsc(9, 1, 1, 1)                                      # n_cols mismatch
     assert lib.sbc_conv_backward(ctypes.byref(csr), ctypes.byref(csc), None, ctypes.byref(g), 8,
-                                 1, 1, 1, 0, 4, 4, 1, 1, 0, 1, 1 << 30, None) == 1
+                                 A, A, A, 0, 4, 4, A, A, 0, A, 1 << 30, None) == 1
+    csc = L.SbcCsc(10, 1, 1, 1)
+    for dY, dF, dW in ((A + 4, A, A), (A, A + 4, A), (A, A, A + 4)):
+        assert lib.sbc_conv_backward(ctypes.byref(csr), ctypes.byref(csc), None, ctypes.byref(g),
+                                     8, A, A, dY, 0, 4, 4, dF, dW, 0, A, 1 << 30, None) == 1
 
 
 @pytest.mark.parametrize("shape", [
