@@ -4,11 +4,14 @@
 // no copy), float32 or bf16 operands (bf16 is widened exactly to float32),
 // float32 MFMA (v_mfma_f32_16x16x4_f32) and float32 accumulation.
 //
-// Tiling: a 256-thread block owns a 64 x 64 tile of C; each of its four
-// waves owns a 32 x 32 quarter as 2 x 2 MFMA tiles of 16 x 16.  K advances in
-// slabs of 16 staged through LDS.  Large K with few tiles is split over
-// blockIdx.z; the partial tiles are summed afterwards in split order, so the
-// result does not depend on scheduling.
+// Tiling: a 256-thread block owns a BM x BN tile of C (128 x 128, or 64 x
+// 64 when C is small and K long); its four waves own BM/2 x BN/2 quarters as
+// grids of 16 x 16 MFMA tiles.  K advances in slabs of 16 held in two LDS
+// buffers: every thread loads its share of slab s+1 into registers while the
+// waves multiply slab s, then stores it into the other buffer (one block
+// barrier per slab).  Large K with few tiles is split over blockIdx.z; the
+// partial tiles are summed afterwards in split order, so the result does not
+// depend on scheduling.
 #include "common.hpp"
 #include "gemm.hpp"
 
@@ -17,77 +20,123 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kTile = 64;
 constexpr int kSlab = 16;
+constexpr int kThreads = 256;
 
 __device__ __forceinline__ float ld(const float *p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float ld(const uint16_t *p, int64_t i) {
     return __uint_as_float((uint32_t)p[i] << 16);
 }
 
-template <typename AT, typename BT>
-__global__ void __launch_bounds__(256)
+// One operand slab, [kSlab][BT] in LDS (BT = the tile's rows of A or columns
+// of B), loaded by 256 threads, BT * kSlab / 256 elements each: runs along the
+// operand's contiguous index (k, or the row / column index), so that
+// neighbouring threads read neighbouring addresses.
+template <int BT, typename T>
+struct SlabLoader {
+    static constexpr int kPer = BT * kSlab / kThreads;  // 8 (128) or 4 (64)
+    float v[kPer];
+    // element (t, k) of the operand at p[t * s_t + k * s_k], t < n_t, k < k_end
+    __device__ __forceinline__ void load(const T *__restrict__ p, int64_t s_t, int64_t s_k,
+                                         int32_t t0, int32_t n_t, int64_t k0, int64_t k_end,
+                                         bool k_contig) {
+        const int tid = threadIdx.x;
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            int tl, kl;
+            if (k_contig) {  // a thread takes kPer consecutive k of one row
+                tl = tid / (kSlab / kPer);
+                kl = (tid % (kSlab / kPer)) * kPer + q;
+            } else {         // a thread takes kPer consecutive rows at one k
+                kl = tid / (BT / kPer);
+                tl = (tid % (BT / kPer)) * kPer + q;
+            }
+            const int32_t t = t0 + tl;
+            const int64_t k = k0 + kl;
+            v[q] = (t < n_t && k < k_end) ? ld(p, (int64_t)t * s_t + k * s_k) : 0.f;
+        }
+    }
+    __device__ __forceinline__ void store(float (*S)[BT + 4], bool k_contig) const {
+        const int tid = threadIdx.x;
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            int tl, kl;
+            if (k_contig) {
+                tl = tid / (kSlab / kPer);
+                kl = (tid % (kSlab / kPer)) * kPer + q;
+            } else {
+                kl = tid / (BT / kPer);
+                tl = (tid % (BT / kPer)) * kPer + q;
+            }
+            S[kl][tl] = v[q];
+        }
+    }
+};
+
+template <int BM, int BN, typename AT, typename BT>
+__global__ void __launch_bounds__(kThreads, 2)
     gemm_kernel(const AT *__restrict__ A, int64_t sa_r, int64_t sa_k, const BT *__restrict__ B,
                 int64_t sb_k, int64_t sb_n, float *__restrict__ C, int64_t sc_r, int64_t sc_n,
                 int32_t R, int32_t N, int64_t K, int64_t k_chunk, float *__restrict__ partial) {
-    __shared__ float As[kSlab][kTile + 4];
-    __shared__ float Bs[kSlab][kTile + 4];
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int32_t r0 = blockIdx.y * kTile;
-    const int32_t n0 = blockIdx.x * kTile;
+    constexpr int TM = BM / 32, TN = BN / 32;  // 16x16 tiles per wave (2 x 2 waves)
+    __shared__ float As[2][kSlab][BM + 4];
+    __shared__ float Bs[2][kSlab][BN + 4];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int32_t r0 = blockIdx.y * BM;
+    const int32_t n0 = blockIdx.x * BN;
     const int64_t kb = (int64_t)blockIdx.z * k_chunk;
     const int64_t ke = (kb + k_chunk < K) ? kb + k_chunk : K;
-    const int wr = (wave >> 1) * 32;
-    const int wn = (wave & 1) * 32;
-    floatx4 acc[2][2];
+    const int wr = (wave >> 1) * (BM / 2);
+    const int wn = (wave & 1) * (BN / 2);
+    const bool a_kc = sa_k == 1, b_kc = sb_k == 1;
+    floatx4 acc[TM][TN];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < TM; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int b = 0; b < TN; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    const bool a_k_contig = sa_k == 1;
-    const bool b_n_contig = sb_n == 1;
+    SlabLoader<BM, AT> la;
+    SlabLoader<BN, BT> lb;
+    la.load(A, sa_r, sa_k, r0, R, kb, ke, a_kc);
+    lb.load(B, sb_n, sb_k, n0, N, kb, ke, b_kc);
+    la.store(As[0], a_kc);
+    lb.store(Bs[0], b_kc);
+    __syncthreads();
+    int buf = 0;
     for (int64_t k0 = kb; k0 < ke; k0 += kSlab) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int idx = tid + 256 * q;
-            int rl, kl;
-            if (a_k_contig) { kl = idx & 15; rl = idx >> 4; } else { rl = idx & 63; kl = idx >> 6; }
-            const int32_t r = r0 + rl;
-            const int64_t k = k0 + kl;
-            As[kl][rl] = (r < R && k < ke) ? ld(A, (int64_t)r * sa_r + k * sa_k) : 0.f;
-            int nl, kl2;
-            if (b_n_contig) { nl = idx & 63; kl2 = idx >> 6; } else { kl2 = idx & 15; nl = idx >> 4; }
-            const int32_t n = n0 + nl;
-            const int64_t k2 = k0 + kl2;
-            Bs[kl2][nl] = (n < N && k2 < ke) ? ld(B, k2 * sb_k + (int64_t)n * sb_n) : 0.f;
+        const bool more = k0 + kSlab < ke;
+        if (more) {
+            la.load(A, sa_r, sa_k, r0, R, k0 + kSlab, ke, a_kc);
+            lb.load(B, sb_n, sb_k, n0, N, k0 + kSlab, ke, b_kc);
         }
-        __syncthreads();
 #pragma unroll
         for (int k4 = 0; k4 < kSlab / 4; ++k4) {
             const int kk = k4 * 4 + (lane >> 4);
-            float a[2], b[2];
+            float a[TM], b[TN];
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                a[t] = As[kk][wr + 16 * t + (lane & 15)];
-                b[t] = Bs[kk][wn + 16 * t + (lane & 15)];
-            }
+            for (int t = 0; t < TM; ++t) a[t] = As[buf][kk][wr + 16 * t + (lane & 15)];
 #pragma unroll
-            for (int ta = 0; ta < 2; ++ta)
+            for (int t = 0; t < TN; ++t) b[t] = Bs[buf][kk][wn + 16 * t + (lane & 15)];
 #pragma unroll
-                for (int tb = 0; tb < 2; ++tb)
+            for (int ta = 0; ta < TM; ++ta)
+#pragma unroll
+                for (int tb = 0; tb < TN; ++tb)
                     acc[ta][tb] =
                         __builtin_amdgcn_mfma_f32_16x16x4f32(a[ta], b[tb], acc[ta][tb], 0, 0, 0);
         }
+        if (more) {
+            la.store(As[buf ^ 1], a_kc);
+            lb.store(Bs[buf ^ 1], b_kc);
+        }
         __syncthreads();
+        buf ^= 1;
     }
     // D layout of a 16x16 MFMA tile: lane holds column (lane & 15), rows 4*(lane >> 4) + 0..3
 #pragma unroll
-    for (int ta = 0; ta < 2; ++ta)
+    for (int ta = 0; ta < TM; ++ta)
 #pragma unroll
-        for (int tb = 0; tb < 2; ++tb)
+        for (int tb = 0; tb < TN; ++tb)
 #pragma unroll
             for (int rr = 0; rr < 4; ++rr) {
                 const int32_t row = r0 + wr + 16 * ta + 4 * (lane >> 4) + rr;
@@ -106,8 +155,16 @@ __global__ void splitk_reduce_kernel(const float *__restrict__ partial, int32_t 
     const int64_t total = (int64_t)R * N;
     for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < total;
          x += (int64_t)gridDim.x * blockDim.x) {
+        // split order, eight partial loads in flight
         float s = 0.f;
-        for (int32_t z = 0; z < S; ++z) s += partial[(int64_t)z * total + x];
+        for (int32_t z0 = 0; z0 < S; z0 += 8) {
+            float v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                v[j] = z0 + j < S ? partial[(int64_t)(z0 + j) * total + x] : 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s += v[j];
+        }
         const int32_t row = (int32_t)(x / N), col = (int32_t)(x % N);
         C[(int64_t)row * sc_r + (int64_t)col * sc_n] = s;
     }
@@ -115,11 +172,19 @@ __global__ void splitk_reduce_kernel(const float *__restrict__ partial, int32_t 
 
 }  // namespace
 
+// Tile of a shape: 128 x 128, or 64 x 64 when the 128 tiles would be too few
+// to spread K over the chip without very short splits.
+static int tile_for(int32_t R, int32_t N) {
+    const int64_t big = (int64_t)((R + 127) / 128) * ((N + 127) / 128);
+    return big >= 64 ? 128 : 64;
+}
+
 int32_t gemm_splits(int32_t R, int32_t N, int64_t K) {
-    const int64_t tiles = (int64_t)((R + kTile - 1) / kTile) * ((N + kTile - 1) / kTile);
+    const int t = tile_for(R, N);
+    const int64_t tiles = (int64_t)((R + t - 1) / t) * ((N + t - 1) / t);
     if (tiles <= 0 || K <= 0) return 1;
-    int64_t s = (1024 + tiles - 1) / tiles;
-    const int64_t by_k = (K + 511) / 512;  // at least 512 of K per split
+    int64_t s = (512 + tiles - 1) / tiles;        // about two blocks per CU
+    const int64_t by_k = (K + 127) / 128;         // at least 128 of K per split
     if (s > by_k) s = by_k;
     if (s > 256) s = 256;
     return s < 1 ? 1 : (int32_t)s;
@@ -140,16 +205,24 @@ sbc_status gemm(const void *A, bool a_bf16, int64_t sa_r, int64_t sa_k, const vo
     int64_t k_chunk = S > 1 ? (K + S - 1) / S : (K > 0 ? K : 1);
     k_chunk = (k_chunk + kSlab - 1) / kSlab * kSlab;
     const int32_t Sz = K > 0 ? (int32_t)((K + k_chunk - 1) / k_chunk) : 1;
-    dim3 grid((N + kTile - 1) / kTile, (R + kTile - 1) / kTile, Sz);
+    const int t = tile_for(R, N);
+    dim3 grid((N + t - 1) / t, (R + t - 1) / t, Sz);
     float *part = Sz > 1 ? partial_ws : nullptr;
-#define SBC_GEMM_LAUNCH(AT, BT)                                                               \
-    hipLaunchKernelGGL((gemm_kernel<AT, BT>), grid, dim3(256), 0, stream,                      \
+#define SBC_GEMM_LAUNCH(TT, AT, BT)                                                           \
+    hipLaunchKernelGGL((gemm_kernel<TT, TT, AT, BT>), grid, dim3(kThreads), 0, stream,         \
                        static_cast<const AT *>(A), sa_r, sa_k, static_cast<const BT *>(B),     \
                        sb_k, sb_n, C, sc_r, sc_n, R, N, K, k_chunk, part)
-    if (!a_bf16 && !b_bf16) SBC_GEMM_LAUNCH(float, float);
-    else if (!a_bf16 && b_bf16) SBC_GEMM_LAUNCH(float, uint16_t);
-    else if (a_bf16 && !b_bf16) SBC_GEMM_LAUNCH(uint16_t, float);
-    else SBC_GEMM_LAUNCH(uint16_t, uint16_t);
+#define SBC_GEMM_TYPES(TT)                                                                    \
+    if (!a_bf16 && !b_bf16) SBC_GEMM_LAUNCH(TT, float, float);                                \
+    else if (!a_bf16 && b_bf16) SBC_GEMM_LAUNCH(TT, float, uint16_t);                         \
+    else if (a_bf16 && !b_bf16) SBC_GEMM_LAUNCH(TT, uint16_t, float);                         \
+    else SBC_GEMM_LAUNCH(TT, uint16_t, uint16_t);
+    if (t == 128) {
+        SBC_GEMM_TYPES(128)
+    } else {
+        SBC_GEMM_TYPES(64)
+    }
+#undef SBC_GEMM_TYPES
 #undef SBC_GEMM_LAUNCH
     SBC_LAUNCH_CHECK();
     if (part) {
