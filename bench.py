@@ -389,7 +389,7 @@ def main(argv=None):
         return Y, dF, dW
 
     n_cus = torch.cuda.get_device_properties(dev).multi_processor_count
-    tr_bwd = 64 if M * co * sf * 64 <= 65536 else 32     # the fused backward's tile rows
+    tr_bwd = 32                                           # the fused backward's tile rows
     blocks_bwd = max(1, min(256, n_cus, (n_in + tr_bwd - 1) // tr_bwd))
     table = kernel_table(w["kind"], plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd)
     L = _lib.lib()

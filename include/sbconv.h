@@ -272,8 +272,12 @@ const char *sbc_kernel_names(void);
  *   *_fused         1 when that pass runs as one fused kernel (gather into
  *                   LDS, basis evaluated inside, MFMA contraction), 0 when it
  *                   runs as separate gather and contraction kernels.
- * AUTO picks the order with fewer multiply-adds (the paper's cost table);
- * for the backward the rule is applied to the transposed problem.
+ * AUTO picks the order with the lower estimated cost: the multiply-adds of
+ * the paper's cost table, plus 5e7 multiply-adds (about 5 us, measured) for
+ * every kernel launch, a fused pass counting as two launches and a pass of
+ * separate gather and contraction kernels as five.  The launch term only
+ * matters for small problems, where it prefers the fused pass.  For the
+ * backward the estimate is applied to the transposed problem.
  */
 typedef struct {
     sbc_order forward_order;
@@ -285,7 +289,9 @@ sbc_status sbc_conv_plan(int32_t n_out, int32_t n_in, int64_t nnz_bound, int32_t
                          int32_t C_in, int32_t C_out, sbc_dtype dtype, sbc_order order,
                          sbc_conv_plan_t *plan);
 
-/* Order AUTO resolves to (SBC_ORDER_SPMM_FIRST or SBC_ORDER_GEMM_FIRST). */
+/* The paper's rule alone: AUTO resolves to the order with fewer
+ * multiply-adds (SBC_ORDER_SPMM_FIRST on a tie); an explicit order is returned
+ * as given.  sbc_conv_plan adds the launch term above. */
 sbc_order sbc_resolve_order(int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t C_in,
                             int32_t C_out, sbc_order order);
 

@@ -144,20 +144,48 @@ size_t route_bytes(Route r, int32_t n_out, int32_t n_in, int64_t nnz, int32_t M,
     return b;
 }
 
+// AUTO: the order with the lower estimated cost, the multiply-adds of the
+// paper's cost table plus a fixed cost per kernel launch (kLaunchMacs, about
+// 5 us of launch and dependency latency at 1e13 multiply-adds/s, as measured
+// with rocprofv3 on MI355X), a fused pass counting as kFusedLaunches and a
+// pass of separate gather and contraction kernels as kSplitLaunches.  The
+// launch term only decides between orders whose multiply-adds differ by less
+// than a few launches' worth, i.e. small problems, where the fused pass wins.
+constexpr double kLaunchMacs = 5e7;
+constexpr double kFusedLaunches = 2, kSplitLaunches = 5;
+
+double order_macs(int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t Ci, int32_t Co,
+                  bool spmm_first) {
+    const double E = (double)(nnz > 0 ? nnz : 0);
+    return spmm_first ? (double)M * Ci * (E + (double)n_out * Co)
+                      : (double)M * Co * (E + (double)n_in * Ci);
+}
+
 Route forward_route(int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t Ci, int32_t Co,
-                    sbc_order order) {
-    return sbc_resolve_order(n_out, n_in, nnz, M, Ci, Co, order) == SBC_ORDER_SPMM_FIRST
-               ? kFwdSpmm
-               : kFwdGemm;
+                    sbc_order order, bool bf) {
+    if (order == SBC_ORDER_SPMM_FIRST) return kFwdSpmm;
+    if (order == SBC_ORDER_GEMM_FIRST) return kFwdGemm;
+    const double spmm = order_macs(n_out, n_in, nnz, M, Ci, Co, true) +
+                        kLaunchMacs * (route_fused(kFwdSpmm, M, Ci, Co, bf) ? kFusedLaunches
+                                                                             : kSplitLaunches);
+    const double gemm = order_macs(n_out, n_in, nnz, M, Ci, Co, false) +
+                        kLaunchMacs * kSplitLaunches;
+    return spmm <= gemm ? kFwdSpmm : kFwdGemm;
 }
 
 // The backward is itself a convolution from the outputs back to the inputs
-// (N^T, channels C_out -> C_in); AUTO applies the same cost rule to it.
+// (N^T, channels C_out -> C_in); AUTO applies the same estimate to it.
 // Explicit orders name what is done first: SPMM_FIRST = D-route, GEMM_FIRST = G-route.
 Route backward_route(int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t Ci, int32_t Co,
-                     sbc_order order) {
-    return sbc_resolve_order(n_in, n_out, nnz, M, Co, Ci, order) == SBC_ORDER_SPMM_FIRST ? kBwdD
-                                                                                       : kBwdG;
+                     sbc_order order, bool bf) {
+    if (order == SBC_ORDER_SPMM_FIRST) return kBwdD;
+    if (order == SBC_ORDER_GEMM_FIRST) return kBwdG;
+    const double d = order_macs(n_in, n_out, nnz, M, Co, Ci, true) +
+                     kLaunchMacs * (route_fused(kBwdD, M, Ci, Co, bf) ? kFusedLaunches
+                                                                       : kSplitLaunches);
+    const double g = order_macs(n_in, n_out, nnz, M, Co, Ci, false) +
+                     kLaunchMacs * kSplitLaunches;
+    return d <= g ? kBwdD : kBwdG;
 }
 
 // feature, weight and gradient rows are moved 16 bytes at a time
@@ -196,10 +224,10 @@ extern "C" sbc_order sbc_resolve_order(int32_t n_out, int32_t n_in, int64_t nnz,
     if (order == SBC_ORDER_SPMM_FIRST || order == SBC_ORDER_GEMM_FIRST) return order;
     // multiply-adds of the two orders (the paper's cost table):
     //   (N F) W:  M C_in (E + n_out C_out);   N (F W):  M C_out (E + n_in C_in)
-    const double E = (double)(nnz > 0 ? nnz : 0);
-    const double spmm_first = (double)M * C_in * (E + (double)n_out * C_out);
-    const double gemm_first = (double)M * C_out * (E + (double)n_in * C_in);
-    return spmm_first <= gemm_first ? SBC_ORDER_SPMM_FIRST : SBC_ORDER_GEMM_FIRST;
+    return order_macs(n_out, n_in, nnz, M, C_in, C_out, true) <=
+                   order_macs(n_out, n_in, nnz, M, C_in, C_out, false)
+               ? SBC_ORDER_SPMM_FIRST
+               : SBC_ORDER_GEMM_FIRST;
 }
 
 extern "C" sbc_status sbc_conv_plan(int32_t n_out, int32_t n_in, int64_t nnz_bound, int32_t M,
@@ -211,8 +239,8 @@ extern "C" sbc_status sbc_conv_plan(int32_t n_out, int32_t n_in, int64_t nnz_bou
         return fail(SBC_ERR_INVALID_ARG, "negative or zero size");
     SBC_TRY(check_order(order));
     const bool bf = dtype == SBC_BF16;
-    const Route f = forward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order);
-    const Route b = backward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order);
+    const Route f = forward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order, bf);
+    const Route b = backward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order, bf);
     plan->forward_order = f == kFwdSpmm ? SBC_ORDER_SPMM_FIRST : SBC_ORDER_GEMM_FIRST;
     plan->backward_order = b == kBwdD ? SBC_ORDER_SPMM_FIRST : SBC_ORDER_GEMM_FIRST;
     plan->forward_fused = route_fused(f, M, C_in, C_out, bf) ? 1 : 0;
@@ -225,8 +253,8 @@ extern "C" size_t sbc_conv_workspace_size(int32_t n_out, int32_t n_in, int64_t n
                                           sbc_dtype dtype, sbc_order order) {
     if (n_out < 0 || n_in < 0 || nnz_bound < 0 || M <= 0 || C_in <= 0 || C_out <= 0) return 0;
     const bool bf = dtype == SBC_BF16;
-    const Route f = forward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order);
-    const Route b = backward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order);
+    const Route f = forward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order, bf);
+    const Route b = backward_route(n_out, n_in, nnz_bound, M, C_in, C_out, order, bf);
     const size_t a = route_bytes(f, n_out, n_in, nnz_bound, M, C_in, C_out, bf);
     const size_t c = route_bytes(b, n_out, n_in, nnz_bound, M, C_in, C_out, bf);
     return a > c ? a : c;
@@ -244,7 +272,7 @@ extern "C" sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v,
     if (!aligned16(Y)) return fail(SBC_ERR_INVALID_ARG, "Y must be 16-byte aligned");
     const int32_t n_out = csr->n_rows, n_in = csr->n_cols;
     const bool bf = dtype == SBC_BF16;
-    const Route r = forward_route(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order);
+    const Route r = forward_route(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order, bf);
     const size_t need = route_bytes(r, n_out, n_in, csr->nnz_bound, M, C_in, C_out, bf);
     if (!workspace || workspace_bytes < need)
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_conv_workspace_size()");
@@ -292,7 +320,7 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
     if (!dF && !dW) return SBC_OK;
     const int32_t n_out = csr->n_rows, n_in = csr->n_cols;
     const bool bf = dtype == SBC_BF16;
-    const Route r = backward_route(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order);
+    const Route r = backward_route(n_out, n_in, csr->nnz_bound, M, C_in, C_out, order, bf);
     const size_t need = route_bytes(r, n_out, n_in, csr->nnz_bound, M, C_in, C_out, bf);
     if (!workspace || workspace_bytes < need)
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_conv_workspace_size()");

@@ -164,6 +164,12 @@ def test_conv_plan(lib):
     p = ops.conv_plan(8192, 32768, 159867, 8, 64, 128)
     assert p["forward_order"] == "spmm_first" and p["backward_order"] == "gemm_first"
     assert p["forward_fused"] and not p["backward_fused"]
+    # a tiny problem: the multiply-adds favour dG first, but by less than the
+    # three launches the fused D-route saves
+    p = ops.conv_plan(256, 1024, 2894, 4, 16, 32)
+    assert p["backward_order"] == "spmm_first" and p["backward_fused"]
+    assert lib.sbc_resolve_order(1024, 256, 2894, 4, 32, 16, L.SBC_ORDER_AUTO) == \
+        L.SBC_ORDER_GEMM_FIRST
     p = ops.conv_plan(100, 100, 500, 8, 5, 7)
     assert not p["forward_fused"] and not p["backward_fused"]
     p = ops.conv_plan(100, 100, 500, 8, 64, 64, order="gemm_first")
