@@ -66,6 +66,21 @@ def source_fingerprint():
     return h.hexdigest()[:16]
 
 
+def kernel_fingerprint(base):
+    """Hash of the HIP source that defines device function `base` and of the
+    shared headers: a kernel's byte counts stay valid while these are unchanged."""
+    h = hashlib.sha256()
+    names = sorted(os.listdir(SRC_DIR))
+    pat = re.compile(r"\b" + re.escape(base) + r"\s*\(")
+    for name in names:
+        path = os.path.join(SRC_DIR, name)
+        if name.endswith(".hpp") or (name.endswith(".hip") and pat.search(open(path).read())):
+            h.update(name.encode())
+            with open(path, "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()[:16]
+
+
 def short_kernel_name(name):
     """'void ns::(anonymous namespace)::f<...>(args)' -> 'f<...>'."""
     name = name.replace("(anonymous namespace)::", "")
@@ -87,23 +102,26 @@ def short_kernel_name(name):
 def read_traffic(workload):
     """HBM bytes per dispatch of each traced kernel from a committed counter summary.
 
-    Returns (table, note): table maps trace name -> bytes per launch, or is None
-    when there is no summary or the sources changed since it was taken.
+    Returns (table, note): table maps trace name -> bytes per launch for the
+    kernels whose source (kernel_fingerprint) is unchanged since the counters
+    were taken; None when there is no summary.
     """
     path = os.path.join(PROFILES, f"hbm_traffic_{workload}.txt")
     if not os.path.exists(path):
         return None, "no counter summary"
-    table, fp = {}, None
+    table, stale = {}, []
     with open(path) as f:
         for line in f:
             parts = line.split()
-            if len(parts) >= 2 and parts[0] == "source_fingerprint:":
-                fp = parts[1]
-            elif len(parts) >= 6 and parts[0] == "traffic":
-                table[parts[1]] = float(parts[5])
-    if fp != source_fingerprint():
-        return None, f"{os.path.basename(path)} was taken on other sources"
-    return table, os.path.basename(path)
+            if len(parts) >= 7 and parts[0] == "traffic":
+                if parts[6] == kernel_fingerprint(parts[2]):
+                    table[parts[1]] = float(parts[5])
+                else:
+                    stale.append(parts[1])
+    note = os.path.basename(path)
+    if stale:
+        note += " (changed since the counters were taken: " + ", ".join(stale) + ")"
+    return table, note
 
 
 def _counter_rows(directory):
@@ -154,7 +172,8 @@ def summarize_traffic(fetch_dir, write_dir, probe_mb, command):
     for b, k, n, fk, wk in sorted(rows_out, reverse=True):
         base = k.split("<")[0]
         if base in TRACE_NAME:
-            out.append(f"traffic {TRACE_NAME[base]} {base} {fk:.1f} {wk:.1f} {b:.0f}")
+            out.append(f"traffic {TRACE_NAME[base]} {base} {fk:.1f} {wk:.1f} {b:.0f} "
+                       f"{kernel_fingerprint(base)}")
     return "\n".join(out) + "\n"
 
 
