@@ -39,6 +39,40 @@ __device__ __forceinline__ int32_t row_of(const int32_t *__restrict__ row_ptr, i
 constexpr int kScatterThreads = 256;
 constexpr int kScatterItems = 4;
 constexpr int kScatterChunk = kScatterThreads * kScatterItems;  // edges per block
+// row_ptr entries a block stages in LDS for the row lookup of its edges
+constexpr int kSpanMax = 2048;
+
+// Rows of a block's edges [e0, e1): two threads locate the rows of the first
+// and last edge; when the span r0..r1 is short (the usual case) its row
+// bounds are staged in LDS and every edge bisects there, else in row_ptr.
+struct ChunkRows {
+    int32_t r0, r1;
+    bool staged;
+};
+
+__device__ __forceinline__ ChunkRows chunk_rows(const int32_t *__restrict__ row_ptr,
+                                                int32_t n_rows, int64_t e0, int64_t e1,
+                                                int32_t *span, int32_t *s_ptr) {
+    if (threadIdx.x < 2) span[threadIdx.x] = row_of(row_ptr, 0, n_rows - 1, threadIdx.x ? e1 - 1 : e0);
+    __syncthreads();
+    ChunkRows c{span[0], span[1], span[1] - span[0] + 1 <= kSpanMax};
+    if (c.staged)
+        for (int32_t k = threadIdx.x; k <= c.r1 - c.r0; k += blockDim.x) s_ptr[k] = row_ptr[c.r0 + k];
+    __syncthreads();
+    return c;
+}
+
+// the row holding edge e of the chunk
+__device__ __forceinline__ int32_t chunk_row(const ChunkRows &c, const int32_t *__restrict__ row_ptr,
+                                             const int32_t *s_ptr, int64_t e) {
+    if (!c.staged) return row_of(row_ptr, c.r0, c.r1, e);
+    int32_t lo = 0, hi = c.r1 - c.r0;
+    while (lo < hi) {
+        const int32_t mid = lo + ((hi - lo + 1) >> 1);
+        if ((int64_t)s_ptr[mid] <= e) lo = mid; else hi = mid - 1;
+    }
+    return c.r0 + lo;
+}
 
 
 
@@ -53,29 +87,28 @@ __global__ void col_count_kernel(const int32_t *__restrict__ row_ptr, int32_t n_
     }
 }
 
-// Each block scatters kScatterChunk consecutive edges.  Two threads locate
-// the rows of the chunk's first and last edges; every edge then finds its row
-// by bisection between those two.
+// Each block scatters kScatterChunk consecutive edges, each finding its row
+// by bisection between the rows of the chunk's first and last edges (in LDS
+// when that span is short).
 __global__ void __launch_bounds__(kScatterThreads)
     col_scatter_kernel(const int32_t *__restrict__ row_ptr, int32_t n_rows, int64_t nnz_bound,
                        int32_t n_cols, const int32_t *__restrict__ col_idx,
                        int32_t *__restrict__ cursor, int32_t *__restrict__ rows_tmp,
                        int32_t *__restrict__ perm_tmp, int32_t *__restrict__ cols_tmp) {
     __shared__ int32_t span[2];
+    __shared__ int32_t s_ptr[kSpanMax];
     const int64_t E = edge_count(row_ptr, n_rows, nnz_bound);
     const int64_t e0 = (int64_t)blockIdx.x * kScatterChunk;
     if (e0 >= E) return;  // the whole block leaves together
     const int64_t e1 = e0 + kScatterChunk < E ? e0 + kScatterChunk : E;
-    if (threadIdx.x < 2) span[threadIdx.x] = row_of(row_ptr, 0, n_rows - 1, threadIdx.x ? e1 - 1 : e0);
-    __syncthreads();
-    const int32_t r0 = span[0], r1 = span[1];
+    const ChunkRows cr = chunk_rows(row_ptr, n_rows, e0, e1, span, s_ptr);
 #pragma unroll
     for (int q = 0; q < kScatterItems; ++q) {
         const int64_t e = e0 + q * kScatterThreads + threadIdx.x;
         if (e >= e1) break;
         const int32_t c = col_idx[e];
         if (c < 0 || c >= n_cols) continue;
-        const int32_t r = row_of(row_ptr, r0, r1, e);
+        const int32_t r = chunk_row(cr, row_ptr, s_ptr, e);
         const int32_t pos = atomicAdd(&cursor[c], 1);
         rows_tmp[pos] = r;
         perm_tmp[pos] = (int32_t)e;
@@ -99,23 +132,22 @@ __global__ void col_keys_kernel(const int32_t *__restrict__ row_ptr, int32_t n_r
 
 
 // rowof[e] = the row holding edge e.  Each block takes 1024 consecutive
-// edges: two threads locate the rows of its first and last edge, and every
-// edge then bisects between those two.
+// edges; every edge bisects between the rows of the chunk's first and last
+// edge (in LDS when that span is short).
 __global__ void __launch_bounds__(256)
     edge_rows_kernel(const int32_t *__restrict__ row_ptr, int32_t n_rows, int64_t nnz_bound,
                      int32_t *__restrict__ rowof) {
     __shared__ int32_t span[2];
+    __shared__ int32_t s_ptr[kSpanMax];
     const int64_t E = edge_count(row_ptr, n_rows, nnz_bound);
     const int64_t e0 = (int64_t)blockIdx.x * 1024;
     if (e0 >= E) return;  // the whole block leaves together
     const int64_t e1 = e0 + 1024 < E ? e0 + 1024 : E;
-    if (threadIdx.x < 2) span[threadIdx.x] = row_of(row_ptr, 0, n_rows - 1, threadIdx.x ? e1 - 1 : e0);
-    __syncthreads();
-    const int32_t r0 = span[0], r1 = span[1];
+    const ChunkRows cr = chunk_rows(row_ptr, n_rows, e0, e1, span, s_ptr);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const int64_t e = e0 + q * 256 + threadIdx.x;
-        if (e < e1) rowof[e] = row_of(row_ptr, r0, r1, e);
+        if (e < e1) rowof[e] = chunk_row(cr, row_ptr, s_ptr, e);
     }
 }
 
