@@ -221,11 +221,16 @@ def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256):
     else:
         t["events_count"] = (1, 24 * n_in, 0, False)
         t["events_fill"] = (1, 28 * n_in + 4 * E, 0, False)
-    t["transpose_count"] = (1, 4 * (n_out + 1) + 4 * E + 4 * n_in, 0, False)
-    t["transpose_scatter"] = (1, 4 * (n_out + 1) + 4 * E + 4 * n_in + 12 * E, 0, False)
-    # rank sort of the scattered (column, edge, row) triples: column bounds,
-    # three input arrays, two outputs
-    t["transpose_sort"] = (1, 8 * (n_in + 1) + 20 * E, 0, False)
+    if kind == "points":
+        # block-diagonal transpose, one workgroup per cloud: row bounds and
+        # column indices in, column bounds, rows and edge positions out
+        t["transpose_batched"] = (1, 4 * (n_out + 1) + 4 * E + 4 * (n_in + 1) + 8 * E, 0, False)
+    else:
+        t["transpose_count"] = (1, 4 * (n_out + 1) + 4 * E + 4 * n_in, 0, False)
+        t["transpose_scatter"] = (1, 4 * (n_out + 1) + 4 * E + 4 * n_in + 12 * E, 0, False)
+        # rank sort of the scattered (column, edge, row) triples: column bounds,
+        # three input arrays, two outputs
+        t["transpose_sort"] = (1, 8 * (n_in + 1) + 20 * E, 0, False)
     basis_launches = 0
     csr_b = 4 * (n_out + 1) + 4 * E + 4 * E * M
     csc_b = 4 * (n_in + 1) + 8 * E + 4 * E * M
@@ -385,6 +390,9 @@ def main(argv=None):
         def search():
             return sbc.neighbour_search_points(x_in, s_in, x_out, s_out, w["radius"],
                                                w["k_cap"], sync=False)
+
+        def transpose(csr):  # the batch is block-diagonal: cloud by cloud
+            return sbc.csr_transpose_batched(csr, s_out, s_in)
     else:
         px, py, tt = T(w["px"]), T(w["py"]), T(w["t"])
         geo = sbc.Geometry("event8", tau=w["tau"], px=px, py=py, t=tt)
@@ -393,6 +401,8 @@ def main(argv=None):
         def search():
             return sbc.neighbour_search_events(px, py, tt, w["width"], w["height"], w["window"],
                                                col_capacity=cap, sync=False)
+
+        transpose = sbc.csr_transpose
 
     n_in, n_out = w["n_in"], w["n_out"]
     csr0 = search()
@@ -403,7 +413,7 @@ def main(argv=None):
     def step():
         csr = search()
         Y = sbc.conv_forward(csr, F, W, geometry=geo, order=a.order)
-        csc = sbc.csr_transpose(csr)
+        csc = transpose(csr)
         dF, dW = sbc.conv_backward(csr, csc, F, W, dY, geometry=geo, order=a.order)
         return Y, dF, dW
 

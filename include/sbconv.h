@@ -221,6 +221,22 @@ sbc_status sbc_csr_transpose(const sbc_csr *csr, int32_t *col_ptr, int32_t *row_
                              int32_t *edge_perm, void *workspace, size_t workspace_bytes,
                              hipStream_t stream);
 
+/* The same transpose for a block-diagonal pattern: the CSR of a ragged batch
+ * (Section 3.1, "Ragged Batching"), whose block b has the rows
+ * row_splits[b] .. row_splits[b+1]-1 and the columns col_splits[b] ..
+ * col_splits[b+1]-1 (for a point search: out_splits and in_splits).  Each
+ * block is transposed on its own (one workgroup, in LDS), and the outputs
+ * equal sbc_csr_transpose's.  No workspace.
+ *   row_splits, col_splits [n_batch + 1]  device, int32, non-decreasing, from
+ *                                         0 to n_rows and to n_cols
+ * Entries whose column lies outside their block's columns are not transposed
+ * (such a pattern is not block-diagonal: col_ptr then does not describe
+ * them); every write stays inside col_ptr, row_idx and edge_perm. */
+sbc_status sbc_csr_transpose_batched(const sbc_csr *csr, const int32_t *row_splits,
+                                     const int32_t *col_splits, int32_t n_batch,
+                                     int32_t *col_ptr, int32_t *row_idx, int32_t *edge_perm,
+                                     hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * 4. Forward: Y [n_out, C_out] float32 = sum_m N^(m) F W^(m) (Section 3.1,
  * the matrix-product form).

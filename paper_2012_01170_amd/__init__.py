@@ -4,9 +4,11 @@ The compute path is the HIP library libsbconv.so behind the C ABI declared in
 include/sbconv.h; this package is its thin torch binding.
 """
 from .ops import (CSC, CSR, Geometry, basis_eval, conv_backward, conv_forward,
-                  conv_plan, conv_workspace_size, csr_transpose, neighbour_search_events,
+                  conv_plan, conv_workspace_size, csr_transpose, csr_transpose_batched,
+                  neighbour_search_events,
                   neighbour_search_points, resolve_order)
 
 __all__ = ["CSC", "CSR", "Geometry", "basis_eval", "conv_backward", "conv_forward",
-           "conv_plan", "conv_workspace_size", "csr_transpose", "neighbour_search_events",
+           "conv_plan", "conv_workspace_size", "csr_transpose", "csr_transpose_batched",
+           "neighbour_search_events",
            "neighbour_search_points", "resolve_order"]

@@ -24,7 +24,7 @@ EXPORTS = [
     "sbc_points_workspace_size", "sbc_neighbour_search_points",
     "sbc_events_workspace_size", "sbc_neighbour_search_events",
     "sbc_basis_eval",
-    "sbc_transpose_workspace_size", "sbc_csr_transpose",
+    "sbc_transpose_workspace_size", "sbc_csr_transpose", "sbc_csr_transpose_batched",
     "sbc_conv_workspace_size", "sbc_conv_forward", "sbc_conv_backward",
     "sbc_resolve_order", "sbc_trace_kernel", "sbc_trace_clear", "sbc_kernel_names",
     "sbc_conv_plan",
@@ -81,6 +81,7 @@ _SIGS = {
     "sbc_basis_eval": (ctypes.c_int, [_csr_p, _geo_p, _vp, _vp]),
     "sbc_transpose_workspace_size": (_sz, [_i32, _i64]),
     "sbc_csr_transpose": (ctypes.c_int, [_csr_p, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "sbc_csr_transpose_batched": (ctypes.c_int, [_csr_p, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),
     "sbc_conv_workspace_size": (_sz, [_i32, _i32, _i64, _i32, _i32, _i32, ctypes.c_int,
                                       ctypes.c_int]),
     "sbc_conv_forward": (ctypes.c_int, [_csr_p, _vp, _geo_p, _i32, _vp, _vp, ctypes.c_int, _i32,

@@ -12,7 +12,7 @@ thread_local std::unordered_map<std::string, std::pair<hipEvent_t, hipEvent_t>> 
 
 const char *kKernelNames =
     "points_count,points_fill,events_count,events_fill,basis,"
-    "transpose_count,transpose_scatter,transpose_sort,"
+    "transpose_count,transpose_scatter,transpose_sort,transpose_batched,"
     "fwd_spmm,fwd_gemm,fwd_gemm_h,fwd_spmm_contract,bwd_spmm,bwd_gemm_dw,bwd_gemm_dg,"
     "bwd_spmm_t,bwd_spmm_t_expand,bwd_gemm_df,bwd_gemm_dw_t,fwd_fused,bwd_fused,bwd_dw_reduce";
 }  // namespace
@@ -30,6 +30,18 @@ void trace_after(const char *name, hipStream_t stream) {
 }
 
 void set_error(const std::string &msg) { g_last_error = msg; }
+
+int device_cus() {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+    }
+    return cus;
+}
 void clear_error() { g_last_error.clear(); }
 sbc_status fail(sbc_status st, const std::string &msg) {
     g_last_error = msg;

@@ -105,6 +105,10 @@ sbc_status radix_sort_pairs(const int32_t *keys, const int32_t *vals, const int6
 sbc_status segment_bounds(const int32_t *sorted, const int64_t *n_dev, int64_t n_bound,
                           int32_t key_bound, int32_t *ptr, hipStream_t stream);
 
+// Compute units of the current device (256 if the query fails); sizes
+// persistent grids.
+int device_cus();
+
 inline int grid_for(int64_t n, int block) {
     int64_t g = (n + block - 1) / block;
     return static_cast<int>(g < 1 ? 1 : g);

@@ -1366,18 +1366,6 @@ int basis_mode_of(const float *v, const sbc_geometry *g) {
     return v ? 0 : (int)g->basis + 1;
 }
 
-int device_cus() {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            cus <= 0)
-            cus = 256;
-    }
-    return cus;
-}
-
 sbc_status launch_perm(const void *W, bool bf_in, bool bf_out, int32_t M, int32_t CI, int32_t CO,
                        int64_t s_m, int64_t s_c, int64_t s_p, void *out, hipStream_t stream) {
     const int64_t total = (int64_t)M * CI * CO;

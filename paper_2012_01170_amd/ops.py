@@ -204,6 +204,27 @@ def csr_transpose(csr: CSR) -> CSC:
     return CSC(col_ptr, row_idx, perm, csr.n_cols)
 
 
+def csr_transpose_batched(csr: CSR, row_splits, col_splits) -> CSC:
+    """Transpose of a block-diagonal pattern, block by block (sbc_csr_transpose_batched).
+
+    row_splits / col_splits: int32 device tensors [n_batch + 1] (for a point
+    search, out_splits and in_splits)."""
+    dev = csr.row_ptr.device
+    _require(row_splits, "row_splits", torch.int32, 1, dev)
+    _require(col_splits, "col_splits", torch.int32, 1, dev)
+    n_batch = int(row_splits.numel()) - 1
+    if n_batch < 1 or int(col_splits.numel()) != n_batch + 1:
+        raise ValueError("row_splits and col_splits must have the same length (>= 2)")
+    col_ptr = torch.empty(csr.n_cols + 1, dtype=torch.int32, device=dev)
+    row_idx = torch.empty(max(1, csr.nnz), dtype=torch.int32, device=dev)
+    perm = torch.empty(max(1, csr.nnz), dtype=torch.int32, device=dev)
+    c = csr.c_struct()
+    L.check(L.lib().sbc_csr_transpose_batched(ctypes.byref(c), _p(row_splits), _p(col_splits),
+                                              n_batch, _p(col_ptr), _p(row_idx), _p(perm),
+                                              _stream(dev)))
+    return CSC(col_ptr, row_idx, perm, csr.n_cols)
+
+
 def _dtype_code(F: torch.Tensor) -> int:
     if F.dtype == torch.float32:
         return L.SBC_F32

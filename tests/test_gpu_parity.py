@@ -237,6 +237,51 @@ def test_isolated_and_empty_outputs_are_exact_zero():
     assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
 
 
+POINT_CASES = ["pts_inplace", "pts_down", "pts_uncapped", "pts_cap1", "pts_mono4_odd", "pts_wide",
+               "fz_pts64", "fz_pts_down128", "fz_tiny_pts", "sphere_1024", "ellipsoids_inplace",
+               "ellipsoids_down"]
+
+
+def check_transpose(csc, rp, ci, n_cols):
+    cp, ri, perm = oracle.csr_transpose(rp, ci, n_cols)
+    assert np.array_equal(csc.col_ptr.cpu().numpy(), cp)
+    assert np.array_equal(csc.row_idx[:len(ci)].cpu().numpy(), ri)
+    assert np.array_equal(csc.edge_perm[:len(ci)].cpu().numpy(), perm)
+
+
+@pytest.mark.parametrize("name", POINT_CASES)
+def test_batched_transpose_bit_exact(name):
+    """Block-by-block transpose of a ragged batch's CSR equals the oracle's."""
+    print(f"[transpose batched] {name}", flush=True)
+    w, rp, ci, _ = case(name)
+    t, csr = gpu_case(name)
+    csc = G.sbc.csr_transpose_batched(csr, t["out_splits"], t["in_splits"])
+    check_transpose(csc, rp, ci, w["n_in"])
+
+
+def test_batched_transpose_large_blocks():
+    """Windows halved when a block's columns hold more entries than the LDS
+    stage, and single columns longer than the stage (rows past the staged
+    row bounds too)."""
+    rng = np.random.default_rng(3)
+    x = (rng.random((1500, 3)) * 0.1).astype(np.float32)
+    w = workloads.points_workload(rng, [(x, x[:40])], workloads.BASIS_MONO8, 0.3, 0, 4, 4)
+    rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"], 0.3, 0)
+    assert len(ci) == 40 * 1500
+    t = G.to_device(w)
+    csr = G.search(w, t)
+    check_transpose(G.sbc.csr_transpose_batched(csr, t["out_splits"], t["in_splits"]), rp, ci,
+                    1500)
+    # two blocks of 4500 rows, each row holding all 3 columns of its block
+    n = 9000
+    rp = np.arange(0, 3 * n + 1, 3, dtype=np.int32)
+    ci = np.concatenate([np.arange(3) + (3 if r >= n // 2 else 0) for r in range(n)]).astype(np.int32)
+    csr = G.sbc.CSR(G.dev(rp), G.dev(ci), n, 6, len(ci))
+    splits_r = G.dev(np.array([0, n // 2, n], np.int32))
+    splits_c = G.dev(np.array([0, 3, 6], np.int32))
+    check_transpose(G.sbc.csr_transpose_batched(csr, splits_r, splits_c), rp, ci, 6)
+
+
 @pytest.mark.parametrize("n_batch,k_cap,radius", [(70, 12, 0.35), (130, 0, 0.2), (63, 5, 0.3)])
 def test_many_clouds(n_batch, k_cap, radius):
     """Batches of 63 to 130 clouds (the splits are read by the wave 64 at a
@@ -256,6 +301,8 @@ def test_many_clouds(n_batch, k_cap, radius):
     csr = G.search(w, t)
     assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
     assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+    check_transpose(G.sbc.csr_transpose_batched(csr, t["out_splits"], t["in_splits"]), rp, ci,
+                    len(x))
 
 
 def test_empty_stream_and_cloud():
