@@ -276,6 +276,8 @@ __global__ void __launch_bounds__(kBThreads)
     __shared__ int32_t st_row[kBStage];
     __shared__ int32_t s_rp[kBRows + 1];
     __shared__ int32_t wsum[kBThreads / 64];
+    __shared__ int32_t win_e[kBStage];  // the window's entries, in no order
+    __shared__ int32_t n_win;
     const int b = blockIdx.x / slices, sl = blockIdx.x % slices;
     const int tid = threadIdx.x;
     auto clampi = [](int64_t x, int64_t lo, int64_t hi) {
@@ -335,9 +337,16 @@ __global__ void __launch_bounds__(kBThreads)
     while (cw < c1) {
         if (W > c1 - cw) W = c1 - cw;
         for (int32_t k = tid; k < W; k += kBThreads) cnt[k] = 0;
+        if (tid == 0) n_win = 0;
         __syncthreads();
-        for_edges([&](int64_t, int32_t c) {
-            if (c >= cw && c < cw + W) atomicAdd(&cnt[c - cw], 1);
+        // count the window's entries per column and list them (while the
+        // list fits; a window that overflows it is halved below)
+        for_edges([&](int64_t e, int32_t c) {
+            if (c >= cw && c < cw + W) {
+                atomicAdd(&cnt[c - cw], 1);
+                const int32_t q = atomicAdd(&n_win, 1);
+                if (q < kBStage) win_e[q] = (int32_t)(e - e0);
+            }
         });
         __syncthreads();
         const int32_t total = block_scan_counts(cnt, start, W, wsum);
@@ -365,16 +374,18 @@ __global__ void __launch_bounds__(kBThreads)
                 }
             }
         } else {
-            // stage every entry at its column's slot (any order within the column)
+            // stage every listed entry at its column's slot (any order within
+            // the column): one listed entry per thread and step, so the row
+            // lookups do not diverge over entries outside the window
             for (int32_t k = tid; k < W; k += kBThreads) cnt[k] = 0;
             __syncthreads();
-            for_edges([&](int64_t e, int32_t c) {
-                if (c >= cw && c < cw + W) {
-                    const int32_t slot = start[c - cw] + atomicAdd(&cnt[c - cw], 1);
-                    st_edge[slot] = (int32_t)e;
-                    st_row[slot] = row_of_edge(e);
-                }
-            });
+            for (int32_t q = tid; q < total; q += kBThreads) {
+                const int64_t e = e0 + win_e[q];
+                const int32_t c = col_idx[e];
+                const int32_t slot = start[c - cw] + atomicAdd(&cnt[c - cw], 1);
+                st_edge[slot] = (int32_t)e;
+                st_row[slot] = row_of_edge(e);
+            }
             __syncthreads();
             // order each column by edge index: an entry's rank among its column's
             for (int32_t q = tid; q < total; q += kBThreads) {
