@@ -56,6 +56,17 @@ __device__ __forceinline__ uint32_t hash_cell(int32_t b, int32_t cx, int32_t cy,
     return h;
 }
 
+// Bucket of cell (cx, cy, cz) of cloud b, whose inputs are j_lo ..
+// j_lo + n_b - 1: every cloud owns the 2 n_b + 1 buckets from 2 j_lo + b, so
+// clouds never share a bucket and a cloud's table can be built on its own.
+// The result is clamped below T (only malformed splits need it).
+__device__ __forceinline__ uint32_t cloud_bucket(int32_t b, int32_t j_lo, int32_t n_b,
+                                                 uint32_t T, int32_t cx, int32_t cy, int32_t cz) {
+    const uint32_t nb = n_b > 0 ? (uint32_t)n_b : 0u;
+    const uint32_t k = 2u * (uint32_t)j_lo + (uint32_t)b + hash_cell(b, cx, cy, cz) % (2u * nb + 1u);
+    return k < T ? k : T - 1u;
+}
+
 __device__ __forceinline__ int32_t cell_coord(float x, double inv_h) {
     double c = floor((double)x * inv_h);
     // clamping is monotone, so adjacent cells stay adjacent; NaN -> 0
@@ -129,7 +140,7 @@ constexpr int kSplitsInLds = 1024;     // key pass: splits bisected in LDS up to
 __global__ void __launch_bounds__(kKeyThreads)
     key_kernel(const float *__restrict__ x_in, int32_t n_in,
                const int32_t *__restrict__ in_splits, const int32_t *__restrict__ out_splits,
-               int32_t n_out, int32_t n_batch, double inv_h, uint32_t table_mask,
+               int32_t n_out, int32_t n_batch, double inv_h, uint32_t T,
                uint32_t *__restrict__ keys, int32_t *__restrict__ counts, uint32_t *status) {
     __shared__ int32_t s_splits[kSplitsInLds];
     const bool lds = n_batch < kSplitsInLds;
@@ -147,10 +158,11 @@ __global__ void __launch_bounds__(kKeyThreads)
         if (bad) atomicOr(status, (uint32_t)kFlagBadSplits);
     }
     if (j >= n_in) return;
-    int32_t b = cloud_of(lds ? s_splits : in_splits, n_batch, j);
+    const int32_t *sp = lds ? s_splits : in_splits;
+    int32_t b = cloud_of(sp, n_batch, j);
     float x = x_in[3 * (int64_t)j], y = x_in[3 * (int64_t)j + 1], z = x_in[3 * (int64_t)j + 2];
-    uint32_t key = hash_cell(b, cell_coord(x, inv_h), cell_coord(y, inv_h), cell_coord(z, inv_h)) &
-                   table_mask;
+    uint32_t key = cloud_bucket(b, sp[b], sp[b + 1] - sp[b], T, cell_coord(x, inv_h),
+                                cell_coord(y, inv_h), cell_coord(z, inv_h));
     keys[j] = key;
     atomicAdd(&counts[key], 1);
 }
@@ -169,6 +181,117 @@ __global__ void scatter_kernel(const float *__restrict__ x_in, int32_t n_in,
     table[pos] = r;
 }
 
+// One workgroup per cloud builds that cloud's cell table (the count, scan
+// and scatter of the multi-kernel build, in one launch): counts in LDS when
+// the cloud's buckets fit (kLdsBuckets), else in the global count array; the
+// scan of the counts runs over the cloud's buckets in chunks with a carried
+// total.  Workgroup 0 also clears the status word and checks the splits.
+constexpr int kCloudThreads = 512;
+constexpr int kLdsBuckets = 8193;      // 2 * 4096 + 1
+constexpr int kLdsPoints = 4096;
+
+__global__ void __launch_bounds__(kCloudThreads)
+    cloud_table_kernel(const float *__restrict__ x_in, int32_t n_in,
+                       const int32_t *__restrict__ in_splits,
+                       const int32_t *__restrict__ out_splits, int32_t n_out, int32_t n_batch,
+                       double inv_h, uint32_t T, uint32_t *__restrict__ keys,
+                       int32_t *__restrict__ counts, int32_t *__restrict__ cell_start,
+                       int32_t *__restrict__ cursor, PointRec *__restrict__ table,
+                       uint32_t *status) {
+    __shared__ int32_t s_cnt[kLdsBuckets];
+    __shared__ uint32_t s_key[kLdsPoints];
+    __shared__ int32_t wsum[kCloudThreads / 64];
+    __shared__ int32_t s_carry;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int b = blockIdx.x;
+    if (b == 0) {
+        if (tid == 0) *status = 0u;
+        __syncthreads();
+        for (int32_t k = tid; k <= n_batch; k += kCloudThreads) {
+            bool bad = false;
+            if (k == 0) bad = in_splits[0] != 0 || out_splits[0] != 0;
+            if (k == n_batch) bad = bad || in_splits[k] != n_in || out_splits[k] != n_out;
+            if (k > 0) bad = bad || in_splits[k] < in_splits[k - 1] || out_splits[k] < out_splits[k - 1];
+            if (bad) atomicOr(status, (uint32_t)kFlagBadSplits);
+        }
+    }
+    const int32_t j_lo = min(max(in_splits[b], 0), n_in);
+    const int32_t j_hi = min(max(in_splits[b + 1], j_lo), n_in);
+    const int32_t n_b = j_hi - j_lo;
+    const uint32_t off = 2u * (uint32_t)j_lo + (uint32_t)b;
+    const uint32_t Tb = 2u * (uint32_t)n_b + 1u;
+    if (off >= T) return;  // only malformed splits get here (the whole workgroup)
+    const uint32_t nbk = off + Tb <= T ? Tb : T - off;  // buckets written
+    const bool lds = Tb <= (uint32_t)kLdsBuckets;
+    int32_t *cnt = lds ? s_cnt : counts + off;
+    for (uint32_t k = tid; k < nbk; k += kCloudThreads) cnt[k] = 0;
+    __syncthreads();
+    for (int32_t p = tid; p < n_b; p += kCloudThreads) {
+        const int32_t j = j_lo + p;
+        const uint32_t key = cloud_bucket(b, j_lo, n_b, T, cell_coord(x_in[3 * (int64_t)j], inv_h),
+                                          cell_coord(x_in[3 * (int64_t)j + 1], inv_h),
+                                          cell_coord(x_in[3 * (int64_t)j + 2], inv_h)) - off;
+        if (lds) s_key[p] = key; else keys[j] = key;
+        atomicAdd(&cnt[key], 1);
+    }
+    __syncthreads();
+    // exclusive scan of the cloud's counts, in place, chunk by chunk
+    if (tid == 0) s_carry = 0;
+    __syncthreads();
+    for (uint32_t c0 = 0; c0 < nbk; c0 += 4 * kCloudThreads) {
+        int32_t v[4], sum = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t k = c0 + 4 * tid + q;
+            v[q] = k < nbk ? cnt[k] : 0;
+            sum += v[q];
+        }
+        int32_t x = sum;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int32_t y = __shfl_up(x, d, 64);
+            if (lane >= d) x += y;
+        }
+        if (lane == 63) wsum[wave] = x;
+        __syncthreads();
+        int32_t before = s_carry, tot = 0;
+#pragma unroll
+        for (int w = 0; w < kCloudThreads / 64; ++w) {
+            before += w < wave ? wsum[w] : 0;
+            tot += wsum[w];
+        }
+        int32_t run = before + x - sum;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t k = c0 + 4 * tid + q;
+            if (k < nbk) {
+                cnt[k] = run;  // now the bucket's start within the cloud
+                cell_start[off + k] = j_lo + run;
+                if (!lds) cursor[off + k] = run;
+            }
+            run += v[q];
+        }
+        __syncthreads();
+        if (tid == 0) s_carry += tot;
+        __syncthreads();
+    }
+    if (tid == 0) cell_start[off + nbk] = j_lo + n_b;  // the next cloud's start, or the end
+    __syncthreads();
+    // scatter the records; the bucket starts serve as cursors
+    int32_t *cur = lds ? s_cnt : cursor + off;
+    for (int32_t p = tid; p < n_b; p += kCloudThreads) {
+        const int32_t j = j_lo + p;
+        const uint32_t key = lds ? s_key[p] : keys[j];
+        const int32_t pos = atomicAdd(&cur[key], 1);
+        PointRec r;
+        r.x = x_in[3 * (int64_t)j];
+        r.y = x_in[3 * (int64_t)j + 1];
+        r.z = x_in[3 * (int64_t)j + 2];
+        r.j = j;
+        table[j_lo + pos] = r;
+    }
+}
+
 struct RowCtx {
     float qx, qy, qz;
     int32_t j_lo, j_hi;  // input range of the row's cloud
@@ -179,7 +302,7 @@ struct RowCtx {
 // removed; lane k < 27 holds cell k.  Returns the candidate count; lane k's
 // range start and its exclusive offset into the flattened candidate list go
 // to lds_start/lds_off (27 entries each).
-__device__ int32_t gather_buckets(const RowCtx &c, int32_t b, double inv_h, uint32_t table_mask,
+__device__ int32_t gather_buckets(const RowCtx &c, int32_t b, double inv_h, uint32_t T,
                                   const int32_t *__restrict__ cell_start, int32_t *lds_start,
                                   int32_t *lds_off) {
     const int lane = threadIdx.x & 63;
@@ -188,7 +311,7 @@ __device__ int32_t gather_buckets(const RowCtx &c, int32_t b, double inv_h, uint
     int32_t s = 0, len = 0;
     if (lane < 27) {
         int32_t dx = lane % 3 - 1, dy = (lane / 3) % 3 - 1, dz = lane / 9 - 1;
-        bucket = hash_cell(b, cx + dx, cy + dy, cz + dz) & table_mask;
+        bucket = cloud_bucket(b, c.j_lo, c.j_hi - c.j_lo, T, cx + dx, cy + dy, cz + dz);
     }
     bool dup = false;
     for (int q = 0; q < 27; ++q) {
@@ -243,7 +366,7 @@ template <int kMode>
 __global__ void __launch_bounds__(kWaves * 64)
     rows_kernel(const float *__restrict__ x_out, int32_t n_out,
                 const int32_t *__restrict__ in_splits, const int32_t *__restrict__ out_splits,
-                int32_t n_batch, float radius, int32_t k_cap, double inv_h, uint32_t table_mask,
+                int32_t n_batch, float radius, int32_t k_cap, double inv_h, uint32_t T,
                 const int32_t *__restrict__ cell_start, const PointRec *__restrict__ table,
                 int32_t *__restrict__ row_len, const int32_t *__restrict__ row_ptr,
                 int32_t *__restrict__ col_idx, int64_t col_capacity) {
@@ -265,7 +388,7 @@ __global__ void __launch_bounds__(kWaves * 64)
     const int32_t b = wave_cloud(out_splits, in_splits, n_batch, i, &c.j_lo, &c.j_hi);
     c.r2 = __fmul_rn(radius, radius);
 
-    const int32_t total = gather_buckets(c, b, inv_h, table_mask, cell_start, s_start[w], s_off[w]);
+    const int32_t total = gather_buckets(c, b, inv_h, T, cell_start, s_start[w], s_off[w]);
     wave_lds_sync();
 
     if (!kFill) {
@@ -436,10 +559,9 @@ __global__ void compact_rows_kernel(const int32_t *__restrict__ rows,
 
 bool one_pass(int32_t k_cap) { return k_cap >= 1 && k_cap <= kStage; }
 
-uint32_t table_size_for(int32_t n_in) {
-    uint32_t t = 1024;
-    while (t < 2u * (uint32_t)(n_in > 0 ? n_in : 1) && t < (1u << 30)) t <<= 1;
-    return t;
+// Buckets of all clouds: 2 n_b + 1 per cloud.
+uint32_t table_size_for(int32_t n_in, int32_t n_batch) {
+    return 2u * (uint32_t)(n_in > 0 ? n_in : 0) + (uint32_t)(n_batch > 0 ? n_batch : 1);
 }
 
 struct PointsWs {
@@ -455,10 +577,10 @@ struct PointsWs {
     void *scan_ws;
 };
 
-PointsWs carve_points(void *base, int32_t n_in, int32_t n_out, int32_t /*n_batch*/,
+PointsWs carve_points(void *base, int32_t n_in, int32_t n_out, int32_t n_batch,
                       int32_t k_cap, size_t *bytes) {
     Carver cv(base);
-    const uint32_t T = table_size_for(n_in);
+    const uint32_t T = table_size_for(n_in, n_batch);
     PointsWs w;
     w.keys = cv.take<uint32_t>(n_in);
     w.cell_count = cv.take<int32_t>(T);
@@ -506,10 +628,18 @@ extern "C" sbc_status sbc_neighbour_search_points(
     if (!workspace || workspace_bytes < need)
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_points_workspace_size()");
 
-    const uint32_t T = table_size_for(n_in);
+    if (n_in > (1 << 30)) return fail(SBC_ERR_INVALID_ARG, "n_in must be at most 2^30");
+    const uint32_t T = table_size_for(n_in, n_batch);
     const double inv_h = 1.0 / ((double)radius * kCellMargin);
 
-    {
+    if ((int64_t)n_in <= 1024 * (int64_t)n_batch) {
+        // clouds of about a thousand points or fewer on average: one workgroup
+        // per cloud builds its table in one launch
+        hipLaunchKernelGGL(cloud_table_kernel, dim3((unsigned)n_batch), dim3(kCloudThreads), 0,
+                           stream, x_in, n_in, in_splits, out_splits, n_out, n_batch, inv_h, T,
+                           ws.keys, ws.cell_count, ws.cell_start, ws.cursor, ws.table, ws.status);
+        SBC_LAUNCH_CHECK();
+    } else {
         const int g = grid_for(T, 256) < 1024 ? grid_for(T, 256) : 1024;
         hipLaunchKernelGGL(init_kernel, dim3(g), dim3(256), 0, stream, ws.cell_count, T,
                            ws.status);
@@ -517,16 +647,16 @@ extern "C" sbc_status sbc_neighbour_search_points(
         const int64_t kn = (int64_t)n_in > (int64_t)n_batch + 1 ? n_in : (int64_t)n_batch + 1;
         hipLaunchKernelGGL(key_kernel, dim3(grid_for(kn, kKeyThreads)), dim3(kKeyThreads), 0,
                            stream, x_in, n_in,
-                           in_splits, out_splits, n_out, n_batch, inv_h, T - 1, ws.keys,
+                           in_splits, out_splits, n_out, n_batch, inv_h, T, ws.keys,
                            ws.cell_count, ws.status);
         SBC_LAUNCH_CHECK();
-    }
-    SBC_TRY(exclusive_scan_i32(ws.cell_count, ws.cell_start, T, ws.total + 1, ws.scan_ws, stream,
-                               ws.cursor));
-    if (n_in > 0) {
-        hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(n_in, 256)), dim3(256), 0, stream, x_in,
-                           n_in, ws.keys, ws.cursor, ws.table);
-        SBC_LAUNCH_CHECK();
+        SBC_TRY(exclusive_scan_i32(ws.cell_count, ws.cell_start, T, ws.total + 1, ws.scan_ws,
+                                   stream, ws.cursor));
+        if (n_in > 0) {
+            hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(n_in, 256)), dim3(256), 0, stream,
+                               x_in, n_in, ws.keys, ws.cursor, ws.table);
+            SBC_LAUNCH_CHECK();
+        }
     }
     const int row_blocks = grid_for(n_out, kWaves);
     const bool single = one_pass(k_cap);
@@ -535,12 +665,12 @@ extern "C" sbc_status sbc_neighbour_search_points(
         if (single)
             hipLaunchKernelGGL((rows_kernel<2>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
                                x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
-                               T - 1, ws.cell_start, ws.table, ws.row_len,
+                               T, ws.cell_start, ws.table, ws.row_len,
                                (const int32_t *)nullptr, ws.rows, (int64_t)n_out * k_cap);
         else
             hipLaunchKernelGGL((rows_kernel<0>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
                                x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
-                               T - 1, ws.cell_start, ws.table, ws.row_len,
+                               T, ws.cell_start, ws.table, ws.row_len,
                                (const int32_t *)nullptr, (int32_t *)nullptr, (int64_t)0);
         SBC_LAUNCH_CHECK();
         trace_after("points_count", stream);
@@ -574,7 +704,7 @@ extern "C" sbc_status sbc_neighbour_search_points(
         } else {
             hipLaunchKernelGGL((rows_kernel<1>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
                                x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap,
-                               inv_h, T - 1, ws.cell_start, ws.table, ws.row_len, row_ptr,
+                               inv_h, T, ws.cell_start, ws.table, ws.row_len, row_ptr,
                                col_idx, col_capacity);
         }
         SBC_LAUNCH_CHECK();

@@ -305,6 +305,24 @@ def test_many_clouds(n_batch, k_cap, radius):
                     len(x))
 
 
+@pytest.mark.parametrize("sizes", [[5000] + [0] * 8 + [10], [1100, 1200]])
+def test_cloud_table_builds(sizes):
+    """Batches whose average cloud is small take the per-cloud table build: a
+    5000-point cloud among empty ones counts in global memory there; a batch
+    of larger clouds takes the multi-kernel build."""
+    print(f"[cloud tables] {sizes}", flush=True)
+    rng = np.random.default_rng(len(sizes))
+    clouds = [workloads.ellipsoid_surface_points(rng, n, np.array([1.0, 0.8, 0.6])) if n else
+              np.zeros((0, 3)) for n in sizes]
+    w = workloads.points_workload(rng, [(x, x) for x in clouds], workloads.BASIS_MONO8, 0.08, 16,
+                                  4, 4)
+    rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"], 0.08, 16)
+    t = G.to_device(w)
+    csr = G.search(w, t)
+    assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
+    assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+
+
 def test_empty_stream_and_cloud():
     z = torch.zeros(0, dtype=torch.int32, device=G.DEV)
     csr = G.sbc.neighbour_search_events(z, z, z, 8, 8, 100)
