@@ -29,7 +29,7 @@
 namespace sbc {
 namespace {
 
-constexpr int kWaves = 4;              // waves per block, one output row per wave
+constexpr int kWaves = 4;              // waves per block
 constexpr int kStage = 512;            // in-ball candidates staged per wave in LDS
 constexpr double kCellMargin = 1.0 + 1.0 / 1024.0;
 
@@ -86,29 +86,48 @@ __device__ __forceinline__ int32_t cloud_of(const int32_t *splits, int32_t n_bat
     return lo;
 }
 
-// Cloud b of the output index i, the same on every lane of the wave, and the
-// input range [*j_lo, *j_hi) of that cloud.  The splits are read across the
-// wave, 64 at a time, and b counts the interior splits at or below i, which
-// for non-decreasing splits is the bisection's answer.  With fewer than 64
-// clouds the input splits are read in the same round trip and picked out by
-// lane.
-__device__ __forceinline__ int32_t wave_cloud(const int32_t *__restrict__ out_splits,
-                                              const int32_t *__restrict__ in_splits,
-                                              int32_t n_batch, int32_t i, int32_t *j_lo,
-                                              int32_t *j_hi) {
-    const int lane = threadIdx.x & 63;
-    if (n_batch < 64) {
-        const int32_t so = lane <= n_batch ? out_splits[lane] : 0;
-        const int32_t si = lane <= n_batch ? in_splits[lane] : 0;
-        const int32_t b = __popcll(__ballot(lane >= 1 && lane < n_batch && so <= i));
-        *j_lo = __shfl(si, b, 64);
-        *j_hi = __shfl(si, b + 1, 64);
+// The L lanes of a wave that serve one row (L = 64 or 32): sl is the lane
+// within the segment; ballots are restricted to the segment's lanes.
+template <int L>
+struct Seg {
+    int lane, sl, grp;
+    uint64_t full;
+    __device__ Seg() {
+        lane = threadIdx.x & 63;
+        sl = lane % L;
+        grp = lane / L;
+        full = L == 64 ? ~0ull : (((1ull << L) - 1ull) << (grp * L));
+    }
+    __device__ uint64_t ballot(bool p) const { return __ballot(p) & full; }
+    // lanes of the segment below this one among those set in m
+    __device__ int below(uint64_t m) const { return __popcll(m & ((1ull << lane) - 1ull)); }
+    __device__ int32_t shfl(int32_t v, int q) const { return __shfl(v, grp * L + q, 64); }
+};
+
+// Cloud b of the output index i, the same on every lane of the segment, and
+// the input range [*j_lo, *j_hi) of that cloud.  The splits are read across
+// the segment, L at a time, and b counts the interior splits at or below i,
+// which for non-decreasing splits is the bisection's answer.  With fewer
+// than L clouds the input splits are read in the same round trip and picked
+// out by lane.
+template <int L>
+__device__ __forceinline__ int32_t seg_cloud(const Seg<L> &sg, const int32_t *__restrict__ out_splits,
+                                             const int32_t *__restrict__ in_splits,
+                                             int32_t n_batch, int32_t i, int32_t *j_lo,
+                                             int32_t *j_hi) {
+    const int sl = sg.sl;
+    if (n_batch < L) {
+        const int32_t so = sl <= n_batch ? out_splits[sl] : 0;
+        const int32_t si = sl <= n_batch ? in_splits[sl] : 0;
+        const int32_t b = __popcll(sg.ballot(sl >= 1 && sl < n_batch && so <= i));
+        *j_lo = sg.shfl(si, b);
+        *j_hi = sg.shfl(si, b + 1);
         return b;
     }
     int32_t b = 0;
-    for (int32_t base = 1; base < n_batch; base += 64) {
-        const int32_t k = base + lane;
-        b += __popcll(__ballot(k < n_batch && out_splits[k] <= i));
+    for (int32_t base = 1; base < n_batch; base += L) {
+        const int32_t k = base + sl;
+        b += __popcll(sg.ballot(k < n_batch && out_splits[k] <= i));
     }
     *j_lo = in_splits[b];
     *j_hi = in_splits[b + 1];
@@ -298,41 +317,43 @@ struct RowCtx {
     float r2;
 };
 
-// Per wave: bucket ranges of the 27 cells around the query, duplicates
-// removed; lane k < 27 holds cell k.  Returns the candidate count; lane k's
-// range start and its exclusive offset into the flattened candidate list go
-// to lds_start/lds_off (27 entries each).
-__device__ int32_t gather_buckets(const RowCtx &c, int32_t b, double inv_h, uint32_t T,
-                                  const int32_t *__restrict__ cell_start, int32_t *lds_start,
-                                  int32_t *lds_off) {
-    const int lane = threadIdx.x & 63;
+// Per segment: bucket ranges of the 27 cells around the query, duplicates
+// removed; lane k < 27 of the segment holds cell k.  Returns the candidate
+// count; lane k's range start and its exclusive offset into the flattened
+// candidate list go to lds_start/lds_off (27 entries each).
+template <int L>
+__device__ int32_t gather_buckets(const Seg<L> &sg, const RowCtx &c, int32_t b, double inv_h,
+                                  uint32_t T, const int32_t *__restrict__ cell_start,
+                                  int32_t *lds_start, int32_t *lds_off) {
+    static_assert(L >= 27, "a lane per cell");
+    const int sl = sg.sl;
     int32_t cx = cell_coord(c.qx, inv_h), cy = cell_coord(c.qy, inv_h), cz = cell_coord(c.qz, inv_h);
     uint32_t bucket = 0xFFFFFFFFu;
     int32_t s = 0, len = 0;
-    if (lane < 27) {
-        int32_t dx = lane % 3 - 1, dy = (lane / 3) % 3 - 1, dz = lane / 9 - 1;
+    if (sl < 27) {
+        int32_t dx = sl % 3 - 1, dy = (sl / 3) % 3 - 1, dz = sl / 9 - 1;
         bucket = cloud_bucket(b, c.j_lo, c.j_hi - c.j_lo, T, cx + dx, cy + dy, cz + dz);
     }
     bool dup = false;
     for (int q = 0; q < 27; ++q) {
-        uint32_t bq = __shfl(bucket, q, 64);
-        if (q < lane && bq == bucket) dup = true;
+        uint32_t bq = (uint32_t)sg.shfl((int32_t)bucket, q);
+        if (q < sl && bq == bucket) dup = true;
     }
-    if (lane < 27 && !dup) {
+    if (sl < 27 && !dup) {
         s = cell_start[bucket];
         len = cell_start[bucket + 1] - s;
     }
-    // exclusive scan of len over the wave
+    // exclusive scan of len over the segment
     int32_t incl = len;
 #pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
+    for (int d = 1; d < L; d <<= 1) {
         int32_t y = __shfl_up(incl, d, 64);
-        if (lane >= d) incl += y;
+        if (sl >= d) incl += y;
     }
-    int32_t total = __shfl(incl, 63, 64);
-    if (lane < 27) {
-        lds_start[lane] = s;
-        lds_off[lane] = incl - len;
+    int32_t total = sg.shfl(incl, L - 1);
+    if (sl < 27) {
+        lds_start[sl] = s;
+        lds_off[sl] = incl - len;
     }
     return total;
 }
@@ -361,8 +382,9 @@ __device__ __forceinline__ bool key_less(float da, int32_t ja, float db, int32_t
 
 // kMode: 0 count pass; 1 fill pass into the CSR (row i at row_ptr[i]);
 // 2 fill pass into rows of stride k_cap (row i at i * k_cap, col_capacity =
-// n_out * k_cap), writing the row lengths too.
-template <int kMode>
+// n_out * k_cap), writing the row lengths too.  A row takes L lanes (a wave
+// holds 64 / L rows), with a stage of kStage * L / 64 candidates.
+template <int kMode, int L>
 __global__ void __launch_bounds__(kWaves * 64)
     rows_kernel(const float *__restrict__ x_out, int32_t n_out,
                 const int32_t *__restrict__ in_splits, const int32_t *__restrict__ out_splits,
@@ -370,60 +392,64 @@ __global__ void __launch_bounds__(kWaves * 64)
                 const int32_t *__restrict__ cell_start, const PointRec *__restrict__ table,
                 int32_t *__restrict__ row_len, const int32_t *__restrict__ row_ptr,
                 int32_t *__restrict__ col_idx, int64_t col_capacity) {
-    __shared__ int32_t s_start[kWaves][27];
-    __shared__ int32_t s_off[kWaves][27];
+    constexpr int G = 64 / L;                 // rows per wave
+    constexpr int kStageL = kStage / G;       // staged candidates per row
+    constexpr int kRows = kWaves * G;         // rows per block
+    __shared__ int32_t s_start[kRows][27];
+    __shared__ int32_t s_off[kRows][27];
     constexpr bool kFill = kMode != 0;
-    __shared__ float s_d2[kFill ? kWaves : 1][kFill ? kStage : 1];
-    __shared__ int32_t s_j[kFill ? kWaves : 1][kFill ? kStage : 1];
+    __shared__ float s_d2[kFill ? kRows : 1][kFill ? kStageL : 1];
+    __shared__ int32_t s_j[kFill ? kRows : 1][kFill ? kStageL : 1];
 
-    const int lane = threadIdx.x & 63;
-    const int w = threadIdx.x >> 6;
-    const int32_t i = blockIdx.x * kWaves + w;
-    if (i >= n_out) return;  // whole wave leaves together: no block barrier below
+    const Seg<L> sg;
+    const int sl = sg.sl;
+    const int rw = (threadIdx.x >> 6) * G + sg.grp;  // row within the block
+    const int32_t i = blockIdx.x * kRows + rw;
+    if (i >= n_out) return;  // a segment leaves on its own: no block barrier below
 
     RowCtx c;
     c.qx = x_out[3 * (int64_t)i];
     c.qy = x_out[3 * (int64_t)i + 1];
     c.qz = x_out[3 * (int64_t)i + 2];
-    const int32_t b = wave_cloud(out_splits, in_splits, n_batch, i, &c.j_lo, &c.j_hi);
+    const int32_t b = seg_cloud(sg, out_splits, in_splits, n_batch, i, &c.j_lo, &c.j_hi);
     c.r2 = __fmul_rn(radius, radius);
 
-    const int32_t total = gather_buckets(c, b, inv_h, T, cell_start, s_start[w], s_off[w]);
+    const int32_t total = gather_buckets(sg, c, b, inv_h, T, cell_start, s_start[rw], s_off[rw]);
     wave_lds_sync();
 
     if (!kFill) {
         int32_t n = 0;
-        for (int32_t base = 0; base < total; base += 64) {
-            int32_t cc = base + lane;
+        for (int32_t base = 0; base < total; base += L) {
+            int32_t cc = base + sl;
             bool hit = false;
             if (cc < total) {
-                PointRec p = table[candidate_pos(cc, s_start[w], s_off[w])];
+                PointRec p = table[candidate_pos(cc, s_start[rw], s_off[rw])];
                 float d2;
                 hit = in_ball(c, p, &d2);
             }
-            n += __popcll(__ballot(hit));
+            n += __popcll(sg.ballot(hit));
         }
-        if (lane == 0) row_len[i] = (k_cap > 0 && n > k_cap) ? k_cap : n;
+        if (sl == 0) row_len[i] = (k_cap > 0 && n > k_cap) ? k_cap : n;
         return;
     }
 
     // ---- fill pass: stage the in-ball candidates
     int32_t n = 0;
-    for (int32_t base = 0; base < total; base += 64) {
-        int32_t cc = base + lane;
+    for (int32_t base = 0; base < total; base += L) {
+        int32_t cc = base + sl;
         bool hit = false;
         float d2 = 0.f;
         int32_t j = 0;
         if (cc < total) {
-            PointRec p = table[candidate_pos(cc, s_start[w], s_off[w])];
+            PointRec p = table[candidate_pos(cc, s_start[rw], s_off[rw])];
             hit = in_ball(c, p, &d2);
             j = p.j;
         }
-        uint64_t mask = __ballot(hit);
-        int32_t slot = n + __popcll(mask & ((1ull << lane) - 1ull));
-        if (hit && slot < kStage) {
-            s_d2[w][slot] = d2;
-            s_j[w][slot] = j;
+        const uint64_t mask = sg.ballot(hit);
+        int32_t slot = n + sg.below(mask);
+        if (hit && slot < kStageL) {
+            s_d2[rw][slot] = d2;
+            s_j[rw][slot] = j;
         }
         n += __popcll(mask);
     }
@@ -431,39 +457,39 @@ __global__ void __launch_bounds__(kWaves * 64)
     const int32_t out0 = kMode == 2 ? i * k_cap : row_ptr[i];
     const bool capped = k_cap > 0 && n > k_cap;
     const int32_t n_keep = capped ? k_cap : n;
-    if (kMode == 2 && lane == 0) row_len[i] = n_keep;
+    if (kMode == 2 && sl == 0) row_len[i] = n_keep;
 
-    if (n <= kStage) {
+    if (n <= kStageL) {
         if (capped) {
             // keep the entries whose rank on (d2, j) is below k_cap; a dropped
             // entry gets bit 31 set in its staged j, which orders it (as an
             // unsigned number) after every kept one
-            constexpr int kPerLane = kStage / 64;
+            constexpr int kPerLane = kStageL / L;
             bool drop[kPerLane];
 #pragma unroll
             for (int u = 0; u < kPerLane; ++u) {
-                const int32_t a = lane + 64 * u;
+                const int32_t a = sl + L * u;
                 drop[u] = false;
                 if (a < n) {
-                    const float da = s_d2[w][a];
-                    const int32_t ja = s_j[w][a];
+                    const float da = s_d2[rw][a];
+                    const int32_t ja = s_j[rw][a];
                     int32_t rank = 0;
-                    for (int32_t q = 0; q < n; ++q) rank += key_less(s_d2[w][q], s_j[w][q], da, ja);
+                    for (int32_t q = 0; q < n; ++q) rank += key_less(s_d2[rw][q], s_j[rw][q], da, ja);
                     drop[u] = rank >= k_cap;
                 }
             }
             wave_lds_sync();
 #pragma unroll
             for (int u = 0; u < kPerLane; ++u)
-                if (drop[u]) s_j[w][lane + 64 * u] |= INT32_MIN;
+                if (drop[u]) s_j[rw][sl + L * u] |= INT32_MIN;
             wave_lds_sync();
         }
         // position among the kept entries by rank on j
-        for (int32_t a = lane; a < n; a += 64) {
-            const uint32_t ja = (uint32_t)s_j[w][a];
+        for (int32_t a = sl; a < n; a += L) {
+            const uint32_t ja = (uint32_t)s_j[rw][a];
             if (ja & 0x80000000u) continue;
             int32_t pos = 0;
-            for (int32_t q = 0; q < n; ++q) pos += ((uint32_t)s_j[w][q] < ja) ? 1 : 0;
+            for (int32_t q = 0; q < n; ++q) pos += ((uint32_t)s_j[rw][q] < ja) ? 1 : 0;
             int64_t dst = (int64_t)out0 + pos;
             if (dst < col_capacity) col_idx[dst] = (int32_t)ja;
         }
@@ -480,44 +506,44 @@ __global__ void __launch_bounds__(kWaves * 64)
         while (lo < hi) {
             const uint64_t mid = lo + ((hi - lo) >> 1);
             int32_t cnt = 0;
-            for (int32_t base = 0; base < total; base += 64) {
-                int32_t cc = base + lane;
+            for (int32_t base = 0; base < total; base += L) {
+                int32_t cc = base + sl;
                 bool le = false;
                 if (cc < total) {
-                    PointRec p = table[candidate_pos(cc, s_start[w], s_off[w])];
+                    PointRec p = table[candidate_pos(cc, s_start[rw], s_off[rw])];
                     float d2;
                     if (in_ball(c, p, &d2))
                         le = (((uint64_t)__float_as_uint(d2) << 32) | (uint32_t)p.j) <= mid;
                 }
-                cnt += __popcll(__ballot(le));
+                cnt += __popcll(sg.ballot(le));
             }
             if (cnt >= k_cap) hi = mid; else lo = mid + 1;
         }
         threshold = lo;
     }
     // stage the kept column indices when they fit, else rank against the cells
-    const bool staged = n_keep <= kStage;
+    const bool staged = n_keep <= kStageL;
     int32_t m = 0;
-    for (int32_t base = 0; base < total; base += 64) {
-        int32_t cc = base + lane;
+    for (int32_t base = 0; base < total; base += L) {
+        int32_t cc = base + sl;
         bool keep = false;
         int32_t j = 0;
         if (cc < total) {
-            PointRec p = table[candidate_pos(cc, s_start[w], s_off[w])];
+            PointRec p = table[candidate_pos(cc, s_start[rw], s_off[rw])];
             float d2;
             if (in_ball(c, p, &d2)) {
                 keep = (((uint64_t)__float_as_uint(d2) << 32) | (uint32_t)p.j) <= threshold;
                 j = p.j;
             }
         }
-        uint64_t mask = __ballot(keep);
+        const uint64_t mask = sg.ballot(keep);
         if (staged) {
-            int32_t slot = m + __popcll(mask & ((1ull << lane) - 1ull));
-            if (keep) s_j[w][slot] = j;
+            int32_t slot = m + sg.below(mask);
+            if (keep) s_j[rw][slot] = j;
         } else if (keep) {
             int32_t pos = 0;
             for (int32_t q = 0; q < total; ++q) {
-                PointRec o = table[candidate_pos(q, s_start[w], s_off[w])];
+                PointRec o = table[candidate_pos(q, s_start[rw], s_off[rw])];
                 float db;
                 if (in_ball(c, o, &db) && o.j < j &&
                     (((uint64_t)__float_as_uint(db) << 32) | (uint32_t)o.j) <= threshold)
@@ -530,10 +556,10 @@ __global__ void __launch_bounds__(kWaves * 64)
     }
     if (staged) {
         wave_lds_sync();
-        for (int32_t a = lane; a < m; a += 64) {
-            int32_t ja = s_j[w][a];
+        for (int32_t a = sl; a < m; a += L) {
+            int32_t ja = s_j[rw][a];
             int32_t pos = 0;
-            for (int32_t q = 0; q < m; ++q) pos += (s_j[w][q] < ja) ? 1 : 0;
+            for (int32_t q = 0; q < m; ++q) pos += (s_j[rw][q] < ja) ? 1 : 0;
             int64_t dst = (int64_t)out0 + pos;
             if (dst < col_capacity) col_idx[dst] = ja;
         }
@@ -558,6 +584,24 @@ __global__ void compact_rows_kernel(const int32_t *__restrict__ rows,
 }
 
 bool one_pass(int32_t k_cap) { return k_cap >= 1 && k_cap <= kStage; }
+
+// Two rows per wave when there are at least twice as many rows as the waves
+// the chip holds at once (eight per SIMD, four SIMDs per CU); fewer rows keep
+// a wave each, so that they still spread over the whole chip.
+bool pair_rows(int32_t n_out) { return (int64_t)n_out >= 64LL * device_cus(); }
+
+// rows_kernel<kMode, 32 or 64 lanes per row> over n_out (the second argument)
+template <int kMode, typename... Args>
+void launch_rows(bool pair, hipStream_t stream, const float *x_out, int32_t n_out,
+                 Args... args) {
+    const dim3 block(kWaves * 64);
+    if (pair)
+        hipLaunchKernelGGL((rows_kernel<kMode, 32>), dim3(grid_for(n_out, 2 * kWaves)), block, 0,
+                           stream, x_out, n_out, args...);
+    else
+        hipLaunchKernelGGL((rows_kernel<kMode, 64>), dim3(grid_for(n_out, kWaves)), block, 0,
+                           stream, x_out, n_out, args...);
+}
 
 // Buckets of all clouds: 2 n_b + 1 per cloud.
 uint32_t table_size_for(int32_t n_in, int32_t n_batch) {
@@ -658,18 +702,16 @@ extern "C" sbc_status sbc_neighbour_search_points(
             SBC_LAUNCH_CHECK();
         }
     }
-    const int row_blocks = grid_for(n_out, kWaves);
+    const bool pair = pair_rows(n_out);
     const bool single = one_pass(k_cap);
     if (n_out > 0) {
         trace_before("points_count", stream);
         if (single)
-            hipLaunchKernelGGL((rows_kernel<2>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
-                               x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
+            launch_rows<2>(pair, stream, x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
                                T, ws.cell_start, ws.table, ws.row_len,
                                (const int32_t *)nullptr, ws.rows, (int64_t)n_out * k_cap);
         else
-            hipLaunchKernelGGL((rows_kernel<0>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
-                               x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
+            launch_rows<0>(pair, stream, x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap, inv_h,
                                T, ws.cell_start, ws.table, ws.row_len,
                                (const int32_t *)nullptr, (int32_t *)nullptr, (int64_t)0);
         SBC_LAUNCH_CHECK();
@@ -702,8 +744,7 @@ extern "C" sbc_status sbc_neighbour_search_points(
                                ws.rows, ws.row_len, row_ptr, n_out, k_cap, col_idx,
                                col_capacity);
         } else {
-            hipLaunchKernelGGL((rows_kernel<1>), dim3(row_blocks), dim3(kWaves * 64), 0, stream,
-                               x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap,
+            launch_rows<1>(pair, stream, x_out, n_out, in_splits, out_splits, n_batch, radius, k_cap,
                                inv_h, T, ws.cell_start, ws.table, ws.row_len, row_ptr,
                                col_idx, col_capacity);
         }

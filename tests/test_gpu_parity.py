@@ -349,6 +349,29 @@ def test_rows_longer_than_the_lds_stage(k_cap):
     assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
 
 
+@pytest.mark.parametrize("k_cap", [0, 16, 200, 300])
+def test_two_rows_per_wave(k_cap):
+    """Enough output rows (over 16384) that each wave searches two rows: a
+    sparse cloud with a dense cluster (1500 points in ball) and a medium one
+    (about 150), so that capped and uncapped rows take the staged, the
+    bisection and the unstaged paths on 32-lane row segments."""
+    print(f"[two rows per wave] k_cap {k_cap}", flush=True)
+    rng = np.random.default_rng(11)
+    dense = (rng.random((1500, 3)) * 0.1).astype(np.float32)
+    medium = (rng.random((150, 3)) * 0.1 + 1.0).astype(np.float32)
+    sparse = (rng.random((18500, 3)) * 10.0 + 2.0).astype(np.float32)
+    x = np.concatenate([dense, medium, sparse])
+    y = np.concatenate([dense[:40], medium[:40], sparse])
+    w = workloads.points_workload(rng, [(x, y)], workloads.BASIS_MONO8, 0.3, k_cap, 4, 4)
+    rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"], 0.3, k_cap)
+    lens = np.diff(rp)
+    assert lens[0] == (k_cap if k_cap else 1500) and len(lens) > 16384
+    t = G.to_device(w)
+    csr = G.search(w, t)
+    assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
+    assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+
+
 def test_unsorted_and_out_of_range_events_are_reported():
     px = torch.tensor([1, 2, 3, 1], dtype=torch.int32, device=G.DEV)
     py = torch.tensor([1, 1, 1, 1], dtype=torch.int32, device=G.DEV)
