@@ -3,7 +3,8 @@
 
 One step = neighbour search -> forward (basis evaluated inside) -> transpose
 -> backward (dF and dW) over one batch of synthetic input already resident in
-HBM.  Prints one JSON line.
+HBM (for event streams the transpose comes out of the search itself, by the
+reverse search over the same pixel lists).  Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--order auto]
 
@@ -226,11 +227,10 @@ def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256):
         # column indices in, column bounds, rows and edge positions out
         t["transpose_batched"] = (1, 4 * (n_out + 1) + 4 * E + 4 * (n_in + 1) + 8 * E, 0, False)
     else:
-        t["transpose_count"] = (1, 4 * (n_out + 1) + 4 * E + 4 * n_in, 0, False)
-        t["transpose_scatter"] = (1, 4 * (n_out + 1) + 4 * E + 4 * n_in + 12 * E, 0, False)
-        # rank sort of the scattered (column, edge, row) triples: column bounds,
-        # three input arrays, two outputs
-        t["transpose_sort"] = (1, 8 * (n_in + 1) + 20 * E, 0, False)
+        # the transpose by the reverse search over the same pixel lists: runs
+        # and counts, then the merge into column bounds and rows
+        t["events_count_t"] = (1, 24 * n_in, 0, False)
+        t["events_fill_t"] = (1, 28 * n_in + 4 * E, 0, False)
     basis_launches = 0
     csr_b = 4 * (n_out + 1) + 4 * E + 4 * E * M
     csc_b = 4 * (n_in + 1) + 8 * E + 4 * E * M
@@ -397,12 +397,15 @@ def main(argv=None):
         px, py, tt = T(w["px"]), T(w["py"]), T(w["t"])
         geo = sbc.Geometry("event8", tau=w["tau"], px=px, py=py, t=tt)
         cap = sbc.neighbour_search_events(px, py, tt, w["width"], w["height"], w["window"]).nnz
+        found = {}
 
-        def search():
-            return sbc.neighbour_search_events(px, py, tt, w["width"], w["height"], w["window"],
-                                               col_capacity=cap, sync=False)
+        def search():  # the pattern and its transpose from one set of pixel lists
+            csr, found["csc"] = sbc.neighbour_search_events_csc(
+                px, py, tt, w["width"], w["height"], w["window"], col_capacity=cap, sync=False)
+            return csr
 
-        transpose = sbc.csr_transpose
+        def transpose(csr):
+            return found["csc"]
 
     n_in, n_out = w["n_in"], w["n_out"]
     csr0 = search()

@@ -113,12 +113,15 @@ typedef struct {
     const int32_t *col_idx;   /* [E]                                            */
 } sbc_csr;
 
-/* Its transpose (rows = inputs), as produced by sbc_csr_transpose. */
+/* Its transpose (rows = inputs), as produced by sbc_csr_transpose.  edge_perm
+ * may be NULL when the basis values are evaluated inside the kernels (v NULL
+ * in sbc_conv_backward): they are then evaluated for the transposed entries
+ * directly and no entry needs its CSR position. */
 typedef struct {
     int32_t n_cols;           /* n_in                                           */
     const int32_t *col_ptr;   /* [n_cols + 1]                                   */
     const int32_t *row_idx;   /* [E] output index of each entry, ascending      */
-    const int32_t *edge_perm; /* [E] CSR position of each entry                 */
+    const int32_t *edge_perm; /* [E] CSR position of each entry, or NULL        */
 } sbc_csc;
 
 /*
@@ -202,6 +205,23 @@ sbc_status sbc_neighbour_search_events(const int32_t *px, const int32_t *py, con
                                        void *workspace, size_t workspace_bytes,
                                        hipStream_t stream);
 
+/* The same search, also emitting the transposed pattern (Section 3.1,
+ * "Symmetry": the reverse neighbourhood), found from the same per-pixel lists
+ * by the reverse search: column j lists the events i > j with |px_i - px_j|
+ * <= half_extent, |py_i - py_j| <= half_extent and t_i - t_j <= window, in
+ * ascending i.  col_ptr [n + 1] and row_idx [capacity] equal what
+ * sbc_csr_transpose gives for row_ptr / col_idx; no edge_perm is produced
+ * (see sbc_csc).  capacity bounds both col_idx and row_idx (E entries each);
+ * the other arguments and the errors are those of sbc_neighbour_search_events,
+ * whose workspace size it uses. */
+sbc_status sbc_neighbour_search_events_csc(const int32_t *px, const int32_t *py,
+                                           const int32_t *t, int32_t n, int32_t width,
+                                           int32_t height, int32_t half_extent, int32_t window,
+                                           int32_t *row_ptr, int32_t *col_idx, int32_t *col_ptr,
+                                           int32_t *row_idx, int64_t capacity,
+                                           int64_t *nnz_host, void *workspace,
+                                           size_t workspace_bytes, hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * 2. Basis values (Section 3.1, the values of the neighbourhood matrices):
  * v[e, m] = p_m(edge e) as float32, edge-major [E, M], in CSR edge order.
@@ -259,7 +279,9 @@ sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v, const sbc_geomet
  *   dY  [n_out, C_out]    float32 or bf16 (dtype)
  *   dF  [n_in, C_in]      float32 output, or NULL to skip
  *   dW  [M, C_in, C_out]  float32 output, or NULL to skip
- *   csc                   the transpose of csr (sbc_csr_transpose)
+ *   csc                   the transpose of csr (sbc_csr_transpose, or
+ *                         sbc_neighbour_search_events_csc); its edge_perm
+ *                         may be NULL only when v is NULL
  * dW sums over every edge of the batch, in a fixed blocked order.
  * ------------------------------------------------------------------------ */
 sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v,

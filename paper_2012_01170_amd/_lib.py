@@ -23,7 +23,7 @@ EXPORTS = [
     "sbc_last_error", "sbc_status_string", "sbc_basis_size",
     "sbc_points_workspace_size", "sbc_neighbour_search_points",
     "sbc_events_workspace_size", "sbc_neighbour_search_events",
-    "sbc_basis_eval",
+    "sbc_neighbour_search_events_csc", "sbc_basis_eval",
     "sbc_transpose_workspace_size", "sbc_csr_transpose", "sbc_csr_transpose_batched",
     "sbc_conv_workspace_size", "sbc_conv_forward", "sbc_conv_backward",
     "sbc_resolve_order", "sbc_trace_kernel", "sbc_trace_clear", "sbc_kernel_names",
@@ -78,6 +78,9 @@ _SIGS = {
     "sbc_events_workspace_size": (_sz, [_i32, _i32, _i32]),
     "sbc_neighbour_search_events": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp,
                                                    _vp, _i64, _i64_p, _vp, _sz, _vp]),
+    "sbc_neighbour_search_events_csc": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32,
+                                                       _i32, _vp, _vp, _vp, _vp, _i64, _i64_p,
+                                                       _vp, _sz, _vp]),
     "sbc_basis_eval": (ctypes.c_int, [_csr_p, _geo_p, _vp, _vp]),
     "sbc_transpose_workspace_size": (_sz, [_i32, _i64]),
     "sbc_csr_transpose": (ctypes.c_int, [_csr_p, _vp, _vp, _vp, _vp, _sz, _vp]),

@@ -17,18 +17,25 @@ __device__ __forceinline__ int32_t row_of_edge(const int32_t *__restrict__ row_p
     return lo;
 }
 
-template <int kBasis>
+// Values of the entries of a compressed pattern in its own entry order: a CSR
+// (segments = outputs i, indices = inputs j) or, with kT, its transpose
+// (segments = inputs j, indices = outputs i).
+template <int kBasis, bool kT>
 __global__ void __launch_bounds__(256)
-    basis_kernel(int32_t n_rows, const int32_t *__restrict__ row_ptr,
-                 const int32_t *__restrict__ col_idx, sbc_geometry g, float *__restrict__ v) {
+    basis_kernel(int32_t n_seg, const int32_t *__restrict__ seg_ptr,
+                 const int32_t *__restrict__ idx, int64_t nnz_bound, sbc_geometry g,
+                 float *__restrict__ v) {
     constexpr int M = kBasis == SBC_BASIS_MONO4 ? 4 : 8;
-    const int32_t E = row_ptr[n_rows];
+    // entries past nnz_bound (a malformed pattern) have no room in v
+    const int64_t E = seg_ptr[n_seg] < nnz_bound ? (int64_t)seg_ptr[n_seg] : nnz_bound;
     const double inv_r = 1.0 / (double)g.radius;
     const float inv_tau = 1.0f / g.tau;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < E;
          e += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t i = row_of_edge(row_ptr, n_rows, (int32_t)e);
-        const int32_t j = col_idx[e];
+        const int32_t sg = row_of_edge(seg_ptr, n_seg, (int32_t)e);
+        const int32_t other = idx[e];
+        const int32_t i = kT ? other : sg;
+        const int32_t j = kT ? sg : other;
         float out[8];
         if constexpr (kBasis == SBC_BASIS_EVENT8) {
 #pragma unroll
@@ -69,29 +76,41 @@ sbc_status check_geometry(const sbc_geometry *g, int32_t n_rows, int32_t n_cols)
     }
 }
 
-sbc_status basis_eval_launch(const sbc_csr *csr, const sbc_geometry *g, float *v,
-                             hipStream_t stream) {
-    if (csr->n_rows == 0 || csr->nnz_bound <= 0) return SBC_OK;
-    int64_t blocks = (csr->nnz_bound + 255) / 256;
+template <bool kT>
+sbc_status basis_launch(int32_t n_seg, const int32_t *seg_ptr, const int32_t *idx, int64_t nnz,
+                        const sbc_geometry *g, float *v, hipStream_t stream) {
+    if (n_seg == 0 || nnz <= 0) return SBC_OK;
+    int64_t blocks = (nnz + 255) / 256;
     if (blocks > 8192) blocks = 8192;
     trace_before("basis", stream);
     switch (g->basis) {
         case SBC_BASIS_MONO4:
-            hipLaunchKernelGGL(basis_kernel<SBC_BASIS_MONO4>, dim3((unsigned)blocks), dim3(256), 0,
-                               stream, csr->n_rows, csr->row_ptr, csr->col_idx, *g, v);
+            hipLaunchKernelGGL((basis_kernel<SBC_BASIS_MONO4, kT>), dim3((unsigned)blocks),
+                               dim3(256), 0, stream, n_seg, seg_ptr, idx, nnz, *g, v);
             break;
         case SBC_BASIS_MONO8:
-            hipLaunchKernelGGL(basis_kernel<SBC_BASIS_MONO8>, dim3((unsigned)blocks), dim3(256), 0,
-                               stream, csr->n_rows, csr->row_ptr, csr->col_idx, *g, v);
+            hipLaunchKernelGGL((basis_kernel<SBC_BASIS_MONO8, kT>), dim3((unsigned)blocks),
+                               dim3(256), 0, stream, n_seg, seg_ptr, idx, nnz, *g, v);
             break;
         default:
-            hipLaunchKernelGGL(basis_kernel<SBC_BASIS_EVENT8>, dim3((unsigned)blocks), dim3(256), 0,
-                               stream, csr->n_rows, csr->row_ptr, csr->col_idx, *g, v);
+            hipLaunchKernelGGL((basis_kernel<SBC_BASIS_EVENT8, kT>), dim3((unsigned)blocks),
+                               dim3(256), 0, stream, n_seg, seg_ptr, idx, nnz, *g, v);
             break;
     }
     SBC_LAUNCH_CHECK();
     trace_after("basis", stream);
     return SBC_OK;
+}
+
+sbc_status basis_eval_launch(const sbc_csr *csr, const sbc_geometry *g, float *v,
+                             hipStream_t stream) {
+    return basis_launch<false>(csr->n_rows, csr->row_ptr, csr->col_idx, csr->nnz_bound, g, v,
+                               stream);
+}
+
+sbc_status basis_eval_t_launch(const sbc_csc *csc, int64_t nnz_bound, const sbc_geometry *g,
+                               float *v, hipStream_t stream) {
+    return basis_launch<true>(csc->n_cols, csc->col_ptr, csc->row_idx, nnz_bound, g, v, stream);
 }
 
 sbc_status check_csr(const sbc_csr *csr) {

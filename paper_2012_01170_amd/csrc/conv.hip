@@ -312,8 +312,10 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
     SBC_TRY(check_conv_args(csr, v, geometry, M, F, W, dtype, C_in, C_out));
     SBC_TRY(check_order(order));
     if (!csc || !csc->col_ptr || csc->n_cols != csr->n_cols ||
-        (csr->nnz_bound > 0 && (!csc->row_idx || !csc->edge_perm)))
+        (csr->nnz_bound > 0 && !csc->row_idx))
         return fail(SBC_ERR_INVALID_ARG, "csc is null or does not match csr");
+    if (csr->nnz_bound > 0 && v && !csc->edge_perm)
+        return fail(SBC_ERR_INVALID_ARG, "csc->edge_perm is needed when v is given");
     if (!dY && csr->n_rows > 0) return fail(SBC_ERR_INVALID_ARG, "dY is null");
     if (!aligned16(dY) || !aligned16(dF) || !aligned16(dW))
         return fail(SBC_ERR_INVALID_ARG, "dY, dF and dW must be 16-byte aligned");
@@ -329,8 +331,18 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
                               workspace, stream);
 
     ConvWs ws = carve_route(workspace, r, n_out, n_in, csr->nnz_bound, M, C_in, C_out, nullptr);
+    // values of the transposed entries: through edge_perm, or (with no
+    // edge_perm, so v is null) evaluated in the transpose's own order into
+    // ws.v once the CSR-ordered values are no longer needed
     const float *vv = v;
-    if (!vv) {
+    const int32_t *perm_t = csc->edge_perm;
+    auto values_t = [&]() -> sbc_status {
+        if (perm_t) return SBC_OK;
+        SBC_TRY(basis_eval_t_launch(csc, csr->nnz_bound, geometry, ws.v, stream));
+        vv = ws.v;
+        return SBC_OK;
+    };
+    if (!vv && (r == kBwdG || perm_t)) {
         SBC_TRY(basis_eval_launch(csr, geometry, ws.v, stream));
         vv = ws.v;
     }
@@ -344,12 +356,14 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
         if (dF) {  // dG = dY W_flat^T, then dF = N^T dG
             SBC_TRY(gemm(dY, bf, C_out, 1, W, bf, 1, C_out, ws.inter2, K1, 1, n_out, (int32_t)K1,
                          C_out, ws.partial, stream, "bwd_gemm_dg"));
-            SBC_TRY(spmm(n_in, csc->col_ptr, csc->row_idx, csc->edge_perm, vv, M, ws.inter2,
-                         false, C_in, true, dF, stream, "bwd_spmm_t"));
+            SBC_TRY(values_t());
+            SBC_TRY(spmm(n_in, csc->col_ptr, csc->row_idx, perm_t, vv, M, ws.inter2, false, C_in,
+                         true, dF, stream, "bwd_spmm_t"));
         }
     } else {
-        SBC_TRY(spmm(n_in, csc->col_ptr, csc->row_idx, csc->edge_perm, vv, M, dY, bf, C_out,
-                     false, ws.inter, stream, "bwd_spmm_t_expand"));
+        SBC_TRY(values_t());
+        SBC_TRY(spmm(n_in, csc->col_ptr, csc->row_idx, perm_t, vv, M, dY, bf, C_out, false,
+                     ws.inter, stream, "bwd_spmm_t_expand"));
         if (dF) {  // Wt [M, C_out, C_in]; dF = D Wt
             SBC_TRY(permute_w(W, bf, M, C_in, C_out, (int64_t)C_out * C_in, 1, C_in, ws.wperm,
                               stream));

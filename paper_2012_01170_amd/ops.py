@@ -9,7 +9,7 @@ from __future__ import annotations
 
 import ctypes
 from dataclasses import dataclass
-from typing import Optional
+from typing import Optional, Tuple
 
 import torch
 
@@ -71,14 +71,16 @@ class CSR:
 
 @dataclass
 class CSC:
-    col_ptr: torch.Tensor      # int32 [n_cols + 1]
-    row_idx: torch.Tensor      # int32 [nnz]
-    edge_perm: torch.Tensor    # int32 [nnz]
+    """Transposed pattern: rows are inputs.  edge_perm (each entry's CSR
+    position) may be None when the basis is evaluated inside the kernels."""
+    col_ptr: torch.Tensor               # int32 [n_cols + 1]
+    row_idx: torch.Tensor               # int32 [nnz]
+    edge_perm: Optional[torch.Tensor]   # int32 [nnz] or None
     n_cols: int
 
     def c_struct(self) -> L.SbcCsc:
-        return L.SbcCsc(self.n_cols, self.col_ptr.data_ptr(), self.row_idx.data_ptr(),
-                        self.edge_perm.data_ptr())
+        perm = self.edge_perm.data_ptr() if self.edge_perm is not None else None
+        return L.SbcCsc(self.n_cols, self.col_ptr.data_ptr(), self.row_idx.data_ptr(), perm)
 
 
 @dataclass
@@ -146,10 +148,7 @@ def neighbour_search_points(x_in, in_splits, x_out, out_splits, radius: float, k
     raise RuntimeError("neighbour search did not converge on a capacity")
 
 
-def neighbour_search_events(px, py, t, width: int, height: int, window: int,
-                            half_extent: int = 1, col_capacity: Optional[int] = None,
-                            sync: bool = True) -> CSR:
-    """Backwards-in-time pixel-block neighbourhoods of an event stream (sbc_neighbour_search_events)."""
+def _search_events(px, py, t, width, height, window, half_extent, col_capacity, sync, csc):
     _require(px, "px", torch.int32, 1)
     dev = px.device
     _require(py, "py", torch.int32, 1, dev)
@@ -164,21 +163,47 @@ def neighbour_search_events(px, py, t, width: int, height: int, window: int,
     lib = L.lib()
     ws = _Workspace(lib.sbc_events_workspace_size(n, width, height), dev)
     row_ptr = torch.empty(n + 1, dtype=torch.int32, device=dev)
+    col_ptr = torch.empty(n + 1, dtype=torch.int32, device=dev) if csc else None
     stream = _stream(dev)
     for _ in range(2):
         col_idx = torch.empty(max(1, col_capacity), dtype=torch.int32, device=dev)
         nnz = ctypes.c_int64(-1)
-        st = lib.sbc_neighbour_search_events(
-            _p(px), _p(py), _p(t), n, int(width), int(height), int(half_extent), int(window),
-            _p(row_ptr), _p(col_idx), int(col_capacity), ctypes.byref(nnz) if sync else None,
-            ws.ptr, ws.nbytes, stream)
+        nnz_p = ctypes.byref(nnz) if sync else None
+        common = (_p(px), _p(py), _p(t), n, int(width), int(height), int(half_extent), int(window),
+                  _p(row_ptr), _p(col_idx))
+        if csc:
+            row_idx = torch.empty(max(1, col_capacity), dtype=torch.int32, device=dev)
+            st = lib.sbc_neighbour_search_events_csc(*common, _p(col_ptr), _p(row_idx),
+                                                     int(col_capacity), nnz_p, ws.ptr, ws.nbytes,
+                                                     stream)
+        else:
+            st = lib.sbc_neighbour_search_events(*common, int(col_capacity), nnz_p, ws.ptr,
+                                                 ws.nbytes, stream)
         if st == 2 and sync:
             col_capacity = int(nnz.value)
             continue
         L.check(st)
         E = int(nnz.value) if sync else int(col_capacity)
-        return CSR(row_ptr, col_idx, n, n, E)
+        csr = CSR(row_ptr, col_idx, n, n, E)
+        return (csr, CSC(col_ptr, row_idx, None, n)) if csc else csr
     raise RuntimeError("neighbour search did not converge on a capacity")
+
+
+def neighbour_search_events(px, py, t, width: int, height: int, window: int,
+                            half_extent: int = 1, col_capacity: Optional[int] = None,
+                            sync: bool = True) -> CSR:
+    """Backwards-in-time pixel-block neighbourhoods of an event stream (sbc_neighbour_search_events)."""
+    return _search_events(px, py, t, width, height, window, half_extent, col_capacity, sync,
+                          False)
+
+
+def neighbour_search_events_csc(px, py, t, width: int, height: int, window: int,
+                                half_extent: int = 1, col_capacity: Optional[int] = None,
+                                sync: bool = True) -> Tuple[CSR, CSC]:
+    """The event neighbourhoods and their transpose from one search
+    (sbc_neighbour_search_events_csc); the CSC has no edge_perm."""
+    return _search_events(px, py, t, width, height, window, half_extent, col_capacity, sync,
+                          True)
 
 
 def basis_eval(csr: CSR, geometry: Geometry) -> torch.Tensor:

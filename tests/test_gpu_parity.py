@@ -430,6 +430,73 @@ def test_event_search_block_sizes(half_extent):
     assert csr.nnz == len(ci)
     assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
     assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+    check_events_csc(px, py, t, W, H, window, half_extent, rp, ci)
+
+
+def check_events_csc(px, py, t, W, H, window, half_extent, rp, ci):
+    """The combined search gives the same CSR and, as its CSC, the oracle's
+    transpose of it (bit-exact)."""
+    csr, csc = G.sbc.neighbour_search_events_csc(G.dev(px), G.dev(py), G.dev(t), W, H, window,
+                                                 half_extent=half_extent)
+    assert csr.nnz == len(ci) and csc.edge_perm is None
+    assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
+    assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+    cp, ri, _ = oracle.csr_transpose(rp, ci, len(px))
+    assert np.array_equal(csc.col_ptr.cpu().numpy(), cp)
+    assert np.array_equal(csc.row_idx[:len(ci)].cpu().numpy(), ri)
+
+
+EVENT_CASES = ["ev_small", "ev_odd", "fz_ev32", "fz_tiny_ev", "events_300k", "events_1m_bf16"]
+
+
+@pytest.mark.parametrize("name", EVENT_CASES)
+def test_events_csc_bit_exact(name):
+    print(f"[events csc] {name}", flush=True)
+    w, rp, ci, _ = case(name)
+    check_events_csc(w["px"], w["py"], w["t"], w["width"], w["height"], w["window"],
+                     w.get("half_extent", 1), rp, ci)
+
+
+@pytest.mark.parametrize("window", [0, 7, 2**31 - 1])
+def test_events_csc_window_edges(window):
+    """Equal timestamps, gaps of exactly the window, and timestamps near the
+    int32 limits with a window that would overflow t + window."""
+    print(f"[events csc window] {window}", flush=True)
+    rng = np.random.default_rng(window % 1000)
+    n, W, H = 3000, 6, 5
+    px = rng.integers(0, W, size=n).astype(np.int32)
+    py = rng.integers(0, H, size=n).astype(np.int32)
+    steps = rng.choice([0, 0, 7, 1, 8], size=n)
+    t = (np.cumsum(steps) + (2**31 - 1 - steps.sum() if window > 1000 else 0)).astype(np.int64)
+    t = t.astype(np.int32)
+    rp, ci = oracle.events_csr(px, py, t, window, 1, W, H)
+    check_events_csc(px, py, t, W, H, window, 1, rp, ci)
+
+
+@pytest.mark.parametrize("order", ORDERS)
+@pytest.mark.parametrize("name", ["ev_small", "ev_bf16", "fz_ev32", "fz_tiny_ev", "pts_down",
+                                  "fz_pts64", "pts_mono4_odd"])
+def test_backward_without_edge_perm(name, order):
+    """With the basis evaluated inside, a CSC without edge_perm gives the same
+    gradients, bit for bit, on the fused and the separate-kernel routes (the
+    values of the transposed entries are then evaluated in their own order)."""
+    print(f"[backward no perm] {name} {order}", flush=True)
+    w, rp, ci, v = case(name)
+    t, csr = gpu_case(name)
+    geo = G.geometry(w, t)
+    csc = G.sbc.csr_transpose(csr)
+    dF, dW = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"], geometry=geo, order=order)
+    bare = G.sbc.CSC(csc.col_ptr, csc.row_idx, None, csc.n_cols)
+    if w["kind"] == "events":
+        csr2, bare = G.sbc.neighbour_search_events_csc(t["px"], t["py"], t["t"], w["width"],
+                                                       w["height"], w["window"])
+        assert np.array_equal(csr2.col_idx[:csr2.nnz].cpu().numpy(), ci)
+    dF2, dW2 = G.sbc.conv_backward(csr, bare, t["F"], t["W"], t["dY"], geometry=geo, order=order)
+    assert np.array_equal(dF2.cpu().numpy(), dF.cpu().numpy())
+    assert np.array_equal(dW2.cpu().numpy(), dW.cpu().numpy())
+    vv = G.sbc.basis_eval(csr, geo)
+    with pytest.raises(G.sbc.ops.L.SbcError, match="INVALID_ARG"):
+        G.sbc.conv_backward(csr, bare, t["F"], t["W"], t["dY"], v=vv, order=order)
 
 
 def test_transpose_by_radix_sort():
