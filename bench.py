@@ -206,7 +206,7 @@ def summarize_trace(trace_dir, command, bench_json=None):
     return "\n".join(out) + "\n"
 
 
-def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256):
+def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256, npix=0):
     """Kernels of one step: name -> (launches per step, algorithmic bytes, flops, on MFMA).
 
     Bytes count every array the kernel must touch once (gathered rows once per
@@ -220,17 +220,15 @@ def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256):
         t["points_count"] = (1, 12 * n_out + 16 * n_in + 4 * n_out, 0, False)
         t["points_fill"] = (1, 12 * n_out + 16 * n_in + 8 * n_out + 4 * E, 0, False)
     else:
-        t["events_count"] = (1, 24 * n_in, 0, False)
-        t["events_fill"] = (1, 28 * n_in + 4 * E, 0, False)
+        # pixel tiles: list bounds and lists (index, time) in; the row and
+        # column lengths out, or the row and column bounds in and the rows
+        # and columns of both patterns out
+        t["events_count"] = (1, 4 * (npix + 1) + 8 * n_in + 8 * n_in, 0, False)
+        t["events_fill"] = (1, 4 * (npix + 1) + 8 * n_in + 8 * (n_in + 1) + 8 * E, 0, False)
     if kind == "points":
         # block-diagonal transpose, one workgroup per cloud: row bounds and
         # column indices in, column bounds, rows and edge positions out
         t["transpose_batched"] = (1, 4 * (n_out + 1) + 4 * E + 4 * (n_in + 1) + 8 * E, 0, False)
-    else:
-        # the transpose by the reverse search over the same pixel lists: runs
-        # and counts, then the merge into column bounds and rows
-        t["events_count_t"] = (1, 24 * n_in, 0, False)
-        t["events_fill_t"] = (1, 28 * n_in + 4 * E, 0, False)
     basis_launches = 0
     csr_b = 4 * (n_out + 1) + 4 * E + 4 * E * M
     csc_b = 4 * (n_in + 1) + 8 * E + 4 * E * M
@@ -423,7 +421,8 @@ def main(argv=None):
     n_cus = torch.cuda.get_device_properties(dev).multi_processor_count
     tr_bwd = 32                                           # the fused backward's tile rows
     blocks_bwd = max(1, min(256, n_cus, (n_in + tr_bwd - 1) // tr_bwd))
-    table = kernel_table(w["kind"], plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd)
+    npix = w["width"] * w["height"] if w["kind"] == "events" else 0
+    table = kernel_table(w["kind"], plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd, npix)
     L = _lib.lib()
     # one (start, stop) event pair per kernel per timed step; record once so the
     # underlying HIP events exist before the library records them again

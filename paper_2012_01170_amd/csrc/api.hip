@@ -11,7 +11,7 @@ thread_local std::string g_last_error;
 thread_local std::unordered_map<std::string, std::pair<hipEvent_t, hipEvent_t>> g_trace;
 
 const char *kKernelNames =
-    "points_count,points_fill,events_count,events_fill,events_count_t,events_fill_t,basis,"
+    "points_count,points_fill,events_count,events_fill,basis,"
     "transpose_count,transpose_scatter,transpose_sort,transpose_batched,"
     "fwd_spmm,fwd_gemm,fwd_gemm_h,fwd_spmm_contract,bwd_spmm,bwd_gemm_dw,bwd_gemm_dg,"
     "bwd_spmm_t,bwd_spmm_t_expand,bwd_gemm_df,bwd_gemm_dw_t,fwd_fused,bwd_fused,bwd_dw_reduce";

@@ -8,26 +8,26 @@
 //      event timestamps alongside the indices;
 //   2. runs: for each pixel q of an event i's block, the events of q with
 //      index < i and t >= t_i - window form one contiguous run of q's list
-//      (indices and times both ascend along it); for blocks up to 3x3 the
-//      runs of all events come from one two-pointer sweep per (pixel,
-//      offset) pair and are stored, for larger blocks each event bisects;
-//      the count pass sums the run lengths per event;
+//      (indices and times both ascend along it), found by two bisections; the
+//      count pass sums the run lengths per event;
 //   3. scan -> row_ptr;
 //   4. fill pass: the (2h+1)^2 runs are merged by index into the row.
-// The transposed pattern (Section 3.1, "Symmetry") comes from the same lists
-// by the reverse search: the block is symmetric, so column j lists the events
-// i > j of j's block with t_i <= t_j + window, again one run per pixel.
+// Steps 2 and 4 work tile by tile over the sensor, with the lists of a tile
+// and its halo staged in LDS.  The transposed pattern (Section 3.1,
+// "Symmetry") comes out of the same passes by the reverse search: the block
+// is symmetric, so column j lists the events i > j of j's block with
+// t_i <= t_j + window, again one run per pixel.
 // Events with a pixel outside the sensor get no neighbours and are in no
 // list; a decreasing timestamp raises a flag.  Neither can make a kernel
 // read or write out of bounds.
 #include <climits>
+#include <cmath>
 
 #include "common.hpp"
 
 namespace sbc {
 namespace {
 
-constexpr int kMaxBlock = 7;  // half_extent <= 3: at most 7x7 pixels
 
 __device__ __forceinline__ bool valid_pixel(int32_t x, int32_t y, int32_t W, int32_t H) {
     return x >= 0 && x < W && y >= 0 && y < H;
@@ -70,20 +70,48 @@ __device__ __forceinline__ int32_t lower_bound(const int32_t *__restrict__ a, in
     return lo;
 }
 
-struct Runs {
-    int32_t lo[kMaxBlock * kMaxBlock];
-    int32_t hi[kMaxBlock * kMaxBlock];
-};
+// Tiles of tx x ty sensor pixels (at most kMaxTile x kMaxTile, sized so that
+// a tile holds about as many events as a workgroup has threads).  A
+// workgroup takes one tile: it stages the lists of the tile's pixels and of
+// the halo around it (the block reaches half_extent pixels beyond the tile)
+// in LDS, then every event of the tile's pixels finds its runs there by
+// bisection, in the pattern and in its transpose, and sums them (count pass)
+// or merges them into its row and its column (fill pass).  Tiles whose lists
+// exceed the stage read them from global memory instead.
+constexpr int kMaxTile = 8;
+constexpr int kTileThreads = 256;
+constexpr int kTileCap = 2048;  // list entries staged per tile
 
-// Runs of event i in the lists of its block's pixels.  Forward: the events
-// j < i with t_j >= t_i - window; reverse (kRev): the events j > i with
-// t_j <= t_i + window.
+// Exclusive scan of one value per thread over the workgroup; *total gets the sum.
+__device__ __forceinline__ int32_t block_excl_scan(int32_t v, int32_t *s_w, int32_t *total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int32_t incl = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int32_t y = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += y;
+    }
+    if (lane == 63) s_w[wave] = incl;
+    __syncthreads();
+    int32_t base = 0, sum = 0;
+    for (int w = 0; w < kTileThreads / 64; ++w) {
+        if (w < wave) base += s_w[w];
+        sum += s_w[w];
+    }
+    *total = sum;
+    return base + incl - v;
+}
+
+// The (kSide x kSide) runs of event i (index i, time ti) of halo pixel p: in
+// the list range [s, e) of each pixel of its block, forward (kRev false) the
+// entries j < i with t_j >= t_i - window, reverse the entries j > i with
+// t_j <= t_i + window.  Li / Lt: list indices and times (LDS or global);
+// start/len: per halo pixel, where its list begins in Li / Lt and its length.
 template <int kSide, bool kRev>
-__device__ __forceinline__ int32_t find_runs(int32_t i, int32_t x, int32_t y, int32_t ti,
-                                             int32_t W, int32_t H, int64_t window,
-                                             const int32_t *__restrict__ pix_start,
-                                             const int32_t *__restrict__ list,
-                                             const int32_t *__restrict__ list_t, Runs &r) {
+__device__ __forceinline__ int32_t tile_runs(int32_t i, int32_t ti, int32_t window, int p, int HX,
+                                             const int32_t *Li, const int32_t *Lt,
+                                             const int32_t *start, const int32_t *len,
+                                             int32_t *lo, int32_t *hi) {
     constexpr int h = kSide / 2;
     // forward: t_j >= t_i - window; reverse: t_j < t_i + window + 1; both
     // without int32 overflow
@@ -93,137 +121,178 @@ __device__ __forceinline__ int32_t find_runs(int32_t i, int32_t x, int32_t y, in
     int32_t count = 0;
 #pragma unroll
     for (int k = 0; k < kSide * kSide; ++k) {
-        const int32_t qx = x + (k % kSide) - h, qy = y + (k / kSide) - h;
-        int32_t lo = 0, hi = 0;
-        if (valid_pixel(qx, qy, W, H)) {
-            const int64_t q = (int64_t)qy * W + qx;
-            const int32_t s = pix_start[q], e = pix_start[q + 1];
-            if constexpr (kRev) {
-                lo = lower_bound(list, s, e, i + 1);  // entries with index > i
-                hi = tnext64 > (int64_t)INT_MAX ? e : lower_bound(list_t, lo, e, (int32_t)tnext64);
-            } else {
-                hi = lower_bound(list, s, e, i);        // entries with index < i
-                lo = lower_bound(list_t, s, hi, tmin);  // ... and t >= t_i - window
-            }
+        const int q = p + (k / kSide - h) * HX + (k % kSide - h);
+        const int32_t s = start[q], e = s + len[q];
+        int32_t a, b;
+        if constexpr (kRev) {
+            a = lower_bound(Li, s, e, i + 1);  // entries with index > i
+            b = tnext64 > (int64_t)INT_MAX ? e : lower_bound(Lt, a, e, (int32_t)tnext64);
+        } else {
+            b = lower_bound(Li, s, e, i);      // entries with index < i
+            a = lower_bound(Lt, s, b, tmin);   // ... and t >= t_i - window
         }
-        r.lo[k] = lo;
-        r.hi[k] = hi;
-        count += hi - lo;
+        lo[k] = a;
+        hi[k] = b;
+        count += b - a;
     }
     return count;
 }
 
-// Runs of every event in the lists of its block's pixels, by a two-pointer
-// sweep: one thread per (pixel p, offset k) walks the events of p in stream
-// order.  For event i the run in the list of q = p + offset is [lo, hi).
-// Forward: hi is the first entry with index >= i and lo the first with
-// t >= t_i - window.  Reverse (kRev): lo is the first entry with index > i
-// and hi the first at or after lo with t > t_i + window.  Every bound only
-// moves forward as i grows (indices and times ascend along every list), so
-// each list is read once per thread instead of bisected per event.
-// runs[i * kRunsK + k] = (lo, hi); offsets past the sensor give (0, 0).
-constexpr int kRunsK = 9;  // stored runs per event: blocks up to 3x3
-
-template <int kSide, bool kRev>
-__global__ void pixel_runs_kernel(int64_t npix, int32_t W, int32_t H, int32_t window,
-                                  const int32_t *__restrict__ pix_start,
-                                  const int32_t *__restrict__ list,
-                                  const int32_t *__restrict__ list_t, int2 *__restrict__ runs) {
-    constexpr int K = kSide * kSide;
-    constexpr int h = kSide / 2;
-    static_assert(K <= kRunsK, "runs are stored for blocks up to 3x3");
-    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (tid >= npix * K) return;
-    const int64_t p = tid / K;
-    const int k = (int)(tid % K);
-    const int32_t x = (int32_t)(p % W), y = (int32_t)(p / W);
-    const int32_t qx = x + (k % kSide) - h, qy = y + (k / kSide) - h;
-    const int32_t ps = pix_start[p], pe = pix_start[p + 1];
-    if (!valid_pixel(qx, qy, W, H)) {
-        for (int32_t a = ps; a < pe; ++a) runs[(int64_t)list[a] * kRunsK + k] = make_int2(0, 0);
-        return;
-    }
-    const int64_t q = (int64_t)qy * W + qx;
-    const int32_t qe = pix_start[q + 1];
-    int32_t lo = pix_start[q], hi = lo;
-    for (int32_t a = ps; a < pe; ++a) {
-        const int32_t i = list[a];
-        if constexpr (kRev) {
-            // t_j <= t_i + window, computed without int32 overflow
-            const int64_t tmax = (int64_t)list_t[a] + window;
-            while (lo < qe && list[lo] <= i) ++lo;
-            if (hi < lo) hi = lo;
-            while (hi < qe && (int64_t)list_t[hi] <= tmax) ++hi;
-        } else {
-            // t_j >= t_i - window, computed without int32 overflow
-            const int64_t tmin64 = (int64_t)list_t[a] - window;
-            const int32_t tmin = tmin64 < (int64_t)INT_MIN ? INT_MIN : (int32_t)tmin64;
-            while (hi < qe && list[hi] < i) ++hi;
-            while (lo < hi && list_t[lo] < tmin) ++lo;
-        }
-        runs[(int64_t)i * kRunsK + k] = make_int2(lo, hi);
-    }
-}
-
-// kStored: runs read from pixel_runs_kernel's output, else found by bisection.
-// kRev: the reverse search (rows of the transposed pattern).
-template <int kSide, bool kStored, bool kRev>
-__global__ void __launch_bounds__(256)
-    event_rows_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
-                      const int32_t *__restrict__ t, int32_t n, int32_t W, int32_t H,
-                      int32_t window, const int32_t *__restrict__ pix_start,
-                      const int32_t *__restrict__ list, const int32_t *__restrict__ list_t,
-                      int32_t *__restrict__ row_len, const int32_t *__restrict__ row_ptr,
-                      int32_t *__restrict__ col_idx, int64_t col_capacity,
-                      const int2 *__restrict__ runs) {
-    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    const int32_t x = px[i], y = py[i];
-    if (!valid_pixel(x, y, W, H)) {
-        if (row_len) row_len[i] = 0;
-        return;
-    }
-    Runs r;
-    int32_t cnt = 0;
-    if constexpr (kStored) {
+// Merge the runs (each ascends by index; they are disjoint) into out[0, cnt),
+// dropping writes at or past cap.
+template <int K>
+__device__ __forceinline__ void merge_runs(const int32_t *Li, int32_t *lo, const int32_t *hi,
+                                           int32_t cnt, int32_t *__restrict__ out, int64_t dst,
+                                           int64_t cap) {
+    int32_t head[K];
 #pragma unroll
-        for (int k = 0; k < kSide * kSide; ++k) {
-            const int2 lh = runs[(int64_t)i * kRunsK + k];
-            r.lo[k] = lh.x;
-            r.hi[k] = lh.y;
-            cnt += lh.y - lh.x;
-        }
-    } else {
-        cnt = find_runs<kSide, kRev>(i, x, y, t[i], W, H, (int64_t)window, pix_start, list, list_t, r);
-    }
-    if (row_len) {
-        row_len[i] = cnt;
-        return;
-    }
-    // merge the runs by event index (each run ascends; runs are disjoint)
-    int64_t dst = row_ptr[i];
-    int32_t head[kSide * kSide];
-#pragma unroll
-    for (int k = 0; k < kSide * kSide; ++k) head[k] = r.lo[k] < r.hi[k] ? list[r.lo[k]] : INT_MAX;
-    for (int32_t out = 0; out < cnt; ++out) {
+    for (int k = 0; k < K; ++k) head[k] = lo[k] < hi[k] ? Li[lo[k]] : INT_MAX;
+    for (int32_t o = 0; o < cnt; ++o) {
         int32_t best = INT_MAX, arg = 0;
 #pragma unroll
-        for (int k = 0; k < kSide * kSide; ++k) {
+        for (int k = 0; k < K; ++k) {
             if (head[k] < best) {
                 best = head[k];
                 arg = k;
             }
         }
 #pragma unroll
-        for (int k = 0; k < kSide * kSide; ++k) {
+        for (int k = 0; k < K; ++k) {
             if (k == arg) {
-                ++r.lo[k];
-                head[k] = r.lo[k] < r.hi[k] ? list[r.lo[k]] : INT_MAX;
+                ++lo[k];
+                head[k] = lo[k] < hi[k] ? Li[lo[k]] : INT_MAX;
             }
         }
-        if (dst < col_capacity) col_idx[dst] = best;
+        if (dst < cap) out[dst] = best;
         ++dst;
     }
+}
+
+struct TileArgs {
+    int32_t n, W, H, window, tx, ty, tiles_x, n_tiles;
+    const int32_t *pix_start, *list, *list_t;
+    int32_t *row_len, *col_len;            // count pass (col_len: null without the transpose)
+    const int32_t *row_ptr, *col_ptr;      // fill pass (col_ptr: null without the transpose)
+    int32_t *col_idx, *row_idx;
+    int64_t cap;
+};
+
+// Every event of the tile's pixels: its row (and column) length, or its row
+// (and column) entries.  c_off: prefix of the list lengths of the tile's own
+// pixels (nc + 1 entries); HX: halo row length.
+template <int kSide, bool kFill>
+__device__ __forceinline__ void tile_events(const TileArgs &A, const int32_t *Li,
+                                            const int32_t *Lt, const int32_t *start,
+                                            const int32_t *len, const int32_t *c_off, int nc,
+                                            int HX) {
+    constexpr int h = kSide / 2;
+    constexpr int K = kSide * kSide;
+    const int32_t total = c_off[nc];
+    for (int32_t u = threadIdx.x; u < total; u += kTileThreads) {
+        int lo = 0, hi = nc - 1;  // the tile pixel holding event u: last c with c_off[c] <= u
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (c_off[mid] <= u) lo = mid; else hi = mid - 1;
+        }
+        const int c = lo;
+        const int p = (c / A.tx + h) * HX + (c % A.tx + h);
+        const int32_t a = start[p] + (u - c_off[c]);
+        const int32_t i = Li[a], ti = Lt[a];
+        int32_t rlo[K], rhi[K];
+        const int32_t cnt = tile_runs<kSide, false>(i, ti, A.window, p, HX, Li, Lt, start, len,
+                                                    rlo, rhi);
+        if constexpr (!kFill) {
+            A.row_len[i] = cnt;
+        } else {
+            merge_runs<K>(Li, rlo, rhi, cnt, A.col_idx, A.row_ptr[i], A.cap);
+        }
+        const bool rev = kFill ? A.col_ptr != nullptr : A.col_len != nullptr;
+        if (rev) {
+            const int32_t cnt_t = tile_runs<kSide, true>(i, ti, A.window, p, HX, Li, Lt, start,
+                                                         len, rlo, rhi);
+            if constexpr (!kFill)
+                A.col_len[i] = cnt_t;
+            else
+                merge_runs<K>(Li, rlo, rhi, cnt_t, A.row_idx, A.col_ptr[i], A.cap);
+        }
+    }
+}
+
+template <int kSide, bool kFill>
+__global__ void __launch_bounds__(kTileThreads) event_tile_kernel(TileArgs A) {
+    constexpr int h = kSide / 2;
+    constexpr int kMaxNP = (kMaxTile + 2 * h) * (kMaxTile + 2 * h);
+    static_assert(kMaxNP <= kTileThreads, "a thread per halo pixel");
+    static_assert(kMaxTile * kMaxTile <= 64, "a lane per tile pixel");
+    __shared__ int32_t s_start[kMaxNP], s_gstart[kMaxNP], s_len[kMaxNP];
+    __shared__ int32_t s_coff[kMaxTile * kMaxTile + 1];
+    __shared__ int32_t s_w[kTileThreads / 64];
+    __shared__ int32_t s_idx[kTileCap], s_t[kTileCap];
+    const int tid = threadIdx.x;
+    const int64_t npix = (int64_t)A.W * A.H;
+    if ((int)blockIdx.x == A.n_tiles) {
+        // events off the sensor (sorted behind every pixel): empty rows and columns
+        if constexpr (!kFill) {
+            for (int32_t a = A.pix_start[npix] + tid; a < A.n; a += kTileThreads) {
+                const int32_t i = A.list[a];
+                A.row_len[i] = 0;
+                if (A.col_len) A.col_len[i] = 0;
+            }
+        }
+        return;
+    }
+    const int HX = A.tx + 2 * h, NP = HX * (A.ty + 2 * h), nc = A.tx * A.ty;
+    const int32_t tx0 = (int32_t)(blockIdx.x % A.tiles_x) * A.tx;
+    const int32_t ty0 = (int32_t)(blockIdx.x / A.tiles_x) * A.ty;
+    int32_t len = 0, gs = 0;
+    if (tid < NP) {
+        const int32_t x = tx0 - h + tid % HX, y = ty0 - h + tid / HX;
+        if (valid_pixel(x, y, A.W, A.H)) {
+            const int64_t q = (int64_t)y * A.W + x;
+            gs = A.pix_start[q];
+            len = A.pix_start[q + 1] - gs;
+        }
+    }
+    int32_t total;
+    const int32_t off = block_excl_scan(len, s_w, &total);
+    if (tid < NP) {
+        s_start[tid] = off;
+        s_gstart[tid] = gs;
+        s_len[tid] = len;
+    }
+    __syncthreads();
+    // the tile's own pixels: prefix of their list lengths (wave 0)
+    if (tid < 64) {
+        const int c = tid;
+        const int32_t v = c < nc ? s_len[(c / A.tx + h) * HX + (c % A.tx + h)] : 0;
+        int32_t incl = v;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int32_t y = __shfl_up(incl, d, 64);
+            if (tid >= d) incl += y;
+        }
+        if (c < nc) s_coff[c] = incl - v;
+        if (c == nc - 1) s_coff[nc] = incl;
+    }
+    const bool staged = total <= kTileCap;
+    if (staged) {
+        for (int32_t a = tid; a < total; a += kTileThreads) {
+            // the halo pixel holding entry a: the last one starting at or before a
+            int lo = 0, hi = NP - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (s_start[mid] <= a) lo = mid; else hi = mid - 1;
+            }
+            const int32_t src = s_gstart[lo] + (a - s_start[lo]);
+            s_idx[a] = A.list[src];
+            s_t[a] = A.list_t[src];
+        }
+    }
+    __syncthreads();
+    if (staged)
+        tile_events<kSide, kFill>(A, s_idx, s_t, s_start, s_len, s_coff, nc, HX);
+    else
+        tile_events<kSide, kFill>(A, A.list, A.list_t, s_gstart, s_len, s_coff, nc, HX);
 }
 
 struct EventsWs {
@@ -233,7 +302,7 @@ struct EventsWs {
     int32_t *list;
     int32_t *list_t;
     int32_t *row_len;
-    int2 *runs;
+    int32_t *col_len;
     int64_t *total;
     uint32_t *status;
     void *scan_ws;
@@ -249,7 +318,7 @@ EventsWs carve_events(void *base, int32_t n, int64_t npix, size_t *bytes) {
     w.list = cv.take<int32_t>(n);
     w.list_t = cv.take<int32_t>(n);
     w.row_len = cv.take<int32_t>(n);
-    w.runs = cv.take<int2>((size_t)n * kRunsK);
+    w.col_len = cv.take<int32_t>(n);
     w.total = cv.take<int64_t>(2);
     w.status = cv.take<uint32_t>(4);
     w.scan_ws = cv.take<char>(scan_workspace_bytes(n));
@@ -258,56 +327,18 @@ EventsWs carve_events(void *base, int32_t n, int64_t npix, size_t *bytes) {
     return w;
 }
 
-template <int kSide, bool kRev>
-void launch_rows(int32_t n, const int32_t *px, const int32_t *py, const int32_t *t, int32_t W,
-                 int32_t H, int32_t window, const EventsWs &ws, int32_t *row_len,
-                 const int32_t *row_ptr, int32_t *col_idx, int64_t cap, hipStream_t stream) {
-    constexpr bool kStored = kSide * kSide <= kRunsK;
-    hipLaunchKernelGGL((event_rows_kernel<kSide, kStored, kRev>), dim3(grid_for(n, 256)),
-                       dim3(256), 0, stream, px, py, t, n, W, H, window, ws.pix_start, ws.list,
-                       ws.list_t, row_len, row_ptr, col_idx, cap, ws.runs);
-}
-
-template <int kSide, bool kRev>
-void launch_runs(int64_t npix, int32_t W, int32_t H, int32_t window, const EventsWs &ws,
-                 hipStream_t stream) {
-    if constexpr (kSide * kSide <= kRunsK) {
-        const int64_t threads = npix * kSide * kSide;
-        hipLaunchKernelGGL((pixel_runs_kernel<kSide, kRev>),
-                           dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, npix, W,
-                           H, window, ws.pix_start, ws.list, ws.list_t, ws.runs);
-    }
-}
-
-template <bool kRev>
-sbc_status runs_dispatch(int32_t half_extent, int64_t npix, int32_t W, int32_t H, int32_t window,
-                         const EventsWs &ws, hipStream_t stream) {
-    switch (half_extent) {
-        case 0: launch_runs<1, kRev>(npix, W, H, window, ws, stream); break;
-        case 1: launch_runs<3, kRev>(npix, W, H, window, ws, stream); break;
-        default: return SBC_OK;  // larger blocks bisect per event
-    }
-    SBC_LAUNCH_CHECK();
-    return SBC_OK;
-}
-
-// Count pass (row_len != null; computes the runs first) or fill pass, of the
-// pattern (kRev false) or of its transpose (kRev true).
-template <bool kRev>
-sbc_status rows_dispatch(int32_t half_extent, int64_t npix, int32_t n, const int32_t *px,
-                         const int32_t *py, const int32_t *t, int32_t W, int32_t H,
-                         int32_t window, const EventsWs &ws, int32_t *row_len,
-                         const int32_t *row_ptr, int32_t *col_idx, int64_t cap,
-                         hipStream_t stream) {
-    const char *name = kRev ? (row_len ? "events_count_t" : "events_fill_t")
-                            : (row_len ? "events_count" : "events_fill");
+// Count pass (kFill false) or fill pass over all tiles, plus one workgroup
+// for the events off the sensor.
+template <bool kFill>
+sbc_status tiles_dispatch(int32_t half_extent, const TileArgs &A, hipStream_t stream) {
+    const char *name = kFill ? "events_fill" : "events_count";
+    const dim3 grid((unsigned)(A.n_tiles + 1)), block(kTileThreads);
     trace_before(name, stream);
-    if (row_len) SBC_TRY(runs_dispatch<kRev>(half_extent, npix, W, H, window, ws, stream));
     switch (half_extent) {
-        case 0: launch_rows<1, kRev>(n, px, py, t, W, H, window, ws, row_len, row_ptr, col_idx, cap, stream); break;
-        case 1: launch_rows<3, kRev>(n, px, py, t, W, H, window, ws, row_len, row_ptr, col_idx, cap, stream); break;
-        case 2: launch_rows<5, kRev>(n, px, py, t, W, H, window, ws, row_len, row_ptr, col_idx, cap, stream); break;
-        case 3: launch_rows<7, kRev>(n, px, py, t, W, H, window, ws, row_len, row_ptr, col_idx, cap, stream); break;
+        case 0: hipLaunchKernelGGL((event_tile_kernel<1, kFill>), grid, block, 0, stream, A); break;
+        case 1: hipLaunchKernelGGL((event_tile_kernel<3, kFill>), grid, block, 0, stream, A); break;
+        case 2: hipLaunchKernelGGL((event_tile_kernel<5, kFill>), grid, block, 0, stream, A); break;
+        case 3: hipLaunchKernelGGL((event_tile_kernel<7, kFill>), grid, block, 0, stream, A); break;
         default: return fail(SBC_ERR_UNSUPPORTED, "half_extent must be 0..3");
     }
     SBC_LAUNCH_CHECK();
@@ -316,7 +347,7 @@ sbc_status rows_dispatch(int32_t half_extent, int64_t npix, int32_t n, const int
 }
 
 // The search; with col_ptr non-null the transposed pattern too (col_ptr,
-// row_idx, from the same pixel lists, after the pattern itself).
+// row_idx), in the same passes over the same pixel lists.
 sbc_status search_events(const int32_t *px, const int32_t *py, const int32_t *t, int32_t n,
                          int32_t width, int32_t height, int32_t half_extent, int32_t window,
                          int32_t *row_ptr, int32_t *col_idx, int32_t *col_ptr,
@@ -339,6 +370,24 @@ sbc_status search_events(const int32_t *px, const int32_t *py, const int32_t *t,
     if (!workspace || workspace_bytes < need)
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_events_workspace_size()");
 
+    TileArgs A{};
+    A.n = n;
+    A.W = width;
+    A.H = height;
+    A.window = window;
+    // square tiles holding about kTileThreads events at the stream's mean
+    // density (a tile of s x s pixels, 1 <= s <= kMaxTile)
+    const double per_pix = npix > 0 ? (double)n / (double)npix : 0.0;
+    int side = per_pix > 0.0 ? (int)std::lround(std::sqrt(kTileThreads / per_pix)) : kMaxTile;
+    side = side < 1 ? 1 : (side > kMaxTile ? kMaxTile : side);
+    A.tx = A.ty = side;
+    A.tiles_x = (width + side - 1) / side;
+    A.n_tiles = (int32_t)((int64_t)A.tiles_x * ((height + side - 1) / side));  // <= W * H
+    A.pix_start = ws.pix_start;
+    A.list = ws.list;
+    A.list_t = ws.list_t;
+    A.cap = col_capacity;
+
     SBC_TRY(fill_i32(reinterpret_cast<int32_t *>(ws.status), 0, 1, stream));
     if (n == 0) SBC_TRY(fill_i32(ws.pix_start, 0, npix + 1, stream));
     if (n > 0) {
@@ -354,8 +403,10 @@ sbc_status search_events(const int32_t *px, const int32_t *py, const int32_t *t,
         hipLaunchKernelGGL(list_times_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream,
                            ws.list, t, ws.pix_start, npix, ws.list_t);
         SBC_LAUNCH_CHECK();
-        SBC_TRY(rows_dispatch<false>(half_extent, npix, n, px, py, t, width, height, window, ws,
-                                     ws.row_len, nullptr, nullptr, 0, stream));
+        TileArgs C = A;
+        C.row_len = ws.row_len;
+        C.col_len = col_ptr ? ws.col_len : nullptr;
+        SBC_TRY(tiles_dispatch<false>(half_extent, C, stream));
     }
     SBC_TRY(exclusive_scan_i32(ws.row_len, row_ptr, n, ws.total, ws.scan_ws, stream));
     if (nnz_host) {
@@ -372,18 +423,15 @@ sbc_status search_events(const int32_t *px, const int32_t *py, const int32_t *t,
             return fail(SBC_ERR_CAPACITY, "col_capacity " + std::to_string(col_capacity) +
                                               " < E = " + std::to_string(host[0]));
     }
-    if (n > 0 && col_capacity > 0)
-        SBC_TRY(rows_dispatch<false>(half_extent, npix, n, px, py, t, width, height, window, ws,
-                                     nullptr, row_ptr, col_idx, col_capacity, stream));
-    if (!col_ptr) return SBC_OK;
-    // the transpose: the runs and row lengths of the pattern are no longer needed
-    if (n > 0)
-        SBC_TRY(rows_dispatch<true>(half_extent, npix, n, px, py, t, width, height, window, ws,
-                                    ws.row_len, nullptr, nullptr, 0, stream));
-    SBC_TRY(exclusive_scan_i32(ws.row_len, col_ptr, n, ws.total, ws.scan_ws, stream));
-    if (n > 0 && col_capacity > 0)
-        SBC_TRY(rows_dispatch<true>(half_extent, npix, n, px, py, t, width, height, window, ws,
-                                    nullptr, col_ptr, row_idx, col_capacity, stream));
+    if (col_ptr) SBC_TRY(exclusive_scan_i32(ws.col_len, col_ptr, n, ws.total, ws.scan_ws, stream));
+    if (n > 0 && col_capacity > 0) {
+        TileArgs F = A;
+        F.row_ptr = row_ptr;
+        F.col_idx = col_idx;
+        F.col_ptr = col_ptr;
+        F.row_idx = col_ptr ? row_idx : nullptr;
+        SBC_TRY(tiles_dispatch<true>(half_extent, F, stream));
+    }
     return SBC_OK;
 }
 
