@@ -44,6 +44,42 @@ def point_basis(x_in, x_out, row_ptr, col_idx, radius, M):
     return np.stack([m * w for m in mono], axis=1)
 
 
+def weighted_point_basis(x_in, x_out, row_ptr, col_idx, radius):
+    """The weighted convolution's values with the full second-order monomials.
+
+    Section 3.1, "Weighted Convolutions" (Eq. 11): every value of row i is
+    multiplied by w_ij / W_i, with w_ij = 1 - |dx_ij| / r, which falls to zero
+    at the ball radius, and W_i the sum of w_ij over the row.  The basis is
+    the full set of monomials up to second order of u = dx / r that the
+    paper's networks use (M = 10): [1, ux, uy, uz, ux^2, uy^2, uz^2, ux*uy,
+    ux*uz, uy*uz], with no other window.  A row whose weights sum to zero gets
+    zero values.  r is the float32 radius of the search; coordinate
+    differences are exact in float64.
+    """
+    r = float(np.float32(radius))
+    rows = edge_rows(row_ptr)
+    cols = np.asarray(col_idx, dtype=np.int64)
+    d = np.asarray(x_out, np.float64)[rows] - np.asarray(x_in, np.float64)[cols]
+    u = d / r
+    ux, uy, uz = u[:, 0], u[:, 1], u[:, 2]
+    w = 1.0 - np.sqrt((d * d).sum(axis=1)) / r
+    n_rows = len(row_ptr) - 1
+    W = np.zeros(n_rows, dtype=np.float64)
+    np.add.at(W, rows, w)
+    Wr = W[rows]
+    scale = np.divide(w, Wr, out=np.zeros_like(w), where=Wr != 0.0)
+    mono = [np.ones_like(ux), ux, uy, uz, ux * ux, uy * uy, uz * uz, ux * uy, ux * uz, uy * uz]
+    return np.stack([m * scale for m in mono], axis=1)
+
+
+def point_values(basis, x_in, x_out, row_ptr, col_idx, radius, M):
+    """Values of a point basis by name: "wmono10" is the weighted convolution,
+    any other name the windowed monomials of M functions."""
+    if basis == "wmono10":
+        return weighted_point_basis(x_in, x_out, row_ptr, col_idx, radius)
+    return point_basis(x_in, x_out, row_ptr, col_idx, radius, M)
+
+
 def event_offset_index(ux, uy, half_extent=1):
     """Basis index of pixel offset (ux, uy): row-major over (uy, ux), centre removed.
 

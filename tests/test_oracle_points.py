@@ -191,3 +191,70 @@ def test_basis_closed_forms():
     assert np.all(v[1] == 0)                                  # |u| = 1: window vanishes
     # u = (0, -0.5, -0.5): |u|^2 = 0.5, w = 0.25
     assert v[2].tolist() == [0.25, 0, -0.125, -0.125, 0, 0.0625, 0.0625, 0]
+
+
+# ---------------------------------------------------------------- weighted convolution (Eq. 11)
+def _frac(x):
+    from fractions import Fraction
+    return float(Fraction(x))
+
+
+def test_weighted_hand_case():
+    """Eq. 11 with the M = 10 monomials on a hand-computed row (fractions in the fixture)."""
+    g = _gold("points_weighted_hand_case.json")
+    x_in, s_in, x_out, s_out = _single(g["x_in"], g["x_out"])
+    rp, ci = oracle.points_csr(x_in, s_in, x_out, s_out, g["radius"], 0)
+    assert rp.tolist() == g["row_ptr"] and ci.tolist() == g["col_idx"]
+    v = oracle.basis.weighted_point_basis(x_in, x_out, rp, ci, g["radius"])
+    want = np.array([[_frac(x) for x in row] for row in g["v"]])
+    assert v.shape == (3, 10)
+    assert np.allclose(v, want, rtol=1e-15, atol=1e-16)
+
+
+def _weighted_cloud(seed, n=600, n_out=150, radius=0.3):
+    rng = np.random.default_rng(seed)
+    x = workloads.ellipsoid_surface_points(rng, n, np.array([1.0, 0.7, 0.5])).astype(np.float32)
+    y = x[:n_out]
+    s_in = np.array([0, n], np.int32)
+    s_out = np.array([0, n_out], np.int32)
+    rp, ci = oracle.points_csr(x, s_in, y, s_out, radius, 0)
+    return x, y, rp, ci, radius
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_weighted_rows_are_a_partition_of_unity(seed):
+    """The constant basis function's values of a row sum to 1 (sum_j w_ij / W_i),
+    and a row with one neighbour gets weight exactly 1."""
+    x, y, rp, ci, r = _weighted_cloud(seed)
+    v = oracle.basis.weighted_point_basis(x, y, rp, ci, r)
+    lens = np.diff(rp)
+    sums = np.add.reduceat(v[:, 0], rp[:-1][lens > 0])
+    assert np.allclose(sums, 1.0, rtol=0, atol=1e-13)
+    single = np.nonzero(lens == 1)[0]
+    assert np.all(v[rp[single], 0] == 1.0)
+    # the weights fall to zero towards the sphere: every value is a weighted
+    # monomial of |u| < 1, so no column exceeds 1 in magnitude
+    assert np.abs(v).max() <= 1.0
+
+
+def test_weighted_translation_invariance():
+    x, y, rp, ci, r = _weighted_cloud(2)
+    shift = np.array([0.5, -0.25, 0.125], np.float64)
+    v = oracle.basis.weighted_point_basis(x, y, rp, ci, r)
+    v2 = oracle.basis.weighted_point_basis(x.astype(np.float64) + shift,
+                                           y.astype(np.float64) + shift, rp, ci, r)
+    assert np.allclose(v, v2, rtol=0, atol=1e-12)
+
+
+def test_weighted_mirror_symmetry():
+    """Mirroring x flips exactly the monomials odd in ux: ux, ux*uy, ux*uz."""
+    x, y, rp, ci, r = _weighted_cloud(3)
+    v = oracle.basis.weighted_point_basis(x, y, rp, ci, r)
+    m = np.array([-1.0, 1.0, 1.0])
+    vm = oracle.basis.weighted_point_basis(x * m, y * m, rp, ci, r)
+    sign = np.array([1, -1, 1, 1, 1, 1, 1, -1, -1, 1], np.float64)
+    assert np.allclose(vm, v * sign, rtol=0, atol=1e-13)
+    my = np.array([1.0, 1.0, -1.0])
+    vz = oracle.basis.weighted_point_basis(x * my, y * my, rp, ci, r)
+    sign_z = np.array([1, 1, 1, -1, 1, 1, 1, 1, -1, -1], np.float64)
+    assert np.allclose(vz, v * sign_z, rtol=0, atol=1e-13)

@@ -26,8 +26,9 @@ ROOT_SEED = 20120117
 BASIS_MONO4 = "mono4"      # {1, ux, uy, uz} x window, M = 4
 BASIS_MONO8 = "mono8"      # {1, ux, uy, uz, ux^2, uy^2, uz^2, ux*uy} x window, M = 8
 BASIS_EVENT8 = "event8"    # 3x3 pixel offsets without the centre, x exp decay, M = 8
+BASIS_WMONO10 = "wmono10"  # weighted convolution, all monomials up to 2nd order, M = 10
 
-BASIS_M = {BASIS_MONO4: 4, BASIS_MONO8: 8, BASIS_EVENT8: 8}
+BASIS_M = {BASIS_MONO4: 4, BASIS_MONO8: 8, BASIS_EVENT8: 8, BASIS_WMONO10: 10}
 
 
 def rng_for(config_index: int, salt: int = 0) -> np.random.Generator:
@@ -253,12 +254,19 @@ def events_1m_bf16():
     return bursty_event_stream()
 
 
+def ellipsoids_weighted():
+    """The in-place ellipsoid batch with the weighted convolution and M = 10:
+    32 clouds x 1024 points, r 0.1, cap 32, 64 -> 64 fp32."""
+    return ellipsoid_batch(seed_index=7, basis=BASIS_WMONO10)
+
+
 WORKLOADS = {
     "sphere_1024": sphere_1024,
     "ellipsoids_inplace": ellipsoids_inplace,
     "ellipsoids_down": ellipsoids_down,
     "events_300k": events_300k,
     "events_1m_bf16": events_1m_bf16,
+    "ellipsoids_weighted": ellipsoids_weighted,
 }
 
 
