@@ -46,6 +46,9 @@ DESCRIPTIONS = {
                    "M 8; 32 -> 32 channels fp32",
     "events_1m_bf16": "1M bursty events, 346x260 pixels, 200 ms; 3x3 block, 5 ms window; M 8; "
                       "64 -> 64 channels bf16 in, fp32 accumulate",
+    "ellipsoids_weighted": "32 clouds x 1024 points on ellipsoid surfaces, in place; r 0.1, "
+                           "cap 32; weighted convolution (Eq. 11), M 10 monomials up to 2nd "
+                           "order; 64 -> 64 channels fp32",
 }
 
 
@@ -284,7 +287,7 @@ def cpu_baseline(w, reps):
         if w["kind"] == "points":
             rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
                                        w["radius"], w["k_cap"])
-            v = oracle.basis.point_basis(w["x_in"], w["x_out"], rp, ci, w["radius"], w["M"])
+            v = oracle.basis.point_values(w["basis"], w["x_in"], w["x_out"], rp, ci, w["radius"], w["M"])
         else:
             rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"],
                                        w["height"])

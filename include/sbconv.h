@@ -77,11 +77,20 @@ typedef enum {
  *   SBC_BASIS_EVENT8  M = 8: p_m = [m == idx(u)] * exp(-dt / tau), with idx
  *                     row-major over (uy, ux) and the centre offset removed
  *                     (same-pixel edges have an all-zero basis row).
+ * Weighted convolution (Section 3.1, "Weighted Convolutions", Eq. 11) with the
+ * full second-order monomial set of the paper's networks, u = (x'_i - x_j) / r:
+ *   SBC_BASIS_WMONO10 M = 10: [1, ux, uy, uz, ux^2, uy^2, uz^2, ux*uy, ux*uz,
+ *                     uy*uz] * w_ij / W_i, with w_ij = 1 - |x'_i - x_j| / r and
+ *                     W_i the sum of w_ij over row i (values 0 if W_i = 0).
+ *                     Its values depend on the whole row, so the unfused
+ *                     routes evaluate them in CSR order and a transpose given
+ *                     to sbc_conv_backward needs its edge_perm.
  */
 typedef enum {
     SBC_BASIS_MONO4 = 0,
     SBC_BASIS_MONO8 = 1,
-    SBC_BASIS_EVENT8 = 2
+    SBC_BASIS_EVENT8 = 2,
+    SBC_BASIS_WMONO10 = 3
 } sbc_basis;
 
 /*
@@ -281,7 +290,8 @@ sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v, const sbc_geomet
  *   dW  [M, C_in, C_out]  float32 output, or NULL to skip
  *   csc                   the transpose of csr (sbc_csr_transpose, or
  *                         sbc_neighbour_search_events_csc); its edge_perm
- *                         may be NULL only when v is NULL
+ *                         may be NULL only when v is NULL and the basis is
+ *                         not SBC_BASIS_WMONO10
  * dW sums over every edge of the batch, in a fixed blocked order.
  * ------------------------------------------------------------------------ */
 sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v,

@@ -16,7 +16,7 @@ STATUS_NAMES = {0: "SBC_OK", 1: "SBC_ERR_INVALID_ARG", 2: "SBC_ERR_CAPACITY",
                 3: "SBC_ERR_OVERFLOW", 4: "SBC_ERR_UNSORTED", 5: "SBC_ERR_OUT_OF_RANGE",
                 6: "SBC_ERR_WORKSPACE", 7: "SBC_ERR_HIP", 8: "SBC_ERR_UNSUPPORTED"}
 SBC_F32, SBC_BF16 = 0, 1
-SBC_BASIS_MONO4, SBC_BASIS_MONO8, SBC_BASIS_EVENT8 = 0, 1, 2
+SBC_BASIS_MONO4, SBC_BASIS_MONO8, SBC_BASIS_EVENT8, SBC_BASIS_WMONO10 = 0, 1, 2, 3
 SBC_ORDER_AUTO, SBC_ORDER_SPMM_FIRST, SBC_ORDER_GEMM_FIRST = 0, 1, 2
 
 EXPORTS = [

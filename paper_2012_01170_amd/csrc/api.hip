@@ -86,6 +86,7 @@ extern "C" int32_t sbc_basis_size(sbc_basis basis) {
         case SBC_BASIS_MONO4: return 4;
         case SBC_BASIS_MONO8: return 8;
         case SBC_BASIS_EVENT8: return 8;
+        case SBC_BASIS_WMONO10: return 10;
     }
     return 0;
 }

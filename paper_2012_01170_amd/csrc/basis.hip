@@ -55,11 +55,49 @@ __global__ void __launch_bounds__(256)
     }
 }
 
+// Weighted values (Eq. 11): a group of kWLanes lanes per row sums the row's
+// weights in float64 (lane partial sums in edge order, then a butterfly, so
+// the sum does not depend on scheduling) and writes every edge's ten values
+// times w / W_i; the row's [E, 10] values are contiguous.
+constexpr int kWLanes = 16;
+
+__global__ void __launch_bounds__(256)
+    weighted_basis_kernel(int32_t n_rows, const int32_t *__restrict__ row_ptr,
+                          const int32_t *__restrict__ col_idx, int64_t nnz_bound, sbc_geometry g,
+                          float *__restrict__ v) {
+    const int sl = threadIdx.x % kWLanes;
+    const int64_t r = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWLanes;
+    if (r >= n_rows) return;  // a group leaves as a whole
+    // entries past nnz_bound (a malformed pattern) have no room in v
+    int64_t e1 = row_ptr[r + 1] < nnz_bound ? (int64_t)row_ptr[r + 1] : nnz_bound;
+    int64_t e0 = row_ptr[r] < e1 ? (int64_t)row_ptr[r] : e1;
+    const double inv_r = 1.0 / (double)g.radius;
+    const float qx = g.x_out[3 * r], qy = g.x_out[3 * r + 1], qz = g.x_out[3 * r + 2];
+    double wsum = 0.0;
+    for (int64_t e = e0 + sl; e < e1; e += kWLanes) {
+        const int64_t j = col_idx[e];
+        wsum += point_weight(qx, qy, qz, g.x_in[3 * j], g.x_in[3 * j + 1], g.x_in[3 * j + 2], inv_r);
+    }
+#pragma unroll
+    for (int d = kWLanes / 2; d >= 1; d >>= 1) wsum += __shfl_xor(wsum, d, kWLanes);
+    for (int64_t e = e0 + sl; e < e1; e += kWLanes) {
+        const int64_t j = col_idx[e];
+        const float px = g.x_in[3 * j], py = g.x_in[3 * j + 1], pz = g.x_in[3 * j + 2];
+        const double w = point_weight(qx, qy, qz, px, py, pz, inv_r);
+        const double s = wsum != 0.0 ? w / wsum : 0.0;
+        float out[10];
+        weighted_mono10(qx, qy, qz, px, py, pz, inv_r, s, out);
+#pragma unroll
+        for (int m = 0; m < 10; ++m) v[e * 10 + m] = out[m];
+    }
+}
+
 sbc_status check_geometry(const sbc_geometry *g, int32_t n_rows, int32_t n_cols) {
     if (!g) return fail(SBC_ERR_INVALID_ARG, "geometry is null");
     switch (g->basis) {
         case SBC_BASIS_MONO4:
         case SBC_BASIS_MONO8:
+        case SBC_BASIS_WMONO10:
             if (!(g->radius > 0.f)) return fail(SBC_ERR_INVALID_ARG, "radius must be > 0");
             if ((n_rows > 0 && !g->x_out) || (n_cols > 0 && !g->x_in))
                 return fail(SBC_ERR_INVALID_ARG, "x_in / x_out is null");
@@ -80,6 +118,16 @@ template <bool kT>
 sbc_status basis_launch(int32_t n_seg, const int32_t *seg_ptr, const int32_t *idx, int64_t nnz,
                         const sbc_geometry *g, float *v, hipStream_t stream) {
     if (n_seg == 0 || nnz <= 0) return SBC_OK;
+    if (g->basis == SBC_BASIS_WMONO10) {
+        // normalised by row sums: only in CSR order
+        if (kT) return fail(SBC_ERR_UNSUPPORTED, "the weighted basis is evaluated in CSR order");
+        trace_before("basis", stream);
+        hipLaunchKernelGGL(weighted_basis_kernel, dim3(grid_for((int64_t)n_seg * kWLanes, 256)),
+                           dim3(256), 0, stream, n_seg, seg_ptr, idx, nnz, *g, v);
+        SBC_LAUNCH_CHECK();
+        trace_after("basis", stream);
+        return SBC_OK;
+    }
     int64_t blocks = (nnz + 255) / 256;
     if (blocks > 8192) blocks = 8192;
     trace_before("basis", stream);

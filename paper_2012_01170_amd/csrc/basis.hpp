@@ -37,6 +37,35 @@ __device__ __forceinline__ void point_basis(float qx, float qy, float qz, float 
     }
 }
 
+// Weighted convolution (Section 3.1, Eq. 11) with every monomial up to second
+// order: an edge's weight w = 1 - |dx| / r, which falls to zero at the ball
+// radius, and its ten monomials of u = dx / r times s (= w / W_i, the row's
+// normaliser), as float32: [1, ux, uy, uz, ux^2, uy^2, uz^2, ux*uy, ux*uz,
+// uy*uz].  Differences are taken in float64 from the float32 coordinates.
+__device__ __forceinline__ double point_weight(float qx, float qy, float qz, float px, float py,
+                                               float pz, double inv_r) {
+    const double dx = (double)qx - (double)px, dy = (double)qy - (double)py,
+                 dz = (double)qz - (double)pz;
+    return 1.0 - sqrt(dx * dx + dy * dy + dz * dz) * inv_r;
+}
+
+__device__ __forceinline__ void weighted_mono10(float qx, float qy, float qz, float px, float py,
+                                                float pz, double inv_r, double s, float *v) {
+    const double ux = ((double)qx - (double)px) * inv_r;
+    const double uy = ((double)qy - (double)py) * inv_r;
+    const double uz = ((double)qz - (double)pz) * inv_r;
+    v[0] = (float)s;
+    v[1] = (float)(ux * s);
+    v[2] = (float)(uy * s);
+    v[3] = (float)(uz * s);
+    v[4] = (float)(ux * ux * s);
+    v[5] = (float)(uy * uy * s);
+    v[6] = (float)(uz * uz * s);
+    v[7] = (float)(ux * uy * s);
+    v[8] = (float)(ux * uz * s);
+    v[9] = (float)(uy * uz * s);
+}
+
 // Event basis: index of pixel offset u = (ux, uy) in the 3x3 block, row-major
 // over (uy, ux) with the centre removed; -1 for the centre (and for offsets
 // outside the block, which no neighbourhood produces).

@@ -194,7 +194,7 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 sbc_status check_conv_args(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,
                            const void *F, const void *W, sbc_dtype dtype, int32_t Ci, int32_t Co) {
     SBC_TRY(check_csr(csr));
-    if (M != 4 && M != 8) return fail(SBC_ERR_UNSUPPORTED, "M must be 4 or 8");
+    if (M != 4 && M != 8 && M != 10) return fail(SBC_ERR_UNSUPPORTED, "M must be 4, 8 or 10");
     if (Ci <= 0 || Co <= 0) return fail(SBC_ERR_INVALID_ARG, "C_in and C_out must be > 0");
     if (dtype != SBC_F32 && dtype != SBC_BF16) return fail(SBC_ERR_INVALID_ARG, "unknown dtype");
     if (!W || (csr->n_cols > 0 && !F)) return fail(SBC_ERR_INVALID_ARG, "F or W is null");
@@ -202,8 +202,8 @@ sbc_status check_conv_args(const sbc_csr *csr, const float *v, const sbc_geometr
         return fail(SBC_ERR_INVALID_ARG, "F and W must be 16-byte aligned");
     if (!v) {
         SBC_TRY(check_geometry(g, csr->n_rows, csr->n_cols));
-        const int32_t gm = g->basis == SBC_BASIS_MONO4 ? 4 : 8;
-        if (gm != M) return fail(SBC_ERR_INVALID_ARG, "M does not match the geometry's basis");
+        if (sbc_basis_size(g->basis) != M)
+            return fail(SBC_ERR_INVALID_ARG, "M does not match the geometry's basis");
     }
     return SBC_OK;
 }
@@ -316,6 +316,11 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
         return fail(SBC_ERR_INVALID_ARG, "csc is null or does not match csr");
     if (csr->nnz_bound > 0 && v && !csc->edge_perm)
         return fail(SBC_ERR_INVALID_ARG, "csc->edge_perm is needed when v is given");
+    // the weighted basis normalises by row (output) sums: its transposed
+    // entries take their values through edge_perm
+    if (csr->nnz_bound > 0 && !v && geometry && geometry->basis == SBC_BASIS_WMONO10 &&
+        !csc->edge_perm)
+        return fail(SBC_ERR_INVALID_ARG, "csc->edge_perm is needed for the weighted basis");
     if (!dY && csr->n_rows > 0) return fail(SBC_ERR_INVALID_ARG, "dY is null");
     if (!aligned16(dY) || !aligned16(dF) || !aligned16(dW))
         return fail(SBC_ERR_INVALID_ARG, "dY, dF and dW must be 16-byte aligned");

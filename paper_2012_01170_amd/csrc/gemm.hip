@@ -172,9 +172,11 @@ __global__ void splitk_reduce_kernel(const float *__restrict__ partial, int32_t 
 
 }  // namespace
 
-// Tile of a shape: 128 x 128, or 64 x 64 when the 128 tiles would be too few
-// to spread K over the chip without very short splits.
+// Tile of a shape: 128 x 128, or 64 x 64 when C has fewer than 128 rows or
+// columns (a 128 tile would be half empty) or when the 128 tiles would be too
+// few to spread K over the chip without very short splits.
 static int tile_for(int32_t R, int32_t N) {
+    if (R < 128 || N < 128) return 64;
     const int64_t big = (int64_t)((R + 127) / 128) * ((N + 127) / 128);
     return big >= 64 ? 128 : 64;
 }

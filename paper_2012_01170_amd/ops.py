@@ -17,8 +17,9 @@ from . import _lib as L
 
 ORDERS = {"auto": L.SBC_ORDER_AUTO, "spmm_first": L.SBC_ORDER_SPMM_FIRST,
           "gemm_first": L.SBC_ORDER_GEMM_FIRST}
-BASES = {"mono4": L.SBC_BASIS_MONO4, "mono8": L.SBC_BASIS_MONO8, "event8": L.SBC_BASIS_EVENT8}
-BASIS_M = {"mono4": 4, "mono8": 8, "event8": 8}
+BASES = {"mono4": L.SBC_BASIS_MONO4, "mono8": L.SBC_BASIS_MONO8, "event8": L.SBC_BASIS_EVENT8,
+         "wmono10": L.SBC_BASIS_WMONO10}
+BASIS_M = {"mono4": 4, "mono8": 8, "event8": 8, "wmono10": 10}
 
 
 def _require(t: torch.Tensor, name: str, dtype, ndim=None, device=None):

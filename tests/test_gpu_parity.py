@@ -44,6 +44,13 @@ SMALL = {
     "fz_tiny_pts": lambda: workloads.small_points(seed=12, n_clouds=1, n=90, c_in=64, c_out=64),
     "fz_tiny_bf16": lambda: workloads.small_events(seed=6, c=64, dtype="bf16", n=70),
     "fz_tiny_bf16_32": lambda: workloads.small_events(seed=13, c=32, dtype="bf16", n=70),
+    # the weighted convolution with M = 10 (unfused routes)
+    "pts_weighted": lambda: workloads.small_points(seed=14, basis=workloads.BASIS_WMONO10,
+                                                   c_in=16, c_out=24),
+    "pts_weighted_odd": lambda: workloads.small_points(seed=15, n_out=50, k_cap=0, c_in=5,
+                                                       c_out=7, basis=workloads.BASIS_WMONO10),
+    "pts_weighted_bf16": lambda: workloads.small_points(seed=16, basis=workloads.BASIS_WMONO10,
+                                                        c_in=32, c_out=32, dtype="bf16"),
 }
 FULL = list(workloads.WORKLOADS)
 ORDERS = ["spmm_first", "gemm_first"]
@@ -55,7 +62,7 @@ def case(name):
     if w["kind"] == "points":
         rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
                                    w["radius"], w["k_cap"])
-        v = oracle.basis.point_basis(w["x_in"], w["x_out"], rp, ci, w["radius"], w["M"])
+        v = oracle.basis.point_values(w["basis"], w["x_in"], w["x_out"], rp, ci, w["radius"], w["M"])
     else:
         rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"],
                                    w["height"])
@@ -153,7 +160,8 @@ def test_forward(name, order):
     assert err < tol(w)
 
 
-@pytest.mark.parametrize("name", ["pts_down", "ev_odd", "sphere_1024", "fz_pts64", "fz_ev32"])
+@pytest.mark.parametrize("name", ["pts_down", "ev_odd", "sphere_1024", "fz_pts64", "fz_ev32",
+                                  "pts_weighted"])
 def test_forward_with_materialised_basis(name):
     w, rp, ci, v = case(name)
     t, csr = gpu_case(name)
@@ -370,6 +378,28 @@ def test_two_rows_per_wave(k_cap):
     csr = G.search(w, t)
     assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
     assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+
+
+def test_weighted_basis_needs_edge_perm():
+    """The weighted basis is normalised per output row, so a transpose without
+    edge positions is refused (before anything is enqueued)."""
+    w, rp, ci, v = case("pts_weighted")
+    t, csr = gpu_case("pts_weighted")
+    csc = G.sbc.csr_transpose(csr)
+    bare = G.sbc.CSC(csc.col_ptr, csc.row_idx, None, csc.n_cols)
+    with pytest.raises(G.sbc.ops.L.SbcError, match="INVALID_ARG"):
+        G.sbc.conv_backward(csr, bare, t["F"], t["W"], t["dY"], geometry=G.geometry(w, t))
+
+
+def test_weighted_rows_sum_to_one_on_the_gpu():
+    """Partition of unity of the GPU's weighted values (Eq. 11): the constant
+    basis function's values of every non-empty row sum to 1."""
+    w, rp, ci, v = case("ellipsoids_weighted")
+    t, csr = gpu_case("ellipsoids_weighted")
+    vv = G.sbc.basis_eval(csr, G.geometry(w, t)).cpu().numpy().astype(np.float64)
+    lens = np.diff(rp)
+    sums = np.add.reduceat(vv[:, 0], rp[:-1][lens > 0])
+    assert np.allclose(sums, 1.0, rtol=0, atol=1e-5)
 
 
 def test_unsorted_and_out_of_range_events_are_reported():
