@@ -138,7 +138,7 @@ bool route_fused(Route r, int32_t M, int32_t Ci, int32_t Co, bool bf) {
 size_t route_bytes(Route r, int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t Ci,
                    int32_t Co, bool bf) {
     if (route_fused(r, M, Ci, Co, bf))
-        return fused_workspace_bytes(M, Ci, Co, n_out > n_in ? n_out : n_in);
+        return fused_workspace_bytes(M, Ci, Co, n_out > n_in ? n_out : n_in, nnz);
     size_t b = 0;
     carve_route(nullptr, r, n_out, n_in, nnz, M, Ci, Co, &b);
     return b;

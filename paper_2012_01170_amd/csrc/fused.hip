@@ -35,6 +35,7 @@
 #include "basis.hpp"
 #include "common.hpp"
 #include "fused.hpp"
+#include "spmm.hpp"
 
 namespace sbc {
 namespace {
@@ -1316,6 +1317,7 @@ BwdFn bwd_for(int basis_mode) {
 // C_in x M*C_out partial of dW per block in registers, so its list is limited
 // to C_in * M * C_out <= 32768.
 #define SBC_FWD_SHAPES(X) \
+    X(10, 64, 64, false)  \
     X(4, 16, 32, false)   \
     X(8, 64, 64, false)   \
     X(8, 64, 128, false)  \
@@ -1402,11 +1404,13 @@ bool fused_backward_available(int32_t M, int32_t CI, int32_t CO, bool bf) {
 }
 
 // Workspace of the fused kernels: a permuted copy of W, the per-block dW
-// partials, and the packed event coordinates.
-size_t fused_workspace_bytes(int32_t M, int32_t CI, int32_t CO, int32_t n_points) {
+// partials, the packed event coordinates, and for M = 10 (the weighted basis,
+// whose values need whole rows) the materialised basis values.
+size_t fused_workspace_bytes(int32_t M, int32_t CI, int32_t CO, int32_t n_points, int64_t nnz) {
     return align_up((size_t)M * CI * CO * 4) +
            align_up((size_t)kMaxBlocksBwd * (size_t)CI * M * CO * 4) +
-           align_up((size_t)(n_points > 0 ? n_points : 0) * sizeof(int4));
+           align_up((size_t)(n_points > 0 ? n_points : 0) * sizeof(int4)) +
+           (M == 10 ? align_up((size_t)(nnz > 0 ? nnz : 0) * M * 4) : 0);
 }
 
 namespace {
@@ -1445,6 +1449,14 @@ sbc_status make_kgeo(const sbc_csr *csr, const float *v, const sbc_geometry *g, 
 sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,
                          const void *F, const void *W, bool bf, int32_t CI, int32_t CO, float *Y,
                          void *ws, hipStream_t stream) {
+    if (!v && g->basis == SBC_BASIS_WMONO10) {
+        // row-normalised values: materialised first, behind the other regions
+        const int32_t n = csr->n_cols > csr->n_rows ? csr->n_cols : csr->n_rows;
+        float *vm = reinterpret_cast<float *>(
+            static_cast<char *>(ws) + fused_workspace_bytes(M, CI, CO, n, 0));
+        SBC_TRY(basis_eval_launch(csr, g, vm, stream));
+        v = vm;
+    }
     FwdFn fn = find_fwd(Shape{M, CI, CO, bf}, basis_mode_of(v, g));
     if (!fn) return fail(SBC_ERR_UNSUPPORTED, "no fused forward for this shape");
     if (csr->n_rows == 0) return SBC_OK;

@@ -51,6 +51,8 @@ SMALL = {
                                                        c_out=7, basis=workloads.BASIS_WMONO10),
     "pts_weighted_bf16": lambda: workloads.small_points(seed=16, basis=workloads.BASIS_WMONO10,
                                                         c_in=32, c_out=32, dtype="bf16"),
+    "fz_pts_weighted64": lambda: workloads.small_points(seed=17, basis=workloads.BASIS_WMONO10,
+                                                        c_in=64, c_out=64),
 }
 FULL = list(workloads.WORKLOADS)
 ORDERS = ["spmm_first", "gemm_first"]
