@@ -98,3 +98,24 @@ def backward(row_ptr, col_idx, v, F, W, dY, n_in, cols_subset=None, want_dW=True
         contrib = np.matmul(K, dYd[rows[e]][:, :, None])[:, :, 0]
         np.add.at(dF, pos_of[cols[e]], contrib)
     return dF, dW
+
+
+def featureless_forward(row_ptr, col_idx, v, Phi):
+    """The featureless convolution (Section 3.1, "Featureless Convolutions",
+    Eq. 9-10): with no input features (F = 1) the convolution reduces to a sum
+    of kernel values over the neighbourhood, Z = G~ Phi_0, where G~[i, m] is the
+    sum over row i of the basis values of function m and Phi_0 is an M x P
+    matrix (P output channels).  Returns (Z [n_out, P], G~ [n_out, M])."""
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    vd = np.asarray(v, dtype=np.float64)
+    n_out = len(row_ptr) - 1
+    Gt = np.zeros((n_out, vd.shape[1]))
+    rows = edge_rows(row_ptr)
+    np.add.at(Gt, rows, vd)
+    return Gt @ np.asarray(Phi, dtype=np.float64), Gt
+
+
+def featureless_backward(row_ptr, col_idx, v, dZ):
+    """Gradient of <Z, dZ> with respect to Phi_0: G~^T dZ (M x P)."""
+    _, Gt = featureless_forward(row_ptr, col_idx, v, np.zeros((np.asarray(v).shape[1], 1)))
+    return Gt.T @ np.asarray(dZ, dtype=np.float64)

@@ -295,3 +295,56 @@ def test_event_conv_equals_deployment_recursion():
         z[y, x] = F[i] + np.exp(-(t - last[y, x]) / tau) * z[y, x]
         last[y, x] = t
     np.testing.assert_allclose(Y, Y_ema, rtol=1e-11, atol=1e-11)
+
+
+# ---------------------------------------------------------------- featureless convolution
+def _featureless_case(seed=0, basis=workloads.BASIS_WMONO10):
+    w = workloads.small_points(seed=seed, basis=basis)
+    rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
+                               w["radius"], w["k_cap"])
+    v = oracle.basis.point_values(w["basis"], w["x_in"], w["x_out"], rp, ci, w["radius"], w["M"])
+    rng = np.random.default_rng(seed)
+    Phi = rng.standard_normal((w["M"], 6))
+    return w, rp, ci, v, Phi, rng
+
+
+@pytest.mark.parametrize("basis", [workloads.BASIS_WMONO10, workloads.BASIS_MONO8])
+def test_featureless_is_the_convolution_of_ones(basis):
+    """Eq. 9-10 is the general convolution with F = 1 (one input channel of ones)
+    and W_m = the m-th row of Phi_0."""
+    w, rp, ci, v, Phi, _ = _featureless_case(1, basis)
+    Z, _ = oracle.conv.featureless_forward(rp, ci, v, Phi)
+    ones = np.ones((w["n_in"], 1))
+    Y = oracle.conv.forward(rp, ci, v, ones, Phi[:, None, :])
+    assert np.allclose(Z, Y, rtol=1e-12, atol=1e-12)
+    dZ = np.random.default_rng(5).standard_normal(Z.shape)
+    dPhi = oracle.conv.featureless_backward(rp, ci, v, dZ)
+    _, dW = oracle.conv.backward(rp, ci, v, ones, Phi[:, None, :], dZ, w["n_in"])
+    assert np.allclose(dPhi, dW[:, 0, :], rtol=1e-12, atol=1e-12)
+
+
+def test_featureless_hand_case():
+    """The weighted hand row (fixture): G~ is the column sums of its values, so
+    the constant function sums to 1 and Z = G~ Phi_0 by hand."""
+    with open(os.path.join(os.path.dirname(__file__), "golden",
+                           "points_weighted_hand_case.json")) as f:
+        g = json.load(f)
+    from fractions import Fraction
+    v = np.array([[float(Fraction(x)) for x in row] for row in g["v"]])
+    Phi = np.zeros((10, 2))
+    Phi[0, 0] = 1.0       # Z[:, 0] = G~[:, 0] = 1
+    Phi[1, 1] = 17.0      # Z[:, 1] = 17 * G~[:, 1] = 17 * (-2/17 - 5/136) = -21/8
+    Z, Gt = oracle.conv.featureless_forward(g["row_ptr"], g["col_idx"], v, Phi)
+    assert np.isclose(Z[0, 0], 1.0, rtol=0, atol=1e-15)
+    assert np.isclose(Z[0, 1], -21.0 / 8.0, rtol=0, atol=1e-14)
+
+
+def test_featureless_adjoint_and_linearity():
+    w, rp, ci, v, Phi, rng = _featureless_case(2)
+    Z, _ = oracle.conv.featureless_forward(rp, ci, v, Phi)
+    dZ = rng.standard_normal(Z.shape)
+    dPhi = oracle.conv.featureless_backward(rp, ci, v, dZ)
+    assert np.isclose((Z * dZ).sum(), (Phi * dPhi).sum(), rtol=1e-12)
+    Z2, _ = oracle.conv.featureless_forward(rp, ci, v, 2.0 * Phi - 1.0)
+    Z1, _ = oracle.conv.featureless_forward(rp, ci, v, np.ones_like(Phi))
+    assert np.allclose(Z2, 2.0 * Z - Z1, rtol=1e-12, atol=1e-12)

@@ -260,6 +260,16 @@ def ellipsoids_weighted():
     return ellipsoid_batch(seed_index=7, basis=BASIS_WMONO10)
 
 
+def ellipsoids_featureless():
+    """The paper's first layer on the in-place ellipsoid batch: a featureless
+    convolution (F = 1) with the weighted M = 10 basis, 32 clouds x 1024 points,
+    r 0.1, cap 32, 32 output channels.  Phi_0 is W[:, 0, :] and dZ is dY."""
+    w = ellipsoid_batch(seed_index=7, basis=BASIS_WMONO10, c_in=1, c_out=32)
+    w["featureless"] = True
+    w["name"] = "ellipsoids32x1024_featureless"
+    return w
+
+
 WORKLOADS = {
     "sphere_1024": sphere_1024,
     "ellipsoids_inplace": ellipsoids_inplace,
@@ -267,6 +277,7 @@ WORKLOADS = {
     "events_300k": events_300k,
     "events_1m_bf16": events_1m_bf16,
     "ellipsoids_weighted": ellipsoids_weighted,
+    "ellipsoids_featureless": ellipsoids_featureless,
 }
 
 
