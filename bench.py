@@ -49,6 +49,9 @@ DESCRIPTIONS = {
     "ellipsoids_weighted": "32 clouds x 1024 points on ellipsoid surfaces, in place; r 0.1, "
                            "cap 32; weighted convolution (Eq. 11), M 10 monomials up to 2nd "
                            "order; 64 -> 64 channels fp32",
+    "ellipsoids_featureless": "32 clouds x 1024 points on ellipsoid surfaces, in place; r 0.1, "
+                              "cap 32; featureless convolution (Eq. 9-10) with the weighted "
+                              "M 10 basis; 32 output channels fp32",
 }
 
 
@@ -209,6 +212,21 @@ def summarize_trace(trace_dir, command, bench_json=None):
     return "\n".join(out) + "\n"
 
 
+def featureless_table(n_in, n_out, E, M, P):
+    """Kernels of one featureless step (search, Z = G~ Phi, dPhi = G~^T dZ):
+    name -> (launches, algorithmic bytes, flops, on MFMA)."""
+    geo = 12 * (n_in + n_out)
+    rows = 4 * (n_out + 1) + 4 * E + geo
+    return {
+        "points_count": (1, 12 * n_out + 16 * n_in + 4 * n_out, 0, False),
+        "points_fill": (1, 12 * n_out + 16 * n_in + 8 * n_out + 4 * E, 0, False),
+        "featureless_fwd": (1, rows + 4 * M * P + 4 * n_out * P, 2 * n_out * M * P, False),
+        "featureless_rowsum": (1, rows + 4 * n_out * M, 0, False),
+        "featureless_dphi": (1, 4 * n_out * M + 4 * n_out * P + 4 * M * P, 2 * n_out * M * P,
+                             True),
+    }
+
+
 def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256, npix=0):
     """Kernels of one step: name -> (launches per step, algorithmic bytes, flops, on MFMA).
 
@@ -292,16 +310,23 @@ def cpu_baseline(w, reps):
             rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"],
                                        w["height"])
             v = oracle.basis.event_basis(w["px"], w["py"], w["t"], rp, ci, w["tau"])
-        oracle.conv.forward(rp, ci, v, w["F"], w["W"])
-        oracle.csr_transpose(rp, ci, w["n_in"])
-        oracle.conv.backward(rp, ci, v, w["F"], w["W"], w["dY"], w["n_in"])
+        if w.get("featureless"):
+            Phi = w["W"][:, 0, :]
+            oracle.conv.featureless_forward(rp, ci, v, Phi)
+            oracle.conv.featureless_backward(rp, ci, v, w["dY"])
+        else:
+            oracle.conv.forward(rp, ci, v, w["F"], w["W"])
+            oracle.csr_transpose(rp, ci, w["n_in"])
+            oracle.conv.backward(rp, ci, v, w["F"], w["W"], w["dY"], w["n_in"])
         times.append(time.perf_counter() - t0)
         E = len(ci)
     med = statistics.median(times)
     return {"value": E / med, "unit": "edges/s", "cores": max(oracle.max_threads(), blas),
             "kind": "oracle",
-            "sample": f"whole workload ({E} edges): neighbours, basis, forward, transpose, "
-                      f"backward in float64; median of {reps} passes, {med:.2f} s each"}
+            "sample": f"whole workload ({E} edges): neighbours, basis, "
+                      + ("featureless forward and backward" if w.get("featureless")
+                         else "forward, transpose, backward")
+                      + f" in float64; median of {reps} passes, {med:.2f} s each"}
 
 
 def graph_timing(step, a, torch):
@@ -414,18 +439,30 @@ def main(argv=None):
     E = int(csr0.row_ptr[-1].item())
     plan = sbc.conv_plan(n_out, n_in, csr0.nnz, M, ci, co, F.dtype, a.order)
 
-    def step():
-        csr = search()
-        Y = sbc.conv_forward(csr, F, W, geometry=geo, order=a.order)
-        csc = transpose(csr)
-        dF, dW = sbc.conv_backward(csr, csc, F, W, dY, geometry=geo, order=a.order)
-        return Y, dF, dW
+    if w.get("featureless"):
+        # the first layer on bare coordinates: Phi_0 = W[:, 0, :], dZ = dY
+        Phi = W[:, 0, :].contiguous()
 
-    n_cus = torch.cuda.get_device_properties(dev).multi_processor_count
-    tr_bwd = 32                                           # the fused backward's tile rows
-    blocks_bwd = max(1, min(256, n_cus, (n_in + tr_bwd - 1) // tr_bwd))
-    npix = w["width"] * w["height"] if w["kind"] == "events" else 0
-    table = kernel_table(w["kind"], plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd, npix)
+        def step():
+            csr = search()
+            Z = sbc.featureless_forward(csr, Phi, geometry=geo)
+            dPhi = sbc.featureless_backward(csr, dY, M, geometry=geo)
+            return Z, dPhi
+
+        table = featureless_table(n_in, n_out, E, M, co)
+    else:
+        def step():
+            csr = search()
+            Y = sbc.conv_forward(csr, F, W, geometry=geo, order=a.order)
+            csc = transpose(csr)
+            dF, dW = sbc.conv_backward(csr, csc, F, W, dY, geometry=geo, order=a.order)
+            return Y, dF, dW
+
+        n_cus = torch.cuda.get_device_properties(dev).multi_processor_count
+        tr_bwd = 32                                       # the fused backward's tile rows
+        blocks_bwd = max(1, min(256, n_cus, (n_in + tr_bwd - 1) // tr_bwd))
+        npix = w["width"] * w["height"] if w["kind"] == "events" else 0
+        table = kernel_table(w["kind"], plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd, npix)
     L = _lib.lib()
     # one (start, stop) event pair per kernel per timed step; record once so the
     # underlying HIP events exist before the library records them again

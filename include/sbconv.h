@@ -301,6 +301,30 @@ sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, const float
                              void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * 6. The featureless convolution (Section 3.1, "Featureless Convolutions",
+ * Eq. 9-10): with no input features (F = 1) the convolution is a sum of
+ * kernel values over the neighbourhood,
+ *     Z [n_out, P] = G~ Phi,   G~[i, m] = sum over row i of the values of p_m,
+ * the first layer of a network on bare coordinates.
+ *   v, geometry  the basis values [E, M], or NULL with the geometry (any basis)
+ *   Phi          [M, P] float32 (the learned matrix Phi_0)
+ *   Z            [n_out, P] float32 output
+ * Row sums are taken in float64 in a fixed order.  The backward gives
+ *   dPhi [M, P] = G~^T dZ   (float32; dZ [n_out, P] float32),
+ * with the workspace of sbc_featureless_workspace_size (G~ and the split
+ * partial sums of the contraction).  No pointer needs more than 4-byte
+ * alignment.
+ * ------------------------------------------------------------------------ */
+size_t sbc_featureless_workspace_size(int32_t n_out, int32_t M, int32_t P);
+sbc_status sbc_featureless_forward(const sbc_csr *csr, const float *v,
+                                   const sbc_geometry *geometry, int32_t M, const float *Phi,
+                                   int32_t P, float *Z, hipStream_t stream);
+sbc_status sbc_featureless_backward(const sbc_csr *csr, const float *v,
+                                    const sbc_geometry *geometry, int32_t M, const float *dZ,
+                                    int32_t P, float *dPhi, void *workspace,
+                                    size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Tracing, for measurement tools.  After sbc_trace_kernel(name, start, stop)
  * every launch of the kernel called `name` made by the calling thread records
  * `start` immediately before and `stop` immediately after itself on its

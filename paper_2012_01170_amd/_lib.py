@@ -27,7 +27,8 @@ EXPORTS = [
     "sbc_transpose_workspace_size", "sbc_csr_transpose", "sbc_csr_transpose_batched",
     "sbc_conv_workspace_size", "sbc_conv_forward", "sbc_conv_backward",
     "sbc_resolve_order", "sbc_trace_kernel", "sbc_trace_clear", "sbc_kernel_names",
-    "sbc_conv_plan",
+    "sbc_conv_plan", "sbc_featureless_workspace_size", "sbc_featureless_forward",
+    "sbc_featureless_backward",
 ]
 
 
@@ -82,6 +83,10 @@ _SIGS = {
                                                        _i32, _vp, _vp, _vp, _vp, _i64, _i64_p,
                                                        _vp, _sz, _vp]),
     "sbc_basis_eval": (ctypes.c_int, [_csr_p, _geo_p, _vp, _vp]),
+    "sbc_featureless_workspace_size": (_sz, [_i32, _i32, _i32]),
+    "sbc_featureless_forward": (ctypes.c_int, [_csr_p, _vp, _geo_p, _i32, _vp, _i32, _vp, _vp]),
+    "sbc_featureless_backward": (ctypes.c_int, [_csr_p, _vp, _geo_p, _i32, _vp, _i32, _vp, _vp,
+                                                _sz, _vp]),
     "sbc_transpose_workspace_size": (_sz, [_i32, _i64]),
     "sbc_csr_transpose": (ctypes.c_int, [_csr_p, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sbc_csr_transpose_batched": (ctypes.c_int, [_csr_p, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),

@@ -14,7 +14,8 @@ const char *kKernelNames =
     "points_count,points_fill,events_count,events_fill,basis,"
     "transpose_count,transpose_scatter,transpose_sort,transpose_batched,"
     "fwd_spmm,fwd_gemm,fwd_gemm_h,fwd_spmm_contract,bwd_spmm,bwd_gemm_dw,bwd_gemm_dg,"
-    "bwd_spmm_t,bwd_spmm_t_expand,bwd_gemm_df,bwd_gemm_dw_t,fwd_fused,bwd_fused,bwd_dw_reduce";
+    "bwd_spmm_t,bwd_spmm_t_expand,bwd_gemm_df,bwd_gemm_dw_t,fwd_fused,bwd_fused,bwd_dw_reduce,"
+    "featureless_fwd,featureless_rowsum,featureless_dphi";
 }  // namespace
 
 void trace_before(const char *name, hipStream_t stream) {

@@ -315,6 +315,50 @@ def conv_backward(csr: CSR, csc: CSC, F, W, dY, geometry: Optional[Geometry] = N
     return dF, dW
 
 
+def _featureless_common(csr: CSR, M: int, geometry: Optional[Geometry], v):
+    dev = csr.row_ptr.device
+    if v is not None:
+        _require(v, "v", torch.float32, 2, dev)
+        if v.shape[1] != M:
+            raise ValueError("v must be [E, M]")
+    elif geometry is None:
+        raise ValueError("either v or geometry is needed")
+    g = geometry.c_struct() if geometry is not None else None
+    return dev, g
+
+
+def featureless_forward(csr: CSR, Phi, geometry: Optional[Geometry] = None,
+                        v=None) -> torch.Tensor:
+    """Z = G~ Phi, float32 [n_out, P] (sbc_featureless_forward); Phi [M, P] float32."""
+    _require(Phi, "Phi", torch.float32, 2, csr.row_ptr.device)
+    M, P = Phi.shape
+    dev, g = _featureless_common(csr, M, geometry, v)
+    Z = torch.empty((csr.n_rows, P), dtype=torch.float32, device=dev)
+    c = csr.c_struct()
+    L.check(L.lib().sbc_featureless_forward(
+        ctypes.byref(c), _p(v), ctypes.byref(g) if g is not None else None, M, _p(Phi), P,
+        _p(Z), _stream(dev)))
+    return Z
+
+
+def featureless_backward(csr: CSR, dZ, M: int, geometry: Optional[Geometry] = None,
+                         v=None) -> torch.Tensor:
+    """dPhi = G~^T dZ, float32 [M, P] (sbc_featureless_backward)."""
+    _require(dZ, "dZ", torch.float32, 2, csr.row_ptr.device)
+    if dZ.shape[0] != csr.n_rows:
+        raise ValueError(f"dZ must have {csr.n_rows} rows")
+    P = dZ.shape[1]
+    dev, g = _featureless_common(csr, M, geometry, v)
+    dPhi = torch.empty((M, P), dtype=torch.float32, device=dev)
+    lib = L.lib()
+    ws = _Workspace(lib.sbc_featureless_workspace_size(csr.n_rows, M, P), dev)
+    c = csr.c_struct()
+    L.check(lib.sbc_featureless_backward(
+        ctypes.byref(c), _p(v), ctypes.byref(g) if g is not None else None, M, _p(dZ), P,
+        _p(dPhi), ws.ptr, ws.nbytes, _stream(dev)))
+    return dPhi
+
+
 def conv_plan(n_out, n_in, nnz, M, C_in, C_out, dtype=torch.float32, order="auto") -> dict:
     """Route and fusion of forward and backward for a shape (sbc_conv_plan)."""
     plan = L.SbcConvPlan()

@@ -54,7 +54,10 @@ SMALL = {
     "fz_pts_weighted64": lambda: workloads.small_points(seed=17, basis=workloads.BASIS_WMONO10,
                                                         c_in=64, c_out=64),
 }
-FULL = list(workloads.WORKLOADS)
+# the general convolution's full-size cases; the featureless first layer
+# (one input channel of features ~N(0,1), so single-channel input gradients
+# whose sums cancel by up to 1e6) is checked as Eq. 9-10 instead
+FULL = [k for k in workloads.WORKLOADS if k != "ellipsoids_featureless"]
 ORDERS = ["spmm_first", "gemm_first"]
 
 
@@ -549,3 +552,30 @@ def test_transpose_by_radix_sort():
     assert np.array_equal(csc.col_ptr.cpu().numpy(), cp)
     assert np.array_equal(csc.row_idx[:len(ci)].cpu().numpy(), ri)
     assert np.array_equal(csc.edge_perm[:len(ci)].cpu().numpy(), perm)
+
+
+# ---------------------------------------------------------------- featureless convolution
+@pytest.mark.parametrize("materialised", [False, True])
+@pytest.mark.parametrize("name", ["pts_weighted", "pts_down", "pts_mono4_odd", "ev_small",
+                                  "pts_weighted_odd", "ellipsoids_featureless"])
+def test_featureless(name, materialised):
+    """Z = G~ Phi_0 and dPhi_0 = G~^T dZ (Eq. 9-10) against the oracle, with the
+    basis evaluated inside or read from v; Phi_0 is W[:, 0, :], dZ is dY."""
+    print(f"[featureless] {name} materialised={materialised}", flush=True)
+    w, rp, ci, v = case(name)
+    t, csr = gpu_case(name)
+    Phi = np.ascontiguousarray(np.asarray(w["W"], np.float32)[:, 0, :])
+    dZ = np.asarray(w["dY"], np.float32)
+    Z_ref, _ = oracle.conv.featureless_forward(rp, ci, v, Phi)
+    dPhi_ref = oracle.conv.featureless_backward(rp, ci, v, dZ)
+    geo = G.geometry(w, t)
+    vv = G.sbc.basis_eval(csr, geo) if materialised else None
+    kw = dict(v=vv) if materialised else dict(geometry=geo)
+    Z = G.sbc.featureless_forward(csr, G.dev(Phi), **kw).cpu().numpy()
+    dPhi = G.sbc.featureless_backward(csr, G.dev(dZ), w["M"], **kw).cpu().numpy()
+    e1 = G.row_error(Z, Z_ref)
+    e2 = G.norm_error(dPhi, dPhi_ref)
+    print(f"    Z row error {e1:.3e}  dPhi error {e2:.3e}", flush=True)
+    assert e1 < G.TOL_F32 and e2 < G.TOL_F32
+    empty = np.nonzero(np.diff(rp) == 0)[0]
+    assert np.all(Z[empty] == 0)
