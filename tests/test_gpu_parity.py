@@ -579,3 +579,39 @@ def test_featureless(name, materialised):
     assert e1 < G.TOL_F32 and e2 < G.TOL_F32
     empty = np.nonzero(np.diff(rp) == 0)[0]
     assert np.all(Z[empty] == 0)
+
+
+# ---------------------------------------------------------------- up-sampling shapes
+def _upsampling_case():
+    """Inputs are a quarter of each cloud, outputs the whole cloud, and the
+    channels shrink (48 -> 16): the up-sampling convolution of Table 1."""
+    rng = np.random.default_rng(21)
+    clouds = []
+    for b in range(3):
+        x = workloads.ellipsoid_surface_points(rng, 400 + 31 * b, rng.uniform(0.5, 1.0, size=3))
+        clouds.append((x[: len(x) // 4], x))
+    w = workloads.points_workload(rng, clouds, workloads.BASIS_MONO8, 0.3, 0, 48, 16)
+    rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
+                               w["radius"], 0)
+    v = oracle.basis.point_values(w["basis"], w["x_in"], w["x_out"], rp, ci, w["radius"], w["M"])
+    return w, rp, ci, v
+
+
+@pytest.mark.parametrize("order", ["auto"] + ORDERS)
+def test_upsampling(order):
+    print(f"[upsampling] {order}", flush=True)
+    w, rp, ci, v = _upsampling_case()
+    assert w["n_out"] > w["n_in"] and w["C_in"] > w["C_out"]
+    t = G.to_device(w)
+    csr = G.search(w, t)
+    assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
+    plan = G.sbc.conv_plan(w["n_out"], w["n_in"], csr.nnz, w["M"], w["C_in"], w["C_out"])
+    assert plan["forward_order"] == "gemm_first"     # Table 1: N (F W) for up-sampling
+    geo = G.geometry(w, t)
+    Y = G.sbc.conv_forward(csr, t["F"], t["W"], geometry=geo, order=order).cpu().numpy()
+    assert G.row_error(Y, oracle.conv.forward(rp, ci, v, w["F"], w["W"])) < G.TOL_F32
+    csc = G.sbc.csr_transpose(csr)
+    dF, dW = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"], geometry=geo, order=order)
+    dF_ref, dW_ref = oracle.conv.backward(rp, ci, v, w["F"], w["W"], w["dY"], w["n_in"])
+    assert G.row_error(dF.cpu().numpy(), dF_ref) < G.TOL_F32
+    assert G.norm_error(dW.cpu().numpy(), dW_ref) < G.TOL_F32
