@@ -309,7 +309,8 @@ def cpu_baseline(w, reps):
         else:
             rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"],
                                        w["height"])
-            v = oracle.basis.event_basis(w["px"], w["py"], w["t"], rp, ci, w["tau"])
+            v = oracle.basis.event_values(w["basis"], w["px"], w["py"], w["t"], rp, ci,
+                                          w["tau"], w.get("decays"))
         if w.get("featureless"):
             Phi = w["W"][:, 0, :]
             oracle.conv.featureless_forward(rp, ci, v, Phi)

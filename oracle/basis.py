@@ -114,3 +114,38 @@ def event_basis(px, py, t, row_ptr, col_idx, tau, half_extent=1):
     hit = m >= 0
     v[np.nonzero(hit)[0], m[hit]] = np.exp(-dt[hit] / float(tau))
     return v
+
+
+def event_values(basis, px, py, t, row_ptr, col_idx, tau, decays=None):
+    """Values of an event basis by name: "event_decays" is the learned-decay
+    kernel with the rates `decays` [8, M_v], any other name the fixed decay 1/tau."""
+    if basis == "event_decays":
+        return event_decay_basis(px, py, t, row_ptr, col_idx, decays)
+    return event_basis(px, py, t, row_ptr, col_idx, tau)
+
+
+def event_decay_basis(px, py, t, row_ptr, col_idx, lam, half_extent=1, derivative=False):
+    """The event kernel with several learned decays per offset (Section 3.2,
+    Eq. 12): g(u, dt) = sum_v exp(-lambda_uv dt) theta_uv, i.e. the basis
+    functions p_uv = [offset == u] exp(-lambda_uv dt), M = M_u M_v of them,
+    numbered m = u M_v + v (u the offset index with the centre removed).
+    lam: [M_u, M_v] decay rates.  derivative: the values of d p_uv / d lambda_uv
+    = -dt p_uv instead (the basis of the decay gradient).
+    """
+    lam = np.asarray(lam, dtype=np.float64)
+    Mu, Mv = lam.shape
+    rows = edge_rows(row_ptr)
+    cols = np.asarray(col_idx, dtype=np.int64)
+    px = np.asarray(px, dtype=np.int64)
+    py = np.asarray(py, dtype=np.int64)
+    t = np.asarray(t, dtype=np.int64)
+    u = event_offset_index(px[rows] - px[cols], py[rows] - py[cols], half_extent)
+    dt = (t[rows] - t[cols]).astype(np.float64)
+    v = np.zeros((len(cols), Mu * Mv), dtype=np.float64)
+    hit = np.nonzero(u >= 0)[0]
+    for q in range(Mv):
+        val = np.exp(-lam[u[hit], q] * dt[hit])
+        if derivative:
+            val = -dt[hit] * val
+        v[hit, u[hit] * Mv + q] = val
+    return v

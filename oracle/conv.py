@@ -119,3 +119,26 @@ def featureless_backward(row_ptr, col_idx, v, dZ):
     """Gradient of <Z, dZ> with respect to Phi_0: G~^T dZ (M x P)."""
     _, Gt = featureless_forward(row_ptr, col_idx, v, np.zeros((np.asarray(v).shape[1], 1)))
     return Gt.T @ np.asarray(dZ, dtype=np.float64)
+
+
+def decay_backward(row_ptr, col_idx, v_deriv, F, W, dY):
+    """Gradient of <Y, dY> with respect to the decay rates of the event kernel
+    (Section 3.2, Eq. 12: lambda_uv is learned), by the chain rule per edge:
+    d<Y, dY>/d lambda_m = sum_e v'[e, m] f_j W_m dy_i^T, with v' the values of
+    d p_m / d lambda_m (oracle.basis.event_decay_basis(..., derivative=True))."""
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    rows = edge_rows(row_ptr)
+    cols = np.asarray(col_idx, dtype=np.int64)
+    Fd = np.asarray(F, dtype=np.float64)
+    Wd = np.asarray(W, dtype=np.float64)
+    dYd = np.asarray(dY, dtype=np.float64)
+    vd = np.asarray(v_deriv, dtype=np.float64)
+    M = Wd.shape[0]
+    out = np.zeros(M)
+    for m in range(M):
+        nz = np.nonzero(vd[:, m])[0]
+        if len(nz) == 0:
+            continue
+        fw = Fd[cols[nz]] @ Wd[m]                      # [n_e, C_out]
+        out[m] = np.sum(vd[nz, m] * np.einsum("ij,ij->i", fw, dYd[rows[nz]]))
+    return out

@@ -71,7 +71,8 @@ def case(name):
     else:
         rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"],
                                    w["height"])
-        v = oracle.basis.event_basis(w["px"], w["py"], w["t"], rp, ci, w["tau"])
+        v = oracle.basis.event_values(w["basis"], w["px"], w["py"], w["t"], rp, ci,
+                                      w["tau"], w.get("decays"))
     return w, rp, ci, v
 
 

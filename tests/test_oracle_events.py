@@ -97,3 +97,81 @@ def test_event_basis_closed_forms():
     assert np.all(nz[~same_pixel] == 1)
     np.testing.assert_allclose(v.sum(axis=1)[~same_pixel], np.exp(-dt[~same_pixel] / w["tau"]),
                                rtol=1e-15, atol=0)
+
+
+# ---------------------------------------------------------------- learned decays (Eq. 12, M_v > 1)
+def _decay_problem(seed=0, n=900, Mv=2):
+    w = workloads.small_events(seed=seed, n=n, width=7, height=6, duration_us=6000,
+                               window_us=2500, c=3)
+    rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"], w["height"])
+    rng = np.random.default_rng(seed)
+    lam = rng.uniform(0.2, 3.0, size=(8, Mv)) / w["tau"]
+    return w, rp, ci, lam
+
+
+def test_single_decay_is_the_fixed_event_basis():
+    """M_v = 1 with lambda = 1/tau everywhere is the fixed-decay basis exactly."""
+    w, rp, ci, _ = _decay_problem(1)
+    lam = np.full((8, 1), 1.0 / w["tau"])
+    v = oracle.basis.event_decay_basis(w["px"], w["py"], w["t"], rp, ci, lam)
+    v0 = oracle.basis.event_basis(w["px"], w["py"], w["t"], rp, ci, w["tau"])
+    assert np.allclose(v, v0, rtol=1e-14, atol=0)
+
+
+def test_decays_equal_the_deployment_recursion():
+    """Eq. 13-15 with M_v = 2 decays per offset: every pixel keeps one decayed
+    sum per (offset, decay); an output decays the block's sums to its own time
+    and applies Theta_uv.  With a window longer than the stream both forms sum
+    over all earlier events of the block."""
+    w = workloads.small_events(seed=7, n=500, width=5, height=4, duration_us=3000,
+                               window_us=10 ** 6, c=3)
+    rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"], w["height"])
+    rng = np.random.default_rng(3)
+    Mv = 2
+    lam = rng.uniform(0.5, 4.0, size=(8, Mv)) / 1000.0
+    v = oracle.basis.event_decay_basis(w["px"], w["py"], w["t"], rp, ci, lam)
+    F = w["F"].astype(np.float64)
+    W = rng.standard_normal((8 * Mv, w["C_in"], 2))
+    Y = oracle.conv.forward(rp, ci, v, F, W)
+    z = np.zeros((w["height"], w["width"], 8, Mv, w["C_in"]))
+    last = np.zeros((w["height"], w["width"]))
+    Y_ema = np.zeros_like(Y)
+    for i in range(w["n_in"]):
+        x, y, t = int(w["px"][i]), int(w["py"][i]), float(w["t"][i])
+        for uy in (-1, 0, 1):
+            for ux in (-1, 0, 1):
+                u = int(oracle.basis.event_offset_index(ux, uy))
+                qx, qy = x - ux, y - uy
+                if u < 0 or not (0 <= qx < w["width"] and 0 <= qy < w["height"]):
+                    continue
+                for q in range(Mv):
+                    dec = np.exp(-lam[u, q] * (t - last[qy, qx]))
+                    Y_ema[i] += dec * z[qy, qx, u, q] @ W[u * Mv + q]
+        for u in range(8):
+            for q in range(Mv):
+                z[y, x, u, q] = F[i] + np.exp(-lam[u, q] * (t - last[y, x])) * z[y, x, u, q]
+        last[y, x] = t
+    np.testing.assert_allclose(Y, Y_ema, rtol=1e-11, atol=1e-11)
+
+
+def test_decay_gradient_matches_finite_differences():
+    w, rp, ci, lam = _decay_problem(2, Mv=2)
+    F = w["F"].astype(np.float64)
+    rng = np.random.default_rng(4)
+    W = rng.standard_normal((16, w["C_in"], 4))
+    dY = rng.standard_normal((w["n_out"], 4))
+
+    def loss(l):
+        v = oracle.basis.event_decay_basis(w["px"], w["py"], w["t"], rp, ci, l)
+        return float((oracle.conv.forward(rp, ci, v, F, W) * dY).sum())
+
+    vd = oracle.basis.event_decay_basis(w["px"], w["py"], w["t"], rp, ci, lam, derivative=True)
+    g = oracle.conv.decay_backward(rp, ci, vd, F, W, dY)
+    for m in [0, 5, 11, 15]:
+        u, q = divmod(m, 2)
+        h = 1e-4 * lam[u, q]
+        lp, lm = lam.copy(), lam.copy()
+        lp[u, q] += h
+        lm[u, q] -= h
+        fd = (loss(lp) - loss(lm)) / (2 * h)
+        assert np.isclose(g[m], fd, rtol=1e-6, atol=1e-9 * max(1.0, abs(fd)))

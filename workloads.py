@@ -27,6 +27,7 @@ BASIS_MONO4 = "mono4"      # {1, ux, uy, uz} x window, M = 4
 BASIS_MONO8 = "mono8"      # {1, ux, uy, uz, ux^2, uy^2, uz^2, ux*uy} x window, M = 8
 BASIS_EVENT8 = "event8"    # 3x3 pixel offsets without the centre, x exp decay, M = 8
 BASIS_WMONO10 = "wmono10"  # weighted convolution, all monomials up to 2nd order, M = 10
+BASIS_EVENT_DECAYS = "event_decays"  # 3x3 offsets without the centre x M_v decays, M = 8 M_v
 
 BASIS_M = {BASIS_MONO4: 4, BASIS_MONO8: 8, BASIS_EVENT8: 8, BASIS_WMONO10: 10}
 
@@ -202,22 +203,35 @@ def bursty_events(rng, n, width, height, duration_us, bin_us=1000, burst=8.0,
     return px, py, t, pol
 
 
+def event_decay_rates(n_decays, window_us):
+    """Decay rates lambda_uv of the learned-decay kernel, [8, n_decays]: the
+    v-th decay is 2^v / window, spread by up to 1/2 over the offsets u."""
+    u = np.arange(8)[:, None]
+    v = np.arange(n_decays)[None, :]
+    return ((2.0 ** v) * (1.0 + u / 16.0) / float(window_us)).astype(np.float32)
+
+
 def events_workload(rng, px, py, t, pol, width, height, window_us, c_in, c_out,
-                    dtype="f32", name=""):
+                    dtype="f32", name="", n_decays=1):
+    """n_decays > 1: the kernel with learned decays (M_v = n_decays per offset)."""
     n = len(t)
+    M = 8 * n_decays
     w = dict(kind="events", name=name, px=px, py=py, t=t, pol=pol, width=int(width),
              height=int(height), window=int(window_us), tau=float(window_us), half_extent=1,
-             basis=BASIS_EVENT8, M=8, C_in=c_in, C_out=c_out, n_in=n, n_out=n)
-    w.update(_features(rng, n, n, 8, c_in, c_out, dtype))
+             basis=BASIS_EVENT8 if n_decays == 1 else BASIS_EVENT_DECAYS, M=M,
+             C_in=c_in, C_out=c_out, n_in=n, n_out=n)
+    if n_decays > 1:
+        w["decays"] = event_decay_rates(n_decays, window_us)
+    w.update(_features(rng, n, n, M, c_in, c_out, dtype))
     return w
 
 
 def event_stream(seed_index=3, n=300_000, width=128, height=128, duration_us=100_000,
-                 window_us=10_000, c=32, dtype="f32"):
+                 window_us=10_000, c=32, dtype="f32", n_decays=1):
     rng = rng_for(seed_index)
     px, py, t, pol = uniform_events(rng, n, width, height, duration_us)
     return events_workload(rng, px, py, t, pol, width, height, window_us, c, c, dtype,
-                           name=f"events{n}_{width}x{height}")
+                           name=f"events{n}_{width}x{height}", n_decays=n_decays)
 
 
 def bursty_event_stream(seed_index=4, n=1_000_000, width=346, height=260,
@@ -270,6 +284,11 @@ def ellipsoids_featureless():
     return w
 
 
+def events_300k_decays2():
+    """The 300k-event stream with learned decays, M_v = 2 per offset (M = 16)."""
+    return event_stream(n_decays=2)
+
+
 WORKLOADS = {
     "sphere_1024": sphere_1024,
     "ellipsoids_inplace": ellipsoids_inplace,
@@ -278,16 +297,17 @@ WORKLOADS = {
     "events_1m_bf16": events_1m_bf16,
     "ellipsoids_weighted": ellipsoids_weighted,
     "ellipsoids_featureless": ellipsoids_featureless,
+    "events_300k_decays2": events_300k_decays2,
 }
 
 
 def small_events(seed=0, n=4000, width=20, height=16, duration_us=20_000, window_us=3000,
-                 c=8, dtype="f32"):
+                 c=8, dtype="f32", n_decays=1):
     """A small uniform stream for tests (several tiles, ragged tail)."""
     rng = rng_for(5, salt=seed + 1)
     px, py, t, pol = uniform_events(rng, n, width, height, duration_us)
     return events_workload(rng, px, py, t, pol, width, height, window_us, c, c, dtype,
-                           name=f"small_events{n}")
+                           name=f"small_events{n}", n_decays=n_decays)
 
 
 def small_points(seed=0, n_clouds=3, n=300, n_out=None, radius=0.25, k_cap=12, c_in=8,
