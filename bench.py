@@ -52,6 +52,9 @@ DESCRIPTIONS = {
     "ellipsoids_featureless": "32 clouds x 1024 points on ellipsoid surfaces, in place; r 0.1, "
                               "cap 32; featureless convolution (Eq. 9-10) with the weighted "
                               "M 10 basis; 32 output channels fp32",
+    "events_300k_decays2": "300k events, 128x128 pixels, 100 ms uniform; 3x3 block, 10 ms "
+                           "window; learned decays, 2 per offset (M 16), with their gradient; "
+                           "32 -> 32 channels fp32",
 }
 
 
@@ -319,6 +322,10 @@ def cpu_baseline(w, reps):
             oracle.conv.forward(rp, ci, v, w["F"], w["W"])
             oracle.csr_transpose(rp, ci, w["n_in"])
             oracle.conv.backward(rp, ci, v, w["F"], w["W"], w["dY"], w["n_in"])
+            if w["basis"] == "event_decays":
+                vd = oracle.basis.event_decay_basis(w["px"], w["py"], w["t"], rp, ci,
+                                                    w["decays"], derivative=True)
+                oracle.conv.decay_backward(rp, ci, vd, w["F"], w["W"], w["dY"])
         times.append(time.perf_counter() - t0)
         E = len(ci)
     med = statistics.median(times)
@@ -422,7 +429,10 @@ def main(argv=None):
             return sbc.csr_transpose_batched(csr, s_out, s_in)
     else:
         px, py, tt = T(w["px"]), T(w["py"]), T(w["t"])
-        geo = sbc.Geometry("event8", tau=w["tau"], px=px, py=py, t=tt)
+        if w["basis"] == "event_decays":
+            geo = sbc.Geometry("event_decays", px=px, py=py, t=tt, decays=T(w["decays"]))
+        else:
+            geo = sbc.Geometry("event8", tau=w["tau"], px=px, py=py, t=tt)
         cap = sbc.neighbour_search_events(px, py, tt, w["width"], w["height"], w["window"]).nnz
         found = {}
 
@@ -452,11 +462,15 @@ def main(argv=None):
 
         table = featureless_table(n_in, n_out, E, M, co)
     else:
+        decays = w["basis"] == "event_decays"
+
         def step():
             csr = search()
             Y = sbc.conv_forward(csr, F, W, geometry=geo, order=a.order)
             csc = transpose(csr)
             dF, dW = sbc.conv_backward(csr, csc, F, W, dY, geometry=geo, order=a.order)
+            if decays:  # the learned decay rates are parameters too
+                return Y, dF, dW, sbc.conv_decay_gradient(csr, F, W, dY, geo)
             return Y, dF, dW
 
         n_cus = torch.cuda.get_device_properties(dev).multi_processor_count
@@ -464,6 +478,14 @@ def main(argv=None):
         blocks_bwd = max(1, min(256, n_cus, (n_in + tr_bwd - 1) // tr_bwd))
         npix = w["width"] * w["height"] if w["kind"] == "events" else 0
         table = kernel_table(w["kind"], plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd, npix)
+        if decays:
+            G_b = 4 * n_out * M * ci
+            table["decay_basis"] = (1, 4 * (n_out + 1) + 4 * E + 12 * n_in + 4 * E * M, 0, False)
+            table["decay_spmm"] = (1, 4 * (n_out + 1) + 8 * E + 4 * E * M + n_in * ci * sf + G_b,
+                                   2 * E * M * ci, False)
+            table["decay_gemm"] = (1, G_b + n_out * co * sf + 4 * M * ci * co,
+                                   2 * n_out * M * ci * co, True)
+            table["decay_dot"] = (1, 4 * M * ci * co + M * ci * co * sf + 4 * M, 0, False)
     L = _lib.lib()
     # one (start, stop) event pair per kernel per timed step; record once so the
     # underlying HIP events exist before the library records them again

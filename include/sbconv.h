@@ -85,12 +85,19 @@ typedef enum {
  *                     Its values depend on the whole row, so the unfused
  *                     routes evaluate them in CSR order and a transpose given
  *                     to sbc_conv_backward needs its edge_perm.
+ * Event kernel with learned decays (Section 3.2, Eq. 12: g(u, dt) =
+ * sum_v exp(-lambda_uv dt) theta_uv, M_v decays per offset):
+ *   SBC_BASIS_EVENT_DECAYS  M = 8 * n_decays (1 <= n_decays <= 4):
+ *                     p_m = [u == idx(offset)] * exp(-lambda_uv * dt) with
+ *                     m = u * n_decays + v, u the SBC_BASIS_EVENT8 offset index
+ *                     and lambda = geometry.decays[u * n_decays + v] (> 0).
  */
 typedef enum {
     SBC_BASIS_MONO4 = 0,
     SBC_BASIS_MONO8 = 1,
     SBC_BASIS_EVENT8 = 2,
-    SBC_BASIS_WMONO10 = 3
+    SBC_BASIS_WMONO10 = 3,
+    SBC_BASIS_EVENT_DECAYS = 4
 } sbc_basis;
 
 /*
@@ -148,6 +155,8 @@ typedef struct {
     const int32_t *px;        /* events: [n] pixel column                       */
     const int32_t *py;        /* events: [n] pixel row                          */
     const int32_t *t;         /* events: [n] timestamps, non-decreasing         */
+    const float *decays;      /* SBC_BASIS_EVENT_DECAYS: [8, n_decays] rates    */
+    int32_t n_decays;         /* SBC_BASIS_EVENT_DECAYS: decays per offset      */
 } sbc_geometry;
 
 /* Thread-local description of the last error of this thread ("" if none). */
@@ -299,6 +308,23 @@ sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, const float
                              const void *W, const void *dY, sbc_dtype dtype, int32_t C_in,
                              int32_t C_out, float *dF, float *dW, sbc_order order,
                              void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * 5b. Gradient with respect to the decay rates of the learned-decay event
+ * kernel (Section 3.2: lambda_uv is a learned parameter):
+ *     dlambda[m] = d<Y, dY>/d lambda_m = sum_e v'[e, m] f_j W_m dy_i^T,
+ * v' = d p_m / d lambda_m = -dt p_m.  Evaluated as G' = N' F (the sparse
+ * product with v'), dW' = G'^T dY, dlambda[m] = <dW'_m, W_m> (sums in a fixed
+ * order).  geometry.basis must be SBC_BASIS_EVENT_DECAYS, M = 8 * n_decays.
+ *   F [n, C_in], W [M, C_in, C_out], dY [n, C_out]  float32 or bf16 (dtype)
+ *   dlambda [M]                                      float32 output
+ * ------------------------------------------------------------------------ */
+size_t sbc_decay_gradient_workspace_size(int32_t n, int64_t nnz_bound, int32_t M, int32_t C_in,
+                                         int32_t C_out);
+sbc_status sbc_conv_decay_gradient(const sbc_csr *csr, const sbc_geometry *geometry, int32_t M,
+                                   const void *F, const void *W, const void *dY, sbc_dtype dtype,
+                                   int32_t C_in, int32_t C_out, float *dlambda, void *workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * 6. The featureless convolution (Section 3.1, "Featureless Convolutions",

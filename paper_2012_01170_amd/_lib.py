@@ -17,6 +17,7 @@ STATUS_NAMES = {0: "SBC_OK", 1: "SBC_ERR_INVALID_ARG", 2: "SBC_ERR_CAPACITY",
                 6: "SBC_ERR_WORKSPACE", 7: "SBC_ERR_HIP", 8: "SBC_ERR_UNSUPPORTED"}
 SBC_F32, SBC_BF16 = 0, 1
 SBC_BASIS_MONO4, SBC_BASIS_MONO8, SBC_BASIS_EVENT8, SBC_BASIS_WMONO10 = 0, 1, 2, 3
+SBC_BASIS_EVENT_DECAYS = 4
 SBC_ORDER_AUTO, SBC_ORDER_SPMM_FIRST, SBC_ORDER_GEMM_FIRST = 0, 1, 2
 
 EXPORTS = [
@@ -28,7 +29,7 @@ EXPORTS = [
     "sbc_conv_workspace_size", "sbc_conv_forward", "sbc_conv_backward",
     "sbc_resolve_order", "sbc_trace_kernel", "sbc_trace_clear", "sbc_kernel_names",
     "sbc_conv_plan", "sbc_featureless_workspace_size", "sbc_featureless_forward",
-    "sbc_featureless_backward",
+    "sbc_featureless_backward", "sbc_decay_gradient_workspace_size", "sbc_conv_decay_gradient",
 ]
 
 
@@ -46,7 +47,8 @@ class SbcCsc(ctypes.Structure):
 class SbcGeometry(ctypes.Structure):
     _fields_ = [("basis", ctypes.c_int), ("radius", ctypes.c_float), ("tau", ctypes.c_float),
                 ("x_in", ctypes.c_void_p), ("x_out", ctypes.c_void_p), ("px", ctypes.c_void_p),
-                ("py", ctypes.c_void_p), ("t", ctypes.c_void_p)]
+                ("py", ctypes.c_void_p), ("t", ctypes.c_void_p), ("decays", ctypes.c_void_p),
+                ("n_decays", ctypes.c_int32)]
 
 
 class SbcConvPlan(ctypes.Structure):
@@ -84,6 +86,9 @@ _SIGS = {
                                                        _vp, _sz, _vp]),
     "sbc_basis_eval": (ctypes.c_int, [_csr_p, _geo_p, _vp, _vp]),
     "sbc_featureless_workspace_size": (_sz, [_i32, _i32, _i32]),
+    "sbc_decay_gradient_workspace_size": (_sz, [_i32, _i64, _i32, _i32, _i32]),
+    "sbc_conv_decay_gradient": (ctypes.c_int, [_csr_p, _geo_p, _i32, _vp, _vp, _vp, ctypes.c_int,
+                                               _i32, _i32, _vp, _vp, _sz, _vp]),
     "sbc_featureless_forward": (ctypes.c_int, [_csr_p, _vp, _geo_p, _i32, _vp, _i32, _vp, _vp]),
     "sbc_featureless_backward": (ctypes.c_int, [_csr_p, _vp, _geo_p, _i32, _vp, _i32, _vp, _vp,
                                                 _sz, _vp]),

@@ -15,7 +15,8 @@ const char *kKernelNames =
     "transpose_count,transpose_scatter,transpose_sort,transpose_batched,"
     "fwd_spmm,fwd_gemm,fwd_gemm_h,fwd_spmm_contract,bwd_spmm,bwd_gemm_dw,bwd_gemm_dg,"
     "bwd_spmm_t,bwd_spmm_t_expand,bwd_gemm_df,bwd_gemm_dw_t,fwd_fused,bwd_fused,bwd_dw_reduce,"
-    "featureless_fwd,featureless_rowsum,featureless_dphi";
+    "featureless_fwd,featureless_rowsum,featureless_dphi,decay_basis,decay_spmm,decay_gemm,"
+    "decay_dot";
 }  // namespace
 
 void trace_before(const char *name, hipStream_t stream) {

@@ -55,6 +55,35 @@ __global__ void __launch_bounds__(256)
     }
 }
 
+// Learned-decay event values (Eq. 12 with n_decays rates per offset), in the
+// entry order of a CSR or (kT) of its transpose: zero except the n_decays
+// entries of the edge's offset, exp(-lambda dt), or with kDeriv their
+// derivatives with respect to lambda, -dt exp(-lambda dt).
+template <bool kT, bool kDeriv>
+__global__ void __launch_bounds__(256)
+    decay_basis_kernel(int32_t n_seg, const int32_t *__restrict__ seg_ptr,
+                       const int32_t *__restrict__ idx, int64_t nnz_bound, sbc_geometry g,
+                       float *__restrict__ v) {
+    const int Mv = g.n_decays, M = 8 * Mv;
+    const int64_t E = seg_ptr[n_seg] < nnz_bound ? (int64_t)seg_ptr[n_seg] : nnz_bound;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < E;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t sg = row_of_edge(seg_ptr, n_seg, (int32_t)e);
+        const int32_t other = idx[e];
+        const int32_t i = kT ? other : sg;
+        const int32_t j = kT ? sg : other;
+        const int k = event_index(g.px[i] - g.px[j], g.py[i] - g.py[j]);
+        const float dt = (float)((int64_t)g.t[i] - (int64_t)g.t[j]);
+        for (int m = 0; m < M; ++m) v[e * M + m] = 0.f;
+        if (k >= 0) {
+            for (int q = 0; q < Mv; ++q) {
+                const float x = expf(-g.decays[k * Mv + q] * dt);
+                v[e * M + k * Mv + q] = kDeriv ? -dt * x : x;
+            }
+        }
+    }
+}
+
 // Weighted values (Eq. 11): a group of kWLanes lanes per row sums the row's
 // weights in float64 (lane partial sums in edge order, then a butterfly, so
 // the sum does not depend on scheduling) and writes every edge's ten values
@@ -102,6 +131,14 @@ sbc_status check_geometry(const sbc_geometry *g, int32_t n_rows, int32_t n_cols)
             if ((n_rows > 0 && !g->x_out) || (n_cols > 0 && !g->x_in))
                 return fail(SBC_ERR_INVALID_ARG, "x_in / x_out is null");
             return SBC_OK;
+        case SBC_BASIS_EVENT_DECAYS:
+            if (g->n_decays < 2 || g->n_decays > 4 || !g->decays)
+                return fail(SBC_ERR_INVALID_ARG, "n_decays must be 2..4 with decays non-null");
+            if (n_rows != n_cols)
+                return fail(SBC_ERR_INVALID_ARG, "event streams are in place (n_rows == n_cols)");
+            if (n_rows > 0 && (!g->px || !g->py || !g->t))
+                return fail(SBC_ERR_INVALID_ARG, "px / py / t is null");
+            return SBC_OK;
         case SBC_BASIS_EVENT8:
             if (!(g->tau > 0.f)) return fail(SBC_ERR_INVALID_ARG, "tau must be > 0");
             if (n_rows != n_cols)
@@ -130,6 +167,14 @@ sbc_status basis_launch(int32_t n_seg, const int32_t *seg_ptr, const int32_t *id
     }
     int64_t blocks = (nnz + 255) / 256;
     if (blocks > 8192) blocks = 8192;
+    if (g->basis == SBC_BASIS_EVENT_DECAYS) {
+        trace_before("basis", stream);
+        hipLaunchKernelGGL((decay_basis_kernel<kT, false>), dim3((unsigned)blocks), dim3(256), 0,
+                           stream, n_seg, seg_ptr, idx, nnz, *g, v);
+        SBC_LAUNCH_CHECK();
+        trace_after("basis", stream);
+        return SBC_OK;
+    }
     trace_before("basis", stream);
     switch (g->basis) {
         case SBC_BASIS_MONO4:
@@ -154,6 +199,19 @@ sbc_status basis_eval_launch(const sbc_csr *csr, const sbc_geometry *g, float *v
                              hipStream_t stream) {
     return basis_launch<false>(csr->n_rows, csr->row_ptr, csr->col_idx, csr->nnz_bound, g, v,
                                stream);
+}
+
+sbc_status decay_derivative_launch(const sbc_csr *csr, const sbc_geometry *g, float *v,
+                                   hipStream_t stream) {
+    if (csr->n_rows == 0 || csr->nnz_bound <= 0) return SBC_OK;
+    int64_t blocks = (csr->nnz_bound + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    trace_before("decay_basis", stream);
+    hipLaunchKernelGGL((decay_basis_kernel<false, true>), dim3((unsigned)blocks), dim3(256), 0,
+                       stream, csr->n_rows, csr->row_ptr, csr->col_idx, csr->nnz_bound, *g, v);
+    SBC_LAUNCH_CHECK();
+    trace_after("decay_basis", stream);
+    return SBC_OK;
 }
 
 sbc_status basis_eval_t_launch(const sbc_csc *csc, int64_t nnz_bound, const sbc_geometry *g,

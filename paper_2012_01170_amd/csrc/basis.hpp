@@ -66,6 +66,18 @@ __device__ __forceinline__ void weighted_mono10(float qx, float qy, float qz, fl
     v[9] = (float)(uy * uz * s);
 }
 
+// Basis size of a geometry (8 n_decays for the learned-decay event kernel).
+inline int32_t geometry_basis_size(const sbc_geometry &g) {
+    if (g.basis == SBC_BASIS_EVENT_DECAYS) return 8 * g.n_decays;
+    switch (g.basis) {
+        case SBC_BASIS_MONO4: return 4;
+        case SBC_BASIS_MONO8:
+        case SBC_BASIS_EVENT8: return 8;
+        case SBC_BASIS_WMONO10: return 10;
+        default: return 0;
+    }
+}
+
 // Event basis: index of pixel offset u = (ux, uy) in the 3x3 block, row-major
 // over (uy, ux) with the centre removed; -1 for the centre (and for offsets
 // outside the block, which no neighbourhood produces).

@@ -194,7 +194,8 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 sbc_status check_conv_args(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,
                            const void *F, const void *W, sbc_dtype dtype, int32_t Ci, int32_t Co) {
     SBC_TRY(check_csr(csr));
-    if (M != 4 && M != 8 && M != 10) return fail(SBC_ERR_UNSUPPORTED, "M must be 4, 8 or 10");
+    if (M != 4 && M != 8 && M != 10 && M != 16 && M != 24 && M != 32)
+        return fail(SBC_ERR_UNSUPPORTED, "M must be 4, 8, 10, 16, 24 or 32");
     if (Ci <= 0 || Co <= 0) return fail(SBC_ERR_INVALID_ARG, "C_in and C_out must be > 0");
     if (dtype != SBC_F32 && dtype != SBC_BF16) return fail(SBC_ERR_INVALID_ARG, "unknown dtype");
     if (!W || (csr->n_cols > 0 && !F)) return fail(SBC_ERR_INVALID_ARG, "F or W is null");
@@ -202,7 +203,7 @@ sbc_status check_conv_args(const sbc_csr *csr, const float *v, const sbc_geometr
         return fail(SBC_ERR_INVALID_ARG, "F and W must be 16-byte aligned");
     if (!v) {
         SBC_TRY(check_geometry(g, csr->n_rows, csr->n_cols));
-        if (sbc_basis_size(g->basis) != M)
+        if (geometry_basis_size(*g) != M)
             return fail(SBC_ERR_INVALID_ARG, "M does not match the geometry's basis");
     }
     return SBC_OK;
@@ -381,5 +382,100 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
             SBC_TRY(permute_w_back(ws.dwperm, M, C_in, C_out, dW, stream));
         }
     }
+    return SBC_OK;
+}
+
+// ---------------------------------------------------------------- decay rates
+namespace sbc {
+namespace {
+
+// dlambda[m] = <dW'_m, W_m> over the C_in x C_out block of m: one block per m,
+// float64 sums over a fixed thread assignment, then a fixed-order tree.
+template <typename WT>
+__global__ void __launch_bounds__(256)
+    decay_dot_kernel(const float *__restrict__ dWp, const WT *__restrict__ W, int64_t per_m,
+                     float *__restrict__ dlambda) {
+    __shared__ double s[256];
+    const int64_t base = (int64_t)blockIdx.x * per_m;
+    double acc = 0.0;
+    for (int64_t x = threadIdx.x; x < per_m; x += 256) {
+        float w;
+        if constexpr (sizeof(WT) == 2)
+            w = __uint_as_float((uint32_t)W[base + x] << 16);
+        else
+            w = W[base + x];
+        acc += (double)dWp[base + x] * (double)w;
+    }
+    s[threadIdx.x] = acc;
+    __syncthreads();
+    for (int d = 128; d >= 1; d >>= 1) {
+        if ((int)threadIdx.x < d) s[threadIdx.x] += s[threadIdx.x + d];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) dlambda[blockIdx.x] = (float)s[0];
+}
+
+struct DecayWs {
+    float *v, *G, *dWp, *partial;
+};
+
+DecayWs carve_decay(void *base, int32_t n, int64_t nnz, int32_t M, int32_t Ci, int32_t Co,
+                    size_t *bytes) {
+    Carver cv(base);
+    DecayWs w;
+    w.v = cv.take<float>((size_t)(nnz > 0 ? nnz : 0) * M);
+    w.G = cv.take<float>((size_t)n * M * Ci);
+    w.dWp = cv.take<float>((size_t)M * Ci * Co);
+    w.partial = cv.take<float>(gemm_workspace_floats(M * Ci, Co, n));
+    if (bytes) *bytes = cv.used;
+    return w;
+}
+
+}  // namespace
+}  // namespace sbc
+
+extern "C" size_t sbc_decay_gradient_workspace_size(int32_t n, int64_t nnz_bound, int32_t M,
+                                                    int32_t C_in, int32_t C_out) {
+    if (n < 0 || nnz_bound < 0 || M <= 0 || C_in <= 0 || C_out <= 0) return 0;
+    size_t bytes = 0;
+    carve_decay(nullptr, n, nnz_bound, M, C_in, C_out, &bytes);
+    return bytes;
+}
+
+extern "C" sbc_status sbc_conv_decay_gradient(const sbc_csr *csr, const sbc_geometry *geometry,
+                                              int32_t M, const void *F, const void *W,
+                                              const void *dY, sbc_dtype dtype, int32_t C_in,
+                                              int32_t C_out, float *dlambda, void *workspace,
+                                              size_t workspace_bytes, hipStream_t stream) {
+    clear_error();
+    SBC_TRY(check_conv_args(csr, nullptr, geometry, M, F, W, dtype, C_in, C_out));
+    if (geometry->basis != SBC_BASIS_EVENT_DECAYS)
+        return fail(SBC_ERR_INVALID_ARG, "the decay gradient needs SBC_BASIS_EVENT_DECAYS");
+    if (!dlambda || (csr->n_rows > 0 && !dY))
+        return fail(SBC_ERR_INVALID_ARG, "dY or dlambda is null");
+    const int32_t n = csr->n_rows;
+    size_t need = 0;
+    DecayWs ws = carve_decay(workspace, n, csr->nnz_bound, M, C_in, C_out, &need);
+    if (!workspace || workspace_bytes < need)
+        return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_decay_gradient_workspace_size()");
+    const bool bf = dtype == SBC_BF16;
+    if (n == 0) return fill_i32(reinterpret_cast<int32_t *>(dlambda), 0, M, stream);
+    // v' = d p / d lambda, G' = N' F, dW' = G'^T dY, dlambda = <dW', W> per m
+    SBC_TRY(decay_derivative_launch(csr, geometry, ws.v, stream));
+    SBC_TRY(spmm(n, csr->row_ptr, csr->col_idx, nullptr, ws.v, M, F, bf, C_in, false, ws.G,
+                 stream, "decay_spmm"));
+    const int64_t K1 = (int64_t)M * C_in;
+    SBC_TRY(gemm(ws.G, false, 1, K1, dY, bf, C_out, 1, ws.dWp, C_out, 1, (int32_t)K1, C_out, n,
+                 ws.partial, stream, "decay_gemm"));
+    trace_before("decay_dot", stream);
+    const int64_t per_m = (int64_t)C_in * C_out;
+    if (bf)
+        hipLaunchKernelGGL(decay_dot_kernel<uint16_t>, dim3(M), dim3(256), 0, stream, ws.dWp,
+                           static_cast<const uint16_t *>(W), per_m, dlambda);
+    else
+        hipLaunchKernelGGL(decay_dot_kernel<float>, dim3(M), dim3(256), 0, stream, ws.dWp,
+                           static_cast<const float *>(W), per_m, dlambda);
+    SBC_LAUNCH_CHECK();
+    trace_after("decay_dot", stream);
     return SBC_OK;
 }

@@ -137,6 +137,8 @@ sbc_status check_featureless(const sbc_csr *csr, const float *v, const sbc_geome
     if (P <= 0) return fail(SBC_ERR_INVALID_ARG, "P must be > 0");
     if (!v) {
         SBC_TRY(check_geometry(g, csr->n_rows, csr->n_cols));
+        if (g->basis == SBC_BASIS_EVENT_DECAYS)
+            return fail(SBC_ERR_UNSUPPORTED, "the learned-decay basis needs v here");
         if (sbc_basis_size(g->basis) != M)
             return fail(SBC_ERR_INVALID_ARG, "M does not match the geometry's basis");
     }

@@ -86,12 +86,18 @@ sbc_status spmm(int32_t n_rows, const int32_t *ptr, const int32_t *idx, const in
                 const float *v, int32_t M, const void *X, bool x_bf16, int32_t C, bool contract,
                 float *out, hipStream_t stream, const char *trace) {
     if (n_rows <= 0 || C <= 0) return SBC_OK;
-    if (M != 4 && M != 8 && M != 10) return fail(SBC_ERR_UNSUPPORTED, "M must be 4, 8 or 10");
+    if (M != 4 && M != 8 && M != 10 && M != 16 && M != 24 && M != 32)
+        return fail(SBC_ERR_UNSUPPORTED, "M must be 4, 8, 10, 16, 24 or 32");
     trace_before(trace, stream);
-    sbc_status st =
-        M == 4 ? launch_m<4>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream)
-        : M == 8 ? launch_m<8>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream)
-                 : launch_m<10>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream);
+    sbc_status st;
+    switch (M) {
+        case 4: st = launch_m<4>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
+        case 8: st = launch_m<8>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
+        case 10: st = launch_m<10>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
+        case 16: st = launch_m<16>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
+        case 24: st = launch_m<24>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
+        default: st = launch_m<32>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
+    }
     trace_after(trace, stream);
     return st;
 }

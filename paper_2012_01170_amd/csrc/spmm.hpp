@@ -21,6 +21,9 @@ sbc_status check_csr(const sbc_csr *csr);
 sbc_status check_geometry(const sbc_geometry *g, int32_t n_rows, int32_t n_cols);
 sbc_status basis_eval_launch(const sbc_csr *csr, const sbc_geometry *g, float *v,
                              hipStream_t stream);
+// the learned-decay basis's derivatives with respect to the rates (CSR order)
+sbc_status decay_derivative_launch(const sbc_csr *csr, const sbc_geometry *g, float *v,
+                                   hipStream_t stream);
 // the same values for the entries of the transpose, in its entry order
 sbc_status basis_eval_t_launch(const sbc_csc *csc, int64_t nnz_bound, const sbc_geometry *g,
                                float *v, hipStream_t stream);

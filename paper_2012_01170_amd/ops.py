@@ -18,7 +18,7 @@ from . import _lib as L
 ORDERS = {"auto": L.SBC_ORDER_AUTO, "spmm_first": L.SBC_ORDER_SPMM_FIRST,
           "gemm_first": L.SBC_ORDER_GEMM_FIRST}
 BASES = {"mono4": L.SBC_BASIS_MONO4, "mono8": L.SBC_BASIS_MONO8, "event8": L.SBC_BASIS_EVENT8,
-         "wmono10": L.SBC_BASIS_WMONO10}
+         "wmono10": L.SBC_BASIS_WMONO10, "event_decays": L.SBC_BASIS_EVENT_DECAYS}
 BASIS_M = {"mono4": 4, "mono8": 8, "event8": 8, "wmono10": 10}
 
 
@@ -86,7 +86,8 @@ class CSC:
 
 @dataclass
 class Geometry:
-    """Coordinates the basis is evaluated from (points: x_in/x_out/radius; events: px/py/t/tau)."""
+    """Coordinates the basis is evaluated from (points: x_in/x_out/radius; events:
+    px/py/t and tau, or for "event_decays" the rates `decays` [8, n_decays])."""
     basis: str
     radius: float = 0.0
     tau: float = 0.0
@@ -95,15 +96,21 @@ class Geometry:
     px: Optional[torch.Tensor] = None
     py: Optional[torch.Tensor] = None
     t: Optional[torch.Tensor] = None
+    decays: Optional[torch.Tensor] = None
 
     @property
     def M(self) -> int:
+        if self.basis == "event_decays":
+            return 8 * int(self.decays.shape[1])
         return BASIS_M[self.basis]
 
     def c_struct(self) -> L.SbcGeometry:
         d = lambda x: x.data_ptr() if x is not None else 0
+        nd = int(self.decays.shape[1]) if self.decays is not None else 0
+        if self.decays is not None:
+            _require(self.decays, "decays", torch.float32, 2)
         return L.SbcGeometry(BASES[self.basis], float(self.radius), float(self.tau), d(self.x_in),
-                             d(self.x_out), d(self.px), d(self.py), d(self.t))
+                             d(self.x_out), d(self.px), d(self.py), d(self.t), d(self.decays), nd)
 
 
 def neighbour_search_points(x_in, in_splits, x_out, out_splits, radius: float, k_cap: int,
@@ -357,6 +364,22 @@ def featureless_backward(csr: CSR, dZ, M: int, geometry: Optional[Geometry] = No
         ctypes.byref(c), _p(v), ctypes.byref(g) if g is not None else None, M, _p(dZ), P,
         _p(dPhi), ws.ptr, ws.nbytes, _stream(dev)))
     return dPhi
+
+
+def conv_decay_gradient(csr: CSR, F, W, dY, geometry: Geometry) -> torch.Tensor:
+    """d<Y, dY>/d lambda [M] float32 for the learned-decay event kernel
+    (sbc_conv_decay_gradient)."""
+    dev, M, C_in, C_out = _conv_common(csr, F, W, None, geometry)
+    _require(dY, "dY", F.dtype, 2, dev)
+    dt = _dtype_code(F)
+    dl = torch.empty(M, dtype=torch.float32, device=dev)
+    lib = L.lib()
+    ws = _Workspace(lib.sbc_decay_gradient_workspace_size(csr.n_rows, csr.nnz, M, C_in, C_out),
+                    dev)
+    c, g = csr.c_struct(), geometry.c_struct()
+    L.check(lib.sbc_conv_decay_gradient(ctypes.byref(c), ctypes.byref(g), M, _p(F), _p(W), _p(dY),
+                                        dt, C_in, C_out, _p(dl), ws.ptr, ws.nbytes, _stream(dev)))
+    return dl
 
 
 def conv_plan(n_out, n_in, nnz, M, C_in, C_out, dtype=torch.float32, order="auto") -> dict:

@@ -28,6 +28,9 @@ def dev_features(w, name):
 def geometry(w, t: dict) -> sbc.Geometry:
     if w["kind"] == "points":
         return sbc.Geometry(w["basis"], radius=w["radius"], x_in=t["x_in"], x_out=t["x_out"])
+    if w["basis"] == "event_decays":
+        return sbc.Geometry("event_decays", px=t["px"], py=t["py"], t=t["t"],
+                            decays=dev(w["decays"]))
     return sbc.Geometry("event8", tau=w["tau"], px=t["px"], py=t["py"], t=t["t"])
 
 

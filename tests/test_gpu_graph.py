@@ -15,27 +15,49 @@ from tests import gpu_common as G
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("name", ["points", "events"])
+@pytest.mark.parametrize("name", ["points", "events", "points_batched", "events_csc",
+                                  "weighted", "featureless"])
 def test_graph_replays_match_eager(name):
-    if name == "points":
+    """Each variant is one of the step forms the benchmark times: the general
+    transpose, the block-diagonal transpose, the transpose from the reverse
+    event search, the weighted basis (materialised inside the forward), and
+    the featureless convolution."""
+    print(f"[graph] {name}", flush=True)
+    if name.startswith("points"):
         w = workloads.small_points(seed=11, c_in=64, c_out=64)
+    elif name == "weighted":
+        w = workloads.small_points(seed=18, c_in=64, c_out=64, basis=workloads.BASIS_WMONO10)
+    elif name == "featureless":
+        w = workloads.small_points(seed=19, c_in=1, c_out=32, basis=workloads.BASIS_WMONO10)
     else:
         w = workloads.small_events(seed=12, c=32)
     t = G.to_device(w)
     geo = G.geometry(w, t)
     cap = G.search(w, t).nnz       # a capacity for the unsynchronised search
+    Phi = t["W"][:, 0, :].contiguous()
 
     def step():
+        csc = None
         if w["kind"] == "points":
             csr = G.sbc.neighbour_search_points(t["x_in"], t["in_splits"], t["x_out"],
                                                 t["out_splits"], w["radius"], w["k_cap"],
                                                 sync=False)
+        elif name == "events_csc":
+            csr, csc = G.sbc.neighbour_search_events_csc(t["px"], t["py"], t["t"], w["width"],
+                                                         w["height"], w["window"],
+                                                         col_capacity=cap, sync=False)
         else:
             csr = G.sbc.neighbour_search_events(t["px"], t["py"], t["t"], w["width"],
                                                 w["height"], w["window"], col_capacity=cap,
                                                 sync=False)
+        if name == "featureless":
+            Z = G.sbc.featureless_forward(csr, Phi, geometry=geo)
+            dPhi = G.sbc.featureless_backward(csr, t["dY"], w["M"], geometry=geo)
+            return csr.row_ptr, Z, dPhi
         Y = G.sbc.conv_forward(csr, t["F"], t["W"], geometry=geo)
-        csc = G.sbc.csr_transpose(csr)
+        if csc is None:
+            csc = (G.sbc.csr_transpose_batched(csr, t["out_splits"], t["in_splits"])
+                   if name == "points_batched" else G.sbc.csr_transpose(csr))
         dF, dW = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"], geometry=geo)
         return csr.row_ptr, Y, dF, dW
 

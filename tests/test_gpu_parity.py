@@ -53,6 +53,10 @@ SMALL = {
                                                         c_in=32, c_out=32, dtype="bf16"),
     "fz_pts_weighted64": lambda: workloads.small_points(seed=17, basis=workloads.BASIS_WMONO10,
                                                         c_in=64, c_out=64),
+    # the event kernel with learned decays (M_v = 2, 3, 4 per offset; unfused routes)
+    "ev_decays2": lambda: workloads.small_events(seed=20, c=8, n_decays=2),
+    "ev_decays3_odd": lambda: workloads.small_events(seed=22, n=3001, c=13, n_decays=3),
+    "ev_decays4_bf16": lambda: workloads.small_events(seed=21, c=16, n_decays=4, dtype="bf16"),
 }
 # the general convolution's full-size cases; the featureless first layer
 # (one input channel of features ~N(0,1), so single-channel input gradients
@@ -616,3 +620,21 @@ def test_upsampling(order):
     dF_ref, dW_ref = oracle.conv.backward(rp, ci, v, w["F"], w["W"], w["dY"], w["n_in"])
     assert G.row_error(dF.cpu().numpy(), dF_ref) < G.TOL_F32
     assert G.norm_error(dW.cpu().numpy(), dW_ref) < G.TOL_F32
+
+
+# ---------------------------------------------------------------- learned decay rates
+@pytest.mark.parametrize("name", ["ev_decays2", "ev_decays3_odd", "ev_decays4_bf16",
+                                  "events_300k_decays2"])
+def test_decay_gradient(name):
+    """d<Y, dY>/d lambda of the learned-decay kernel (Eq. 12) against the oracle's
+    per-edge chain rule."""
+    print(f"[decay gradient] {name}", flush=True)
+    w, rp, ci, v = case(name)
+    t, csr = gpu_case(name)
+    dl = G.sbc.conv_decay_gradient(csr, t["F"], t["W"], t["dY"], G.geometry(w, t)).cpu().numpy()
+    vd = oracle.basis.event_decay_basis(w["px"], w["py"], w["t"], rp, ci, w["decays"],
+                                        derivative=True)
+    ref = oracle.conv.decay_backward(rp, ci, vd, w["F"], w["W"], w["dY"])
+    err = G.norm_error(dl, ref)
+    print(f"    dlambda error {err:.3e}", flush=True)
+    assert err < tol(w)
