@@ -470,7 +470,7 @@ def main(argv=None):
             csc = transpose(csr)
             dF, dW = sbc.conv_backward(csr, csc, F, W, dY, geometry=geo, order=a.order)
             if decays:  # the learned decay rates are parameters too
-                return Y, dF, dW, sbc.conv_decay_gradient(csr, F, W, dY, geo)
+                return Y, dF, dW, sbc.conv_decay_gradient(csr, F, W, dY, geo, csc=csc)
             return Y, dF, dW
 
         n_cus = torch.cuda.get_device_properties(dev).multi_processor_count
@@ -479,12 +479,20 @@ def main(argv=None):
         npix = w["width"] * w["height"] if w["kind"] == "events" else 0
         table = kernel_table(w["kind"], plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd, npix)
         if decays:
-            G_b = 4 * n_out * M * ci
-            table["decay_basis"] = (1, 4 * (n_out + 1) + 4 * E + 12 * n_in + 4 * E * M, 0, False)
-            table["decay_spmm"] = (1, 4 * (n_out + 1) + 8 * E + 4 * E * M + n_in * ci * sf + G_b,
-                                   2 * E * M * ci, False)
-            table["decay_gemm"] = (1, G_b + n_out * co * sf + 4 * M * ci * co,
-                                   2 * n_out * M * ci * co, True)
+            if plan["backward_fused"]:
+                # the fused D-route with the derivative values, dF skipped
+                part = 4 * blocks_bwd * ci * M * co
+                table["decay_fused"] = (1, 4 * (n_in + 1) + 4 * E + 12 * n_in + n_out * co * sf
+                                        + n_in * ci * sf + part, 2 * n_in * M * ci * co, True)
+                table["decay_dw_reduce"] = (1, part + 4 * M * ci * co, 0, False)
+            else:
+                G_b = 4 * n_out * M * ci
+                table["decay_basis"] = (1, 4 * (n_out + 1) + 4 * E + 12 * n_in + 4 * E * M, 0,
+                                        False)
+                table["decay_spmm"] = (1, 4 * (n_out + 1) + 8 * E + 4 * E * M + n_in * ci * sf
+                                       + G_b, 2 * E * M * ci, False)
+                table["decay_gemm"] = (1, G_b + n_out * co * sf + 4 * M * ci * co,
+                                       2 * n_out * M * ci * co, True)
             table["decay_dot"] = (1, 4 * M * ci * co + M * ci * co * sf + 4 * M, 0, False)
     L = _lib.lib()
     # one (start, stop) event pair per kernel per timed step; record once so the

@@ -313,17 +313,21 @@ sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, const float
  * 5b. Gradient with respect to the decay rates of the learned-decay event
  * kernel (Section 3.2: lambda_uv is a learned parameter):
  *     dlambda[m] = d<Y, dY>/d lambda_m = sum_e v'[e, m] f_j W_m dy_i^T,
- * v' = d p_m / d lambda_m = -dt p_m.  Evaluated as G' = N' F (the sparse
- * product with v'), dW' = G'^T dY, dlambda[m] = <dW'_m, W_m> (sums in a fixed
- * order).  geometry.basis must be SBC_BASIS_EVENT_DECAYS, M = 8 * n_decays.
+ * v' = d p_m / d lambda_m = -dt p_m.  dW' = sum_e v'[e, :] f_j^T dy_i is
+ * formed like dW of the backward: with the transpose (csc non-NULL, its
+ * edge_perm may be NULL) by the fused D-route where the shape has one, else
+ * as G' = N' F (the sparse product with v') and dW' = G'^T dY; then
+ * dlambda[m] = <dW'_m, W_m>.  Sums are taken in a fixed order.
+ * geometry.basis must be SBC_BASIS_EVENT_DECAYS, M = 8 * n_decays.
  *   F [n, C_in], W [M, C_in, C_out], dY [n, C_out]  float32 or bf16 (dtype)
  *   dlambda [M]                                      float32 output
  * ------------------------------------------------------------------------ */
 size_t sbc_decay_gradient_workspace_size(int32_t n, int64_t nnz_bound, int32_t M, int32_t C_in,
-                                         int32_t C_out);
-sbc_status sbc_conv_decay_gradient(const sbc_csr *csr, const sbc_geometry *geometry, int32_t M,
-                                   const void *F, const void *W, const void *dY, sbc_dtype dtype,
-                                   int32_t C_in, int32_t C_out, float *dlambda, void *workspace,
+                                         int32_t C_out, sbc_dtype dtype);
+sbc_status sbc_conv_decay_gradient(const sbc_csr *csr, const sbc_csc *csc,
+                                   const sbc_geometry *geometry, int32_t M, const void *F,
+                                   const void *W, const void *dY, sbc_dtype dtype, int32_t C_in,
+                                   int32_t C_out, float *dlambda, void *workspace,
                                    size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------

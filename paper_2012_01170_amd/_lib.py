@@ -86,9 +86,9 @@ _SIGS = {
                                                        _vp, _sz, _vp]),
     "sbc_basis_eval": (ctypes.c_int, [_csr_p, _geo_p, _vp, _vp]),
     "sbc_featureless_workspace_size": (_sz, [_i32, _i32, _i32]),
-    "sbc_decay_gradient_workspace_size": (_sz, [_i32, _i64, _i32, _i32, _i32]),
-    "sbc_conv_decay_gradient": (ctypes.c_int, [_csr_p, _geo_p, _i32, _vp, _vp, _vp, ctypes.c_int,
-                                               _i32, _i32, _vp, _vp, _sz, _vp]),
+    "sbc_decay_gradient_workspace_size": (_sz, [_i32, _i64, _i32, _i32, _i32, ctypes.c_int]),
+    "sbc_conv_decay_gradient": (ctypes.c_int, [_csr_p, _csc_p, _geo_p, _i32, _vp, _vp, _vp,
+                                               ctypes.c_int, _i32, _i32, _vp, _vp, _sz, _vp]),
     "sbc_featureless_forward": (ctypes.c_int, [_csr_p, _vp, _geo_p, _i32, _vp, _i32, _vp, _vp]),
     "sbc_featureless_backward": (ctypes.c_int, [_csr_p, _vp, _geo_p, _i32, _vp, _i32, _vp, _vp,
                                                 _sz, _vp]),

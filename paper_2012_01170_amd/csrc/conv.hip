@@ -435,17 +435,23 @@ DecayWs carve_decay(void *base, int32_t n, int64_t nnz, int32_t M, int32_t Ci, i
 }  // namespace sbc
 
 extern "C" size_t sbc_decay_gradient_workspace_size(int32_t n, int64_t nnz_bound, int32_t M,
-                                                    int32_t C_in, int32_t C_out) {
+                                                    int32_t C_in, int32_t C_out,
+                                                    sbc_dtype dtype) {
     if (n < 0 || nnz_bound < 0 || M <= 0 || C_in <= 0 || C_out <= 0) return 0;
     size_t bytes = 0;
     carve_decay(nullptr, n, nnz_bound, M, C_in, C_out, &bytes);
-    return bytes;
+    // the fused D-route: its own workspace, then dW'
+    const size_t fused = fused_workspace_bytes(M, C_in, C_out, n, nnz_bound) +
+                         align_up((size_t)M * C_in * C_out * 4);
+    return fused_backward_available(M, C_in, C_out, dtype == SBC_BF16) && fused > bytes ? fused
+                                                                                        : bytes;
 }
 
-extern "C" sbc_status sbc_conv_decay_gradient(const sbc_csr *csr, const sbc_geometry *geometry,
-                                              int32_t M, const void *F, const void *W,
-                                              const void *dY, sbc_dtype dtype, int32_t C_in,
-                                              int32_t C_out, float *dlambda, void *workspace,
+extern "C" sbc_status sbc_conv_decay_gradient(const sbc_csr *csr, const sbc_csc *csc,
+                                              const sbc_geometry *geometry, int32_t M,
+                                              const void *F, const void *W, const void *dY,
+                                              sbc_dtype dtype, int32_t C_in, int32_t C_out,
+                                              float *dlambda, void *workspace,
                                               size_t workspace_bytes, hipStream_t stream) {
     clear_error();
     SBC_TRY(check_conv_args(csr, nullptr, geometry, M, F, W, dtype, C_in, C_out));
@@ -453,27 +459,41 @@ extern "C" sbc_status sbc_conv_decay_gradient(const sbc_csr *csr, const sbc_geom
         return fail(SBC_ERR_INVALID_ARG, "the decay gradient needs SBC_BASIS_EVENT_DECAYS");
     if (!dlambda || (csr->n_rows > 0 && !dY))
         return fail(SBC_ERR_INVALID_ARG, "dY or dlambda is null");
+    if (csc && (!csc->col_ptr || csc->n_cols != csr->n_cols ||
+                (csr->nnz_bound > 0 && !csc->row_idx)))
+        return fail(SBC_ERR_INVALID_ARG, "csc does not match csr");
     const int32_t n = csr->n_rows;
-    size_t need = 0;
-    DecayWs ws = carve_decay(workspace, n, csr->nnz_bound, M, C_in, C_out, &need);
+    const bool bf = dtype == SBC_BF16;
+    const size_t need = sbc_decay_gradient_workspace_size(n, csr->nnz_bound, M, C_in, C_out, dtype);
     if (!workspace || workspace_bytes < need)
         return fail(SBC_ERR_WORKSPACE, "workspace smaller than sbc_decay_gradient_workspace_size()");
-    const bool bf = dtype == SBC_BF16;
     if (n == 0) return fill_i32(reinterpret_cast<int32_t *>(dlambda), 0, M, stream);
-    // v' = d p / d lambda, G' = N' F, dW' = G'^T dY, dlambda = <dW', W> per m
-    SBC_TRY(decay_derivative_launch(csr, geometry, ws.v, stream));
-    SBC_TRY(spmm(n, csr->row_ptr, csr->col_idx, nullptr, ws.v, M, F, bf, C_in, false, ws.G,
-                 stream, "decay_spmm"));
-    const int64_t K1 = (int64_t)M * C_in;
-    SBC_TRY(gemm(ws.G, false, 1, K1, dY, bf, C_out, 1, ws.dWp, C_out, 1, (int32_t)K1, C_out, n,
-                 ws.partial, stream, "decay_gemm"));
+    float *dWp;
+    if (csc && fused_backward_available(M, C_in, C_out, bf)) {
+        // D' = N'^T dY gathered with the derivative values, dW' = F^T D' (dF skipped)
+        const int32_t np = n > csr->n_cols ? n : csr->n_cols;
+        dWp = reinterpret_cast<float *>(static_cast<char *>(workspace) +
+                                        fused_workspace_bytes(M, C_in, C_out, np, csr->nnz_bound));
+        SBC_TRY(fused_backward(csr, csc, nullptr, geometry, M, F, W, dY, bf, C_in, C_out, nullptr,
+                               dWp, workspace, stream, true));
+    } else {
+        // v' = d p / d lambda, G' = N' F, dW' = G'^T dY
+        DecayWs ws = carve_decay(workspace, n, csr->nnz_bound, M, C_in, C_out, nullptr);
+        SBC_TRY(decay_derivative_launch(csr, geometry, ws.v, stream));
+        SBC_TRY(spmm(n, csr->row_ptr, csr->col_idx, nullptr, ws.v, M, F, bf, C_in, false, ws.G,
+                     stream, "decay_spmm"));
+        const int64_t K1 = (int64_t)M * C_in;
+        SBC_TRY(gemm(ws.G, false, 1, K1, dY, bf, C_out, 1, ws.dWp, C_out, 1, (int32_t)K1, C_out,
+                     n, ws.partial, stream, "decay_gemm"));
+        dWp = ws.dWp;
+    }
     trace_before("decay_dot", stream);
     const int64_t per_m = (int64_t)C_in * C_out;
     if (bf)
-        hipLaunchKernelGGL(decay_dot_kernel<uint16_t>, dim3(M), dim3(256), 0, stream, ws.dWp,
+        hipLaunchKernelGGL(decay_dot_kernel<uint16_t>, dim3(M), dim3(256), 0, stream, dWp,
                            static_cast<const uint16_t *>(W), per_m, dlambda);
     else
-        hipLaunchKernelGGL(decay_dot_kernel<float>, dim3(M), dim3(256), 0, stream, ws.dWp,
+        hipLaunchKernelGGL(decay_dot_kernel<float>, dim3(M), dim3(256), 0, stream, dWp,
                            static_cast<const float *>(W), per_m, dlambda);
     SBC_LAUNCH_CHECK();
     trace_after("decay_dot", stream);

@@ -78,7 +78,12 @@ struct KGeo {
     float inv_tau;
     const float *x_in, *x_out;
     const int4 *ev;
+    const float *decays;  // learned-decay rates [8, M / 8]
 };
+
+// Basis mode of the fused kernels for the derivatives of the learned-decay
+// basis with respect to its rates (the decay gradient's D-route pass).
+constexpr int kDecayDerivMode = 16;
 
 __global__ void pack_events_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
                                    const int32_t *__restrict__ t, int32_t n,
@@ -88,8 +93,10 @@ __global__ void pack_events_kernel(const int32_t *__restrict__ px, const int32_t
 }
 
 // ---------------------------------------------------------------- basis per edge
-// kBasis: 0 = read v[ev, :], SBC_BASIS_MONO4 + 1, SBC_BASIS_MONO8 + 1, SBC_BASIS_EVENT8 + 1
-// (i = output index, j = input index of the edge, ev = its CSR position).
+// kBasis: 0 = read v[ev, :], SBC_BASIS_MONO4 + 1, SBC_BASIS_MONO8 + 1, SBC_BASIS_EVENT8 + 1,
+// SBC_BASIS_EVENT_DECAYS + 1 (M / 8 rates per offset), kDecayDerivMode (their
+// derivatives with respect to the rates) (i = output index, j = input index
+// of the edge, ev = its CSR position).
 template <int M, int kBasis>
 __device__ __forceinline__ void edge_basis(const KGeo &g, const float *__restrict__ v,
                                            int32_t i, int32_t j, int64_t ev, double inv_r,
@@ -103,6 +110,20 @@ __device__ __forceinline__ void edge_basis(const KGeo &g, const float *__restric
         const float d = event_decay(a.z, b.z, inv_tau);
 #pragma unroll
         for (int m = 0; m < M; ++m) out[m] = (m == k) ? d : 0.f;
+    } else if constexpr (kBasis == SBC_BASIS_EVENT_DECAYS + 1 || kBasis == kDecayDerivMode) {
+        // the same expression as the basis values kernel, so the values agree bitwise
+        constexpr int Mv = M / 8;
+        const int4 a = g.ev[i], b = g.ev[j];
+        const int k = event_index(a.x - b.x, a.y - b.y);
+        const float dt = (float)((int64_t)a.z - (int64_t)b.z);
+        float x[Mv];
+#pragma unroll
+        for (int q = 0; q < Mv; ++q) {
+            x[q] = k >= 0 ? expf(-g.decays[k * Mv + q] * dt) : 0.f;
+            if (kBasis == kDecayDerivMode) x[q] = -dt * x[q];
+        }
+#pragma unroll
+        for (int m = 0; m < M; ++m) out[m] = (m / Mv == k) ? x[m % Mv] : 0.f;
     } else {
         point_basis<M>(g.x_out[3 * (int64_t)i], g.x_out[3 * (int64_t)i + 1],
                        g.x_out[3 * (int64_t)i + 2], g.x_in[3 * (int64_t)j],
@@ -899,7 +920,8 @@ struct WsCfg {
 
 template <int M, int CI, int CO, bool kBf>
 constexpr WsCfg ws_cfg() {
-    if (!kBf && CI <= 32 && CO <= 32) return WsCfg{8, 4, 32, kWRegs};
+    if (!kBf && CI <= 32 && CO <= 32)  // wider D rows (M*CO > 256) leave LDS for 4 gather waves
+        return M * CO <= 256 ? WsCfg{8, 4, 32, kWRegs} : WsCfg{4, 4, 32, kWGlobal};
     // 16 columns of Wt per matrix wave (one dF column block), K2 = M*CO rows
     return WsCfg{4, 4, 32, (kBf ? M * CO <= 512 : M * CO <= 256) ? kWRegs : kWGlobal};
 }
@@ -1271,6 +1293,10 @@ FwdFn fwd_for(int basis_mode) {
         case SBC_BASIS_EVENT8 + 1:
             if constexpr (M == 8) return fwd_fused_kernel<M, CI, CO, SBC_BASIS_EVENT8 + 1, kBf>;
             return nullptr;
+        case SBC_BASIS_EVENT_DECAYS + 1:
+            if constexpr (M >= 16 && M % 8 == 0)
+                return fwd_fused_kernel<M, CI, CO, SBC_BASIS_EVENT_DECAYS + 1, kBf>;
+            return nullptr;
     }
     return nullptr;
 }
@@ -1291,6 +1317,10 @@ RegFn reg_for(int basis_mode) {
             case SBC_BASIS_EVENT8 + 1:
                 if constexpr (M == 8) return fwd_reg_kernel<M, CI, CO, SBC_BASIS_EVENT8 + 1, kBf>;
                 return nullptr;
+            case SBC_BASIS_EVENT_DECAYS + 1:
+                if constexpr (M >= 16 && M % 8 == 0)
+                    return fwd_reg_kernel<M, CI, CO, SBC_BASIS_EVENT_DECAYS + 1, kBf>;
+                return nullptr;
         }
         return nullptr;
     }
@@ -1309,6 +1339,14 @@ BwdFn bwd_for(int basis_mode) {
         case SBC_BASIS_EVENT8 + 1:
             if constexpr (M == 8) return bwd_ws_kernel<M, CI, CO, SBC_BASIS_EVENT8 + 1, kBf>;
             return nullptr;
+        case SBC_BASIS_EVENT_DECAYS + 1:
+            if constexpr (M >= 16 && M % 8 == 0)
+                return bwd_ws_kernel<M, CI, CO, SBC_BASIS_EVENT_DECAYS + 1, kBf>;
+            return nullptr;
+        case kDecayDerivMode:
+            if constexpr (M >= 16 && M % 8 == 0)
+                return bwd_ws_kernel<M, CI, CO, kDecayDerivMode, kBf>;
+            return nullptr;
     }
     return nullptr;
 }
@@ -1317,6 +1355,7 @@ BwdFn bwd_for(int basis_mode) {
 // C_in x M*C_out partial of dW per block in registers, so its list is limited
 // to C_in * M * C_out <= 32768.
 #define SBC_FWD_SHAPES(X) \
+    X(16, 32, 32, false)  \
     X(10, 64, 64, false)  \
     X(4, 16, 32, false)   \
     X(8, 64, 64, false)   \
@@ -1325,6 +1364,7 @@ BwdFn bwd_for(int basis_mode) {
     X(8, 64, 64, true)    \
     X(8, 32, 32, true)
 #define SBC_BWD_SHAPES(X) \
+    X(16, 32, 32, false)  \
     X(4, 16, 32, false)   \
     X(8, 64, 64, false)   \
     X(8, 32, 32, false)   \
@@ -1426,7 +1466,8 @@ sbc_status make_kgeo(const sbc_csr *csr, const float *v, const sbc_geometry *g, 
     kg->inv_tau = 1.0f / g->tau;
     kg->x_in = g->x_in;
     kg->x_out = g->x_out;
-    if (g->basis == SBC_BASIS_EVENT8) {
+    kg->decays = g->decays;
+    if (g->basis == SBC_BASIS_EVENT8 || g->basis == SBC_BASIS_EVENT_DECAYS) {
         // event streams are in place: rows and columns index the same events
         const int32_t n = csr->n_cols > csr->n_rows ? csr->n_cols : csr->n_rows;
         int4 *pk = reinterpret_cast<int4 *>(static_cast<char *>(ws) +
@@ -1494,8 +1535,8 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
 sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v,
                           const sbc_geometry *g, int32_t M, const void *F, const void *W,
                           const void *dY, bool bf, int32_t CI, int32_t CO, float *dF, float *dW,
-                          void *ws, hipStream_t stream) {
-    BwdFn fn = find_bwd(Shape{M, CI, CO, bf}, basis_mode_of(v, g));
+                          void *ws, hipStream_t stream, bool decay_derivative) {
+    BwdFn fn = find_bwd(Shape{M, CI, CO, bf}, decay_derivative ? kDecayDerivMode : basis_mode_of(v, g));
     if (!fn) return fail(SBC_ERR_UNSUPPORTED, "no fused backward for this shape");
     const int32_t n_in = csr->n_cols;
     char *base = static_cast<char *>(ws);
@@ -1512,21 +1553,21 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
     KGeo gg;
     SBC_TRY(make_kgeo(csr, v, g, M, CI, CO, ws, stream, &gg));
     if (n_in > 0 && (dF || dW)) {
-        trace_before("bwd_fused", stream);
+        trace_before(decay_derivative ? "decay_fused" : "bwd_fused", stream);
         hipLaunchKernelGGL(fn, dim3(blocks), dim3(nw * 64), 0, stream, n_in, n_tiles, csc->col_ptr,
                            csc->row_idx, csc->edge_perm, v, gg, F, dY, W, dF,
                            dW ? part : nullptr);
         SBC_LAUNCH_CHECK();
-        trace_after("bwd_fused", stream);
+        trace_after(decay_derivative ? "decay_fused" : "bwd_fused", stream);
     }
     if (!dW) return SBC_OK;
     const int64_t total = (int64_t)M * CI * CO;
     const int64_t rb = (total + kReducePos - 1) / kReducePos;
-    trace_before("bwd_dw_reduce", stream);
+    trace_before(decay_derivative ? "decay_dw_reduce" : "bwd_dw_reduce", stream);
     hipLaunchKernelGGL(dw_reduce_kernel, dim3((unsigned)rb), dim3(256), 0, stream, part,
                        n_in > 0 ? blocks : 0, M, CI, CO, dW);
     SBC_LAUNCH_CHECK();
-    trace_after("bwd_dw_reduce", stream);
+    trace_after(decay_derivative ? "decay_dw_reduce" : "bwd_dw_reduce", stream);
     return SBC_OK;
 }
 

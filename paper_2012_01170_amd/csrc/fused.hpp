@@ -26,6 +26,6 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
 sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v,
                           const sbc_geometry *g, int32_t M, const void *F, const void *W,
                           const void *dY, bool bf, int32_t CI, int32_t CO, float *dF, float *dW,
-                          void *ws, hipStream_t stream);
+                          void *ws, hipStream_t stream, bool decay_derivative = false);
 
 }  // namespace sbc

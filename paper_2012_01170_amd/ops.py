@@ -366,19 +366,22 @@ def featureless_backward(csr: CSR, dZ, M: int, geometry: Optional[Geometry] = No
     return dPhi
 
 
-def conv_decay_gradient(csr: CSR, F, W, dY, geometry: Geometry) -> torch.Tensor:
+def conv_decay_gradient(csr: CSR, F, W, dY, geometry: Geometry,
+                        csc: Optional[CSC] = None) -> torch.Tensor:
     """d<Y, dY>/d lambda [M] float32 for the learned-decay event kernel
-    (sbc_conv_decay_gradient)."""
+    (sbc_conv_decay_gradient); with the transpose it takes the fused route."""
     dev, M, C_in, C_out = _conv_common(csr, F, W, None, geometry)
     _require(dY, "dY", F.dtype, 2, dev)
     dt = _dtype_code(F)
     dl = torch.empty(M, dtype=torch.float32, device=dev)
     lib = L.lib()
-    ws = _Workspace(lib.sbc_decay_gradient_workspace_size(csr.n_rows, csr.nnz, M, C_in, C_out),
-                    dev)
+    ws = _Workspace(lib.sbc_decay_gradient_workspace_size(csr.n_rows, csr.nnz, M, C_in, C_out,
+                                                          dt), dev)
     c, g = csr.c_struct(), geometry.c_struct()
-    L.check(lib.sbc_conv_decay_gradient(ctypes.byref(c), ctypes.byref(g), M, _p(F), _p(W), _p(dY),
-                                        dt, C_in, C_out, _p(dl), ws.ptr, ws.nbytes, _stream(dev)))
+    k = csc.c_struct() if csc is not None else None
+    L.check(lib.sbc_conv_decay_gradient(ctypes.byref(c), ctypes.byref(k) if k is not None else None,
+                                        ctypes.byref(g), M, _p(F), _p(W), _p(dY), dt, C_in, C_out,
+                                        _p(dl), ws.ptr, ws.nbytes, _stream(dev)))
     return dl
 
 

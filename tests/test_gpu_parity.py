@@ -57,6 +57,7 @@ SMALL = {
     "ev_decays2": lambda: workloads.small_events(seed=20, c=8, n_decays=2),
     "ev_decays3_odd": lambda: workloads.small_events(seed=22, n=3001, c=13, n_decays=3),
     "ev_decays4_bf16": lambda: workloads.small_events(seed=21, c=16, n_decays=4, dtype="bf16"),
+    "fz_ev_decays2_32": lambda: workloads.small_events(seed=23, c=32, n=5003, n_decays=2),
 }
 # the general convolution's full-size cases; the featureless first layer
 # (one input channel of features ~N(0,1), so single-channel input gradients
@@ -623,15 +624,22 @@ def test_upsampling(order):
 
 
 # ---------------------------------------------------------------- learned decay rates
+@pytest.mark.parametrize("route", ["sparse_product", "fused"])
 @pytest.mark.parametrize("name", ["ev_decays2", "ev_decays3_odd", "ev_decays4_bf16",
-                                  "events_300k_decays2"])
-def test_decay_gradient(name):
+                                  "fz_ev_decays2_32", "events_300k_decays2"])
+def test_decay_gradient(name, route):
     """d<Y, dY>/d lambda of the learned-decay kernel (Eq. 12) against the oracle's
-    per-edge chain rule."""
-    print(f"[decay gradient] {name}", flush=True)
+    per-edge chain rule: without the transpose (G' = N' F route), and with the
+    transpose from the reverse search (the fused D-route where the shape has one)."""
+    print(f"[decay gradient] {name} {route}", flush=True)
     w, rp, ci, v = case(name)
     t, csr = gpu_case(name)
-    dl = G.sbc.conv_decay_gradient(csr, t["F"], t["W"], t["dY"], G.geometry(w, t)).cpu().numpy()
+    csc = None
+    if route == "fused":
+        _, csc = G.sbc.neighbour_search_events_csc(t["px"], t["py"], t["t"], w["width"],
+                                                   w["height"], w["window"])
+    dl = G.sbc.conv_decay_gradient(csr, t["F"], t["W"], t["dY"], G.geometry(w, t),
+                                   csc=csc).cpu().numpy()
     vd = oracle.basis.event_decay_basis(w["px"], w["py"], w["t"], rp, ci, w["decays"],
                                         derivative=True)
     ref = oracle.conv.decay_backward(rp, ci, vd, w["F"], w["W"], w["dY"])
