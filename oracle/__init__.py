@@ -14,9 +14,9 @@ search, invariants, the dense-matrix form, the textbook 2D convolution, the
 deployment recursion of the event convolution, adjoint identities and finite
 differences).  No function is left unpinned.
 """
-from . import basis, conv
+from . import basis, conv, sampling
 from ._native import (build, csr_transpose, events_csr, max_threads, points_csr,
                       points_d2)
 
-__all__ = ["basis", "conv", "build", "csr_transpose", "events_csr", "max_threads",
+__all__ = ["basis", "conv", "sampling", "build", "csr_transpose", "events_csr", "max_threads",
            "points_csr", "points_d2"]

@@ -1,0 +1,113 @@
+"""Subsampling of point clouds (Section 3.1, "Subsampling"; the supplementary
+algorithms for iterative farthest point selection, its neighbourhood-limited
+approximation and rejection sampling), in float32 where a comparison decides.
+
+CPU ORACLE -- test infrastructure only (see the package docstring).
+
+Distances are compared as squared float32 distances in the canonical form of
+the neighbour search, d2 = ((dx*dx) + (dy*dy)) + (dz*dz) with dx = a.x - b.x
+(the order of the square roots is the order of the squares).  Ties of the
+farthest-point choice go to the lowest index.  Clouds are the ranges
+splits[b] .. splits[b+1]-1 of a ragged batch; indices are global.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def _d2(x, j):
+    """float32 squared distances from every point of x to x[j]."""
+    d = x - x[j]
+    return (d[:, 0] * d[:, 0] + d[:, 1] * d[:, 1]) + d[:, 2] * d[:, 2]
+
+
+def ifp(x, splits, counts):
+    """Iterative farthest points (the supplementary's first algorithm): start
+    with every distance infinite, repeatedly take the point farthest from the
+    points taken so far (argmax; the printed argmin is read as argmax, since
+    with infinite initial distances argmin would take the first point again)
+    and lower every distance to the new point.  Returns the global indices of
+    each cloud's counts[b] points in the order taken, and the final squared
+    distances [n]."""
+    x = np.asarray(x, dtype=np.float32)
+    out = []
+    dall = np.full(len(x), np.inf, dtype=np.float32)
+    for b in range(len(splits) - 1):
+        s, e = int(splits[b]), int(splits[b + 1])
+        xb = x[s:e]
+        dmin = dall[s:e]
+        for _ in range(int(counts[b])):
+            j = int(np.argmax(dmin))         # first index of the maximum
+            out.append(s + j)
+            dmin[:] = np.minimum(dmin, _d2(xb, j))
+    return np.asarray(out, dtype=np.int32), dall
+
+
+def rejection_sampling(x, splits, row_ptr, col_idx):
+    """Rejection sampling (the supplementary's fourth algorithm): visit the
+    inputs in order; an input not yet visited is taken, and it and its ball
+    neighbours (the in-place, uncapped neighbourhood CSR) are marked visited,
+    each neighbour's distance lowered to its distance from the taken point.
+    Returns (taken flags [n] int32, d_min squared [n] float32)."""
+    x = np.asarray(x, dtype=np.float32)
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    col_idx = np.asarray(col_idx, dtype=np.int64)
+    n = len(x)
+    taken = np.zeros(n, dtype=np.int32)
+    visited = np.zeros(n, dtype=bool)
+    dmin = np.full(n, np.inf, dtype=np.float32)
+    for i in range(n):
+        if visited[i]:
+            continue
+        taken[i] = 1
+        nb = col_idx[row_ptr[i]:row_ptr[i + 1]]
+        visited[nb] = True
+        d = x[nb] - x[i]
+        d2 = (d[:, 0] * d[:, 0] + d[:, 1] * d[:, 1]) + d[:, 2] * d[:, 2]
+        dmin[nb] = np.minimum(dmin[nb], d2)
+    return taken, dmin
+
+
+def approx_ifp(x, splits, counts, row_ptr, col_idx, dmin=None):
+    """Farthest points with distance updates limited to the ball neighbourhood
+    of each taken point (the supplementary's approximate variant with a
+    priority queue): take the input of largest d_min (ties: lowest index),
+    then lower the d_min of its neighbours to their distance from it.  dmin:
+    initial squared distances (rejection sampling's, for the variant that
+    continues after it), else infinite.  Returns the global indices taken,
+    cloud by cloud, counts[b] per cloud, and the final squared distances."""
+    x = np.asarray(x, dtype=np.float32)
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    col_idx = np.asarray(col_idx, dtype=np.int64)
+    d = (np.full(len(x), np.inf, dtype=np.float32) if dmin is None
+         else np.array(dmin, dtype=np.float32))
+    out = []
+    for b in range(len(splits) - 1):
+        s, e = int(splits[b]), int(splits[b + 1])
+        for _ in range(int(counts[b])):
+            j = s + int(np.argmax(d[s:e]))
+            out.append(j)
+            nb = col_idx[row_ptr[j]:row_ptr[j + 1]]
+            dd = x[nb] - x[j]
+            d2 = (dd[:, 0] * dd[:, 0] + dd[:, 1] * dd[:, 1]) + dd[:, 2] * dd[:, 2]
+            d[nb] = np.minimum(d[nb], d2)
+    return np.asarray(out, dtype=np.int32), d
+
+
+def approx_ifp_after_rejection(x, splits, per_cloud, row_ptr, col_idx):
+    """Rejection sampling, then the approximate farthest points from its
+    distances (the supplementary's last algorithm), per_cloud points per cloud
+    (at most the cloud's size): the taken points first, in input order, then
+    the farthest points.  When rejection takes more than per_cloud points the
+    first per_cloud of them are kept (the output size is fixed; a reading, the
+    algorithm leaves that case open).  Returns (indices, final squared distances)."""
+    taken, d = rejection_sampling(x, splits, row_ptr, col_idx)
+    out = []
+    for b in range(len(splits) - 1):
+        s, e = int(splits[b]), int(splits[b + 1])
+        S = min(int(per_cloud), e - s)
+        first = (s + np.nonzero(taken[s:e])[0])[:S]
+        more, d = approx_ifp(x, [s, e], [S - len(first)], row_ptr, col_idx, d)
+        out.extend(first.tolist())
+        out.extend(more.tolist())
+    return np.asarray(out, dtype=np.int32), d
