@@ -134,13 +134,14 @@ __device__ __forceinline__ int32_t seg_cloud(const Seg<L> &sg, const int32_t *__
     return b;
 }
 
-// Canonical float32 squared distance: no contraction, fixed association.
+// Canonical float32 squared distance: fixed association and no contraction
+// (the rounding intrinsics alone do not stop the compiler from fusing the
+// products into the sums; the pragma does).
 __device__ __forceinline__ float sq_dist(float ax, float ay, float az, float bx, float by,
                                          float bz) {
-    float dx = __fsub_rn(ax, bx);
-    float dy = __fsub_rn(ay, by);
-    float dz = __fsub_rn(az, bz);
-    return __fadd_rn(__fadd_rn(__fmul_rn(dx, dx), __fmul_rn(dy, dy)), __fmul_rn(dz, dz));
+#pragma clang fp contract(off)
+    const float dx = ax - bx, dy = ay - by, dz = az - bz;
+    return (dx * dx + dy * dy) + dz * dz;
 }
 
 // Zeroes the cell counts and the status word.
