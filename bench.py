@@ -55,6 +55,9 @@ DESCRIPTIONS = {
     "events_300k_decays2": "300k events, 128x128 pixels, 100 ms uniform; 3x3 block, 10 ms "
                            "window; learned decays, 2 per offset (M 16), with their gradient; "
                            "32 -> 32 channels fp32",
+    "ellipsoids_sampling": "32 clouds x 1024 points on ellipsoid surfaces; uncapped in-place "
+                           "ball r 0.1, then rejection sampling and approximate farthest points "
+                           "up to 256 per cloud",
 }
 
 
@@ -215,6 +218,17 @@ def summarize_trace(trace_dir, command, bench_json=None):
     return "\n".join(out) + "\n"
 
 
+def sampling_table(n, E, n_batch):
+    """Kernels of one sampling step (uncapped ball search, rejection sampling
+    and approximate farthest points): name -> (launches, bytes, flops, MFMA)."""
+    return {
+        "points_count": (1, 12 * n + 16 * n + 4 * n, 0, False),
+        "points_fill": (1, 12 * n + 16 * n + 8 * n + 4 * E, 0, False),
+        "sample_count": (1, 4 * (n_batch + 1) + 4 * (n + 1) + 4 * E + 12 * n, 0, False),
+        "sample": (1, 4 * (n_batch + 1) + 4 * (n + 1) + 4 * E + 12 * n + 8 * n, 0, False),
+    }
+
+
 def featureless_table(n_in, n_out, E, M, P):
     """Kernels of one featureless step (search, Z = G~ Phi, dPhi = G~^T dZ):
     name -> (launches, algorithmic bytes, flops, on MFMA)."""
@@ -308,13 +322,18 @@ def cpu_baseline(w, reps):
         if w["kind"] == "points":
             rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
                                        w["radius"], w["k_cap"])
-            v = oracle.basis.point_values(w["basis"], w["x_in"], w["x_out"], rp, ci, w["radius"], w["M"])
+            v = oracle.basis.point_values(w["basis"], w["x_in"], w["x_out"], rp, ci,
+                                          w["radius"], w["M"])
         else:
             rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"],
                                        w["height"])
             v = oracle.basis.event_values(w["basis"], w["px"], w["py"], w["t"], rp, ci,
                                           w["tau"], w.get("decays"))
-        if w.get("featureless"):
+        if w.get("sampling"):
+            smp = w["sampling"]
+            oracle.sampling.approx_ifp_after_rejection(w["x_in"], w["in_splits"],
+                                                       smp["per_cloud"], rp, ci)
+        elif w.get("featureless"):
             Phi = w["W"][:, 0, :]
             oracle.conv.featureless_forward(rp, ci, v, Phi)
             oracle.conv.featureless_backward(rp, ci, v, w["dY"])
@@ -332,7 +351,8 @@ def cpu_baseline(w, reps):
     return {"value": E / med, "unit": "edges/s", "cores": max(oracle.max_threads(), blas),
             "kind": "oracle",
             "sample": f"whole workload ({E} edges): neighbours, basis, "
-                      + ("featureless forward and backward" if w.get("featureless")
+                      + ("rejection sampling and farthest points" if w.get("sampling")
+                         else "featureless forward and backward" if w.get("featureless")
                          else "forward, transpose, backward")
                       + f" in float64; median of {reps} passes, {med:.2f} s each"}
 
@@ -421,9 +441,13 @@ def main(argv=None):
         s_in, s_out = T(w["in_splits"]), T(w["out_splits"])
         geo = sbc.Geometry(w["basis"], radius=w["radius"], x_in=x_in, x_out=x_out)
 
+        # an uncapped search needs a capacity to run unsynchronised
+        cap_ball = None if w["k_cap"] > 0 else sbc.neighbour_search_points(
+            x_in, s_in, x_out, s_out, w["radius"], 0).nnz
+
         def search():
             return sbc.neighbour_search_points(x_in, s_in, x_out, s_out, w["radius"],
-                                               w["k_cap"], sync=False)
+                                               w["k_cap"], col_capacity=cap_ball, sync=False)
 
         def transpose(csr):  # the batch is block-diagonal: cloud by cloud
             return sbc.csr_transpose_batched(csr, s_out, s_in)
@@ -450,7 +474,19 @@ def main(argv=None):
     E = int(csr0.row_ptr[-1].item())
     plan = sbc.conv_plan(n_out, n_in, csr0.nnz, M, ci, co, F.dtype, a.order)
 
-    if w.get("featureless"):
+    if w.get("sampling"):
+        # down-sampling for the next layer: the uncapped ball, then the sampler
+        smp = w["sampling"]
+        n_batch = len(w["in_splits"]) - 1
+        max_cloud = int(np.diff(w["in_splits"]).max())
+
+        def step():
+            csr = search()
+            return sbc.sample_points(x_in, s_in, smp["method"], smp["per_cloud"], ball=csr,
+                                     max_cloud=max_cloud)
+
+        table = sampling_table(n_in, E, n_batch)
+    elif w.get("featureless"):
         # the first layer on bare coordinates: Phi_0 = W[:, 0, :], dZ = dY
         Phi = W[:, 0, :].contiguous()
 

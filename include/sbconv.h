@@ -355,6 +355,53 @@ sbc_status sbc_featureless_backward(const sbc_csr *csr, const float *v,
                                     size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * 7. Subsampling of a ragged point batch (Section 3.1, "Subsampling", and the
+ * supplementary algorithms), cloud by cloud:
+ *   SBC_SAMPLE_IFP                  iterative farthest points: repeatedly the
+ *                                   point farthest from those taken (all
+ *                                   distances start infinite, so the cloud's
+ *                                   first point comes first);
+ *   SBC_SAMPLE_APPROX_IFP           the same with each taken point lowering the
+ *                                   distances of its ball neighbours only;
+ *   SBC_SAMPLE_REJECTION            rejection sampling: in input order, every
+ *                                   point that no earlier taken point has in
+ *                                   its ball (a variable number per cloud);
+ *   SBC_SAMPLE_APPROX_IFP_REJECTION rejection sampling, then the approximate
+ *                                   farthest points from its distances up to
+ *                                   per_cloud points (the taken points first,
+ *                                   in input order; if rejection takes more,
+ *                                   the first per_cloud of them).
+ * Distances are compared as float32 squared distances in the canonical form of
+ * the neighbour search; ties go to the lowest index.  Results are exact and
+ * deterministic.
+ *   x [n_points, 3], splits [n_batch + 1]  device; clouds of at most max_cloud
+ *                                          <= 8192 points (a larger cloud gets
+ *                                          no outputs)
+ *   ball        the in-place ball pattern of x (sbc_neighbour_search_points
+ *               with x as inputs and outputs, k_cap <= 0); NULL for IFP
+ *   per_cloud   outputs per cloud (min(per_cloud, cloud size)); ignored by
+ *               SBC_SAMPLE_REJECTION
+ *   out_idx     [n_points] device, output: global indices of the outputs,
+ *               cloud by cloud, in the order taken
+ *   out_splits  [n_batch + 1] device, output: cloud b's outputs are
+ *               out_idx[out_splits[b] .. out_splits[b+1])
+ *   dmin2       [n_points] device, output (may be NULL): each point's squared
+ *               distance to its nearest taken point as the algorithm tracked it
+ * ------------------------------------------------------------------------ */
+typedef enum {
+    SBC_SAMPLE_IFP = 0,
+    SBC_SAMPLE_APPROX_IFP = 1,
+    SBC_SAMPLE_REJECTION = 2,
+    SBC_SAMPLE_APPROX_IFP_REJECTION = 3
+} sbc_sampling;
+size_t sbc_sampling_workspace_size(int32_t n_batch);
+sbc_status sbc_sample_points(const float *x, const int32_t *splits, int32_t n_batch,
+                             int32_t n_points, int32_t max_cloud, const sbc_csr *ball,
+                             sbc_sampling method, int32_t per_cloud, int32_t *out_idx,
+                             int32_t *out_splits, float *dmin2, void *workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Tracing, for measurement tools.  After sbc_trace_kernel(name, start, stop)
  * every launch of the kernel called `name` made by the calling thread records
  * `start` immediately before and `stop` immediately after itself on its

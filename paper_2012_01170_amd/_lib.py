@@ -30,6 +30,7 @@ EXPORTS = [
     "sbc_resolve_order", "sbc_trace_kernel", "sbc_trace_clear", "sbc_kernel_names",
     "sbc_conv_plan", "sbc_featureless_workspace_size", "sbc_featureless_forward",
     "sbc_featureless_backward", "sbc_decay_gradient_workspace_size", "sbc_conv_decay_gradient",
+    "sbc_sampling_workspace_size", "sbc_sample_points",
 ]
 
 
@@ -86,6 +87,9 @@ _SIGS = {
                                                        _vp, _sz, _vp]),
     "sbc_basis_eval": (ctypes.c_int, [_csr_p, _geo_p, _vp, _vp]),
     "sbc_featureless_workspace_size": (_sz, [_i32, _i32, _i32]),
+    "sbc_sampling_workspace_size": (_sz, [_i32]),
+    "sbc_sample_points": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _csr_p, ctypes.c_int, _i32,
+                                         _vp, _vp, _vp, _vp, _sz, _vp]),
     "sbc_decay_gradient_workspace_size": (_sz, [_i32, _i64, _i32, _i32, _i32, ctypes.c_int]),
     "sbc_conv_decay_gradient": (ctypes.c_int, [_csr_p, _csc_p, _geo_p, _i32, _vp, _vp, _vp,
                                                ctypes.c_int, _i32, _i32, _vp, _vp, _sz, _vp]),

@@ -385,6 +385,38 @@ def conv_decay_gradient(csr: CSR, F, W, dY, geometry: Geometry,
     return dl
 
 
+SAMPLING = {"ifp": 0, "approx_ifp": 1, "rejection": 2, "approx_ifp_rejection": 3}
+
+
+def sample_points(x, splits, method: str, per_cloud: int = 0, ball: Optional[CSR] = None,
+                  max_cloud: Optional[int] = None, with_dmin: bool = False):
+    """Subsample a ragged point batch (sbc_sample_points).
+
+    Returns (out_idx, out_splits) or, with with_dmin, (out_idx, out_splits,
+    dmin2); out_idx holds capacity for every point, cloud b's outputs are
+    out_idx[out_splits[b]:out_splits[b+1]].  ball: the in-place uncapped ball
+    CSR (not needed for "ifp"); max_cloud: the largest cloud (read from splits
+    when None, which synchronises)."""
+    _require(x, "x", torch.float32, 2)
+    dev = x.device
+    _require(splits, "splits", torch.int32, 1, dev)
+    n = x.shape[0]
+    n_batch = splits.numel() - 1
+    if max_cloud is None:
+        max_cloud = int(torch.diff(splits).max().item()) if n_batch > 0 else 0
+    out_idx = torch.empty(max(1, n), dtype=torch.int32, device=dev)
+    out_splits = torch.empty(n_batch + 1, dtype=torch.int32, device=dev)
+    dmin2 = torch.empty(max(1, n), dtype=torch.float32, device=dev) if with_dmin else None
+    lib = L.lib()
+    ws = _Workspace(lib.sbc_sampling_workspace_size(n_batch), dev)
+    c = ball.c_struct() if ball is not None else None
+    L.check(lib.sbc_sample_points(_p(x), _p(splits), n_batch, n, int(max_cloud),
+                                  ctypes.byref(c) if c is not None else None, SAMPLING[method],
+                                  int(per_cloud), _p(out_idx), _p(out_splits), _p(dmin2), ws.ptr,
+                                  ws.nbytes, _stream(dev)))
+    return (out_idx, out_splits, dmin2) if with_dmin else (out_idx, out_splits)
+
+
 def conv_plan(n_out, n_in, nnz, M, C_in, C_out, dtype=torch.float32, order="auto") -> dict:
     """Route and fusion of forward and backward for a shape (sbc_conv_plan)."""
     plan = L.SbcConvPlan()

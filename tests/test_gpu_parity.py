@@ -62,7 +62,8 @@ SMALL = {
 # the general convolution's full-size cases; the featureless first layer
 # (one input channel of features ~N(0,1), so single-channel input gradients
 # whose sums cancel by up to 1e6) is checked as Eq. 9-10 instead
-FULL = [k for k in workloads.WORKLOADS if k != "ellipsoids_featureless"]
+FULL = [k for k in workloads.WORKLOADS
+        if k not in ("ellipsoids_featureless", "ellipsoids_sampling")]
 ORDERS = ["spmm_first", "gemm_first"]
 
 
@@ -646,3 +647,46 @@ def test_decay_gradient(name, route):
     err = G.norm_error(dl, ref)
     print(f"    dlambda error {err:.3e}", flush=True)
     assert err < tol(w)
+
+
+# ---------------------------------------------------------------- subsampling
+def _sampling_batch(seed, sizes):
+    rng = np.random.default_rng(seed)
+    xs = [workloads.ellipsoid_surface_points(rng, n, rng.uniform(0.5, 1.0, size=3))
+          if n else np.zeros((0, 3)) for n in sizes]
+    x = np.concatenate(xs).astype(np.float32)
+    return x, np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+
+
+SAMPLING_CASES = {"small": (30, [300, 0, 1, 450], 0.2, 100),
+                  "c2_clouds": (31, [1024] * 32, 0.1, 256),
+                  "large_cloud": (32, [8192, 700], 0.05, 2000)}
+
+
+@pytest.mark.parametrize("method", ["ifp", "approx_ifp", "rejection", "approx_ifp_rejection"])
+@pytest.mark.parametrize("case_name", list(SAMPLING_CASES))
+def test_sampling_bit_exact(case_name, method):
+    """Indices, bounds and squared distances equal the oracle's exactly."""
+    print(f"[sampling] {case_name} {method}", flush=True)
+    seed, sizes, radius, per = SAMPLING_CASES[case_name]
+    x, splits = _sampling_batch(seed, sizes)
+    rp, ci = oracle.points_csr(x, splits, x, splits, radius, 0)
+    xd, sd = G.dev(x), G.dev(splits)
+    ball = G.sbc.neighbour_search_points(xd, sd, xd, sd, radius, 0)
+    idx, osp, d2 = G.sbc.sample_points(xd, sd, method, per, ball=ball, with_dmin=True)
+    if method == "ifp":
+        ref, dref = oracle.sampling.ifp(x, splits, [min(per, n) for n in sizes])
+    elif method == "approx_ifp":
+        ref, dref = oracle.sampling.approx_ifp(x, splits, [min(per, n) for n in sizes], rp, ci)
+    elif method == "rejection":
+        taken, dref = oracle.sampling.rejection_sampling(x, splits, rp, ci)
+        ref = np.nonzero(taken)[0].astype(np.int32)
+    else:
+        ref, dref = oracle.sampling.approx_ifp_after_rejection(x, splits, per, rp, ci)
+    osp = osp.cpu().numpy()
+    assert osp[-1] == len(ref)
+    assert np.array_equal(idx.cpu().numpy()[:len(ref)], ref)
+    assert np.array_equal(d2.cpu().numpy()[:len(x)], dref)
+    if method == "rejection":
+        want = np.searchsorted(ref, splits)      # taken points per cloud, in order
+        assert np.array_equal(osp, want)

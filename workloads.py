@@ -284,6 +284,16 @@ def ellipsoids_featureless():
     return w
 
 
+def ellipsoids_sampling():
+    """Down-sampling the ellipsoid batch for the next layer: the uncapped
+    in-place ball (r 0.1) of 32 clouds x 1024 points, then rejection sampling
+    and the approximate farthest points up to 256 points per cloud."""
+    w = ellipsoid_batch(seed_index=1, k_cap=0)
+    w["sampling"] = {"method": "approx_ifp_rejection", "per_cloud": 256}
+    w["name"] = "ellipsoids32x1024_sampling"
+    return w
+
+
 def events_300k_decays2():
     """The 300k-event stream with learned decays, M_v = 2 per offset (M = 16)."""
     return event_stream(n_decays=2)
@@ -298,6 +308,7 @@ WORKLOADS = {
     "ellipsoids_weighted": ellipsoids_weighted,
     "ellipsoids_featureless": ellipsoids_featureless,
     "events_300k_decays2": events_300k_decays2,
+    "ellipsoids_sampling": ellipsoids_sampling,
 }
 
 
