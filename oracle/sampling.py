@@ -111,3 +111,45 @@ def approx_ifp_after_rejection(x, splits, per_cloud, row_ptr, col_idx):
         out.extend(first.tolist())
         out.extend(more.tolist())
     return np.asarray(out, dtype=np.int32), d
+
+
+
+def lif_receptive(x, kernel, stride, n_out):
+    """Output cells (one dimension) whose receptive field holds input coordinate
+    x.  Reading: cell o sees the kernel inputs centred on its own position o *
+    stride, i.e. [o*stride - p, o*stride - p + kernel) with p = (kernel-1)//2,
+    and there are ceil(size / stride) cells (a padded strided convolution, so
+    each down-sampling halves the sensor as in the event networks)."""
+    p = (kernel - 1) // 2
+    return [o for o in range(n_out) if o * stride - p <= x < o * stride - p + kernel]
+
+
+def lif(px, py, t, width, height, kernel, stride, decay, v_thresh, v_reset):
+    """The leaky integrate-and-fire event sampler (the supplementary's
+    algorithm for generating the next, coarser stream).  Every output cell
+    keeps a potential V and the time T of its last update, both starting at 0.
+    For each input event in stream order, each output cell of its receptive
+    field N (row-major over (oy, ox)) decays its potential to the event's time,
+    adds 1/n (n = |N|, the number of cells the event reaches), and, when the
+    result exceeds v_thresh, resets it to v_reset and emits an output event at
+    that cell with the input's time.  Potentials are float64.  Returns the
+    (input event index, ox, oy) of every output event in emission order; the
+    output grid has ceil(width / stride) x ceil(height / stride) cells."""
+    Wo, Ho = -(-int(width) // stride), -(-int(height) // stride)
+    V = np.zeros((Ho, Wo))
+    T = np.zeros((Ho, Wo))
+    out = []
+    for i in range(len(t)):
+        xs = lif_receptive(int(px[i]), kernel, stride, Wo)
+        ys = lif_receptive(int(py[i]), kernel, stride, Ho)
+        n = len(xs) * len(ys)
+        ti = float(t[i])
+        for oy in ys:
+            for ox in xs:
+                v = V[oy, ox] * np.exp(-(ti - T[oy, ox]) / decay) + 1.0 / n
+                if v > v_thresh:
+                    v = v_reset
+                    out.append((i, ox, oy))
+                V[oy, ox] = v
+                T[oy, ox] = ti
+    return np.asarray(out, dtype=np.int64).reshape(-1, 3)
