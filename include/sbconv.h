@@ -402,6 +402,46 @@ sbc_status sbc_sample_points(const float *x, const int32_t *splits, int32_t n_ba
                              size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * 8. Event stream sampling by leaky integrate-and-fire (the supplementary's
+ * algorithm for the coarser streams of the event networks, Section 4).
+ *
+ * The output grid has Wo = ceil(width / stride) x Ho = ceil(height / stride)
+ * cells; cell (ox, oy) sees the kernel x kernel input pixels centred on
+ * (ox * stride, oy * stride) (offsets -(kernel-1)/2 .. kernel/2, rounded down,
+ * as in a padded strided convolution).  Every cell holds a potential V and the
+ * time T of its last update, both 0 at the start.  For each input event i, in
+ * stream order, every cell that sees its pixel (row-major over (oy, ox); n of
+ * them) sets v = V * exp(-(t_i - T) / decay) + 1 / n; if v > v_thresh it emits
+ * an output event (ox, oy, t_i) and sets v = v_reset; then V = v, T = t_i.
+ * Potentials are float64, evaluated in that order with no fused multiply-add.
+ * Output events come in emission order: by input event, then oy, then ox, so
+ * their times are non-decreasing.  Deterministic.
+ *   px, py, t   [n] int32 device: pixels in [0, width) x [0, height), times
+ *               non-decreasing (an event off the sensor reaches no cell)
+ *   kernel      1..5; stride >= 1 (with stride > kernel some pixels reach no
+ *               cell, and their events change nothing)
+ *   decay       the decay time (> 0; +inf: no decay); v_thresh, v_reset
+ *   out_x, out_y, out_t  [capacity] int32 device, output: output events;
+ *               out_src [capacity] (may be NULL): the input event that
+ *               caused each.  At most n * ((kernel-1)/stride + 1)^2 events.
+ *               Events past capacity are counted but not written.
+ *   n_out_dev   int64 device (may be NULL): the number of output events
+ *   n_out_host  (may be NULL) the same on the host; the call then synchronises
+ *               the stream and reports SBC_ERR_OUT_OF_RANGE, SBC_ERR_UNSORTED
+ *               or SBC_ERR_CAPACITY (without it, no synchronisation and no
+ *               such checks, so the call can be captured in a graph)
+ * ------------------------------------------------------------------------ */
+size_t sbc_lif_workspace_size(int32_t n, int32_t width, int32_t height, int32_t kernel,
+                              int32_t stride);
+sbc_status sbc_lif_sample_events(const int32_t *px, const int32_t *py, const int32_t *t,
+                                 int32_t n, int32_t width, int32_t height, int32_t kernel,
+                                 int32_t stride, double decay, double v_thresh, double v_reset,
+                                 int32_t *out_x, int32_t *out_y, int32_t *out_t,
+                                 int32_t *out_src, int64_t capacity, int64_t *n_out_dev,
+                                 int64_t *n_out_host, void *workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Tracing, for measurement tools.  After sbc_trace_kernel(name, start, stop)
  * every launch of the kernel called `name` made by the calling thread records
  * `start` immediately before and `stop` immediately after itself on its

@@ -31,6 +31,7 @@ EXPORTS = [
     "sbc_conv_plan", "sbc_featureless_workspace_size", "sbc_featureless_forward",
     "sbc_featureless_backward", "sbc_decay_gradient_workspace_size", "sbc_conv_decay_gradient",
     "sbc_sampling_workspace_size", "sbc_sample_points",
+    "sbc_lif_workspace_size", "sbc_lif_sample_events",
 ]
 
 
@@ -90,6 +91,11 @@ _SIGS = {
     "sbc_sampling_workspace_size": (_sz, [_i32]),
     "sbc_sample_points": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _csr_p, ctypes.c_int, _i32,
                                          _vp, _vp, _vp, _vp, _sz, _vp]),
+    "sbc_lif_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32]),
+    "sbc_lif_sample_events": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
+                                             ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                             _vp, _vp, _vp, _vp, _i64, _vp, _i64_p, _vp, _sz,
+                                             _vp]),
     "sbc_decay_gradient_workspace_size": (_sz, [_i32, _i64, _i32, _i32, _i32, ctypes.c_int]),
     "sbc_conv_decay_gradient": (ctypes.c_int, [_csr_p, _csc_p, _geo_p, _i32, _vp, _vp, _vp,
                                                ctypes.c_int, _i32, _i32, _vp, _vp, _sz, _vp]),

@@ -417,6 +417,44 @@ def sample_points(x, splits, method: str, per_cloud: int = 0, ball: Optional[CSR
     return (out_idx, out_splits, dmin2) if with_dmin else (out_idx, out_splits)
 
 
+def lif_sample_events(px, py, t, width: int, height: int, kernel: int = 3, stride: int = 2,
+                      decay: float = 1000.0, v_thresh: float = 1.5, v_reset: float = -3.0,
+                      capacity: Optional[int] = None, sync: bool = True):
+    """The coarser event stream by leaky integrate-and-fire (sbc_lif_sample_events).
+
+    Returns (x, y, t, src, count): output pixels on the ceil(width / stride) x
+    ceil(height / stride) grid, times, the input event behind each, and the
+    number of output events.  With sync (the default) the arrays are trimmed
+    to that number and count is an int; without, they keep their capacity
+    (default: the most events possible) and count is an int64 device tensor."""
+    _require(px, "px", torch.int32, 1)
+    dev = px.device
+    _require(py, "py", torch.int32, 1, dev)
+    _require(t, "t", torch.int32, 1, dev)
+    n = int(px.numel())
+    if int(py.numel()) != n or int(t.numel()) != n:
+        raise ValueError("px, py and t must have the same length")
+    lib = L.lib()
+    nsd = (int(kernel) - 1) // max(int(stride), 1) + 1
+    if capacity is None:
+        capacity = n * nsd * nsd
+    cap = max(1, int(capacity))
+    out = [torch.empty(cap, dtype=torch.int32, device=dev) for _ in range(4)]
+    count = torch.zeros(1, dtype=torch.int64, device=dev)
+    ws = _Workspace(lib.sbc_lif_workspace_size(n, width, height, kernel, stride), dev)
+    host = ctypes.c_int64(0)
+    L.check(lib.sbc_lif_sample_events(_p(px), _p(py), _p(t), n, width, height, kernel, stride,
+                                      float(decay), float(v_thresh), float(v_reset),
+                                      _p(out[0]), _p(out[1]), _p(out[2]), _p(out[3]),
+                                      int(capacity), _p(count),
+                                      ctypes.byref(host) if sync else None, ws.ptr, ws.nbytes,
+                                      _stream(dev)))
+    if sync:
+        k = int(host.value)
+        return tuple(o[:k] for o in out) + (k,)
+    return tuple(out) + (count,)
+
+
 def conv_plan(n_out, n_in, nnz, M, C_in, C_out, dtype=torch.float32, order="auto") -> dict:
     """Route and fusion of forward and backward for a shape (sbc_conv_plan)."""
     plan = L.SbcConvPlan()

@@ -79,3 +79,35 @@ def test_graph_replays_match_eager(name):
         for a, b in zip(eager, outs):
             assert np.array_equal(a, b.cpu().numpy()), f"replay {r} differs"
         assert torch.isfinite(junk)
+
+
+def test_lif_graph_replays_match_eager():
+    """The unsynchronised LIF sampler (sort, cells, scan, emission) captured in
+    a graph reproduces the eager output events and count on every replay."""
+    print("[graph] lif", flush=True)
+    px, py, t, _ = workloads.uniform_events(np.random.default_rng(47), 20_000, 34, 34, 30_000)
+    args = [torch.from_numpy(a).to(G.DEV) for a in (px, py, t)]
+
+    def step():
+        return G.sbc.lif_sample_events(*args, 34, 34, 3, 2, 2000.0, 1.5, -3.0, sync=False)
+
+    eager = [x.cpu().numpy().copy() for x in step()]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        outs = step()
+    k = int(eager[4][0])
+    assert k > 0
+    for r in range(3):
+        junk = torch.randn(1 << 16, device=G.DEV).sum()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert int(outs[4].item()) == k, f"replay {r}: count differs"
+        for a, b in zip(eager[:4], outs[:4]):
+            assert np.array_equal(a[:k], b.cpu().numpy()[:k]), f"replay {r} differs"
+        assert torch.isfinite(junk)

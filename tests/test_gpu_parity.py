@@ -690,3 +690,93 @@ def test_sampling_bit_exact(case_name, method):
     if method == "rejection":
         want = np.searchsorted(ref, splits)      # taken points per cloud, in order
         assert np.array_equal(osp, want)
+
+
+# ---------------------------------------------------------------- LIF event sampler
+# (seed, n, width, height, duration, kernel, stride, decay, thresh, reset)
+LIF_CASES = {
+    "nmnist_k3s2": (40, 5000, 34, 34, 30_000, 3, 2, 2000.0, 1.5, -3.0),
+    "k5s1": (41, 4000, 23, 17, 20_000, 5, 1, 1000.0, 1.25, -2.0),
+    "k4s2_even": (42, 4000, 19, 21, 20_000, 4, 2, 1500.0, 1.0, -3.0),
+    "k1s2_unreached": (43, 3000, 15, 9, 10_000, 1, 2, 3000.0, 1.5, 0.0),
+    "k2s3": (44, 3000, 31, 12, 10_000, 2, 3, 500.0, 0.7, 0.1),
+    "cifar_k3s2_300k": (45, 300_000, 128, 128, 100_000, 3, 2, 4000.0, 1.6, -3.0),
+}
+
+
+def _lif_ref(px, py, t, W, H, k, S, decay, th, rs):
+    out = oracle.sampling.lif(px, py, t, W, H, k, S, decay, th, rs)
+    return out[:, 1].astype(np.int32), out[:, 2].astype(np.int32), t[out[:, 0]], \
+        out[:, 0].astype(np.int32)
+
+
+def _lif_check(px, py, t, W, H, k, S, decay, th, rs):
+    x, y, tt, src, cnt = G.sbc.lif_sample_events(G.dev(px), G.dev(py), G.dev(t), W, H, k, S,
+                                                 decay, th, rs)
+    rx, ry, rt, rsrc = _lif_ref(px, py, t, W, H, k, S, decay, th, rs)
+    print(f"    {len(px)} events -> {cnt} (oracle {len(rx)})", flush=True)
+    assert cnt == len(rx)
+    for a, b in [(src, rsrc), (x, rx), (y, ry), (tt, rt)]:
+        assert np.array_equal(a.cpu().numpy(), b)
+    return cnt
+
+
+@pytest.mark.parametrize("case_name", list(LIF_CASES))
+def test_lif_bit_exact(case_name):
+    """Output events (cell, time, source event), in emission order, equal the
+    oracle's exactly."""
+    print(f"[lif] {case_name}", flush=True)
+    seed, n, W, H, dur, k, S, decay, th, rs = LIF_CASES[case_name]
+    px, py, t, _ = workloads.uniform_events(np.random.default_rng(seed), n, W, H, dur)
+    assert _lif_check(px, py, t, W, H, k, S, decay, th, rs) > 0
+
+
+def test_lif_exact_ties_and_bursts():
+    """No decay, equal times and thresholds the potentials reach exactly
+    (multiples of 1/4 and 1/2): the comparison is strict on both sides.  Also a
+    bursty stream with a long decay (many spikes per cell)."""
+    print("[lif] ties", flush=True)
+    rng = np.random.default_rng(46)
+    n = 6000
+    px = rng.integers(0, 8, n).astype(np.int32)
+    py = rng.integers(0, 8, n).astype(np.int32)
+    t = np.sort(rng.integers(0, 50, n)).astype(np.int32)
+    _lif_check(px, py, t, 8, 8, 3, 2, np.inf, 1.0, 0.0)
+    _lif_check(px, py, t, 8, 8, 3, 2, 1e12, 1.5, -0.5)
+    px, py, t, _ = workloads.bursty_events(rng, 20_000, 40, 30, 40_000)
+    _lif_check(px, py, t, 40, 30, 3, 2, 20_000.0, 1.5, -2.0)
+
+
+def test_lif_empty_and_capacity():
+    """An empty stream gives no events; a capacity below the count keeps the
+    first events and, when synchronised, reports the shortfall; without
+    synchronisation the device count is exact."""
+    print("[lif] empty / capacity", flush=True)
+    e = G.dev(np.zeros(0, np.int32))
+    assert G.sbc.lif_sample_events(e, e, e, 10, 10)[4] == 0
+    seed, n, W, H, dur, k, S, decay, th, rs = LIF_CASES["nmnist_k3s2"]
+    px, py, t, _ = workloads.uniform_events(np.random.default_rng(seed), n, W, H, dur)
+    rx, ry, rt, rsrc = _lif_ref(px, py, t, W, H, k, S, decay, th, rs)
+    args = (G.dev(px), G.dev(py), G.dev(t), W, H, k, S, decay, th, rs)
+    with pytest.raises(G.sbc.ops.L.SbcError, match="capacity"):
+        G.sbc.lif_sample_events(*args, capacity=len(rx) - 1)
+    x, y, tt, src, cnt = G.sbc.lif_sample_events(*args, capacity=100, sync=False)
+    assert int(cnt.item()) == len(rx)
+    assert np.array_equal(src[:100].cpu().numpy(), rsrc[:100])
+    assert np.array_equal(x[:100].cpu().numpy(), rx[:100])
+
+
+def test_lif_rejects_bad_streams():
+    """Pixels off the sensor and decreasing times are reported (synchronised
+    calls); kernel sizes past 5 are refused before any launch."""
+    print("[lif] errors", flush=True)
+    px = G.dev(np.array([0, 1, 40], np.int32))
+    py = G.dev(np.array([0, 1, 2], np.int32))
+    t = G.dev(np.array([0, 5, 9], np.int32))
+    with pytest.raises(G.sbc.ops.L.SbcError, match="outside"):
+        G.sbc.lif_sample_events(px, py, t, 10, 10)
+    px = G.dev(np.array([0, 1, 2], np.int32))
+    with pytest.raises(G.sbc.ops.L.SbcError, match="non-decreasing"):
+        G.sbc.lif_sample_events(px, py, G.dev(np.array([0, 9, 5], np.int32)), 10, 10)
+    with pytest.raises(G.sbc.ops.L.SbcError, match="kernel"):
+        G.sbc.lif_sample_events(px, py, t, 10, 10, kernel=6)
