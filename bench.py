@@ -58,6 +58,9 @@ DESCRIPTIONS = {
     "ellipsoids_sampling": "32 clouds x 1024 points on ellipsoid surfaces; uncapped in-place "
                            "ball r 0.1, then rejection sampling and approximate farthest points "
                            "up to 256 per cloud",
+    "events_300k_lif": "300k events, 128x128 pixels, 100 ms uniform -> the 64x64 stream by "
+                       "leaky integrate-and-fire: 3x3 fields, stride 2, decay 4 ms, threshold "
+                       "1.6, reset -3; float64 potentials",
 }
 
 
@@ -65,7 +68,19 @@ SRC_DIR = os.path.join(ROOT, "paper_2012_01170_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
 # device function -> the name the library's trace hook gives its launch
 TRACE_NAME = {"bwd_ws_kernel": "bwd_fused", "fwd_fused_kernel": "fwd_fused",
-              "fwd_reg_kernel": "fwd_fused", "dw_reduce_kernel": "bwd_dw_reduce"}
+              "fwd_reg_kernel": "fwd_fused", "dw_reduce_kernel": "bwd_dw_reduce",
+              "sample_kernel<true>": "sample", "sample_kernel<false>": "sample_count",
+              "lif_cell_kernel": "lif_cells", "lif_emit_kernel": "lif_emit"}
+
+
+def trace_name(kernel):
+    """The trace-hook name of a profiled kernel ('f<args>'), or None."""
+    if kernel in TRACE_NAME:
+        return TRACE_NAME[kernel]
+    base = kernel.split("<")[0]
+    if base == "featureless_kernel":  # <M, mode, writes Z>
+        return "featureless_fwd" if kernel.rstrip(">").endswith("true") else "featureless_rowsum"
+    return TRACE_NAME.get(base)
 
 
 def source_fingerprint():
@@ -184,8 +199,8 @@ def summarize_traffic(fetch_dir, write_dir, probe_mb, command):
     # one line per traced launch name, the form bench.py reads back
     for b, k, n, fk, wk in sorted(rows_out, reverse=True):
         base = k.split("<")[0]
-        if base in TRACE_NAME:
-            out.append(f"traffic {TRACE_NAME[base]} {base} {fk:.1f} {wk:.1f} {b:.0f} "
+        if trace_name(k):
+            out.append(f"traffic {trace_name(k)} {base} {fk:.1f} {wk:.1f} {b:.0f} "
                        f"{kernel_fingerprint(base)}")
     return "\n".join(out) + "\n"
 
@@ -226,6 +241,17 @@ def sampling_table(n, E, n_batch):
         "points_fill": (1, 12 * n + 16 * n + 8 * n + 4 * E, 0, False),
         "sample_count": (1, 4 * (n_batch + 1) + 4 * (n + 1) + 4 * E + 12 * n, 0, False),
         "sample": (1, 4 * (n_batch + 1) + 4 * (n + 1) + 4 * E + 12 * n + 8 * n, 0, False),
+    }
+
+
+def lif_table(n, npix, slots, spikes):
+    """Kernels of one LIF step (pixel lists, the cells, the emission): name ->
+    (launches, algorithmic bytes, flops, MFMA).  lif_sort spans the key,
+    sort, bounds and time kernels and the flag clear."""
+    return {
+        "lif_sort": (1, 12 * n + 8 * n + 4 * (npix + 1) + 4 * n * slots, 0, False),
+        "lif_cells": (1, 4 * (npix + 1) + 8 * n + 4 * spikes, 0, False),
+        "lif_emit": (1, 8 * n * slots + 12 * spikes + 16 * spikes, 0, False),
     }
 
 
@@ -316,6 +342,19 @@ def cpu_baseline(w, reps):
         blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # threadpoolctl missing: report the OpenMP count only
         blas = 1
+    if w["kind"] == "lif":
+        times = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            out = oracle.sampling.lif(w["px"], w["py"], w["t"], w["width"], w["height"],
+                                      w["kernel"], w["stride"], w["decay"], w["v_thresh"],
+                                      w["v_reset"])
+            times.append(time.perf_counter() - t0)
+        med = statistics.median(times)
+        return {"value": w["n_in"] / med, "unit": "events/s", "cores": 1, "kind": "oracle",
+                "sample": f"whole stream ({w['n_in']} events -> {len(out)}) through the "
+                          f"sequential sampler in float64; median of {reps} passes, "
+                          f"{med:.2f} s each"}
     times, E = [], 0
     for _ in range(reps):
         t0 = time.perf_counter()
@@ -357,6 +396,76 @@ def cpu_baseline(w, reps):
                       + f" in float64; median of {reps} passes, {med:.2f} s each"}
 
 
+def measure(a, w, table, step, torch, _lib, dev):
+    """Warm-up, eager steps with every kernel bracketed by HIP events (the
+    library's trace hook), then HIP-graph replays of the captured step (the
+    timed region).  Returns (ms per step, eager ms per step, wall s, the
+    per-kernel table, the roofline of the dominant kernel)."""
+    L = _lib.lib()
+    # one (start, stop) event pair per kernel per timed step; record once so the
+    # underlying HIP events exist before the library records them again
+    ev = [{k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for k in table} for _ in range(a.steps)]
+    for d in ev:
+        for s0, s1 in d.values():
+            s0.record()
+            s1.record()
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # (1) eager steps with every kernel bracketed by HIP events (trace hook)
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    t_start.record()
+    for s in range(a.steps):
+        for k, (s0, s1) in ev[s].items():
+            _lib.check(L.sbc_trace_kernel(k.encode(), s0.cuda_event, s1.cuda_event))
+        step()
+    t_stop.record()
+    torch.cuda.synchronize()
+    L.sbc_trace_clear()
+    eager_ms = t_start.elapsed_time(t_stop) / a.steps
+
+    # (2) the same step captured once in a HIP graph (it never synchronises
+    # with the host), then replayed: the timed region
+    if a.no_graph:
+        ms, wall = eager_ms, float("nan")
+    else:
+        ms, wall = graph_timing(step, a, torch)
+    if a.copy_probe_mb > 0:
+        src = torch.ones(a.copy_probe_mb << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    kernels = {}
+    for k, (launches, nbytes, flops, mfma) in table.items():
+        us = statistics.mean(ev[s][k][0].elapsed_time(ev[s][k][1]) for s in range(a.steps)) * 1e3
+        kernels[k] = {"us": round(us, 2), "launches": launches,
+                      "GB_s": round(nbytes / (us * 1e-6) / 1e9, 1),
+                      "TFLOP_s": round(flops / (us * 1e-6) / 1e12, 3) if flops else 0.0}
+    dom = max(kernels, key=lambda k: kernels[k]["us"] * kernels[k]["launches"])
+    _, nbytes, flops, mfma = table[dom]
+    dt = w["dtype"]
+    us = kernels[dom]["us"]
+    if mfma and flops / (MFMA_PEAK_TFLOPS[dt] * 1e12) > nbytes / (HBM_PEAK_GBS * 1e9):
+        achieved, peak, unit, bound = flops / (us * 1e-6) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s", "mfma"
+    else:
+        achieved, peak, unit, bound = nbytes / (us * 1e-6) / 1e9, HBM_PEAK_GBS, "GB/s", "hbm"
+    traffic, traffic_src = read_traffic(a.workload)
+    traffic = traffic.get(dom) if traffic else None
+    roof = {"bound": bound, "kernel": dom, "achieved": round(achieved, 3), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 4),
+            "traffic": round(traffic) if traffic is not None else None,
+            "per_launch": {"bytes": nbytes, "flops": flops, "us": us,
+                           "traffic_source": traffic_src}}
+
+    return ms, eager_ms, wall, kernels, roof
+
+
 def graph_timing(step, a, torch):
     """ms per step of HIP-graph replays of one captured step, and the wall time."""
     side = torch.cuda.Stream()
@@ -380,6 +489,38 @@ def graph_timing(step, a, torch):
     t_stop.record()
     torch.cuda.synchronize()
     return t_start.elapsed_time(t_stop) / a.steps, time.perf_counter() - wall0
+
+
+def lif_main(a, w, T, torch, sbc, _lib, dev):
+    """One step: the input stream (resident in HBM) through the LIF sampler to
+    the next stream, unsynchronised; the value is input events per second."""
+    px, py, tt = T(w["px"]), T(w["py"]), T(w["t"])
+    args = (px, py, tt, w["width"], w["height"], w["kernel"], w["stride"], w["decay"],
+            w["v_thresh"], w["v_reset"])
+    spikes = sbc.lif_sample_events(*args)[4]
+    nsd = (w["kernel"] - 1) // w["stride"] + 1
+
+    def step():
+        return sbc.lif_sample_events(*args, sync=False)
+
+    n = w["n_in"]
+    table = lif_table(n, w["width"] * w["height"], nsd * nsd, spikes)
+    ms, eager_ms, wall, kernels, roof = measure(a, w, table, step, torch, _lib, dev)
+    out = {"metric": "LIF event sampler throughput (input events per second)",
+           "value": n / (ms * 1e-3), "unit": "events/s", "n_gpus": 1, "steps": a.steps,
+           "warmup": a.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": w["dtype"],
+           "data": "synthetic (seeded generators; inputs resident in HBM)",
+           "config": {"workload": f"{a.workload}: {DESCRIPTIONS[a.workload]}", "n_in": n,
+                      "n_out_events": spikes, "grid": [-(-w["width"] // w["stride"]),
+                                                       -(-w["height"] // w["stride"])],
+                      "timing": "eager steps" if a.no_graph else "HIP graph replays of the captured step",
+                      "eager_ms_per_step": round(eager_ms, 4), "wall_s": round(wall, 3)},
+           "roofline": roof, "kernels": kernels}
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, a.cpu_reps)
+    print(json.dumps(out), flush=True)
+    return 0
 
 
 def main(argv=None):
@@ -428,6 +569,8 @@ def main(argv=None):
     torch.cuda.set_device(dev)
     w = workloads.WORKLOADS[a.workload]()
     T = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+    if w["kind"] == "lif":
+        return lif_main(a, w, T, torch, sbc, _lib, dev)
     if w["dtype"] == "bf16":
         feat = lambda k: T(w[k + "_bits"].view(np.int16)).view(torch.bfloat16)
         sf = 2
@@ -530,68 +673,8 @@ def main(argv=None):
                 table["decay_gemm"] = (1, G_b + n_out * co * sf + 4 * M * ci * co,
                                        2 * n_out * M * ci * co, True)
             table["decay_dot"] = (1, 4 * M * ci * co + M * ci * co * sf + 4 * M, 0, False)
-    L = _lib.lib()
-    # one (start, stop) event pair per kernel per timed step; record once so the
-    # underlying HIP events exist before the library records them again
-    ev = [{k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for k in table} for _ in range(a.steps)]
-    for d in ev:
-        for s0, s1 in d.values():
-            s0.record()
-            s1.record()
-
-    for _ in range(a.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # (1) eager steps with every kernel bracketed by HIP events (trace hook)
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_stop = torch.cuda.Event(enable_timing=True)
-    t_start.record()
-    for s in range(a.steps):
-        for k, (s0, s1) in ev[s].items():
-            _lib.check(L.sbc_trace_kernel(k.encode(), s0.cuda_event, s1.cuda_event))
-        step()
-    t_stop.record()
-    torch.cuda.synchronize()
-    L.sbc_trace_clear()
-    eager_ms = t_start.elapsed_time(t_stop) / a.steps
-
-    # (2) the same step captured once in a HIP graph (it never synchronises
-    # with the host), then replayed: the timed region
-    if a.no_graph:
-        ms, wall = eager_ms, float("nan")
-    else:
-        ms, wall = graph_timing(step, a, torch)
-    if a.copy_probe_mb > 0:
-        src = torch.ones(a.copy_probe_mb << 18, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-
-    kernels = {}
-    for k, (launches, nbytes, flops, mfma) in table.items():
-        us = statistics.mean(ev[s][k][0].elapsed_time(ev[s][k][1]) for s in range(a.steps)) * 1e3
-        kernels[k] = {"us": round(us, 2), "launches": launches,
-                      "GB_s": round(nbytes / (us * 1e-6) / 1e9, 1),
-                      "TFLOP_s": round(flops / (us * 1e-6) / 1e12, 3) if flops else 0.0}
-    dom = max(kernels, key=lambda k: kernels[k]["us"] * kernels[k]["launches"])
-    _, nbytes, flops, mfma = table[dom]
+    ms, eager_ms, wall, kernels, roof = measure(a, w, table, step, torch, _lib, dev)
     dt = w["dtype"]
-    us = kernels[dom]["us"]
-    if mfma and flops / (MFMA_PEAK_TFLOPS[dt] * 1e12) > nbytes / (HBM_PEAK_GBS * 1e9):
-        achieved, peak, unit, bound = flops / (us * 1e-6) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s", "mfma"
-    else:
-        achieved, peak, unit, bound = nbytes / (us * 1e-6) / 1e9, HBM_PEAK_GBS, "GB/s", "hbm"
-    traffic, traffic_src = read_traffic(a.workload)
-    traffic = traffic.get(dom) if traffic else None
-    roof = {"bound": bound, "kernel": dom, "achieved": round(achieved, 3), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 4),
-            "traffic": round(traffic) if traffic is not None else None,
-            "per_launch": {"bytes": nbytes, "flops": flops, "us": us,
-                           "traffic_source": traffic_src}}
-
     out = {"metric": METRIC, "value": E / (ms * 1e-3), "unit": "edges/s", "n_gpus": 1,
            "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 4),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dt,

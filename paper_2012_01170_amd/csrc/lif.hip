@@ -6,26 +6,30 @@
 // the threshold it is reset and the cell emits an event at the input's time.
 //
 // A cell's potential depends only on the events of its own receptive field, in
-// stream order, so the cells run in parallel, a thread each:
-//   1. the events are sorted by pixel (stable, so each pixel's list keeps
-//      stream order), with their times alongside;
-//   2. each cell merges the lists of its k x k input pixels by event index
-//      (the smallest head first), advancing its potential in float64; a spike
-//      of event i at the cell sets flag[i * slots + slot], slot being the
-//      cell's row-major place among the cells event i reaches;
+// stream order, so the cells run in parallel:
+//   1. each pixel's events are listed, sorted by event index, with their times
+//      alongside (counted, placed, then sorted within each pixel; the count
+//      also clears the spike flags);
+//   2. a wave per cell stages the lists of its k x k input pixels in LDS and
+//      merges them in parallel, each entry finding its place by binary search
+//      in the other lists; the decay factors exp(-(t_s - t_{s-1}) / decay) of
+//      the merged sequence do not depend on the potential and are computed in
+//      parallel too; one lane then runs the recursion v = V e_s + 1/n_s with
+//      its threshold and reset (float64).  A spike of event i at the cell sets
+//      flag[i * slots + slot], slot being the cell's row-major place among the
+//      cells event i reaches.  A cell with more events than the LDS holds runs
+//      the same recursion on one lane, merging the lists from global memory;
 //   3. a scan over the flags gives every spike its place in the output, which
 //      is thereby ordered by input event, then cell row, then cell column (the
 //      sequential emission order), and a last kernel writes the events.
-// The receptive field of cell (ox, oy) is the k x k block of pixels centred on
-// (ox * S, oy * S) (a padded strided convolution: the output grid has
-// ceil(W / S) x ceil(H / S) cells).
 #include "common.hpp"
 
 namespace sbc {
 namespace {
 
-constexpr int kLifThreads = 64;
+constexpr int kLifThreads = 64;  // one wave per cell
 constexpr int kLifMaxKernel = 5;
+constexpr int kLifCap = 1024;    // events of one cell's receptive field held in LDS
 
 struct LifArgs {
     const int32_t *px, *py;
@@ -45,63 +49,87 @@ __device__ __forceinline__ void cell_range(int32_t x, const LifArgs &A, int32_t 
     hi = hi < n_out - 1 ? hi : n_out - 1;
 }
 
-__global__ void lif_key_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
-                               const int32_t *__restrict__ t, int32_t n, int32_t W, int32_t H,
-                               int32_t *__restrict__ keys, uint32_t *status) {
+// Each event's pixel, counted; the atomic's value is the event's provisional
+// place in its pixel's list (sorted by index afterwards).  Raises the
+// out-of-range and unsorted flags.
+__global__ void lif_count_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
+                                 const int32_t *__restrict__ t, int32_t n, int32_t W, int32_t H,
+                                 int32_t slots, int32_t *__restrict__ counts,
+                                 int32_t *__restrict__ keys, int32_t *__restrict__ place,
+                                 int32_t *__restrict__ flags, uint32_t *status) {
     const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
+    for (int32_t s = 0; s < slots; ++s) flags[(int64_t)i * slots + s] = 0;
     const int32_t x = px[i], y = py[i];
     if (i > 0 && t[i] < t[i - 1]) atomicOr(status, (uint32_t)kFlagUnsorted);
     if (x < 0 || x >= W || y < 0 || y >= H) {
         atomicOr(status, (uint32_t)kFlagOutOfRange);
-        keys[i] = W * H;  // behind every pixel, seen by no cell
+        keys[i] = -1;  // seen by no cell
         return;
     }
-    keys[i] = y * W + x;
+    const int32_t p = y * W + x;
+    keys[i] = p;
+    place[i] = atomicAdd(&counts[p], 1);
 }
 
-__global__ void lif_times_kernel(const int32_t *__restrict__ list, const int32_t *__restrict__ t,
-                                 int32_t n, int32_t *__restrict__ list_t) {
-    const int32_t p = blockIdx.x * blockDim.x + threadIdx.x;
-    if (p < n) list_t[p] = t[list[p]];
+// Each listed event to a place of its pixel's list, with its time (the list
+// is put in stream order afterwards).
+__global__ void lif_place_kernel(const int32_t *__restrict__ keys,
+                                 const int32_t *__restrict__ place,
+                                 const int32_t *__restrict__ pix_start,
+                                 const int32_t *__restrict__ t, int32_t n,
+                                 int32_t *__restrict__ unsorted, int32_t *__restrict__ unsorted_t,
+                                 int32_t *__restrict__ seg_of) {
+    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n || keys[i] < 0) return;
+    const int32_t p = keys[i];
+    const int32_t pos = pix_start[p] + place[i];
+    unsorted[pos] = i;
+    unsorted_t[pos] = t[i];
+    seg_of[pos] = p;
 }
 
-// One thread per output cell; K is the kernel size.
+// The receptive field of cell (ox, oy): list q (row-major over the k x k
+// pixels) starts at *start and holds *len events; inc is 1/n of its pixel and
+// slot the cell's place among the cells that pixel reaches.  Off the sensor:
+// an empty list.
+__device__ __forceinline__ void field_list(const LifArgs &A, int32_t ox, int32_t oy, int q,
+                                           int32_t &start, int32_t &len, double &inc,
+                                           int32_t &slot) {
+    const int32_t x = ox * A.S - A.pad + q % A.k, y = oy * A.S - A.pad + q / A.k;
+    start = len = slot = 0;
+    inc = 0.0;
+    if (x < 0 || x >= A.W || y < 0 || y >= A.H) return;
+    const int32_t p = y * A.W + x;
+    start = A.pix_start[p];
+    len = A.pix_start[p + 1] - start;
+    int32_t lx, hx, ly, hy;
+    cell_range(x, A, A.Wo, lx, hx);
+    cell_range(y, A, A.Ho, ly, hy);
+    inc = 1.0 / (double)((hx - lx + 1) * (hy - ly + 1));  // this cell is one of them
+    slot = (oy - ly) * A.nsd + (ox - lx);
+}
+
+// One cell on one thread: a K*K-way merge of the lists from global memory,
+// the earliest head first, advancing the potential at each event.
 template <int K>
-__global__ void __launch_bounds__(kLifThreads) lif_cell_kernel(LifArgs A) {
+__device__ void cell_sequential(const LifArgs &A, int32_t ox, int32_t oy) {
 #pragma clang fp contract(off)
     constexpr int Q = K * K;
     constexpr int32_t kNone = INT32_MAX;
-    const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= A.Wo * A.Ho) return;
-    const int32_t ox = c % A.Wo, oy = c / A.Wo;
-    const int32_t x0 = ox * A.S - A.pad, y0 = oy * A.S - A.pad;
     int32_t pos[Q], end[Q], head[Q], head_t[Q], slot[Q];
     double inc[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
-        const int32_t x = x0 + q % K, y = y0 + q / K;
-        pos[q] = end[q] = 0;
-        slot[q] = 0;
-        inc[q] = 0.0;
-        if (x >= 0 && x < A.W && y >= 0 && y < A.H) {
-            const int32_t p = y * A.W + x;
-            pos[q] = A.pix_start[p];
-            end[q] = A.pix_start[p + 1];
-            int32_t lx, hx, ly, hy;
-            cell_range(x, A, A.Wo, lx, hx);
-            cell_range(y, A, A.Ho, ly, hy);
-            // this cell is among them, so n >= 1
-            inc[q] = 1.0 / (double)((hx - lx + 1) * (hy - ly + 1));
-            slot[q] = (oy - ly) * A.nsd + (ox - lx);
-        }
+        int32_t len;
+        field_list(A, ox, oy, q, pos[q], len, inc[q], slot[q]);
+        end[q] = pos[q] + len;
         head[q] = pos[q] < end[q] ? A.list[pos[q]] : kNone;
         head_t[q] = pos[q] < end[q] ? A.list_t[pos[q]] : 0;
     }
     const int64_t nslots = (int64_t)A.nsd * A.nsd;
     double V = 0.0, T = 0.0;
     for (;;) {
-        // the earliest pending event of the receptive field
         int32_t best = kNone, bt = 0, bs = 0, bq = -1;
         double binc = 0.0;
 #pragma unroll
@@ -114,7 +142,6 @@ __global__ void __launch_bounds__(kLifThreads) lif_cell_kernel(LifArgs A) {
                 bq = q;
             }
         if (best == kNone) break;
-        // advance that list (one load of the next head and its time)
         int32_t np = 0, ne = 0;
 #pragma unroll
         for (int q = 0; q < Q; ++q)
@@ -143,6 +170,143 @@ __global__ void __launch_bounds__(kLifThreads) lif_cell_kernel(LifArgs A) {
     }
 }
 
+// Lane l's value of x, for every lane.
+__device__ __forceinline__ double readlane_f64(double x, int32_t l) {
+    const int32_t lo = __builtin_amdgcn_readlane(__double2loint(x), l);
+    const int32_t hi = __builtin_amdgcn_readlane(__double2hiint(x), l);
+    return __hiloint2double(hi, lo);
+}
+
+// One wave per output cell (block = one wave); K is the kernel size.
+template <int K>
+__global__ void __launch_bounds__(kLifThreads) lif_cell_kernel(LifArgs A) {
+#pragma clang fp contract(off)
+    constexpr int Q = K * K;
+    __shared__ int32_t s_idx[kLifCap];   // the staged lists (list q from off[q])
+    __shared__ int32_t s_t[kLifCap];
+    __shared__ int32_t m_idx[kLifCap];   // the merged sequence: event, time, list
+    __shared__ int32_t m_t[kLifCap];
+    __shared__ uint8_t m_q[kLifCap];
+    __shared__ int32_t s_start[Q], s_len[Q], s_slot[Q];
+    __shared__ double s_inc[Q];
+    const int lane = threadIdx.x;
+    const int32_t c = blockIdx.x;
+    const int32_t ox = c % A.Wo, oy = c / A.Wo;
+    if (lane < Q) {
+        int32_t start, len, slot;
+        double inc;
+        field_list(A, ox, oy, lane, start, len, inc, slot);
+        s_start[lane] = start;
+        s_len[lane] = len;
+        s_slot[lane] = slot;
+        s_inc[lane] = inc;
+    }
+    __syncthreads();
+    // list offsets (every lane keeps them) and the longest list
+    int32_t off[Q + 1], longest = 0;
+    off[0] = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int32_t len = s_len[q];
+        off[q + 1] = off[q] + len;
+        longest = len > longest ? len : longest;
+    }
+    const int32_t L = off[Q];
+    if (L > kLifCap) {  // beyond the LDS staging: one lane, global lists
+        if (lane == 0) cell_sequential<K>(A, ox, oy);
+        return;
+    }
+    // stage the lists: the first 64 events of every list in one round of
+    // independent loads, longer lists after
+    {
+        int32_t vi[Q], vt[Q];
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+            if (lane < off[q + 1] - off[q]) {
+                vi[q] = A.list[s_start[q] + lane];
+                vt[q] = A.list_t[s_start[q] + lane];
+            }
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+            if (lane < off[q + 1] - off[q]) {
+                s_idx[off[q] + lane] = vi[q];
+                s_t[off[q] + lane] = vt[q];
+            }
+        if (longest > kLifThreads)
+            for (int q = 0; q < Q; ++q)
+                for (int32_t j = kLifThreads + lane; j < off[q + 1] - off[q]; j += kLifThreads) {
+                    s_idx[off[q] + j] = A.list[s_start[q] + j];
+                    s_t[off[q] + j] = A.list_t[s_start[q] + j];
+                }
+    }
+    __syncthreads();
+    // merge: an entry's place is its place in its own list plus, for every
+    // other list, the entries there with a smaller event index (binary
+    // searches run in lockstep over the lists, so their reads overlap)
+    const int steps = 32 - __clz(longest);  // halvings that empty the longest range
+    for (int32_t e = lane; e < L; e += kLifThreads) {
+        int q = 0;
+#pragma unroll
+        for (int q2 = 1; q2 < Q; ++q2) q += e >= off[q2] ? 1 : 0;
+        const int32_t idx = s_idx[e];
+        int32_t base[Q], cnt[Q];
+#pragma unroll
+        for (int q2 = 0; q2 < Q; ++q2) {
+            base[q2] = off[q2];
+            cnt[q2] = q2 == q ? 0 : off[q2 + 1] - off[q2];
+        }
+        for (int it = 0; it < steps; ++it)
+#pragma unroll
+            for (int q2 = 0; q2 < Q; ++q2)
+                if (cnt[q2] > 0) {
+                    const int32_t half = cnt[q2] >> 1;
+                    if (s_idx[base[q2] + half] < idx) {
+                        base[q2] += half + 1;
+                        cnt[q2] -= half + 1;
+                    } else {
+                        cnt[q2] = half;
+                    }
+                }
+        int32_t r = 0;
+#pragma unroll
+        for (int q2 = 0; q2 < Q; ++q2) r += base[q2] - off[q2];
+        r += e - off[q];
+        m_idx[r] = idx;  // the merged arrays do not overlap the staged lists
+        m_t[r] = s_t[e];
+        m_q[r] = (uint8_t)q;
+    }
+    __syncthreads();
+    // the recursion, 64 merged entries at a time: lane l computes entry
+    // r0 + l's decay factor (T is the previous event's time, 0 before the
+    // first) and 1/n, then the whole wave runs the 64 steps in lockstep,
+    // reading each step's operands from the owning lane's registers, and the
+    // spikes of the chunk gather in one 64-bit mask
+    const int64_t nslots = (int64_t)A.nsd * A.nsd;
+    double V = 0.0;
+    for (int32_t r0 = 0; r0 < L; r0 += kLifThreads) {
+        const int32_t r = r0 + lane;
+        double ec = 0.0, ic = 0.0;
+        if (r < L) {
+            const double ti = (double)m_t[r];
+            const double T = r > 0 ? (double)m_t[r - 1] : 0.0;
+            ec = exp(-(ti - T) / A.decay);
+            ic = s_inc[m_q[r]];
+        }
+        const int32_t n_l =
+            __builtin_amdgcn_readfirstlane(L - r0 < kLifThreads ? L - r0 : kLifThreads);
+        uint64_t mask = 0;
+        for (int32_t l = 0; l < n_l; ++l) {
+            const double v = V * readlane_f64(ec, l) + readlane_f64(ic, l);
+            // every lane holds the same v: the ballot is all lanes or none
+            const uint64_t b = __ballot(v > A.thresh);
+            V = b ? A.reset : v;
+            mask |= b & (1ull << l);
+        }
+        if (r < L && ((mask >> lane) & 1))
+            A.flags[(int64_t)m_idx[r] * nslots + s_slot[m_q[r]]] = 1;
+    }
+}
+
 // One thread per (event, slot): the spikes, in scan order.
 __global__ void lif_emit_kernel(LifArgs A, const int32_t *__restrict__ flags,
                                 const int32_t *__restrict__ place, const int32_t *__restrict__ t,
@@ -165,10 +329,11 @@ __global__ void lif_emit_kernel(LifArgs A, const int32_t *__restrict__ flags,
 }
 
 struct LifWs {
-    int32_t *keys, *sorted, *list, *list_t, *pix_start, *flags, *place;
-    int64_t *total;
+    int32_t *counts, *keys, *place, *unsorted, *unsorted_t, *seg_of, *list, *list_t, *pix_start,
+        *flags, *fpos;
+    int64_t *total, *total_pix;
     uint32_t *status;
-    void *scan_ws, *sort_ws;
+    void *scan_ws;
 };
 
 int32_t lif_slots(int32_t kernel, int32_t stride) {
@@ -179,17 +344,21 @@ int32_t lif_slots(int32_t kernel, int32_t stride) {
 LifWs carve_lif(void *base, int32_t n, int64_t npix, int64_t nflags, size_t *bytes) {
     Carver cv(base);
     LifWs w;
+    w.counts = cv.take<int32_t>(npix);
     w.keys = cv.take<int32_t>(n);
-    w.sorted = cv.take<int32_t>(n);
+    w.place = cv.take<int32_t>(n);
+    w.unsorted = cv.take<int32_t>(n);
+    w.unsorted_t = cv.take<int32_t>(n);
+    w.seg_of = cv.take<int32_t>(n);
     w.list = cv.take<int32_t>(n);
     w.list_t = cv.take<int32_t>(n);
     w.pix_start = cv.take<int32_t>(npix + 1);
     w.flags = cv.take<int32_t>(nflags);
-    w.place = cv.take<int32_t>(nflags + 1);
+    w.fpos = cv.take<int32_t>(nflags + 1);
     w.total = cv.take<int64_t>(2);
+    w.total_pix = cv.take<int64_t>(2);
     w.status = cv.take<uint32_t>(4);
-    w.scan_ws = cv.take<char>(scan_workspace_bytes(nflags));
-    w.sort_ws = cv.take<char>(radix_sort_workspace_bytes(n));
+    w.scan_ws = cv.take<char>(scan_workspace_bytes(nflags > npix ? nflags : npix));
     if (bytes) *bytes = cv.used;
     return w;
 }
@@ -271,19 +440,22 @@ extern "C" sbc_status sbc_lif_sample_events(const int32_t *px, const int32_t *py
     SBC_TRY(fill_i32(reinterpret_cast<int32_t *>(ws.status), 0, 1, stream));
     if (n > 0) {
         trace_before("lif_sort", stream);
-        hipLaunchKernelGGL(lif_key_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream, px, py, t,
-                           n, width, height, ws.keys, ws.status);
+        const dim3 eg(grid_for(n, 256)), eb(256);
+        SBC_TRY(fill_i32(ws.counts, 0, npix, stream));
+        hipLaunchKernelGGL(lif_count_kernel, eg, eb, 0, stream, px, py, t, n, width, height,
+                           slots, ws.counts, ws.keys, ws.place, ws.flags, ws.status);
         SBC_LAUNCH_CHECK();
-        SBC_TRY(radix_sort_pairs(ws.keys, nullptr, nullptr, n, (int32_t)npix + 1, ws.sorted,
-                                 ws.list, ws.sort_ws, stream));
-        SBC_TRY(segment_bounds(ws.sorted, nullptr, n, (int32_t)npix, ws.pix_start, stream));
-        hipLaunchKernelGGL(lif_times_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream,
-                           ws.list, t, n, ws.list_t);
+        SBC_TRY(exclusive_scan_i32(ws.counts, ws.pix_start, npix, ws.total_pix, ws.scan_ws,
+                                   stream));
+        hipLaunchKernelGGL(lif_place_kernel, eg, eb, 0, stream, ws.keys, ws.place, ws.pix_start,
+                           t, n, ws.unsorted, ws.unsorted_t, ws.seg_of);
         SBC_LAUNCH_CHECK();
-        SBC_TRY(fill_i32(ws.flags, 0, nflags, stream));
+        // each pixel's list in stream order (indices are distinct), times alongside
+        SBC_TRY(segmented_sort_pairs(ws.pix_start, (int32_t)npix, ws.seg_of, n, ws.unsorted,
+                                     ws.unsorted_t, ws.list, ws.list_t, stream));
         trace_after("lif_sort", stream);
         const int64_t cells = (int64_t)A.Wo * A.Ho;
-        const dim3 grid(grid_for(cells, kLifThreads)), block(kLifThreads);
+        const dim3 grid((unsigned)cells), block(kLifThreads);  // a wave per cell
         trace_before("lif_cells", stream);
         switch (kernel) {
             case 1: hipLaunchKernelGGL(lif_cell_kernel<1>, grid, block, 0, stream, A); break;
@@ -295,11 +467,11 @@ extern "C" sbc_status sbc_lif_sample_events(const int32_t *px, const int32_t *py
         SBC_LAUNCH_CHECK();
         trace_after("lif_cells", stream);
     }
-    SBC_TRY(exclusive_scan_i32(ws.flags, ws.place, nflags, total, ws.scan_ws, stream));
+    SBC_TRY(exclusive_scan_i32(ws.flags, ws.fpos, nflags, total, ws.scan_ws, stream));
     if (nflags > 0 && capacity > 0) {
         trace_before("lif_emit", stream);
         hipLaunchKernelGGL(lif_emit_kernel, dim3(grid_for(nflags, 256)), dim3(256), 0, stream, A,
-                           ws.flags, ws.place, t, capacity, out_x, out_y, out_t, out_src);
+                           ws.flags, ws.fpos, t, capacity, out_x, out_y, out_t, out_src);
         SBC_LAUNCH_CHECK();
         trace_after("lif_emit", stream);
     }

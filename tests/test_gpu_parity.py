@@ -63,7 +63,7 @@ SMALL = {
 # (one input channel of features ~N(0,1), so single-channel input gradients
 # whose sums cancel by up to 1e6) is checked as Eq. 9-10 instead
 FULL = [k for k in workloads.WORKLOADS
-        if k not in ("ellipsoids_featureless", "ellipsoids_sampling")]
+        if k not in ("ellipsoids_featureless", "ellipsoids_sampling", "events_300k_lif")]
 ORDERS = ["spmm_first", "gemm_first"]
 
 
@@ -700,7 +700,6 @@ LIF_CASES = {
     "k4s2_even": (42, 4000, 19, 21, 20_000, 4, 2, 1500.0, 1.0, -3.0),
     "k1s2_unreached": (43, 3000, 15, 9, 10_000, 1, 2, 3000.0, 1.5, 0.0),
     "k2s3": (44, 3000, 31, 12, 10_000, 2, 3, 500.0, 0.7, 0.1),
-    "cifar_k3s2_300k": (45, 300_000, 128, 128, 100_000, 3, 2, 4000.0, 1.6, -3.0),
 }
 
 
@@ -731,6 +730,15 @@ def test_lif_bit_exact(case_name):
     assert _lif_check(px, py, t, W, H, k, S, decay, th, rs) > 0
 
 
+def test_lif_full_size_workload():
+    """The benchmarked stream (300k events on 128 x 128, 3 x 3 fields, stride
+    2, the CIFAR10-DVS settings), every output event against the oracle."""
+    print("[lif] events_300k_lif", flush=True)
+    w = workloads.events_300k_lif()
+    assert _lif_check(w["px"], w["py"], w["t"], w["width"], w["height"], w["kernel"],
+                      w["stride"], w["decay"], w["v_thresh"], w["v_reset"]) > 10_000
+
+
 def test_lif_exact_ties_and_bursts():
     """No decay, equal times and thresholds the potentials reach exactly
     (multiples of 1/4 and 1/2): the comparison is strict on both sides.  Also a
@@ -745,6 +753,24 @@ def test_lif_exact_ties_and_bursts():
     _lif_check(px, py, t, 8, 8, 3, 2, 1e12, 1.5, -0.5)
     px, py, t, _ = workloads.bursty_events(rng, 20_000, 40, 30, 40_000)
     _lif_check(px, py, t, 40, 30, 3, 2, 20_000.0, 1.5, -2.0)
+
+
+def test_lif_crowded_cells():
+    """Cells whose receptive field holds more events than the LDS staging (a
+    hot pixel, and a tiny sensor) take the one-lane path; the rest of the grid
+    the wave path; both equal the oracle."""
+    print("[lif] crowded", flush=True)
+    rng = np.random.default_rng(48)
+    n = 12_000
+    px = rng.integers(0, 30, n).astype(np.int32)
+    py = rng.integers(0, 20, n).astype(np.int32)
+    hot = rng.random(n) < 0.25
+    px[hot], py[hot] = 5, 5
+    t = np.sort(rng.integers(0, 60_000, n)).astype(np.int32)
+    _lif_check(px, py, t, 30, 20, 3, 2, 2000.0, 1.5, -3.0)
+    px, py, t, _ = workloads.uniform_events(rng, 20_000, 4, 4, 50_000)
+    _lif_check(px, py, t, 4, 4, 3, 2, 2000.0, 1.5, -3.0)
+    _lif_check(px, py, t, 4, 4, 5, 1, 500.0, 1.2, -1.0)
 
 
 def test_lif_empty_and_capacity():

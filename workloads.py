@@ -299,6 +299,18 @@ def events_300k_decays2():
     return event_stream(n_decays=2)
 
 
+def events_300k_lif():
+    """The next, coarser stream of the 300k-event 128x128 stream by leaky
+    integrate-and-fire: 3x3 receptive fields, stride 2 (a 64x64 grid), decay
+    time 4 ms, threshold 1.6, reset -3 (the CIFAR10-DVS settings of the
+    supplementary's dataset table)."""
+    rng = rng_for(3)
+    px, py, t, _ = uniform_events(rng, 300_000, 128, 128, 100_000)
+    return dict(kind="lif", name="lif300k_128x128", px=px, py=py, t=t, width=128, height=128,
+                kernel=3, stride=2, decay=4000.0, v_thresh=1.6, v_reset=-3.0, n_in=len(t),
+                dtype="f64")
+
+
 WORKLOADS = {
     "sphere_1024": sphere_1024,
     "ellipsoids_inplace": ellipsoids_inplace,
@@ -309,6 +321,7 @@ WORKLOADS = {
     "ellipsoids_featureless": ellipsoids_featureless,
     "events_300k_decays2": events_300k_decays2,
     "ellipsoids_sampling": ellipsoids_sampling,
+    "events_300k_lif": events_300k_lif,
 }
 
 
