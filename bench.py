@@ -78,6 +78,9 @@ def trace_name(kernel):
     if kernel in TRACE_NAME:
         return TRACE_NAME[kernel]
     base = kernel.split("<")[0]
+    if base == "bwd_ws_kernel":  # <M, CI, CO, basis, ...>: basis 16 is the decay derivative
+        args = kernel[len(base) + 1:].split(",")
+        return "decay_fused" if len(args) > 3 and args[3].strip() == "16" else "bwd_fused"
     if base == "featureless_kernel":  # <M, mode, writes Z>
         return "featureless_fwd" if kernel.rstrip(">").endswith("true") else "featureless_rowsum"
     return TRACE_NAME.get(base)
