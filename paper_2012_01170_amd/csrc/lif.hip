@@ -27,9 +27,8 @@
 namespace sbc {
 namespace {
 
-constexpr int kLifThreads = 64;  // one wave per cell
+constexpr int kLifThreads = 64;  // a wave
 constexpr int kLifMaxKernel = 5;
-constexpr int kLifCap = 1024;    // events of one cell's receptive field held in LDS
 
 struct LifArgs {
     const int32_t *px, *py;
@@ -170,141 +169,200 @@ __device__ void cell_sequential(const LifArgs &A, int32_t ox, int32_t oy) {
     }
 }
 
-// Lane l's value of x, for every lane.
-__device__ __forceinline__ double readlane_f64(double x, int32_t l) {
-    const int32_t lo = __builtin_amdgcn_readlane(__double2loint(x), l);
-    const int32_t hi = __builtin_amdgcn_readlane(__double2hiint(x), l);
-    return __hiloint2double(hi, lo);
-}
-
-// One wave per output cell (block = one wave); K is the kernel size.
+// Cells per block (a wave each while staging and merging; their recursions
+// then run side by side on one wave, a lane per cell), and the LDS sizes.
 template <int K>
-__global__ void __launch_bounds__(kLifThreads) lif_cell_kernel(LifArgs A) {
+struct LifTile {
+    static constexpr int kCells = K <= 3 ? 16 : 8;
+    static constexpr int kStage = 512;                // one cell's events, staged
+    static constexpr int kMerged = kCells * 256;      // the block's merged events
+};
+
+template <int K>
+__global__ void __launch_bounds__(LifTile<K>::kCells * 64) lif_cell_kernel(LifArgs A) {
 #pragma clang fp contract(off)
     constexpr int Q = K * K;
-    __shared__ int32_t s_idx[kLifCap];   // the staged lists (list q from off[q])
-    __shared__ int32_t s_t[kLifCap];
-    __shared__ int32_t m_idx[kLifCap];   // the merged sequence: event, time, list
-    __shared__ int32_t m_t[kLifCap];
-    __shared__ uint8_t m_q[kLifCap];
-    __shared__ int32_t s_start[Q], s_len[Q], s_slot[Q];
-    __shared__ double s_inc[Q];
-    const int lane = threadIdx.x;
-    const int32_t c = blockIdx.x;
-    const int32_t ox = c % A.Wo, oy = c / A.Wo;
-    if (lane < Q) {
+    constexpr int C = LifTile<K>::kCells, S = LifTile<K>::kStage, MG = LifTile<K>::kMerged;
+    __shared__ int32_t s_idx[C][S];   // each wave's staged lists (list q from off[q])
+    __shared__ int32_t s_t[C][S];
+    __shared__ int32_t m_idx[MG];     // merged sequences, cell w's from s_moff[w]
+    __shared__ int32_t m_t[MG];
+    __shared__ uint8_t m_q[MG];
+    __shared__ double m_e[MG];        // decay factor of each merged event
+    __shared__ int32_t s_start[C][Q], s_len[C][Q], s_slot[C][Q], s_L[C], s_moff[C];
+    __shared__ double s_inc[C][Q];
+    const int w = threadIdx.x / kLifThreads, lane = threadIdx.x % kLifThreads;
+    const int64_t cells = (int64_t)A.Wo * A.Ho;
+    const int64_t cell = (int64_t)blockIdx.x * C + w;
+    const bool valid = cell < cells;
+    const int32_t ox = valid ? (int32_t)(cell % A.Wo) : 0, oy = valid ? (int32_t)(cell / A.Wo) : 0;
+    if (valid && lane < Q) {
         int32_t start, len, slot;
         double inc;
         field_list(A, ox, oy, lane, start, len, inc, slot);
-        s_start[lane] = start;
-        s_len[lane] = len;
-        s_slot[lane] = slot;
-        s_inc[lane] = inc;
+        s_start[w][lane] = start;
+        s_len[w][lane] = len;
+        s_slot[w][lane] = slot;
+        s_inc[w][lane] = inc;
     }
     __syncthreads();
-    // list offsets (every lane keeps them) and the longest list
+    // list offsets (every lane of the wave keeps them) and the longest list
     int32_t off[Q + 1], longest = 0;
     off[0] = 0;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
-        const int32_t len = s_len[q];
+        const int32_t len = valid ? s_len[w][q] : 0;
         off[q + 1] = off[q] + len;
         longest = len > longest ? len : longest;
     }
     const int32_t L = off[Q];
-    if (L > kLifCap) {  // beyond the LDS staging: one lane, global lists
-        if (lane == 0) cell_sequential<K>(A, ox, oy);
-        return;
+    if (lane == 0) s_L[w] = L;
+    __syncthreads();
+    if (threadIdx.x == 0) {  // merged space: cells that fit, in order; the rest run alone
+        int32_t o = 0;
+        for (int c = 0; c < C; ++c) {
+            const bool fits = s_L[c] <= S && o + s_L[c] <= MG;
+            s_moff[c] = fits ? o : -1;
+            o += fits ? s_L[c] : 0;
+        }
     }
-    // stage the lists: the first 64 events of every list in one round of
-    // independent loads, longer lists after
-    {
+    __syncthreads();
+    const int32_t mo = s_moff[w];
+    const bool staged = valid && mo >= 0;
+    if (staged) {
+        // stage the lists: the first 64 events of every list in one round of
+        // independent loads, longer lists after
         int32_t vi[Q], vt[Q];
 #pragma unroll
         for (int q = 0; q < Q; ++q)
             if (lane < off[q + 1] - off[q]) {
-                vi[q] = A.list[s_start[q] + lane];
-                vt[q] = A.list_t[s_start[q] + lane];
+                vi[q] = A.list[s_start[w][q] + lane];
+                vt[q] = A.list_t[s_start[w][q] + lane];
             }
 #pragma unroll
         for (int q = 0; q < Q; ++q)
             if (lane < off[q + 1] - off[q]) {
-                s_idx[off[q] + lane] = vi[q];
-                s_t[off[q] + lane] = vt[q];
+                s_idx[w][off[q] + lane] = vi[q];
+                s_t[w][off[q] + lane] = vt[q];
             }
         if (longest > kLifThreads)
             for (int q = 0; q < Q; ++q)
                 for (int32_t j = kLifThreads + lane; j < off[q + 1] - off[q]; j += kLifThreads) {
-                    s_idx[off[q] + j] = A.list[s_start[q] + j];
-                    s_t[off[q] + j] = A.list_t[s_start[q] + j];
+                    s_idx[w][off[q] + j] = A.list[s_start[w][q] + j];
+                    s_t[w][off[q] + j] = A.list_t[s_start[w][q] + j];
                 }
     }
     __syncthreads();
-    // merge: an entry's place is its place in its own list plus, for every
-    // other list, the entries there with a smaller event index (binary
-    // searches run in lockstep over the lists, so their reads overlap)
-    const int steps = 32 - __clz(longest);  // halvings that empty the longest range
-    for (int32_t e = lane; e < L; e += kLifThreads) {
-        int q = 0;
+    if (staged) {
+        // merge: an entry's place is its place in its own list plus, for every
+        // other list, the entries there with a smaller event index (binary
+        // searches run in lockstep over the lists, so their reads overlap)
+        const int steps = 32 - __clz(longest);  // halvings that empty the longest range
+        const int32_t *si = s_idx[w];
+        for (int32_t e = lane; e < L; e += kLifThreads) {
+            int q = 0;
 #pragma unroll
-        for (int q2 = 1; q2 < Q; ++q2) q += e >= off[q2] ? 1 : 0;
-        const int32_t idx = s_idx[e];
-        int32_t base[Q], cnt[Q];
+            for (int q2 = 1; q2 < Q; ++q2) q += e >= off[q2] ? 1 : 0;
+            const int32_t idx = si[e];
+            int32_t base[Q], cnt[Q];
 #pragma unroll
-        for (int q2 = 0; q2 < Q; ++q2) {
-            base[q2] = off[q2];
-            cnt[q2] = q2 == q ? 0 : off[q2 + 1] - off[q2];
-        }
-        for (int it = 0; it < steps; ++it)
+            for (int q2 = 0; q2 < Q; ++q2) {
+                base[q2] = off[q2];
+                cnt[q2] = q2 == q ? 0 : off[q2 + 1] - off[q2];
+            }
+            for (int it = 0; it < steps; ++it)
 #pragma unroll
-            for (int q2 = 0; q2 < Q; ++q2)
-                if (cnt[q2] > 0) {
-                    const int32_t half = cnt[q2] >> 1;
-                    if (s_idx[base[q2] + half] < idx) {
-                        base[q2] += half + 1;
-                        cnt[q2] -= half + 1;
-                    } else {
-                        cnt[q2] = half;
+                for (int q2 = 0; q2 < Q; ++q2)
+                    if (cnt[q2] > 0) {
+                        const int32_t half = cnt[q2] >> 1;
+                        if (si[base[q2] + half] < idx) {
+                            base[q2] += half + 1;
+                            cnt[q2] -= half + 1;
+                        } else {
+                            cnt[q2] = half;
+                        }
                     }
-                }
-        int32_t r = 0;
+            int32_t r = e - off[q];
 #pragma unroll
-        for (int q2 = 0; q2 < Q; ++q2) r += base[q2] - off[q2];
-        r += e - off[q];
-        m_idx[r] = idx;  // the merged arrays do not overlap the staged lists
-        m_t[r] = s_t[e];
-        m_q[r] = (uint8_t)q;
+            for (int q2 = 0; q2 < Q; ++q2) r += base[q2] - off[q2];
+            m_idx[mo + r] = idx;
+            m_t[mo + r] = s_t[w][e];
+            m_q[mo + r] = (uint8_t)q;
+        }
     }
     __syncthreads();
-    // the recursion, 64 merged entries at a time: lane l computes entry
-    // r0 + l's decay factor (T is the previous event's time, 0 before the
-    // first) and 1/n, then the whole wave runs the 64 steps in lockstep,
-    // reading each step's operands from the owning lane's registers, and the
-    // spikes of the chunk gather in one 64-bit mask
-    const int64_t nslots = (int64_t)A.nsd * A.nsd;
-    double V = 0.0;
-    for (int32_t r0 = 0; r0 < L; r0 += kLifThreads) {
-        const int32_t r = r0 + lane;
-        double ec = 0.0, ic = 0.0;
-        if (r < L) {
-            const double ti = (double)m_t[r];
-            const double T = r > 0 ? (double)m_t[r - 1] : 0.0;
-            ec = exp(-(ti - T) / A.decay);
-            ic = s_inc[m_q[r]];
+    if (staged)  // decay factors: T is the previous event's time, 0 before the first
+        for (int32_t r = lane; r < L; r += kLifThreads) {
+            const double ti = (double)m_t[mo + r];
+            const double T = r > 0 ? (double)m_t[mo + r - 1] : 0.0;
+            m_e[mo + r] = exp(-(ti - T) / A.decay);
         }
-        const int32_t n_l =
-            __builtin_amdgcn_readfirstlane(L - r0 < kLifThreads ? L - r0 : kLifThreads);
-        uint64_t mask = 0;
-        for (int32_t l = 0; l < n_l; ++l) {
-            const double v = V * readlane_f64(ec, l) + readlane_f64(ic, l);
-            // every lane holds the same v: the ballot is all lanes or none
-            const uint64_t b = __ballot(v > A.thresh);
-            V = b ? A.reset : v;
-            mask |= b & (1ull << l);
+    __syncthreads();
+    if (w == 0) {
+        // the recursions of the block's staged cells, a lane each; a spike
+        // marks its merged entry (bit 7 of m_q) and the flags are written
+        // after.  Operands come a chunk ahead: m_e and m_q of chunk c+1 are
+        // read while chunk c runs, and its 1/n from them one chunk later;
+        // reads past a cell's end are clamped into the array and unused.
+        const int g = lane;
+        const bool mine = g < C && (int64_t)blockIdx.x * C + g < cells && s_moff[g] >= 0;
+        const int32_t go = mine ? s_moff[g] : 0, gL = mine ? s_L[g] : 0;
+        const int gg = g < C ? g : 0;
+        constexpr int kC = 8;
+        auto at = [&](int32_t r) { return go + r < MG ? go + r : MG - 1; };
+        auto inc_of = [&](int q) { return s_inc[gg][q < Q ? q : 0]; };
+        double e_c[kC], i_c[kC], e_n[kC];
+        int q_n[kC];
+#pragma unroll
+        for (int u = 0; u < kC; ++u) {
+            e_c[u] = m_e[at(u)];
+            i_c[u] = inc_of(m_q[at(u)]);
+            q_n[u] = m_q[at(kC + u)];
+            e_n[u] = m_e[at(kC + u)];
         }
-        if (r < L && ((mask >> lane) & 1))
-            A.flags[(int64_t)m_idx[r] * nslots + s_slot[m_q[r]]] = 1;
+        double V = 0.0;
+        for (int32_t r0 = 0; r0 < gL; r0 += kC) {
+            double i_n[kC], e_nn[kC];
+            int q_nn[kC];
+#pragma unroll
+            for (int u = 0; u < kC; ++u) {
+                i_n[u] = inc_of(q_n[u]);
+                q_nn[u] = m_q[at(r0 + 2 * kC + u)];
+                e_nn[u] = m_e[at(r0 + 2 * kC + u)];
+            }
+#pragma unroll
+            for (int u = 0; u < kC; ++u) {
+                if (r0 + u < gL) {
+                    const double v = V * e_c[u] + i_c[u];
+                    const bool fire = v > A.thresh;
+                    V = fire ? A.reset : v;
+                    if (fire) m_q[go + r0 + u] |= 0x80;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kC; ++u) {
+                e_c[u] = e_n[u];
+                i_c[u] = i_n[u];
+                e_n[u] = e_nn[u];
+                q_n[u] = q_nn[u];
+            }
+        }
+    } else if (lane == 0) {
+        // cells beyond the staging run alone, one lane each, on the other waves
+        for (int g = w - 1; g < C; g += C - 1) {
+            const int64_t c = (int64_t)blockIdx.x * C + g;
+            if (c < cells && s_moff[g] < 0)
+                cell_sequential<K>(A, (int32_t)(c % A.Wo), (int32_t)(c / A.Wo));
+        }
     }
+    __syncthreads();
+    const int64_t nslots = (int64_t)A.nsd * A.nsd;
+    if (staged)  // the spikes of this wave's cell
+        for (int32_t r = lane; r < L; r += kLifThreads) {
+            const int q = m_q[mo + r];
+            if (q & 0x80)
+                A.flags[(int64_t)m_idx[mo + r] * nslots + s_slot[w][q & 0x7f]] = 1;
+        }
 }
 
 // One thread per (event, slot): the spikes, in scan order.
@@ -455,15 +513,18 @@ extern "C" sbc_status sbc_lif_sample_events(const int32_t *px, const int32_t *py
                                      ws.unsorted_t, ws.list, ws.list_t, stream));
         trace_after("lif_sort", stream);
         const int64_t cells = (int64_t)A.Wo * A.Ho;
-        const dim3 grid((unsigned)cells), block(kLifThreads);  // a wave per cell
         trace_before("lif_cells", stream);
+#define SBC_LIF_CELLS(KK)                                                                      \
+    hipLaunchKernelGGL(lif_cell_kernel<KK>, dim3(grid_for(cells, LifTile<KK>::kCells)),      \
+                       dim3(LifTile<KK>::kCells * kLifThreads), 0, stream, A)
         switch (kernel) {
-            case 1: hipLaunchKernelGGL(lif_cell_kernel<1>, grid, block, 0, stream, A); break;
-            case 2: hipLaunchKernelGGL(lif_cell_kernel<2>, grid, block, 0, stream, A); break;
-            case 3: hipLaunchKernelGGL(lif_cell_kernel<3>, grid, block, 0, stream, A); break;
-            case 4: hipLaunchKernelGGL(lif_cell_kernel<4>, grid, block, 0, stream, A); break;
-            default: hipLaunchKernelGGL(lif_cell_kernel<5>, grid, block, 0, stream, A); break;
+            case 1: SBC_LIF_CELLS(1); break;
+            case 2: SBC_LIF_CELLS(2); break;
+            case 3: SBC_LIF_CELLS(3); break;
+            case 4: SBC_LIF_CELLS(4); break;
+            default: SBC_LIF_CELLS(5); break;
         }
+#undef SBC_LIF_CELLS
         SBC_LAUNCH_CHECK();
         trace_after("lif_cells", stream);
     }
