@@ -142,3 +142,32 @@ def decay_backward(row_ptr, col_idx, v_deriv, F, W, dY):
         fw = Fd[cols[nz]] @ Wd[m]                      # [n_e, C_out]
         out[m] = np.sum(vd[nz, m] * np.einsum("ij,ij->i", fw, dYd[rows[nz]]))
     return out
+
+
+def deployment_stream(px, py, t, F, W, width, height, tau, z=None, last=None):
+    """The event convolution's deployment form (Section 3.2, Eq. 13-15), with
+    one decay rate 1/tau for every offset: each pixel x keeps z_x, the decayed
+    sum of the features of its events, and tau_x, the time of its last update
+    (both 0 at the start).  An event (x, t) with features f first reads its
+    output, sum over the 8 offsets u of exp(-(t - tau_q) / tau) z_q W_m(u) with
+    q = x - u on the sensor (the centre has no function), then updates its own
+    pixel: z_x <- f + exp(-(t - tau_x) / tau) z_x, tau_x <- t.  Events in
+    stream order, float64.  z [H, W, C_in] and last [H, W] carry the state
+    between calls (a stream fed in pieces); returns (Y, z, last)."""
+    from .basis import event_offset_index
+    C_in, C_out = W.shape[1], W.shape[2]
+    z = np.zeros((height, width, C_in)) if z is None else np.array(z, dtype=np.float64)
+    last = np.zeros((height, width)) if last is None else np.array(last, dtype=np.float64)
+    Y = np.zeros((len(t), C_out))
+    for i in range(len(t)):
+        x, y, ti = int(px[i]), int(py[i]), float(t[i])
+        for uy in (-1, 0, 1):
+            for ux in (-1, 0, 1):
+                m = int(event_offset_index(ux, uy))
+                qx, qy = x - ux, y - uy
+                if m < 0 or not (0 <= qx < width and 0 <= qy < height):
+                    continue
+                Y[i] += np.exp(-(ti - last[qy, qx]) / tau) * z[qy, qx] @ W[m]
+        z[y, x] = F[i] + np.exp(-(ti - last[y, x]) / tau) * z[y, x]
+        last[y, x] = ti
+    return Y, z, last

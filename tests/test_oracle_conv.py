@@ -277,24 +277,33 @@ def test_event_conv_equals_deployment_recursion():
     rp, ci, v = _events_problem(w)
     F, W = w["F"].astype(np.float64), w["W"].astype(np.float64)
     Y = oracle.conv.forward(rp, ci, v, F, W)
-    tau = w["tau"]
-    z = np.zeros((w["height"], w["width"], w["C_in"]))
-    last = np.zeros((w["height"], w["width"]))
-    Y_ema = np.zeros_like(Y)
-    for i in range(w["n_in"]):
-        x, y, t = int(w["px"][i]), int(w["py"][i]), float(w["t"][i])
-        out = np.zeros(w["C_out"])
-        for uy in (-1, 0, 1):
-            for ux in (-1, 0, 1):
-                m = int(event_offset_index(ux, uy))
-                qx, qy = x - ux, y - uy
-                if m < 0 or not (0 <= qx < w["width"] and 0 <= qy < w["height"]):
-                    continue
-                out += np.exp(-(t - last[qy, qx]) / tau) * z[qy, qx] @ W[m]
-        Y_ema[i] = out
-        z[y, x] = F[i] + np.exp(-(t - last[y, x]) / tau) * z[y, x]
-        last[y, x] = t
+    Y_ema, _, _ = oracle.conv.deployment_stream(w["px"], w["py"], w["t"], F, W, w["width"],
+                                                w["height"], w["tau"])
     np.testing.assert_allclose(Y, Y_ema, rtol=1e-11, atol=1e-11)
+
+
+def test_deployment_stream_in_pieces():
+    """Feeding the stream in pieces, carrying (z, last), gives the outputs and
+    final state of one pass; a lone event reads a zero state; the state of a
+    pixel with events at t1 < t2 only is f2 + exp(-(t2 - t1)/tau) f1."""
+    w = workloads.small_events(seed=7, n=900, width=7, height=6, duration_us=5000, c=4)
+    F, W = w["F"].astype(np.float64), w["W"].astype(np.float64)
+    args = (w["width"], w["height"], w["tau"])
+    Y, z, last = oracle.conv.deployment_stream(w["px"], w["py"], w["t"], F, W, *args)
+    Ys, zs, ls = [], None, None
+    for a, b in [(0, 1), (1, 300), (300, 301), (301, 900)]:
+        Yp, zs, ls = oracle.conv.deployment_stream(w["px"][a:b], w["py"][a:b], w["t"][a:b],
+                                                   F[a:b], W, *args, z=zs, last=ls)
+        Ys.append(Yp)
+    np.testing.assert_allclose(np.concatenate(Ys), Y, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(zs, z, rtol=1e-13, atol=1e-13)
+    assert np.array_equal(ls, last)
+    assert np.all(Y[0] == 0)
+    px, py, t = np.array([3, 3]), np.array([2, 2]), np.array([100, 250])
+    f = np.array([[1.0, 2.0], [0.5, -1.0]])
+    _, z2, l2 = oracle.conv.deployment_stream(px, py, t, f, np.zeros((8, 2, 1)), 5, 4, 100.0)
+    np.testing.assert_allclose(z2[2, 3], f[1] + np.exp(-1.5) * f[0], rtol=1e-15)
+    assert l2[2, 3] == 250 and np.count_nonzero(l2) == 1
 
 
 # ---------------------------------------------------------------- featureless convolution
