@@ -58,6 +58,9 @@ DESCRIPTIONS = {
     "ellipsoids_sampling": "32 clouds x 1024 points on ellipsoid surfaces; uncapped in-place "
                            "ball r 0.1, then rejection sampling and approximate farthest points "
                            "up to 256 per cloud",
+    "events_stream": "300k events, 128x128 pixels, 100 ms uniform, through the deployment form "
+                     "(per-pixel decayed sums, Eq. 13-15) in batches of 4096; tau 10 ms; "
+                     "32 -> 32 channels fp32",
     "events_300k_lif": "300k events, 128x128 pixels, 100 ms uniform -> the 64x64 stream by "
                        "leaky integrate-and-fire: 3x3 fields, stride 2, decay 4 ms, threshold "
                        "1.6, reset -3; float64 potentials",
@@ -70,7 +73,8 @@ PROFILES = os.path.join(ROOT, "profiles")
 TRACE_NAME = {"bwd_ws_kernel": "bwd_fused", "fwd_fused_kernel": "fwd_fused",
               "fwd_reg_kernel": "fwd_fused", "dw_reduce_kernel": "bwd_dw_reduce",
               "sample_kernel<true>": "sample", "sample_kernel<false>": "sample_count",
-              "lif_cell_kernel": "lif_cells", "lif_emit_kernel": "lif_emit"}
+              "lif_cell_kernel": "lif_cells", "lif_emit_kernel": "lif_emit",
+              "stream_gather_kernel": "stream_gather", "stream_update_kernel": "stream_update"}
 
 
 def trace_name(kernel):
@@ -258,6 +262,20 @@ def lif_table(n, npix, slots, spikes):
     }
 
 
+def stream_table(B, npix, C, P):
+    """Kernels of one batch of the deployment form (each runs once per batch):
+    name -> (launches per batch, algorithmic bytes, flops, MFMA)."""
+    lists = 12 * B + 8 * B + 4 * (npix + 1)
+    return {
+        "stream_lists": (1, lists, 0, False),
+        "stream_gather": (1, lists + 4 * npix + 4 * npix * C + 4 * B * C + 4 * B * 8 * C, 0,
+                          False),
+        "stream_gemm": (1, 4 * B * 8 * C + 4 * 8 * C * P + 4 * B * P, 2 * B * 8 * C * P, True),
+        "stream_update": (1, 4 * (npix + 1) + 8 * B + 4 * B * C + 8 * npix * C + 8 * npix, 0,
+                          False),
+    }
+
+
 def featureless_table(n_in, n_out, E, M, P):
     """Kernels of one featureless step (search, Z = G~ Phi, dPhi = G~^T dZ):
     name -> (launches, algorithmic bytes, flops, on MFMA)."""
@@ -345,6 +363,15 @@ def cpu_baseline(w, reps):
         blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # threadpoolctl missing: report the OpenMP count only
         blas = 1
+    if w["kind"] == "stream":
+        t0 = time.perf_counter()
+        oracle.conv.deployment_stream(w["px"], w["py"], w["t"], w["F"].astype("float64"),
+                                      w["W"].astype("float64"), w["width"], w["height"],
+                                      w["tau"])
+        sec = time.perf_counter() - t0
+        return {"value": w["n_in"] / sec, "unit": "events/s", "cores": 1, "kind": "oracle",
+                "sample": f"whole stream ({w['n_in']} events) through the per-event recursion "
+                          f"in float64, one pass of {sec:.2f} s"}
     if w["kind"] == "lif":
         times = []
         for _ in range(reps):
@@ -526,6 +553,40 @@ def lif_main(a, w, T, torch, sbc, _lib, dev):
     return 0
 
 
+def stream_main(a, w, T, torch, sbc, _lib, dev):
+    """One step: the whole input stream (resident in HBM) through the
+    deployment form in batches, the state starting from zero; the value is
+    input events per second."""
+    px, py, tt, F, W = T(w["px"]), T(w["py"]), T(w["t"]), T(w["F"]), T(w["W"])
+    n, B, C, P = w["n_in"], w["batch"], w["C_in"], w["C_out"]
+    st = sbc.EventStream(w["width"], w["height"], C, w["tau"], device=dev)
+
+    def step():
+        st.z.zero_()
+        st.z_time.zero_()
+        return [st.step(px[a0:a0 + B], py[a0:a0 + B], tt[a0:a0 + B], F[a0:a0 + B], W)
+                for a0 in range(0, n, B)]
+
+    batches = (n + B - 1) // B
+    table = {k: (batches, b, f, m) for k, (_, b, f, m) in
+             stream_table(B, w["width"] * w["height"], C, P).items()}
+    ms, eager_ms, wall, kernels, roof = measure(a, w, table, step, torch, _lib, dev)
+    out = {"metric": "deployment-form stream throughput (input events per second)",
+           "value": n / (ms * 1e-3), "unit": "events/s", "n_gpus": 1, "steps": a.steps,
+           "warmup": a.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": w["dtype"],
+           "data": "synthetic (seeded generators; inputs resident in HBM)",
+           "config": {"workload": f"{a.workload}: {DESCRIPTIONS[a.workload]}", "n_in": n,
+                      "batch": B, "batches": batches, "C_in": C, "C_out": P,
+                      "timing": "eager steps" if a.no_graph else "HIP graph replays of the captured step",
+                      "eager_ms_per_step": round(eager_ms, 4), "wall_s": round(wall, 3)},
+           "roofline": roof, "kernels": kernels}
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, a.cpu_reps)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -574,6 +635,8 @@ def main(argv=None):
     T = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
     if w["kind"] == "lif":
         return lif_main(a, w, T, torch, sbc, _lib, dev)
+    if w["kind"] == "stream":
+        return stream_main(a, w, T, torch, sbc, _lib, dev)
     if w["dtype"] == "bf16":
         feat = lambda k: T(w[k + "_bits"].view(np.int16)).view(torch.bfloat16)
         sf = 2

@@ -442,6 +442,40 @@ sbc_status sbc_lif_sample_events(const int32_t *px, const int32_t *py, const int
                                  hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * 9. The event convolution's deployment form (Section 3.2, Eq. 13-15), for a
+ * stream fed in batches, with the fixed decay of SBC_BASIS_EVENT8 (rate 1/tau
+ * for every offset).
+ *
+ * The caller keeps the state: z [height * width, C_in] float32 and z_time
+ * [height * width] int32, pixel y * width + x, both zero before the stream's
+ * first batch (the paper's initial state).  For each event i of the batch, in
+ * stream order, the output is read before the event's own update:
+ *   Y[i] = sum over the 8 offsets u (the 3 x 3 block without its centre, basis
+ *          index m(u) as in SBC_BASIS_EVENT8) of
+ *          exp(-(t_i - z_time[q]) / tau) z[q] W[m(u)],  q = (px_i - ux, py_i - uy)
+ *          on the sensor,
+ * then z[x_i] = F[i] + exp(-(t_i - z_time[x_i]) / tau) z[x_i], z_time[x_i] = t_i.
+ * The batch is computed in parallel with the recursion's value (decays of
+ * earlier events in the batch compose with those of the state); sums and
+ * decay factors are float64, z and Y float32.  Unlike the training form there
+ * is no window: every earlier event counts, decayed.
+ *   px, py, t  [n] int32 device: pixels on the sensor, times non-decreasing and
+ *              not before the state's (not checked: no synchronisation; an
+ *              event off the sensor reads its neighbours and updates no pixel)
+ *   F          [n, C_in] float32 device; W [8, C_in, C_out] float32 device
+ *   Y          [n, C_out] float32 device, output
+ * The call never synchronises and allocates nothing, so a stream step can be
+ * captured in a graph.
+ * ------------------------------------------------------------------------ */
+size_t sbc_event_stream_workspace_size(int32_t n, int32_t width, int32_t height, int32_t C_in,
+                                       int32_t C_out);
+sbc_status sbc_event_stream_step(const int32_t *px, const int32_t *py, const int32_t *t,
+                                 const float *F, int32_t n, int32_t width, int32_t height,
+                                 float tau, const float *W, int32_t C_in, int32_t C_out,
+                                 float *z, int32_t *z_time, float *Y, void *workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Tracing, for measurement tools.  After sbc_trace_kernel(name, start, stop)
  * every launch of the kernel called `name` made by the calling thread records
  * `start` immediately before and `stop` immediately after itself on its

@@ -32,6 +32,7 @@ EXPORTS = [
     "sbc_featureless_backward", "sbc_decay_gradient_workspace_size", "sbc_conv_decay_gradient",
     "sbc_sampling_workspace_size", "sbc_sample_points",
     "sbc_lif_workspace_size", "sbc_lif_sample_events",
+    "sbc_event_stream_workspace_size", "sbc_event_stream_step",
 ]
 
 
@@ -96,6 +97,9 @@ _SIGS = {
                                              ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                              _vp, _vp, _vp, _vp, _i64, _vp, _i64_p, _vp, _sz,
                                              _vp]),
+    "sbc_event_stream_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32]),
+    "sbc_event_stream_step": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _f32, _vp,
+                                             _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sbc_decay_gradient_workspace_size": (_sz, [_i32, _i64, _i32, _i32, _i32, ctypes.c_int]),
     "sbc_conv_decay_gradient": (ctypes.c_int, [_csr_p, _csc_p, _geo_p, _i32, _vp, _vp, _vp,
                                                ctypes.c_int, _i32, _i32, _vp, _vp, _sz, _vp]),

@@ -16,7 +16,8 @@ const char *kKernelNames =
     "fwd_spmm,fwd_gemm,fwd_gemm_h,fwd_spmm_contract,bwd_spmm,bwd_gemm_dw,bwd_gemm_dg,"
     "bwd_spmm_t,bwd_spmm_t_expand,bwd_gemm_df,bwd_gemm_dw_t,fwd_fused,bwd_fused,bwd_dw_reduce,"
     "featureless_fwd,featureless_rowsum,featureless_dphi,decay_basis,decay_spmm,decay_gemm,"
-    "decay_dot,decay_fused,decay_dw_reduce,sample_count,sample,lif_sort,lif_cells,lif_emit";
+    "decay_dot,decay_fused,decay_dw_reduce,sample_count,sample,lif_sort,lif_cells,lif_emit,stream_lists,stream_gather,stream_gemm,"
+    "stream_update";
 }  // namespace
 
 void trace_before(const char *name, hipStream_t stream) {

@@ -23,6 +23,7 @@
 //      is thereby ordered by input event, then cell row, then cell column (the
 //      sequential emission order), and a last kernel writes the events.
 #include "common.hpp"
+#include "pixel_lists.hpp"
 
 namespace sbc {
 namespace {
@@ -46,46 +47,6 @@ __device__ __forceinline__ void cell_range(int32_t x, const LifArgs &A, int32_t 
     lo = a <= 0 ? 0 : (a + A.S - 1) / A.S;
     hi = (x + A.pad) / A.S;
     hi = hi < n_out - 1 ? hi : n_out - 1;
-}
-
-// Each event's pixel, counted; the atomic's value is the event's provisional
-// place in its pixel's list (sorted by index afterwards).  Raises the
-// out-of-range and unsorted flags.
-__global__ void lif_count_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
-                                 const int32_t *__restrict__ t, int32_t n, int32_t W, int32_t H,
-                                 int32_t slots, int32_t *__restrict__ counts,
-                                 int32_t *__restrict__ keys, int32_t *__restrict__ place,
-                                 int32_t *__restrict__ flags, uint32_t *status) {
-    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    for (int32_t s = 0; s < slots; ++s) flags[(int64_t)i * slots + s] = 0;
-    const int32_t x = px[i], y = py[i];
-    if (i > 0 && t[i] < t[i - 1]) atomicOr(status, (uint32_t)kFlagUnsorted);
-    if (x < 0 || x >= W || y < 0 || y >= H) {
-        atomicOr(status, (uint32_t)kFlagOutOfRange);
-        keys[i] = -1;  // seen by no cell
-        return;
-    }
-    const int32_t p = y * W + x;
-    keys[i] = p;
-    place[i] = atomicAdd(&counts[p], 1);
-}
-
-// Each listed event to a place of its pixel's list, with its time (the list
-// is put in stream order afterwards).
-__global__ void lif_place_kernel(const int32_t *__restrict__ keys,
-                                 const int32_t *__restrict__ place,
-                                 const int32_t *__restrict__ pix_start,
-                                 const int32_t *__restrict__ t, int32_t n,
-                                 int32_t *__restrict__ unsorted, int32_t *__restrict__ unsorted_t,
-                                 int32_t *__restrict__ seg_of) {
-    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n || keys[i] < 0) return;
-    const int32_t p = keys[i];
-    const int32_t pos = pix_start[p] + place[i];
-    unsorted[pos] = i;
-    unsorted_t[pos] = t[i];
-    seg_of[pos] = p;
 }
 
 // The receptive field of cell (ox, oy): list q (row-major over the k x k
@@ -387,9 +348,9 @@ __global__ void lif_emit_kernel(LifArgs A, const int32_t *__restrict__ flags,
 }
 
 struct LifWs {
-    int32_t *counts, *keys, *place, *unsorted, *unsorted_t, *seg_of, *list, *list_t, *pix_start,
-        *flags, *fpos;
-    int64_t *total, *total_pix;
+    PixelLists pl;
+    int32_t *flags, *fpos;
+    int64_t *total;
     uint32_t *status;
     void *scan_ws;
 };
@@ -402,21 +363,12 @@ int32_t lif_slots(int32_t kernel, int32_t stride) {
 LifWs carve_lif(void *base, int32_t n, int64_t npix, int64_t nflags, size_t *bytes) {
     Carver cv(base);
     LifWs w;
-    w.counts = cv.take<int32_t>(npix);
-    w.keys = cv.take<int32_t>(n);
-    w.place = cv.take<int32_t>(n);
-    w.unsorted = cv.take<int32_t>(n);
-    w.unsorted_t = cv.take<int32_t>(n);
-    w.seg_of = cv.take<int32_t>(n);
-    w.list = cv.take<int32_t>(n);
-    w.list_t = cv.take<int32_t>(n);
-    w.pix_start = cv.take<int32_t>(npix + 1);
+    w.pl = carve_pixel_lists(cv, n, npix);
     w.flags = cv.take<int32_t>(nflags);
     w.fpos = cv.take<int32_t>(nflags + 1);
     w.total = cv.take<int64_t>(2);
-    w.total_pix = cv.take<int64_t>(2);
     w.status = cv.take<uint32_t>(4);
-    w.scan_ws = cv.take<char>(scan_workspace_bytes(nflags > npix ? nflags : npix));
+    w.scan_ws = cv.take<char>(scan_workspace_bytes(nflags));
     if (bytes) *bytes = cv.used;
     return w;
 }
@@ -489,28 +441,17 @@ extern "C" sbc_status sbc_lif_sample_events(const int32_t *px, const int32_t *py
     A.decay = decay;
     A.thresh = v_thresh;
     A.reset = v_reset;
-    A.pix_start = ws.pix_start;
-    A.list = ws.list;
-    A.list_t = ws.list_t;
+    A.pix_start = ws.pl.pix_start;
+    A.list = ws.pl.list;
+    A.list_t = ws.pl.list_t;
     A.flags = ws.flags;
     int64_t *total = n_out_dev ? n_out_dev : ws.total;
 
     SBC_TRY(fill_i32(reinterpret_cast<int32_t *>(ws.status), 0, 1, stream));
     if (n > 0) {
         trace_before("lif_sort", stream);
-        const dim3 eg(grid_for(n, 256)), eb(256);
-        SBC_TRY(fill_i32(ws.counts, 0, npix, stream));
-        hipLaunchKernelGGL(lif_count_kernel, eg, eb, 0, stream, px, py, t, n, width, height,
-                           slots, ws.counts, ws.keys, ws.place, ws.flags, ws.status);
-        SBC_LAUNCH_CHECK();
-        SBC_TRY(exclusive_scan_i32(ws.counts, ws.pix_start, npix, ws.total_pix, ws.scan_ws,
-                                   stream));
-        hipLaunchKernelGGL(lif_place_kernel, eg, eb, 0, stream, ws.keys, ws.place, ws.pix_start,
-                           t, n, ws.unsorted, ws.unsorted_t, ws.seg_of);
-        SBC_LAUNCH_CHECK();
-        // each pixel's list in stream order (indices are distinct), times alongside
-        SBC_TRY(segmented_sort_pairs(ws.pix_start, (int32_t)npix, ws.seg_of, n, ws.unsorted,
-                                     ws.unsorted_t, ws.list, ws.list_t, stream));
+        SBC_TRY(build_pixel_lists(px, py, t, n, width, height, ws.pl, ws.status, ws.flags, slots,
+                                  stream));
         trace_after("lif_sort", stream);
         const int64_t cells = (int64_t)A.Wo * A.Ho;
         trace_before("lif_cells", stream);

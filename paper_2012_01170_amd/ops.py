@@ -455,6 +455,41 @@ def lif_sample_events(px, py, t, width: int, height: int, kernel: int = 3, strid
     return tuple(out) + (count,)
 
 
+class EventStream:
+    """The state of the event convolution's deployment form (Eq. 13-15) over
+    a width x height sensor: z [height * width, C_in] and z_time [height *
+    width], zero at the start.  step() feeds one batch (sbc_event_stream_step)
+    and returns its outputs Y [n, C_out]."""
+
+    def __init__(self, width: int, height: int, C_in: int, tau: float, device="cuda"):
+        self.width, self.height, self.C_in, self.tau = int(width), int(height), int(C_in), tau
+        self.z = torch.zeros((self.width * self.height, self.C_in), dtype=torch.float32,
+                             device=device)
+        self.z_time = torch.zeros(self.width * self.height, dtype=torch.int32, device=device)
+
+    def step(self, px, py, t, F, W) -> torch.Tensor:
+        dev = self.z.device
+        _require(px, "px", torch.int32, 1, dev)
+        _require(py, "py", torch.int32, 1, dev)
+        _require(t, "t", torch.int32, 1, dev)
+        _require(F, "F", torch.float32, 2, dev)
+        _require(W, "W", torch.float32, 3, dev)
+        n = int(px.numel())
+        if int(py.numel()) != n or int(t.numel()) != n or F.shape != (n, self.C_in) \
+                or W.shape[:2] != (8, self.C_in):
+            raise ValueError("px, py, t [n], F [n, C_in] and W [8, C_in, C_out] expected")
+        C_out = int(W.shape[2])
+        Y = torch.empty((max(n, 1), C_out), dtype=torch.float32, device=dev)
+        lib = L.lib()
+        ws = _Workspace(lib.sbc_event_stream_workspace_size(n, self.width, self.height,
+                                                            self.C_in, C_out), dev)
+        L.check(lib.sbc_event_stream_step(_p(px), _p(py), _p(t), _p(F), n, self.width,
+                                          self.height, float(self.tau), _p(W), self.C_in, C_out,
+                                          _p(self.z), _p(self.z_time), _p(Y), ws.ptr, ws.nbytes,
+                                          _stream(dev)))
+        return Y[:n]
+
+
 def conv_plan(n_out, n_in, nnz, M, C_in, C_out, dtype=torch.float32, order="auto") -> dict:
     """Route and fusion of forward and backward for a shape (sbc_conv_plan)."""
     plan = L.SbcConvPlan()

@@ -63,7 +63,8 @@ SMALL = {
 # (one input channel of features ~N(0,1), so single-channel input gradients
 # whose sums cancel by up to 1e6) is checked as Eq. 9-10 instead
 FULL = [k for k in workloads.WORKLOADS
-        if k not in ("ellipsoids_featureless", "ellipsoids_sampling", "events_300k_lif")]
+        if k not in ("ellipsoids_featureless", "ellipsoids_sampling", "events_300k_lif",
+                     "events_stream")]
 ORDERS = ["spmm_first", "gemm_first"]
 
 
@@ -806,3 +807,60 @@ def test_lif_rejects_bad_streams():
         G.sbc.lif_sample_events(px, py, G.dev(np.array([0, 9, 5], np.int32)), 10, 10)
     with pytest.raises(G.sbc.ops.L.SbcError, match="kernel"):
         G.sbc.lif_sample_events(px, py, t, 10, 10, kernel=6)
+
+
+# ---------------------------------------------------------------- deployment stream
+@pytest.mark.parametrize("pieces", [[3000], [1, 699, 0, 1, 1299, 1000]])
+def test_event_stream_matches_the_recursion(pieces):
+    """The stream fed in batches (the state carried on the device) gives the
+    outputs and final state of the oracle's per-event recursion over the whole
+    stream, within 1e-5 (row-normwise; the state is float32 and the batch sums
+    come in another order); the last-update times are exact.  Channel counts
+    that are not multiples of 4 and C_in != C_out."""
+    print(f"[stream] pieces {pieces}", flush=True)
+    rng = np.random.default_rng(50)
+    n, Wd, H, tau = 3000, 20, 16, 3000.0
+    px, py, t, _ = workloads.uniform_events(rng, n, Wd, H, 30_000)
+    F = rng.standard_normal((n, 6)).astype(np.float32)
+    W = (rng.standard_normal((8, 6, 10)) / np.sqrt(48)).astype(np.float32)
+    Y_ref, z_ref, last_ref = oracle.conv.deployment_stream(px, py, t, F.astype(np.float64),
+                                                           W.astype(np.float64), Wd, H, tau)
+    st = G.sbc.EventStream(Wd, H, 6, tau, device=G.DEV)
+    Wd_dev = G.dev(W)
+    Ys, a = [], 0
+    for k in pieces:
+        b = a + k
+        Ys.append(st.step(G.dev(px[a:b]), G.dev(py[a:b]), G.dev(t[a:b]), G.dev(F[a:b]), Wd_dev)
+                  .cpu().numpy())
+        a = b
+    assert a == n
+    Y = np.concatenate(Ys)
+    err = G.row_error(Y, Y_ref)
+    zerr = G.row_error(st.z.cpu().numpy(), z_ref.reshape(Wd * H, 6))
+    print(f"    Y {err:.2e}  z {zerr:.2e}", flush=True)
+    assert err < 1e-5 and zerr < 1e-5
+    assert np.array_equal(st.z_time.cpu().numpy(), last_ref.reshape(-1).astype(np.int32))
+
+
+def test_event_stream_full_size_batches():
+    """The benchmarked form: the 300k-event stream (128 x 128, 32 -> 32
+    channels, tau 10 ms) in batches of 4096; sampled outputs of the last batch
+    and the final state against the oracle's recursion over the whole stream."""
+    print("[stream] events_stream", flush=True)
+    w = workloads.events_stream()
+    n, B = w["n_in"], w["batch"]
+    Y_ref, z_ref, last_ref = oracle.conv.deployment_stream(
+        w["px"], w["py"], w["t"], w["F"].astype(np.float64), w["W"].astype(np.float64),
+        w["width"], w["height"], w["tau"])
+    st = G.sbc.EventStream(w["width"], w["height"], w["C_in"], w["tau"], device=G.DEV)
+    t = G.to_device(w)
+    Wdev = t["W"]
+    for a in range(0, n, B):
+        Y = st.step(t["px"][a:a + B], t["py"][a:a + B], t["t"][a:a + B], t["F"][a:a + B], Wdev)
+    last = Y.cpu().numpy()
+    a = (n - 1) // B * B
+    err = G.row_error(last, Y_ref[a:])
+    zerr = G.row_error(st.z.cpu().numpy(), z_ref.reshape(-1, w["C_in"]))
+    print(f"    Y {err:.2e}  z {zerr:.2e}", flush=True)
+    assert err < 1e-5 and zerr < 1e-5
+    assert np.array_equal(st.z_time.cpu().numpy(), last_ref.reshape(-1).astype(np.int32))

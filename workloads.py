@@ -311,6 +311,17 @@ def events_300k_lif():
                 dtype="f64")
 
 
+def events_stream():
+    """The 300k-event 128x128 stream through the convolution's deployment form
+    (per-pixel decayed sums, Eq. 13-15) in batches of 4096 events: tau 10 ms,
+    32 -> 32 channels fp32, the state carried from batch to batch."""
+    w = event_stream()
+    w["batch"] = 4096
+    w["kind"] = "stream"
+    w["name"] = "stream300k_128x128"
+    return w
+
+
 WORKLOADS = {
     "sphere_1024": sphere_1024,
     "ellipsoids_inplace": ellipsoids_inplace,
@@ -322,6 +333,7 @@ WORKLOADS = {
     "events_300k_decays2": events_300k_decays2,
     "ellipsoids_sampling": ellipsoids_sampling,
     "events_300k_lif": events_300k_lif,
+    "events_stream": events_stream,
 }
 
 
