@@ -810,19 +810,20 @@ def test_lif_rejects_bad_streams():
 
 
 # ---------------------------------------------------------------- deployment stream
-@pytest.mark.parametrize("pieces", [[3000], [1, 699, 0, 1, 1299, 1000]])
-def test_event_stream_matches_the_recursion(pieces):
+@pytest.mark.parametrize("pieces,P", [([3000], 10), ([1, 699, 0, 1, 1299, 1000], 10),
+                                      ([1, 1500, 1499], 136)])
+def test_event_stream_matches_the_recursion(pieces, P):
     """The stream fed in batches (the state carried on the device) gives the
     outputs and final state of the oracle's per-event recursion over the whole
     stream, within 1e-5 (row-normwise; the state is float32 and the batch sums
     come in another order); the last-update times are exact.  Channel counts
-    that are not multiples of 4 and C_in != C_out."""
-    print(f"[stream] pieces {pieces}", flush=True)
+    that are not multiples of 4, C_in != C_out, and a wide output (136)."""
+    print(f"[stream] pieces {pieces} P {P}", flush=True)
     rng = np.random.default_rng(50)
     n, Wd, H, tau = 3000, 20, 16, 3000.0
     px, py, t, _ = workloads.uniform_events(rng, n, Wd, H, 30_000)
     F = rng.standard_normal((n, 6)).astype(np.float32)
-    W = (rng.standard_normal((8, 6, 10)) / np.sqrt(48)).astype(np.float32)
+    W = (rng.standard_normal((8, 6, P)) / np.sqrt(48)).astype(np.float32)
     Y_ref, z_ref, last_ref = oracle.conv.deployment_stream(px, py, t, F.astype(np.float64),
                                                            W.astype(np.float64), Wd, H, tau)
     st = G.sbc.EventStream(Wd, H, 6, tau, device=G.DEV)
