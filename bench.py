@@ -58,6 +58,10 @@ DESCRIPTIONS = {
     "ellipsoids_sampling": "32 clouds x 1024 points on ellipsoid surfaces; uncapped in-place "
                            "ball r 0.1, then rejection sampling and approximate farthest points "
                            "up to 256 per cloud",
+    "table2_flexconv": "the paper's Table 2 operator shape: 8 clouds x 4096 points in the unit "
+                       "cube, in place, the 9 nearest within r 0.25 (E 294,912); M 4; 64 -> 64 "
+                       "channels fp32; forward, transpose and backward, the search left out as "
+                       "in the table",
     "events_stream": "300k events, 128x128 pixels, 100 ms uniform, through the deployment form "
                      "(per-pixel decayed sums, Eq. 13-15) in batches of 4096; tau 10 ms; "
                      "32 -> 32 channels fp32",
@@ -386,11 +390,15 @@ def cpu_baseline(w, reps):
                           f"sequential sampler in float64; median of {reps} passes, "
                           f"{med:.2f} s each"}
     times, E = [], 0
+    in_step = w.get("search_in_step", True)
+    if not in_step:  # left out of the timed step, as on the GPU
+        fixed = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
+                                  w["radius"], w["k_cap"])
     for _ in range(reps):
         t0 = time.perf_counter()
         if w["kind"] == "points":
             rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
-                                       w["radius"], w["k_cap"])
+                                       w["radius"], w["k_cap"]) if in_step else fixed
             v = oracle.basis.point_values(w["basis"], w["x_in"], w["x_out"], rp, ci,
                                           w["radius"], w["M"])
         else:
@@ -419,7 +427,8 @@ def cpu_baseline(w, reps):
     med = statistics.median(times)
     return {"value": E / med, "unit": "edges/s", "cores": max(oracle.max_threads(), blas),
             "kind": "oracle",
-            "sample": f"whole workload ({E} edges): neighbours, basis, "
+            "sample": f"whole workload ({E} edges): "
+                      + ("neighbours, " if in_step else "") + "basis, "
                       + ("rejection sampling and farthest points" if w.get("sampling")
                          else "featureless forward and backward" if w.get("featureless")
                          else "forward, transpose, backward")
@@ -658,8 +667,14 @@ def main(argv=None):
             return sbc.neighbour_search_points(x_in, s_in, x_out, s_out, w["radius"],
                                                w["k_cap"], col_capacity=cap_ball, sync=False)
 
-        def transpose(csr):  # the batch is block-diagonal: cloud by cloud
-            return sbc.csr_transpose_batched(csr, s_out, s_in)
+        # the batch is block-diagonal: cloud by cloud, while a cloud's row
+        # bounds fit the batched kernel's LDS (2048 rows); larger clouds take
+        # the general transpose
+        by_cloud = int(np.diff(w["out_splits"]).max()) < 2048
+
+        def transpose(csr):
+            return (sbc.csr_transpose_batched(csr, s_out, s_in) if by_cloud
+                    else sbc.csr_transpose(csr))
     else:
         px, py, tt = T(w["px"]), T(w["py"]), T(w["t"])
         if w["basis"] == "event_decays":
@@ -709,8 +724,10 @@ def main(argv=None):
     else:
         decays = w["basis"] == "event_decays"
 
+        in_step = w.get("search_in_step", True)
+
         def step():
-            csr = search()
+            csr = search() if in_step else csr0
             Y = sbc.conv_forward(csr, F, W, geometry=geo, order=a.order)
             csc = transpose(csr)
             dF, dW = sbc.conv_backward(csr, csc, F, W, dY, geometry=geo, order=a.order)
@@ -723,6 +740,16 @@ def main(argv=None):
         blocks_bwd = max(1, min(256, n_cus, (n_in + tr_bwd - 1) // tr_bwd))
         npix = w["width"] * w["height"] if w["kind"] == "events" else 0
         table = kernel_table(w["kind"], plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd, npix)
+        if not in_step:
+            for k in ("points_count", "points_fill"):
+                table.pop(k, None)
+        if w["kind"] == "points" and not by_cloud:
+            # the general transpose: column counts, a scatter, then the
+            # in-column ordering
+            table.pop("transpose_batched")
+            table["transpose_count"] = (1, 4 * (n_out + 1) + 4 * E + 4 * n_in, 0, False)
+            table["transpose_scatter"] = (1, 4 * (n_out + 1) + 4 * E + 12 * E, 0, False)
+            table["transpose_sort"] = (1, 4 * (n_in + 1) + 16 * E, 0, False)
         if decays:
             if plan["backward_fused"]:
                 # the fused D-route with the derivative values, dF skipped
@@ -741,9 +768,13 @@ def main(argv=None):
             table["decay_dot"] = (1, 4 * M * ci * co + M * ci * co * sf + 4 * M, 0, False)
     ms, eager_ms, wall, kernels, roof = measure(a, w, table, step, torch, _lib, dev)
     dt = w["dtype"]
+    # the paper's own number for this exact workload: Table 2's full training
+    # pass (4.1 ms, N(F Theta) with JIT) over the same 294,912 edges, on a
+    # GTX-1080Ti; the search is left out on both sides
+    vs = E / (ms * 1e-3) / (E / 4.1e-3) if a.workload == "table2_flexconv" else None
     out = {"metric": METRIC, "value": E / (ms * 1e-3), "unit": "edges/s", "n_gpus": 1,
            "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 4),
-           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dt,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": vs, "dtype": dt,
            "data": "synthetic (seeded generators; inputs resident in HBM)",
            "config": {"workload": f"{a.workload}: {DESCRIPTIONS[a.workload]}", "n_in": n_in,
                       "n_out": n_out, "edges": E, "M": M, "C_in": ci, "C_out": co,

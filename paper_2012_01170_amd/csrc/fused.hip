@@ -1357,6 +1357,7 @@ BwdFn bwd_for(int basis_mode) {
 #define SBC_FWD_SHAPES(X) \
     X(16, 32, 32, false)  \
     X(10, 64, 64, false)  \
+    X(4, 64, 64, false)   \
     X(4, 16, 32, false)   \
     X(8, 64, 64, false)   \
     X(8, 64, 128, false)  \
@@ -1365,6 +1366,7 @@ BwdFn bwd_for(int basis_mode) {
     X(8, 32, 32, true)
 #define SBC_BWD_SHAPES(X) \
     X(16, 32, 32, false)  \
+    X(4, 64, 64, false)   \
     X(4, 16, 32, false)   \
     X(8, 64, 64, false)   \
     X(8, 32, 32, false)   \

@@ -322,6 +322,22 @@ def events_stream():
     return w
 
 
+def table2_flexconv():
+    """The operator benchmark shape of the paper's Table 2: 8 clouds x 4096
+    points (uniform in the unit cube; the table gives no distribution), in
+    place, the 9 nearest (the point itself included) within r = 0.25, which
+    always holds at least 9 (E = 294,912); M 4; 64 -> 64 channels fp32.  Like
+    the table, the step leaves out the neighbour search."""
+    rng = rng_for(7, salt=1)
+    clouds = []
+    for _ in range(8):
+        x = rng.uniform(0.0, 1.0, size=(4096, 3))
+        clouds.append((x, x))
+    w = points_workload(rng, clouds, BASIS_MONO4, 0.25, 9, 64, 64, name="table2_8x4096")
+    w["search_in_step"] = False
+    return w
+
+
 WORKLOADS = {
     "sphere_1024": sphere_1024,
     "ellipsoids_inplace": ellipsoids_inplace,
@@ -334,6 +350,7 @@ WORKLOADS = {
     "ellipsoids_sampling": ellipsoids_sampling,
     "events_300k_lif": events_300k_lif,
     "events_stream": events_stream,
+    "table2_flexconv": table2_flexconv,
 }
 
 
