@@ -10,15 +10,18 @@
 //   1. each pixel's events are listed, sorted by event index, with their times
 //      alongside (counted, placed, then sorted within each pixel; the count
 //      also clears the spike flags);
-//   2. a wave per cell stages the lists of its k x k input pixels in LDS and
-//      merges them in parallel, each entry finding its place by binary search
-//      in the other lists; the decay factors exp(-(t_s - t_{s-1}) / decay) of
-//      the merged sequence do not depend on the potential and are computed in
-//      parallel too; one lane then runs the recursion v = V e_s + 1/n_s with
-//      its threshold and reset (float64).  A spike of event i at the cell sets
-//      flag[i * slots + slot], slot being the cell's row-major place among the
-//      cells event i reaches.  A cell with more events than the LDS holds runs
-//      the same recursion on one lane, merging the lists from global memory;
+//   2. blocks of 16 cells (8 for kernels of 4 and 5), a wave per cell: the
+//      wave stages the lists of its cell's k x k input pixels in LDS and merges
+//      them in parallel, each entry finding its place by binary searches in
+//      the other lists; the decay factors exp(-(t_s - t_{s-1}) / decay) of the
+//      merged sequence do not depend on the potential and are computed in
+//      parallel too.  Then one wave runs the block's recursions
+//      v = V e_s + 1/n_s (threshold, reset; float64) side by side, a lane per
+//      cell; a spike marks its merged entry, and every wave then sets
+//      flag[i * slots + slot] for the spikes of its cell (slot: the cell's
+//      row-major place among the cells event i reaches).  A cell with more
+//      events than the staging holds runs the same recursion on one lane of
+//      another wave, merging its lists from global memory;
 //   3. a scan over the flags gives every spike its place in the output, which
 //      is thereby ordered by input event, then cell row, then cell column (the
 //      sequential emission order), and a last kernel writes the events.
