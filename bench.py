@@ -628,7 +628,7 @@ def main(argv=None):
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if a.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the hot path is built and timed on a single MI355X; "
-              "multi-GPU sharding is described in DESIGN.md but not run", file=sys.stderr)
+              "runs on more than one GPU are not made", file=sys.stderr)
         return 2
 
     import numpy as np

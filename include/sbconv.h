@@ -57,7 +57,7 @@ typedef enum {
     SBC_ERR_OUT_OF_RANGE = 5, /* pixel outside the sensor, split outside [0, n]   */
     SBC_ERR_WORKSPACE = 6,    /* workspace smaller than the size query's answer   */
     SBC_ERR_HIP = 7,          /* a HIP runtime call failed                        */
-    SBC_ERR_UNSUPPORTED = 8   /* shape or basis with no kernel in this build      */
+    SBC_ERR_UNSUPPORTED = 8   /* shape or basis with no kernel in the library    */
 } sbc_status;
 
 typedef enum {
