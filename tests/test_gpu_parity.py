@@ -865,3 +865,14 @@ def test_event_stream_full_size_batches():
     print(f"    Y {err:.2e}  z {zerr:.2e}", flush=True)
     assert err < 1e-5 and zerr < 1e-5
     assert np.array_equal(st.z_time.cpu().numpy(), last_ref.reshape(-1).astype(np.int32))
+
+
+def test_lif_bursty_1m_stream():
+    """The 1M-event bursty stream on 346 x 260 (a 173 x 130 grid, 3 x 3 fields,
+    stride 2) with the N-Caltech101 settings of the supplementary's table
+    (decay 1 ms, threshold 1.25, reset -2): every output event against the
+    oracle."""
+    print("[lif] bursty 1M", flush=True)
+    w = workloads.bursty_event_stream()
+    assert _lif_check(w["px"], w["py"], w["t"], w["width"], w["height"], 3, 2, 1000.0, 1.25,
+                      -2.0) > 10_000
