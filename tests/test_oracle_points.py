@@ -193,6 +193,24 @@ def test_basis_closed_forms():
     assert v[2].tolist() == [0.25, 0, -0.125, -0.125, 0, 0.0625, 0.0625, 0]
 
 
+def test_mono8_hand_case_every_column():
+    """Each of the eight M = 8 columns at an edge whose components are all
+    nonzero with distinct magnitudes (exact fractions in the fixture): the
+    eighth column is ux*uy*w, not one of the monomials the set leaves out."""
+    from fractions import Fraction
+    g = _gold("points_mono8_hand_case.json")
+    x_in, s_in, x_out, s_out = _single(g["x_in"], g["x_out"])
+    rp, ci = oracle.points_csr(x_in, s_in, x_out, s_out, g["radius"], 0)
+    assert rp.tolist() == [0, 1] and ci.tolist() == [0]
+    v = oracle.basis.point_basis(x_in, x_out, rp, ci, g["radius"], 8)
+    want = [float(Fraction(x)) for x in g["v"]]
+    assert v[0].tolist() == want
+    for other in g["left_out"].values():
+        assert v[0, 7] != float(Fraction(other))
+    # the values are pairwise distinct, so a swap of two columns shows
+    assert len(set(np.abs(v[0]).tolist())) == 8
+
+
 # ---------------------------------------------------------------- weighted convolution (Eq. 11)
 def _frac(x):
     from fractions import Fraction
