@@ -57,7 +57,9 @@ typedef enum {
     SBC_ERR_OUT_OF_RANGE = 5, /* pixel outside the sensor, split outside [0, n]   */
     SBC_ERR_WORKSPACE = 6,    /* workspace smaller than the size query's answer   */
     SBC_ERR_HIP = 7,          /* a HIP runtime call failed                        */
-    SBC_ERR_UNSUPPORTED = 8   /* shape or basis with no kernel in the library    */
+    SBC_ERR_UNSUPPORTED = 8,  /* shape or basis with no kernel in the library    */
+    SBC_ERR_INTERNAL = 9      /* a kernel's own consistency check failed; its    */
+                              /* stores were skipped (a library defect)           */
 } sbc_status;
 
 typedef enum {
@@ -87,7 +89,7 @@ typedef enum {
  *                     to sbc_conv_backward needs its edge_perm.
  * Event kernel with learned decays (Section 3.2, Eq. 12: g(u, dt) =
  * sum_v exp(-lambda_uv dt) theta_uv, M_v decays per offset):
- *   SBC_BASIS_EVENT_DECAYS  M = 8 * n_decays (1 <= n_decays <= 4):
+ *   SBC_BASIS_EVENT_DECAYS  M = 8 * n_decays (2 <= n_decays <= 4):
  *                     p_m = [u == idx(offset)] * exp(-lambda_uv * dt) with
  *                     m = u * n_decays + v, u the SBC_BASIS_EVENT8 offset index
  *                     and lambda = geometry.decays[u * n_decays + v] (> 0).
@@ -332,8 +334,8 @@ sbc_status sbc_conv_decay_gradient(const sbc_csr *csr, const sbc_csc *csc,
 
 /* ------------------------------------------------------------------------
  * 6. The featureless convolution (Section 3.1, "Featureless Convolutions",
- * Eq. 9-10): with no input features (F = 1) the convolution is a sum of
- * kernel values over the neighbourhood,
+ * Eq. 9-10): every input carries the constant feature 1 (F = 1), so the
+ * feature matrix drops out of the product,
  *     Z [n_out, P] = G~ Phi,   G~[i, m] = sum over row i of the values of p_m,
  * the first layer of a network on bare coordinates.
  *   v, geometry  the basis values [E, M], or NULL with the geometry (any basis)

@@ -102,10 +102,10 @@ def backward(row_ptr, col_idx, v, F, W, dY, n_in, cols_subset=None, want_dW=True
 
 def featureless_forward(row_ptr, col_idx, v, Phi):
     """The featureless convolution (Section 3.1, "Featureless Convolutions",
-    Eq. 9-10): with no input features (F = 1) the convolution reduces to a sum
-    of kernel values over the neighbourhood, Z = G~ Phi_0, where G~[i, m] is the
-    sum over row i of the basis values of function m and Phi_0 is an M x P
-    matrix (P output channels).  Returns (Z [n_out, P], G~ [n_out, M])."""
+    Eq. 9-10): every input carries the constant feature 1 (F = 1), so Z =
+    G~ Phi_0, where G~[i, m] adds up the values of basis function m along row i
+    and Phi_0 is an M x P matrix (P output channels).  Returns (Z [n_out, P],
+    G~ [n_out, M])."""
     row_ptr = np.asarray(row_ptr, dtype=np.int64)
     vd = np.asarray(v, dtype=np.float64)
     n_out = len(row_ptr) - 1

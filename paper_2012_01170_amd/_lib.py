@@ -14,7 +14,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsbconv.s
 SBC_OK = 0
 STATUS_NAMES = {0: "SBC_OK", 1: "SBC_ERR_INVALID_ARG", 2: "SBC_ERR_CAPACITY",
                 3: "SBC_ERR_OVERFLOW", 4: "SBC_ERR_UNSORTED", 5: "SBC_ERR_OUT_OF_RANGE",
-                6: "SBC_ERR_WORKSPACE", 7: "SBC_ERR_HIP", 8: "SBC_ERR_UNSUPPORTED"}
+                6: "SBC_ERR_WORKSPACE", 7: "SBC_ERR_HIP", 8: "SBC_ERR_UNSUPPORTED",
+                9: "SBC_ERR_INTERNAL"}
 SBC_F32, SBC_BF16 = 0, 1
 SBC_BASIS_MONO4, SBC_BASIS_MONO8, SBC_BASIS_EVENT8, SBC_BASIS_WMONO10 = 0, 1, 2, 3
 SBC_BASIS_EVENT_DECAYS = 4

@@ -80,6 +80,7 @@ extern "C" const char *sbc_status_string(sbc_status status) {
         case SBC_ERR_WORKSPACE: return "workspace too small";
         case SBC_ERR_HIP: return "HIP runtime error";
         case SBC_ERR_UNSUPPORTED: return "unsupported shape or basis";
+        case SBC_ERR_INTERNAL: return "internal consistency check failed";
     }
     return "unknown status";
 }

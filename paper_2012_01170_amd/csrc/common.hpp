@@ -71,6 +71,7 @@ enum : uint32_t {
     kFlagUnsorted = 2u,
     kFlagCapacity = 4u,
     kFlagBadSplits = 8u,
+    kFlagInternal = 16u,  // a kernel's own index check failed (its store was skipped)
 };
 
 // ---------------------------------------------------------------- primitives (scan.hip)

@@ -288,7 +288,7 @@ extern "C" sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v,
     }
     if (r == kFwdSpmm) {
         SBC_TRY(spmm(n_out, csr->row_ptr, csr->col_idx, nullptr, vv, M, F, bf, C_in, false,
-                     ws.inter, stream, "fwd_spmm"));
+                     csr->nnz_bound, ws.inter, stream, "fwd_spmm"));
         SBC_TRY(gemm(ws.inter, false, (int64_t)M * C_in, 1, W, bf, C_out, 1, Y, C_out, 1, n_out,
                      C_out, (int64_t)M * C_in, ws.partial, stream, "fwd_gemm"));
     } else {
@@ -298,7 +298,7 @@ extern "C" sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v,
                      (int64_t)M * C_out, 1, n_in, M * C_out, C_in, ws.partial, stream,
                      "fwd_gemm_h"));
         SBC_TRY(spmm(n_out, csr->row_ptr, csr->col_idx, nullptr, vv, M, ws.inter, false, C_out,
-                     true, Y, stream, "fwd_spmm_contract"));
+                     true, csr->nnz_bound, Y, stream, "fwd_spmm_contract"));
     }
     return SBC_OK;
 }
@@ -355,7 +355,7 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
     const int64_t K1 = (int64_t)M * C_in, K2 = (int64_t)M * C_out;
     if (r == kBwdG) {
         SBC_TRY(spmm(n_out, csr->row_ptr, csr->col_idx, nullptr, vv, M, F, bf, C_in, false,
-                     ws.inter, stream, "bwd_spmm"));
+                     csr->nnz_bound, ws.inter, stream, "bwd_spmm"));
         if (dW)  // dW [M*C_in, C_out] = G^T dY
             SBC_TRY(gemm(ws.inter, false, 1, K1, dY, bf, C_out, 1, dW, C_out, 1, (int32_t)K1,
                          C_out, n_out, ws.partial, stream, "bwd_gemm_dw"));
@@ -364,12 +364,12 @@ extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, 
                          C_out, ws.partial, stream, "bwd_gemm_dg"));
             SBC_TRY(values_t());
             SBC_TRY(spmm(n_in, csc->col_ptr, csc->row_idx, perm_t, vv, M, ws.inter2, false, C_in,
-                         true, dF, stream, "bwd_spmm_t"));
+                         true, csr->nnz_bound, dF, stream, "bwd_spmm_t"));
         }
     } else {
         SBC_TRY(values_t());
         SBC_TRY(spmm(n_in, csc->col_ptr, csc->row_idx, perm_t, vv, M, dY, bf, C_out, false,
-                     ws.inter, stream, "bwd_spmm_t_expand"));
+                     csr->nnz_bound, ws.inter, stream, "bwd_spmm_t_expand"));
         if (dF) {  // Wt [M, C_out, C_in]; dF = D Wt
             SBC_TRY(permute_w(W, bf, M, C_in, C_out, (int64_t)C_out * C_in, 1, C_in, ws.wperm,
                               stream));
@@ -480,8 +480,8 @@ extern "C" sbc_status sbc_conv_decay_gradient(const sbc_csr *csr, const sbc_csc 
         // v' = d p / d lambda, G' = N' F, dW' = G'^T dY
         DecayWs ws = carve_decay(workspace, n, csr->nnz_bound, M, C_in, C_out, nullptr);
         SBC_TRY(decay_derivative_launch(csr, geometry, ws.v, stream));
-        SBC_TRY(spmm(n, csr->row_ptr, csr->col_idx, nullptr, ws.v, M, F, bf, C_in, false, ws.G,
-                     stream, "decay_spmm"));
+        SBC_TRY(spmm(n, csr->row_ptr, csr->col_idx, nullptr, ws.v, M, F, bf, C_in, false,
+                     csr->nnz_bound, ws.G, stream, "decay_spmm"));
         const int64_t K1 = (int64_t)M * C_in;
         SBC_TRY(gemm(ws.G, false, 1, K1, dY, bf, C_out, 1, ws.dWp, C_out, 1, (int32_t)K1, C_out,
                      n, ws.partial, stream, "decay_gemm"));

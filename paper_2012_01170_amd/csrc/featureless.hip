@@ -1,7 +1,7 @@
 // The featureless convolution (Section 3.1, "Featureless Convolutions",
-// Eq. 9-10): with no input features the convolution reduces to a sum of
-// kernel values over the neighbourhood, Z = G~ Phi_0, where G~[i, m] sums the
-// basis values of function m over row i and Phi_0 is an M x P matrix.
+// Eq. 9-10): when every input carries the constant feature 1, the feature
+// matrix drops out and Z = G~ Phi_0, where G~[i, m] adds up the values of
+// basis function m along row i and Phi_0 is an M x P matrix.
 //
 // Forward: a group of kFLanes lanes per row takes the row's edges in turn,
 // evaluates their basis values (or reads them), and adds them up in float64,

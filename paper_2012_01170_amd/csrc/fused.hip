@@ -76,6 +76,7 @@ __device__ __forceinline__ bf16x8 lds_column8(const uint16_t *p, int s) {
 struct KGeo {
     double inv_r;
     float inv_tau;
+    int32_t nnz;  // edge bound of the pattern: row extents are clamped to [0, nnz]
     const float *x_in, *x_out;
     const int4 *ev;
     const float *decays;  // learned-decay rates [8, M / 8]
@@ -203,13 +204,14 @@ __device__ __forceinline__ void fma_row(float (&acc)[M][VEC], const RawVec<kXbf>
 // what gather_rows needs to start, loadable one call ahead.
 template <int RPW>
 __device__ __forceinline__ int32_t load_bound(const int32_t *__restrict__ ptr, int32_t n_rows,
-                                              int32_t row_begin) {
+                                              int32_t row_begin, int32_t nnz) {
     const int lane = threadIdx.x & 63;
     if (lane > RPW) return 0;
     int32_t r = row_begin + lane;
     r = r < n_rows ? r : n_rows;
     r = r > 0 ? r : 0;
-    return ptr[r];
+    const int32_t b = ptr[r];
+    return b < 0 ? 0 : (b < nnz ? b : nnz);
 }
 
 // Gather of one wave's RPW consecutive rows into an LDS tile.
@@ -273,7 +275,7 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
 
     if (lane <= RPW) st.bounds[lane] = pre.bound;
     const int32_t next_bound =
-        next_row_begin >= 0 ? load_bound<RPW>(ptr, n_rows, next_row_begin) : 0;
+        next_row_begin >= 0 ? load_bound<RPW>(ptr, n_rows, next_row_begin, g.nnz) : 0;
     wave_lds_sync();
     const int32_t wb = st.bounds[0], we = st.bounds[RPW];
     int32_t rs[NB], re[NB];
@@ -646,7 +648,8 @@ __global__ void __launch_bounds__(kFwdWaves * 64, fwd_tile_rows(M * CI, CO, kBf)
 
     gather_rows<M, CI, kBasis, kBf, kBf, false, RPW, false>(
         row0 + w * RPW, n_out, row_ptr, col_idx, nullptr, v, g, F, Gs, S, w * RPW, stage[w],
-        inv_r, inv_tau, GatherAhead{load_bound<RPW>(row_ptr, n_out, row0 + w * RPW), 0, false},
+        inv_r, inv_tau,
+        GatherAhead{load_bound<RPW>(row_ptr, n_out, row0 + w * RPW, g.nnz), 0, false},
         -1);
     __syncthreads();
 
@@ -765,6 +768,8 @@ __global__ void __launch_bounds__(kRegWaves * 64)
         if (row < n_out) {
             e0 = row_ptr[row];
             e1 = row_ptr[row + 1];
+            e0 = e0 < 0 ? 0 : (e0 < g.nnz ? e0 : g.nnz);
+            e1 = e1 < e0 ? e0 : (e1 < g.nnz ? e1 : g.nnz);
         }
         int32_t len = e1 - e0;
 #pragma unroll
@@ -981,8 +986,8 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
 
     // row bounds (and first neighbour indices) of the gather's next tile,
     // loaded one tile ahead
-    GatherAhead ahead{n_my > 0 ? load_bound<RPW>(col_ptr, n_in, t_first * TR + w * RPW) : 0, 0,
-                      false};
+    GatherAhead ahead{
+        n_my > 0 ? load_bound<RPW>(col_ptr, n_in, t_first * TR + w * RPW, g.nnz) : 0, 0, false};
     auto load_tile = [&](int32_t s, int buf) {
         const int32_t row0 = (t_first + s * gx) * TR;
         if (dW_part) {  // F rows of the tile, row-major (zero past the last row), 16 B per load
@@ -1463,6 +1468,7 @@ namespace {
 sbc_status make_kgeo(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,
                      int32_t CI, int32_t CO, void *ws, hipStream_t stream, KGeo *kg) {
     *kg = KGeo{};
+    kg->nnz = csr->nnz_bound > INT32_MAX ? INT32_MAX : (int32_t)csr->nnz_bound;
     if (v || !g) return SBC_OK;
     kg->inv_r = 1.0 / (double)g->radius;
     kg->inv_tau = 1.0f / g->tau;

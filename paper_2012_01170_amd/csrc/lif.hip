@@ -40,7 +40,20 @@ struct LifArgs {
     double decay, thresh, reset;
     const int32_t *pix_start, *list, *list_t;
     int32_t *flags;                           // [n * nsd * nsd]
+    uint32_t *status;                         // kFlagInternal on a bad flag index
 };
+
+// Marks the spike of event `ev` at its cell slot `slot`.  Both come out of the
+// kernel's own merge, so they are always in range; the check keeps a defect
+// there from turning into a store outside the flags (it raises the status
+// word, which the synchronising call reports, instead).
+__device__ __forceinline__ void mark_spike(const LifArgs &A, int64_t ev, int64_t slot) {
+    const int64_t nslots = (int64_t)A.nsd * A.nsd;
+    if (ev >= 0 && ev < A.n && slot >= 0 && slot < nslots)
+        A.flags[ev * nslots + slot] = 1;
+    else
+        atomicOr(A.status, kFlagInternal);
+}
 
 // Cells o (one dimension) whose receptive field [o*S - pad, o*S - pad + k)
 // holds input coordinate x: lo..hi (empty when hi < lo).
@@ -90,7 +103,6 @@ __device__ void cell_sequential(const LifArgs &A, int32_t ox, int32_t oy) {
         head[q] = pos[q] < end[q] ? A.list[pos[q]] : kNone;
         head_t[q] = pos[q] < end[q] ? A.list_t[pos[q]] : 0;
     }
-    const int64_t nslots = (int64_t)A.nsd * A.nsd;
     double V = 0.0, T = 0.0;
     for (;;) {
         int32_t best = kNone, bt = 0, bs = 0, bq = -1;
@@ -126,7 +138,7 @@ __device__ void cell_sequential(const LifArgs &A, int32_t ox, int32_t oy) {
         double v = V * exp(-(ti - T) / A.decay) + binc;
         if (v > A.thresh) {
             v = A.reset;
-            A.flags[(int64_t)best * nslots + bs] = 1;
+            mark_spike(A, best, bs);
         }
         V = v;
         T = ti;
@@ -320,12 +332,11 @@ __global__ void __launch_bounds__(LifTile<K>::kCells * 64) lif_cell_kernel(LifAr
         }
     }
     __syncthreads();
-    const int64_t nslots = (int64_t)A.nsd * A.nsd;
     if (staged)  // the spikes of this wave's cell
         for (int32_t r = lane; r < L; r += kLifThreads) {
             const int q = m_q[mo + r];
             if (q & 0x80)
-                A.flags[(int64_t)m_idx[mo + r] * nslots + s_slot[w][q & 0x7f]] = 1;
+                mark_spike(A, m_idx[mo + r], s_slot[w][q & 0x7f]);
         }
 }
 
@@ -448,6 +459,7 @@ extern "C" sbc_status sbc_lif_sample_events(const int32_t *px, const int32_t *py
     A.list = ws.pl.list;
     A.list_t = ws.pl.list_t;
     A.flags = ws.flags;
+    A.status = ws.status;
     int64_t *total = n_out_dev ? n_out_dev : ws.total;
 
     SBC_TRY(fill_i32(reinterpret_cast<int32_t *>(ws.status), 0, 1, stream));
@@ -487,6 +499,8 @@ extern "C" sbc_status sbc_lif_sample_events(const int32_t *px, const int32_t *py
         SBC_HIP_TRY(hipMemcpyAsync(&st, ws.status, sizeof(st), hipMemcpyDeviceToHost, stream));
         SBC_HIP_TRY(hipStreamSynchronize(stream));
         *n_out_host = count;
+        if (st & kFlagInternal)
+            return fail(SBC_ERR_INTERNAL, "a spike flag index fell outside the flags");
         if (st & kFlagOutOfRange) return fail(SBC_ERR_OUT_OF_RANGE, "pixel outside the sensor");
         if (st & kFlagUnsorted) return fail(SBC_ERR_UNSORTED, "timestamps must be non-decreasing");
         if (count > capacity)

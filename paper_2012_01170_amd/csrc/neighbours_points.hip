@@ -455,7 +455,7 @@ __global__ void __launch_bounds__(kWaves * 64)
         n += __popcll(mask);
     }
     wave_lds_sync();
-    const int32_t out0 = kMode == 2 ? i * k_cap : row_ptr[i];
+    const int64_t out0 = kMode == 2 ? (int64_t)i * k_cap : (int64_t)row_ptr[i];
     const bool capped = k_cap > 0 && n > k_cap;
     const int32_t n_keep = capped ? k_cap : n;
     if (kMode == 2 && sl == 0) row_len[i] = n_keep;

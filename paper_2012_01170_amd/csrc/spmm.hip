@@ -23,11 +23,14 @@ template <int M, bool kContract, typename XT>
 __global__ void __launch_bounds__(256)
     spmm_kernel(int32_t n_rows, const int32_t *__restrict__ ptr, const int32_t *__restrict__ idx,
                 const int32_t *__restrict__ perm, const float *__restrict__ v,
-                const XT *__restrict__ X, int32_t C, float *__restrict__ out) {
+                const XT *__restrict__ X, int32_t C, int32_t nnz, float *__restrict__ out) {
     const int lane = threadIdx.x & 63;
     const int32_t r = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (r >= n_rows) return;
-    const int32_t e0 = ptr[r], e1 = ptr[r + 1];
+    // edges past the pattern's bound (a row pointer beyond it) are not read
+    int32_t e0 = ptr[r], e1 = ptr[r + 1];
+    e0 = e0 < 0 ? 0 : (e0 < nnz ? e0 : nnz);
+    e1 = e1 < e0 ? e0 : (e1 < nnz ? e1 : nnz);
     for (int32_t c0 = 0; c0 < C; c0 += 64) {
         const int32_t c = c0 + lane;
         const bool on = c < C;
@@ -65,11 +68,11 @@ __global__ void __launch_bounds__(256)
 template <int M>
 sbc_status launch_m(int32_t n_rows, const int32_t *ptr, const int32_t *idx, const int32_t *perm,
                     const float *v, const void *X, bool x_bf16, int32_t C, bool contract,
-                    float *out, hipStream_t stream) {
+                    int32_t nnz, float *out, hipStream_t stream) {
     dim3 grid(grid_for(n_rows, 4)), block(256);
 #define SBC_SPMM(CONTRACT, XT)                                                                  \
     hipLaunchKernelGGL((spmm_kernel<M, CONTRACT, XT>), grid, block, 0, stream, n_rows, ptr, idx, \
-                       perm, v, static_cast<const XT *>(X), C, out)
+                       perm, v, static_cast<const XT *>(X), C, nnz, out)
     if (contract) {
         if (x_bf16) SBC_SPMM(true, uint16_t); else SBC_SPMM(true, float);
     } else {
@@ -84,19 +87,20 @@ sbc_status launch_m(int32_t n_rows, const int32_t *ptr, const int32_t *idx, cons
 
 sbc_status spmm(int32_t n_rows, const int32_t *ptr, const int32_t *idx, const int32_t *perm,
                 const float *v, int32_t M, const void *X, bool x_bf16, int32_t C, bool contract,
-                float *out, hipStream_t stream, const char *trace) {
+                int64_t nnz_bound, float *out, hipStream_t stream, const char *trace) {
     if (n_rows <= 0 || C <= 0) return SBC_OK;
+    const int32_t nnz = nnz_bound < 0 ? 0 : (nnz_bound > INT32_MAX ? INT32_MAX : (int32_t)nnz_bound);
     if (M != 4 && M != 8 && M != 10 && M != 16 && M != 24 && M != 32)
         return fail(SBC_ERR_UNSUPPORTED, "M must be 4, 8, 10, 16, 24 or 32");
     trace_before(trace, stream);
     sbc_status st;
     switch (M) {
-        case 4: st = launch_m<4>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
-        case 8: st = launch_m<8>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
-        case 10: st = launch_m<10>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
-        case 16: st = launch_m<16>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
-        case 24: st = launch_m<24>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
-        default: st = launch_m<32>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, out, stream); break;
+        case 4: st = launch_m<4>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, nnz, out, stream); break;
+        case 8: st = launch_m<8>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, nnz, out, stream); break;
+        case 10: st = launch_m<10>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, nnz, out, stream); break;
+        case 16: st = launch_m<16>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, nnz, out, stream); break;
+        case 24: st = launch_m<24>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, nnz, out, stream); break;
+        default: st = launch_m<32>(n_rows, ptr, idx, perm, v, X, x_bf16, C, contract, nnz, out, stream); break;
     }
     trace_after(trace, stream);
     return st;

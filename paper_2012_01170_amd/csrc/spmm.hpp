@@ -12,9 +12,10 @@ namespace sbc {
 // Rows r < n_rows of the pattern (ptr [n_rows + 1], idx [E]); perm maps a
 // pattern position to its row of v (nullptr: identity).  Expand writes
 // out [n_rows, M*C]; contract reads X [*, M*C] and writes out [n_rows, C].
+// Row extents are clamped to [0, nnz_bound] (the sizes idx and v were given).
 sbc_status spmm(int32_t n_rows, const int32_t *ptr, const int32_t *idx, const int32_t *perm,
                 const float *v, int32_t M, const void *X, bool x_bf16, int32_t C, bool contract,
-                float *out, hipStream_t stream, const char *trace);
+                int64_t nnz_bound, float *out, hipStream_t stream, const char *trace);
 
 // basis.hip
 sbc_status check_csr(const sbc_csr *csr);

@@ -104,6 +104,35 @@ class Geometry:
             return 8 * int(self.decays.shape[1])
         return BASIS_M[self.basis]
 
+    def check(self, csr: "CSR") -> None:
+        """Dtype, device, contiguity and length of every coordinate tensor the
+        basis reads, against the pattern's sizes (the kernels index them by
+        the pattern's rows and columns)."""
+        if self.basis not in BASES:
+            raise ValueError(f"unknown basis {self.basis!r}")
+        dev = csr.row_ptr.device
+        if self.basis in ("mono4", "mono8", "wmono10"):
+            for name, x, n in (("x_in", self.x_in, csr.n_cols), ("x_out", self.x_out, csr.n_rows)):
+                if x is None:
+                    raise ValueError(f"geometry.{name} is needed for the point basis")
+                _require(x, name, torch.float32, 2, dev)
+                if tuple(x.shape) != (n, 3):
+                    raise ValueError(f"{name} must be [{n}, 3], got {tuple(x.shape)}")
+            return
+        n = max(csr.n_rows, csr.n_cols)     # an event stream is in place
+        for name, x in (("px", self.px), ("py", self.py), ("t", self.t)):
+            if x is None:
+                raise ValueError(f"geometry.{name} is needed for the event basis")
+            _require(x, name, torch.int32, 1, dev)
+            if x.numel() != n:
+                raise ValueError(f"{name} must hold {n} events, got {x.numel()}")
+        if self.basis == "event_decays":
+            if self.decays is None:
+                raise ValueError("geometry.decays is needed for the learned-decay basis")
+            _require(self.decays, "decays", torch.float32, 2, dev)
+            if self.decays.shape[0] != 8 or not 2 <= self.decays.shape[1] <= 4:
+                raise ValueError("decays must be [8, n_decays] with 2 <= n_decays <= 4")
+
     def c_struct(self) -> L.SbcGeometry:
         d = lambda x: x.data_ptr() if x is not None else 0
         nd = int(self.decays.shape[1]) if self.decays is not None else 0
@@ -217,6 +246,7 @@ def neighbour_search_events_csc(px, py, t, width: int, height: int, window: int,
 def basis_eval(csr: CSR, geometry: Geometry) -> torch.Tensor:
     """Per-edge basis values v [E, M] float32 (sbc_basis_eval)."""
     dev = csr.row_ptr.device
+    geometry.check(csr)
     v = torch.empty((max(csr.nnz, 0), geometry.M), dtype=torch.float32, device=dev)
     c, g = csr.c_struct(), geometry.c_struct()
     L.check(L.lib().sbc_basis_eval(ctypes.byref(c), ctypes.byref(g), _p(v), _stream(dev)))
@@ -279,6 +309,8 @@ def _conv_common(csr, F, W, v, geometry):
             raise ValueError("v must be [E, M]")
     elif geometry is None:
         raise ValueError("either v or geometry is needed")
+    if geometry is not None:
+        geometry.check(csr)
     return dev, M, C_in, C_out
 
 
@@ -330,6 +362,8 @@ def _featureless_common(csr: CSR, M: int, geometry: Optional[Geometry], v):
             raise ValueError("v must be [E, M]")
     elif geometry is None:
         raise ValueError("either v or geometry is needed")
+    if geometry is not None:
+        geometry.check(csr)
     g = geometry.c_struct() if geometry is not None else None
     return dev, g
 
