@@ -335,10 +335,12 @@ def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256, npix
         t["fwd_gemm_h"] = (1, n_in * ci * sf + W + H, 2 * n_in * ci * M * co, True)
         t["fwd_spmm_contract"] = (1, csr_b + H + 4 * n_out * co, 2 * E * M * co, False)
     if plan["backward_fused"]:
-        part = 4 * blocks_bwd * ci * M * co
+        # compulsory bytes only: the per-block dW partials the kernel writes
+        # for the ordered reduction are its own scratch, not algorithmic
+        # traffic (the byte counters show them)
         t["bwd_fused"] = (1, 4 * (n_in + 1) + 4 * E + geo + n_out * co * sf + n_in * ci * sf
-                          + W + 4 * n_in * ci + part, 4 * n_in * M * ci * co, True)
-        t["bwd_dw_reduce"] = (1, part + 4 * M * ci * co, 0, False)
+                          + W + 4 * n_in * ci, 4 * n_in * M * ci * co, True)
+        t["bwd_dw_reduce"] = (1, 4 * M * ci * co, 0, False)
     elif plan["backward_order"] == "spmm_first":
         basis_launches += 1
         D = 4 * n_in * M * co
@@ -359,14 +361,101 @@ def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256, npix
     return t
 
 
-def cpu_baseline(w, reps):
-    """The oracle on the whole workload: neighbours, basis, forward, transpose, backward."""
-    import oracle
+def _blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # threadpoolctl missing: report the OpenMP count only
-        blas = 1
+        return 1
+
+
+def event_prefix(w, n_events):
+    """The first n_events of an event workload: a stream of its own whose
+    pattern is exactly the first n_events rows of the whole one (an event's
+    neighbours all come before it), so its timings are a bounded sample of
+    the same work."""
+    if n_events >= w["n_in"]:
+        return w, w["n_in"]
+    v = dict(w)
+    for k in ("px", "py", "t", "F", "dY"):
+        v[k] = w[k][:n_events]
+    v["n_in"] = v["n_out"] = n_events
+    return v, n_events
+
+
+def oracle_stages(w):
+    """One pass of the oracle over workload w, stage by stage: (seconds per
+    stage, edge count)."""
+    import oracle
+    st = {}
+    in_step = w.get("search_in_step", True)
+    t0 = time.perf_counter()
+    if w["kind"] == "points":
+        rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
+                                   w["radius"], w["k_cap"])
+    else:
+        rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"],
+                                   w["height"])
+    t1 = time.perf_counter()
+    if in_step:
+        st["neighbours"] = t1 - t0
+    if w["kind"] == "points":
+        v = oracle.basis.point_values(w["basis"], w["x_in"], w["x_out"], rp, ci, w["radius"],
+                                      w["M"])
+    else:
+        v = oracle.basis.event_values(w["basis"], w["px"], w["py"], w["t"], rp, ci, w["tau"],
+                                      w.get("decays"))
+    t2 = time.perf_counter()
+    st["basis"] = t2 - t1
+    if w.get("sampling"):
+        smp = w["sampling"]
+        oracle.sampling.approx_ifp_after_rejection(w["x_in"], w["in_splits"], smp["per_cloud"],
+                                                   rp, ci)
+        st["sampling"] = time.perf_counter() - t2
+        return st, len(ci)
+    if w.get("featureless"):
+        Phi = w["W"][:, 0, :]
+        oracle.conv.featureless_forward(rp, ci, v, Phi)
+        t3 = time.perf_counter()
+        oracle.conv.featureless_backward(rp, ci, v, w["dY"])
+        st["forward"], st["backward"] = t3 - t2, time.perf_counter() - t3
+        return st, len(ci)
+    oracle.conv.forward(rp, ci, v, w["F"], w["W"])
+    t3 = time.perf_counter()
+    oracle.csr_transpose(rp, ci, w["n_in"])
+    t4 = time.perf_counter()
+    oracle.conv.backward(rp, ci, v, w["F"], w["W"], w["dY"], w["n_in"])
+    t5 = time.perf_counter()
+    st["forward"], st["transpose"], st["backward"] = t3 - t2, t4 - t3, t5 - t4
+    if w["basis"] == "event_decays":
+        vd = oracle.basis.event_decay_basis(w["px"], w["py"], w["t"], rp, ci, w["decays"],
+                                            derivative=True)
+        oracle.conv.decay_backward(rp, ci, vd, w["F"], w["W"], w["dY"])
+        st["decay_gradient"] = time.perf_counter() - t5
+    return st, len(ci)
+
+
+def _median_stages(w, reps):
+    runs, E = [], 0
+    for _ in range(reps):
+        st, E = oracle_stages(w)
+        runs.append(st)
+    stages = {k: statistics.median(r[k] for r in runs) for k in runs[0]}
+    total = statistics.median(sum(r.values()) for r in runs)
+    return stages, total, E
+
+
+# events per bounded oracle sample of an event workload (a prefix of the
+# stream): about 10-30 s of float64 work on a 16-thread host
+ORACLE_EVENT_SAMPLE = 100_000
+
+
+def cpu_baseline(w, reps):
+    """The oracle as written (float64, untuned), timed stage by stage on this
+    host's cores: neighbours, basis, forward, transpose, backward.  Point
+    workloads run whole, and once more on one thread; event streams run on a
+    prefix of ORACLE_EVENT_SAMPLE events."""
+    import oracle
     if w["kind"] == "stream":
         t0 = time.perf_counter()
         oracle.conv.deployment_stream(w["px"], w["py"], w["t"], w["F"].astype("float64"),
@@ -389,57 +478,63 @@ def cpu_baseline(w, reps):
                 "sample": f"whole stream ({w['n_in']} events -> {len(out)}) through the "
                           f"sequential sampler in float64; median of {reps} passes, "
                           f"{med:.2f} s each"}
-    times, E = [], 0
-    in_step = w.get("search_in_step", True)
-    if not in_step:  # left out of the timed step, as on the GPU
-        fixed = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
-                                  w["radius"], w["k_cap"])
-    for _ in range(reps):
-        t0 = time.perf_counter()
-        if w["kind"] == "points":
-            rp, ci = oracle.points_csr(w["x_in"], w["in_splits"], w["x_out"], w["out_splits"],
-                                       w["radius"], w["k_cap"]) if in_step else fixed
-            v = oracle.basis.point_values(w["basis"], w["x_in"], w["x_out"], rp, ci,
-                                          w["radius"], w["M"])
-        else:
-            rp, ci = oracle.events_csr(w["px"], w["py"], w["t"], w["window"], 1, w["width"],
-                                       w["height"])
-            v = oracle.basis.event_values(w["basis"], w["px"], w["py"], w["t"], rp, ci,
-                                          w["tau"], w.get("decays"))
-        if w.get("sampling"):
-            smp = w["sampling"]
-            oracle.sampling.approx_ifp_after_rejection(w["x_in"], w["in_splits"],
-                                                       smp["per_cloud"], rp, ci)
-        elif w.get("featureless"):
-            Phi = w["W"][:, 0, :]
-            oracle.conv.featureless_forward(rp, ci, v, Phi)
-            oracle.conv.featureless_backward(rp, ci, v, w["dY"])
-        else:
-            oracle.conv.forward(rp, ci, v, w["F"], w["W"])
-            oracle.csr_transpose(rp, ci, w["n_in"])
-            oracle.conv.backward(rp, ci, v, w["F"], w["W"], w["dY"], w["n_in"])
-            if w["basis"] == "event_decays":
-                vd = oracle.basis.event_decay_basis(w["px"], w["py"], w["t"], rp, ci,
-                                                    w["decays"], derivative=True)
-                oracle.conv.decay_backward(rp, ci, vd, w["F"], w["W"], w["dY"])
-        times.append(time.perf_counter() - t0)
-        E = len(ci)
-    med = statistics.median(times)
-    return {"value": E / med, "unit": "edges/s", "cores": max(oracle.max_threads(), blas),
-            "kind": "oracle",
-            "sample": f"whole workload ({E} edges): "
-                      + ("neighbours, " if in_step else "") + "basis, "
-                      + ("rejection sampling and farthest points" if w.get("sampling")
-                         else "featureless forward and backward" if w.get("featureless")
-                         else "forward, transpose, backward")
-                      + f" in float64; median of {reps} passes, {med:.2f} s each"}
+    if w["kind"] == "events":
+        ws, n_s = event_prefix(w, ORACLE_EVENT_SAMPLE)
+        what = (f"the first {n_s} of the stream's {w['n_in']} events (a prefix is the same "
+                f"pattern's first rows)")
+    else:
+        ws, what = w, "whole workload"
+    stages, total, E = _median_stages(ws, reps)
+    cores = max(oracle.max_threads(), _blas_threads())
+    steps = ", ".join(stages)
+    out = {"value": E / total, "unit": "edges/s", "cores": cores, "kind": "oracle",
+           "sample": f"{what}, {E} edges: {steps} in float64; median of {reps} passes, "
+                     f"{total:.2f} s each",
+           "stages": {k: {"s": round(t, 4), "edges_per_s": round(E / t, 1) if t > 0 else None}
+                      for k, t in stages.items()}}
+    if w["kind"] == "points":
+        try:
+            from threadpoolctl import threadpool_limits
+        except ImportError:
+            threadpool_limits = None
+        if threadpool_limits is not None:
+            with threadpool_limits(limits=1):
+                st1, tot1, _ = _median_stages(ws, reps)
+            out["single_thread"] = {
+                "value": E / tot1, "unit": "edges/s", "cores": 1,
+                "stages": {k: {"s": round(t, 4),
+                               "edges_per_s": round(E / t, 1) if t > 0 else None}
+                           for k, t in st1.items()}}
+    return out
+
+
+def replay_distribution(graph, steps, torch, flush=None):
+    """Per-replay times (ms) of a captured step: each replay bracketed by its
+    own events; with `flush`, a write of a 512 MiB buffer runs before each
+    bracket, evicting the 256 MB last-level cache (cold inputs)."""
+    times = []
+    for _ in range(steps):
+        if flush is not None:
+            flush.fill_(1.0)
+        s0 = torch.cuda.Event(enable_timing=True)
+        s1 = torch.cuda.Event(enable_timing=True)
+        s0.record()
+        graph.replay()
+        s1.record()
+        torch.cuda.synchronize()
+        times.append(s0.elapsed_time(s1))
+    times.sort()
+    q = lambda f: times[min(len(times) - 1, int(round(f * (len(times) - 1))))]
+    return {"median_ms": round(statistics.median(times), 4), "p10_ms": round(q(0.1), 4),
+            "p90_ms": round(q(0.9), 4), "replays": len(times)}
 
 
 def measure(a, w, table, step, torch, _lib, dev):
     """Warm-up, eager steps with every kernel bracketed by HIP events (the
     library's trace hook), then HIP-graph replays of the captured step (the
     timed region).  Returns (ms per step, eager ms per step, wall s, the
-    per-kernel table, the roofline of the dominant kernel)."""
+    per-kernel table, the roofline of the dominant kernel, the single-replay
+    distributions hot and cold)."""
     L = _lib.lib()
     # one (start, stop) event pair per kernel per timed step; record once so the
     # underlying HIP events exist before the library records them again
@@ -470,9 +565,9 @@ def measure(a, w, table, step, torch, _lib, dev):
     # (2) the same step captured once in a HIP graph (it never synchronises
     # with the host), then replayed: the timed region
     if a.no_graph:
-        ms, wall = eager_ms, float("nan")
+        ms, wall, dist = eager_ms, float("nan"), None
     else:
-        ms, wall = graph_timing(step, a, torch)
+        ms, wall, dist = graph_timing(step, a, torch)
     if a.copy_probe_mb > 0:
         src = torch.ones(a.copy_probe_mb << 18, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
@@ -500,9 +595,11 @@ def measure(a, w, table, step, torch, _lib, dev):
             "unit": unit, "frac": round(achieved / peak, 4),
             "traffic": round(traffic) if traffic is not None else None,
             "per_launch": {"bytes": nbytes, "flops": flops, "us": us,
+                           "traffic_over_algorithmic":
+                               round(traffic / nbytes, 3) if traffic is not None else None,
                            "traffic_source": traffic_src}}
 
-    return ms, eager_ms, wall, kernels, roof
+    return ms, eager_ms, wall, kernels, roof, dist
 
 
 def graph_timing(step, a, torch):
@@ -527,7 +624,15 @@ def graph_timing(step, a, torch):
         graph.replay()
     t_stop.record()
     torch.cuda.synchronize()
-    return t_start.elapsed_time(t_stop) / a.steps, time.perf_counter() - wall0
+    ms, wall = t_start.elapsed_time(t_stop) / a.steps, time.perf_counter() - wall0
+    # the spread of single replays, with the inputs hot in the caches and
+    # with the last-level cache evicted before each replay
+    dist = {"hot": replay_distribution(graph, a.steps, torch)}
+    if not a.no_cold:
+        flush = torch.empty(512 << 18, dtype=torch.float32, device=torch.device("cuda:0"))
+        dist["cold"] = replay_distribution(graph, a.steps, torch, flush=flush)
+        del flush
+    return ms, wall, dist
 
 
 def lif_main(a, w, T, torch, sbc, _lib, dev):
@@ -544,7 +649,7 @@ def lif_main(a, w, T, torch, sbc, _lib, dev):
 
     n = w["n_in"]
     table = lif_table(n, w["width"] * w["height"], nsd * nsd, spikes)
-    ms, eager_ms, wall, kernels, roof = measure(a, w, table, step, torch, _lib, dev)
+    ms, eager_ms, wall, kernels, roof, dist = measure(a, w, table, step, torch, _lib, dev)
     out = {"metric": "LIF event sampler throughput (input events per second)",
            "value": n / (ms * 1e-3), "unit": "events/s", "n_gpus": 1, "steps": a.steps,
            "warmup": a.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
@@ -554,7 +659,8 @@ def lif_main(a, w, T, torch, sbc, _lib, dev):
                       "n_out_events": spikes, "grid": [-(-w["width"] // w["stride"]),
                                                        -(-w["height"] // w["stride"])],
                       "timing": "eager steps" if a.no_graph else "HIP graph replays of the captured step",
-                      "eager_ms_per_step": round(eager_ms, 4), "wall_s": round(wall, 3)},
+                      "eager_ms_per_step": round(eager_ms, 4), "wall_s": round(wall, 3),
+                      "replays": dist},
            "roofline": roof, "kernels": kernels}
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, a.cpu_reps)
@@ -579,7 +685,7 @@ def stream_main(a, w, T, torch, sbc, _lib, dev):
     batches = (n + B - 1) // B
     table = {k: (batches, b, f, m) for k, (_, b, f, m) in
              stream_table(B, w["width"] * w["height"], C, P).items()}
-    ms, eager_ms, wall, kernels, roof = measure(a, w, table, step, torch, _lib, dev)
+    ms, eager_ms, wall, kernels, roof, dist = measure(a, w, table, step, torch, _lib, dev)
     out = {"metric": "deployment-form stream throughput (input events per second)",
            "value": n / (ms * 1e-3), "unit": "events/s", "n_gpus": 1, "steps": a.steps,
            "warmup": a.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
@@ -588,7 +694,8 @@ def stream_main(a, w, T, torch, sbc, _lib, dev):
            "config": {"workload": f"{a.workload}: {DESCRIPTIONS[a.workload]}", "n_in": n,
                       "batch": B, "batches": batches, "C_in": C, "C_out": P,
                       "timing": "eager steps" if a.no_graph else "HIP graph replays of the captured step",
-                      "eager_ms_per_step": round(eager_ms, 4), "wall_s": round(wall, 3)},
+                      "eager_ms_per_step": round(eager_ms, 4), "wall_s": round(wall, 3),
+                      "replays": dist},
            "roofline": roof, "kernels": kernels}
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, a.cpu_reps)
@@ -601,10 +708,12 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="ellipsoids_inplace", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--workload", default="events_300k", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--order", default="auto", choices=["auto", "spmm_first", "gemm_first"])
     ap.add_argument("--cpu-reps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the single replays with the last-level cache evicted")
     ap.add_argument("--no-graph", action="store_true",
                     help="time eager steps only (for counter collection, which serialises)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -753,10 +862,9 @@ def main(argv=None):
         if decays:
             if plan["backward_fused"]:
                 # the fused D-route with the derivative values, dF skipped
-                part = 4 * blocks_bwd * ci * M * co
                 table["decay_fused"] = (1, 4 * (n_in + 1) + 4 * E + 12 * n_in + n_out * co * sf
-                                        + n_in * ci * sf + part, 2 * n_in * M * ci * co, True)
-                table["decay_dw_reduce"] = (1, part + 4 * M * ci * co, 0, False)
+                                        + n_in * ci * sf, 2 * n_in * M * ci * co, True)
+                table["decay_dw_reduce"] = (1, 4 * M * ci * co, 0, False)
             else:
                 G_b = 4 * n_out * M * ci
                 table["decay_basis"] = (1, 4 * (n_out + 1) + 4 * E + 12 * n_in + 4 * E * M, 0,
@@ -766,7 +874,7 @@ def main(argv=None):
                 table["decay_gemm"] = (1, G_b + n_out * co * sf + 4 * M * ci * co,
                                        2 * n_out * M * ci * co, True)
             table["decay_dot"] = (1, 4 * M * ci * co + M * ci * co * sf + 4 * M, 0, False)
-    ms, eager_ms, wall, kernels, roof = measure(a, w, table, step, torch, _lib, dev)
+    ms, eager_ms, wall, kernels, roof, dist = measure(a, w, table, step, torch, _lib, dev)
     dt = w["dtype"]
     # the paper's own number for this exact workload: Table 2's full training
     # pass (4.1 ms, N(F Theta) with JIT) over the same 294,912 edges, on a
@@ -780,7 +888,8 @@ def main(argv=None):
                       "n_out": n_out, "edges": E, "M": M, "C_in": ci, "C_out": co,
                       "plan": plan,
                       "timing": "eager steps" if a.no_graph else "HIP graph replays of the captured step",
-                      "eager_ms_per_step": round(eager_ms, 4), "wall_s": round(wall, 3)},
+                      "eager_ms_per_step": round(eager_ms, 4), "wall_s": round(wall, 3),
+                      "replays": dist},
            "roofline": roof, "kernels": kernels}
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, a.cpu_reps)
