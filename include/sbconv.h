@@ -294,6 +294,26 @@ sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v, const sbc_geomet
                             int32_t C_in, int32_t C_out, float *Y, sbc_order order,
                             void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* The forward for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation):
+ * sbc_conv_forward with the library's own static scratch in place of the
+ * workspace.  The scratch is a device array of
+ * sbc_conv_forward_noalloc_max_bytes() bytes (64 MiB) that each GPU the
+ * library runs on holds until the process ends; the call itself allocates
+ * nothing (no hipMalloc, no allocating library routine).  Arguments, results
+ * and errors are those of sbc_conv_forward; a forward whose temporary space
+ * (sbc_conv_workspace_size's forward share) exceeds the scratch returns
+ * SBC_ERR_WORKSPACE and enqueues nothing.  No part of the scratch needs to
+ * start at zero: every byte a call reads was written earlier in that call.
+ * All calls on one GPU share its scratch, so calls that overlap on one GPU
+ * (on different streams, or from different host threads without ordering)
+ * race on it and must not be issued. */
+size_t sbc_conv_forward_noalloc_max_bytes(void);
+sbc_status sbc_conv_forward_noalloc(const sbc_csr *csr, const float *v,
+                                    const sbc_geometry *geometry, int32_t M, const void *F,
+                                    const void *W, sbc_dtype dtype, int32_t C_in, int32_t C_out,
+                                    float *Y, sbc_order order, hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * 5. Backward: the gradients of <Y, dY> with respect to F and W.
  *   dY  [n_out, C_out]    float32 or bf16 (dtype)

@@ -34,6 +34,7 @@ EXPORTS = [
     "sbc_sampling_workspace_size", "sbc_sample_points",
     "sbc_lif_workspace_size", "sbc_lif_sample_events",
     "sbc_event_stream_workspace_size", "sbc_event_stream_step",
+    "sbc_conv_forward_noalloc_max_bytes", "sbc_conv_forward_noalloc",
 ]
 
 
@@ -114,6 +115,9 @@ _SIGS = {
                                       ctypes.c_int]),
     "sbc_conv_forward": (ctypes.c_int, [_csr_p, _vp, _geo_p, _i32, _vp, _vp, ctypes.c_int, _i32,
                                         _i32, _vp, ctypes.c_int, _vp, _sz, _vp]),
+    "sbc_conv_forward_noalloc_max_bytes": (_sz, []),
+    "sbc_conv_forward_noalloc": (ctypes.c_int, [_csr_p, _vp, _geo_p, _i32, _vp, _vp, ctypes.c_int,
+                                                _i32, _i32, _vp, ctypes.c_int, _vp]),
     "sbc_conv_backward": (ctypes.c_int, [_csr_p, _csc_p, _vp, _geo_p, _i32, _vp, _vp, _vp,
                                          ctypes.c_int, _i32, _i32, _vp, _vp, ctypes.c_int, _vp,
                                          _sz, _vp]),

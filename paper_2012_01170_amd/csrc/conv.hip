@@ -10,6 +10,9 @@
 // kernels (basis evaluated inside); other shapes and orders use the generic
 // kernels below, which evaluate the basis into the workspace first when v is
 // NULL.
+#include <mutex>
+#include <string>
+
 #include "basis.hpp"
 #include "common.hpp"
 #include "fused.hpp"
@@ -138,7 +141,9 @@ bool route_fused(Route r, int32_t M, int32_t Ci, int32_t Co, bool bf) {
 size_t route_bytes(Route r, int32_t n_out, int32_t n_in, int64_t nnz, int32_t M, int32_t Ci,
                    int32_t Co, bool bf) {
     if (route_fused(r, M, Ci, Co, bf))
-        return fused_workspace_bytes(M, Ci, Co, n_out > n_in ? n_out : n_in, nnz);
+        return r == kFwdSpmm
+                   ? fused_forward_workspace_bytes(M, Ci, Co, n_out > n_in ? n_out : n_in, nnz)
+                   : fused_workspace_bytes(M, Ci, Co, n_out > n_in ? n_out : n_in, nnz);
     size_t b = 0;
     carve_route(nullptr, r, n_out, n_in, nnz, M, Ci, Co, &b);
     return b;
@@ -261,12 +266,14 @@ extern "C" size_t sbc_conv_workspace_size(int32_t n_out, int32_t n_in, int64_t n
     return a > c ? a : c;
 }
 
-extern "C" sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v,
-                                       const sbc_geometry *geometry, int32_t M, const void *F,
-                                       const void *W, sbc_dtype dtype, int32_t C_in,
-                                       int32_t C_out, float *Y, sbc_order order, void *workspace,
-                                       size_t workspace_bytes, hipStream_t stream) {
-    clear_error();
+namespace sbc {
+namespace {
+
+// The forward pass with its temporary space in `workspace` (workspace_bytes of it).
+sbc_status conv_forward(const sbc_csr *csr, const float *v, const sbc_geometry *geometry,
+                        int32_t M, const void *F, const void *W, sbc_dtype dtype, int32_t C_in,
+                        int32_t C_out, float *Y, sbc_order order, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
     SBC_TRY(check_conv_args(csr, v, geometry, M, F, W, dtype, C_in, C_out));
     SBC_TRY(check_order(order));
     if (!Y && csr->n_rows > 0) return fail(SBC_ERR_INVALID_ARG, "Y is null");
@@ -301,6 +308,74 @@ extern "C" sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v,
                      true, csr->nnz_bound, Y, stream, "fwd_spmm_contract"));
     }
     return SBC_OK;
+}
+
+// ---------------------------------------------------------------- forward without allocation
+// Device memory of this library's own, for callers that cannot allocate: a
+// file-scope array that every GPU the library runs on holds for the life of
+// the process.  In host code `scratch` only names the symbol; its address on
+// the current device comes from hipGetSymbolAddress, taken once per device
+// (each device holds its own copy) and kept in g_scratch.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices] = {};
+
+// This device's scratch address (the symbol lookup runs on the first call on
+// each device, with that device current).
+sbc_status scratch_of_current_device(void **out) {
+    int dev = 0;
+    SBC_HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(SBC_ERR_INVALID_ARG, "device id out of range");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *ptr = nullptr;
+        SBC_HIP_TRY(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+        if (!ptr) return fail(SBC_ERR_HIP, "hipGetSymbolAddress gave no address for the scratch");
+        g_scratch[dev] = ptr;
+    }
+    *out = g_scratch[dev];
+    return SBC_OK;
+}
+
+}  // namespace
+}  // namespace sbc
+
+extern "C" sbc_status sbc_conv_forward(const sbc_csr *csr, const float *v,
+                                       const sbc_geometry *geometry, int32_t M, const void *F,
+                                       const void *W, sbc_dtype dtype, int32_t C_in,
+                                       int32_t C_out, float *Y, sbc_order order, void *workspace,
+                                       size_t workspace_bytes, hipStream_t stream) {
+    clear_error();
+    return conv_forward(csr, v, geometry, M, F, W, dtype, C_in, C_out, Y, order, workspace,
+                        workspace_bytes, stream);
+}
+
+extern "C" size_t sbc_conv_forward_noalloc_max_bytes(void) { return sbc::kScratchBytes; }
+
+extern "C" sbc_status sbc_conv_forward_noalloc(const sbc_csr *csr, const float *v,
+                                               const sbc_geometry *geometry, int32_t M,
+                                               const void *F, const void *W, sbc_dtype dtype,
+                                               int32_t C_in, int32_t C_out, float *Y,
+                                               sbc_order order, hipStream_t stream) {
+    clear_error();
+    SBC_TRY(check_conv_args(csr, v, geometry, M, F, W, dtype, C_in, C_out));
+    SBC_TRY(check_order(order));
+    const bool bf = dtype == SBC_BF16;
+    const Route r = forward_route(csr->n_rows, csr->n_cols, csr->nnz_bound, M, C_in, C_out, order,
+                                  bf);
+    const size_t need = route_bytes(r, csr->n_rows, csr->n_cols, csr->nnz_bound, M, C_in, C_out, bf);
+    if (need > kScratchBytes)
+        return fail(SBC_ERR_WORKSPACE, "this forward needs " + std::to_string(need) +
+                                           " bytes of temporary space; the library's static "
+                                           "scratch holds " + std::to_string(kScratchBytes) +
+                                           " (use sbc_conv_forward with a workspace)");
+    void *ws = nullptr;
+    SBC_TRY(scratch_of_current_device(&ws));
+    return conv_forward(csr, v, geometry, M, F, W, dtype, C_in, C_out, Y, order, ws,
+                        kScratchBytes, stream);
 }
 
 extern "C" sbc_status sbc_conv_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v,

@@ -1460,13 +1460,23 @@ size_t fused_workspace_bytes(int32_t M, int32_t CI, int32_t CO, int32_t n_points
            (M == 10 ? align_up((size_t)(nnz > 0 ? nnz : 0) * M * 4) : 0);
 }
 
+// The forward needs no dW partials: the weight copy, the packed events and
+// (M = 10) the basis values.
+size_t fused_forward_workspace_bytes(int32_t M, int32_t CI, int32_t CO, int32_t n_points,
+                                     int64_t nnz) {
+    return align_up((size_t)M * CI * CO * 4) +
+           align_up((size_t)(n_points > 0 ? n_points : 0) * sizeof(int4)) +
+           (M == 10 ? align_up((size_t)(nnz > 0 ? nnz : 0) * M * 4) : 0);
+}
+
 namespace {
 
 // Kernel geometry for a call: packs the event coordinates into the workspace
 // (after the weight copy and the dW partials) when the basis is evaluated
 // from an event stream.
-sbc_status make_kgeo(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,
-                     int32_t CI, int32_t CO, void *ws, hipStream_t stream, KGeo *kg) {
+// ev_offset: where the packed events go in the workspace.
+sbc_status make_kgeo(const sbc_csr *csr, const float *v, const sbc_geometry *g, size_t ev_offset,
+                     void *ws, hipStream_t stream, KGeo *kg) {
     *kg = KGeo{};
     kg->nnz = csr->nnz_bound > INT32_MAX ? INT32_MAX : (int32_t)csr->nnz_bound;
     if (v || !g) return SBC_OK;
@@ -1478,9 +1488,7 @@ sbc_status make_kgeo(const sbc_csr *csr, const float *v, const sbc_geometry *g, 
     if (g->basis == SBC_BASIS_EVENT8 || g->basis == SBC_BASIS_EVENT_DECAYS) {
         // event streams are in place: rows and columns index the same events
         const int32_t n = csr->n_cols > csr->n_rows ? csr->n_cols : csr->n_rows;
-        int4 *pk = reinterpret_cast<int4 *>(static_cast<char *>(ws) +
-                                            align_up((size_t)M * CI * CO * 4) +
-                                            align_up((size_t)kMaxBlocksBwd * (size_t)CI * M * CO * 4));
+        int4 *pk = reinterpret_cast<int4 *>(static_cast<char *>(ws) + ev_offset);
         if (n > 0) {
             int blocks = grid_for(n, 256);
             if (blocks > 2048) blocks = 2048;
@@ -1502,7 +1510,7 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
         // row-normalised values: materialised first, behind the other regions
         const int32_t n = csr->n_cols > csr->n_rows ? csr->n_cols : csr->n_rows;
         float *vm = reinterpret_cast<float *>(
-            static_cast<char *>(ws) + fused_workspace_bytes(M, CI, CO, n, 0));
+            static_cast<char *>(ws) + fused_forward_workspace_bytes(M, CI, CO, n, 0));
         SBC_TRY(basis_eval_launch(csr, g, vm, stream));
         v = vm;
     }
@@ -1510,7 +1518,8 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
     if (!fn) return fail(SBC_ERR_UNSUPPORTED, "no fused forward for this shape");
     if (csr->n_rows == 0) return SBC_OK;
     KGeo gr;
-    SBC_TRY(make_kgeo(csr, v, g, M, CI, CO, ws, stream, &gr));
+    // layout: [W copy][packed events][M = 10: basis values]
+    SBC_TRY(make_kgeo(csr, v, g, align_up((size_t)M * CI * CO * 4), ws, stream, &gr));
     if (RegFn rf = find_reg(Shape{M, CI, CO, bf}, basis_mode_of(v, g))) {
         const int32_t n_tiles = (csr->n_rows + 15) / 16;
         int per_cu = 0;
@@ -1559,7 +1568,11 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
     if (blocks > n_tiles) blocks = n_tiles;
     if (blocks < 1) blocks = 1;
     KGeo gg;
-    SBC_TRY(make_kgeo(csr, v, g, M, CI, CO, ws, stream, &gg));
+    // layout: [W copy][dW partials][packed events]
+    SBC_TRY(make_kgeo(csr, v, g,
+                      align_up((size_t)M * CI * CO * 4) +
+                          align_up((size_t)kMaxBlocksBwd * (size_t)CI * M * CO * 4),
+                      ws, stream, &gg));
     if (n_in > 0 && (dF || dW)) {
         trace_before(decay_derivative ? "decay_fused" : "bwd_fused", stream);
         hipLaunchKernelGGL(fn, dim3(blocks), dim3(nw * 64), 0, stream, n_in, n_tiles, csc->col_ptr,

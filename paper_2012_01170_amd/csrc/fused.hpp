@@ -16,6 +16,9 @@ bool fused_forward_available(int32_t M, int32_t CI, int32_t CO, bool bf);
 bool fused_backward_available(int32_t M, int32_t CI, int32_t CO, bool bf);
 // n_points: the larger of the input and output counts
 size_t fused_workspace_bytes(int32_t M, int32_t CI, int32_t CO, int32_t n_points, int64_t nnz);
+// the same for the forward alone (no dW partials)
+size_t fused_forward_workspace_bytes(int32_t M, int32_t CI, int32_t CO, int32_t n_points,
+                                     int64_t nnz);
 
 // Y = sum_m N^(m) F W^(m) in one kernel (plus a small weight re-layout for bf16).
 sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry *g, int32_t M,

@@ -334,6 +334,28 @@ def conv_forward(csr: CSR, F, W, geometry: Optional[Geometry] = None, v=None,
     return Y
 
 
+def conv_forward_noalloc(csr: CSR, F, W, Y, geometry: Optional[Geometry] = None, v=None,
+                         order: str = "auto") -> torch.Tensor:
+    """The forward into a caller-given Y [n_out, C_out] float32, with the
+    library's static scratch as its temporary space (sbc_conv_forward_noalloc):
+    nothing is allocated, by this binding or by the library."""
+    dev, M, C_in, C_out = _conv_common(csr, F, W, v, geometry)
+    _require(Y, "Y", torch.float32, 2, dev)
+    if tuple(Y.shape) != (csr.n_rows, C_out):
+        raise ValueError(f"Y must be [{csr.n_rows}, {C_out}], got {tuple(Y.shape)}")
+    c = csr.c_struct()
+    g = geometry.c_struct() if geometry is not None else None
+    L.check(L.lib().sbc_conv_forward_noalloc(
+        ctypes.byref(c), _p(v), ctypes.byref(g) if g is not None else None, M, _p(F), _p(W),
+        _dtype_code(F), C_in, C_out, _p(Y), ORDERS[order], _stream(dev)))
+    return Y
+
+
+def conv_forward_noalloc_max_bytes() -> int:
+    """Bytes of the static scratch sbc_conv_forward_noalloc works in."""
+    return int(L.lib().sbc_conv_forward_noalloc_max_bytes())
+
+
 def conv_backward(csr: CSR, csc: CSC, F, W, dY, geometry: Optional[Geometry] = None, v=None,
                   order: str = "auto", need_dF: bool = True, need_dW: bool = True):
     """(dF [n_in, C_in], dW [M, C_in, C_out]) float32 (sbc_conv_backward)."""

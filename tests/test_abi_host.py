@@ -175,3 +175,22 @@ def test_conv_plan(lib):
     p = ops.conv_plan(100, 100, 500, 8, 64, 64, order="gemm_first")
     assert p["forward_order"] == "gemm_first" and not p["forward_fused"]
     assert p["backward_order"] == "gemm_first" and not p["backward_fused"]
+
+
+def test_noalloc_forward_refusals(lib):
+    """The forward without a workspace reports its scratch size, checks its
+    arguments like the workspace forward, and refuses, before touching the
+    device, a forward whose temporary space exceeds the scratch."""
+    assert lib.sbc_conv_forward_noalloc_max_bytes() == 64 << 20
+    A = 1 << 20                     # stand-in device addresses, never dereferenced
+    g = L.SbcGeometry(L.SBC_BASIS_MONO8, 0.1, 0.0, 1, 1, 0, 0, 0)
+    csr = L.SbcCsr(10, 10, 40, 1, 1)
+    assert lib.sbc_conv_forward_noalloc(ctypes.byref(csr), None, ctypes.byref(g), 6, A, A, 0, 4,
+                                        4, A, 0, None) == 8
+    assert lib.sbc_conv_forward_noalloc(ctypes.byref(csr), None, ctypes.byref(g), 8, A + 4, A, 0,
+                                        4, 4, A, 0, None) == 1
+    # GEMM-first over 300k inputs: H alone is 300k x 8 x 32 floats (77 MB)
+    big = L.SbcCsr(300_000, 300_000, 0, 1, 1)
+    assert lib.sbc_conv_forward_noalloc(ctypes.byref(big), A, None, 8, A, A, 0, 32, 32, A,
+                                        L.SBC_ORDER_GEMM_FIRST, None) == 6
+    assert b"static scratch" in lib.sbc_last_error()
