@@ -315,7 +315,10 @@ sbc_status sbc_conv_forward_noalloc(const sbc_csr *csr, const float *v,
                                     float *Y, sbc_order order, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
- * 5. Backward: the gradients of <Y, dY> with respect to F and W.
+ * 5. Backward: the gradients of <Y, dY> with respect to F and W (Section 4,
+ * Table 2: the backward pass of the matrix-product form, its gradients with
+ * respect to the features and the kernel weights; as the forward, it can be
+ * evaluated in either order of the products, Section 3.1 and Table 1).
  *   dY  [n_out, C_out]    float32 or bf16 (dtype)
  *   dF  [n_in, C_in]      float32 output, or NULL to skip
  *   dW  [M, C_in, C_out]  float32 output, or NULL to skip
