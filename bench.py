@@ -216,6 +216,64 @@ def summarize_traffic(fetch_dir, write_dir, probe_mb, command):
     return "\n".join(out) + "\n"
 
 
+def _counter_by_kernel(directory, counter):
+    """Per profiled kernel (short name): the list of one counter's readings
+    over its dispatches, and the largest reading of a copy kernel (the probe)."""
+    per, probe = {}, 0.0
+    for r in _counter_rows(directory):
+        if r["Counter_Name"] != counter:
+            continue
+        if "copyBuffer" in r["Kernel_Name"]:
+            probe = max(probe, float(r["Counter_Value"]))
+            continue
+        per.setdefault(short_kernel_name(r["Kernel_Name"]), []).append(float(r["Counter_Value"]))
+    return per, probe
+
+
+def summarize_route(workload, runs, probe_mb, command, steps):
+    """Side-by-side summary of the evaluation orders of one workload (Table 1's
+    two orders): per order, the graph-timed step and its kernels' HIP-event
+    times, then per profiled kernel its dispatches per step, HBM bytes per
+    dispatch (FETCH_SIZE + WRITE_SIZE scaled by the copy probe) and MFMA-busy
+    cycles per dispatch (summed over SIMDs), and the step's totals.
+    runs: order -> (bench json, fetch dir, write dir, mfma dir); steps: the
+    profiled runs' step count (warm-up included)."""
+    out = ["# evaluation orders compared on one workload: step time, kernel times, HBM bytes "
+           "and MFMA-busy cycles",
+           "# (dispatches per step count the profiled run's warm-up and timed steps; the "
+           "search also runs twice while the benchmark is set up)", f"# command: {command}",
+           f"source_fingerprint: {source_fingerprint()}", f"workload: {workload}"]
+    for order, (bj, fdir, wdir, mdir) in runs.items():
+        with open(bj) as f:
+            b = json.loads([l for l in f if l.startswith("{")][-1])
+        fetch, probe_f = _counter_by_kernel(fdir, "FETCH_SIZE")
+        write, probe_w = _counter_by_kernel(wdir, "WRITE_SIZE")
+        mfma, _ = _counter_by_kernel(mdir, "SQ_VALU_MFMA_BUSY_CYCLES")
+        ff = probe_mb * 1024.0 / probe_f if probe_f else float("nan")
+        wf = probe_mb * 1024.0 / probe_w if probe_w else float("nan")
+        out.append(f"order {order}: plan {b['config']['plan']}; step {b['ms_per_step'] * 1e3:.1f} us "
+                   f"(graph replays)")
+        out.append("#   trace name  us  launches")
+        for k, v in b["kernels"].items():
+            out.append(f"  {order} time {k} {v['us']:.1f} {v['launches']}")
+        out.append("#   profiled kernel  dispatches_per_step  HBM_MB_per_dispatch  "
+                   "MFMA_busy_Mcycles_per_dispatch")
+        tot_b = tot_m = 0.0
+        for k in sorted(fetch, key=lambda k: -sum(fetch[k])):
+            if k not in write or k.startswith("vectorized_elementwise"):
+                continue  # torch's own fill of the copy probe
+            n = len(fetch[k])
+            mb = (statistics.mean(fetch[k]) * ff + statistics.mean(write[k]) * wf) * 1024.0 / 1e6
+            mc = statistics.mean(mfma[k]) / 1e6 if k in mfma else 0.0
+            per_step = n / steps
+            tot_b += mb * per_step
+            tot_m += mc * per_step
+            if mb * per_step >= 0.5 or mc > 0:
+                out.append(f"  {order} counters {k} {per_step:g} {mb:.1f} {mc:.2f}")
+        out.append(f"  {order} step_total HBM_MB {tot_b:.1f} MFMA_busy_Mcycles {tot_m:.2f}")
+    return "\n".join(out) + "\n"
+
+
 def summarize_trace(trace_dir, command, bench_json=None):
     """Text summary of a rocprofv3 --kernel-trace --stats run (top kernels by time)."""
     files = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
@@ -349,7 +407,9 @@ def kernel_table(kind, plan, n_in, n_out, E, M, ci, co, sf, blocks_bwd=256, npix
         t["bwd_gemm_dw_t"] = (1, n_in * ci * sf + D + 4 * M * ci * co, 2 * n_in * ci * M * co,
                               True)
     else:
-        basis_launches += 1
+        # an event stream's transpose comes from the search without edge
+        # positions: the transposed entries' values are evaluated once more
+        basis_launches += 2 if kind == "events" else 1
         G = 4 * n_out * M * ci
         t["bwd_spmm"] = (1, csr_b + n_in * ci * sf + G, 2 * E * M * ci, False)
         t["bwd_gemm_dw"] = (1, G + n_out * co * sf + 4 * M * ci * co, 2 * n_out * M * ci * co,
@@ -724,10 +784,22 @@ def main(argv=None):
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print per-dispatch HBM bytes from two rocprofv3 --pmc outputs and exit")
     ap.add_argument("--bench-json", help="with --summarize-trace: the profiled run's bench line")
+    ap.add_argument("--summarize-route", nargs="+", metavar="ARG",
+                    help="WORKLOAD then, per order, ORDER BENCH_JSON FETCH_DIR WRITE_DIR MFMA_DIR: "
+                         "print the evaluation orders side by side and exit")
     ap.add_argument("--command", default="", help="the profiled command, quoted in a summary")
     a = ap.parse_args(argv)
     if a.summarize_trace:
         sys.stdout.write(summarize_trace(a.summarize_trace, a.command, a.bench_json))
+        return 0
+    if a.summarize_route:
+        w, rest = a.summarize_route[0], a.summarize_route[1:]
+        if len(rest) % 5 or a.copy_probe_mb <= 0:
+            ap.error("--summarize-route: WORKLOAD (ORDER JSON FETCH WRITE MFMA)... and "
+                     "--copy-probe-mb")
+        runs = {rest[i]: tuple(rest[i + 1:i + 5]) for i in range(0, len(rest), 5)}
+        sys.stdout.write(summarize_route(w, runs, a.copy_probe_mb, a.command,
+                                         a.steps + a.warmup))
         return 0
     if a.summarize_traffic:
         if a.copy_probe_mb <= 0:
