@@ -170,6 +170,7 @@ __device__ __forceinline__ void merge_runs(const int32_t *Li, int32_t *lo, const
 
 struct TileArgs {
     int32_t n, W, H, window, tx, ty, tiles_x, n_tiles;
+    int32_t dirs;                          // workgroups per tile: 1, or 2 (rows, then columns)
     const int32_t *pix_start, *list, *list_t;
     int32_t *row_len, *col_len;            // count pass (col_len: null without the transpose)
     const int32_t *row_ptr, *col_ptr;      // fill pass (col_ptr: null without the transpose)
@@ -180,11 +181,12 @@ struct TileArgs {
 // Every event of the tile's pixels: its row (and column) length, or its row
 // (and column) entries.  c_off: prefix of the list lengths of the tile's own
 // pixels (nc + 1 entries); HX: halo row length.
+// dir: 0 rows and columns, 1 rows only, 2 columns only.
 template <int kSide, bool kFill>
 __device__ __forceinline__ void tile_events(const TileArgs &A, const int32_t *Li,
                                             const int32_t *Lt, const int32_t *start,
                                             const int32_t *len, const int32_t *c_off, int nc,
-                                            int HX) {
+                                            int HX, int dir) {
     constexpr int h = kSide / 2;
     constexpr int K = kSide * kSide;
     const int32_t total = c_off[nc];
@@ -199,15 +201,17 @@ __device__ __forceinline__ void tile_events(const TileArgs &A, const int32_t *Li
         const int32_t a = start[p] + (u - c_off[c]);
         const int32_t i = Li[a], ti = Lt[a];
         int32_t rlo[K], rhi[K];
-        const int32_t cnt = tile_runs<kSide, false>(i, ti, A.window, p, HX, Li, Lt, start, len,
-                                                    rlo, rhi);
-        if constexpr (!kFill) {
-            A.row_len[i] = cnt;
-        } else {
-            merge_runs<K>(Li, rlo, rhi, cnt, A.col_idx, A.row_ptr[i], A.cap);
+        if (dir != 2) {
+            const int32_t cnt = tile_runs<kSide, false>(i, ti, A.window, p, HX, Li, Lt, start,
+                                                        len, rlo, rhi);
+            if constexpr (!kFill) {
+                A.row_len[i] = cnt;
+            } else {
+                merge_runs<K>(Li, rlo, rhi, cnt, A.col_idx, A.row_ptr[i], A.cap);
+            }
         }
         const bool rev = kFill ? A.col_ptr != nullptr : A.col_len != nullptr;
-        if (rev) {
+        if (rev && dir != 1) {
             const int32_t cnt_t = tile_runs<kSide, true>(i, ti, A.window, p, HX, Li, Lt, start,
                                                          len, rlo, rhi);
             if constexpr (!kFill)
@@ -230,7 +234,11 @@ __global__ void __launch_bounds__(kTileThreads) event_tile_kernel(TileArgs A) {
     __shared__ int32_t s_idx[kTileCap], s_t[kTileCap];
     const int tid = threadIdx.x;
     const int64_t npix = (int64_t)A.W * A.H;
-    if ((int)blockIdx.x == A.n_tiles) {
+    // with two workgroups per tile, the first gives the tile's rows and the
+    // second its columns (twice the workgroups, half of each thread's chain)
+    const int32_t tile = (int32_t)blockIdx.x / A.dirs;
+    const int dir = A.dirs == 1 ? 0 : 1 + (int)(blockIdx.x % A.dirs);
+    if (tile == A.n_tiles) {
         // events off the sensor (sorted behind every pixel): empty rows and columns
         if constexpr (!kFill) {
             for (int32_t a = A.pix_start[npix] + tid; a < A.n; a += kTileThreads) {
@@ -242,8 +250,8 @@ __global__ void __launch_bounds__(kTileThreads) event_tile_kernel(TileArgs A) {
         return;
     }
     const int HX = A.tx + 2 * h, NP = HX * (A.ty + 2 * h), nc = A.tx * A.ty;
-    const int32_t tx0 = (int32_t)(blockIdx.x % A.tiles_x) * A.tx;
-    const int32_t ty0 = (int32_t)(blockIdx.x / A.tiles_x) * A.ty;
+    const int32_t tx0 = (tile % A.tiles_x) * A.tx;
+    const int32_t ty0 = (tile / A.tiles_x) * A.ty;
     int32_t len = 0, gs = 0;
     if (tid < NP) {
         const int32_t x = tx0 - h + tid % HX, y = ty0 - h + tid / HX;
@@ -290,9 +298,9 @@ __global__ void __launch_bounds__(kTileThreads) event_tile_kernel(TileArgs A) {
     }
     __syncthreads();
     if (staged)
-        tile_events<kSide, kFill>(A, s_idx, s_t, s_start, s_len, s_coff, nc, HX);
+        tile_events<kSide, kFill>(A, s_idx, s_t, s_start, s_len, s_coff, nc, HX, dir);
     else
-        tile_events<kSide, kFill>(A, A.list, A.list_t, s_gstart, s_len, s_coff, nc, HX);
+        tile_events<kSide, kFill>(A, A.list, A.list_t, s_gstart, s_len, s_coff, nc, HX, dir);
 }
 
 struct EventsWs {
@@ -332,7 +340,8 @@ EventsWs carve_events(void *base, int32_t n, int64_t npix, size_t *bytes) {
 template <bool kFill>
 sbc_status tiles_dispatch(int32_t half_extent, const TileArgs &A, hipStream_t stream) {
     const char *name = kFill ? "events_fill" : "events_count";
-    const dim3 grid((unsigned)(A.n_tiles + 1)), block(kTileThreads);
+    // n_tiles * dirs tile workgroups, then the one for the events off the sensor
+    const dim3 grid((unsigned)((int64_t)A.n_tiles * A.dirs + 1)), block(kTileThreads);
     trace_before(name, stream);
     switch (half_extent) {
         case 0: hipLaunchKernelGGL((event_tile_kernel<1, kFill>), grid, block, 0, stream, A); break;
@@ -387,6 +396,7 @@ sbc_status search_events(const int32_t *px, const int32_t *py, const int32_t *t,
     A.list = ws.list;
     A.list_t = ws.list_t;
     A.cap = col_capacity;
+    A.dirs = col_ptr ? 2 : 1;
 
     SBC_TRY(fill_i32(reinterpret_cast<int32_t *>(ws.status), 0, 1, stream));
     if (n == 0) SBC_TRY(fill_i32(ws.pix_start, 0, npix + 1, stream));
