@@ -144,30 +144,49 @@ def decay_backward(row_ptr, col_idx, v_deriv, F, W, dY):
     return out
 
 
-def deployment_stream(px, py, t, F, W, width, height, tau, z=None, last=None):
-    """The event convolution's deployment form (Section 3.2, Eq. 13-15), with
-    one decay rate 1/tau for every offset: each pixel x keeps z_x, the decayed
-    sum of the features of its events, and tau_x, the time of its last update
-    (both 0 at the start).  An event (x, t) with features f first reads its
-    output, sum over the 8 offsets u of exp(-(t - tau_q) / tau) z_q W_m(u) with
-    q = x - u on the sensor (the centre has no function), then updates its own
-    pixel: z_x <- f + exp(-(t - tau_x) / tau) z_x, tau_x <- t.  Events in
-    stream order, float64.  z [H, W, C_in] and last [H, W] carry the state
-    between calls (a stream fed in pieces); returns (Y, z, last)."""
+def deployment_stream(px, py, t, F, W, width, height, tau, z=None, last=None, decays=None):
+    """The event convolution's deployment form (Section 3.2, Eq. 13-15): each
+    pixel x keeps, for every basis function (u, v), z_x^(uv), the sum of the
+    features of its events decayed at rate lambda_uv, and tau_x, the time of
+    its last update (all 0 at the start).  An event (x, t) with features f
+    first reads its output, the sum over the 8 offsets u and the decays v of
+    exp(-lambda_uv (t - tau_q)) z_q^(uv) W_(u,v) with q = x - u on the sensor
+    (the centre has no function), then updates its own pixel:
+    z_x^(uv) <- f + exp(-lambda_uv (t - tau_x)) z_x^(uv), tau_x <- t.
+    Events in stream order, float64.
+
+    decays None: one rate 1/tau for every function (M_v = 1); every z^(u) of a
+    pixel is then the same, so one is kept, z [H, W, C_in], and W is
+    [8, C_in, C_out].  decays [8, M_v]: lambda_uv, z [H, W, 8, M_v, C_in] and W
+    [8 M_v, C_in, C_out] with function m = u M_v + v.  z and last carry the
+    state between calls (a stream fed in pieces); returns (Y, z, last)."""
     from .basis import event_offset_index
     C_in, C_out = W.shape[1], W.shape[2]
-    z = np.zeros((height, width, C_in)) if z is None else np.array(z, dtype=np.float64)
+    lam = (np.full((8, 1), 1.0 / tau) if decays is None
+           else np.asarray(decays, dtype=np.float64))
+    Mv = lam.shape[1]
+    shape = (height, width, C_in) if decays is None else (height, width, 8, Mv, C_in)
+    z = np.zeros(shape) if z is None else np.array(z, dtype=np.float64)
     last = np.zeros((height, width)) if last is None else np.array(last, dtype=np.float64)
+    state = (lambda y, x, u, v: z[y, x]) if decays is None else \
+        (lambda y, x, u, v: z[y, x, u, v])
     Y = np.zeros((len(t), C_out))
     for i in range(len(t)):
         x, y, ti = int(px[i]), int(py[i]), float(t[i])
         for uy in (-1, 0, 1):
             for ux in (-1, 0, 1):
-                m = int(event_offset_index(ux, uy))
+                u = int(event_offset_index(ux, uy))
                 qx, qy = x - ux, y - uy
-                if m < 0 or not (0 <= qx < width and 0 <= qy < height):
+                if u < 0 or not (0 <= qx < width and 0 <= qy < height):
                     continue
-                Y[i] += np.exp(-(ti - last[qy, qx]) / tau) * z[qy, qx] @ W[m]
-        z[y, x] = F[i] + np.exp(-(ti - last[y, x]) / tau) * z[y, x]
+                for v in range(Mv):
+                    Y[i] += (np.exp(-lam[u, v] * (ti - last[qy, qx])) * state(qy, qx, u, v)
+                             @ W[u * Mv + v])
+        if decays is None:
+            z[y, x] = F[i] + np.exp(-lam[0, 0] * (ti - last[y, x])) * z[y, x]
+        else:
+            for u in range(8):
+                for v in range(Mv):
+                    z[y, x, u, v] = F[i] + np.exp(-lam[u, v] * (ti - last[y, x])) * z[y, x, u, v]
         last[y, x] = ti
     return Y, z, last

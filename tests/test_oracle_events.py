@@ -133,25 +133,41 @@ def test_decays_equal_the_deployment_recursion():
     F = w["F"].astype(np.float64)
     W = rng.standard_normal((8 * Mv, w["C_in"], 2))
     Y = oracle.conv.forward(rp, ci, v, F, W)
-    z = np.zeros((w["height"], w["width"], 8, Mv, w["C_in"]))
-    last = np.zeros((w["height"], w["width"]))
-    Y_ema = np.zeros_like(Y)
-    for i in range(w["n_in"]):
-        x, y, t = int(w["px"][i]), int(w["py"][i]), float(w["t"][i])
-        for uy in (-1, 0, 1):
-            for ux in (-1, 0, 1):
-                u = int(oracle.basis.event_offset_index(ux, uy))
-                qx, qy = x - ux, y - uy
-                if u < 0 or not (0 <= qx < w["width"] and 0 <= qy < w["height"]):
-                    continue
-                for q in range(Mv):
-                    dec = np.exp(-lam[u, q] * (t - last[qy, qx]))
-                    Y_ema[i] += dec * z[qy, qx, u, q] @ W[u * Mv + q]
-        for u in range(8):
-            for q in range(Mv):
-                z[y, x, u, q] = F[i] + np.exp(-lam[u, q] * (t - last[y, x])) * z[y, x, u, q]
-        last[y, x] = t
+    Y_ema, z, _ = oracle.conv.deployment_stream(w["px"], w["py"], w["t"], F, W, w["width"],
+                                                w["height"], None, decays=lam)
     np.testing.assert_allclose(Y, Y_ema, rtol=1e-11, atol=1e-11)
+    assert z.shape == (w["height"], w["width"], 8, Mv, w["C_in"])
+
+
+def test_equal_decays_deploy_as_the_fixed_form():
+    """With every lambda_uv = 1/tau the per-(offset, decay) states of a pixel
+    coincide, and the learned-decay deployment form equals the fixed-decay one
+    with W_u = sum_v W_(u,v); fed in pieces it carries its state like one pass."""
+    w = workloads.small_events(seed=8, n=600, width=6, height=5, duration_us=4000, c=3)
+    rng = np.random.default_rng(9)
+    Mv = 3
+    lam = np.full((8, Mv), 1.0 / w["tau"])
+    F = w["F"].astype(np.float64)
+    W = rng.standard_normal((8 * Mv, w["C_in"], 4))
+    args = (w["width"], w["height"], w["tau"])
+    Y, z, last = oracle.conv.deployment_stream(w["px"], w["py"], w["t"], F, W, *args, decays=lam)
+    Y0, z0, last0 = oracle.conv.deployment_stream(w["px"], w["py"], w["t"], F,
+                                                  W.reshape(8, Mv, w["C_in"], 4).sum(axis=1),
+                                                  *args)
+    np.testing.assert_allclose(Y, Y0, rtol=1e-11, atol=1e-11)
+    for u in range(8):
+        for v in range(Mv):
+            np.testing.assert_allclose(z[:, :, u, v], z0, rtol=1e-13, atol=1e-13)
+    assert np.array_equal(last, last0)
+    lam2 = rng.uniform(0.5, 3.0, size=(8, Mv)) / w["tau"]
+    Y2, z2, l2 = oracle.conv.deployment_stream(w["px"], w["py"], w["t"], F, W, *args, decays=lam2)
+    Ys, zs, ls = [], None, None
+    for a, b in [(0, 250), (250, 251), (251, 600)]:
+        Yp, zs, ls = oracle.conv.deployment_stream(w["px"][a:b], w["py"][a:b], w["t"][a:b], F[a:b],
+                                                   W, *args, z=zs, last=ls, decays=lam2)
+        Ys.append(Yp)
+    np.testing.assert_allclose(np.concatenate(Ys), Y2, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(zs, z2, rtol=1e-13, atol=1e-13)
 
 
 def test_decay_gradient_matches_finite_differences():
