@@ -501,6 +501,35 @@ sbc_status sbc_event_stream_step(const int32_t *px, const int32_t *py, const int
                                  size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * 10. The deployment form with learned decays (Section 3.2, Eq. 12-15): the
+ * kernel of SBC_BASIS_EVENT_DECAYS, M_v = n_decays rates lambda_uv per offset
+ * u, run as a recursion.  A pixel keeps one decayed sum per basis function
+ * m = u * n_decays + v, since the functions of an offset decay at different
+ * rates:
+ *   Y[i] = sum over u, v of exp(-lambda_uv (t_i - z_time[q])) z[q, m] W[m],
+ *          q = (px_i - ux, py_i - uy) on the sensor,
+ * then z[x_i, m] = F[i] + exp(-lambda_uv (t_i - z_time[x_i])) z[x_i, m] for
+ * every m, z_time[x_i] = t_i.  With every lambda_uv = 1/tau this is section 9
+ * with W summed over v.
+ *   decays     [8, n_decays] float32 device, the rates lambda_uv (> 0, not
+ *              checked), 1 <= n_decays <= 4
+ *   W          [8 * n_decays, C_in, C_out] float32 device
+ *   z          [height * width, 8 * n_decays, C_in] float32 device, state;
+ *              z_time [height * width] int32 device, state (both zero at the
+ *              start, caller-owned)
+ * Everything else, including the workspace, errors and synchronisation, is as
+ * in section 9.  The workspace query returns 0 for invalid sizes.
+ * ------------------------------------------------------------------------ */
+size_t sbc_event_stream_decays_workspace_size(int32_t n, int32_t width, int32_t height,
+                                              int32_t n_decays, int32_t C_in, int32_t C_out);
+sbc_status sbc_event_stream_step_decays(const int32_t *px, const int32_t *py, const int32_t *t,
+                                        const float *F, int32_t n, int32_t width, int32_t height,
+                                        const float *decays, int32_t n_decays, const float *W,
+                                        int32_t C_in, int32_t C_out, float *z, int32_t *z_time,
+                                        float *Y, void *workspace, size_t workspace_bytes,
+                                        hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Tracing, for measurement tools.  After sbc_trace_kernel(name, start, stop)
  * every launch of the kernel called `name` made by the calling thread records
  * `start` immediately before and `stop` immediately after itself on its

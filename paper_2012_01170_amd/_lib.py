@@ -34,6 +34,7 @@ EXPORTS = [
     "sbc_sampling_workspace_size", "sbc_sample_points",
     "sbc_lif_workspace_size", "sbc_lif_sample_events",
     "sbc_event_stream_workspace_size", "sbc_event_stream_step",
+    "sbc_event_stream_decays_workspace_size", "sbc_event_stream_step_decays",
     "sbc_conv_forward_noalloc_max_bytes", "sbc_conv_forward_noalloc",
 ]
 
@@ -102,6 +103,10 @@ _SIGS = {
     "sbc_event_stream_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32]),
     "sbc_event_stream_step": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _f32, _vp,
                                              _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "sbc_event_stream_decays_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),
+    "sbc_event_stream_step_decays": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _vp,
+                                                    _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp,
+                                                    _sz, _vp]),
     "sbc_decay_gradient_workspace_size": (_sz, [_i32, _i64, _i32, _i32, _i32, ctypes.c_int]),
     "sbc_conv_decay_gradient": (ctypes.c_int, [_csr_p, _csc_p, _geo_p, _i32, _vp, _vp, _vp,
                                                ctypes.c_int, _i32, _i32, _vp, _vp, _sz, _vp]),

@@ -513,15 +513,32 @@ def lif_sample_events(px, py, t, width: int, height: int, kernel: int = 3, strid
 
 class EventStream:
     """The state of the event convolution's deployment form (Eq. 13-15) over
-    a width x height sensor: z [height * width, C_in] and z_time [height *
-    width], zero at the start.  step() feeds one batch (sbc_event_stream_step)
-    and returns its outputs Y [n, C_out]."""
+    a width x height sensor, zero at the start, and step(), which feeds one
+    batch and returns its outputs Y [n, C_out].
 
-    def __init__(self, width: int, height: int, C_in: int, tau: float, device="cuda"):
+    decays None: the fixed decay, rate 1/tau for every offset
+    (sbc_event_stream_step); z [height * width, C_in], W [8, C_in, C_out].
+    decays [8, M_v] float32 (learned rates lambda_uv, Eq. 12): one sum per
+    basis function (sbc_event_stream_step_decays); z [height * width, 8 M_v,
+    C_in], W [8 M_v, C_in, C_out], function m = u M_v + v.  z_time [height *
+    width] int32 either way."""
+
+    def __init__(self, width: int, height: int, C_in: int, tau: float = None, device="cuda",
+                 decays: torch.Tensor = None):
         self.width, self.height, self.C_in, self.tau = int(width), int(height), int(C_in), tau
-        self.z = torch.zeros((self.width * self.height, self.C_in), dtype=torch.float32,
-                             device=device)
-        self.z_time = torch.zeros(self.width * self.height, dtype=torch.int32, device=device)
+        npix = self.width * self.height
+        if decays is None:
+            if tau is None or not tau > 0:
+                raise ValueError("tau > 0 expected without decays")
+            self.decays, self.M = None, 8
+            self.z = torch.zeros((npix, self.C_in), dtype=torch.float32, device=device)
+        else:
+            _require(decays, "decays", torch.float32, 2, torch.device(device))
+            if decays.shape[0] != 8 or not 1 <= decays.shape[1] <= 4:
+                raise ValueError("decays [8, M_v] with 1 <= M_v <= 4 expected")
+            self.decays, self.M = decays.contiguous(), 8 * int(decays.shape[1])
+            self.z = torch.zeros((npix, self.M, self.C_in), dtype=torch.float32, device=device)
+        self.z_time = torch.zeros(npix, dtype=torch.int32, device=device)
 
     def step(self, px, py, t, F, W) -> torch.Tensor:
         dev = self.z.device
@@ -532,17 +549,26 @@ class EventStream:
         _require(W, "W", torch.float32, 3, dev)
         n = int(px.numel())
         if int(py.numel()) != n or int(t.numel()) != n or F.shape != (n, self.C_in) \
-                or W.shape[:2] != (8, self.C_in):
-            raise ValueError("px, py, t [n], F [n, C_in] and W [8, C_in, C_out] expected")
+                or W.shape[:2] != (self.M, self.C_in):
+            raise ValueError(f"px, py, t [n], F [n, C_in] and W [{self.M}, C_in, C_out] expected")
         C_out = int(W.shape[2])
         Y = torch.empty((max(n, 1), C_out), dtype=torch.float32, device=dev)
         lib = L.lib()
-        ws = _Workspace(lib.sbc_event_stream_workspace_size(n, self.width, self.height,
-                                                            self.C_in, C_out), dev)
-        L.check(lib.sbc_event_stream_step(_p(px), _p(py), _p(t), _p(F), n, self.width,
-                                          self.height, float(self.tau), _p(W), self.C_in, C_out,
-                                          _p(self.z), _p(self.z_time), _p(Y), ws.ptr, ws.nbytes,
-                                          _stream(dev)))
+        if self.decays is None:
+            ws = _Workspace(lib.sbc_event_stream_workspace_size(n, self.width, self.height,
+                                                                self.C_in, C_out), dev)
+            L.check(lib.sbc_event_stream_step(_p(px), _p(py), _p(t), _p(F), n, self.width,
+                                              self.height, float(self.tau), _p(W), self.C_in,
+                                              C_out, _p(self.z), _p(self.z_time), _p(Y), ws.ptr,
+                                              ws.nbytes, _stream(dev)))
+        else:
+            Mv = self.M // 8
+            ws = _Workspace(lib.sbc_event_stream_decays_workspace_size(
+                n, self.width, self.height, Mv, self.C_in, C_out), dev)
+            L.check(lib.sbc_event_stream_step_decays(
+                _p(px), _p(py), _p(t), _p(F), n, self.width, self.height, _p(self.decays), Mv,
+                _p(W), self.C_in, C_out, _p(self.z), _p(self.z_time), _p(Y), ws.ptr, ws.nbytes,
+                _stream(dev)))
         return Y[:n]
 
 

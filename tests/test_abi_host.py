@@ -47,6 +47,24 @@ def test_workspace_queries(lib):
     s2 = lib.sbc_conv_workspace_size(1000, 1000, 8000, 8, 16, 16, L.SBC_F32, L.SBC_ORDER_GEMM_FIRST)
     assert s1 > 8000 * 8 * 4 and s2 > 8000 * 8 * 4
     assert lib.sbc_conv_workspace_size(-1, 10, 10, 8, 1, 1, 0, 0) == 0
+    # the learned-decay stream keeps M = 8 M_v gathered rows per event
+    s8 = lib.sbc_event_stream_workspace_size(4096, 128, 128, 32, 32)
+    s16 = lib.sbc_event_stream_decays_workspace_size(4096, 128, 128, 2, 32, 32)
+    assert s8 > 4096 * 8 * 32 * 4 and s16 >= s8 + 4096 * 8 * 32 * 4
+    assert lib.sbc_event_stream_decays_workspace_size(4096, 128, 128, 1, 32, 32) >= s8
+    assert lib.sbc_event_stream_decays_workspace_size(4096, 128, 128, 5, 32, 32) == 0
+    assert lib.sbc_event_stream_decays_workspace_size(4096, 128, 128, 0, 32, 32) == 0
+
+
+def test_stream_decays_argument_errors(lib):
+    """Refusals the library decides before any device work."""
+    L.lib()
+    st = lib.sbc_event_stream_step_decays(None, None, None, None, 0, 8, 8, None, 2, None, 4, 4,
+                                          None, None, None, None, 0, None)
+    assert st == 1 and b"decays" in lib.sbc_last_error()
+    st = lib.sbc_event_stream_step_decays(None, None, None, None, 0, 8, 8, None, 5, None, 4, 4,
+                                          None, None, None, None, 0, None)
+    assert st == 1 and b"n_decays" in lib.sbc_last_error()
 
 
 def test_basis_sizes_and_strings(lib):

@@ -113,18 +113,24 @@ def test_lif_graph_replays_match_eager():
         assert torch.isfinite(junk)
 
 
-def test_event_stream_graph_replays_match_eager():
-    """Three batches of the deployment form, the state reset at the start,
-    captured in a graph: every replay reproduces the eager outputs and final
-    state bit for bit."""
-    print("[graph] event stream", flush=True)
+@pytest.mark.parametrize("Mv", [0, 2])
+def test_event_stream_graph_replays_match_eager(Mv):
+    """Three batches of the deployment form (fixed decay, or two learned
+    decays per offset), the state reset at the start, captured in a graph:
+    every replay reproduces the eager outputs and final state bit for bit."""
+    print(f"[graph] event stream Mv {Mv}", flush=True)
     rng = np.random.default_rng(51)
     n, Wd, H = 6000, 24, 18
     px, py, t, _ = workloads.uniform_events(rng, n, Wd, H, 40_000)
+    M = 8 * max(Mv, 1)
     F = torch.from_numpy(rng.standard_normal((n, 8)).astype(np.float32)).to(G.DEV)
-    W = torch.from_numpy((rng.standard_normal((8, 8, 16)) / 8).astype(np.float32)).to(G.DEV)
+    W = torch.from_numpy((rng.standard_normal((M, 8, 16)) / 8).astype(np.float32)).to(G.DEV)
     ev = [torch.from_numpy(a).to(G.DEV) for a in (px, py, t)]
-    st = G.sbc.EventStream(Wd, H, 8, 2500.0, device=G.DEV)
+    if Mv:
+        lam = torch.from_numpy(rng.uniform(1e-4, 1e-3, (8, Mv)).astype(np.float32)).to(G.DEV)
+        st = G.sbc.EventStream(Wd, H, 8, device=G.DEV, decays=lam)
+    else:
+        st = G.sbc.EventStream(Wd, H, 8, 2500.0, device=G.DEV)
 
     def step():
         st.z.zero_()

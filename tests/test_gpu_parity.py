@@ -839,6 +839,75 @@ def test_event_stream_matches_the_recursion(pieces, P):
     assert np.array_equal(st.z_time.cpu().numpy(), last_ref.reshape(-1).astype(np.int32))
 
 
+@pytest.mark.parametrize("Mv,C_in,pieces", [(1, 10, [4000]), (2, 6, [1, 1999, 0, 2000]),
+                                             (3, 5, [700, 3300]), (4, 10, [2500, 1500])])
+def test_event_stream_learned_decays(Mv, C_in, pieces):
+    """The deployment form with learned decays (M_v rates per offset, a state
+    per basis function) fed in batches against the oracle's recursion over
+    the whole stream: outputs and final state within 1e-5, times exact.  Ten
+    input channels give three 4-channel chunks per state, so one pixel's
+    threads straddle waves."""
+    print(f"[stream] decays Mv {Mv} C_in {C_in} pieces {pieces}", flush=True)
+    rng = np.random.default_rng(52 + Mv)
+    n, Wd, H, P = 4000, 18, 14, 12
+    px, py, t, _ = workloads.uniform_events(rng, n, Wd, H, 40_000)
+    lam = rng.uniform(1 / 20_000, 1 / 500, (8, Mv)).astype(np.float32)
+    F = rng.standard_normal((n, C_in)).astype(np.float32)
+    W = (rng.standard_normal((8 * Mv, C_in, P)) / np.sqrt(8 * Mv * C_in)).astype(np.float32)
+    Y_ref, z_ref, last_ref = oracle.conv.deployment_stream(
+        px, py, t, F.astype(np.float64), W.astype(np.float64), Wd, H, None,
+        decays=lam.astype(np.float64))
+    st = G.sbc.EventStream(Wd, H, C_in, device=G.DEV, decays=G.dev(lam))
+    Wdev = G.dev(W)
+    Ys, a = [], 0
+    for k in pieces:
+        b = a + k
+        Ys.append(st.step(G.dev(px[a:b]), G.dev(py[a:b]), G.dev(t[a:b]), G.dev(F[a:b]), Wdev)
+                  .cpu().numpy())
+        a = b
+    assert a == n
+    err = G.row_error(np.concatenate(Ys), Y_ref)
+    zerr = G.row_error(st.z.cpu().numpy().reshape(-1, C_in), z_ref.reshape(-1, C_in))
+    print(f"    Y {err:.2e}  z {zerr:.2e}", flush=True)
+    assert err < 1e-5 and zerr < 1e-5
+    assert np.array_equal(st.z_time.cpu().numpy(), last_ref.reshape(-1).astype(np.int32))
+
+
+def test_event_stream_wide_fixed_decay_state():
+    """The fixed-decay form with ten input channels (three chunks a pixel, a
+    pixel's threads in two waves) and one batch: times and state exact to
+    the recursion within 1e-5."""
+    print("[stream] fixed decay C_in 10", flush=True)
+    rng = np.random.default_rng(56)
+    n, Wd, H, tau = 3000, 12, 10, 4000.0
+    px, py, t, _ = workloads.uniform_events(rng, n, Wd, H, 30_000)
+    F = rng.standard_normal((n, 10)).astype(np.float32)
+    W = (rng.standard_normal((8, 10, 4)) / 9).astype(np.float32)
+    Y_ref, z_ref, last_ref = oracle.conv.deployment_stream(px, py, t, F.astype(np.float64),
+                                                           W.astype(np.float64), Wd, H, tau)
+    st = G.sbc.EventStream(Wd, H, 10, tau, device=G.DEV)
+    Y = st.step(G.dev(px), G.dev(py), G.dev(t), G.dev(F), G.dev(W)).cpu().numpy()
+    err = G.row_error(Y, Y_ref)
+    zerr = G.row_error(st.z.cpu().numpy(), z_ref.reshape(-1, 10))
+    print(f"    Y {err:.2e}  z {zerr:.2e}", flush=True)
+    assert err < 1e-5 and zerr < 1e-5
+    assert np.array_equal(st.z_time.cpu().numpy(), last_ref.reshape(-1).astype(np.int32))
+
+
+def test_event_stream_decays_rejects_bad_arguments():
+    """Rates of the wrong shape, too many decays and a mismatched W are refused."""
+    print("[stream] decays refusals", flush=True)
+    with pytest.raises(ValueError, match="M_v"):
+        G.sbc.EventStream(8, 8, 4, device=G.DEV, decays=G.dev(np.ones((8, 5), np.float32)))
+    with pytest.raises(ValueError, match="tau"):
+        G.sbc.EventStream(8, 8, 4, device=G.DEV)
+    st = G.sbc.EventStream(8, 8, 4, device=G.DEV, decays=G.dev(np.ones((8, 2), np.float32)))
+    e = G.dev(np.zeros(3, np.int32))
+    with pytest.raises(ValueError, match="16"):
+        st.step(e, e, e, G.dev(np.zeros((3, 4), np.float32)),
+                G.dev(np.zeros((8, 4, 2), np.float32)))
+
+
 def test_event_stream_full_size_batches():
     """The benchmarked form: the 300k-event stream (128 x 128, 32 -> 32
     channels, tau 10 ms) in batches of 4096; sampled outputs of the last batch
