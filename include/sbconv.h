@@ -397,8 +397,9 @@ sbc_status sbc_featureless_backward(const sbc_csr *csr, const float *v,
  *                                   in input order; if rejection takes more,
  *                                   the first per_cloud of them).
  * Distances are compared as float32 squared distances in the canonical form of
- * the neighbour search; ties go to the lowest index.  Results are exact and
- * deterministic.
+ * the neighbour search; ties go to the lowest index, and the farthest-point
+ * steps choose among the points not yet taken, so no point is output twice
+ * (coincident points included).  Results are exact and deterministic.
  *   x [n_points, 3], splits [n_batch + 1]  device; clouds of at most max_cloud
  *                                          <= 8192 points (a larger cloud gets
  *                                          no outputs)

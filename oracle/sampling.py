@@ -26,9 +26,11 @@ def ifp(x, splits, counts):
     with every distance infinite, repeatedly take the point farthest from the
     points taken so far (argmax; the printed argmin is read as argmax, since
     with infinite initial distances argmin would take the first point again)
-    and lower every distance to the new point.  Returns the global indices of
-    each cloud's counts[b] points in the order taken, and the final squared
-    distances [n]."""
+    and lower every distance to the new point.  The choice is among the points
+    not yet taken (the farthest *remaining* point; it matters only once every
+    remaining distance is 0, i.e. for coincident points).  Returns the global
+    indices of each cloud's counts[b] points in the order taken, and the final
+    squared distances [n]."""
     x = np.asarray(x, dtype=np.float32)
     out = []
     dall = np.full(len(x), np.inf, dtype=np.float32)
@@ -36,8 +38,10 @@ def ifp(x, splits, counts):
         s, e = int(splits[b]), int(splits[b + 1])
         xb = x[s:e]
         dmin = dall[s:e]
+        taken = np.zeros(e - s, dtype=bool)
         for _ in range(int(counts[b])):
-            j = int(np.argmax(dmin))         # first index of the maximum
+            j = int(np.argmax(np.where(taken, -1.0, dmin)))   # first index of the maximum
+            taken[j] = True
             out.append(s + j)
             dmin[:] = np.minimum(dmin, _d2(xb, j))
     return np.asarray(out, dtype=np.int32), dall
@@ -68,24 +72,28 @@ def rejection_sampling(x, splits, row_ptr, col_idx):
     return taken, dmin
 
 
-def approx_ifp(x, splits, counts, row_ptr, col_idx, dmin=None):
+def approx_ifp(x, splits, counts, row_ptr, col_idx, dmin=None, taken=None):
     """Farthest points with distance updates limited to the ball neighbourhood
     of each taken point (the supplementary's approximate variant with a
-    priority queue): take the input of largest d_min (ties: lowest index),
-    then lower the d_min of its neighbours to their distance from it.  dmin:
-    initial squared distances (rejection sampling's, for the variant that
-    continues after it), else infinite.  Returns the global indices taken,
-    cloud by cloud, counts[b] per cloud, and the final squared distances."""
+    priority queue): take the remaining input of largest d_min (ties: lowest
+    index; the queue gives up each input once, so a taken input is never
+    taken again), then lower the d_min of its neighbours to their distance
+    from it.  dmin: initial squared distances (rejection sampling's, for the
+    variant that continues after it), else infinite; taken: inputs already
+    taken (bool [n]), else none.  Returns the global indices taken, cloud by
+    cloud, counts[b] per cloud, and the final squared distances."""
     x = np.asarray(x, dtype=np.float32)
     row_ptr = np.asarray(row_ptr, dtype=np.int64)
     col_idx = np.asarray(col_idx, dtype=np.int64)
     d = (np.full(len(x), np.inf, dtype=np.float32) if dmin is None
          else np.array(dmin, dtype=np.float32))
+    done = np.zeros(len(x), dtype=bool) if taken is None else np.array(taken, dtype=bool)
     out = []
     for b in range(len(splits) - 1):
         s, e = int(splits[b]), int(splits[b + 1])
         for _ in range(int(counts[b])):
-            j = s + int(np.argmax(d[s:e]))
+            j = s + int(np.argmax(np.where(done[s:e], -1.0, d[s:e])))
+            done[j] = True
             out.append(j)
             nb = col_idx[row_ptr[j]:row_ptr[j + 1]]
             dd = x[nb] - x[j]
@@ -107,7 +115,9 @@ def approx_ifp_after_rejection(x, splits, per_cloud, row_ptr, col_idx):
         s, e = int(splits[b]), int(splits[b + 1])
         S = min(int(per_cloud), e - s)
         first = (s + np.nonzero(taken[s:e])[0])[:S]
-        more, d = approx_ifp(x, [s, e], [S - len(first)], row_ptr, col_idx, d)
+        kept = np.zeros(len(x), dtype=bool)
+        kept[first] = True
+        more, d = approx_ifp(x, [s, e], [S - len(first)], row_ptr, col_idx, d, kept)
         out.extend(first.tolist())
         out.extend(more.tolist())
     return np.asarray(out, dtype=np.int32), d

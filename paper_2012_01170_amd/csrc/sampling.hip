@@ -12,9 +12,9 @@
 //     else rejected.  The lowest undecided point always decides, so the rounds
 //     end, and a decision depends only on final states, so the result is the
 //     sequential one whatever the timing;
-//   - farthest points: each step is an argmax over the cloud (ties to the
-//     lowest index), then the distances are lowered to the new point (all of
-//     them, or its ball neighbours).
+//   - farthest points: each step is an argmax over the points not yet taken
+//     (ties to the lowest index), then the distances are lowered to the new
+//     point (all of them, or its ball neighbours).
 // Squared distances are float32 in the canonical form of the neighbour search,
 // so every choice is exact.
 #include "common.hpp"
@@ -143,12 +143,14 @@ __global__ void __launch_bounds__(kSampThreads) sample_kernel(SampleArgs A) {
         pos = cap;
     }
     for (int32_t it = pos; it < total; ++it) {
-        // argmax of the distances, ties to the lowest index
+        // argmax of the distances over the points not yet taken, ties to the
+        // lowest index (a taken point is never taken again, which matters
+        // once every remaining distance is 0: coincident points)
         float bv = -1.f;
         int32_t bi = 0;
         for (int32_t j = tid; j < n; j += kSampThreads) {
             const float d = s_d[j];
-            if (d > bv) { bv = d; bi = j; }
+            if (s_st[j] != 1 && d > bv) { bv = d; bi = j; }
         }
         s_bv[tid] = bv;
         s_bi[tid] = bi;
@@ -165,7 +167,10 @@ __global__ void __launch_bounds__(kSampThreads) sample_kernel(SampleArgs A) {
             __syncthreads();
         }
         const int32_t sel = s_bi[0];
-        if (tid == 0) A.out_idx[base + it] = s + sel;
+        if (tid == 0) {
+            A.out_idx[base + it] = s + sel;
+            s_st[sel] = 1;  // read again only after the barrier closing this step
+        }
         if (approx) {
             const int32_t e0 = A.row_ptr[s + sel], e1 = A.row_ptr[s + sel + 1];
             for (int32_t e = e0 + tid; e < e1; e += kSampThreads) {

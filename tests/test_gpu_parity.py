@@ -647,17 +647,25 @@ def test_decay_gradient(name, route):
 
 
 # ---------------------------------------------------------------- subsampling
-def _sampling_batch(seed, sizes):
+def _sampling_batch(seed, sizes, doubled=False):
+    """Ellipsoid clouds; doubled: each cloud is sizes[b] / 2 distinct points
+    followed by a copy of each (coincident points)."""
     rng = np.random.default_rng(seed)
-    xs = [workloads.ellipsoid_surface_points(rng, n, rng.uniform(0.5, 1.0, size=3))
-          if n else np.zeros((0, 3)) for n in sizes]
+    xs = []
+    for n in sizes:
+        m = n // 2 if doubled else n
+        c = (workloads.ellipsoid_surface_points(rng, m, rng.uniform(0.5, 1.0, size=3))
+             if m else np.zeros((0, 3)))
+        xs.append(np.concatenate([c, c]) if doubled else c)
     x = np.concatenate(xs).astype(np.float32)
     return x, np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
 
 
+# (seed, cloud sizes, ball radius, points per cloud[, doubled])
 SAMPLING_CASES = {"small": (30, [300, 0, 1, 450], 0.2, 100),
                   "c2_clouds": (31, [1024] * 32, 0.1, 256),
-                  "large_cloud": (32, [8192, 700], 0.05, 2000)}
+                  "large_cloud": (32, [8192, 700], 0.05, 2000),
+                  "coincident_whole_clouds": (33, [80, 600, 2], 0.15, 600, True)}
 
 
 @pytest.mark.parametrize("method", ["ifp", "approx_ifp", "rejection", "approx_ifp_rejection"])
@@ -665,8 +673,8 @@ SAMPLING_CASES = {"small": (30, [300, 0, 1, 450], 0.2, 100),
 def test_sampling_bit_exact(case_name, method):
     """Indices, bounds and squared distances equal the oracle's exactly."""
     print(f"[sampling] {case_name} {method}", flush=True)
-    seed, sizes, radius, per = SAMPLING_CASES[case_name]
-    x, splits = _sampling_batch(seed, sizes)
+    seed, sizes, radius, per, *doubled = SAMPLING_CASES[case_name]
+    x, splits = _sampling_batch(seed, sizes, bool(doubled))
     rp, ci = oracle.points_csr(x, splits, x, splits, radius, 0)
     xd, sd = G.dev(x), G.dev(splits)
     ball = G.sbc.neighbour_search_points(xd, sd, xd, sd, radius, 0)
@@ -687,6 +695,8 @@ def test_sampling_bit_exact(case_name, method):
     if method == "rejection":
         want = np.searchsorted(ref, splits)      # taken points per cloud, in order
         assert np.array_equal(osp, want)
+    elif doubled:                                # whole clouds: every point once
+        assert sorted(ref.tolist()) == list(range(len(x)))
 
 
 # ---------------------------------------------------------------- LIF event sampler

@@ -24,6 +24,22 @@ def _clouds(seed, sizes, scale=1.0):
     return x, splits
 
 
+def _farthest_remaining(x, s, e, count):
+    """Brute force: each step recomputes every remaining point's distance to
+    its nearest chosen point and takes the largest (lowest index on ties)."""
+    chosen = []
+    for _ in range(count):
+        best, arg = -1.0, -1
+        for j in range(s, e):
+            if j in chosen:
+                continue
+            dj = min((_d2(x[j], x[c]) for c in chosen), default=np.float32(np.inf))
+            if dj > best:
+                best, arg = dj, j
+        chosen.append(arg)
+    return chosen
+
+
 @pytest.mark.parametrize("seed", [0, 1])
 def test_ifp_matches_brute_force(seed):
     x, splits = _clouds(seed, [37, 1, 25])
@@ -32,18 +48,34 @@ def test_ifp_matches_brute_force(seed):
     k = 0
     for b in range(3):
         s, e = splits[b], splits[b + 1]
-        chosen = []
-        for _ in range(counts[b]):
-            # the distance of every point to its nearest chosen point, afresh
-            best, arg = -1.0, -1
-            for j in range(s, e):
-                dj = min((_d2(x[j], x[c]) for c in chosen), default=np.float32(np.inf))
-                if dj > best:
-                    best, arg = dj, j
-            chosen.append(arg)
+        chosen = _farthest_remaining(x, s, e, counts[b])
         assert got[k:k + counts[b]].tolist() == chosen
         assert chosen[0] == s                  # all distances infinite: the first point
         k += counts[b]
+
+
+def _doubled(seed, n):
+    """A cloud of n distinct points followed by a copy of each."""
+    x, _ = _clouds(seed, [n])
+    return np.concatenate([x, x]), np.array([0, 2 * n], np.int32)
+
+
+def test_coincident_points_are_each_taken_once():
+    """With every point doubled, asking for the whole cloud takes every index
+    once: after the distinct points the remaining distances are all 0, and
+    the farthest remaining point is the lowest remaining index.  Exact IFP
+    against the brute force; the ball-limited variant and rejection followed
+    by it give permutations."""
+    x, splits = _doubled(5, 20)
+    got, d = oracle.sampling.ifp(x, splits, [40])
+    assert got.tolist() == _farthest_remaining(x, 0, 40, 40)
+    assert sorted(got.tolist()) == list(range(40)) and not d.any()
+    assert sorted(got[20:].tolist()) == list(range(20, 40))    # the copies come last
+    rp, ci = _ball(x, splits, 0.3)
+    a, _ = oracle.sampling.approx_ifp(x, splits, [40], rp, ci)
+    assert sorted(a.tolist()) == list(range(40))
+    r, _ = oracle.sampling.approx_ifp_after_rejection(x, splits, 40, rp, ci)
+    assert sorted(r.tolist()) == list(range(40))
 
 
 def _ball(x, splits, radius):
