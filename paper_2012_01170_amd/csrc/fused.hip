@@ -238,6 +238,7 @@ struct GatherAhead {
     int32_t bound;
     int32_t idx0;
     bool have_idx;
+    int32_t idx1;  // the one-hot gather's second chunk: idx[first edge + 64 + lane]
 };
 
 template <int M, int C, int kBasis, bool kXbf, bool kOutBf, bool kT, int RPW, bool kPipelined>
@@ -448,6 +449,172 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
     if (kPipelined && next_row_begin >= 0) {
         const int32_t nb0 = __shfl(next_bound, 0, 64), nb1 = __shfl(next_bound, RPW, 64);
         ahead.idx0 = nb0 + lane < nb1 ? idx[nb0 + lane] : 0;
+        ahead.have_idx = true;
+    }
+    return ahead;
+}
+
+// ---------------------------------------------------------------- one-hot event gather
+// The fixed-decay event basis (SBC_BASIS_EVENT8) has one nonzero value per
+// edge, at the offset index k of its pixel step (none for a same-pixel edge),
+// so a gathered row's sum over its edges only adds each edge into one of the
+// M = 8 column blocks.  gather_rows_onehot builds the same tile rows as
+// gather_rows without the other seven products.  Per chunk of 64 edges:
+//   1. the endpoint coordinates of each edge are loaded (its offset index and
+//      decay), then the chunk's 64 neighbour rows are copied into LDS by the
+//      direct global-to-LDS loads, all in one memory round trip;
+//   2. one wave ballot per offset marks the chunk's edges of that offset;
+//   3. lane (row r, offset m, channel part h) walks the set bits of its
+//      offset's ballot within row r's lanes, lowest first, and adds up those
+//      rows, CH channels of each, from LDS.
+// So a (row, offset) sum takes its edges in pattern order, one product each.
+// The neighbour indices of a wave's first two chunks are loaded one call
+// ahead.
+template <int C>
+struct OneHotStage {
+    float f[64][C];             // the chunk's neighbour rows (direct loads)
+    int32_t nb[64];             // neighbour index of each staged edge
+    float sv[64];               // basis value of each staged edge
+    int32_t bounds[17];         // pattern bounds of the wave's rows
+};
+
+// Bits [0, n) of a 64-bit lane mask.
+__device__ __forceinline__ uint64_t lanes_below(int n) {
+    return n >= 64 ? ~0ull : (n <= 0 ? 0ull : ((1ull << n) - 1ull));
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int C, int RPW, bool kT>
+__device__ __forceinline__ GatherAhead gather_rows_onehot(
+    int32_t row_begin, int32_t n_rows, const int32_t *__restrict__ ptr,
+    const int32_t *__restrict__ idx, const KGeo &g, const float *__restrict__ X, float *out_tile,
+    int S, int local_row0, OneHotStage<C> &st, float inv_tau, GatherAhead pre,
+    int32_t next_row_begin) {
+    constexpr int M = 8;
+    constexpr int H = 64 / (RPW * M);          // lanes sharing a bucket (channel parts)
+    static_assert(H >= 1 && RPW * M * H == 64 && RPW <= 16, "a lane per (row, offset, part)");
+    constexpr int CH = C / H;                  // channels per lane
+    constexpr int NP = CH / 4;                 // 16-byte pieces per lane
+    static_assert(CH % 4 == 0 && C % 4 == 0, "16-byte pieces");
+    constexpr int P = C / 4;                   // 16-byte pieces per row
+    static_assert(64 % P == 0, "whole rows per direct load");
+    constexpr int RPL = 64 / P;                // rows per direct load instruction
+    const int lane = threadIdx.x & 63;
+    // this lane's bucket
+    const int br = lane / (M * H), bm = (lane / H) % M, bh = lane % H;
+
+    if (lane <= RPW) st.bounds[lane] = pre.bound;
+    const int32_t next_bound =
+        next_row_begin >= 0 ? load_bound<RPW>(ptr, n_rows, next_row_begin, g.nnz) : 0;
+    wave_lds_sync();
+    const int32_t wb = st.bounds[0], we = st.bounds[RPW];
+    const int32_t brs = st.bounds[br], bre = st.bounds[br + 1];
+    float acc[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) acc[c] = 0.f;
+
+#pragma unroll 1
+    for (int32_t c0 = wb; c0 < we; c0 += 64) {
+        const int32_t e = c0 + lane;
+        const bool has = e < we;
+        int32_t other = 0, s = 0;
+        if (has) {
+#pragma unroll
+            for (int q = 1; q < RPW; ++q)
+                if (st.bounds[q] <= e) s = q;
+            other = !pre.have_idx || c0 > wb + 64 ? idx[e] : (c0 == wb ? pre.idx0 : pre.idx1);
+        }
+        const int32_t other0 = __shfl(other, 0, 64);  // lane 0 always holds an edge
+        other = has ? other : other0;
+        // 1. the edge's offset index and decay (its endpoints' coordinates), then
+        // the neighbour rows into LDS: instruction q copies rows q*RPL .. q*RPL+RPL-1
+        int4 ga = make_int4(0, 0, 0, 0), gb = ga;
+        if (has) {
+            const int32_t row = row_begin + s;
+            ga = g.ev[kT ? other : row];
+            gb = g.ev[kT ? row : other];
+        }
+        st.nb[lane] = other;
+        wave_lds_sync();
+#pragma unroll
+        for (int q = 0; q < P; ++q) {
+            const int32_t src = st.nb[q * RPL + lane / P];
+            const float *gp = X + (int64_t)src * C + 4 * (lane % P);
+            __builtin_amdgcn_global_load_lds((const void *)gp,
+                                             (lds_void_t *)&st.f[q * RPL][0], 16, 0, 0);
+        }
+        const int k = has ? event_index(ga.x - gb.x, ga.y - gb.y) : -1;
+        st.sv[lane] = has ? event_decay(ga.z, gb.z, inv_tau) : 0.f;
+        // 2. this lane's bucket: the lanes of its row with its offset
+        uint64_t bsel = 0ull;
+#pragma unroll
+        for (int kk = 0; kk < M; ++kk) {
+            const uint64_t bk = __ballot(k == kk);
+            if (kk == bm) bsel = bk;
+        }
+        {
+            const int32_t lo = (brs > c0 ? brs : c0) - c0;
+            const int32_t hi = (bre < c0 + 64 ? bre : c0 + 64) - c0;
+            bsel &= lanes_below(hi) & ~lanes_below(lo);
+        }
+        int32_t steps = __popcll(bsel);
+#pragma unroll
+        for (int dd = 1; dd < 64; dd <<= 1) {
+            const int32_t o = __shfl_xor(steps, dd, 64);
+            steps = o > steps ? o : steps;
+        }
+        wave_lds_sync();
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the direct loads have landed
+        // 3. the bucket's rows, four at a time, lowest lane first: the reads of a
+        // group are issued (by the lanes whose bucket reaches that far) before
+        // its products, which take weight 0 past the bucket's end
+#pragma unroll 1
+        for (int32_t q0 = 0; q0 < steps; q0 += 4) {
+            int32_t li[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                li[u] = bsel != 0ull ? (int32_t)__builtin_ctzll(bsel) : 64;
+                bsel &= bsel - 1ull;
+            }
+            float vv[4];
+            float4 x[4][NP];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                vv[u] = 0.f;
+#pragma unroll
+                for (int c = 0; c < NP; ++c) x[u][c] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (li[u] < 64) {
+                    vv[u] = st.sv[li[u]];
+                    const float4 *fr = reinterpret_cast<const float4 *>(&st.f[li[u]][bh * CH]);
+                    // pieces in an order rotated by the offset, so the lanes of one
+                    // LDS cycle read different banks (rows are 128 B apart)
+#pragma unroll
+                    for (int c = 0; c < NP; ++c) x[u][c] = fr[(c + bm) % NP];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int c = 0; c < NP; ++c) {
+                    acc[4 * c] += vv[u] * x[u][c].x;
+                    acc[4 * c + 1] += vv[u] * x[u][c].y;
+                    acc[4 * c + 2] += vv[u] * x[u][c].z;
+                    acc[4 * c + 3] += vv[u] * x[u][c].w;
+                }
+        }
+        wave_lds_sync();  // the stage is rewritten by the next chunk
+    }
+    float4 *o = reinterpret_cast<float4 *>(out_tile + (int64_t)(local_row0 + br) * S + bm * C +
+                                           bh * CH);
+#pragma unroll
+    for (int c = 0; c < NP; ++c)
+        o[(c + bm) % NP] = make_float4(acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]);
+    GatherAhead ahead{next_bound, 0, false, 0};
+    if (next_row_begin >= 0) {
+        const int32_t nb0 = __shfl(next_bound, 0, 64), nb1 = __shfl(next_bound, RPW, 64);
+        ahead.idx0 = nb0 + lane < nb1 ? idx[nb0 + lane] : 0;
+        ahead.idx1 = nb0 + 64 + lane < nb1 ? idx[nb0 + 64 + lane] : 0;
         ahead.have_idx = true;
     }
     return ahead;
@@ -965,7 +1132,14 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     using DT = typename std::conditional<kBf, uint16_t, float>::type;
     __shared__ __attribute__((aligned(16))) DT Ds[2][TR * SD];
     __shared__ __attribute__((aligned(16))) DT Fs[2][TR * SF];
-    __shared__ EdgeStage<M> stage[kWsGather];
+    // the fixed-decay event basis in float32 takes the one-hot gather
+    // while its stage (a chunk of neighbour rows per gather wave) fits in LDS
+    constexpr bool kOneHot =
+        kBasis == SBC_BASIS_EVENT8 + 1 && M == 8 && !kBf && RPW * M <= 64 &&
+        64 % (RPW * M) == 0 &&
+        2 * TR * (SD + SF) * sizeof(float) + kWsGather * sizeof(OneHotStage<CO>) <= 163840;
+    using Stage = typename std::conditional<kOneHot, OneHotStage<CO>, EdgeStage<M>>::type;
+    __shared__ __attribute__((aligned(16))) Stage stage[kWsGather];
 
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
@@ -1014,9 +1188,14 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
             }
         }
         const int32_t next = s + 1 < n_my ? (t_first + (s + 1) * gx) * TR + w * RPW : -1;
-        ahead = gather_rows<M, CO, kBasis, kBf, kBf, true, RPW, true>(
-            row0 + w * RPW, n_in, col_ptr, row_idx, perm, v, g, dY, Ds[buf], SD, w * RPW,
-            stage[w], inv_r, inv_tau, ahead, next);
+        if constexpr (kOneHot)
+            ahead = gather_rows_onehot<CO, RPW, true>(
+                row0 + w * RPW, n_in, col_ptr, row_idx, g, static_cast<const float *>(dY),
+                Ds[buf], SD, w * RPW, stage[w], inv_tau, ahead, next);
+        else
+            ahead = gather_rows<M, CO, kBasis, kBf, kBf, true, RPW, true>(
+                row0 + w * RPW, n_in, col_ptr, row_idx, perm, v, g, dY, Ds[buf], SD, w * RPW,
+                stage[w], inv_r, inv_tau, ahead, next);
     };
 
     // The two roles run separate loops (so the matrix waves' dW accumulators
