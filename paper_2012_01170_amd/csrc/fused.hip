@@ -782,6 +782,45 @@ __device__ __forceinline__ int32_t xcd_tile(int32_t b, int32_t n) {
     return x < rem ? x * (per + 1) + l : rem * (per + 1) + (x - rem) * per + l;
 }
 
+// First tile of XCD x's range when the persistent kernels split n_tiles tiles
+// of TR rows over X XCDs: the ranges hold equal shares of the work estimate
+// (edges + kRowCost per row, from the pattern's pointer array), so an XCD
+// whose part of a bursty stream is dense gets fewer tiles.  Every block of
+// the range still takes a fixed set of its tiles, so results do not depend
+// on timing.
+constexpr int64_t kRowCost = 8;
+
+__device__ __forceinline__ int32_t xcd_range_begin(int32_t x, int32_t X, int32_t n_tiles, int TR,
+                                                   const int32_t *__restrict__ ptr,
+                                                   int32_t n_rows, int32_t nnz) {
+    if (x <= 0) return 0;
+    if (x >= X) return n_tiles;
+    auto work = [&](int32_t t) {  // work estimate of the rows before tile t
+        int32_t r = t * TR;
+        r = r < n_rows ? r : n_rows;
+        int32_t e = ptr[r];
+        e = e < 0 ? 0 : (e < nnz ? e : nnz);
+        return (int64_t)e + kRowCost * r;
+    };
+    const int64_t target = (work(n_tiles) * x) / X;
+    if (target <= 0) return 0;
+    // the first tile t with work(t) >= target, in (lo, hi]: each round the 64
+    // lanes of the wave probe 64 points of the interval (work(0) = 0 < target)
+    const int lane = threadIdx.x & 63;
+    int32_t lo = 0, hi = n_tiles;
+    while (hi - lo > 1) {
+        const int64_t span = hi - lo;
+        const int32_t t = lo + (int32_t)(((lane + 1) * span + 63) / 64);
+        const uint64_t ge = __ballot(work(t) >= target);  // lane 63 probes hi: always set
+        const int f = __builtin_ctzll(ge);
+        const int32_t nhi = lo + (int32_t)(((f + 1) * span + 63) / 64);
+        const int32_t nlo = f == 0 ? lo : lo + (int32_t)((f * span + 63) / 64);
+        lo = nlo;
+        hi = nhi;
+    }
+    return hi;
+}
+
 // ================================================================ forward
 constexpr int kFwdWaves = 4;
 
@@ -925,8 +964,8 @@ __global__ void __launch_bounds__(kRegWaves * 64)
     const int32_t gx = G / X + (x < G % X ? 1 : 0);
     const int32_t waves_x = gx * kRegWaves;
     const int32_t lw = (blockIdx.x / X) * kRegWaves + w;
-    const int32_t t_begin = (int32_t)((int64_t)x * n_tiles / X);
-    const int32_t t_end = (int32_t)((int64_t)(x + 1) * n_tiles / X);
+    const int32_t t_begin = xcd_range_begin(x, X, n_tiles, 16, row_ptr, n_out, g.nnz);
+    const int32_t t_end = xcd_range_begin(x + 1, X, n_tiles, 16, row_ptr, n_out, g.nnz);
 
 #pragma unroll 1
     for (int32_t tile = t_begin + lw; tile < t_end; tile += waves_x) {
@@ -1154,8 +1193,8 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     const int32_t G = gridDim.x, X = G < 8 ? G : 8;
     const int32_t x = blockIdx.x % X, l = blockIdx.x / X;
     const int32_t gx = G / X + (x < G % X ? 1 : 0);
-    const int32_t t_first = (int32_t)((int64_t)x * n_tiles / X) + l;
-    const int32_t t_end = (int32_t)((int64_t)(x + 1) * n_tiles / X);
+    const int32_t t_first = xcd_range_begin(x, X, n_tiles, TR, col_ptr, n_in, g.nnz) + l;
+    const int32_t t_end = xcd_range_begin(x + 1, X, n_tiles, TR, col_ptr, n_in, g.nnz);
     const int32_t n_my = t_first < t_end ? (t_end - t_first + gx - 1) / gx : 0;
 
     // row bounds (and first neighbour indices) of the gather's next tile,
