@@ -470,9 +470,9 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
 // So a (row, offset) sum takes its edges in pattern order, one product each.
 // The neighbour indices of a wave's first two chunks are loaded one call
 // ahead.
-template <int C>
+template <int RB>  // bytes per gathered row
 struct OneHotStage {
-    float f[64][C];             // the chunk's neighbour rows (direct loads)
+    uint4 f[64][RB / 16];       // the chunk's neighbour rows (direct loads)
     int32_t nb[64];             // neighbour index of each staged edge
     float sv[64];               // basis value of each staged edge
     int32_t bounds[17];         // pattern bounds of the wave's rows
@@ -485,21 +485,33 @@ __device__ __forceinline__ uint64_t lanes_below(int n) {
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-template <int C, int RPW, bool kT>
+// Element k of a 16-byte piece of float32 (4) or bf16 (8) values, as float32.
+template <bool kBf>
+__device__ __forceinline__ float piece_elem(const uint4 &x, int k) {
+    const uint32_t w = k < (kBf ? 2 : 1) ? x.x : k < (kBf ? 4 : 2) ? x.y : k < (kBf ? 6 : 3) ? x.z : x.w;
+    if constexpr (kBf) return __uint_as_float((k & 1) ? (w & 0xFFFF0000u) : (w << 16));
+    else return __uint_as_float(w);
+}
+
+// X [*, C] float32 or bf16 (kBf), tile rows of the same type.
+template <int C, int RPW, bool kT, bool kBf>
 __device__ __forceinline__ GatherAhead gather_rows_onehot(
     int32_t row_begin, int32_t n_rows, const int32_t *__restrict__ ptr,
-    const int32_t *__restrict__ idx, const KGeo &g, const float *__restrict__ X, float *out_tile,
-    int S, int local_row0, OneHotStage<C> &st, float inv_tau, GatherAhead pre,
+    const int32_t *__restrict__ idx, const KGeo &g, const void *__restrict__ X, void *out_tile,
+    int S, int local_row0, OneHotStage<C * (kBf ? 2 : 4)> &st, float inv_tau, GatherAhead pre,
     int32_t next_row_begin) {
     constexpr int M = 8;
+    constexpr int ES = kBf ? 2 : 4;            // bytes per element
+    constexpr int VPP = 16 / ES;               // values per 16-byte piece
     constexpr int H = 64 / (RPW * M);          // lanes sharing a bucket (channel parts)
     static_assert(H >= 1 && RPW * M * H == 64 && RPW <= 16, "a lane per (row, offset, part)");
     constexpr int CH = C / H;                  // channels per lane
-    constexpr int NP = CH / 4;                 // 16-byte pieces per lane
-    static_assert(CH % 4 == 0 && C % 4 == 0, "16-byte pieces");
-    constexpr int P = C / 4;                   // 16-byte pieces per row
+    static_assert(CH % VPP == 0, "whole 16-byte pieces per lane");
+    constexpr int NP = CH / VPP;               // 16-byte pieces per lane
+    constexpr int P = C / VPP;                 // 16-byte pieces per row
     static_assert(64 % P == 0, "whole rows per direct load");
     constexpr int RPL = 64 / P;                // rows per direct load instruction
+    constexpr int U = NP <= 4 ? 4 : 2;         // bucket rows read together
     const int lane = threadIdx.x & 63;
     // this lane's bucket
     const int br = lane / (M * H), bm = (lane / H) % M, bh = lane % H;
@@ -540,7 +552,7 @@ __device__ __forceinline__ GatherAhead gather_rows_onehot(
 #pragma unroll
         for (int q = 0; q < P; ++q) {
             const int32_t src = st.nb[q * RPL + lane / P];
-            const float *gp = X + (int64_t)src * C + 4 * (lane % P);
+            const char *gp = static_cast<const char *>(X) + ((int64_t)src * C) * ES + 16 * (lane % P);
             __builtin_amdgcn_global_load_lds((const void *)gp,
                                              (lds_void_t *)&st.f[q * RPL][0], 16, 0, 0);
         }
@@ -566,50 +578,62 @@ __device__ __forceinline__ GatherAhead gather_rows_onehot(
         }
         wave_lds_sync();
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the direct loads have landed
-        // 3. the bucket's rows, four at a time, lowest lane first: the reads of a
+        // 3. the bucket's rows, U at a time, lowest lane first: the reads of a
         // group are issued (by the lanes whose bucket reaches that far) before
         // its products, which take weight 0 past the bucket's end
 #pragma unroll 1
-        for (int32_t q0 = 0; q0 < steps; q0 += 4) {
-            int32_t li[4];
+        for (int32_t q0 = 0; q0 < steps; q0 += U) {
+            int32_t li[U];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < U; ++u) {
                 li[u] = bsel != 0ull ? (int32_t)__builtin_ctzll(bsel) : 64;
                 bsel &= bsel - 1ull;
             }
-            float vv[4];
-            float4 x[4][NP];
+            float vv[U];
+            uint4 x[U][NP];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < U; ++u) {
                 vv[u] = 0.f;
 #pragma unroll
-                for (int c = 0; c < NP; ++c) x[u][c] = make_float4(0.f, 0.f, 0.f, 0.f);
+                for (int c = 0; c < NP; ++c) x[u][c] = uint4{0u, 0u, 0u, 0u};
                 if (li[u] < 64) {
                     vv[u] = st.sv[li[u]];
-                    const float4 *fr = reinterpret_cast<const float4 *>(&st.f[li[u]][bh * CH]);
                     // pieces in an order rotated by the offset, so the lanes of one
                     // LDS cycle read different banks (rows are 128 B apart)
 #pragma unroll
-                    for (int c = 0; c < NP; ++c) x[u][c] = fr[(c + bm) % NP];
+                    for (int c = 0; c < NP; ++c) x[u][c] = st.f[li[u]][bh * NP + (c + bm) % NP];
                 }
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < U; ++u)
 #pragma unroll
-                for (int c = 0; c < NP; ++c) {
-                    acc[4 * c] += vv[u] * x[u][c].x;
-                    acc[4 * c + 1] += vv[u] * x[u][c].y;
-                    acc[4 * c + 2] += vv[u] * x[u][c].z;
-                    acc[4 * c + 3] += vv[u] * x[u][c].w;
-                }
+                for (int c = 0; c < NP; ++c)
+#pragma unroll
+                    for (int q = 0; q < VPP; ++q)
+                        acc[VPP * c + q] += vv[u] * piece_elem<kBf>(x[u][c], q);
         }
         wave_lds_sync();  // the stage is rewritten by the next chunk
     }
-    float4 *o = reinterpret_cast<float4 *>(out_tile + (int64_t)(local_row0 + br) * S + bm * C +
-                                           bh * CH);
+    // this lane's (row, offset, part) block of the tile row; piece c of acc is
+    // piece (c + bm) % NP of the block
+    char *o = static_cast<char *>(out_tile) +
+              ((int64_t)(local_row0 + br) * S + bm * C + bh * CH) * ES;
 #pragma unroll
-    for (int c = 0; c < NP; ++c)
-        o[(c + bm) % NP] = make_float4(acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]);
+    for (int c = 0; c < NP; ++c) {
+        uint4 v;
+        if constexpr (kBf) {
+            uint32_t w[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                w[q] = (uint32_t)f2bf(acc[VPP * c + 2 * q]) |
+                       ((uint32_t)f2bf(acc[VPP * c + 2 * q + 1]) << 16);
+            v = uint4{w[0], w[1], w[2], w[3]};
+        } else {
+            v = uint4{__float_as_uint(acc[VPP * c]), __float_as_uint(acc[VPP * c + 1]),
+                      __float_as_uint(acc[VPP * c + 2]), __float_as_uint(acc[VPP * c + 3])};
+        }
+        *reinterpret_cast<uint4 *>(o + 16 * ((c + bm) % NP)) = v;
+    }
     GatherAhead ahead{next_bound, 0, false, 0};
     if (next_row_begin >= 0) {
         const int32_t nb0 = __shfl(next_bound, 0, 64), nb1 = __shfl(next_bound, RPW, 64);
@@ -1174,10 +1198,12 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     // the fixed-decay event basis in float32 takes the one-hot gather
     // while its stage (a chunk of neighbour rows per gather wave) fits in LDS
     constexpr bool kOneHot =
-        kBasis == SBC_BASIS_EVENT8 + 1 && M == 8 && !kBf && RPW * M <= 64 &&
-        64 % (RPW * M) == 0 &&
-        2 * TR * (SD + SF) * sizeof(float) + kWsGather * sizeof(OneHotStage<CO>) <= 163840;
-    using Stage = typename std::conditional<kOneHot, OneHotStage<CO>, EdgeStage<M>>::type;
+        kBasis == SBC_BASIS_EVENT8 + 1 && M == 8 && RPW * M <= 64 && 64 % (RPW * M) == 0 &&
+        (CO * sizeof(DT)) % 16 == 0 && 64 % (CO * sizeof(DT) / 16) == 0 &&
+        2 * TR * (SD + SF) * sizeof(DT) + kWsGather * sizeof(OneHotStage<CO * sizeof(DT)>) <=
+            163840;
+    using Stage = typename std::conditional<kOneHot, OneHotStage<CO * sizeof(DT)>,
+                                            EdgeStage<M>>::type;
     __shared__ __attribute__((aligned(16))) Stage stage[kWsGather];
 
     const int lane = threadIdx.x & 63;
@@ -1228,9 +1254,9 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
         }
         const int32_t next = s + 1 < n_my ? (t_first + (s + 1) * gx) * TR + w * RPW : -1;
         if constexpr (kOneHot)
-            ahead = gather_rows_onehot<CO, RPW, true>(
-                row0 + w * RPW, n_in, col_ptr, row_idx, g, static_cast<const float *>(dY),
-                Ds[buf], SD, w * RPW, stage[w], inv_tau, ahead, next);
+            ahead = gather_rows_onehot<CO, RPW, true, kBf>(
+                row0 + w * RPW, n_in, col_ptr, row_idx, g, dY, Ds[buf], SD, w * RPW, stage[w],
+                inv_tau, ahead, next);
         else
             ahead = gather_rows<M, CO, kBasis, kBf, kBf, true, RPW, true>(
                 row0 + w * RPW, n_in, col_ptr, row_idx, perm, v, g, dY, Ds[buf], SD, w * RPW,
