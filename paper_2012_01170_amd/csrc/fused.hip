@@ -907,6 +907,86 @@ __global__ void __launch_bounds__(kFwdWaves * 64, fwd_tile_rows(M * CI, CO, kBf)
             }
 }
 
+// ================================================================ row order
+// The register-resident forward runs a tile's 16 rows in step, as long as its
+// longest row.  Rows are ordered by length within windows of kOrderWindow
+// consecutive rows (longest first, ties by index): a tile then holds rows of
+// similar length, while a window stays a short stretch of the pattern (the
+// rows an XCD gathers stay local to its L2).  order[p] is the row at
+// position p; each row's result is the same whatever tile it is in.
+// A wave sorts a window in registers (four rows a lane, a bitonic network
+// whose cross-lane steps are lane shuffles).
+constexpr int kOrderWindow = 256;
+constexpr int kOrderThreads = 256;  // a window per wave
+
+__global__ void __launch_bounds__(kOrderThreads)
+    row_order_kernel(int32_t n_rows, const int32_t *__restrict__ ptr, int32_t nnz,
+                     int32_t *__restrict__ order) {
+    const int lane = threadIdx.x & 63;
+    const int32_t win = blockIdx.x * (kOrderThreads / 64) + (threadIdx.x >> 6);
+    const int32_t r0 = win * kOrderWindow;
+    if (r0 >= n_rows) return;
+    // key: (longest first) length complement above the index in the window;
+    // positions past the last row sort behind every row
+    uint32_t k[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int32_t r = r0 + 4 * lane + j;
+        k[j] = 0xFFFFFFFFu;
+        if (r < n_rows) {
+            int32_t a = ptr[r], b = ptr[r + 1];
+            a = a < 0 ? 0 : (a < nnz ? a : nnz);
+            b = b < a ? a : (b < nnz ? b : nnz);
+            const uint32_t len = (uint32_t)(b - a) < 0xFFFFFFu ? (uint32_t)(b - a) : 0xFFFFFFu;
+            k[j] = ((0xFFFFFFu - len) << 8) | (uint32_t)(4 * lane + j);
+        }
+    }
+    // bitonic sort, ascending, of element i = 4 lane + j
+#pragma unroll
+    for (int size = 2; size <= kOrderWindow; size <<= 1) {
+#pragma unroll
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            if (stride >= 4) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t o = __shfl_xor(k[j], stride >> 2, 64);
+                    const int i = 4 * lane + j;
+                    const bool asc = (i & size) == 0, lower = (i & stride) == 0;
+                    k[j] = (asc == lower) ? (k[j] < o ? k[j] : o) : (k[j] > o ? k[j] : o);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (j & stride) continue;
+                    const int i = 4 * lane + j;
+                    const bool asc = (i & size) == 0;
+                    const uint32_t x = k[j], y = k[j | stride];
+                    if ((x > y) == asc) {
+                        k[j] = y;
+                        k[j | stride] = x;
+                    }
+                }
+            }
+        }
+    }
+    // The persistent forward hands each wave tiles a fixed stride apart, often a
+    // multiple of a window's tiles, so a wave would sit at the same place in
+    // every window: a full window's tiles are rotated by a hash of its index
+    // (the last, partial window keeps its rows in front).  Position q = 4 lane
+    // + j takes sorted element ((q / 16 + rot) % 16) * 16 + q % 16, which has
+    // the same j.
+    constexpr int kTiles = kOrderWindow / 16;
+    const bool full = r0 + kOrderWindow <= n_rows;
+    const uint32_t rot = full ? ((uint32_t)win * 2654435761u) >> 28 : 0u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int q = 4 * lane + j;
+        const int src = (int)(((uint32_t)(q / 16) + rot) % kTiles) * 16 + q % 16;
+        const uint32_t key = __shfl(k[j], src >> 2, 64);
+        if (r0 + q < n_rows) order[r0 + q] = r0 + (int32_t)(key & 255u);
+    }
+}
+
 // ================================================================ forward, G in registers
 // Each wave owns tiles of 16 output rows: lane l serves row (l & 15) and
 // channel group g = l >> 4, i.e. channels [g*CI/4, (g+1)*CI/4) of every basis
@@ -945,7 +1025,7 @@ __global__ void __launch_bounds__(kRegWaves * 64)
     fwd_reg_kernel(int32_t n_out, int32_t n_tiles, const int32_t *__restrict__ row_ptr,
                    const int32_t *__restrict__ col_idx, const float *__restrict__ v,
                    KGeo g, const void *__restrict__ Fv, const void *__restrict__ Wv,
-                   float *__restrict__ Y) {
+                   float *__restrict__ Y, const int32_t *__restrict__ order) {
     constexpr int K = M * CI;
     constexpr int CG = CI / 4;          // channels per lane group
     constexpr int NCB = CO / 16;        // 16-column blocks of Y
@@ -993,7 +1073,8 @@ __global__ void __launch_bounds__(kRegWaves * 64)
 
 #pragma unroll 1
     for (int32_t tile = t_begin + lw; tile < t_end; tile += waves_x) {
-        const int32_t row = tile * 16 + rl;
+        // the tile's rows: positions tile*16 .. tile*16+15 of the row order
+        const int32_t row = tile * 16 + rl < n_out ? order[tile * 16 + rl] : n_out;
         int32_t e0 = 0, e1 = 0;
         if (row < n_out) {
             e0 = row_ptr[row];
@@ -1121,12 +1202,16 @@ __global__ void __launch_bounds__(kRegWaves * 64)
                     __builtin_amdgcn_sched_barrier(0);
                 }
         }
-        // D layout: lane holds rows 4*(l >> 4) + r, column l & 15 of each block
+        // D layout: lane holds tile rows 4*(l >> 4) + r, column l & 15 of each
+        // block; lane 4 g + r (row 4 g + r of the tile) knows that row's index
+        int32_t yrow[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) yrow[r] = __shfl(row, 4 * gq + r, 64);
 #pragma unroll
         for (int nb = 0; nb < NCB; ++nb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int32_t yr = tile * 16 + 4 * gq + r;
+                const int32_t yr = yrow[r];
                 if (yr < n_out) Y[(int64_t)yr * CO + 16 * nb + rl] = ay[nb][r];
             }
     }
@@ -1519,7 +1604,7 @@ __global__ void w_perm_f32_kernel(const float *__restrict__ W, int32_t M, int32_
 using FwdFn = void (*)(int32_t, const int32_t *, const int32_t *, const float *, KGeo,
                        const void *, const void *, float *);
 using RegFn = void (*)(int32_t, int32_t, const int32_t *, const int32_t *, const float *,
-                       KGeo, const void *, const void *, float *);
+                       KGeo, const void *, const void *, float *, const int32_t *);
 using BwdFn = void (*)(int32_t, int32_t, const int32_t *, const int32_t *, const int32_t *,
                        const float *, KGeo, const void *, const void *, const void *,
                        float *, float *);
@@ -1704,12 +1789,13 @@ size_t fused_workspace_bytes(int32_t M, int32_t CI, int32_t CO, int32_t n_points
            (M == 10 ? align_up((size_t)(nnz > 0 ? nnz : 0) * M * 4) : 0);
 }
 
-// The forward needs no dW partials: the weight copy, the packed events and
-// (M = 10) the basis values.
+// The forward needs no dW partials: the weight copy, the packed events, the
+// row order of the register-resident forward and (M = 10) the basis values.
 size_t fused_forward_workspace_bytes(int32_t M, int32_t CI, int32_t CO, int32_t n_points,
                                      int64_t nnz) {
-    return align_up((size_t)M * CI * CO * 4) +
-           align_up((size_t)(n_points > 0 ? n_points : 0) * sizeof(int4)) +
+    const size_t n = (size_t)(n_points > 0 ? n_points : 0);
+    return align_up((size_t)M * CI * CO * 4) + align_up(n * sizeof(int4)) +
+           align_up(n * sizeof(int32_t)) +
            (M == 10 ? align_up((size_t)(nnz > 0 ? nnz : 0) * M * 4) : 0);
 }
 
@@ -1762,10 +1848,19 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
     if (!fn) return fail(SBC_ERR_UNSUPPORTED, "no fused forward for this shape");
     if (csr->n_rows == 0) return SBC_OK;
     KGeo gr;
-    // layout: [W copy][packed events][M = 10: basis values]
+    // layout: [W copy][packed events][row order][M = 10: basis values]
     SBC_TRY(make_kgeo(csr, v, g, align_up((size_t)M * CI * CO * 4), ws, stream, &gr));
     if (RegFn rf = find_reg(Shape{M, CI, CO, bf}, basis_mode_of(v, g))) {
         const int32_t n_tiles = (csr->n_rows + 15) / 16;
+        const int32_t np = csr->n_cols > csr->n_rows ? csr->n_cols : csr->n_rows;
+        int32_t *order = reinterpret_cast<int32_t *>(
+            static_cast<char *>(ws) + align_up((size_t)M * CI * CO * 4) +
+            align_up((size_t)np * sizeof(int4)));
+        hipLaunchKernelGGL(row_order_kernel,
+                           dim3(grid_for(csr->n_rows, kOrderWindow * (kOrderThreads / 64))),
+                           dim3(kOrderThreads), 0, stream, csr->n_rows, csr->row_ptr, gr.nnz,
+                           order);
+        SBC_LAUNCH_CHECK();
         int per_cu = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(rf),
                                                          kRegWaves * 64, 0) != hipSuccess ||
@@ -1775,7 +1870,7 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
         if (blocks > device_cus() * per_cu) blocks = device_cus() * per_cu;
         trace_before("fwd_fused", stream);
         hipLaunchKernelGGL(rf, dim3(blocks), dim3(kRegWaves * 64), 0, stream, csr->n_rows,
-                           n_tiles, csr->row_ptr, csr->col_idx, v, gr, F, W, Y);
+                           n_tiles, csr->row_ptr, csr->col_idx, v, gr, F, W, Y, order);
         SBC_LAUNCH_CHECK();
         trace_after("fwd_fused", stream);
         return SBC_OK;
