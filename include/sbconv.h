@@ -32,7 +32,10 @@
  *     same inputs give bitwise-identical outputs on every run.
  *
  * CSR layout of the neighbourhoods: rows are outputs i, row_ptr [n_out + 1],
- * col_idx [E] holds input indices j, ascending within a row.  A ragged batch
+ * col_idx [E] holds input indices j: ascending within a row for point
+ * patterns, in block order for event patterns (section 1b).  The matrix is
+ * defined entry by entry, so the order within a row only fixes the order in
+ * which the kernels add up a row's terms.  A ragged batch
  * of clouds is the block-diagonal matrix of the per-cloud matrices with
  * global column indices (Section 3.1, "Ragged Batching").
  */
@@ -138,7 +141,9 @@ typedef struct {
 typedef struct {
     int32_t n_cols;           /* n_in                                           */
     const int32_t *col_ptr;   /* [n_cols + 1]                                   */
-    const int32_t *row_idx;   /* [E] output index of each entry, ascending      */
+    const int32_t *row_idx;   /* [E] output index of each entry: ascending from
+                                 sbc_csr_transpose, in block order from the
+                                 event search                                   */
     const int32_t *edge_perm; /* [E] CSR position of each entry, or NULL        */
 } sbc_csc;
 
@@ -208,8 +213,10 @@ sbc_status sbc_neighbour_search_points(const float *x_in, int32_t n_in, const in
  * 1b. Event neighbourhoods (Section 3.2: a small spatial block, extending
  * backwards in time only): event i's neighbours are the events j < i with
  * |px_i - px_j| <= half_extent, |py_i - py_j| <= half_extent and
- * t_i - t_j <= window, in ascending j.  The stream is in place (outputs =
- * inputs).
+ * t_i - t_j <= window.  A row lists them in block order: the block's pixels
+ * row-major (dy, then dx, relative to event i's pixel), each pixel's events
+ * in ascending j (the order a per-pixel search visits them).  The stream is
+ * in place (outputs = inputs).
  *
  *   px, py, t [n]   device, int32; 0 <= px < width, 0 <= py < height, t
  *                   non-decreasing.  Events violating this never fault: they
@@ -229,9 +236,10 @@ sbc_status sbc_neighbour_search_events(const int32_t *px, const int32_t *py, con
  * "Symmetry": the reverse neighbourhood), found from the same per-pixel lists
  * by the reverse search: column j lists the events i > j with |px_i - px_j|
  * <= half_extent, |py_i - py_j| <= half_extent and t_i - t_j <= window, in
- * ascending i.  col_ptr [n + 1] and row_idx [capacity] equal what
- * sbc_csr_transpose gives for row_ptr / col_idx; no edge_perm is produced
- * (see sbc_csc).  capacity bounds both col_idx and row_idx (E entries each);
+ * block order around j (its block's pixels row-major relative to j's pixel,
+ * ascending i within a pixel).  col_ptr [n + 1] equals what sbc_csr_transpose
+ * gives for row_ptr / col_idx and row_idx holds the same entries per column,
+ * in that order; no edge_perm is produced (see sbc_csc).  capacity bounds both col_idx and row_idx (E entries each);
  * the other arguments and the errors are those of sbc_neighbour_search_events,
  * whose workspace size it uses. */
 sbc_status sbc_neighbour_search_events_csc(const int32_t *px, const int32_t *py,

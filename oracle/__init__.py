@@ -15,8 +15,9 @@ deployment recursion of the event convolution, adjoint identities and finite
 differences).  No function is left unpinned.
 """
 from . import basis, conv, sampling
-from ._native import (build, csr_transpose, events_csr, max_threads, points_csr,
-                      points_d2)
+from ._native import (block_order, build, csr_transpose, events_csc, events_csr, max_threads,
+                      points_csr, points_d2)
 
-__all__ = ["basis", "conv", "sampling", "build", "csr_transpose", "events_csr", "max_threads",
+__all__ = ["basis", "conv", "sampling", "block_order", "build", "csr_transpose", "events_csc",
+           "events_csr", "max_threads",
            "points_csr", "points_d2"]

@@ -96,11 +96,29 @@ def points_d2(x_in, x_out, row_ptr, col_idx):
     return d2[:len(col_idx)]
 
 
+def block_order(ptr, idx, px, py, half_extent):
+    """Entries of each segment r (ptr[r] .. ptr[r+1]) of an event pattern, the
+    events near event r, ordered by the position of their pixel in r's block,
+    row-major over (dy, dx) relative to r's pixel, then by index (stream
+    order within a pixel)."""
+    ptr = np.asarray(ptr, dtype=np.int64)
+    idx = np.asarray(idx, dtype=np.int32)
+    px = np.asarray(px, dtype=np.int64)
+    py = np.asarray(py, dtype=np.int64)
+    h = int(half_extent)
+    seg = np.repeat(np.arange(len(ptr) - 1), np.diff(ptr))
+    pos = (py[idx] - py[seg] + h) * (2 * h + 1) + (px[idx] - px[seg] + h)
+    return idx[np.lexsort((idx, pos, seg))].astype(np.int32)
+
+
 def events_csr(px, py, t, window, half_extent=1, width=None, height=None, method="pixels"):
     """CSR of the backwards-in-time pixel-block neighbourhoods of an event stream.
+    A row lists the block's pixels in row-major order, each pixel's events in
+    stream order (block_order): the order a per-pixel search visits them.
 
     method: 'pixels' (per-pixel lists), 'scan' (every event of the time window
-    tested) or 'quadratic' (every earlier event tested).
+    tested) or 'quadratic' (every earlier event tested); each finds a row's
+    events in stream order, then the row is put in block order.
     """
     px = np.ascontiguousarray(px, dtype=np.int32)
     py = np.ascontiguousarray(py, dtype=np.int32)
@@ -124,7 +142,17 @@ def events_csr(px, py, t, window, half_extent=1, width=None, height=None, method
     E = f(_p(row_ptr, _i32p), None)
     col_idx = np.zeros(max(E, 1), dtype=np.int32)
     f(_p(row_ptr, _i32p), _p(col_idx, _i32p))
-    return row_ptr, col_idx[:E]
+    return row_ptr, block_order(row_ptr, col_idx[:E], px, py, half_extent)
+
+
+def events_csc(px, py, t, window, half_extent=1, width=None, height=None, method="pixels"):
+    """The transposed event pattern (the reverse neighbourhoods): column j
+    lists the events i > j whose block holds j's pixel and t_i - t_j <=
+    window, in block order around j (block_order with j as the centre).
+    Returns (col_ptr, row_idx)."""
+    rp, ci = events_csr(px, py, t, window, half_extent, width, height, method)
+    cp, ri, _ = csr_transpose(rp, ci, len(np.asarray(t)))
+    return cp, block_order(cp, ri, px, py, half_extent)
 
 
 def csr_transpose(row_ptr, col_idx, n_cols):

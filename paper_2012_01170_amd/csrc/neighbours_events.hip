@@ -11,12 +11,17 @@
 //      (indices and times both ascend along it), found by two bisections; the
 //      count pass sums the run lengths per event;
 //   3. scan -> row_ptr;
-//   4. fill pass: the (2h+1)^2 runs are merged by index into the row.
+//   4. fill pass: the (2h+1)^2 runs are copied into the row one after
+//      another, block pixel by block pixel (row-major around the event), so
+//      a row lists its neighbours pixel by pixel, in stream order within a
+//      pixel (the order of a row's entries is free: the matrix is defined
+//      entry by entry).
 // Steps 2 and 4 work tile by tile over the sensor, with the lists of a tile
 // and its halo staged in LDS.  The transposed pattern (Section 3.1,
 // "Symmetry") comes out of the same passes by the reverse search: the block
 // is symmetric, so column j lists the events i > j of j's block with
-// t_i <= t_j + window, again one run per pixel.
+// t_i <= t_j + window, again one run per pixel, in the same block order
+// around j.
 // Events with a pixel outside the sensor get no neighbours and are in no
 // list; a decreasing timestamp raises a flag.  Neither can make a kernel
 // read or write out of bounds.
@@ -138,33 +143,17 @@ __device__ __forceinline__ int32_t tile_runs(int32_t i, int32_t ti, int32_t wind
     return count;
 }
 
-// Merge the runs (each ascends by index; they are disjoint) into out[0, cnt),
-// dropping writes at or past cap.
+// The runs, block pixel by block pixel (each run in stream order), into
+// out[dst, dst + cnt), dropping writes at or past cap.
 template <int K>
-__device__ __forceinline__ void merge_runs(const int32_t *Li, int32_t *lo, const int32_t *hi,
-                                           int32_t cnt, int32_t *__restrict__ out, int64_t dst,
-                                           int64_t cap) {
-    int32_t head[K];
+__device__ __forceinline__ void copy_runs(const int32_t *Li, const int32_t *lo, const int32_t *hi,
+                                          int32_t *__restrict__ out, int64_t dst, int64_t cap) {
 #pragma unroll
-    for (int k = 0; k < K; ++k) head[k] = lo[k] < hi[k] ? Li[lo[k]] : INT_MAX;
-    for (int32_t o = 0; o < cnt; ++o) {
-        int32_t best = INT_MAX, arg = 0;
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            if (head[k] < best) {
-                best = head[k];
-                arg = k;
-            }
+    for (int k = 0; k < K; ++k) {
+        for (int32_t a = lo[k]; a < hi[k]; ++a) {
+            if (dst < cap) out[dst] = Li[a];
+            ++dst;
         }
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            if (k == arg) {
-                ++lo[k];
-                head[k] = lo[k] < hi[k] ? Li[lo[k]] : INT_MAX;
-            }
-        }
-        if (dst < cap) out[dst] = best;
-        ++dst;
     }
 }
 
@@ -207,7 +196,7 @@ __device__ __forceinline__ void tile_events(const TileArgs &A, const int32_t *Li
             if constexpr (!kFill) {
                 A.row_len[i] = cnt;
             } else {
-                merge_runs<K>(Li, rlo, rhi, cnt, A.col_idx, A.row_ptr[i], A.cap);
+                copy_runs<K>(Li, rlo, rhi, A.col_idx, A.row_ptr[i], A.cap);
             }
         }
         const bool rev = kFill ? A.col_ptr != nullptr : A.col_len != nullptr;
@@ -217,7 +206,7 @@ __device__ __forceinline__ void tile_events(const TileArgs &A, const int32_t *Li
             if constexpr (!kFill)
                 A.col_len[i] = cnt_t;
             else
-                merge_runs<K>(Li, rlo, rhi, cnt_t, A.row_idx, A.col_ptr[i], A.cap);
+                copy_runs<K>(Li, rlo, rhi, A.row_idx, A.col_ptr[i], A.cap);
         }
     }
 }

@@ -474,13 +474,14 @@ def test_event_search_block_sizes(half_extent):
 
 def check_events_csc(px, py, t, W, H, window, half_extent, rp, ci):
     """The combined search gives the same CSR and, as its CSC, the oracle's
-    transpose of it (bit-exact)."""
+    reverse pattern (the same entries as the transpose, columns in block
+    order), bit-exact."""
     csr, csc = G.sbc.neighbour_search_events_csc(G.dev(px), G.dev(py), G.dev(t), W, H, window,
                                                  half_extent=half_extent)
     assert csr.nnz == len(ci) and csc.edge_perm is None
     assert np.array_equal(csr.row_ptr.cpu().numpy(), rp)
     assert np.array_equal(csr.col_idx[:csr.nnz].cpu().numpy(), ci)
-    cp, ri, _ = oracle.csr_transpose(rp, ci, len(px))
+    cp, ri = oracle.events_csc(px, py, t, window, half_extent, W, H)
     assert np.array_equal(csc.col_ptr.cpu().numpy(), cp)
     assert np.array_equal(csc.row_idx[:len(ci)].cpu().numpy(), ri)
 
@@ -518,7 +519,10 @@ def test_events_csc_window_edges(window):
 def test_backward_without_edge_perm(name, order):
     """With the basis evaluated inside, a CSC without edge_perm gives the same
     gradients, bit for bit, on the fused and the separate-kernel routes (the
-    values of the transposed entries are then evaluated in their own order)."""
+    values of the transposed entries are then evaluated in their own order).
+    For an event stream, the CSC of the search itself (its columns in block
+    order, so another order of the same sums) gives them within the case's
+    tolerance."""
     print(f"[backward no perm] {name} {order}", flush=True)
     w, rp, ci, v = case(name)
     t, csr = gpu_case(name)
@@ -526,13 +530,17 @@ def test_backward_without_edge_perm(name, order):
     csc = G.sbc.csr_transpose(csr)
     dF, dW = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"], geometry=geo, order=order)
     bare = G.sbc.CSC(csc.col_ptr, csc.row_idx, None, csc.n_cols)
-    if w["kind"] == "events":
-        csr2, bare = G.sbc.neighbour_search_events_csc(t["px"], t["py"], t["t"], w["width"],
-                                                       w["height"], w["window"])
-        assert np.array_equal(csr2.col_idx[:csr2.nnz].cpu().numpy(), ci)
     dF2, dW2 = G.sbc.conv_backward(csr, bare, t["F"], t["W"], t["dY"], geometry=geo, order=order)
     assert np.array_equal(dF2.cpu().numpy(), dF.cpu().numpy())
     assert np.array_equal(dW2.cpu().numpy(), dW.cpu().numpy())
+    if w["kind"] == "events":
+        csr2, found = G.sbc.neighbour_search_events_csc(t["px"], t["py"], t["t"], w["width"],
+                                                        w["height"], w["window"])
+        assert np.array_equal(csr2.col_idx[:csr2.nnz].cpu().numpy(), ci)
+        dF3, dW3 = G.sbc.conv_backward(csr, found, t["F"], t["W"], t["dY"], geometry=geo,
+                                       order=order)
+        assert G.row_error(dF3.cpu().numpy(), dF.cpu().numpy()) < tol(w)
+        assert G.norm_error(dW3.cpu().numpy(), dW.cpu().numpy()) < tol(w)
     vv = G.sbc.basis_eval(csr, geo)
     with pytest.raises(G.sbc.ops.L.SbcError, match="INVALID_ARG"):
         G.sbc.conv_backward(csr, bare, t["F"], t["W"], t["dY"], v=vv, order=order)

@@ -191,3 +191,61 @@ def test_decay_gradient_matches_finite_differences():
         lm[u, q] -= h
         fd = (loss(lp) - loss(lm)) / (2 * h)
         assert np.isclose(g[m], fd, rtol=1e-6, atol=1e-9 * max(1.0, abs(fd)))
+
+
+def _brute_block_pattern(px, py, t, window, h, reverse):
+    """Rows (reverse: columns) from the definition, each in block order: the
+    (2h+1)^2 pixels around the centre event row-major, then stream order."""
+    n = len(t)
+    out = []
+    for c in range(n):
+        ent = []
+        for o in range(n):
+            later, earlier = (o, c) if reverse else (c, o)
+            if not (earlier < later and 0 <= int(t[later]) - int(t[earlier]) <= window):
+                continue
+            dx, dy = int(px[o]) - int(px[c]), int(py[o]) - int(py[c])
+            if abs(dx) <= h and abs(dy) <= h:
+                ent.append(((dy + h) * (2 * h + 1) + (dx + h), o))
+        out.append([o for _, o in sorted(ent)])
+    return out
+
+
+@pytest.mark.parametrize("h", [1, 2])
+def test_rows_and_columns_in_block_order(h):
+    """Rows and columns of the event pattern against a brute force written from
+    the definition: a row holds the earlier events of its block within the
+    window, a column the later ones, each listed pixel by pixel (row-major
+    around the centre event) and in stream order within a pixel."""
+    rng = np.random.default_rng(60 + h)
+    n, W, H = 400, 6, 5
+    px = rng.integers(0, W, n).astype(np.int32)
+    py = rng.integers(0, H, n).astype(np.int32)
+    t = np.sort(rng.integers(0, 5000, n)).astype(np.int32)
+    rp, ci = oracle.events_csr(px, py, t, 300, h, W, H)
+    cp, ri = oracle.events_csc(px, py, t, 300, h, W, H)
+    rows = _brute_block_pattern(px, py, t, 300, h, False)
+    cols = _brute_block_pattern(px, py, t, 300, h, True)
+    assert [ci[rp[i]:rp[i + 1]].tolist() for i in range(n)] == rows
+    assert [ri[cp[j]:cp[j + 1]].tolist() for j in range(n)] == cols
+    assert any(r != sorted(r) for r in rows)      # the order is not the index order
+
+
+def test_block_order_hand_case():
+    """Event 3 at (2, 2) sees event 0 at (3, 2) (position 5 of its 3x3 block),
+    event 1 at (1, 1) (position 0) and event 2 at (2, 2) (position 4, its own
+    pixel): its row is [1, 2, 0].  Event 0's column holds events 2 and 3, both
+    at position 3 around it, in stream order.  In the second stream event 0 at
+    (2, 2) is seen by event 1 at (3, 3) (position 8 around event 0) and event 2
+    at (1, 1) (position 0): its column is [2, 1]."""
+    px = np.array([3, 1, 2, 2], np.int32)
+    py = np.array([2, 1, 2, 2], np.int32)
+    t = np.array([0, 1, 2, 3], np.int32)
+    rp, ci = oracle.events_csr(px, py, t, 100, 1, 5, 5)
+    assert ci[rp[3]:rp[4]].tolist() == [1, 2, 0]
+    cp, ri = oracle.events_csc(px, py, t, 100, 1, 5, 5)
+    assert ri[cp[0]:cp[1]].tolist() == [2, 3]
+    px = np.array([2, 3, 1], np.int32)
+    py = np.array([2, 3, 1], np.int32)
+    cp, ri = oracle.events_csc(px, py, np.array([0, 1, 2], np.int32), 100, 1, 5, 5)
+    assert ri[cp[0]:cp[1]].tolist() == [2, 1]
