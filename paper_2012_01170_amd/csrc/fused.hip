@@ -1314,29 +1314,6 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
         n_my > 0 ? load_bound<RPW>(col_ptr, n_in, t_first * TR + w * RPW, g.nnz) : 0, 0, false};
     auto load_tile = [&](int32_t s, int buf) {
         const int32_t row0 = (t_first + s * gx) * TR;
-        if (dW_part) {  // F rows of the tile, row-major (zero past the last row), 16 B per load
-            constexpr int CPR = CI * (int)sizeof(DT) / 16;
-            constexpr int NQ = (TR * CPR + kWsGather * 64 - 1) / (kWsGather * 64);
-            uint4 val[NQ];
-#pragma unroll
-            for (int k = 0; k < NQ; ++k) {
-                const int q = threadIdx.x + k * kWsGather * 64;
-                const int r = q / CPR, c16 = q % CPR;
-                val[k] = uint4{0u, 0u, 0u, 0u};
-                if (q < TR * CPR && row0 + r < n_in)
-                    val[k] = *reinterpret_cast<const uint4 *>(
-                        static_cast<const char *>(Fv) + (int64_t)(row0 + r) * CI * sizeof(DT) +
-                        16 * c16);
-            }
-#pragma unroll
-            for (int k = 0; k < NQ; ++k) {
-                const int q = threadIdx.x + k * kWsGather * 64;
-                const int r = q / CPR, c16 = q % CPR;
-                if (q < TR * CPR)
-                    *reinterpret_cast<uint4 *>(reinterpret_cast<char *>(&Fs[buf][r * SF]) +
-                                               16 * c16) = val[k];
-            }
-        }
         const int32_t next = s + 1 < n_my ? (t_first + (s + 1) * gx) * TR + w * RPW : -1;
         if constexpr (kOneHot)
             ahead = gather_rows_onehot<CO, RPW, true, kBf>(
@@ -1389,10 +1366,48 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
                         Wop)[bt_offset<K2, CI, CO>(16 * (wc + NCBW * t) + lc, 4 * ks + lr)];
             }
     }
+    // F rows of tile s (row-major, zero past the last row, 16 B per load) for
+    // the dW product, into Fs[s & 1]: the matrix waves load those of the next
+    // tile before their products and store them after, so the loads' latency
+    // hides behind the products (the gather waves have none of it)
+    constexpr int CPR = CI * (int)sizeof(DT) / 16;
+    constexpr int NQ = (TR * CPR + kWsMma * 64 - 1) / (kWsMma * 64);
+    const int mt = threadIdx.x - kWsGather * 64;  // thread within the matrix role
+    auto load_f = [&](int32_t s, uint4 (&val)[NQ]) {
+        const int32_t row0 = (t_first + s * gx) * TR;
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+            const int q = mt + k * kWsMma * 64;
+            const int r = q / CPR, c16 = q % CPR;
+            val[k] = uint4{0u, 0u, 0u, 0u};
+            if (q < TR * CPR && row0 + r < n_in)
+                val[k] = *reinterpret_cast<const uint4 *>(
+                    static_cast<const char *>(Fv) + (int64_t)(row0 + r) * CI * sizeof(DT) +
+                    16 * c16);
+        }
+    };
+    auto store_f = [&](int buf, const uint4 (&val)[NQ]) {
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+            const int q = mt + k * kWsMma * 64;
+            const int r = q / CPR, c16 = q % CPR;
+            if (q < TR * CPR)
+                *reinterpret_cast<uint4 *>(reinterpret_cast<char *>(&Fs[buf][r * SF]) +
+                                           16 * c16) = val[k];
+        }
+    };
+    if (dW_part && n_my > 0) {
+        uint4 val[NQ];
+        load_f(0, val);
+        store_f(0, val);
+    }
     __syncthreads();
 #pragma unroll 1
     for (int32_t s = 0; s < n_my; ++s) {
         const int buf = s & 1;
+        uint4 fnext[NQ];
+        const bool more = dW_part && s + 1 < n_my;
+        if (more) load_f(s + 1, fnext);
         {
             const int32_t row0 = (t_first + s * gx) * TR;
             const DT *D = Ds[buf];
@@ -1499,6 +1514,7 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
                 }
             }
         }
+        if (more) store_f((s + 1) & 1, fnext);
         __syncthreads();
     }
     if (!dW_part) return;
