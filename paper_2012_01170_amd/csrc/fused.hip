@@ -814,9 +814,13 @@ __device__ __forceinline__ int32_t xcd_tile(int32_t b, int32_t n) {
 // on timing.
 constexpr int64_t kRowCost = 8;
 
+// quant: the workers (blocks or waves) that share an XCD's range.  When the
+// tiles divide evenly among all workers, the ranges are rounded to multiples
+// of quant, so every worker keeps the same number of tiles (a tile more for
+// some would cost the kernel a whole tile's time).
 __device__ __forceinline__ int32_t xcd_range_begin(int32_t x, int32_t X, int32_t n_tiles, int TR,
                                                    const int32_t *__restrict__ ptr,
-                                                   int32_t n_rows, int32_t nnz) {
+                                                   int32_t n_rows, int32_t nnz, int32_t quant) {
     if (x <= 0) return 0;
     if (x >= X) return n_tiles;
     auto work = [&](int32_t t) {  // work estimate of the rows before tile t
@@ -841,6 +845,10 @@ __device__ __forceinline__ int32_t xcd_range_begin(int32_t x, int32_t X, int32_t
         const int32_t nlo = f == 0 ? lo : lo + (int32_t)((f * span + 63) / 64);
         lo = nlo;
         hi = nhi;
+    }
+    if (quant > 0 && n_tiles % ((int64_t)X * quant) == 0) {
+        const int32_t r = (hi + quant / 2) / quant * quant;
+        return r < n_tiles ? r : n_tiles;
     }
     return hi;
 }
@@ -1068,8 +1076,11 @@ __global__ void __launch_bounds__(kRegWaves * 64)
     const int32_t gx = G / X + (x < G % X ? 1 : 0);
     const int32_t waves_x = gx * kRegWaves;
     const int32_t lw = (blockIdx.x / X) * kRegWaves + w;
-    const int32_t t_begin = xcd_range_begin(x, X, n_tiles, 16, row_ptr, n_out, g.nnz);
-    const int32_t t_end = xcd_range_begin(x + 1, X, n_tiles, 16, row_ptr, n_out, g.nnz);
+    // (rounding needs the same worker count on every XCD: the ranges' shared ends
+    // are computed on both sides)
+    const int32_t quant = G % X == 0 ? waves_x : 0;
+    const int32_t t_begin = xcd_range_begin(x, X, n_tiles, 16, row_ptr, n_out, g.nnz, quant);
+    const int32_t t_end = xcd_range_begin(x + 1, X, n_tiles, 16, row_ptr, n_out, g.nnz, quant);
 
 #pragma unroll 1
     for (int32_t tile = t_begin + lw; tile < t_end; tile += waves_x) {
@@ -1304,8 +1315,9 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     const int32_t G = gridDim.x, X = G < 8 ? G : 8;
     const int32_t x = blockIdx.x % X, l = blockIdx.x / X;
     const int32_t gx = G / X + (x < G % X ? 1 : 0);
-    const int32_t t_first = xcd_range_begin(x, X, n_tiles, TR, col_ptr, n_in, g.nnz) + l;
-    const int32_t t_end = xcd_range_begin(x + 1, X, n_tiles, TR, col_ptr, n_in, g.nnz);
+    const int32_t quant = G % X == 0 ? gx : 0;  // the same on every XCD (shared range ends)
+    const int32_t t_first = xcd_range_begin(x, X, n_tiles, TR, col_ptr, n_in, g.nnz, quant) + l;
+    const int32_t t_end = xcd_range_begin(x + 1, X, n_tiles, TR, col_ptr, n_in, g.nnz, quant);
     const int32_t n_my = t_first < t_end ? (t_end - t_first + gx - 1) / gx : 0;
 
     // row bounds (and first neighbour indices) of the gather's next tile,
