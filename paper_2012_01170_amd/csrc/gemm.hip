@@ -28,11 +28,54 @@ __device__ __forceinline__ float ld(const uint16_t *p, int64_t i) {
     return __uint_as_float((uint32_t)p[i] << 16);
 }
 
+// kPer consecutive elements of a unit-stride run starting at p[off], of which
+// the first `valid` exist (the rest read as 0): 16-byte loads when the run is
+// whole (kVec: the caller has checked that such runs are 16-byte aligned),
+// else element by element.
+template <typename T, int kPer, bool kVec>
+__device__ __forceinline__ void load_run(const T *__restrict__ p, int64_t off, int valid,
+                                         float *out) {
+    if constexpr (kVec) {
+        if (valid >= kPer) {
+            if constexpr (sizeof(T) == 4) {
+#pragma unroll
+                for (int q = 0; q < kPer; q += 4) {
+                    const float4 x = *reinterpret_cast<const float4 *>(p + off + q);
+                    out[q] = x.x;
+                    out[q + 1] = x.y;
+                    out[q + 2] = x.z;
+                    out[q + 3] = x.w;
+                }
+            } else if constexpr (kPer == 8) {
+                const uint4 x = *reinterpret_cast<const uint4 *>(p + off);
+                const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    out[2 * q] = __uint_as_float(w[q] << 16);
+                    out[2 * q + 1] = __uint_as_float(w[q] & 0xFFFF0000u);
+                }
+            } else {
+                const uint2 x = *reinterpret_cast<const uint2 *>(p + off);
+                const uint32_t w[2] = {x.x, x.y};
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    out[2 * q] = __uint_as_float(w[q] << 16);
+                    out[2 * q + 1] = __uint_as_float(w[q] & 0xFFFF0000u);
+                }
+            }
+            return;
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) out[q] = q < valid ? ld(p, off + q) : 0.f;
+}
+
 // One operand slab, [kSlab][BT] in LDS (BT = the tile's rows of A or columns
 // of B), loaded by 256 threads, BT * kSlab / 256 elements each: runs along the
 // operand's contiguous index (k, or the row / column index), so that
-// neighbouring threads read neighbouring addresses.
-template <int BT, typename T>
+// neighbouring threads read neighbouring addresses.  kVec: the contiguous
+// index has unit stride and its runs are 16-byte aligned (vector loads).
+template <int BT, typename T, bool kVec>
 struct SlabLoader {
     static constexpr int kPer = BT * kSlab / kThreads;  // 8 (128) or 4 (64)
     float v[kPer];
@@ -41,6 +84,26 @@ struct SlabLoader {
                                          int32_t t0, int32_t n_t, int64_t k0, int64_t k_end,
                                          bool k_contig) {
         const int tid = threadIdx.x;
+        if (kVec && k_contig) {  // a thread takes kPer consecutive k of one row
+            const int tl = tid / (kSlab / kPer);
+            const int kl = (tid % (kSlab / kPer)) * kPer;
+            const int32_t t = t0 + tl;
+            const int64_t k = k0 + kl;
+            const int64_t left = k_end - k;
+            const int valid = t < n_t ? (left >= kPer ? kPer : (left > 0 ? (int)left : 0)) : 0;
+            load_run<T, kPer, kVec>(p, (int64_t)t * s_t + k, valid, v);
+            return;
+        }
+        if (kVec) {              // a thread takes kPer consecutive rows at one k
+            const int kl = tid / (BT / kPer);
+            const int tl = (tid % (BT / kPer)) * kPer;
+            const int32_t t = t0 + tl;
+            const int64_t k = k0 + kl;
+            const int32_t left = n_t - t;
+            const int valid = k < k_end ? (left >= kPer ? kPer : (left > 0 ? left : 0)) : 0;
+            load_run<T, kPer, kVec>(p, (int64_t)t + k * s_k, valid, v);
+            return;
+        }
 #pragma unroll
         for (int q = 0; q < kPer; ++q) {
             int tl, kl;
@@ -73,7 +136,7 @@ struct SlabLoader {
     }
 };
 
-template <int BM, int BN, typename AT, typename BT>
+template <int BM, int BN, typename AT, typename BT, bool kVecA, bool kVecB>
 __global__ void __launch_bounds__(kThreads, 2)
     gemm_kernel(const AT *__restrict__ A, int64_t sa_r, int64_t sa_k, const BT *__restrict__ B,
                 int64_t sb_k, int64_t sb_n, float *__restrict__ C, int64_t sc_r, int64_t sc_n,
@@ -96,8 +159,8 @@ __global__ void __launch_bounds__(kThreads, 2)
 #pragma unroll
         for (int b = 0; b < TN; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    SlabLoader<BM, AT> la;
-    SlabLoader<BN, BT> lb;
+    SlabLoader<BM, AT, kVecA> la;
+    SlabLoader<BN, BT, kVecB> lb;
     la.load(A, sa_r, sa_k, r0, R, kb, ke, a_kc);
     lb.load(B, sb_n, sb_k, n0, N, kb, ke, b_kc);
     la.store(As[0], a_kc);
@@ -210,10 +273,25 @@ sbc_status gemm(const void *A, bool a_bf16, int64_t sa_r, int64_t sa_k, const vo
     const int t = tile_for(R, N);
     dim3 grid((N + t - 1) / t, (R + t - 1) / t, Sz);
     float *part = Sz > 1 ? partial_ws : nullptr;
-#define SBC_GEMM_LAUNCH(TT, AT, BT)                                                           \
-    hipLaunchKernelGGL((gemm_kernel<TT, TT, AT, BT>), grid, dim3(kThreads), 0, stream,         \
+    // vector loads along an operand's unit-stride index when its runs are
+    // 16-byte aligned: the base and the other stride a multiple of 16 bytes
+    auto vec_ok = [](const void *p, bool bf, int64_t s_t, int64_t s_k) {
+        const int64_t ve = bf ? 8 : 4;  // elements per 16 bytes
+        if (reinterpret_cast<uintptr_t>(p) % 16 != 0) return false;
+        if (s_k == 1) return s_t % ve == 0;
+        if (s_t == 1) return s_k % ve == 0;
+        return false;
+    };
+    const bool va = vec_ok(A, a_bf16, sa_r, sa_k), vb = vec_ok(B, b_bf16, sb_n, sb_k);
+#define SBC_GEMM_LAUNCH1(TT, AT, BT, VA, VB)                                                  \
+    hipLaunchKernelGGL((gemm_kernel<TT, TT, AT, BT, VA, VB>), grid, dim3(kThreads), 0, stream, \
                        static_cast<const AT *>(A), sa_r, sa_k, static_cast<const BT *>(B),     \
                        sb_k, sb_n, C, sc_r, sc_n, R, N, K, k_chunk, part)
+#define SBC_GEMM_LAUNCH(TT, AT, BT)                                                           \
+    if (va && vb) SBC_GEMM_LAUNCH1(TT, AT, BT, true, true);                                   \
+    else if (va) SBC_GEMM_LAUNCH1(TT, AT, BT, true, false);                                   \
+    else if (vb) SBC_GEMM_LAUNCH1(TT, AT, BT, false, true);                                   \
+    else SBC_GEMM_LAUNCH1(TT, AT, BT, false, false)
 #define SBC_GEMM_TYPES(TT)                                                                    \
     if (!a_bf16 && !b_bf16) SBC_GEMM_LAUNCH(TT, float, float);                                \
     else if (!a_bf16 && b_bf16) SBC_GEMM_LAUNCH(TT, float, uint16_t);                         \
@@ -226,6 +304,7 @@ sbc_status gemm(const void *A, bool a_bf16, int64_t sa_r, int64_t sa_k, const vo
     }
 #undef SBC_GEMM_TYPES
 #undef SBC_GEMM_LAUNCH
+#undef SBC_GEMM_LAUNCH1
     SBC_LAUNCH_CHECK();
     if (part) {
         int64_t blocks = ((int64_t)R * N + 255) / 256;
