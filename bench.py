@@ -91,7 +91,17 @@ def trace_name(kernel):
         return "decay_fused" if len(args) > 3 and args[3].strip() == "16" else "bwd_fused"
     if base == "featureless_kernel":  # <M, mode, writes Z>
         return "featureless_fwd" if kernel.rstrip(">").endswith("true") else "featureless_rowsum"
+    if base == "spmm_kernel":  # <M, contract, X type>: named by direction, see SPMM_DIRECTION
+        args = kernel[len(base) + 1:].split(",")
+        return "spmm_contract" if len(args) > 1 and args[1].strip() == "true" else "spmm_expand"
     return TRACE_NAME.get(base)
+
+
+# The generic gather kernel serves several launches; each workload's step has
+# at most one launch per direction, so its counters are filed by direction.
+SPMM_DIRECTION = {"fwd_spmm": "spmm_expand", "bwd_spmm": "spmm_expand",
+                  "bwd_spmm_t_expand": "spmm_expand", "decay_spmm": "spmm_expand",
+                  "fwd_spmm_contract": "spmm_contract", "bwd_spmm_t": "spmm_contract"}
 
 
 def source_fingerprint():
@@ -650,7 +660,7 @@ def measure(a, w, table, step, torch, _lib, dev):
     else:
         achieved, peak, unit, bound = nbytes / (us * 1e-6) / 1e9, HBM_PEAK_GBS, "GB/s", "hbm"
     traffic, traffic_src = read_traffic(a.workload)
-    traffic = traffic.get(dom) if traffic else None
+    traffic = traffic.get(SPMM_DIRECTION.get(dom, dom)) if traffic else None
     roof = {"bound": bound, "kernel": dom, "achieved": round(achieved, 3), "peak": peak,
             "unit": unit, "frac": round(achieved / peak, 4),
             "traffic": round(traffic) if traffic is not None else None,

@@ -31,10 +31,21 @@ def test_more_than_one_gpu_is_refused():
     ("sample_kernel<true>", "sample"),
     ("sample_kernel<false>", "sample_count"),
     ("lif_cell_kernel<3>", "lif_cells"),
-    ("gemm_kernel<64, 64, float, float>", None),
+    ("gemm_kernel<64, 64, float, float, true, true>", None),
+    ("spmm_kernel<8, true, float>", "spmm_contract"),
+    ("spmm_kernel<10, false, unsigned short>", "spmm_expand"),
 ])
 def test_trace_names(kernel, name):
     assert bench.trace_name(kernel) == name
+
+
+def test_spmm_launches_file_their_counters_by_direction():
+    """Every launch of the generic gather maps onto the counter line of its
+    direction, so a workload's dominant gather finds its measured bytes."""
+    assert bench.SPMM_DIRECTION["bwd_spmm_t"] == "spmm_contract"
+    assert bench.SPMM_DIRECTION["fwd_spmm_contract"] == "spmm_contract"
+    for n in ("fwd_spmm", "bwd_spmm", "bwd_spmm_t_expand", "decay_spmm"):
+        assert bench.SPMM_DIRECTION[n] == "spmm_expand"
 
 
 def _counter_dir(tmp_path, tag, counter, rows):
