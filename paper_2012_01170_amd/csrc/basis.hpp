@@ -87,9 +87,16 @@ __device__ __forceinline__ int event_index(int32_t ux, int32_t uy) {
     return k == 4 ? -1 : (k < 4 ? k : k - 1);
 }
 
-// exp(-dt / tau) for an integer time gap dt >= 0.
+// exp(-dt / tau) for an integer time gap dt >= 0.  The gap is converted to
+// float from its int32 difference when that does not overflow (the same
+// value, rounded once), else from the int64 one.
 __device__ __forceinline__ float event_decay(int32_t ti, int32_t tj, float inv_tau) {
-    const float dt = (float)((int64_t)ti - (int64_t)tj);
+    const int32_t d = (int32_t)((uint32_t)ti - (uint32_t)tj);
+    float dt;
+    if (__builtin_expect(((ti ^ tj) & (ti ^ d)) < 0, 0))
+        dt = (float)((int64_t)ti - (int64_t)tj);
+    else
+        dt = (float)d;
     return expf(-dt * inv_tau);
 }
 

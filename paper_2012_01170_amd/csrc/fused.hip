@@ -238,7 +238,6 @@ struct GatherAhead {
     int32_t bound;
     int32_t idx0;
     bool have_idx;
-    int32_t idx1;  // the one-hot gather's second chunk: idx[first edge + 64 + lane]
 };
 
 template <int M, int C, int kBasis, bool kXbf, bool kOutBf, bool kT, int RPW, bool kPipelined>
@@ -459,47 +458,168 @@ __device__ __forceinline__ GatherAhead gather_rows(int32_t row_begin, int32_t n_
 // edge, at the offset index k of its pixel step (none for a same-pixel edge),
 // so a gathered row's sum over its edges only adds each edge into one of the
 // M = 8 column blocks.  gather_rows_onehot builds the same tile rows as
-// gather_rows without the other seven products.  Per chunk of 64 edges:
-//   1. the endpoint coordinates of each edge are loaded (its offset index and
-//      decay), then the chunk's 64 neighbour rows are copied into LDS by the
-//      direct global-to-LDS loads, all in one memory round trip;
-//   2. one wave ballot per offset marks the chunk's edges of that offset;
-//   3. lane (row r, offset m, channel part h) walks the set bits of its
-//      offset's ballot within row r's lanes, lowest first, and adds up those
-//      rows, CH channels of each, from LDS.
-// So a (row, offset) sum takes its edges in pattern order, one product each.
-// The neighbour indices of a wave's first two chunks are loaded one call
-// ahead.
-template <int RB>  // bytes per gathered row
+// gather_rows without the other seven products.  A wave takes its rows'
+// edges in chunks of CK (32 or 64); per chunk:
+//   1. the chunk's CK neighbour rows, loaded into registers while the
+//      previous chunk was summed, are written to LDS, and each edge's offset
+//      index and decay come from its endpoints' coordinates (loaded with the
+//      rows);
+//   2. the loads of the following chunk are issued (the wave's next chunk of
+//      these rows, else the first chunk of its rows in the next tile);
+//   3. wave ballots of the bits of each edge's offset and row mark, for lane
+//      (row r, offset m, channel part h), the chunk's edges of row r with
+//      offset m (its bucket);
+//   4. each lane walks the set bits of its bucket, lowest first, and adds up
+//      those rows, CH channels of each, from LDS.
+// So a (row, offset) sum takes its edges in pattern order, one product each,
+// and a chunk's memory round trip overlaps the previous chunk's sums.  The
+// indices that step 2 needs are loaded a chunk (or a tile) earlier, and the
+// row bounds two tiles earlier, so no step waits on a load issued in the
+// same step.
+// 16 bytes as a native vector (its copies stay in registers, which those of
+// the HIP uint4 struct do not always)
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int RB, int CK>  // bytes per gathered row, edges per chunk
 struct OneHotStage {
-    uint4 f[64][RB / 16];       // the chunk's neighbour rows (direct loads)
-    int32_t nb[64];             // neighbour index of each staged edge
-    float sv[64];               // basis value of each staged edge
-    int32_t bounds[17];         // pattern bounds of the wave's rows
+    u32x4 f[CK + 1][RB / 16];   // the chunk's neighbour rows, then a row of zeros
+    float sv[CK + 1];           // basis value of each staged edge, then 0
 };
+
+// The stage's row of zeros and its basis value 0, which the bucket walk
+// reads past a bucket's end (so its reads need no branch).
+template <int RB, int CK>
+__device__ __forceinline__ void onehot_stage_init(OneHotStage<RB, CK> &st) {
+    const int lane = threadIdx.x & 63;
+    if (lane < RB / 16) st.f[CK][lane] = u32x4{0u, 0u, 0u, 0u};
+    if (lane == 0) st.sv[CK] = 0.f;
+}
 
 // Bits [0, n) of a 64-bit lane mask.
 __device__ __forceinline__ uint64_t lanes_below(int n) {
     return n >= 64 ? ~0ull : (n <= 0 ? 0ull : ((1ull << n) - 1ull));
 }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-
 // Element k of a 16-byte piece of float32 (4) or bf16 (8) values, as float32.
 template <bool kBf>
-__device__ __forceinline__ float piece_elem(const uint4 &x, int k) {
-    const uint32_t w = k < (kBf ? 2 : 1) ? x.x : k < (kBf ? 4 : 2) ? x.y : k < (kBf ? 6 : 3) ? x.z : x.w;
+__device__ __forceinline__ float piece_elem(const u32x4 &x, int k) {
+    const uint32_t w = x[kBf ? k / 2 : k];
     if constexpr (kBf) return __uint_as_float((k & 1) ? (w & 0xFFFF0000u) : (w << 16));
     else return __uint_as_float(w);
 }
 
-// X [*, C] float32 or bf16 (kBf), tile rows of the same type.
-template <int C, int RPW, bool kT, bool kBf>
-__device__ __forceinline__ GatherAhead gather_rows_onehot(
-    int32_t row_begin, int32_t n_rows, const int32_t *__restrict__ ptr,
+// The one-hot gather's loads in flight from one tile to the next (per lane).
+// Tile t of the wave's sequence: b0 = its row bounds (lanes 0..RPW), b1
+// those of the next tile, b2 those of the one after as loaded (unclamped,
+// onehot_bound_raw); j1 = idx of the next tile's first chunk (lane e: its
+// edge e); i1 = idx of this tile's second chunk; rows, ga, gb = the
+// neighbour-row pieces and endpoint coordinates of this tile's first chunk
+// (or, inside a call, of the chunk after the one being summed).
+template <int NR>  // 16-byte row pieces per lane and chunk (CK = NR RPL)
+struct OneHotPipe {
+    int32_t b0, b1, b2, j1, i1;
+    u32x4 rows[NR];
+    int4 ga, gb;
+    int32_t es;  // the row (0 .. RPW-1) of the lane's edge in the chunk
+};
+
+// Row begins of the wave's tiles t .. t+3 (-1 past its last tile).
+struct OneHotTiles {
+    int32_t r0, r1, r2, r3;
+};
+
+// load_bound without its clamp and without a branch: every lane loads
+// (lanes past RPW repeat lane RPW's row; a missing tile, row_begin < 0, reads
+// from row 0), so no wait for the load lands before the value's use, where
+// onehot_bound_clamp finishes it.
+template <int RPW>
+__device__ __forceinline__ int32_t onehot_bound_raw(const int32_t *__restrict__ ptr,
+                                                    int32_t n_rows, int32_t row_begin) {
+    const int lane = threadIdx.x & 63;
+    int32_t r = (row_begin > 0 ? row_begin : 0) + (lane < RPW ? lane : RPW);
+    r = r < n_rows ? r : n_rows;
+    return ptr[r];
+}
+
+__device__ __forceinline__ int32_t onehot_bound_clamp(int32_t b, int32_t nnz) {
+    return b < 0 ? 0 : (b < nnz ? b : nnz);
+}
+
+// idx of the chunk at edge c0 (lane e: edge c0 + e), loaded by every lane
+// without a branch: the edge is clamped into [0, nnz) (nnz > 0), and what a
+// lane past its rows' end holds is not used (onehot_issue).
+__device__ __forceinline__ int32_t onehot_chunk_idx(const int32_t *__restrict__ idx, int32_t c0,
+                                                    int32_t nnz) {
+    int32_t e = c0 + (int32_t)(threadIdx.x & 63);
+    e = e < nnz ? e : nnz - 1;
+    e = e > 0 ? e : 0;
+    return idx[e];
+}
+
+// Issue the loads of the chunk at edge c0 (c0 < the rows' end) of the rows
+// [row_begin, row_begin + RPW) with bounds bnd and chunk indices other (from
+// onehot_chunk_idx): lane l's endpoint coordinates for edge c0 + l, and row
+// piece q of lane l, piece l % P of staged row q RPL + l / P.  Lanes past the
+// rows' end or the chunk's CK edges load lane 0's edge, so every lane's
+// addresses are in bounds.
+template <int C, int RPW, bool kT, bool kBf, int NR>
+__device__ __forceinline__ void onehot_issue(int32_t row_begin, int32_t bnd, int32_t c0,
+                                             int32_t other, const KGeo &g,
+                                             const void *__restrict__ X, OneHotPipe<NR> &p) {
+    constexpr int ES = kBf ? 2 : 4;
+    constexpr int P = C * ES / 16;     // 16-byte pieces per row
+    constexpr int RPL = 64 / P;        // rows per load instruction
+    constexpr int CK = NR * RPL;       // edges per chunk
+    static_assert(CK == 32 || CK == 64, "chunk size");
+    const int lane = threadIdx.x & 63;
+    const int32_t e = c0 + lane;
+    int s = 0;
+#pragma unroll
+    for (int q = 1; q < RPW; ++q)
+        if (__shfl(bnd, q, 64) <= e) s = q;
+    const bool has = lane < CK && e < __shfl(bnd, RPW, 64);
+    const int32_t other0 = __shfl(other, 0, 64), s0 = __shfl(s, 0, 64);
+    other = has ? other : other0;
+    s = has ? s : s0;
+#pragma unroll
+    for (int q = 0; q < NR; ++q) {
+        const int32_t src = __shfl(other, q * RPL + lane / P, 64);
+        p.rows[q] = *reinterpret_cast<const u32x4 *>(static_cast<const char *>(X) +
+                                                     (int64_t)src * C * ES + 16 * (lane % P));
+    }
+    const int32_t row = row_begin + s;
+    p.ga = g.ev[kT ? other : row];
+    p.gb = g.ev[kT ? row : other];
+    p.es = s;
+}
+
+// The pipeline's start for the wave's first tile (rows at tl.r0 >= 0).
+template <int C, int RPW, bool kT, bool kBf, int NR>
+__device__ __forceinline__ void onehot_prologue(const OneHotTiles &tl, int32_t n_rows,
+                                                const int32_t *__restrict__ ptr,
+                                                const int32_t *__restrict__ idx, const KGeo &g,
+                                                const void *__restrict__ X, OneHotPipe<NR> &p) {
+    p.b0 = load_bound<RPW>(ptr, n_rows, tl.r0, g.nnz);
+    p.b1 = tl.r1 >= 0 ? load_bound<RPW>(ptr, n_rows, tl.r1, g.nnz) : 0;
+    p.b2 = onehot_bound_raw<RPW>(ptr, n_rows, tl.r2);
+    p.i1 = p.j1 = 0;
+    if (g.nnz == 0) return;  // no edges in any tile
+    const int32_t wb = __shfl(p.b0, 0, 64), we = __shfl(p.b0, RPW, 64);
+    constexpr int CK = NR * (64 / (C * (kBf ? 2 : 4) / 16));
+    const int32_t i0 = onehot_chunk_idx(idx, wb, g.nnz);
+    p.i1 = onehot_chunk_idx(idx, wb + CK, g.nnz);
+    p.j1 = onehot_chunk_idx(idx, __shfl(p.b1, 0, 64), g.nnz);
+    if (wb < we) onehot_issue<C, RPW, kT, kBf, NR>(tl.r0, p.b0, wb, i0, g, X, p);
+}
+
+// X [*, C] float32 or bf16 (kBf), tile rows of the same type.  p holds the
+// state described at OneHotPipe for tile tl.r0 and is advanced to the next.
+template <int C, int RPW, bool kT, bool kBf, int NR>
+__device__ __forceinline__ void gather_rows_onehot(
+    const OneHotTiles &tl, int32_t n_rows, const int32_t *__restrict__ ptr,
     const int32_t *__restrict__ idx, const KGeo &g, const void *__restrict__ X, void *out_tile,
-    int S, int local_row0, OneHotStage<C * (kBf ? 2 : 4)> &st, float inv_tau, GatherAhead pre,
-    int32_t next_row_begin) {
+    int S, int local_row0, OneHotStage<C * (kBf ? 2 : 4), NR * (64 / (C * (kBf ? 2 : 4) / 16))> &st,
+    float inv_tau, OneHotPipe<NR> &p) {
     constexpr int M = 8;
     constexpr int ES = kBf ? 2 : 4;            // bytes per element
     constexpr int VPP = 16 / ES;               // values per 16-byte piece
@@ -509,110 +629,110 @@ __device__ __forceinline__ GatherAhead gather_rows_onehot(
     static_assert(CH % VPP == 0, "whole 16-byte pieces per lane");
     constexpr int NP = CH / VPP;               // 16-byte pieces per lane
     constexpr int P = C / VPP;                 // 16-byte pieces per row
-    static_assert(64 % P == 0, "whole rows per direct load");
-    constexpr int RPL = 64 / P;                // rows per direct load instruction
-    constexpr int U = NP <= 4 ? 4 : 2;         // bucket rows read together
+    static_assert(64 % P == 0, "whole rows per load instruction");
+    constexpr int RPL = 64 / P;                // rows per load instruction
+    constexpr int CK = NR * RPL;               // edges per chunk
+    // bucket rows read together (four, with the next chunk's rows in flight in
+    // registers, took more instructions per product and ran slower)
+    constexpr int U = CK == 32 && NP <= 4 ? 4 : 2;
+    constexpr int NPX = U * NP > 8 ? 8 / U : NP;  // pieces per row and read pass
+    static_assert(NP % NPX == 0, "whole read passes");
     const int lane = threadIdx.x & 63;
     // this lane's bucket
     const int br = lane / (M * H), bm = (lane / H) % M, bh = lane % H;
 
-    if (lane <= RPW) st.bounds[lane] = pre.bound;
-    const int32_t next_bound =
-        next_row_begin >= 0 ? load_bound<RPW>(ptr, n_rows, next_row_begin, g.nnz) : 0;
-    wave_lds_sync();
-    const int32_t wb = st.bounds[0], we = st.bounds[RPW];
-    const int32_t brs = st.bounds[br], bre = st.bounds[br + 1];
+    // loads for later tiles: bounds three tiles ahead, the first chunk's
+    // indices two tiles ahead, the second chunk's one tile ahead.  They are
+    // issued after the first chunk's rows are taken and after the next
+    // chunk's loads: loads complete in issue order, so no wait for a chunk's
+    // rows waits for a load issued after them
+    const int32_t b2 = onehot_bound_clamp(p.b2, g.nnz);
+    int32_t b3 = 0, j2 = 0, i1n = 0;
+    auto ahead_loads = [&]() {
+        b3 = onehot_bound_raw<RPW>(ptr, n_rows, tl.r3);
+        j2 = onehot_chunk_idx(idx, __shfl(b2, 0, 64), g.nnz);
+        i1n = onehot_chunk_idx(idx, __shfl(p.b1, 0, 64) + CK, g.nnz);
+    };
+
+    const int32_t wb = __shfl(p.b0, 0, 64), we = __shfl(p.b0, RPW, 64);
+    const int32_t nb0 = __shfl(p.b1, 0, 64), nb1 = __shfl(p.b1, RPW, 64);
+    constexpr int SB = RPW <= 1 ? 0 : RPW <= 2 ? 1 : RPW <= 4 ? 2 : RPW <= 8 ? 3 : 4;  // row bits
     float acc[CH];
 #pragma unroll
     for (int c = 0; c < CH; ++c) acc[c] = 0.f;
 
 #pragma unroll 1
-    for (int32_t c0 = wb; c0 < we; c0 += 64) {
-        const int32_t e = c0 + lane;
-        const bool has = e < we;
-        int32_t other = 0, s = 0;
-        if (has) {
+    for (int32_t c0 = wb; c0 < we; c0 += CK) {
+        // 1. the chunk's rows into LDS; its edges' offsets and decays
 #pragma unroll
-            for (int q = 1; q < RPW; ++q)
-                if (st.bounds[q] <= e) s = q;
-            other = !pre.have_idx || c0 > wb + 64 ? idx[e] : (c0 == wb ? pre.idx0 : pre.idx1);
+        for (int q = 0; q < NR; ++q) st.f[q * RPL + lane / P][lane % P] = p.rows[q];
+        const bool has = lane < CK && c0 + lane < we;
+        const int k = has ? event_index(p.ga.x - p.gb.x, p.ga.y - p.gb.y) : -1;
+        const float sv = has ? event_decay(p.ga.z, p.gb.z, inv_tau) : 0.f;
+        if (lane < CK) st.sv[lane] = sv;
+        const int es = p.es;
+        // 2. the next chunk's loads, then (first chunk) those for later tiles
+        if (c0 + CK < we) {
+            onehot_issue<C, RPW, kT, kBf, NR>(tl.r0, p.b0, c0 + CK, p.i1, g, X, p);
+            p.i1 = onehot_chunk_idx(idx, c0 + 2 * CK, g.nnz);
+        } else if (tl.r1 >= 0 && nb0 < nb1) {
+            onehot_issue<C, RPW, kT, kBf, NR>(tl.r1, p.b1, nb0, p.j1, g, X, p);
         }
-        const int32_t other0 = __shfl(other, 0, 64);  // lane 0 always holds an edge
-        other = has ? other : other0;
-        // 1. the edge's offset index and decay (its endpoints' coordinates), then
-        // the neighbour rows into LDS: instruction q copies rows q*RPL .. q*RPL+RPL-1
-        int4 ga = make_int4(0, 0, 0, 0), gb = ga;
-        if (has) {
-            const int32_t row = row_begin + s;
-            ga = g.ev[kT ? other : row];
-            gb = g.ev[kT ? row : other];
-        }
-        st.nb[lane] = other;
-        wave_lds_sync();
+        if (c0 == wb) ahead_loads();
+        // 3. this lane's bucket: the chunk's edges whose offset bits equal bm's
+        // and whose row bits equal br's
+        uint64_t bsel = __ballot(k >= 0);
 #pragma unroll
-        for (int q = 0; q < P; ++q) {
-            const int32_t src = st.nb[q * RPL + lane / P];
-            const char *gp = static_cast<const char *>(X) + ((int64_t)src * C) * ES + 16 * (lane % P);
-            __builtin_amdgcn_global_load_lds((const void *)gp,
-                                             (lds_void_t *)&st.f[q * RPL][0], 16, 0, 0);
+        for (int b = 0; b < 3; ++b) {
+            const uint64_t v = __ballot((k >> b) & 1);
+            bsel &= (bm >> b) & 1 ? v : ~v;
         }
-        const int k = has ? event_index(ga.x - gb.x, ga.y - gb.y) : -1;
-        st.sv[lane] = has ? event_decay(ga.z, gb.z, inv_tau) : 0.f;
-        // 2. this lane's bucket: the lanes of its row with its offset
-        uint64_t bsel = 0ull;
 #pragma unroll
-        for (int kk = 0; kk < M; ++kk) {
-            const uint64_t bk = __ballot(k == kk);
-            if (kk == bm) bsel = bk;
-        }
-        {
-            const int32_t lo = (brs > c0 ? brs : c0) - c0;
-            const int32_t hi = (bre < c0 + 64 ? bre : c0 + 64) - c0;
-            bsel &= lanes_below(hi) & ~lanes_below(lo);
-        }
-        int32_t steps = __popcll(bsel);
-#pragma unroll
-        for (int dd = 1; dd < 64; dd <<= 1) {
-            const int32_t o = __shfl_xor(steps, dd, 64);
-            steps = o > steps ? o : steps;
+        for (int b = 0; b < SB; ++b) {
+            const uint64_t v = __ballot((es >> b) & 1);
+            bsel &= (br >> b) & 1 ? v : ~v;
         }
         wave_lds_sync();
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the direct loads have landed
-        // 3. the bucket's rows, U at a time, lowest lane first: the reads of a
-        // group are issued (by the lanes whose bucket reaches that far) before
-        // its products, which take weight 0 past the bucket's end
-#pragma unroll 1
-        for (int32_t q0 = 0; q0 < steps; q0 += U) {
-            int32_t li[U];
+        // 4. the bucket's rows, U at a time, lowest lane first: the reads of a
+        // group are issued before its products; past the bucket's end a lane
+        // reads the row of zeros with weight 0
+        if (__ballot(bsel != 0ull) != 0ull) do {
+            int32_t li[U];  // staged edge, or CK (the row of zeros) past the bucket's end
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                li[u] = bsel != 0ull ? (int32_t)__builtin_ctzll(bsel) : 64;
+                li[u] = bsel != 0ull ? (int32_t)__builtin_ctzll(bsel) : CK;
                 bsel &= bsel - 1ull;
             }
             float vv[U];
-            uint4 x[U][NP];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                vv[u] = 0.f;
+            for (int u = 0; u < U; ++u) vv[u] = st.sv[li[u]];
+            // the pieces in passes of NPX (eight 16-byte reads in flight), in an
+            // order rotated by the offset, so the lanes of one LDS cycle read
+            // different banks (rows are 128 B apart)
 #pragma unroll
-                for (int c = 0; c < NP; ++c) x[u][c] = uint4{0u, 0u, 0u, 0u};
-                if (li[u] < 64) {
-                    vv[u] = st.sv[li[u]];
-                    // pieces in an order rotated by the offset, so the lanes of one
-                    // LDS cycle read different banks (rows are 128 B apart)
+            for (int c0p = 0; c0p < NP; c0p += NPX) {
+                u32x4 x[U][NPX];
 #pragma unroll
-                    for (int c = 0; c < NP; ++c) x[u][c] = st.f[li[u]][bh * NP + (c + bm) % NP];
-                }
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int c = 0; c < NPX; ++c)
+                        x[u][c] = st.f[li[u]][bh * NP + (c0p + c + bm) % NP];
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int c = 0; c < NPX; ++c)
+#pragma unroll
+                        for (int q = 0; q < VPP; ++q)
+                            acc[VPP * (c0p + c) + q] += vv[u] * piece_elem<kBf>(x[u][c], q);
             }
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-#pragma unroll
-                for (int c = 0; c < NP; ++c)
-#pragma unroll
-                    for (int q = 0; q < VPP; ++q)
-                        acc[VPP * c + q] += vv[u] * piece_elem<kBf>(x[u][c], q);
-        }
+        } while (__ballot(bsel != 0ull) != 0ull);
         wave_lds_sync();  // the stage is rewritten by the next chunk
+    }
+    // rows without edges: the next tile's first chunk, and the loads ahead
+    if (wb >= we) {
+        if (tl.r1 >= 0 && nb0 < nb1)
+            onehot_issue<C, RPW, kT, kBf, NR>(tl.r1, p.b1, nb0, p.j1, g, X, p);
+        if (g.nnz > 0) ahead_loads();
     }
     // this lane's (row, offset, part) block of the tile row; piece c of acc is
     // piece (c + bm) % NP of the block
@@ -620,28 +740,19 @@ __device__ __forceinline__ GatherAhead gather_rows_onehot(
               ((int64_t)(local_row0 + br) * S + bm * C + bh * CH) * ES;
 #pragma unroll
     for (int c = 0; c < NP; ++c) {
-        uint4 v;
-        if constexpr (kBf) {
-            uint32_t w[4];
+        u32x4 v;
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                w[q] = (uint32_t)f2bf(acc[VPP * c + 2 * q]) |
-                       ((uint32_t)f2bf(acc[VPP * c + 2 * q + 1]) << 16);
-            v = uint4{w[0], w[1], w[2], w[3]};
-        } else {
-            v = uint4{__float_as_uint(acc[VPP * c]), __float_as_uint(acc[VPP * c + 1]),
-                      __float_as_uint(acc[VPP * c + 2]), __float_as_uint(acc[VPP * c + 3])};
-        }
-        *reinterpret_cast<uint4 *>(o + 16 * ((c + bm) % NP)) = v;
+        for (int q = 0; q < 4; ++q)
+            v[q] = kBf ? (uint32_t)f2bf(acc[VPP * c + 2 * q]) |
+                             ((uint32_t)f2bf(acc[VPP * c + 2 * q + 1]) << 16)
+                       : __float_as_uint(acc[VPP * c + q]);
+        *reinterpret_cast<u32x4 *>(o + 16 * ((c + bm) % NP)) = v;
     }
-    GatherAhead ahead{next_bound, 0, false, 0};
-    if (next_row_begin >= 0) {
-        const int32_t nb0 = __shfl(next_bound, 0, 64), nb1 = __shfl(next_bound, RPW, 64);
-        ahead.idx0 = nb0 + lane < nb1 ? idx[nb0 + lane] : 0;
-        ahead.idx1 = nb0 + 64 + lane < nb1 ? idx[nb0 + 64 + lane] : 0;
-        ahead.have_idx = true;
-    }
-    return ahead;
+    p.b0 = p.b1;
+    p.b1 = b2;
+    p.b2 = b3;
+    p.j1 = j2;
+    p.i1 = i1n;
 }
 
 // acc[u][t] += A_tile[16 rb_u .., :] x B[:, 16 cb_t ..] for the 16x16 blocks of
@@ -1291,15 +1402,18 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     using DT = typename std::conditional<kBf, uint16_t, float>::type;
     __shared__ __attribute__((aligned(16))) DT Ds[2][TR * SD];
     __shared__ __attribute__((aligned(16))) DT Fs[2][TR * SF];
-    // the fixed-decay event basis in float32 takes the one-hot gather
-    // while its stage (a chunk of neighbour rows per gather wave) fits in LDS
+    // the fixed-decay event basis takes the one-hot gather while its stage (a
+    // chunk of 64 neighbour rows per gather wave) fits in LDS.  (Chunks of 32
+    // leave the registers for four bucket rows read together, but a chunk
+    // then spans about half of a wave's rows, and the walk ran slower.)
+    constexpr int CK = 64;
+    constexpr int RBY = CO * (int)sizeof(DT);  // bytes per gathered row
     constexpr bool kOneHot =
         kBasis == SBC_BASIS_EVENT8 + 1 && M == 8 && RPW * M <= 64 && 64 % (RPW * M) == 0 &&
-        (CO * sizeof(DT)) % 16 == 0 && 64 % (CO * sizeof(DT) / 16) == 0 &&
-        2 * TR * (SD + SF) * sizeof(DT) + kWsGather * sizeof(OneHotStage<CO * sizeof(DT)>) <=
-            163840;
-    using Stage = typename std::conditional<kOneHot, OneHotStage<CO * sizeof(DT)>,
-                                            EdgeStage<M>>::type;
+        RBY % 16 == 0 && 64 % (RBY / 16) == 0 && CK % (64 / (RBY / 16)) == 0 &&
+        2 * TR * (SD + SF) * sizeof(DT) + kWsGather * sizeof(OneHotStage<RBY, CK>) <= 163840;
+    using Stage =
+        typename std::conditional<kOneHot, OneHotStage<RBY, CK>, EdgeStage<M>>::type;
     __shared__ __attribute__((aligned(16))) Stage stage[kWsGather];
 
     const int lane = threadIdx.x & 63;
@@ -1321,26 +1435,40 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     const int32_t n_my = t_first < t_end ? (t_end - t_first + gx - 1) / gx : 0;
 
     // row bounds (and first neighbour indices) of the gather's next tile,
-    // loaded one tile ahead
+    // loaded one tile ahead; the one-hot gather keeps its own loads in flight
+    // further ahead (OneHotPipe)
     GatherAhead ahead{
-        n_my > 0 ? load_bound<RPW>(col_ptr, n_in, t_first * TR + w * RPW, g.nnz) : 0, 0, false};
+        n_my > 0 && !kOneHot ? load_bound<RPW>(col_ptr, n_in, t_first * TR + w * RPW, g.nnz) : 0,
+        0, false};
+    constexpr int NR = kOneHot ? CK / (64 / (RBY / 16)) : 1;  // row pieces per lane and chunk
+    OneHotPipe<NR> pipe;
+    auto wave_rows = [&](int32_t s) {
+        return s < n_my ? (t_first + s * gx) * TR + w * RPW : -1;
+    };
     auto load_tile = [&](int32_t s, int buf) {
-        const int32_t row0 = (t_first + s * gx) * TR;
-        const int32_t next = s + 1 < n_my ? (t_first + (s + 1) * gx) * TR + w * RPW : -1;
-        if constexpr (kOneHot)
-            ahead = gather_rows_onehot<CO, RPW, true, kBf>(
-                row0 + w * RPW, n_in, col_ptr, row_idx, g, dY, Ds[buf], SD, w * RPW, stage[w],
-                inv_tau, ahead, next);
-        else
+        if constexpr (kOneHot) {
+            const OneHotTiles tl{wave_rows(s), wave_rows(s + 1), wave_rows(s + 2),
+                                 wave_rows(s + 3)};
+            gather_rows_onehot<CO, RPW, true, kBf, NR>(tl, n_in, col_ptr, row_idx, g, dY,
+                                                       Ds[buf], SD, w * RPW, stage[w], inv_tau,
+                                                       pipe);
+        } else {
             ahead = gather_rows<M, CO, kBasis, kBf, kBf, true, RPW, true>(
-                row0 + w * RPW, n_in, col_ptr, row_idx, perm, v, g, dY, Ds[buf], SD, w * RPW,
-                stage[w], inv_r, inv_tau, ahead, next);
+                wave_rows(s), n_in, col_ptr, row_idx, perm, v, g, dY, Ds[buf], SD, w * RPW,
+                stage[w], inv_r, inv_tau, ahead, wave_rows(s + 1));
+        }
     };
 
     // The two roles run separate loops (so the matrix waves' dW accumulators
     // are not live in the gather code); each role passes the block barrier
     // exactly n_my + 1 times, in the same steps.
     if (gatherer) {
+        if constexpr (kOneHot) onehot_stage_init(stage[w]);
+        if constexpr (kOneHot)
+            if (n_my > 0)
+                onehot_prologue<CO, RPW, true, kBf, NR>(
+                    OneHotTiles{wave_rows(0), wave_rows(1), wave_rows(2), -1}, n_in, col_ptr,
+                    row_idx, g, dY, pipe);
         if (n_my > 0) load_tile(0, 0);
         __syncthreads();
 #pragma unroll 1
