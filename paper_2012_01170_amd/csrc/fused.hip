@@ -29,6 +29,7 @@
 //                  does not depend on scheduling.
 // Sums over edges run in pattern order inside a lane; no floating-point
 // atomics are used anywhere.
+#include <cstdlib>
 #include <type_traits>
 #include <utility>
 
@@ -86,6 +87,12 @@ struct KGeo {
 // basis with respect to its rates (the decay gradient's D-route pass).
 constexpr int kDecayDerivMode = 16;
 
+// Basis mode of the backward for the fixed-decay event basis when the
+// gathered rows, the packed events or the pattern arrays pass 4 GiB: the
+// generic gather (64-bit addressing) instead of the one-hot gather, whose
+// loads take 32-bit byte offsets from their arrays' bases.
+constexpr int kEvent8WideMode = 17;
+
 __global__ void pack_events_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
                                    const int32_t *__restrict__ t, int32_t n,
                                    int4 *__restrict__ out) {
@@ -105,7 +112,7 @@ __device__ __forceinline__ void edge_basis(const KGeo &g, const float *__restric
     if constexpr (kBasis == 0) {
 #pragma unroll
         for (int m = 0; m < M; ++m) out[m] = v[ev * M + m];
-    } else if constexpr (kBasis == SBC_BASIS_EVENT8 + 1) {
+    } else if constexpr (kBasis == SBC_BASIS_EVENT8 + 1 || kBasis == kEvent8WideMode) {
         const int4 a = g.ev[i], b = g.ev[j];
         const int k = event_index(a.x - b.x, a.y - b.y);
         const float d = event_decay(a.z, b.z, inv_tau);
@@ -547,13 +554,15 @@ __device__ __forceinline__ int32_t onehot_bound_clamp(int32_t b, int32_t nnz) {
 
 // idx of the chunk at edge c0 (lane e: edge c0 + e), loaded by every lane
 // without a branch: the edge is clamped into [0, nnz) (nnz > 0), and what a
-// lane past its rows' end holds is not used (onehot_issue).
+// lane past its rows' end holds is not used (onehot_issue).  (The one-hot
+// gather's loads use 32-bit byte offsets: nnz * 4 < 2^32.)
 __device__ __forceinline__ int32_t onehot_chunk_idx(const int32_t *__restrict__ idx, int32_t c0,
                                                     int32_t nnz) {
     int32_t e = c0 + (int32_t)(threadIdx.x & 63);
     e = e < nnz ? e : nnz - 1;
     e = e > 0 ? e : 0;
-    return idx[e];
+    return *reinterpret_cast<const int32_t *>(reinterpret_cast<const char *>(idx) +
+                                              ((uint32_t)e << 2));
 }
 
 // Issue the loads of the chunk at edge c0 (c0 < the rows' end) of the rows
@@ -561,7 +570,8 @@ __device__ __forceinline__ int32_t onehot_chunk_idx(const int32_t *__restrict__ 
 // onehot_chunk_idx): lane l's endpoint coordinates for edge c0 + l, and row
 // piece q of lane l, piece l % P of staged row q RPL + l / P.  Lanes past the
 // rows' end or the chunk's CK edges load lane 0's edge, so every lane's
-// addresses are in bounds.
+// addresses are in bounds.  Byte offsets from X and from the packed events
+// are 32-bit (the host checks that both arrays are under 4 GiB).
 template <int C, int RPW, bool kT, bool kBf, int NR>
 __device__ __forceinline__ void onehot_issue(int32_t row_begin, int32_t bnd, int32_t c0,
                                              int32_t other, const KGeo &g,
@@ -573,23 +583,27 @@ __device__ __forceinline__ void onehot_issue(int32_t row_begin, int32_t bnd, int
     static_assert(CK == 32 || CK == 64, "chunk size");
     const int lane = threadIdx.x & 63;
     const int32_t e = c0 + lane;
+    // the row of the lane's edge: the row starts (bounds 1 .. RPW-1, read as
+    // wave-uniform values) at or below it
     int s = 0;
 #pragma unroll
-    for (int q = 1; q < RPW; ++q)
-        if (__shfl(bnd, q, 64) <= e) s = q;
-    const bool has = lane < CK && e < __shfl(bnd, RPW, 64);
-    const int32_t other0 = __shfl(other, 0, 64), s0 = __shfl(s, 0, 64);
+    for (int q = 1; q < RPW; ++q) s += __builtin_amdgcn_readlane(bnd, q) <= e ? 1 : 0;
+    const bool has = lane < CK && e < __builtin_amdgcn_readlane(bnd, RPW);
+    const int32_t other0 = __builtin_amdgcn_readlane(other, 0);
+    const int32_t s0 = __builtin_amdgcn_readlane(s, 0);
     other = has ? other : other0;
     s = has ? s : s0;
+    const char *Xb = static_cast<const char *>(X);
 #pragma unroll
     for (int q = 0; q < NR; ++q) {
         const int32_t src = __shfl(other, q * RPL + lane / P, 64);
-        p.rows[q] = *reinterpret_cast<const u32x4 *>(static_cast<const char *>(X) +
-                                                     (int64_t)src * C * ES + 16 * (lane % P));
+        p.rows[q] = *reinterpret_cast<const u32x4 *>(
+            Xb + ((uint32_t)src * (uint32_t)(C * ES) + (uint32_t)(16 * (lane % P))));
     }
     const int32_t row = row_begin + s;
-    p.ga = g.ev[kT ? other : row];
-    p.gb = g.ev[kT ? row : other];
+    const char *evb = reinterpret_cast<const char *>(g.ev);
+    p.ga = *reinterpret_cast<const int4 *>(evb + ((uint32_t)(kT ? other : row) << 4));
+    p.gb = *reinterpret_cast<const int4 *>(evb + ((uint32_t)(kT ? row : other) << 4));
     p.es = s;
 }
 
@@ -650,12 +664,14 @@ __device__ __forceinline__ void gather_rows_onehot(
     int32_t b3 = 0, j2 = 0, i1n = 0;
     auto ahead_loads = [&]() {
         b3 = onehot_bound_raw<RPW>(ptr, n_rows, tl.r3);
-        j2 = onehot_chunk_idx(idx, __shfl(b2, 0, 64), g.nnz);
-        i1n = onehot_chunk_idx(idx, __shfl(p.b1, 0, 64) + CK, g.nnz);
+        j2 = onehot_chunk_idx(idx, __builtin_amdgcn_readlane(b2, 0), g.nnz);
+        i1n = onehot_chunk_idx(idx, __builtin_amdgcn_readlane(p.b1, 0) + CK, g.nnz);
     };
 
-    const int32_t wb = __shfl(p.b0, 0, 64), we = __shfl(p.b0, RPW, 64);
-    const int32_t nb0 = __shfl(p.b1, 0, 64), nb1 = __shfl(p.b1, RPW, 64);
+    const int32_t wb = __builtin_amdgcn_readlane(p.b0, 0);
+    const int32_t we = __builtin_amdgcn_readlane(p.b0, RPW);
+    const int32_t nb0 = __builtin_amdgcn_readlane(p.b1, 0);
+    const int32_t nb1 = __builtin_amdgcn_readlane(p.b1, RPW);
     constexpr int SB = RPW <= 1 ? 0 : RPW <= 2 ? 1 : RPW <= 4 ? 2 : RPW <= 8 ? 3 : 4;  // row bits
     float acc[CH];
 #pragma unroll
@@ -1837,6 +1853,9 @@ BwdFn bwd_for(int basis_mode) {
             if constexpr (M >= 16 && M % 8 == 0)
                 return bwd_ws_kernel<M, CI, CO, kDecayDerivMode, kBf>;
             return nullptr;
+        case kEvent8WideMode:
+            if constexpr (M == 8) return bwd_ws_kernel<M, CI, CO, kEvent8WideMode, kBf>;
+            return nullptr;
     }
     return nullptr;
 }
@@ -2048,7 +2067,21 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
                           const sbc_geometry *g, int32_t M, const void *F, const void *W,
                           const void *dY, bool bf, int32_t CI, int32_t CO, float *dF, float *dW,
                           void *ws, hipStream_t stream, bool decay_derivative) {
-    BwdFn fn = find_bwd(Shape{M, CI, CO, bf}, decay_derivative ? kDecayDerivMode : basis_mode_of(v, g));
+    int mode = decay_derivative ? kDecayDerivMode : basis_mode_of(v, g);
+    if (mode == SBC_BASIS_EVENT8 + 1) {
+        // the one-hot gather's 32-bit byte offsets: dY rows, packed events,
+        // the pattern's indices and column bounds under 4 GiB.  The
+        // environment variable SBC_EVENT8_WIDE_PATH=1 takes the other path at
+        // any size (so that tests can run it).
+        const int64_t n_ev = csr->n_cols > csr->n_rows ? csr->n_cols : csr->n_rows;
+        const int64_t lim = (int64_t)1 << 32;
+        const char *force = std::getenv("SBC_EVENT8_WIDE_PATH");
+        if ((int64_t)csr->n_rows * CO * (bf ? 2 : 4) >= lim || n_ev * 16 >= lim ||
+            csr->nnz_bound * 4 >= lim || ((int64_t)csr->n_cols + 1) * 4 >= lim ||
+            (force && force[0] == '1'))
+            mode = kEvent8WideMode;
+    }
+    BwdFn fn = find_bwd(Shape{M, CI, CO, bf}, mode);
     if (!fn) return fail(SBC_ERR_UNSUPPORTED, "no fused backward for this shape");
     const int32_t n_in = csr->n_cols;
     char *base = static_cast<char *>(ws);

@@ -546,6 +546,25 @@ def test_backward_without_edge_perm(name, order):
         G.sbc.conv_backward(csr, bare, t["F"], t["W"], t["dY"], v=vv, order=order)
 
 
+@pytest.mark.parametrize("name", ["ev_small", "ev_bf16", "fz_ev32", "fz_tiny_ev"])
+def test_event_backward_wide_offset_path(name, monkeypatch):
+    """The fixed-decay event backward takes the generic gather (64-bit
+    addressing) when its arrays pass 4 GiB; the environment variable
+    SBC_EVENT8_WIDE_PATH=1 takes it at any size.  Both paths agree with the
+    oracle."""
+    print(f"[backward wide path] {name}", flush=True)
+    w, rp, ci, v = case(name)
+    t, csr = gpu_case(name)
+    csc = G.sbc.csr_transpose(csr)
+    dF_ref, dW_ref = oracle_backward(name)
+    monkeypatch.setenv("SBC_EVENT8_WIDE_PATH", "1")
+    dF, dW = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"], geometry=G.geometry(w, t),
+                                 order="spmm_first")
+    monkeypatch.delenv("SBC_EVENT8_WIDE_PATH")
+    assert G.row_error(dF.cpu().numpy(), dF_ref) < tol(w)
+    assert G.norm_error(dW.cpu().numpy(), dW_ref) < tol(w)
+
+
 def test_transpose_by_radix_sort():
     """Patterns of 2^21 edges or more are transposed by the radix sort; trailing
     columns without edges must still get their (empty) ranges."""
