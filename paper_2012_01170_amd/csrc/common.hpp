@@ -82,6 +82,13 @@ enum : uint32_t {
 size_t scan_workspace_bytes(int64_t n);
 sbc_status exclusive_scan_i32(const int32_t *counts, int32_t *out, int64_t n, int64_t *total64,
                               void *ws, hipStream_t stream, int32_t *out2 = nullptr);
+// Exclusive scans of two arrays of n items (a into a_out, b into b_out, each
+// with its total at [n]) in one pair of launches; workspace
+// scan2_workspace_bytes(n).
+size_t scan2_workspace_bytes(int64_t n);
+sbc_status exclusive_scan2_i32(const int32_t *a, int32_t *a_out, const int32_t *b,
+                               int32_t *b_out, int64_t n, int64_t *a_total64,
+                               int64_t *b_total64, void *ws, hipStream_t stream);
 
 // Fill n int32 words with a value (a kernel, not a memset node).
 sbc_status fill_i32(int32_t *p, int32_t value, int64_t n, hipStream_t stream);

@@ -318,7 +318,7 @@ EventsWs carve_events(void *base, int32_t n, int64_t npix, size_t *bytes) {
     w.col_len = cv.take<int32_t>(n);
     w.total = cv.take<int64_t>(2);
     w.status = cv.take<uint32_t>(4);
-    w.scan_ws = cv.take<char>(scan_workspace_bytes(n));
+    w.scan_ws = cv.take<char>(scan2_workspace_bytes(n));
     w.sort_ws = cv.take<char>(radix_sort_workspace_bytes(n));
     if (bytes) *bytes = cv.used;
     return w;
@@ -407,7 +407,13 @@ sbc_status search_events(const int32_t *px, const int32_t *py, const int32_t *t,
         C.col_len = col_ptr ? ws.col_len : nullptr;
         SBC_TRY(tiles_dispatch<false>(half_extent, C, stream));
     }
-    SBC_TRY(exclusive_scan_i32(ws.row_len, row_ptr, n, ws.total, ws.scan_ws, stream));
+    // row and column pointers (the column lengths are written by the same
+    // count pass), in one pair of scan launches
+    if (col_ptr)
+        SBC_TRY(exclusive_scan2_i32(ws.row_len, row_ptr, ws.col_len, col_ptr, n, ws.total,
+                                    ws.total + 1, ws.scan_ws, stream));
+    else
+        SBC_TRY(exclusive_scan_i32(ws.row_len, row_ptr, n, ws.total, ws.scan_ws, stream));
     if (nnz_host) {
         int64_t host[2];
         uint32_t st = 0;
@@ -422,7 +428,6 @@ sbc_status search_events(const int32_t *px, const int32_t *py, const int32_t *t,
             return fail(SBC_ERR_CAPACITY, "col_capacity " + std::to_string(col_capacity) +
                                               " < E = " + std::to_string(host[0]));
     }
-    if (col_ptr) SBC_TRY(exclusive_scan_i32(ws.col_len, col_ptr, n, ws.total, ws.scan_ws, stream));
     if (n > 0 && col_capacity > 0) {
         TileArgs F = A;
         F.row_ptr = row_ptr;

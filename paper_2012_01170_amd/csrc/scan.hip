@@ -40,10 +40,17 @@ __device__ int64_t block_inclusive_scan(int64_t x, int64_t *lds /*[4]*/, int64_t
     return x + before;
 }
 
+// Block totals; with in2 (two arrays of n items scanned in one launch) blocks
+// nb .. 2 nb - 1 take in2, and sums holds the first array's totals, then the
+// second's.
 template <typename T>
-__global__ void __launch_bounds__(kThreads) block_sums_kernel(const T *in, int64_t n, int64_t *sums) {
+__global__ void __launch_bounds__(kThreads)
+    block_sums_kernel(const T *in, int64_t n, int64_t *sums, const T *in2, int64_t nb) {
     __shared__ int64_t lds[kThreads / 64];
-    const int64_t base = (int64_t)blockIdx.x * kPerBlock + (int64_t)threadIdx.x * kItems;
+    const bool second = in2 && (int64_t)blockIdx.x >= nb;
+    if (second) in = in2;
+    const int64_t blk = second ? (int64_t)blockIdx.x - nb : (int64_t)blockIdx.x;
+    const int64_t base = blk * kPerBlock + (int64_t)threadIdx.x * kItems;
     int64_t s = 0;
 #pragma unroll
     for (int k = 0; k < kItems; ++k)
@@ -169,15 +176,29 @@ __global__ void __launch_bounds__(kSmallThreads)
 
 // Second pass of the two-kernel scan: block b first adds up the totals of
 // blocks 0..b-1 (all 256 threads, then a block reduction; the order is fixed),
-// then scans its own items with that offset.
+// then scans its own items with that offset.  With in2 (a second array of n
+// items), blocks nb .. 2 nb - 1 scan in2 into outb with the second array's
+// totals (sums + nb), and its grand total goes to totalb.
 __global__ void __launch_bounds__(kThreads)
     self_offset_scan_kernel(const int32_t *__restrict__ in, int64_t n,
                             const int64_t *__restrict__ sums, int32_t *__restrict__ out,
-                            int32_t *__restrict__ out2, int64_t *__restrict__ total64) {
+                            int32_t *__restrict__ out2, int64_t *__restrict__ total64,
+                            const int32_t *__restrict__ in2, int32_t *__restrict__ outb,
+                            int64_t *__restrict__ totalb, int64_t nb) {
     __shared__ int64_t lds[kThreads / 64];
     __shared__ int64_t red[kThreads];
+    const bool second = in2 && (int64_t)blockIdx.x >= nb;
+    const int64_t blk = second ? (int64_t)blockIdx.x - nb : (int64_t)blockIdx.x;
+    const int64_t last_blk = in2 ? nb - 1 : (int64_t)gridDim.x - 1;
+    if (second) {
+        in = in2;
+        out = outb;
+        out2 = nullptr;
+        total64 = totalb;
+        sums += nb;
+    }
     int64_t part = 0;
-    for (int64_t q = threadIdx.x; q < (int64_t)blockIdx.x; q += kThreads) part += sums[q];
+    for (int64_t q = threadIdx.x; q < blk; q += kThreads) part += sums[q];
     red[threadIdx.x] = part;
     __syncthreads();
     for (int w = kThreads / 2; w > 0; w >>= 1) {
@@ -185,7 +206,7 @@ __global__ void __launch_bounds__(kThreads)
         __syncthreads();
     }
     const int64_t offset = red[0];
-    const int64_t base = (int64_t)blockIdx.x * kPerBlock + (int64_t)threadIdx.x * kItems;
+    const int64_t base = blk * kPerBlock + (int64_t)threadIdx.x * kItems;
     int64_t v[kItems];
     int64_t s = 0;
 #pragma unroll
@@ -205,7 +226,7 @@ __global__ void __launch_bounds__(kThreads)
         }
         run += v[k];
     }
-    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == kThreads - 1) {
+    if (blk == last_blk && threadIdx.x == kThreads - 1) {
         const int64_t grand = offset + total;
         const int32_t o = (int32_t)(grand > (int64_t)INT_MAX ? (int64_t)INT_MAX : grand);
         out[n] = o;
@@ -228,7 +249,7 @@ sbc_status scan_i64_inplace(int64_t *a, int64_t n, char *ws, hipStream_t stream)
     int64_t *sums = reinterpret_cast<int64_t *>(ws);
     char *rest = ws + align_up(nb * sizeof(int64_t));
     hipLaunchKernelGGL((block_sums_kernel<int64_t>), dim3((unsigned)nb), dim3(kThreads), 0, stream,
-                       a, n, sums);
+                       a, n, sums, (const int64_t *)nullptr, nb);
     SBC_LAUNCH_CHECK();
     SBC_TRY(scan_i64_inplace(sums, nb, rest, stream));
     hipLaunchKernelGGL((block_scan_kernel<int64_t, int64_t>), dim3((unsigned)nb), dim3(kThreads),
@@ -309,17 +330,44 @@ sbc_status exclusive_scan_i32(const int32_t *counts, int32_t *out, int64_t n, in
     int64_t *sums = reinterpret_cast<int64_t *>(w);
     char *rest = w + align_up(nb * sizeof(int64_t));
     hipLaunchKernelGGL((block_sums_kernel<int32_t>), dim3((unsigned)nb), dim3(kThreads), 0, stream,
-                       counts, n, sums);
+                       counts, n, sums, (const int32_t *)nullptr, nb);
     SBC_LAUNCH_CHECK();
     if (nb <= kSelfOffsetBlocks) {
         hipLaunchKernelGGL(self_offset_scan_kernel, dim3((unsigned)nb), dim3(kThreads), 0, stream,
-                           counts, n, (const int64_t *)sums, out, out2, total64);
+                           counts, n, (const int64_t *)sums, out, out2, total64,
+                           (const int32_t *)nullptr, (int32_t *)nullptr, (int64_t *)nullptr, nb);
         SBC_LAUNCH_CHECK();
         return SBC_OK;
     }
     SBC_TRY(scan_i64_inplace(sums, nb, rest, stream));
     hipLaunchKernelGGL((block_scan_kernel<int32_t, int32_t>), dim3((unsigned)nb), dim3(kThreads),
                        0, stream, counts, n, (const int64_t *)sums, out, total64, true, out2);
+    SBC_LAUNCH_CHECK();
+    return SBC_OK;
+}
+
+size_t scan2_workspace_bytes(int64_t n) {
+    const int64_t nb = (n + kPerBlock - 1) / kPerBlock;
+    const size_t pair = align_up((nb > 0 ? 2 * nb : 1) * sizeof(int64_t));
+    const size_t one = scan_workspace_bytes(n);
+    return pair > one ? pair : one;
+}
+
+sbc_status exclusive_scan2_i32(const int32_t *a, int32_t *a_out, const int32_t *b,
+                               int32_t *b_out, int64_t n, int64_t *a_total64,
+                               int64_t *b_total64, void *ws, hipStream_t stream) {
+    const int64_t nb = (n + kPerBlock - 1) / kPerBlock;
+    if (n <= kSmallMax || nb > kSelfOffsetBlocks) {
+        SBC_TRY(exclusive_scan_i32(a, a_out, n, a_total64, ws, stream));
+        return exclusive_scan_i32(b, b_out, n, b_total64, ws, stream);
+    }
+    int64_t *sums = static_cast<int64_t *>(ws);
+    hipLaunchKernelGGL((block_sums_kernel<int32_t>), dim3((unsigned)(2 * nb)), dim3(kThreads), 0,
+                       stream, a, n, sums, b, nb);
+    SBC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(self_offset_scan_kernel, dim3((unsigned)(2 * nb)), dim3(kThreads), 0, stream,
+                       a, n, (const int64_t *)sums, a_out, (int32_t *)nullptr, a_total64, b, b_out,
+                       b_total64, nb);
     SBC_LAUNCH_CHECK();
     return SBC_OK;
 }
