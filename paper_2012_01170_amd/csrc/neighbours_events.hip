@@ -189,6 +189,14 @@ __device__ __forceinline__ void tile_events(const TileArgs &A, const int32_t *Li
         const int p = (c / A.tx + h) * HX + (c % A.tx + h);
         const int32_t a = start[p] + (u - c_off[c]);
         const int32_t i = Li[a], ti = Lt[a];
+        const bool rev = kFill ? A.col_ptr != nullptr : A.col_len != nullptr;
+        // the fill's output positions, loaded before the searches so that their
+        // latency passes during them
+        int32_t row_dst = 0, col_dst = 0;
+        if constexpr (kFill) {
+            if (dir != 2) row_dst = A.row_ptr[i];
+            if (rev && dir != 1) col_dst = A.col_ptr[i];
+        }
         int32_t rlo[K], rhi[K];
         if (dir != 2) {
             const int32_t cnt = tile_runs<kSide, false>(i, ti, A.window, p, HX, Li, Lt, start,
@@ -196,17 +204,16 @@ __device__ __forceinline__ void tile_events(const TileArgs &A, const int32_t *Li
             if constexpr (!kFill) {
                 A.row_len[i] = cnt;
             } else {
-                copy_runs<K>(Li, rlo, rhi, A.col_idx, A.row_ptr[i], A.cap);
+                copy_runs<K>(Li, rlo, rhi, A.col_idx, row_dst, A.cap);
             }
         }
-        const bool rev = kFill ? A.col_ptr != nullptr : A.col_len != nullptr;
         if (rev && dir != 1) {
             const int32_t cnt_t = tile_runs<kSide, true>(i, ti, A.window, p, HX, Li, Lt, start,
                                                          len, rlo, rhi);
             if constexpr (!kFill)
                 A.col_len[i] = cnt_t;
             else
-                copy_runs<K>(Li, rlo, rhi, A.row_idx, A.col_ptr[i], A.cap);
+                copy_runs<K>(Li, rlo, rhi, A.row_idx, col_dst, A.cap);
         }
     }
 }
