@@ -284,6 +284,37 @@ def summarize_route(workload, runs, probe_mb, command, steps):
     return "\n".join(out) + "\n"
 
 
+def summarize_counters(dirs, command):
+    """Text summary of rocprofv3 --pmc runs of SQ counters: per profiled kernel
+    (those with at least 2% of the largest one's wave-cycles), each counter's
+    reading per dispatch
+    (summed over the chip as the profiler reports it), averaged over the
+    dispatches."""
+    per = {}
+    for d in dirs:
+        for r in _counter_rows(d):
+            k = short_kernel_name(r["Kernel_Name"])
+            per.setdefault(k, {}).setdefault(r["Counter_Name"], {}).setdefault(
+                r.get("Dispatch_Id", ""), 0.0)
+            per[k][r["Counter_Name"]][r.get("Dispatch_Id", "")] += float(r["Counter_Value"])
+    out = ["# rocprofv3 SQ counters per dispatch (mean over dispatches)", f"# command: {command}",
+           f"source_fingerprint: {source_fingerprint()}"]
+    def weight(k):
+        return statistics.mean(per[k].get("SQ_WAVE_CYCLES", {"": 0.0}).values())
+
+    order = sorted(per, key=lambda k: -weight(k))
+    top = weight(order[0]) if order else 0.0
+    for k in order:
+        cs = per[k]
+        if "SQ_WAVE_CYCLES" not in cs or weight(k) < 0.02 * top:
+            continue  # kernels below 2% of the largest one's wave-cycles are left out
+        out.append(f"kernel {k}")
+        for c in sorted(cs):
+            vals = list(cs[c].values())
+            out.append(f"  {c} {statistics.mean(vals):.4g}  ({len(vals)} dispatches)")
+    return "\n".join(out) + "\n"
+
+
 def summarize_trace(trace_dir, command, bench_json=None):
     """Text summary of a rocprofv3 --kernel-trace --stats run (top kernels by time)."""
     files = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
@@ -797,10 +828,15 @@ def main(argv=None):
     ap.add_argument("--summarize-route", nargs="+", metavar="ARG",
                     help="WORKLOAD then, per order, ORDER BENCH_JSON FETCH_DIR WRITE_DIR MFMA_DIR: "
                          "print the evaluation orders side by side and exit")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="DIR",
+                    help="print per-kernel means of rocprofv3 --pmc counter runs and exit")
     ap.add_argument("--command", default="", help="the profiled command, quoted in a summary")
     a = ap.parse_args(argv)
     if a.summarize_trace:
         sys.stdout.write(summarize_trace(a.summarize_trace, a.command, a.bench_json))
+        return 0
+    if a.summarize_counters:
+        sys.stdout.write(summarize_counters(a.summarize_counters, a.command))
         return 0
     if a.summarize_route:
         w, rest = a.summarize_route[0], a.summarize_route[1:]
