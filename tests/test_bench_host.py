@@ -74,6 +74,31 @@ def test_traffic_summary_is_calibrated_by_the_copy_probe(tmp_path):
     assert line[6] == bench.kernel_fingerprint("bwd_ws_kernel")
 
 
+def test_counter_summary_averages_dispatches_and_drops_small_kernels(tmp_path):
+    """Per kernel, a counter's readings are averaged over dispatches; kernels
+    under 2% of the largest one's wave-cycles are left out."""
+    big = "void sbc::(anonymous namespace)::fwd_reg_kernel<8, 32, 32, 3, false>(A)"
+    small = "void sbc::(anonymous namespace)::pack_events_kernel(A)"
+    d = tmp_path / "sq"
+    d.mkdir()
+    with open(d / "a_counter_collection.csv", "w", newline="") as f:
+        wr = csv.DictWriter(f, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name",
+                                           "Counter_Value"])
+        wr.writeheader()
+        for i, v in ((1, 100.0), (2, 300.0)):
+            wr.writerow({"Dispatch_Id": i, "Kernel_Name": big, "Counter_Name": "SQ_WAVE_CYCLES",
+                         "Counter_Value": v})
+            wr.writerow({"Dispatch_Id": i, "Kernel_Name": big, "Counter_Name": "SQ_INSTS_VALU",
+                         "Counter_Value": 2 * v})
+        wr.writerow({"Dispatch_Id": 3, "Kernel_Name": small, "Counter_Name": "SQ_WAVE_CYCLES",
+                     "Counter_Value": 1.0})
+    text = bench.summarize_counters([str(d)], "cmd")
+    assert "kernel fwd_reg_kernel<8, 32, 32, 3, false>" in text
+    assert "pack_events_kernel" not in text
+    assert "SQ_WAVE_CYCLES 200  (2 dispatches)" in text
+    assert "SQ_INSTS_VALU 400  (2 dispatches)" in text
+
+
 def test_workload_shapes():
     """The benchmark workloads have the sizes their descriptions give."""
     w = workloads.table2_flexconv()
