@@ -82,9 +82,11 @@ inline int32_t geometry_basis_size(const sbc_geometry &g) {
 // over (uy, ux) with the centre removed; -1 for the centre (and for offsets
 // outside the block, which no neighbourhood produces).
 __device__ __forceinline__ int event_index(int32_t ux, int32_t uy) {
-    if (ux < -1 || ux > 1 || uy < -1 || uy > 1) return -1;
-    const int k = (uy + 1) * 3 + (ux + 1);
-    return k == 4 ? -1 : (k < 4 ? k : k - 1);
+    // (without branches: ux + 1 and uy + 1 are in 0..2 exactly when their
+    // unsigned forms are at most 2)
+    const uint32_t bx = (uint32_t)ux + 1u, by = (uint32_t)uy + 1u;
+    const int k = (int)(by * 3u + bx);
+    return (bx <= 2u && by <= 2u && k != 4) ? k - (k > 4 ? 1 : 0) : -1;
 }
 
 // exp(-dt / tau) for an integer time gap dt >= 0.  The gap is converted to

@@ -1355,6 +1355,262 @@ __global__ void __launch_bounds__(kRegWaves * 64)
     }
 }
 
+// ---------------------------------------------------------------- one-hot event forward
+// The fixed-decay event basis gives an edge a single nonzero value, at its
+// offset index k (none for the centre pixel), so of the M x CG products per
+// edge and lane of the register forward, CG carry the sum.  A register cannot
+// be chosen by a per-lane index, an LDS address can: here each lane keeps the
+// G values it owns (one tile row, CG channels, all 8 offsets) in a
+// lane-private LDS slot, [offset][16-byte piece][lane], and an edge adds its
+// CG products into the slot of its offset, a read, CG FMAs and a write.
+// Lanes touch only their own slot, so no barrier is needed; LDS accesses of
+// one wave complete in order, so consecutive edges of one offset chain
+// correctly.  Per step the 4 lanes of a row take 4 edges in pattern order, one
+// each (index, coordinates, offset and decay), share offset and weight by
+// cross-lane reads, and each adds its channels of all 4 neighbour rows.  The
+// next step's rows and coordinates are loaded while this step is summed, and
+// the indices two steps ahead, across tiles.  Then Y rows = G W on the matrix
+// cores, W in LDS as in the register forward.  The per-(row, offset, channel)
+// sums take their edges in pattern order, as in the register forward.
+constexpr int kOhWaves = 8;
+
+template <int CI, int CO>
+constexpr bool onehot_forward_fits() {
+    return CI == 32 && CO % 16 == 0 &&
+           8 * CI * CO * 4 + kOhWaves * 8 * CI * 16 * 4 <= 163840;
+}
+
+template <int CI, int CO>
+__global__ void __launch_bounds__(kOhWaves * 64, 1)
+    fwd_onehot_kernel(int32_t n_out, int32_t n_tiles, const int32_t *__restrict__ row_ptr,
+                      const int32_t *__restrict__ col_idx, KGeo g, const float *__restrict__ F,
+                      const float *__restrict__ W, float *__restrict__ Y,
+                      const int32_t *__restrict__ order) {
+    constexpr int M = 8;
+    constexpr int K = M * CI;
+    constexpr int CG = CI / 4;    // channels per lane
+    constexpr int NP = CG / 4;    // 16-byte pieces per lane and offset
+    constexpr int NCB = CO / 16;  // 16-column blocks of Y
+    constexpr int NT = kOhWaves * 64;
+    static_assert(onehot_forward_fits<CI, CO>(), "shape");
+    __shared__ __attribute__((aligned(16))) float Wf[K * CO];  // [K][16][NCB]
+    __shared__ float4 Gs[kOhWaves][M * NP][64];
+
+    for (int q = threadIdx.x; q < K * CO; q += NT) {
+        const int k = q / CO, n = q % CO;
+        Wf[(k * 16 + (n & 15)) * NCB + (n >> 4)] = W[q];
+    }
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    const int rl = lane & 15;  // row within the tile
+    const int gq = lane >> 4;  // channel group
+    float4 *gl = &Gs[w][0][lane];
+#pragma unroll
+    for (int p = 0; p < M * NP; ++p) gl[64 * p] = make_float4(0.f, 0.f, 0.f, 0.f);
+    __syncthreads();
+
+    const float inv_tau = g.inv_tau;
+    const int32_t nnz = g.nnz;
+    const int32_t G = gridDim.x, X = G < 8 ? G : 8;
+    const int32_t x = blockIdx.x % X;
+    const int32_t gx = G / X + (x < G % X ? 1 : 0);
+    const int32_t waves_x = gx * kOhWaves;
+    const int32_t lw = (blockIdx.x / X) * kOhWaves + w;
+    const int32_t quant = G % X == 0 ? waves_x : 0;
+    const int32_t t_begin = xcd_range_begin(x, X, n_tiles, 16, row_ptr, n_out, nnz, quant);
+    const int32_t t_end = xcd_range_begin(x + 1, X, n_tiles, 16, row_ptr, n_out, nnz, quant);
+
+    // Loads take 32-bit byte offsets from the arrays' bases: the host takes
+    // this kernel while F, the packed events and the pattern are under 4 GiB
+    // (so rows and tiles are far below 2^31), and only with nnz >= 1.  Index
+    // loads read positions clamped into [0, nnz) and use the value only
+    // inside the row; past its end an edge weighs 0 and reads row 0.
+    const char *Fb = reinterpret_cast<const char *>(F);
+    const char *Eb = reinterpret_cast<const char *>(g.ev);
+    const char *Ib = reinterpret_cast<const char *>(col_idx);
+    const uint32_t fo = (uint32_t)(gq * CG * 4);  // the lane's channels
+    auto idx_raw = [&](int32_t e) {
+        const uint32_t c = (uint32_t)(e < nnz ? e : nnz - 1);
+        return *reinterpret_cast<const int32_t *>(Ib + (c << 2));
+    };
+    auto ev_at = [&](int32_t r) {
+        return *reinterpret_cast<const int4 *>(Eb + ((uint32_t)r << 4));
+    };
+    auto load_step = [&](int32_t j, int4 &ev, float4 (&f)[4][NP]) {
+        ev = ev_at(j);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint32_t ju = (uint32_t)__shfl(j, rl + 16 * u, 64);
+#pragma unroll
+            for (int p = 0; p < NP; ++p)
+                f[u][p] = *reinterpret_cast<const float4 *>(Fb + (ju * (uint32_t)(CI * 4) + fo +
+                                                                  16 * p));
+        }
+    };
+    // a tile's row of this lane: loaded at a clamped position, replaced by
+    // n_out past the wave's tiles or the rows
+    auto order_raw = [&](int32_t t) {
+        const int32_t q = t * 16 + rl;
+        return order[q < n_out ? q : n_out - 1];
+    };
+    auto row_of = [&](int32_t t, int32_t raw) {
+        return t < t_end && t * 16 + rl < n_out ? raw : n_out;
+    };
+    auto bounds_raw = [&](int32_t r, int32_t &b0, int32_t &b1) {
+        const int32_t q = r < n_out ? r : n_out - 1;
+        b0 = row_ptr[q];
+        b1 = row_ptr[q + 1];
+    };
+    auto clamp_bounds = [&](int32_t r, int32_t b0, int32_t b1, int32_t &e0, int32_t &e1) {
+        b0 = b0 < 0 ? 0 : (b0 < nnz ? b0 : nnz);
+        b1 = b1 < b0 ? b0 : (b1 < nnz ? b1 : nnz);
+        e0 = r < n_out ? b0 : 0;
+        e1 = r < n_out ? b1 : 0;
+    };
+    auto wave_steps = [&](int32_t e0, int32_t e1) {  // steps of 4 edges of the longest row
+        int32_t len = e1 - e0;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int32_t o = __shfl_xor(len, d, 64);
+            len = o > len ? o : len;
+        }
+        return __builtin_amdgcn_readfirstlane((len + 3) >> 2);
+    };
+
+    int32_t tile = t_begin + lw;
+    if (tile >= t_end) return;  // (wave-uniform; no barrier follows)
+    // The tile pipeline: at the start of tile t the bounds of tile t + 1 are
+    // there (loaded at the start of t - 1) and the rows of t + 2; its
+    // coordinates, the bounds of t + 2 and the rows of t + 3 are loaded then.
+    int32_t row = row_of(tile, order_raw(tile));
+    int32_t row_n = row_of(tile + waves_x, order_raw(tile + waves_x));
+    int32_t row_nn_raw = order_raw(tile + 2 * waves_x);
+    int32_t e0, e1, b0n, b1n;
+    {
+        int32_t b0, b1;
+        bounds_raw(row, b0, b1);
+        clamp_bounds(row, b0, b1, e0, e1);
+    }
+    bounds_raw(row_n, b0n, b1n);
+    int4 a = ev_at(row < n_out ? row : 0);
+    int32_t steps = wave_steps(e0, e1);
+    int32_t jx = idx_raw(e0 + gq);
+    int32_t jy = idx_raw(e0 + 4 + gq);
+    int4 eva, evb;
+    float4 fa[4][NP], fb[4][NP];
+    load_step(e0 + gq < e1 ? jx : 0, eva, fa);
+
+    // The edge of this lane in a step: offset and decay (weight 0 past the
+    // row's end and for the centre pixel), shared with the row's lanes, and
+    // the sums of the step's four edges into their slots.
+    auto sum_step = [&](int32_t e, const int4 &ev, const float4 (&f)[4][NP]) {
+        int k = event_index(a.x - ev.x, a.y - ev.y);
+        float d = event_decay(a.z, ev.z, inv_tau);
+        const bool live = e < e1 && k >= 0;
+        k = live ? k : 0;
+        d = live ? d : 0.f;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int ku = __shfl(k, rl + 16 * u, 64);
+            const float du = __shfl(d, rl + 16 * u, 64);
+            float4 *sl = gl + 64 * NP * ku;
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+                float4 acc = sl[64 * p];
+                acc.x = fmaf(du, f[u][p].x, acc.x);
+                acc.y = fmaf(du, f[u][p].y, acc.y);
+                acc.z = fmaf(du, f[u][p].z, acc.z);
+                acc.w = fmaf(du, f[u][p].w, acc.w);
+                sl[64 * p] = acc;
+            }
+        }
+    };
+
+#pragma unroll 1
+    for (;;) {
+        const int32_t tn = tile + waves_x;
+        const int32_t row_nn = row_of(tn + waves_x, row_nn_raw);
+        row_nn_raw = order_raw(tn + 2 * waves_x);
+        int32_t e0n, e1n;
+        clamp_bounds(row_n, b0n, b1n, e0n, e1n);
+        bounds_raw(row_nn, b0n, b1n);
+        const int4 an = ev_at(row_n < n_out ? row_n : 0);
+        // Step s takes edges e0 + 4 s .. + 3 of each row.  Its indices are
+        // loaded at step s - 2 and its rows and coordinates at s - 1, into
+        // two register sets used in turn (a copy between them would wait for
+        // the loads).  The steps of consecutive tiles form one stream: the
+        // last pair of a tile loads the next tile's first steps, which land
+        // while this tile's products run.  Every pair issues the same loads
+        // (its second step is summed only if the tile has it), so the
+        // compiler's waits stay those of one step ahead.
+        int32_t e = e0 + gq;
+        int32_t s = 0;
+        do {
+            const bool last = s + 2 >= steps;
+            jx = idx_raw(last ? e0n + gq : e + 8);
+            load_step(e + 4 < e1 ? jy : 0, evb, fb);
+            __builtin_amdgcn_sched_barrier(0);  // the loads go out before the sums wait
+            sum_step(e, eva, fa);
+            e += 4;
+            jy = idx_raw(last ? e0n + 4 + gq : e + 8);
+            load_step((last ? e0n + gq < e1n : e + 4 < e1) ? jx : 0, eva, fa);
+            __builtin_amdgcn_sched_barrier(0);
+            if (s + 1 < steps) sum_step(e, evb, fb);
+            e += 4;
+            s += 2;
+        } while (s < steps);
+
+        // ---- Y rows of the tile = G W on the matrix cores; the slot is
+        // cleared for the next tile as it is read
+        floatx4 ay[NCB];
+#pragma unroll
+        for (int nb = 0; nb < NCB; ++nb) ay[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+            float av[CG];
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+                const float4 v4 = gl[64 * (NP * m + p)];
+                av[4 * p] = v4.x;
+                av[4 * p + 1] = v4.y;
+                av[4 * p + 2] = v4.z;
+                av[4 * p + 3] = v4.w;
+                gl[64 * (NP * m + p)] = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int t = 0; t < CG; ++t) {
+                const int kB = m * CI + gq * CG + t;
+                float b[NCB];
+#pragma unroll
+                for (int nb = 0; nb < NCB; ++nb) b[nb] = Wf[(kB * 16 + rl) * NCB + nb];
+#pragma unroll
+                for (int nb = 0; nb < NCB; ++nb)
+                    ay[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[t], b[nb], ay[nb], 0, 0, 0);
+                if ((t & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        int32_t yrow[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) yrow[r] = __shfl(row, 4 * gq + r, 64);
+#pragma unroll
+        for (int nb = 0; nb < NCB; ++nb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int32_t yr = yrow[r];
+                if (yr < n_out) Y[(int64_t)yr * CO + 16 * nb + rl] = ay[nb][r];
+            }
+
+        tile = tn;
+        if (tile >= t_end) break;
+        row = row_n;
+        row_n = row_nn;
+        a = an;
+        e0 = e0n;
+        e1 = e1n;
+        steps = wave_steps(e0, e1);
+    }
+}
+
 // ================================================================ backward, wave-specialised
 // Persistent blocks over tiles of TR input rows, with the waves in two roles:
 // NG gather waves build tile s+1 (D rows through the transposed pattern, and
@@ -2025,7 +2281,22 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
     KGeo gr;
     // layout: [W copy][packed events][row order][M = 10: basis values]
     SBC_TRY(make_kgeo(csr, v, g, align_up((size_t)M * CI * CO * 4), ws, stream, &gr));
-    if (RegFn rf = find_reg(Shape{M, CI, CO, bf}, basis_mode_of(v, g))) {
+    RegFn rf = find_reg(Shape{M, CI, CO, bf}, basis_mode_of(v, g));
+    // the fixed-decay event basis on rows of 32 float32 channels: the one-hot
+    // forward, whose loads take 32-bit byte offsets (F rows, packed events and
+    // the pattern's indices under 4 GiB; else, or with SBC_EVENT8_WIDE_PATH=1,
+    // the register forward)
+    bool onehot = basis_mode_of(v, g) == SBC_BASIS_EVENT8 + 1 && M == 8 && CI == 32 &&
+                  CO == 32 && !bf;
+    if (onehot) {
+        const int64_t n_ev = csr->n_cols > csr->n_rows ? csr->n_cols : csr->n_rows;
+        const int64_t lim = (int64_t)1 << 32;
+        const char *force = std::getenv("SBC_EVENT8_WIDE_PATH");
+        if ((int64_t)csr->n_cols * CI * 4 >= lim || n_ev * 16 >= lim ||
+            csr->nnz_bound * 4 >= lim || csr->nnz_bound < 1 || (force && force[0] == '1'))
+            onehot = false;
+    }
+    if (rf || onehot) {
         const int32_t n_tiles = (csr->n_rows + 15) / 16;
         const int32_t np = csr->n_cols > csr->n_rows ? csr->n_cols : csr->n_rows;
         int32_t *order = reinterpret_cast<int32_t *>(
@@ -2036,6 +2307,19 @@ sbc_status fused_forward(const sbc_csr *csr, const float *v, const sbc_geometry 
                            dim3(kOrderThreads), 0, stream, csr->n_rows, csr->row_ptr, gr.nnz,
                            order);
         SBC_LAUNCH_CHECK();
+        if (onehot) {
+            // one block per CU (its LDS holds W and the eight waves' G slots)
+            int blocks = (n_tiles + kOhWaves - 1) / kOhWaves;
+            if (blocks > device_cus()) blocks = device_cus();
+            trace_before("fwd_fused", stream);
+            hipLaunchKernelGGL((fwd_onehot_kernel<32, 32>), dim3(blocks), dim3(kOhWaves * 64), 0,
+                               stream, csr->n_rows, n_tiles, csr->row_ptr, csr->col_idx, gr,
+                               static_cast<const float *>(F), static_cast<const float *>(W), Y,
+                               order);
+            SBC_LAUNCH_CHECK();
+            trace_after("fwd_fused", stream);
+            return SBC_OK;
+        }
         int per_cu = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(rf),
                                                          kRegWaves * 64, 0) != hipSuccess ||

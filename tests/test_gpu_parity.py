@@ -565,6 +565,27 @@ def test_event_backward_wide_offset_path(name, monkeypatch):
     assert G.norm_error(dW.cpu().numpy(), dW_ref) < tol(w)
 
 
+@pytest.mark.parametrize("name", ["fz_ev32", "fz_tiny_ev", "events_300k"])
+def test_event_forward_one_hot_path(name, monkeypatch):
+    """The fixed-decay event forward on rows of 32 float32 channels keeps each
+    lane's G values for all offsets in LDS and adds an edge into its offset's
+    only; with SBC_EVENT8_WIDE_PATH=1 (or arrays past 4 GiB) it takes the
+    register forward, which multiplies all offsets.  Both take the edges of a
+    (row, offset, channel) sum in pattern order and contract G W in the same
+    order, so they agree exactly, and with the oracle."""
+    print(f"[forward one-hot path] {name}", flush=True)
+    w, rp, ci, v = case(name)
+    assert w["C_in"] == 32 and w["C_out"] == 32 and w["dtype"] == "f32"
+    t, csr = gpu_case(name)
+    Y = G.sbc.conv_forward(csr, t["F"], t["W"], geometry=G.geometry(w, t), order="spmm_first")
+    monkeypatch.setenv("SBC_EVENT8_WIDE_PATH", "1")
+    Y_reg = G.sbc.conv_forward(csr, t["F"], t["W"], geometry=G.geometry(w, t), order="spmm_first")
+    monkeypatch.delenv("SBC_EVENT8_WIDE_PATH")
+    Y, Y_reg = Y.cpu().numpy(), Y_reg.cpu().numpy()
+    assert np.array_equal(Y, Y_reg)
+    assert G.row_error(Y, oracle_forward(name)) < tol(w)
+
+
 def test_transpose_by_radix_sort():
     """Patterns of 2^21 edges or more are transposed by the radix sort; trailing
     columns without edges must still get their (empty) ranges."""
