@@ -1360,14 +1360,14 @@ __global__ void __launch_bounds__(kRegWaves * 64)
 // offset index k (none for the centre pixel), so of the M x CG products per
 // edge and lane of the register forward, CG carry the sum.  A register cannot
 // be chosen by a per-lane index, an LDS address can: here each lane keeps the
-// G values it owns (one tile row, CG channels, all 8 offsets) in a
-// lane-private LDS slot, [offset][16-byte piece][lane], and an edge adds its
-// CG products into the slot of its offset, a read, CG FMAs and a write.
-// Lanes touch only their own slot, so no barrier is needed; LDS accesses of
-// one wave complete in order, so consecutive edges of one offset chain
-// correctly.  Per step the 4 lanes of a row take 4 edges in pattern order, one
-// each (index, coordinates, offset and decay), share offset and weight by
-// cross-lane reads, and each adds its channels of all 4 neighbour rows.  The
+// G values it owns (4 channels of two tile rows, all 8 offsets) in a
+// lane-private LDS slot, and an edge adds its 4 products per row into the
+// slot of its offset, a read, 4 FMAs and a write.  Lanes write only their
+// own slot, so no barrier is needed; LDS accesses of one wave complete in
+// order, so consecutive edges of one offset chain correctly.  Per step the 4
+// lanes of a row take 4 edges in pattern order, one each (index,
+// coordinates, offset and decay), and share index, offset and weight by
+// cross-lane reads; each lane adds its piece of the neighbour rows.  The
 // next step's rows and coordinates are loaded while this step is summed, and
 // the indices two steps ahead, across tiles.  Then Y rows = G W on the matrix
 // cores, W in LDS as in the register forward.  The per-(row, offset, channel)
@@ -1388,13 +1388,13 @@ __global__ void __launch_bounds__(kOhWaves * 64, 1)
                       const int32_t *__restrict__ order) {
     constexpr int M = 8;
     constexpr int K = M * CI;
-    constexpr int CG = CI / 4;    // channels per lane
-    constexpr int NP = CG / 4;    // 16-byte pieces per lane and offset
+    constexpr int CG = CI / 4;    // channels of a tile row per lane in the products
     constexpr int NCB = CO / 16;  // 16-column blocks of Y
     constexpr int NT = kOhWaves * 64;
     static_assert(onehot_forward_fits<CI, CO>(), "shape");
     __shared__ __attribute__((aligned(16))) float Wf[K * CO];  // [K][16][NCB]
-    __shared__ float4 Gs[kOhWaves][M * NP][64];
+    // G of a wave: [offset k][half h][position], 16 bytes each (below)
+    __shared__ float4 Gs[kOhWaves][2 * M][64];
 
     for (int q = threadIdx.x; q < K * CO; q += NT) {
         const int k = q / CO, n = q % CO;
@@ -1402,11 +1402,22 @@ __global__ void __launch_bounds__(kOhWaves * 64, 1)
     }
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
-    const int rl = lane & 15;  // row within the tile
-    const int gq = lane >> 4;  // channel group
-    float4 *gl = &Gs[w][0][lane];
+    // Two roles per lane.  As a basis lane it takes edge gq of each step of
+    // tile row rl: index, coordinates, offset and decay.  As a sum lane it
+    // loads piece pc (16 bytes, 4 channels) of the neighbour rows of tile
+    // rows r8 and r8 + 8, so one load instruction takes 8 whole rows, and
+    // keeps the G values of those two rows and 4 channels for all offsets.
+    // The 16 bytes of sum lane L sit at position L ^ (L / 8 mod 8), which
+    // keeps both its own accesses and the products' reads (lanes 8 apart)
+    // on distinct banks.
+    const int rl = lane & 15;  // basis lane: row within the tile
+    const int gq = lane >> 4;  //             edge of the step
+    const int r8 = lane >> 3;  // sum lane: tile rows r8, r8 + 8
+    const int pc = lane & 7;   //           piece of the row
+    auto pos = [](int L) { return L ^ ((L >> 3) & 7); };
+    float4 *gl = &Gs[w][0][pos(lane)];
 #pragma unroll
-    for (int p = 0; p < M * NP; ++p) gl[64 * p] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int p = 0; p < 2 * M; ++p) gl[64 * p] = make_float4(0.f, 0.f, 0.f, 0.f);
     __syncthreads();
 
     const float inv_tau = g.inv_tau;
@@ -1428,7 +1439,7 @@ __global__ void __launch_bounds__(kOhWaves * 64, 1)
     const char *Fb = reinterpret_cast<const char *>(F);
     const char *Eb = reinterpret_cast<const char *>(g.ev);
     const char *Ib = reinterpret_cast<const char *>(col_idx);
-    const uint32_t fo = (uint32_t)(gq * CG * 4);  // the lane's channels
+    const uint32_t fo = (uint32_t)(pc * 16);  // the sum lane's piece
     auto idx_raw = [&](int32_t e) {
         const uint32_t c = (uint32_t)(e < nnz ? e : nnz - 1);
         return *reinterpret_cast<const int32_t *>(Ib + (c << 2));
@@ -1436,16 +1447,17 @@ __global__ void __launch_bounds__(kOhWaves * 64, 1)
     auto ev_at = [&](int32_t r) {
         return *reinterpret_cast<const int4 *>(Eb + ((uint32_t)r << 4));
     };
-    auto load_step = [&](int32_t j, int4 &ev, float4 (&f)[4][NP]) {
+    // j: the basis lane's neighbour; f[u][h]: the sum lane's piece of the
+    // neighbour of edge u of tile row r8 + 8 h
+    auto load_step = [&](int32_t j, int4 &ev, float4 (&f)[4][2]) {
         ev = ev_at(j);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const uint32_t ju = (uint32_t)__shfl(j, rl + 16 * u, 64);
+        for (int u = 0; u < 4; ++u)
 #pragma unroll
-            for (int p = 0; p < NP; ++p)
-                f[u][p] = *reinterpret_cast<const float4 *>(Fb + (ju * (uint32_t)(CI * 4) + fo +
-                                                                  16 * p));
-        }
+            for (int h = 0; h < 2; ++h) {
+                const uint32_t ju = (uint32_t)__shfl(j, r8 + 8 * h + 16 * u, 64);
+                f[u][h] = *reinterpret_cast<const float4 *>(Fb + (ju * (uint32_t)(CI * 4) + fo));
+            }
     };
     // a tile's row of this lane: loaded at a clamped position, replaced by
     // n_out past the wave's tiles or the rows
@@ -1497,33 +1509,32 @@ __global__ void __launch_bounds__(kOhWaves * 64, 1)
     int32_t jx = idx_raw(e0 + gq);
     int32_t jy = idx_raw(e0 + 4 + gq);
     int4 eva, evb;
-    float4 fa[4][NP], fb[4][NP];
+    float4 fa[4][2], fb[4][2];
     load_step(e0 + gq < e1 ? jx : 0, eva, fa);
 
     // The edge of this lane in a step: offset and decay (weight 0 past the
     // row's end and for the centre pixel), shared with the row's lanes, and
     // the sums of the step's four edges into their slots.
-    auto sum_step = [&](int32_t e, const int4 &ev, const float4 (&f)[4][NP]) {
+    auto sum_step = [&](int32_t e, const int4 &ev, const float4 (&f)[4][2]) {
         int k = event_index(a.x - ev.x, a.y - ev.y);
         float d = event_decay(a.z, ev.z, inv_tau);
         const bool live = e < e1 && k >= 0;
         k = live ? k : 0;
         d = live ? d : 0.f;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int ku = __shfl(k, rl + 16 * u, 64);
-            const float du = __shfl(d, rl + 16 * u, 64);
-            float4 *sl = gl + 64 * NP * ku;
+        for (int u = 0; u < 4; ++u)
 #pragma unroll
-            for (int p = 0; p < NP; ++p) {
-                float4 acc = sl[64 * p];
-                acc.x = fmaf(du, f[u][p].x, acc.x);
-                acc.y = fmaf(du, f[u][p].y, acc.y);
-                acc.z = fmaf(du, f[u][p].z, acc.z);
-                acc.w = fmaf(du, f[u][p].w, acc.w);
-                sl[64 * p] = acc;
+            for (int h = 0; h < 2; ++h) {
+                const int ku = __shfl(k, r8 + 8 * h + 16 * u, 64);
+                const float du = __shfl(d, r8 + 8 * h + 16 * u, 64);
+                float4 *sl = gl + 64 * (2 * ku + h);
+                float4 acc = *sl;
+                acc.x = fmaf(du, f[u][h].x, acc.x);
+                acc.y = fmaf(du, f[u][h].y, acc.y);
+                acc.z = fmaf(du, f[u][h].z, acc.z);
+                acc.w = fmaf(du, f[u][h].w, acc.w);
+                *sl = acc;
             }
-        }
     };
 
 #pragma unroll 1
@@ -1565,18 +1576,24 @@ __global__ void __launch_bounds__(kOhWaves * 64, 1)
         floatx4 ay[NCB];
 #pragma unroll
         for (int nb = 0; nb < NCB; ++nb) ay[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        // lane (rl, gq) takes channels 8 gq .. 8 gq + 7 of tile row rl: pieces
+        // 2 gq, 2 gq + 1 of the sum lanes of that row
+        float4 *gr = &Gs[w][rl >> 3][0];
+        const int pr0 = pos(8 * (rl & 7) + 2 * gq), pr1 = pos(8 * (rl & 7) + 2 * gq + 1);
 #pragma unroll
         for (int m = 0; m < M; ++m) {
             float av[CG];
-#pragma unroll
-            for (int p = 0; p < NP; ++p) {
-                const float4 v4 = gl[64 * (NP * m + p)];
-                av[4 * p] = v4.x;
-                av[4 * p + 1] = v4.y;
-                av[4 * p + 2] = v4.z;
-                av[4 * p + 3] = v4.w;
-                gl[64 * (NP * m + p)] = make_float4(0.f, 0.f, 0.f, 0.f);
-            }
+            const float4 v0 = gr[128 * m + pr0], v1 = gr[128 * m + pr1];
+            av[0] = v0.x;
+            av[1] = v0.y;
+            av[2] = v0.z;
+            av[3] = v0.w;
+            av[4] = v1.x;
+            av[5] = v1.y;
+            av[6] = v1.z;
+            av[7] = v1.w;
+            gr[128 * m + pr0] = make_float4(0.f, 0.f, 0.f, 0.f);
+            gr[128 * m + pr1] = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
             for (int t = 0; t < CG; ++t) {
                 const int kB = m * CI + gq * CG + t;
