@@ -75,7 +75,8 @@ SRC_DIR = os.path.join(ROOT, "paper_2012_01170_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
 # device function -> the name the library's trace hook gives its launch
 TRACE_NAME = {"bwd_ws_kernel": "bwd_fused", "fwd_fused_kernel": "fwd_fused",
-              "fwd_reg_kernel": "fwd_fused", "dw_reduce_kernel": "bwd_dw_reduce",
+              "fwd_reg_kernel": "fwd_fused", "fwd_onehot_kernel": "fwd_fused",
+              "dw_reduce_kernel": "bwd_dw_reduce",
               "sample_kernel<true>": "sample", "sample_kernel<false>": "sample_count",
               "lif_cell_kernel": "lif_cells", "lif_emit_kernel": "lif_emit",
               "stream_gather_kernel": "stream_gather", "stream_update_kernel": "stream_update"}

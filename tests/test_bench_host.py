@@ -26,6 +26,7 @@ def test_more_than_one_gpu_is_refused():
     ("bwd_ws_kernel<8, 64, 64, 2, false, 4, 4, 32, 0>", "bwd_fused"),
     ("bwd_ws_kernel<16, 32, 32, 16, false, 4, 4, 32, 0>", "decay_fused"),
     ("fwd_reg_kernel<8, 32, 32, 3, false>", "fwd_fused"),
+    ("fwd_onehot_kernel<32, 32>", "fwd_fused"),
     ("featureless_kernel<10, 3, true>", "featureless_fwd"),
     ("featureless_kernel<10, 3, false>", "featureless_rowsum"),
     ("sample_kernel<true>", "sample"),
