@@ -771,6 +771,240 @@ __device__ __forceinline__ void gather_rows_onehot(
     p.i1 = i1n;
 }
 
+// One-hot gather of the transposed pattern into the D tile in place, for
+// rows of 32 float32 channels and RPW = 4 or 8 rows per wave: the LPR = 64 /
+// RPW lanes of a row each own CO / LPR channels of it for all offsets and add
+// every edge of the row into those channels at the edge's offset (an LDS
+// read, the FMAs and a write: about two VALU instructions per edge and wave
+// where the bucket walk takes eight).  The lanes of a row load one neighbour
+// row, 128 contiguous bytes, per step.  Edges come in chunks of LPR per row
+// (at least one chunk per tile): lane p takes index, coordinates, offset and
+// decay of edge p of the chunk, broadcast to the row's lanes by DPP.  Rows of
+// a wave have their own lanes, so no two lanes write one address; LDS
+// accesses of one wave complete in order, so consecutive edges of one offset
+// chain correctly.
+//
+// The chunks of the wave's tiles form one stream, across the block barrier:
+// a chunk's neighbour rows are loaded during the chunk before it (step s of
+// chunk c loads the row of step s of chunk c + 1 into the register it has
+// just used), its coordinates at the start of the chunk before, and its
+// indices two chunks ahead; row bounds come three tiles ahead.
+// f(std::integral_constant<int, s>) for s = 0 .. N - 1, unrolled whatever
+// the body's size (register arrays indexed by s stay in registers)
+template <typename F, int... S>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, S...>) {
+    (f(std::integral_constant<int, S>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+template <int LPR>
+struct RmwPipe {
+    int32_t e0a, e1a, e0b, e1b, e0c, e1c;  // bounds of this lane's row in tiles s, s + 1, s + 2
+    int32_t C0, C1, S0;    // chunks of tiles s and s + 1, steps of tile s (wave-uniform)
+    int4 bc, bn;           // coordinates of the row in tiles s and s + 1
+    int32_t i1;            // index of edge p of the next chunk (in flight until used)
+    bool v1;               // whether that edge lies inside its row
+    int4 ev1;              // coordinates of the next chunk's neighbours (in flight)
+    using PT = typename std::conditional<LPR == 16, float2, float4>::type;
+    PT y[LPR];             // the lane's pieces of the current chunk's rows (in flight)
+};
+
+template <int CO, int RPW>
+struct RmwGather {
+    static constexpr int LPR = 64 / RPW;  // lanes per row
+    static constexpr int CH = CO / LPR;   // channels per lane
+    static_assert(CO == 32 && (RPW == 4 || RPW == 8), "rows of 32 float32 channels");
+    using PT = typename RmwPipe<LPR>::PT;
+    using Pipe = RmwPipe<LPR>;
+    const int32_t *ptr, *idx;
+    const int4 *ev;
+    const float *X;
+    int32_t n_rows, nnz;
+    float inv_tau;
+    int r, p;
+
+    __device__ __forceinline__ void bounds_raw(int32_t row_begin, int32_t &b0, int32_t &b1) const {
+        const int32_t row = row_begin + r;
+        const int32_t q = row_begin >= 0 && row < n_rows ? row : 0;
+        b0 = ptr[q];
+        b1 = ptr[q + 1];
+    }
+    __device__ __forceinline__ void clamp(int32_t row_begin, int32_t b0, int32_t b1, int32_t &e0,
+                                          int32_t &e1) const {
+        const bool ok = row_begin >= 0 && row_begin + r < n_rows;
+        b0 = b0 < 0 ? 0 : (b0 < nnz ? b0 : nnz);
+        b1 = b1 < b0 ? b0 : (b1 < nnz ? b1 : nnz);
+        e0 = ok ? b0 : 0;
+        e1 = ok ? b1 : 0;
+    }
+    // steps (the longest row's edges) of a tile, and its chunks (at least 1)
+    __device__ __forceinline__ int32_t steps(int32_t e0, int32_t e1) const {
+        int32_t len = e1 - e0;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int32_t o = __shfl_xor(len, d, 64);
+            len = o > len ? o : len;
+        }
+        return __builtin_amdgcn_readfirstlane(len);
+    }
+    static __device__ __forceinline__ int32_t chunks(int32_t S) {
+        return S > LPR ? (S + LPR - 1) / LPR : 1;
+    }
+    __device__ __forceinline__ int4 coords(int32_t row_begin) const {
+        const int32_t row = row_begin + r;
+        return ev[row_begin >= 0 && row < n_rows ? row : 0];
+    }
+    // (nnz >= 1: the host takes this gather only then; positions are clamped
+    // into [0, nnz) and the value is used only inside the row)
+    __device__ __forceinline__ int32_t idx_raw(int32_t e) const {
+        return idx[e < nnz ? e : nnz - 1];
+    }
+    // value v of lane s of this lane's row (a DPP broadcast within the 16
+    // lanes of a DPP row: a plain VALU move, where a cross-lane read through
+    // LDS took a round trip; with 8 lanes per row, the upper 8 of a DPP row
+    // take lane 8 + s)
+    template <int S>
+    static __device__ __forceinline__ int32_t row_lane(int32_t v) {
+        if constexpr (LPR == 16) {
+            return __builtin_amdgcn_mov_dpp(v, 0x150 + S, 0xf, 0xf, false);
+        } else {
+            const int32_t lo = __builtin_amdgcn_mov_dpp(v, 0x150 + S, 0xf, 0xf, false);
+            const int32_t hi = __builtin_amdgcn_mov_dpp(v, 0x158 + S, 0xf, 0xf, false);
+            return (threadIdx.x & 8) ? hi : lo;
+        }
+    }
+    // (32-bit byte offsets: the host takes this gather while the gathered
+    // rows are under 4 GiB)
+    template <int S>
+    __device__ __forceinline__ void load_row(int32_t i, PT &yv) const {
+        const uint32_t j = (uint32_t)row_lane<S>(i);
+        yv = *reinterpret_cast<const PT *>(reinterpret_cast<const char *>(X) +
+                                           (j * (uint32_t)(CO * 4) + 4 * CH * p));
+    }
+    // the indices of the chunk two ahead of chunk c of tile s
+    __device__ __forceinline__ void issue_idx(Pipe &P, int32_t c) const {
+        int32_t t = c + 2, tt = 0;
+        if (t >= P.C0) {
+            t -= P.C0;
+            tt = 1;
+            if (t >= P.C1) {
+                t -= P.C1;
+                tt = 2;
+            }
+        }
+        // (as differences: a select between two members became a load through
+        // a selected address, which kept the whole pipe in memory)
+        const int32_t e0 = P.e0a + (tt >= 1 ? P.e0b - P.e0a : 0) + (tt >= 2 ? P.e0c - P.e0b : 0);
+        const int32_t e1 = P.e1a + (tt >= 1 ? P.e1b - P.e1a : 0) + (tt >= 2 ? P.e1c - P.e1b : 0);
+        const int32_t e = e0 + LPR * t + p;
+        P.i1 = idx_raw(e);
+        P.v1 = e < e1;
+    }
+};
+
+// Before the first tile (rows rb0 .. rb2 of tiles 0 .. 2): their bounds, the
+// loads of the first chunk and the indices of the second.
+template <class G_>
+__device__ __forceinline__ void rmw_prologue(const G_ &G, int32_t rb0, int32_t rb1, int32_t rb2,
+                                             typename G_::Pipe &P) {
+    int32_t b0, b1;
+    G.bounds_raw(rb0, b0, b1);
+    G.clamp(rb0, b0, b1, P.e0a, P.e1a);
+    G.bounds_raw(rb1, b0, b1);
+    G.clamp(rb1, b0, b1, P.e0b, P.e1b);
+    G.bounds_raw(rb2, b0, b1);
+    G.clamp(rb2, b0, b1, P.e0c, P.e1c);
+    P.S0 = G.steps(P.e0a, P.e1a);
+    P.C0 = G.chunks(P.S0);
+    P.C1 = G.chunks(G.steps(P.e0b, P.e1b));
+    P.bc = G.coords(rb0);
+    P.bn = G.coords(rb1);
+    const int32_t e = P.e0a + G.p;
+    int32_t i0 = G.idx_raw(e);
+    i0 = e < P.e1a ? i0 : 0;
+    {  // the second chunk: chunk 1 of tile 0, or chunk 0 of tile 1
+        const bool nt = P.C0 < 2;
+        const int32_t e0 = P.e0a + (nt ? P.e0b - P.e0a : G_::LPR),
+                      e1 = P.e1a + (nt ? P.e1b - P.e1a : 0);
+        P.i1 = G.idx_raw(e0 + G.p);
+        P.v1 = e0 + G.p < e1;
+    }
+    P.ev1 = G.ev[i0];
+    static_for<G_::LPR>(
+        [&](auto sc) { G.template load_row<decltype(sc)::value>(i0, P.y[sc.value]); });
+}
+
+// Tile s of the stream into the wave's rows of out_tile (row_begin: the
+// wave's first row in tile s; rb2, rb3: in tiles s + 2, s + 3; -1 where there
+// is none).
+template <class G_>
+__device__ __forceinline__ void gather_rows_rmw(const G_ &G, int32_t rb2, int32_t rb3,
+                                                float *out_tile, int SD, int local_row0,
+                                                typename G_::Pipe &P) {
+    constexpr int LPR = G_::LPR, CH = G_::CH, CO = G_::CH * G_::LPR;
+    using PT = typename G_::PT;
+    const int r = G.r, p = G.p;
+    float *drow = out_tile + (local_row0 + r) * SD;
+    // (the row's 8 CO values, 4 LPR floats per 16-byte store of its lanes)
+#pragma unroll
+    for (int q = 0; q < 8 * CO / (4 * LPR); ++q)
+        *reinterpret_cast<float4 *>(drow + 4 * LPR * q + 4 * p) = make_float4(0.f, 0.f, 0.f, 0.f);
+    // the tile pipeline: bounds of tile s + 3, coordinates of the rows of s + 2
+    int32_t b0n, b1n;
+    G.bounds_raw(rb3, b0n, b1n);
+    const int4 bnn = G.coords(rb2);
+    const int4 bc = P.bc;
+#pragma unroll 1
+    for (int32_t c = 0; c < P.C0; ++c) {
+        // this chunk: offset and decay of edge p of the row (its coordinates
+        // were loaded at the start of the chunk before)
+        const int4 a = P.ev1;
+        int k = event_index(a.x - bc.x, a.y - bc.y);
+        float d = event_decay(a.z, bc.z, G.inv_tau);
+        const int32_t e = P.e0a + LPR * c + p;
+        const bool live = e < P.e1a && k >= 0;
+        const int32_t koff = live ? k * CO : 0;
+        d = live ? d : 0.f;
+        // the next chunk: its indices (loaded a chunk ago), its coordinates
+        // now and its rows step by step below; the indices of the one after
+        const int32_t i1 = P.v1 ? P.i1 : 0;
+        P.ev1 = G.ev[i1];
+        G.issue_idx(P, c);
+        const int32_t ns = P.S0 - LPR * c;
+        static_for<LPR>([&](auto sc) {
+            constexpr int s = decltype(sc)::value;
+            if (s < ns) {
+                const int32_t o = G_::template row_lane<s>(koff);
+                const float dd = __int_as_float(G_::template row_lane<s>(__float_as_int(d)));
+                PT *q = reinterpret_cast<PT *>(drow + o + CH * p);
+                PT acc = *q;
+                acc.x = fmaf(dd, P.y[s].x, acc.x);
+                acc.y = fmaf(dd, P.y[s].y, acc.y);
+                if constexpr (CH == 4) {
+                    acc.z = fmaf(dd, P.y[s].z, acc.z);
+                    acc.w = fmaf(dd, P.y[s].w, acc.w);
+                }
+                *q = acc;
+            }
+            G.template load_row<s>(i1, P.y[s]);
+        });
+    }
+    // the next tile
+    P.e0a = P.e0b;
+    P.e1a = P.e1b;
+    P.e0b = P.e0c;
+    P.e1b = P.e1c;
+    G.clamp(rb3, b0n, b1n, P.e0c, P.e1c);
+    P.C0 = P.C1;
+    P.S0 = G.steps(P.e0a, P.e1a);
+    P.C1 = G.chunks(G.steps(P.e0b, P.e1b));
+    P.bc = P.bn;
+    P.bn = bnn;
+}
+
 // acc[u][t] += A_tile[16 rb_u .., :] x B[:, 16 cb_t ..] for the 16x16 blocks of
 // one wave (rb_u = wr + NRG u, cb_t = wc + NCBW t).  A sits in LDS (row stride
 // S elements), B in global memory as B^T [NCOL, K].  The B fragments of
@@ -1649,6 +1883,11 @@ struct WsCfg {
     int ng, nm, tr, wloc;
 };
 
+// Tile rows of the fixed-decay event backward on rows of 32 float32
+// channels: its in-place gather keeps no stage in LDS, which leaves room for
+// 64-row tiles (half the block barriers of 32-row ones)
+constexpr int kEventRmwTR = 64;
+
 template <int M, int CI, int CO, bool kBf>
 constexpr WsCfg ws_cfg() {
     if (!kBf && CI <= 32 && CO <= 32)  // wider D rows (M*CO > 256) leave LDS for 4 gather waves
@@ -1697,12 +1936,21 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     // then spans about half of a wave's rows, and the walk ran slower.)
     constexpr int CK = 64;
     constexpr int RBY = CO * (int)sizeof(DT);  // bytes per gathered row
-    constexpr bool kOneHot =
+    constexpr bool kOneHotShape =
         kBasis == SBC_BASIS_EVENT8 + 1 && M == 8 && RPW * M <= 64 && 64 % (RPW * M) == 0 &&
-        RBY % 16 == 0 && 64 % (RBY / 16) == 0 && CK % (64 / (RBY / 16)) == 0 &&
-        2 * TR * (SD + SF) * sizeof(DT) + kWsGather * sizeof(OneHotStage<RBY, CK>) <= 163840;
-    using Stage =
-        typename std::conditional<kOneHot, OneHotStage<RBY, CK>, EdgeStage<M>>::type;
+        RBY % 16 == 0 && 64 % (RBY / 16) == 0 && CK % (64 / (RBY / 16)) == 0;
+    // rows of 32 float32 channels, 4 or 8 per gather wave: the in-place
+    // one-hot gather (no stage)
+    constexpr bool kRmw = kOneHotShape && !kBf && CO == 32 && (RPW == 4 || RPW == 8) &&
+                          2 * TR * (SD + SF) * sizeof(DT) <= 163840;
+    constexpr bool kOneHot =
+        kOneHotShape &&
+        (kRmw ||
+         2 * TR * (SD + SF) * sizeof(DT) + kWsGather * sizeof(OneHotStage<RBY, CK>) <= 163840);
+    struct NoStage {};
+    using Stage = typename std::conditional<
+        kRmw, NoStage,
+        typename std::conditional<kOneHot, OneHotStage<RBY, CK>, EdgeStage<M>>::type>::type;
     __shared__ __attribute__((aligned(16))) Stage stage[kWsGather];
 
     const int lane = threadIdx.x & 63;
@@ -1731,11 +1979,18 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
         0, false};
     constexpr int NR = kOneHot ? CK / (64 / (RBY / 16)) : 1;  // row pieces per lane and chunk
     OneHotPipe<NR> pipe;
+    using RG = RmwGather<32, kRmw ? RPW : 4>;
+    const RG rmw{col_ptr, row_idx, g.ev, static_cast<const float *>(dY), n_in, g.nnz, inv_tau,
+                 lane / RG::LPR, lane % RG::LPR};
+    typename RG::Pipe rpipe;
     auto wave_rows = [&](int32_t s) {
         return s < n_my ? (t_first + s * gx) * TR + w * RPW : -1;
     };
     auto load_tile = [&](int32_t s, int buf) {
-        if constexpr (kOneHot) {
+        if constexpr (kRmw) {
+            gather_rows_rmw(rmw, wave_rows(s + 2), wave_rows(s + 3),
+                            reinterpret_cast<float *>(Ds[buf]), SD, w * RPW, rpipe);
+        } else if constexpr (kOneHot) {
             const OneHotTiles tl{wave_rows(s), wave_rows(s + 1), wave_rows(s + 2),
                                  wave_rows(s + 3)};
             gather_rows_onehot<CO, RPW, true, kBf, NR>(tl, n_in, col_ptr, row_idx, g, dY,
@@ -1752,8 +2007,10 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     // are not live in the gather code); each role passes the block barrier
     // exactly n_my + 1 times, in the same steps.
     if (gatherer) {
-        if constexpr (kOneHot) onehot_stage_init(stage[w]);
-        if constexpr (kOneHot)
+        if constexpr (kRmw)
+            if (n_my > 0) rmw_prologue(rmw, wave_rows(0), wave_rows(1), wave_rows(2), rpipe);
+        if constexpr (kOneHot && !kRmw) onehot_stage_init(stage[w]);
+        if constexpr (kOneHot && !kRmw)
             if (n_my > 0)
                 onehot_prologue<CO, RPW, true, kBf, NR>(
                     OneHotTiles{wave_rows(0), wave_rows(1), wave_rows(2), -1}, n_in, col_ptr,
@@ -2116,7 +2373,11 @@ BwdFn bwd_for(int basis_mode) {
             if constexpr (M == 8) return bwd_ws_kernel<M, CI, CO, SBC_BASIS_MONO8 + 1, kBf>;
             return nullptr;
         case SBC_BASIS_EVENT8 + 1:
-            if constexpr (M == 8) return bwd_ws_kernel<M, CI, CO, SBC_BASIS_EVENT8 + 1, kBf>;
+            if constexpr (M == 8 && CI == 32 && CO == 32 && !kBf)
+                return bwd_ws_kernel<M, CI, CO, SBC_BASIS_EVENT8 + 1, kBf, 8, 4, kEventRmwTR,
+                                     kWRegs>;
+            else if constexpr (M == 8)
+                return bwd_ws_kernel<M, CI, CO, SBC_BASIS_EVENT8 + 1, kBf>;
             return nullptr;
         case SBC_BASIS_EVENT_DECAYS + 1:
             if constexpr (M >= 16 && M % 8 == 0)
@@ -2379,7 +2640,7 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
         const char *force = std::getenv("SBC_EVENT8_WIDE_PATH");
         if ((int64_t)csr->n_rows * CO * (bf ? 2 : 4) >= lim || n_ev * 16 >= lim ||
             csr->nnz_bound * 4 >= lim || ((int64_t)csr->n_cols + 1) * 4 >= lim ||
-            (force && force[0] == '1'))
+            csr->nnz_bound < 1 || (force && force[0] == '1'))
             mode = kEvent8WideMode;
     }
     BwdFn fn = find_bwd(Shape{M, CI, CO, bf}, mode);
@@ -2389,7 +2650,9 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
     float *part = reinterpret_cast<float *>(base + align_up((size_t)M * CI * CO * 4));
     // the kernel reads W [M, CI, CO] in place as Wt [CI, M*CO]
     const WsCfg cfg = ws_cfg_rt(M, CI, CO, bf);
-    const int TR = cfg.tr;
+    const int TR = mode == SBC_BASIS_EVENT8 + 1 && M == 8 && CI == 32 && CO == 32 && !bf
+                       ? kEventRmwTR
+                       : cfg.tr;
     const int32_t n_tiles = (n_in + TR - 1) / TR;
     const int nw = cfg.ng + cfg.nm;
     int blocks = device_cus();
