@@ -92,6 +92,10 @@ constexpr int kDecayDerivMode = 16;
 // generic gather (64-bit addressing) instead of the one-hot gather, whose
 // loads take 32-bit byte offsets from their arrays' bases.
 constexpr int kEvent8WideMode = 17;
+// The same for the learned-decay basis and its derivatives (M / 8 values per
+// edge), whose in-place gather takes 32-bit byte offsets too.
+constexpr int kDecaysWideMode = 18;
+constexpr int kDecayDerivWideMode = 19;
 
 __global__ void pack_events_kernel(const int32_t *__restrict__ px, const int32_t *__restrict__ py,
                                    const int32_t *__restrict__ t, int32_t n,
@@ -812,16 +816,22 @@ struct RmwPipe {
     PT y[LPR];             // the lane's pieces of the current chunk's rows (in flight)
 };
 
-template <int CO, int RPW>
+// The edge's basis: kValues 0, the fixed decay exp(-dt / tau) (one value per
+// edge); 1, the learned decays exp(-lambda_{k,q} dt) (MV values per edge, at
+// slots k MV + q); 2, their derivatives -dt exp(-lambda_{k,q} dt).
+template <int CO, int RPW, int MV = 1, int kValues = 0>
 struct RmwGather {
     static constexpr int LPR = 64 / RPW;  // lanes per row
     static constexpr int CH = CO / LPR;   // channels per lane
     static_assert(CO == 32 && (RPW == 4 || RPW == 8), "rows of 32 float32 channels");
+    static_assert(kValues == 0 ? MV == 1 : MV >= 1, "values per edge");
+    static constexpr int kMV = MV, kVal = kValues;
     using PT = typename RmwPipe<LPR>::PT;
     using Pipe = RmwPipe<LPR>;
     const int32_t *ptr, *idx;
     const int4 *ev;
     const float *X;
+    const float *decays;  // [8, MV] (kValues 1 and 2)
     int32_t n_rows, nnz;
     float inv_tau;
     int r, p;
@@ -944,13 +954,13 @@ template <class G_>
 __device__ __forceinline__ void gather_rows_rmw(const G_ &G, int32_t rb2, int32_t rb3,
                                                 float *out_tile, int SD, int local_row0,
                                                 typename G_::Pipe &P) {
-    constexpr int LPR = G_::LPR, CH = G_::CH, CO = G_::CH * G_::LPR;
+    constexpr int LPR = G_::LPR, CH = G_::CH, CO = G_::CH * G_::LPR, MV = G_::kMV;
     using PT = typename G_::PT;
     const int r = G.r, p = G.p;
     float *drow = out_tile + (local_row0 + r) * SD;
-    // (the row's 8 CO values, 4 LPR floats per 16-byte store of its lanes)
+    // (the row's 8 MV CO values, 4 LPR floats per 16-byte store of its lanes)
 #pragma unroll
-    for (int q = 0; q < 8 * CO / (4 * LPR); ++q)
+    for (int q = 0; q < 8 * MV * CO / (4 * LPR); ++q)
         *reinterpret_cast<float4 *>(drow + 4 * LPR * q + 4 * p) = make_float4(0.f, 0.f, 0.f, 0.f);
     // the tile pipeline: bounds of tile s + 3, coordinates of the rows of s + 2
     int32_t b0n, b1n;
@@ -959,15 +969,28 @@ __device__ __forceinline__ void gather_rows_rmw(const G_ &G, int32_t rb2, int32_
     const int4 bc = P.bc;
 #pragma unroll 1
     for (int32_t c = 0; c < P.C0; ++c) {
-        // this chunk: offset and decay of edge p of the row (its coordinates
-        // were loaded at the start of the chunk before)
+        // this chunk: offset and basis values of edge p of the row (its
+        // coordinates were loaded at the start of the chunk before), in the
+        // expressions of the basis values kernel, so the values agree bitwise
         const int4 a = P.ev1;
-        int k = event_index(a.x - bc.x, a.y - bc.y);
-        float d = event_decay(a.z, bc.z, G.inv_tau);
+        const int k = event_index(a.x - bc.x, a.y - bc.y);
+        float d[MV];
+        if constexpr (G_::kVal == 0) {
+            d[0] = event_decay(a.z, bc.z, G.inv_tau);
+        } else {
+            const float dt = (float)((int64_t)a.z - (int64_t)bc.z);
+            const int kk = k >= 0 ? k : 0;
+#pragma unroll
+            for (int q = 0; q < MV; ++q) {
+                d[q] = expf(-G.decays[kk * MV + q] * dt);
+                if constexpr (G_::kVal == 2) d[q] = -dt * d[q];
+            }
+        }
         const int32_t e = P.e0a + LPR * c + p;
         const bool live = e < P.e1a && k >= 0;
-        const int32_t koff = live ? k * CO : 0;
-        d = live ? d : 0.f;
+        const int32_t koff = live ? k * MV * CO : 0;
+#pragma unroll
+        for (int q = 0; q < MV; ++q) d[q] = live ? d[q] : 0.f;
         // the next chunk: its indices (loaded a chunk ago), its coordinates
         // now and its rows step by step below; the indices of the one after
         const int32_t i1 = P.v1 ? P.i1 : 0;
@@ -978,16 +1001,20 @@ __device__ __forceinline__ void gather_rows_rmw(const G_ &G, int32_t rb2, int32_
             constexpr int s = decltype(sc)::value;
             if (s < ns) {
                 const int32_t o = G_::template row_lane<s>(koff);
-                const float dd = __int_as_float(G_::template row_lane<s>(__float_as_int(d)));
-                PT *q = reinterpret_cast<PT *>(drow + o + CH * p);
-                PT acc = *q;
-                acc.x = fmaf(dd, P.y[s].x, acc.x);
-                acc.y = fmaf(dd, P.y[s].y, acc.y);
-                if constexpr (CH == 4) {
-                    acc.z = fmaf(dd, P.y[s].z, acc.z);
-                    acc.w = fmaf(dd, P.y[s].w, acc.w);
+#pragma unroll
+                for (int v = 0; v < MV; ++v) {
+                    const float dd =
+                        __int_as_float(G_::template row_lane<s>(__float_as_int(d[v])));
+                    PT *q = reinterpret_cast<PT *>(drow + o + v * CO + CH * p);
+                    PT acc = *q;
+                    acc.x = fmaf(dd, P.y[s].x, acc.x);
+                    acc.y = fmaf(dd, P.y[s].y, acc.y);
+                    if constexpr (CH == 4) {
+                        acc.z = fmaf(dd, P.y[s].z, acc.z);
+                        acc.w = fmaf(dd, P.y[s].w, acc.w);
+                    }
+                    *q = acc;
                 }
-                *q = acc;
             }
             G.template load_row<s>(i1, P.y[s]);
         });
@@ -1900,7 +1927,7 @@ template <int M, int CI, int CO, int kBasis, bool kBf,
           int kWsGather = ws_cfg<M, CI, CO, kBf>().ng,
           int kWsMma = ws_cfg<M, CI, CO, kBf>().nm,
           int kTR = ws_cfg<M, CI, CO, kBf>().tr,
-          int kWLoc = ws_cfg<M, CI, CO, kBf>().wloc>
+          int kWLoc = ws_cfg<M, CI, CO, kBf>().wloc, bool kAllowRmw = true>
 __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
     bwd_ws_kernel(int32_t n_in, int32_t n_tiles, const int32_t *__restrict__ col_ptr,
                   const int32_t *__restrict__ row_idx, const int32_t *__restrict__ perm,
@@ -1941,8 +1968,11 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
         RBY % 16 == 0 && 64 % (RBY / 16) == 0 && CK % (64 / (RBY / 16)) == 0;
     // rows of 32 float32 channels, 4 or 8 per gather wave: the in-place
     // one-hot gather (no stage)
-    constexpr bool kRmw = kOneHotShape && !kBf && CO == 32 && (RPW == 4 || RPW == 8) &&
-                          2 * TR * (SD + SF) * sizeof(DT) <= 163840;
+    // (also the learned decays and their derivatives, M / 8 values per edge)
+    constexpr bool kDecayBasis =
+        (kBasis == SBC_BASIS_EVENT_DECAYS + 1 || kBasis == kDecayDerivMode) && M % 8 == 0;
+    constexpr bool kRmw = kAllowRmw && (kOneHotShape || kDecayBasis) && !kBf && CO == 32 &&
+                          (RPW == 4 || RPW == 8) && 2 * TR * (SD + SF) * sizeof(DT) <= 163840;
     constexpr bool kOneHot =
         kOneHotShape &&
         (kRmw ||
@@ -1979,9 +2009,10 @@ __global__ void __launch_bounds__((kWsGather + kWsMma) * 64, 1)
         0, false};
     constexpr int NR = kOneHot ? CK / (64 / (RBY / 16)) : 1;  // row pieces per lane and chunk
     OneHotPipe<NR> pipe;
-    using RG = RmwGather<32, kRmw ? RPW : 4>;
-    const RG rmw{col_ptr, row_idx, g.ev, static_cast<const float *>(dY), n_in, g.nnz, inv_tau,
-                 lane / RG::LPR, lane % RG::LPR};
+    using RG = RmwGather<32, kRmw ? RPW : 4, kRmw && kDecayBasis ? M / 8 : 1,
+                         !(kRmw && kDecayBasis) ? 0 : (kBasis == kDecayDerivMode ? 2 : 1)>;
+    const RG rmw{col_ptr, row_idx, g.ev, static_cast<const float *>(dY), g.decays, n_in, g.nnz,
+                 inv_tau, lane / RG::LPR, lane % RG::LPR};
     typename RG::Pipe rpipe;
     auto wave_rows = [&](int32_t s) {
         return s < n_my ? (t_first + s * gx) * TR + w * RPW : -1;
@@ -2390,6 +2421,18 @@ BwdFn bwd_for(int basis_mode) {
         case kEvent8WideMode:
             if constexpr (M == 8) return bwd_ws_kernel<M, CI, CO, kEvent8WideMode, kBf>;
             return nullptr;
+        case kDecaysWideMode:
+        case kDecayDerivWideMode:
+            // the learned-decay bases through the generic gather (64-bit addressing)
+            if constexpr (M >= 16 && M % 8 == 0) {
+                constexpr WsCfg c = ws_cfg<M, CI, CO, kBf>();
+                if (basis_mode == kDecaysWideMode)
+                    return bwd_ws_kernel<M, CI, CO, SBC_BASIS_EVENT_DECAYS + 1, kBf, c.ng, c.nm,
+                                         c.tr, c.wloc, false>;
+                return bwd_ws_kernel<M, CI, CO, kDecayDerivMode, kBf, c.ng, c.nm, c.tr, c.wloc,
+                                     false>;
+            }
+            return nullptr;
     }
     return nullptr;
 }
@@ -2642,6 +2685,16 @@ sbc_status fused_backward(const sbc_csr *csr, const sbc_csc *csc, const float *v
             csr->nnz_bound * 4 >= lim || ((int64_t)csr->n_cols + 1) * 4 >= lim ||
             csr->nnz_bound < 1 || (force && force[0] == '1'))
             mode = kEvent8WideMode;
+    }
+    if (mode == SBC_BASIS_EVENT_DECAYS + 1 || mode == kDecayDerivMode) {
+        // the learned decays' in-place gather: the same limits
+        const int64_t n_ev = csr->n_cols > csr->n_rows ? csr->n_cols : csr->n_rows;
+        const int64_t lim = (int64_t)1 << 32;
+        const char *force = std::getenv("SBC_EVENT8_WIDE_PATH");
+        if ((int64_t)csr->n_rows * CO * (bf ? 2 : 4) >= lim || n_ev * 16 >= lim ||
+            csr->nnz_bound * 4 >= lim || ((int64_t)csr->n_cols + 1) * 4 >= lim ||
+            csr->nnz_bound < 1 || (force && force[0] == '1'))
+            mode = mode == kDecayDerivMode ? kDecayDerivWideMode : kDecaysWideMode;
     }
     BwdFn fn = find_bwd(Shape{M, CI, CO, bf}, mode);
     if (!fn) return fail(SBC_ERR_UNSUPPORTED, "no fused backward for this shape");

@@ -694,6 +694,34 @@ def test_decay_gradient(name, route):
     assert err < tol(w)
 
 
+@pytest.mark.parametrize("name", ["fz_ev_decays2_32", "events_300k_decays2"])
+def test_decay_backward_wide_offset_path(name, monkeypatch):
+    """The learned-decay backward and decay gradient on rows of 32 float32
+    channels take the in-place gather (32-bit byte offsets); past 4 GiB, or
+    with SBC_EVENT8_WIDE_PATH=1, the generic gather.  Both paths agree with
+    the oracle."""
+    print(f"[decay wide path] {name}", flush=True)
+    w, rp, ci, v = case(name)
+    assert w["C_in"] == 32 and w["C_out"] == 32 and w["dtype"] == "f32"
+    t, csr = gpu_case(name)
+    csc = G.sbc.csr_transpose(csr)
+    dF_ref, dW_ref = oracle_backward(name)
+    vd = oracle.basis.event_decay_basis(w["px"], w["py"], w["t"], rp, ci, w["decays"],
+                                        derivative=True)
+    dl_ref = oracle.conv.decay_backward(rp, ci, vd, w["F"], w["W"], w["dY"])
+    for wide in (False, True):
+        if wide:
+            monkeypatch.setenv("SBC_EVENT8_WIDE_PATH", "1")
+        dF, dW = G.sbc.conv_backward(csr, csc, t["F"], t["W"], t["dY"],
+                                     geometry=G.geometry(w, t), order="spmm_first")
+        dl = G.sbc.conv_decay_gradient(csr, t["F"], t["W"], t["dY"], G.geometry(w, t),
+                                       csc=csc).cpu().numpy()
+        monkeypatch.delenv("SBC_EVENT8_WIDE_PATH", raising=False)
+        assert G.row_error(dF.cpu().numpy(), dF_ref) < tol(w)
+        assert G.norm_error(dW.cpu().numpy(), dW_ref) < tol(w)
+        assert G.norm_error(dl, dl_ref) < tol(w)
+
+
 # ---------------------------------------------------------------- subsampling
 def _sampling_batch(seed, sizes, doubled=False):
     """Ellipsoid clouds; doubled: each cloud is sizes[b] / 2 distinct points
