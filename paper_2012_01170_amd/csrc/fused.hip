@@ -775,12 +775,23 @@ __device__ __forceinline__ void gather_rows_onehot(
     p.i1 = i1n;
 }
 
+// f(std::integral_constant<int, s>) for s = 0 .. N - 1, unrolled whatever
+// the body's size (register arrays indexed by s stay in registers)
+template <typename F, int... S>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, S...>) {
+    (f(std::integral_constant<int, S>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 // One-hot gather of the transposed pattern into the D tile in place, for
 // rows of 32 float32 channels and RPW = 4 or 8 rows per wave: the LPR = 64 /
 // RPW lanes of a row each own CO / LPR channels of it for all offsets and add
 // every edge of the row into those channels at the edge's offset (an LDS
-// read, the FMAs and a write: about two VALU instructions per edge and wave
-// where the bucket walk takes eight).  The lanes of a row load one neighbour
+// read, the FMAs and a write; no stage, no ballots and no bucket walk, which
+// frees the LDS for tiles of 64 rows).  The lanes of a row load one neighbour
 // row, 128 contiguous bytes, per step.  Edges come in chunks of LPR per row
 // (at least one chunk per tile): lane p takes index, coordinates, offset and
 // decay of edge p of the chunk, broadcast to the row's lanes by DPP.  Rows of
@@ -793,17 +804,6 @@ __device__ __forceinline__ void gather_rows_onehot(
 // chunk c loads the row of step s of chunk c + 1 into the register it has
 // just used), its coordinates at the start of the chunk before, and its
 // indices two chunks ahead; row bounds come three tiles ahead.
-// f(std::integral_constant<int, s>) for s = 0 .. N - 1, unrolled whatever
-// the body's size (register arrays indexed by s stay in registers)
-template <typename F, int... S>
-__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, S...>) {
-    (f(std::integral_constant<int, S>{}), ...);
-}
-template <int N, typename F>
-__device__ __forceinline__ void static_for(F &&f) {
-    static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
-
 template <int LPR>
 struct RmwPipe {
     int32_t e0a, e1a, e0b, e1b, e0c, e1c;  // bounds of this lane's row in tiles s, s + 1, s + 2
