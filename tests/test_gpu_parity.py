@@ -58,6 +58,10 @@ SMALL = {
     "ev_decays3_odd": lambda: workloads.small_events(seed=22, n=3001, c=13, n_decays=3),
     "ev_decays4_bf16": lambda: workloads.small_events(seed=21, c=16, n_decays=4, dtype="bf16"),
     "fz_ev_decays2_32": lambda: workloads.small_events(seed=23, c=32, n=5003, n_decays=2),
+    # uncapped wide balls: rows and columns of more than 64 edges with a ragged
+    # tail (the generic gathers fetch a row's edges 64 at a time)
+    "pts_dense": lambda: workloads.small_points(seed=24, n_clouds=2, n=200, radius=0.9, k_cap=0,
+                                                c_in=16, c_out=24),
 }
 # the general convolution's full-size cases; the featureless first layer
 # (one input channel of features ~N(0,1), so single-channel input gradients
