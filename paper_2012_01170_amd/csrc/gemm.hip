@@ -6,7 +6,8 @@
 //
 // Tiling: a 256-thread block owns a BM x BN tile of C (128 x 128, or 64 x
 // 64 when C is small and K long); its four waves own BM/2 x BN/2 quarters as
-// grids of 16 x 16 MFMA tiles.  K advances in slabs of 16 held in two LDS
+// grids of 16 x 16 MFMA tiles.  K advances in slabs of 16 (32 for the 64 x 64
+// tile on vector loads) held in two LDS
 // buffers: every thread loads its share of slab s+1 into registers while the
 // waves multiply slab s, then stores it into the other buffer (one block
 // barrier per slab).  Large K with few tiles is split over blockIdx.z; the
@@ -20,8 +21,17 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kSlab = 16;
 constexpr int kThreads = 256;
+// K per LDS slab: 16, or kDeepSlab for the 64 x 64 tile with both operands
+// on vector loads, whose short slabs would otherwise leave its few MFMAs per
+// slab waiting on each slab's memory round trip (the element-wise loaders
+// would spill at that depth, and the 128 x 128 tile's registers hold only
+// 16).  Split-K chunks are multiples of kChunkAlign, a multiple of both.
+constexpr int kDeepSlab = 32;
+constexpr int kChunkAlign = 64;
+template <int BT, bool kVecA, bool kVecB>
+constexpr int slab_for() { return (BT == 64 && kVecA && kVecB) ? kDeepSlab : 16; }
+static_assert(kChunkAlign % kDeepSlab == 0 && kChunkAlign % 16 == 0, "chunks hold whole slabs");
 
 __device__ __forceinline__ float ld(const float *p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float ld(const uint16_t *p, int64_t i) {
@@ -46,15 +56,19 @@ __device__ __forceinline__ void load_run(const T *__restrict__ p, int64_t off, i
                     out[q + 2] = x.z;
                     out[q + 3] = x.w;
                 }
-            } else if constexpr (kPer == 8) {
-                const uint4 x = *reinterpret_cast<const uint4 *>(p + off);
-                const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+            } else if constexpr (kPer % 8 == 0) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    out[2 * q] = __uint_as_float(w[q] << 16);
-                    out[2 * q + 1] = __uint_as_float(w[q] & 0xFFFF0000u);
+                for (int q8 = 0; q8 < kPer; q8 += 8) {
+                    const uint4 x = *reinterpret_cast<const uint4 *>(p + off + q8);
+                    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        out[q8 + 2 * q] = __uint_as_float(w[q] << 16);
+                        out[q8 + 2 * q + 1] = __uint_as_float(w[q] & 0xFFFF0000u);
+                    }
                 }
             } else {
+                static_assert(kPer == 4, "runs of 4, or of a multiple of 8, bf16 elements");
                 const uint2 x = *reinterpret_cast<const uint2 *>(p + off);
                 const uint32_t w[2] = {x.x, x.y};
 #pragma unroll
@@ -75,9 +89,9 @@ __device__ __forceinline__ void load_run(const T *__restrict__ p, int64_t off, i
 // operand's contiguous index (k, or the row / column index), so that
 // neighbouring threads read neighbouring addresses.  kVec: the contiguous
 // index has unit stride and its runs are 16-byte aligned (vector loads).
-template <int BT, typename T, bool kVec>
+template <int BT, int kSlab, typename T, bool kVec>
 struct SlabLoader {
-    static constexpr int kPer = BT * kSlab / kThreads;  // 8 (128) or 4 (64)
+    static constexpr int kPer = BT * kSlab / kThreads;  // 8 (128 x 16, 64 x 32) or 4 (64 x 16)
     float v[kPer];
     // element (t, k) of the operand at p[t * s_t + k * s_k], t < n_t, k < k_end
     __device__ __forceinline__ void load(const T *__restrict__ p, int64_t s_t, int64_t s_k,
@@ -142,6 +156,8 @@ __global__ void __launch_bounds__(kThreads, 2)
                 int64_t sb_k, int64_t sb_n, float *__restrict__ C, int64_t sc_r, int64_t sc_n,
                 int32_t R, int32_t N, int64_t K, int64_t k_chunk, float *__restrict__ partial) {
     constexpr int TM = BM / 32, TN = BN / 32;  // 16x16 tiles per wave (2 x 2 waves)
+    static_assert(BM == BN, "square tiles");
+    constexpr int kSlab = slab_for<BM, kVecA, kVecB>();
     __shared__ float As[2][kSlab][BM + 4];
     __shared__ float Bs[2][kSlab][BN + 4];
     const int lane = threadIdx.x & 63;
@@ -159,8 +175,8 @@ __global__ void __launch_bounds__(kThreads, 2)
 #pragma unroll
         for (int b = 0; b < TN; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    SlabLoader<BM, AT, kVecA> la;
-    SlabLoader<BN, BT, kVecB> lb;
+    SlabLoader<BM, kSlab, AT, kVecA> la;
+    SlabLoader<BN, kSlab, BT, kVecB> lb;
     la.load(A, sa_r, sa_k, r0, R, kb, ke, a_kc);
     lb.load(B, sb_n, sb_k, n0, N, kb, ke, b_kc);
     la.store(As[0], a_kc);
@@ -268,7 +284,7 @@ sbc_status gemm(const void *A, bool a_bf16, int64_t sa_r, int64_t sa_k, const vo
     trace_before(trace, stream);
     const int32_t S = gemm_splits(R, N, K);
     int64_t k_chunk = S > 1 ? (K + S - 1) / S : (K > 0 ? K : 1);
-    k_chunk = (k_chunk + kSlab - 1) / kSlab * kSlab;
+    k_chunk = (k_chunk + kChunkAlign - 1) / kChunkAlign * kChunkAlign;
     const int32_t Sz = K > 0 ? (int32_t)((K + k_chunk - 1) / k_chunk) : 1;
     const int t = tile_for(R, N);
     dim3 grid((N + t - 1) / t, (R + t - 1) / t, Sz);
