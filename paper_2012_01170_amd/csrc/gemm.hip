@@ -252,12 +252,13 @@ __global__ void splitk_reduce_kernel(const float *__restrict__ partial, int32_t 
 }  // namespace
 
 // Tile of a shape: 128 x 128, or 64 x 64 when C has fewer than 128 rows or
-// columns (a 128 tile would be half empty) or when the 128 tiles would be too
-// few to spread K over the chip without very short splits.
+// columns (a 128 tile would be half empty) or when the 128 tiles would give
+// fewer than two blocks per CU (the 64 x 64 tiles then keep four per CU
+// busy: C of 8192 x 512 with K = 128, 24.5 -> 21.6 us).
 static int tile_for(int32_t R, int32_t N) {
     if (R < 128 || N < 128) return 64;
     const int64_t big = (int64_t)((R + 127) / 128) * ((N + 127) / 128);
-    return big >= 64 ? 128 : 64;
+    return big >= 512 ? 128 : 64;
 }
 
 int32_t gemm_splits(int32_t R, int32_t N, int64_t K) {
